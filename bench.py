@@ -1,0 +1,257 @@
+"""Benchmark of the shard halo-convolution hot path on one MI355X.
+
+One step = one pass of the whole per-shard hot path over one synthetic shard:
+pack the boundary faces this shard sends, unpack the received slabs into its
+margins, forward convolution, weight gradient. All inputs are resident in HBM
+before the timed region. Geometry and slab shapes come from the library
+itself; the CPU oracle is used only by the cpu_baseline leg. Prints ONE JSON
+line on stdout (progress goes to stderr).
+
+    python bench.py [--steps K] [--warmup W] [--workload c3] [--no-cpu-baseline]
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK = {"bf16": 2516.6, "f32": 157.3}   # dense MFMA TFLOP/s, MI355X (AMD spec)
+HBM_PEAK = 8000.0                        # GB/s
+
+DESCR = {
+    "c1": "2d_fp32_c8_64x64_split2H_shard0_k3",
+    "c2": "2d_bf16_c64_4096x4096_split4H_shard1_k3",
+    "c3": "3d_bf16_c32_512cube_split4D_shard1_k3_smooth",
+    "c4": "3d_bf16_c16to64_256cube_split2x2DH_corner_k5",
+    "c5": "3d_fp32_c64to128_384cube_split8D_shard3_k3_s2",
+}
+
+
+def log(msg):
+    print(msg, file=sys.stderr, flush=True)
+
+
+def geometry(sc, w, idx):
+    off, ext = w.interior(idx)
+    sharded = [1 if p > 1 else 0 for p in w.parts]
+    g = sc.shard_conv_geometry(w.G, off, ext, w.K, w.S, sharded)
+    g["off"], g["ext"] = off, ext
+    return g
+
+
+def margin_box(g, axis, side):
+    """Tile-coordinate box of the margin on (axis, side): the slab layout of the
+    library (padded extent on earlier axes, interior on later ones)."""
+    lo, ext, hi = g["halo_lo"], g["ext"], g["halo_hi"]
+    b0, b1 = [], []
+    for b in range(len(ext)):
+        if b == axis:
+            r = (0, lo[b]) if side == 0 else (lo[b] + ext[b], lo[b] + ext[b] + hi[b])
+        elif b < axis:
+            r = (0, lo[b] + ext[b] + hi[b])
+        else:
+            r = (lo[b], lo[b] + ext[b])
+        b0.append(r[0])
+        b1.append(r[1])
+    return b0, b1
+
+
+def dev(arr):
+    import numpy as np
+    import torch
+    if arr.dtype == np.uint16:
+        return torch.from_numpy(np.ascontiguousarray(arr).view(np.int16)).view(torch.bfloat16).cuda()
+    return torch.from_numpy(np.ascontiguousarray(arr)).cuda()
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="c3", choices=sorted(DESCR))
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU's shard; --gpus {args.gpus} is not supported: this build has no "
+              "multi-GPU path (no collectives or sharding across devices)", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    import synth
+    from synth.workloads import SHORT
+    from paper_2605_11111_amd import shardconv as sc
+
+    w = SHORT[args.workload]
+    torch.cuda.set_device(0)
+    g = geometry(sc, w, w.shard)
+    lo, hi, ext = g["halo_lo"], g["halo_hi"], g["ext"]
+    tile_lo = [o - h for o, h in zip(g["off"], lo)]
+    tile_hi = [o + e + h for o, e, h in zip(g["off"], ext, hi)]
+    t0 = time.time()
+    full_h = w.x_box(tile_lo, tile_hi)
+    log(f"generated padded box {full_h.shape} in {time.time() - t0:.1f}s ({synth.threads()} threads)")
+    tile = dev(full_h)
+    desc = sc.tile_desc(w.N, w.cin, ext, lo, hi)
+    tdt = torch.float32 if w.dtype == "f32" else torch.bfloat16
+
+    recv, send = [], []
+    for axis in range(w.nd):
+        for side in (0, 1):
+            width = lo[axis] if side == 0 else hi[axis]
+            if width > 0:
+                b0, b1 = margin_box(g, axis, side)
+                box = (slice(None),) + tuple(slice(a, b) for a, b in zip(b0, b1)) + (slice(None),)
+                nbytes = full_h[box].size * full_h.itemsize
+                slab = dev(full_h[box]) if w.neighbour_exists(w.shard, axis, side) else None
+                recv.append((axis, side, slab, nbytes))
+            if w.neighbour_exists(w.shard, axis, side):
+                nb = list(w.shard)
+                nb[axis] += 1 if side else -1
+                ng = geometry(sc, w, tuple(nb))
+                nwidth = ng["halo_lo"][axis] if side == 1 else ng["halo_hi"][axis]
+                if nwidth > 0:
+                    buf = torch.empty(sc.shard_halo_slab_shape(desc, axis, nwidth), dtype=tdt, device="cuda")
+                    send.append((axis, side, nwidth, buf, buf.numel() * buf.element_size()))
+    del full_h
+    O = g["out_ext"]
+    wt = dev(w.weights_host())
+    full_out = sc.shard_conv_geometry(w.G, [0] * w.nd, list(w.G), w.K, w.S, [0] * w.nd)["out_ext"]
+    t0 = time.time()
+    dyh = w.dy_field(full_out).box((0, 0, *g["out_off"]), (w.N, w.cout, *[o + e for o, e in zip(g["out_off"], O)]),
+                                   out=w.out)
+    dy = dev(dyh)
+    del dyh
+    log(f"generated dy in {time.time() - t0:.1f}s")
+    y = torch.empty([w.N] + list(O) + [w.cout], dtype=tdt, device="cuda")
+    dw = torch.empty((w.cout, w.cin) + tuple(w.K), dtype=torch.float32, device="cuda")
+    code = sc.SHARD_F32 if w.dtype == "f32" else sc.SHARD_BF16
+    wsf = torch.empty(max(16, sc.shard_conv_workspace_bytes(0, desc, code, w.cout, w.K, w.S, O)),
+                      dtype=torch.uint8, device="cuda")
+    wsw = torch.empty(max(16, sc.shard_conv_workspace_bytes(1, desc, code, w.cout, w.K, w.S, O)),
+                      dtype=torch.uint8, device="cuda")
+    stream = torch.cuda.current_stream()
+
+    ops = []
+    for (axis, side, nwidth, buf, nbytes) in send:
+        ops.append((f"pack_a{axis}s{side}", "pack", 2 * nbytes,
+                    lambda axis=axis, side=side, nwidth=nwidth, buf=buf:
+                    sc.shard_halo_pack(desc, tile, axis, side, nwidth, buf)))
+    for (axis, side, slab, nbytes) in recv:
+        moved = 2 * nbytes if slab is not None else nbytes
+        ops.append((f"unpack_a{axis}s{side}", "unpack", moved,
+                    lambda axis=axis, side=side, slab=slab: sc.shard_halo_unpack(desc, tile, axis, side, slab)))
+    flops = 2.0 * w.N * int(np.prod(O)) * w.cout * w.cin * int(np.prod(w.K))
+    ops.append(("conv_fwd", "fwd", flops,
+                lambda: sc.shard_conv_fwd(desc, tile, wt, w.cout, w.K, w.S, g["pad_lo"], O, y, wsf)))
+    ops.append(("conv_wgrad", "wgrad", flops,
+                lambda: sc.shard_conv_wgrad(desc, tile, dy, w.cout, w.K, w.S, g["pad_lo"], O, dw, wsw)))
+
+    def step(events=None):
+        for i, op in enumerate(ops):
+            if events is not None:
+                events[i][0].record(stream)
+            op[3]()
+            if events is not None:
+                events[i][1].record(stream)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    log("warmup done")
+    ev = [[[torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)] for _ in ops]
+          for _ in range(args.steps)]
+    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    start.record(stream)
+    for k in range(args.steps):
+        step(ev[k])
+    stop.record(stream)
+    torch.cuda.synchronize()
+    ms_step = start.elapsed_time(stop) / args.steps
+    per_op = {}
+    for i, (label, kind, work, _) in enumerate(ops):
+        per_op[label] = (kind, work, float(np.mean([ev[k][i][0].elapsed_time(ev[k][i][1])
+                                                     for k in range(args.steps)])))
+    log("timed region done")
+
+    dt = w.dtype
+    value = 2 * flops / (ms_step * 1e-3) / 1e12
+    detail = {}
+    for label, (kind, work, ms) in per_op.items():
+        if kind in ("fwd", "wgrad"):
+            tf = work / (ms * 1e-3) / 1e12
+            detail[label] = {"ms": round(ms, 4), "tflops": round(tf, 2), "frac_mfma_peak": round(tf / PEAK[dt], 4)}
+        else:
+            gbs = work / (ms * 1e-3) / 1e9
+            detail[label] = {"ms": round(ms, 4), "gbs": round(gbs, 1), "frac_hbm_peak": round(gbs / HBM_PEAK, 4),
+                             "bytes": int(work)}
+    dom = max(("conv_fwd", "conv_wgrad"), key=lambda k: per_op[k][2])
+    ach = per_op[dom][1] / (per_op[dom][2] * 1e-3) / 1e12
+    roofline = {"kernel": dom, "bound": "mfma", "achieved": round(ach, 2), "peak": PEAK[dt], "unit": "TFLOP/s",
+                "frac": round(ach / PEAK[dt], 4), "traffic": None,
+                "work_per_launch": f"{flops:.4e} flop: 2*Cout*Cin*prod(K) per output voxel x {int(np.prod(O))} voxels"}
+
+    cpu = None if args.no_cpu_baseline else cpu_baseline(w, g, tile_lo)
+    line = {
+        "metric": "shard conv fwd+wgrad TFLOP/s (% MFMA peak); halo pack/unpack GB/s (% HBM)",
+        "value": round(value, 3), "unit": "TFLOP/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 4), "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "bf16" if dt == "bf16" else "f32", "data": "synthetic (seeded counter-based generator)",
+        "config": {"workload": DESCR[args.workload],
+                   "tile_padded": [w.N] + [l + e + h for l, e, h in zip(lo, ext, hi)] + [w.cin],
+                   "out": [w.N] + list(O) + [w.cout], "kernel": list(w.K), "stride": list(w.S),
+                   "accumulate": "f32"},
+        "ops": detail, "roofline": roofline, "cpu_baseline": cpu,
+    }
+    print(json.dumps(line), flush=True)
+
+
+def cpu_baseline(w, g, tile_lo):
+    """The oracle (float64 NumPy) timed on a bounded sample of the same shard:
+    forward and weight gradient over a few output planes along axis 0."""
+    import numpy as np
+    from oracle import conv as oconv
+    from synth.workloads import as_f64
+    try:
+        from threadpoolctl import threadpool_info
+        cores = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
+    except Exception:
+        cores = os.cpu_count()
+    planes = 2
+    L = g["out_ext"][0]
+    p0 = L // 2
+    r0 = p0 * w.S[0] - g["pad_lo"][0]
+    r1 = (p0 + planes - 1) * w.S[0] - g["pad_lo"][0] + w.K[0]
+    sharded = [p > 1 for p in w.parts]
+    pad = [0 if sharded[a] else (w.K[a] - 1) // 2 for a in range(w.nd)]
+    lo_t = [tile_lo[0] + r0] + [0 - pad[a] if not sharded[a] else tile_lo[a] for a in range(1, w.nd)]
+    hi_t = [tile_lo[0] + r1] + [w.G[a] + pad[a] if not sharded[a] else
+                                tile_lo[a] + g["halo_lo"][a] + g["ext"][a] + g["halo_hi"][a] for a in range(1, w.nd)]
+    xw = np.moveaxis(as_f64(w.x_box(lo_t, hi_t)), -1, 1)
+    w64 = as_f64(w.weights_host())
+    lo = list(g["out_off"])
+    hi = [o + e for o, e in zip(g["out_off"], g["out_ext"])]
+    lo[0], hi[0] = lo[0] + p0, lo[0] + p0 + planes
+    full_out = [(G + 2 * ((K - 1) // 2) - K) // S + 1 for G, K, S in zip(w.G, w.K, w.S)]
+    dy64 = np.moveaxis(as_f64(w.dy_field(full_out).box((0, 0, *lo), (w.N, w.cout, *hi), out=w.out)), -1, 1)
+    t0 = time.time()
+    oconv.conv_forward_window(xw, lo_t, w.G, w64, w.S, lo, hi)
+    oconv.conv_wgrad_window(xw, lo_t, w.G, dy64, w.K, w.S, lo, hi)
+    sec = time.time() - t0
+    vox = w.N * int(np.prod([h - l for l, h in zip(lo, hi)]))
+    fl = 2 * 2.0 * vox * w.cout * w.cin * int(np.prod(w.K))
+    return {"value": round(fl / sec / 1e12, 6), "unit": "TFLOP/s", "cores": int(cores), "kind": "oracle",
+            "sample": f"fwd+wgrad over {planes} of {L} output planes along axis 0 of the same shard "
+                      f"({sec:.1f}s, float64 NumPy)"}
+
+
+if __name__ == "__main__":
+    main()

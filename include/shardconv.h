@@ -1,0 +1,193 @@
+/*
+ * shardconv - the per-shard hot path of domain-parallel convolution on one
+ * MI355X (gfx950) GPU.
+ *
+ * In domain parallelism a tensor [B][C][spatial...] is split along its spatial
+ * axes below batch size one (ShardTensor paper, section "Introduction"). Each
+ * shard owns a box of the input with arbitrary per-rank extents (section
+ * "ShardTensor", Table 2, "sharding shapes"). A convolution on a shard first
+ * fetches the adjacent rows ("halo") from its neighbours so that it is
+ * numerically consistent with the unsharded operation (section "PyTorch
+ * Dispatch"), and because a convolution changes the global shape its output
+ * chunks are uneven (section "ShardTensor"). This library implements that
+ * per-shard work:
+ *
+ *   shard_conv_geometry   which outputs a shard owns and the halo it needs (host)
+ *   shard_halo_pack       copy a boundary face of the tile into a dense slab
+ *   shard_halo_unpack     copy a received slab into a margin, or zero-fill it
+ *   shard_conv_fwd        convolution read off the padded tile
+ *   shard_conv_wgrad      the shard's partial weight gradient
+ *
+ * Convolution semantics are PyTorch's cross-correlation (no bias, dilation 1,
+ * groups 1), which the paper's programming model keeps (section "Benchmarks
+ * and Applications", Algorithm 1, step 4).
+ *
+ * Conventions shared by every call:
+ *  - Spatial axes are numbered outermost first (3D: D=0, H=1, W=2; 2D: H=0,
+ *    W=1). Entries of per-axis arrays at index >= ndim are ignored.
+ *  - A padded tile is dense, channels-last:
+ *        [n][P0][P1][P2][c],  P_a = halo_lo[a] + ext[a] + halo_hi[a]
+ *    (axes >= ndim have extent 1). Row halo_lo[a] of axis a is the shard's
+ *    first interior row; the margins hold neighbour rows (or zero padding at a
+ *    global boundary).
+ *  - Activations (tile, y, dy, slabs) are SHARD_F32 (binary32) or SHARD_BF16
+ *    (bfloat16); weights w have the activation dtype; dw is always binary32.
+ *    Convolutions accumulate in binary32; a bf16 y is rounded to nearest-even
+ *    from the binary32 sum.
+ *  - Every device pointer is owned by the caller. The library never allocates,
+ *    frees or synchronises; every device call is enqueued on `stream` and
+ *    returns immediately. Buffers must not overlap.
+ *  - Every argument is checked on the host before any launch; on an error
+ *    nothing is written. No exception crosses this interface, and the library
+ *    keeps no mutable global state (calls from several host threads are safe).
+ *  - Device pointers must be aligned to their element size (2 or 4 bytes);
+ *    16-byte aligned buffers take the vectorised paths.
+ */
+#ifndef SHARDCONV_H
+#define SHARDCONV_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    SHARD_OK = 0,
+    SHARD_ERR_INVALID = 1,      /* a malformed argument (null pointer, negative size, bad axis, ...) */
+    SHARD_ERR_UNSUPPORTED = 2,  /* well formed but outside what is implemented (see each call) */
+    SHARD_ERR_HIP = 3           /* the HIP runtime rejected a launch */
+} shard_status_t;
+
+typedef enum { SHARD_F32 = 0, SHARD_BF16 = 1 } shard_dtype_t;
+
+/* Descriptor of a padded tile (see the layout above). ndim in {1, 2, 3};
+ * n >= 0 batch items, c >= 1 channels, ext[a] >= 0 interior rows,
+ * halo_lo[a], halo_hi[a] >= 0 margin rows. */
+typedef struct {
+    int32_t ndim;
+    int64_t n, c;
+    int64_t ext[3];
+    int64_t halo_lo[3], halo_hi[3];
+} shard_tile_t;
+
+/*
+ * Geometry of one shard (host only, no device work).
+ *
+ * Per axis a: the full domain has global_ext[a] rows; this shard's interior is
+ * [shard_off[a], shard_off[a] + shard_ext[a]); kernel[a] is odd, stride[a] >= 1;
+ * the convolution pads the full domain with P = (kernel - 1) / 2 zeros per side
+ * ("same" padding), so the full output has (G + 2P - K) / S + 1 rows.
+ * Output j is owned by the shard whose interior contains its anchor j*S (the
+ * reading this library takes of the paper's uneven output chunks).
+ *
+ * Outputs per axis:
+ *   out_off, out_ext  the owned output rows [out_off, out_off + out_ext) of the
+ *                     full output (out_ext may be 0: the shard owns nothing);
+ *   halo_lo, halo_hi  margin rows the padded tile needs below / above the
+ *                     interior; on a sharded axis margins outside the domain are
+ *                     zero padding (unpack with slab = NULL), on an unsharded
+ *                     axis (sharded_mask[a] == 0, shard_off 0, shard_ext = G)
+ *                     they are 0;
+ *   pad_lo            the value to pass to shard_conv_fwd/wgrad: P on unsharded
+ *                     axes; on sharded axes <= 0, negative when the first owned
+ *                     output's window starts inside the interior (stride > P+1).
+ * Errors: SHARD_ERR_INVALID for null pointers, ndim outside 1..3, even or
+ * non-positive kernel, stride < 1, global_ext < 1, or an interior box outside
+ * the domain (or not the whole axis when unsharded).
+ */
+shard_status_t shard_conv_geometry(int32_t ndim, const int64_t global_ext[], const int64_t shard_off[],
+                                   const int64_t shard_ext[], const int64_t kernel[], const int64_t stride[],
+                                   const int64_t sharded_mask[], int64_t halo_lo[], int64_t halo_hi[],
+                                   int64_t pad_lo[], int64_t out_off[], int64_t out_ext[]);
+
+/*
+ * Shape of the slab exchanged along `axis` with the given width: writes
+ * shape_out[5] = {n, s0, s1, s2, c} with s_axis = width, s_b the padded extent
+ * for b < axis and the interior extent for b > axis (axes are exchanged in
+ * ascending order, so a slab carries the corner rows of every earlier axis),
+ * and 1 for b >= ndim. The slab is dense in that order. Host only.
+ * Errors: SHARD_ERR_INVALID for a bad descriptor, axis or negative width.
+ */
+shard_status_t shard_halo_slab_shape(const shard_tile_t* x, int32_t axis, int64_t width, int64_t shape_out[5]);
+
+/*
+ * Halo pack (the sending half of the halo exchange, section "PyTorch Dispatch"):
+ * copy the `width` interior rows of the tile nearest to `side` (0 = low,
+ * 1 = high) along `axis` into the dense slab (shape from shard_halo_slab_shape).
+ * `width` is the receiving neighbour's margin on the facing side.
+ * Bit-exact copy. width == 0 or an empty slab is a no-op (slab may be NULL).
+ * Errors: SHARD_ERR_INVALID (bad descriptor, dtype, axis, side, width < 0, null
+ * pointer); SHARD_ERR_UNSUPPORTED when width > ext[axis] (the neighbour would
+ * need rows beyond this shard: a multi-hop halo).
+ */
+shard_status_t shard_halo_pack(const shard_tile_t* x, shard_dtype_t dtype, const void* tile, int32_t axis,
+                               int32_t side, int64_t width, void* slab, hipStream_t stream);
+
+/*
+ * Halo unpack (the receiving half): write the slab into the margin on
+ * (axis, side), whose width is halo_lo[axis] (side 0) or halo_hi[axis] (side 1);
+ * the slab shape is shard_halo_slab_shape(x, axis, width). slab == NULL fills
+ * the margin with zeros (a global boundary: the convolution's zero padding).
+ * Bit-exact copy; a zero-width margin is a no-op.
+ * Errors: SHARD_ERR_INVALID (bad descriptor, dtype, axis, side, null tile).
+ */
+shard_status_t shard_halo_unpack(const shard_tile_t* x, shard_dtype_t dtype, void* tile, int32_t axis,
+                                 int32_t side, const void* slab, hipStream_t stream);
+
+/*
+ * Forward convolution over a padded tile:
+ *   y[n][j][co] = sum_{ci, t} w[co][ci][t] * tile[n][j*S + t - pad_lo][ci]
+ * per axis (j the output row, t the tap), with tile rows outside [0, P_a) read
+ * as zero. With the values from shard_conv_geometry this is exactly the shard's
+ * slice of the full-domain convolution.
+ *   w     [c_out][x->c][kernel0][kernel1][kernel2]  (PyTorch layout), dtype
+ *   y     [n][out_ext0][out_ext1][out_ext2][c_out], dtype (overwritten)
+ *   ws    device workspace of at least shard_conv_workspace_bytes(0, ...) bytes
+ *         (may be NULL when that is 0); contents are scratch.
+ * kernel[a] in 1..64, stride[a] in 1..64, out_ext[a] >= 0, |pad_lo[a]| < 2^30.
+ * Empty output (n or any out_ext 0) is a no-op.
+ * Errors: SHARD_ERR_INVALID for malformed arguments or a short workspace;
+ * SHARD_ERR_HIP if a launch fails.
+ */
+shard_status_t shard_conv_fwd(const shard_tile_t* x, shard_dtype_t dtype, const void* tile, const void* w,
+                              int64_t c_out, const int64_t kernel[], const int64_t stride[],
+                              const int64_t pad_lo[], const int64_t out_ext[], void* y, void* ws,
+                              size_t ws_bytes, hipStream_t stream);
+
+/*
+ * Weight gradient of the shard (its partial; summing the partials of all
+ * shards gives the full-domain weight gradient):
+ *   dw[co][ci][t] = sum_{n, j} dy[n][j][co] * tile[n][j*S + t - pad_lo][ci]
+ * over the shard's outputs j, same tile reading rule as shard_conv_fwd.
+ *   dy    [n][out_ext0][out_ext1][out_ext2][c_out], dtype
+ *   dw    [c_out][x->c][kernel0][kernel1][kernel2], binary32 (overwritten)
+ *   ws    device workspace of at least shard_conv_workspace_bytes(1, ...) bytes.
+ * The summation order is fixed: repeated calls give bit-identical dw.
+ * An empty output box writes dw = 0.
+ * Errors: as shard_conv_fwd.
+ */
+shard_status_t shard_conv_wgrad(const shard_tile_t* x, shard_dtype_t dtype, const void* tile, const void* dy,
+                                int64_t c_out, const int64_t kernel[], const int64_t stride[],
+                                const int64_t pad_lo[], const int64_t out_ext[], float* dw, void* ws,
+                                size_t ws_bytes, hipStream_t stream);
+
+/*
+ * Workspace bytes shard_conv_fwd (op 0) or shard_conv_wgrad (op 1) needs for
+ * these arguments. A pure function of its arguments (the launch plan does not
+ * depend on the device); host only. Returns (size_t)-1 for malformed arguments.
+ */
+size_t shard_conv_workspace_bytes(int32_t op, const shard_tile_t* x, shard_dtype_t dtype, int64_t c_out,
+                                  const int64_t kernel[], const int64_t stride[], const int64_t out_ext[]);
+
+/* Static, human-readable text for a status code. Never NULL. */
+const char* shard_status_string(shard_status_t status);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SHARDCONV_H */

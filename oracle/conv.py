@@ -194,3 +194,17 @@ def tile_conv(tile, w, stride, pad_lo, out_ext) -> np.ndarray:
         wt = w[(slice(None), slice(None)) + tap]
         y += np.moveaxis(np.tensordot(wt, xs, axes=([1], [1])), 0, 1)
     return y
+
+
+def round_bf16(v: np.ndarray) -> np.ndarray:
+    """Output rounding of a bf16 convolution: the exact value rounded to
+    binary32 (nearest even), then to bfloat16 (nearest even on the upper 16
+    bits). Returns the bfloat16 bit patterns (uint16)."""
+    b = np.ascontiguousarray(v, dtype=np.float64).astype(np.float32).view(np.uint32).astype(np.uint64)
+    r = (b + 0x7FFF + ((b >> 16) & 1)) >> 16
+    return r.astype(np.uint16)
+
+
+def bf16_value(bits: np.ndarray) -> np.ndarray:
+    """bfloat16 bit patterns -> exact float64 values."""
+    return (np.asarray(bits, dtype=np.uint16).astype(np.uint32) << 16).view(np.float32).astype(np.float64)

@@ -1,0 +1,279 @@
+// C-ABI entry points: argument validation on the host (before any launch, so
+// an error writes nothing), normalisation to three spatial axes, dispatch.
+#include <cstdlib>
+#include <cstring>
+
+#include "internal.h"
+
+namespace shardconv {
+
+bool force_generic()
+{
+    const char* v = std::getenv("SHARDCONV_ALGO");
+    return v && std::strcmp(v, "generic") == 0;
+}
+
+size_t generic_wgrad_workspace(const Tile3& t, const Conv3& cv);
+hipError_t generic_conv_wgrad(const Tile3& t, const Conv3& cv, shard_dtype_t dt, const void* tile, const void* dy,
+                              float* dw, void* ws, hipStream_t s);
+
+}  // namespace shardconv
+
+using namespace shardconv;
+
+namespace {
+
+constexpr int64_t kMaxDim = int64_t(1) << 40;
+
+bool valid_dtype(shard_dtype_t d) { return d == SHARD_F32 || d == SHARD_BF16; }
+int esize(shard_dtype_t d) { return d == SHARD_F32 ? 4 : 2; }
+bool aligned(const void* p, int a) { return (reinterpret_cast<uintptr_t>(p) % uintptr_t(a)) == 0; }
+
+// Product of non-negative sizes with an overflow guard (false if >= 2^62).
+bool safe_mul(int64_t& acc, int64_t v)
+{
+    if (v == 0) {
+        acc = 0;
+        return true;
+    }
+    if (acc > (int64_t(1) << 62) / v) return false;
+    acc *= v;
+    return true;
+}
+
+bool norm_tile(const shard_tile_t* x, shard_dtype_t dt, Tile3& t)
+{
+    if (!x || x->ndim < 1 || x->ndim > 3 || !valid_dtype(dt)) return false;
+    if (x->n < 0 || x->n > kMaxDim || x->c < 1 || x->c > kMaxDim) return false;
+    t.n = x->n;
+    t.c = x->c;
+    t.esz = esize(dt);
+    const int off = 3 - x->ndim;
+    for (int k = 0; k < 3; ++k) {
+        t.lo[k] = t.hi[k] = 0;
+        t.ext[k] = 1;
+    }
+    for (int a = 0; a < x->ndim; ++a) {
+        const int k = off + a;
+        if (x->ext[a] < 0 || x->halo_lo[a] < 0 || x->halo_hi[a] < 0) return false;
+        if (x->ext[a] > kMaxDim || x->halo_lo[a] > kMaxDim || x->halo_hi[a] > kMaxDim) return false;
+        t.lo[k] = x->halo_lo[a];
+        t.ext[k] = x->ext[a];
+        t.hi[k] = x->halo_hi[a];
+    }
+    int64_t total = t.n;
+    for (int k = 0; k < 3; ++k) {
+        t.P[k] = t.lo[k] + t.ext[k] + t.hi[k];
+        if (!safe_mul(total, t.P[k])) return false;
+    }
+    int64_t bytes = total;
+    return safe_mul(bytes, t.c * t.esz);
+}
+
+int64_t tile_elems(const Tile3& t) { return t.n * t.P[0] * t.P[1] * t.P[2] * t.c; }
+
+bool norm_conv(const shard_tile_t* x, const Tile3& t, int64_t c_out, const int64_t kernel[], const int64_t stride[],
+               const int64_t pad_lo[], const int64_t out_ext[], Conv3& cv)
+{
+    if (c_out < 1 || c_out > kMaxDim || !kernel || !stride || !out_ext) return false;
+    const int off = 3 - x->ndim;
+    cv.cout = c_out;
+    for (int k = 0; k < 3; ++k) {
+        cv.K[k] = 1;
+        cv.S[k] = 1;
+        cv.pad[k] = 0;
+        cv.O[k] = 1;
+    }
+    for (int a = 0; a < x->ndim; ++a) {
+        const int k = off + a;
+        if (kernel[a] < 1 || kernel[a] > 64 || stride[a] < 1 || stride[a] > 64) return false;
+        if (out_ext[a] < 0 || out_ext[a] > kMaxDim) return false;
+        const int64_t p = pad_lo ? pad_lo[a] : 0;
+        if (p <= -(int64_t(1) << 30) || p >= (int64_t(1) << 30)) return false;
+        cv.K[k] = kernel[a];
+        cv.S[k] = stride[a];
+        cv.pad[k] = p;
+        cv.O[k] = out_ext[a];
+    }
+    int64_t total = t.n;
+    for (int k = 0; k < 3; ++k)
+        if (!safe_mul(total, cv.O[k])) return false;
+    int64_t wsz = cv.cout;
+    if (!safe_mul(wsz, t.c) || !safe_mul(wsz, cv.taps())) return false;
+    return safe_mul(total, cv.cout);
+}
+
+// The box a slab covers on internal axis k: rows [r0, r1) on k, the padded
+// extent on earlier axes, the interior on later ones.
+void slab_spans(const Tile3& t, int k, int64_t r0, int64_t r1, int64_t start[3], int64_t cnt[3])
+{
+    for (int b = 0; b < 3; ++b) {
+        if (b < k) {
+            start[b] = 0;
+            cnt[b] = t.P[b];
+        } else if (b == k) {
+            start[b] = r0;
+            cnt[b] = r1 - r0;
+        } else {
+            start[b] = t.lo[b];
+            cnt[b] = t.ext[b];
+        }
+    }
+}
+
+BoxCopy make_box(const Tile3& t, int k, int64_t r0, int64_t r1)
+{
+    int64_t start[3], cnt[3];
+    slab_spans(t, k, r0, r1, start, cnt);
+    const int64_t es = t.esz;
+    // dims outermost first: n, axis0, axis1, axis2; byte strides in the tile
+    int64_t dcnt[4] = {t.n, cnt[0], cnt[1], cnt[2]};
+    int64_t dstr[4] = {t.P[0] * t.P[1] * t.P[2] * t.c * es, t.P[1] * t.P[2] * t.c * es, t.P[2] * t.c * es, t.c * es};
+    int64_t full[4] = {t.n, t.P[0], t.P[1], t.P[2]};
+    BoxCopy b{};
+    b.base = ((start[0] * t.P[1] + start[1]) * t.P[2] + start[2]) * t.c * es;
+    // merge contiguous inner dims into the run
+    int64_t run = t.c * es;
+    int d = 3;
+    run *= dcnt[d];  // axis 2 rows are always contiguous
+    --d;
+    while (d >= 0 && dcnt[d + 1] == full[d + 1] && dstr[d] == run) {
+        run *= dcnt[d];
+        --d;
+    }
+    b.run = run;
+    // remaining outer dims 0..d (at most 3), right-aligned into cnt[3]
+    for (int i = 0; i < 3; ++i) {
+        b.cnt[i] = 1;
+        b.tstride[i] = 0;
+    }
+    for (int i = d, j = 2; i >= 0; --i, --j) {
+        b.cnt[j] = dcnt[i];
+        b.tstride[j] = dstr[i];
+    }
+    return b;
+}
+
+shard_status_t map_hip(hipError_t e) { return e == hipSuccess ? SHARD_OK : SHARD_ERR_HIP; }
+
+}  // namespace
+
+extern "C" {
+
+const char* shard_status_string(shard_status_t s)
+{
+    switch (s) {
+    case SHARD_OK:
+        return "ok";
+    case SHARD_ERR_INVALID:
+        return "invalid argument";
+    case SHARD_ERR_UNSUPPORTED:
+        return "unsupported argument";
+    case SHARD_ERR_HIP:
+        return "HIP runtime error";
+    default:
+        return "unknown status";
+    }
+}
+
+shard_status_t shard_halo_slab_shape(const shard_tile_t* x, int32_t axis, int64_t width, int64_t shape_out[5])
+{
+    Tile3 t;
+    if (!shape_out || !norm_tile(x, SHARD_F32, t) || axis < 0 || axis >= x->ndim || width < 0 || width > kMaxDim)
+        return SHARD_ERR_INVALID;
+    shape_out[0] = x->n;
+    for (int b = 0; b < 3; ++b) {
+        if (b >= x->ndim)
+            shape_out[1 + b] = 1;
+        else if (b < axis)
+            shape_out[1 + b] = x->halo_lo[b] + x->ext[b] + x->halo_hi[b];
+        else if (b == axis)
+            shape_out[1 + b] = width;
+        else
+            shape_out[1 + b] = x->ext[b];
+    }
+    shape_out[4] = x->c;
+    return SHARD_OK;
+}
+
+shard_status_t shard_halo_pack(const shard_tile_t* x, shard_dtype_t dtype, const void* tile, int32_t axis,
+                               int32_t side, int64_t width, void* slab, hipStream_t stream)
+{
+    Tile3 t;
+    if (!norm_tile(x, dtype, t) || axis < 0 || axis >= x->ndim || (side != 0 && side != 1) || width < 0)
+        return SHARD_ERR_INVALID;
+    const int k = 3 - x->ndim + axis;
+    if (width > t.ext[k]) return SHARD_ERR_UNSUPPORTED;
+    const int64_t r0 = side == 0 ? t.lo[k] : t.lo[k] + t.ext[k] - width;
+    int64_t start[3], cnt[3];
+    slab_spans(t, k, r0, r0 + width, start, cnt);
+    if (t.n * cnt[0] * cnt[1] * cnt[2] == 0) return SHARD_OK;
+    if (!tile || !slab || !aligned(tile, t.esz) || !aligned(slab, t.esz)) return SHARD_ERR_INVALID;
+    return map_hip(launch_box_copy(make_box(t, k, r0, r0 + width), TILE_TO_SLAB, tile, slab, stream));
+}
+
+shard_status_t shard_halo_unpack(const shard_tile_t* x, shard_dtype_t dtype, void* tile, int32_t axis,
+                                 int32_t side, const void* slab, hipStream_t stream)
+{
+    Tile3 t;
+    if (!norm_tile(x, dtype, t) || axis < 0 || axis >= x->ndim || (side != 0 && side != 1))
+        return SHARD_ERR_INVALID;
+    const int k = 3 - x->ndim + axis;
+    const int64_t r0 = side == 0 ? 0 : t.lo[k] + t.ext[k];
+    const int64_t r1 = side == 0 ? t.lo[k] : t.P[k];
+    int64_t start[3], cnt[3];
+    slab_spans(t, k, r0, r1, start, cnt);
+    if (t.n * cnt[0] * cnt[1] * cnt[2] == 0) return SHARD_OK;
+    if (!tile || !aligned(tile, t.esz) || (slab && !aligned(slab, t.esz))) return SHARD_ERR_INVALID;
+    const BoxCopy b = make_box(t, k, r0, r1);
+    if (!slab) return map_hip(launch_box_copy(b, ZERO_TILE, nullptr, tile, stream));
+    return map_hip(launch_box_copy(b, SLAB_TO_TILE, slab, tile, stream));
+}
+
+size_t shard_conv_workspace_bytes(int32_t op, const shard_tile_t* x, shard_dtype_t dtype, int64_t c_out,
+                                  const int64_t kernel[], const int64_t stride[], const int64_t out_ext[])
+{
+    Tile3 t;
+    Conv3 cv;
+    if ((op != 0 && op != 1) || !norm_tile(x, dtype, t) || !norm_conv(x, t, c_out, kernel, stride, nullptr, out_ext, cv))
+        return size_t(-1);
+    if (op == 0) return conv_fwd_workspace(t, cv, dtype);
+    return conv_wgrad_workspace(t, cv, dtype);
+}
+
+shard_status_t shard_conv_fwd(const shard_tile_t* x, shard_dtype_t dtype, const void* tile, const void* w,
+                              int64_t c_out, const int64_t kernel[], const int64_t stride[], const int64_t pad_lo[],
+                              const int64_t out_ext[], void* y, void* ws, size_t ws_bytes, hipStream_t stream)
+{
+    Tile3 t;
+    Conv3 cv;
+    if (!norm_tile(x, dtype, t) || !pad_lo || !norm_conv(x, t, c_out, kernel, stride, pad_lo, out_ext, cv))
+        return SHARD_ERR_INVALID;
+    if (t.n * cv.out_voxels() == 0) return SHARD_OK;
+    const size_t need = conv_fwd_workspace(t, cv, dtype);
+    if (ws_bytes < need || (need > 0 && !ws)) return SHARD_ERR_INVALID;
+    if ((tile_elems(t) > 0 && !tile) || !w || !y) return SHARD_ERR_INVALID;
+    if (!aligned(tile, t.esz) || !aligned(w, t.esz) || !aligned(y, t.esz) || !aligned(ws, 16))
+        return SHARD_ERR_INVALID;
+    return map_hip(launch_conv_fwd(t, cv, dtype, tile, w, y, ws, stream));
+}
+
+shard_status_t shard_conv_wgrad(const shard_tile_t* x, shard_dtype_t dtype, const void* tile, const void* dy,
+                                int64_t c_out, const int64_t kernel[], const int64_t stride[], const int64_t pad_lo[],
+                                const int64_t out_ext[], float* dw, void* ws, size_t ws_bytes, hipStream_t stream)
+{
+    Tile3 t;
+    Conv3 cv;
+    if (!norm_tile(x, dtype, t) || !pad_lo || !norm_conv(x, t, c_out, kernel, stride, pad_lo, out_ext, cv))
+        return SHARD_ERR_INVALID;
+    const size_t need = conv_wgrad_workspace(t, cv, dtype);
+    if (ws_bytes < need || (need > 0 && !ws)) return SHARD_ERR_INVALID;
+    if (!dw || !aligned(dw, 4) || !aligned(ws, 16)) return SHARD_ERR_INVALID;
+    const bool empty = t.n * cv.out_voxels() == 0;
+    if (!empty && ((tile_elems(t) > 0 && !tile) || !dy)) return SHARD_ERR_INVALID;
+    if (!aligned(tile, t.esz) || !aligned(dy, t.esz)) return SHARD_ERR_INVALID;
+    if (empty) return map_hip(generic_conv_wgrad(t, cv, dtype, tile, dy, dw, ws, stream));
+    return map_hip(launch_conv_wgrad(t, cv, dtype, tile, dy, dw, ws, stream));
+}
+
+}  // extern "C"

@@ -1,0 +1,460 @@
+// Forward convolution over a padded tile as an implicit GEMM on MFMA.
+//
+// GEMM view: M = output voxels, N = output channels, K = taps x input
+// channels. Nothing is materialised: a workgroup owns an output brick of
+// BO0 x BO1 x BO2 voxels (flattened row-major, W fastest) and all-or-part of
+// the output channels. It stages the brick's input footprint (the brick grown
+// by the kernel reach, which is where the halo margins of the tile enter) in
+// LDS once per channel pass, then every tap reads its A operand from that LDS
+// copy at a shifted voxel offset; out-of-tile voxels are written as zeros while
+// staging, which is the zero padding on unsharded axes.
+//
+// MFMA operand layout (32x32 output tile, 64 lanes, lane group g = lane/32):
+//   bf16 v_mfma_f32_32x32x16_bf16: lane holds 8 consecutive K (= 8 channels of
+//        one voxel) for row lane%32 -> one 16-byte LDS read per lane.
+//   f32  v_mfma_f32_32x32x2_f32: lane holds 1 K value; four MFMAs consume one
+//        16-byte read of 4 consecutive channels (K order permuted so that lane
+//        group g of step s holds channel 8*c + 4*g + s in both operands).
+// The B operand (weights) is pre-arranged by `wfrag_kernel` so that one
+// coalesced 1 KiB load per wave yields a ready fragment.
+//
+// LDS layout: voxel v of the input brick occupies NQ 16-byte units; unit q
+// of voxel v sits at v*NQ + (q ^ swz(v)), an XOR swizzle that spreads the 16
+// lanes of a ds_read_b128 phase over distinct bank groups for unit-stride rows.
+#include <algorithm>
+#include <cstdlib>
+#include <type_traits>
+
+#include "common.h"
+#include "internal.h"
+
+namespace shardconv {
+
+typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8_t;
+typedef __attribute__((ext_vector_type(16))) float f32x16_t;
+
+namespace {
+
+constexpr int kWaves = 4;
+constexpr int kThreads = 64 * kWaves;
+
+struct FwdArgs {
+    const char* tile;
+    const uint4* wfrag;
+    char* y;
+    int64_t n, cin, cout;
+    int64_t P[3];      // padded tile extents
+    int64_t O[3];      // output extents
+    int32_t K[3], S[3], pad[3];
+    int32_t BO[3];     // output brick
+    int32_t BI[3];     // input brick
+    int32_t NB[3];     // bricks per axis
+    int32_t nq;        // 16-byte units per voxel in LDS (per pass)
+    int32_t vpl_s;     // swizzle divisor (voxels per 256 B line, times W stride)
+    int32_t qmask;     // swizzle mask
+    int32_t cc;        // channels per pass
+    int32_t npass;
+    int32_t nkc;       // K-chunks over all input channels
+    int32_t nt;        // 32-wide N tiles over all output channels
+    int32_t ng;        // N groups (workgroups along N)
+    int64_t nblocks;
+};
+
+struct PlanF {
+    int rm, rn;
+    FwdArgs a;
+    size_t lds;
+    bool ok;
+};
+
+template <typename T>
+struct Traits;
+template <>
+struct Traits<bf16_t> {
+    static constexpr int kc = 16;  // channels per MFMA K-chunk
+    static constexpr int esz = 2;
+};
+template <>
+struct Traits<float> {
+    static constexpr int kc = 8;
+    static constexpr int esz = 4;
+};
+
+__device__ __forceinline__ int swz(int v, int vpl_s, int qmask) { return (v / vpl_s) & qmask; }
+
+// Stage the input brick channels [c0, c0 + cc) into LDS.
+template <typename T>
+__device__ __forceinline__ void stage_brick(const FwdArgs& a, uint4* lds, int64_t nn, const int64_t i0[3], int c0)
+{
+    constexpr int kPerUnit = 16 / Traits<T>::esz;
+    const int nq = a.nq;
+    const int biv = a.BI[0] * a.BI[1] * a.BI[2];
+    const int total = biv * nq;
+    const bool vec_ok = (a.cin * Traits<T>::esz) % 16 == 0;
+    for (int u = threadIdx.x; u < total; u += kThreads) {
+        const int q = u % nq;
+        const int v = u / nq;
+        const int x = v % a.BI[2];
+        const int yz = v / a.BI[2];
+        const int y = yz % a.BI[1];
+        const int z = yz / a.BI[1];
+        const int64_t t0 = i0[0] + z, t1 = i0[1] + y, t2 = i0[2] + x;
+        const int c = c0 + q * kPerUnit;
+        uint4 val = make_uint4(0, 0, 0, 0);
+        if (t0 >= 0 && t0 < a.P[0] && t1 >= 0 && t1 < a.P[1] && t2 >= 0 && t2 < a.P[2] && c < a.cin) {
+            const int64_t off = ((((nn * a.P[0] + t0) * a.P[1] + t1) * a.P[2] + t2) * a.cin + c) * Traits<T>::esz;
+            if (vec_ok && c + kPerUnit <= a.cin) {
+                val = *reinterpret_cast<const uint4*>(a.tile + off);
+            } else {
+                T tmp[kPerUnit];
+                const T* src = reinterpret_cast<const T*>(a.tile + off);
+#pragma unroll
+                for (int e = 0; e < kPerUnit; ++e) tmp[e] = (c + e < a.cin) ? src[e] : T(0);
+                val = *reinterpret_cast<const uint4*>(tmp);
+            }
+        }
+        lds[v * nq + (q ^ swz(v, a.vpl_s, a.qmask))] = val;
+    }
+}
+
+template <typename T>
+__device__ __forceinline__ void mfma_step(f32x16_t& acc, uint4 av, uint4 bv);
+
+template <>
+__device__ __forceinline__ void mfma_step<bf16_t>(f32x16_t& acc, uint4 av, uint4 bv)
+{
+    acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8_t, av), __builtin_bit_cast(bf16x8_t, bv),
+                                                   acc, 0, 0, 0);
+}
+
+template <>
+__device__ __forceinline__ void mfma_step<float>(f32x16_t& acc, uint4 av, uint4 bv)
+{
+    acc = __builtin_amdgcn_mfma_f32_32x32x2f32(__uint_as_float(av.x), __uint_as_float(bv.x), acc, 0, 0, 0);
+    acc = __builtin_amdgcn_mfma_f32_32x32x2f32(__uint_as_float(av.y), __uint_as_float(bv.y), acc, 0, 0, 0);
+    acc = __builtin_amdgcn_mfma_f32_32x32x2f32(__uint_as_float(av.z), __uint_as_float(bv.z), acc, 0, 0, 0);
+    acc = __builtin_amdgcn_mfma_f32_32x32x2f32(__uint_as_float(av.w), __uint_as_float(bv.w), acc, 0, 0, 0);
+}
+
+template <typename T, int RM, int RN>
+__global__ __launch_bounds__(kThreads, 2) void conv_fwd_tiled(FwdArgs a)
+{
+    extern __shared__ uint4 lds[];
+    const int lane = threadIdx.x & 63;
+    const int wave = threadIdx.x >> 6;
+    const int g = lane >> 5;
+    const int row = lane & 31;
+
+    // block -> (n, brick, N group), XCD-aware
+    int64_t b = xcd_remap(blockIdx.x, a.nblocks);
+    const int ngi = int(b % a.ng);
+    b /= a.ng;
+    const int bx = int(b % a.NB[2]);
+    b /= a.NB[2];
+    const int by = int(b % a.NB[1]);
+    b /= a.NB[1];
+    const int bz = int(b % a.NB[0]);
+    const int64_t nn = b / a.NB[0];
+    const int64_t ob[3] = {int64_t(bz) * a.BO[0], int64_t(by) * a.BO[1], int64_t(bx) * a.BO[2]};
+    const int64_t i0[3] = {ob[0] * a.S[0] - a.pad[0], ob[1] * a.S[1] - a.pad[1], ob[2] * a.S[2] - a.pad[2]};
+    const int nt0 = ngi * RN;
+    const int bov = a.BO[0] * a.BO[1] * a.BO[2];
+
+    // per-lane LDS voxel base of each of this wave's M tiles
+    int vbase[RM];
+#pragma unroll
+    for (int i = 0; i < RM; ++i) {
+        const int f = (wave * RM + i) * 32 + row;
+        const int ff = f < bov ? f : 0;
+        const int ox = ff % a.BO[2];
+        const int oy = (ff / a.BO[2]) % a.BO[1];
+        const int oz = ff / (a.BO[2] * a.BO[1]);
+        vbase[i] = (oz * a.S[0] * a.BI[1] + oy * a.S[1]) * a.BI[2] + ox * a.S[2];
+    }
+
+    f32x16_t acc[RM][RN];
+#pragma unroll
+    for (int i = 0; i < RM; ++i)
+#pragma unroll
+        for (int j = 0; j < RN; ++j)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
+
+    const int taps = a.K[0] * a.K[1] * a.K[2];
+    const int kcp = a.cc / Traits<T>::kc;  // K-chunks per pass
+    const int plane = a.BI[1] * a.BI[2];
+    for (int p = 0; p < a.npass; ++p) {
+        if (p > 0) __syncthreads();
+        stage_brick<T>(a, lds, nn, i0, p * a.cc);
+        __syncthreads();
+        const int iters = taps * kcp;
+        // software pipeline: fetch the B fragments of the next iteration early
+        uint4 bcur[RN];
+        {
+            const int64_t fb = (int64_t(0) * a.nkc + p * kcp) * a.nt + nt0;
+#pragma unroll
+            for (int j = 0; j < RN; ++j) bcur[j] = a.wfrag[(fb + j) * 64 + lane];
+        }
+        int t0 = 0, t1 = 0, t2 = 0, kc = 0;
+        for (int it = 0; it < iters; ++it) {
+            // next (tap, kc)
+            int nkc_ = kc + 1, n2 = t2, n1 = t1, n0 = t0;
+            if (nkc_ == kcp) {
+                nkc_ = 0;
+                if (++n2 == a.K[2]) {
+                    n2 = 0;
+                    if (++n1 == a.K[1]) {
+                        n1 = 0;
+                        ++n0;
+                    }
+                }
+            }
+            uint4 bnext[RN];
+            if (it + 1 < iters) {
+                const int ntap = (n0 * a.K[1] + n1) * a.K[2] + n2;
+                const int64_t fb = (int64_t(ntap) * a.nkc + p * kcp + nkc_) * a.nt + nt0;
+#pragma unroll
+                for (int j = 0; j < RN; ++j) bnext[j] = a.wfrag[(fb + j) * 64 + lane];
+            }
+            const int toff = t0 * plane + t1 * a.BI[2] + t2;
+            const int q = 2 * kc + g;
+            uint4 av[RM];
+#pragma unroll
+            for (int i = 0; i < RM; ++i) {
+                const int v = vbase[i] + toff;
+                av[i] = lds[v * a.nq + (q ^ swz(v, a.vpl_s, a.qmask))];
+            }
+#pragma unroll
+            for (int i = 0; i < RM; ++i)
+#pragma unroll
+                for (int j = 0; j < RN; ++j) mfma_step<T>(acc[i][j], av[i], bcur[j]);
+#pragma unroll
+            for (int j = 0; j < RN; ++j) bcur[j] = bnext[j];
+            kc = nkc_;
+            t0 = n0;
+            t1 = n1;
+            t2 = n2;
+        }
+    }
+
+    // epilogue: lane holds column lane%32, rows 8*(r/4) + 4*g + (r%4)
+    T* y = reinterpret_cast<T*>(a.y);
+#pragma unroll
+    for (int i = 0; i < RM; ++i) {
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+            const int f = (wave * RM + i) * 32 + 8 * (r >> 2) + 4 * g + (r & 3);
+            if (f >= bov) continue;
+            const int ox = f % a.BO[2];
+            const int oy = (f / a.BO[2]) % a.BO[1];
+            const int oz = f / (a.BO[2] * a.BO[1]);
+            const int64_t o0 = ob[0] + oz, o1 = ob[1] + oy, o2 = ob[2] + ox;
+            if (o0 >= a.O[0] || o1 >= a.O[1] || o2 >= a.O[2]) continue;
+            const int64_t vox = ((nn * a.O[0] + o0) * a.O[1] + o1) * a.O[2] + o2;
+#pragma unroll
+            for (int j = 0; j < RN; ++j) {
+                const int64_t co = int64_t(nt0 + j) * 32 + row;
+                if (co < a.cout) y[vox * a.cout + co] = from_f32<T>(acc[i][j][r]);
+            }
+        }
+    }
+}
+
+// wfrag[((tap * nkc + kc) * nt + ntile) * 64 + lane] = 16 bytes of weights in
+// MFMA B-fragment order (see the file comment); zero past cin / cout.
+template <typename T>
+__global__ __launch_bounds__(256) void wfrag_kernel(const T* w, uint4* wfrag, int64_t cin, int64_t cout, int taps,
+                                                    int nkc, int nt)
+{
+    constexpr int kPer = 16 / Traits<T>::esz;
+    const int64_t total = int64_t(taps) * nkc * nt * 64;
+    for (int64_t e = int64_t(blockIdx.x) * 256 + threadIdx.x; e < total; e += int64_t(gridDim.x) * 256) {
+        const int lane = int(e % 64);
+        int64_t r = e / 64;
+        const int ntile = int(r % nt);
+        r /= nt;
+        const int kc = int(r % nkc);
+        const int tap = int(r / nkc);
+        const int64_t co = int64_t(ntile) * 32 + (lane & 31);
+        const int g = lane >> 5;
+        T vals[kPer];
+#pragma unroll
+        for (int s = 0; s < kPer; ++s) {
+            const int64_t ci = int64_t(kc) * Traits<T>::kc + g * kPer + s;
+            vals[s] = (co < cout && ci < cin) ? w[(co * cin + ci) * taps + tap] : T(0);
+        }
+        wfrag[e] = *reinterpret_cast<const uint4*>(vals);
+    }
+}
+
+template <typename T>
+PlanF plan_fwd_t(const Tile3& t, const Conv3& cv)
+{
+    PlanF pl{};
+    constexpr int kc = Traits<T>::kc;
+    constexpr int esz = Traits<T>::esz;
+    const int64_t nt = ceil_div(cv.cout, 32);
+    int rn, rm;
+    if (std::is_same<T, bf16_t>::value) {
+        rn = nt >= 2 ? 2 : 1;
+        rm = 4;
+    } else {
+        rn = nt >= 4 ? 4 : (nt >= 2 ? 2 : 1);
+        rm = rn == 4 ? 1 : (rn == 2 ? 2 : 4);
+    }
+    const int64_t cap = int64_t(kWaves) * rm * 32;
+    const int64_t cfull = round_up(t.c, kc);
+    const size_t kLdsPref = 80 * 1024, kLdsMax = 160 * 1024;
+
+    double best = 1e300;
+    FwdArgs bestA{};
+    size_t bestLds = 0;
+    auto consider = [&](int64_t b0, int64_t b1, int64_t b2) {
+        if (b0 < 1 || b1 < 1 || b2 < 1 || b0 * b1 * b2 > cap) return;
+        int64_t bi[3], bo[3] = {b0, b1, b2};
+        int64_t biv = 1;
+        for (int k = 0; k < 3; ++k) {
+            bi[k] = (bo[k] - 1) * cv.S[k] + cv.K[k];
+            biv *= bi[k];
+        }
+        // channel pass width: the largest multiple of kc whose brick fits
+        int64_t cc = cfull;
+        while (cc > kc && size_t(biv * cc * esz) > kLdsPref) cc = round_up(cc / 2, kc);
+        size_t lds = size_t(biv * cc * esz);
+        if (lds > kLdsMax) return;
+        double eff = double(b0 * b1 * b2) / double(cap);
+        for (int k = 0; k < 3; ++k) {
+            const int64_t nb = ceil_div(cv.O[k], bo[k]);
+            eff *= double(cv.O[k]) / double(nb * bo[k]);
+        }
+        double cost = double(biv) / double(b0 * b1 * b2) / eff;
+        if (lds > kLdsPref) cost *= 1.5;
+        cost *= 1.0 + 0.02 * double(ceil_div(cfull, cc) - 1);
+        if (cost < best) {
+            best = cost;
+            bestLds = lds;
+            FwdArgs a{};
+            for (int k = 0; k < 3; ++k) {
+                a.BO[k] = int32_t(bo[k]);
+                a.BI[k] = int32_t(bi[k]);
+                a.NB[k] = int32_t(ceil_div(cv.O[k], bo[k]));
+            }
+            a.cc = int32_t(cc);
+            bestA = a;
+        }
+    };
+    for (int64_t b2 = 1; b2 <= cap; b2 *= 2) {
+        const int64_t w2 = std::min(b2, cv.O[2]);
+        for (int64_t b1 = 1; b1 * w2 <= cap; b1 *= 2) {
+            const int64_t w1 = std::min(b1, cv.O[1]);
+            const int64_t w0 = std::min(cap / (w1 * w2), cv.O[0]);
+            consider(w0, w1, w2);
+            for (int64_t b0 = 1; b0 < w0; b0 *= 2) consider(b0, w1, w2);
+        }
+    }
+    if (best >= 1e299) return pl;
+    FwdArgs& a = bestA;
+    a.n = t.n;
+    a.cin = t.c;
+    a.cout = cv.cout;
+    for (int k = 0; k < 3; ++k) {
+        a.P[k] = t.P[k];
+        a.O[k] = cv.O[k];
+        a.K[k] = int32_t(cv.K[k]);
+        a.S[k] = int32_t(cv.S[k]);
+        a.pad[k] = int32_t(cv.pad[k]);
+    }
+    a.nq = int32_t(a.cc * esz / 16);
+    const int vpl = std::max(1, 16 / a.nq);
+    a.vpl_s = int32_t(vpl * a.S[2]);
+    // XOR swizzle only when the unit count is a power of two (stays inside the voxel)
+    a.qmask = (a.nq & (a.nq - 1)) == 0 ? int32_t(std::min(a.nq, 16) - 1) : 0;
+    a.npass = int32_t(ceil_div(cfull, a.cc));
+    // fragment counts cover every index the kernel forms: npass * (cc / kc)
+    // K-chunks and ng * rn N tiles; the padding holds zero weights
+    a.nkc = int32_t(int64_t(a.npass) * (a.cc / kc));
+    a.ng = int32_t(ceil_div(nt, rn));
+    a.nt = int32_t(int64_t(a.ng) * rn);
+    a.nblocks = t.n * int64_t(a.NB[0]) * a.NB[1] * a.NB[2] * a.ng;
+    pl.rm = rm;
+    pl.rn = rn;
+    pl.a = a;
+    pl.lds = bestLds;
+    pl.ok = a.nblocks > 0 && a.nblocks < (int64_t(1) << 31);
+    return pl;
+}
+
+bool tiled_supported(const Tile3& t, const Conv3& cv)
+{
+    // int32 LDS/brick indexing and per-axis sizes; the host planner checks LDS.
+    for (int k = 0; k < 3; ++k)
+        if (cv.K[k] > 64 || cv.S[k] > 64 || cv.O[k] > (int64_t(1) << 30) || std::abs(cv.pad[k]) > (1 << 29))
+            return false;
+    return t.c <= 4096 && cv.cout <= 4096;
+}
+
+template <typename T>
+size_t wfrag_bytes(const Tile3& t, const Conv3& cv)
+{
+    const PlanF pl = plan_fwd_t<T>(t, cv);
+    if (!pl.ok) return 0;
+    return size_t(cv.taps()) * size_t(pl.a.nkc) * size_t(pl.a.nt) * 64 * 16;
+}
+
+template <typename T, int RM, int RN>
+hipError_t launch_tiled(const PlanF& pl, hipStream_t s)
+{
+    auto fn = &conv_fwd_tiled<T, RM, RN>;
+    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(fn), hipFuncAttributeMaxDynamicSharedMemorySize,
+                                       int(pl.lds));
+    if (e != hipSuccess) return e;
+    FwdArgs a = pl.a;
+    void* args[] = {&a};
+    return hipLaunchKernel(reinterpret_cast<const void*>(fn), dim3(unsigned(a.nblocks)), dim3(kThreads), args,
+                           pl.lds, s);
+}
+
+template <typename T>
+hipError_t run_fwd(const Tile3& t, const Conv3& cv, const void* tile, const void* w, void* y, void* ws,
+                   hipStream_t s)
+{
+    PlanF pl = plan_fwd_t<T>(t, cv);
+    if (!pl.ok) return hipErrorInvalidValue;
+    pl.a.tile = static_cast<const char*>(tile);
+    pl.a.wfrag = static_cast<const uint4*>(ws);
+    pl.a.y = static_cast<char*>(y);
+    const int taps = int(cv.taps());
+    const int64_t frag_total = int64_t(taps) * pl.a.nkc * pl.a.nt * 64;
+    const unsigned fg = unsigned(std::max<int64_t>(1, std::min<int64_t>(ceil_div(frag_total, 256), 4096)));
+    hipLaunchKernelGGL(wfrag_kernel<T>, dim3(fg), dim3(256), 0, s, static_cast<const T*>(w),
+                       static_cast<uint4*>(ws), t.c, cv.cout, taps, pl.a.nkc, pl.a.nt);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    if (pl.rm == 4 && pl.rn == 1) return launch_tiled<T, 4, 1>(pl, s);
+    if (pl.rm == 4 && pl.rn == 2) return launch_tiled<T, 4, 2>(pl, s);
+    if (pl.rm == 2 && pl.rn == 2) return launch_tiled<T, 2, 2>(pl, s);
+    if (pl.rm == 1 && pl.rn == 4) return launch_tiled<T, 1, 4>(pl, s);
+    return hipErrorInvalidValue;
+}
+
+}  // namespace
+
+size_t generic_wgrad_workspace(const Tile3& t, const Conv3& cv);
+hipError_t generic_conv_fwd(const Tile3& t, const Conv3& cv, shard_dtype_t dt, const void* tile, const void* w,
+                            void* y, hipStream_t s);
+
+size_t conv_fwd_workspace(const Tile3& t, const Conv3& cv, shard_dtype_t dt)
+{
+    return dt == SHARD_BF16 ? wfrag_bytes<bf16_t>(t, cv) : wfrag_bytes<float>(t, cv);
+}
+
+hipError_t launch_conv_fwd(const Tile3& t, const Conv3& cv, shard_dtype_t dt, const void* tile, const void* w,
+                           void* y, void* ws, hipStream_t s)
+{
+    const bool tiled = !force_generic() && tiled_supported(t, cv) &&
+                       (dt == SHARD_BF16 ? plan_fwd_t<bf16_t>(t, cv).ok : plan_fwd_t<float>(t, cv).ok);
+    if (!tiled) return generic_conv_fwd(t, cv, dt, tile, w, y, s);
+    return dt == SHARD_BF16 ? run_fwd<bf16_t>(t, cv, tile, w, y, ws, s) : run_fwd<float>(t, cv, tile, w, y, ws, s);
+}
+
+}  // namespace shardconv

@@ -1,0 +1,130 @@
+// Halo pack / unpack / zero-fill: a box copy between a padded tile and a dense
+// slab (the two halves of the halo exchange a shard performs before its local
+// convolution, ShardTensor section "PyTorch Dispatch").
+//
+// The box is `rows` runs of `run` contiguous bytes (contiguous inner axes are
+// merged on the host). Each thread moves U vectors of V bytes, all loads issued
+// before any store; consecutive lanes touch consecutive vectors, so every wave
+// instruction covers 64*V contiguous bytes. A single-run box (the common case
+// of a slab along the outermost sharded axis, which is one contiguous block of
+// the tile) takes a specialisation with no index arithmetic.
+#include <algorithm>
+
+#include "internal.h"
+
+namespace shardconv {
+namespace {
+
+struct CopyArgs {
+    const char* src;
+    char* dst;
+    int64_t base;        // tile byte offset of the first run
+    int64_t cnt1, cnt2;  // inner two outer counts (cnt0 is implied by total)
+    int64_t t0, t1, t2;  // tile byte strides of the three outer dims
+    int64_t nvec_row;    // vectors per run
+    int64_t total;       // total vectors
+    int dir;             // CopyDir
+};
+
+constexpr int kThreads = 256;
+constexpr int kUnroll = 4;
+
+template <int V>
+struct Vec;
+template <>
+struct Vec<16> { using T = uint4; };
+template <>
+struct Vec<4> { using T = uint32_t; };
+template <>
+struct Vec<2> { using T = uint16_t; };
+
+template <int V, bool kSingleRun>
+__device__ __forceinline__ int64_t tile_offset(const CopyArgs& a, int64_t v)
+{
+    if (kSingleRun) return a.base + v * V;
+    const int64_t row = v / a.nvec_row;
+    const int64_t col = v - row * a.nvec_row;
+    const int64_t i2 = row % a.cnt2;
+    const int64_t r1 = row / a.cnt2;
+    const int64_t i1 = r1 % a.cnt1;
+    const int64_t i0 = r1 / a.cnt1;
+    return a.base + i0 * a.t0 + i1 * a.t1 + i2 * a.t2 + col * V;
+}
+
+template <int V, bool kSingleRun>
+__global__ __launch_bounds__(kThreads) void box_copy_kernel(CopyArgs a)
+{
+    using T = typename Vec<V>::T;
+    const int64_t nthreads = int64_t(gridDim.x) * kThreads;
+    const int64_t tid = int64_t(blockIdx.x) * kThreads + threadIdx.x;
+    for (int64_t v0 = tid; v0 < a.total; v0 += nthreads * kUnroll) {
+        T val[kUnroll];
+        int64_t off[kUnroll];
+#pragma unroll
+        for (int u = 0; u < kUnroll; ++u) {
+            const int64_t v = v0 + u * nthreads;
+            off[u] = v < a.total ? tile_offset<V, kSingleRun>(a, v) : 0;
+            if (v < a.total) {
+                if (a.dir == TILE_TO_SLAB) {
+                    val[u] = *reinterpret_cast<const T*>(a.src + off[u]);
+                } else if (a.dir == SLAB_TO_TILE) {
+                    val[u] = *reinterpret_cast<const T*>(a.src + v * V);
+                } else {
+                    val[u] = T{};
+                }
+            }
+        }
+#pragma unroll
+        for (int u = 0; u < kUnroll; ++u) {
+            const int64_t v = v0 + u * nthreads;
+            if (v < a.total) {
+                if (a.dir == TILE_TO_SLAB) {
+                    *reinterpret_cast<T*>(a.dst + v * V) = val[u];
+                } else {
+                    *reinterpret_cast<T*>(a.dst + off[u]) = val[u];
+                }
+            }
+        }
+    }
+}
+
+template <int V>
+hipError_t launch_v(const BoxCopy& b, CopyDir dir, const void* src, void* dst, hipStream_t s)
+{
+    CopyArgs a;
+    a.src = static_cast<const char*>(src);
+    a.dst = static_cast<char*>(dst);
+    a.base = b.base;
+    a.cnt1 = b.cnt[1];
+    a.cnt2 = b.cnt[2];
+    a.t0 = b.tstride[0];
+    a.t1 = b.tstride[1];
+    a.t2 = b.tstride[2];
+    a.nvec_row = b.run / V;
+    const int64_t rows = b.cnt[0] * b.cnt[1] * b.cnt[2];
+    a.total = rows * a.nvec_row;
+    a.dir = dir;
+    const int64_t per_block = int64_t(kThreads) * kUnroll;
+    const int64_t blocks = std::max<int64_t>(1, std::min<int64_t>(ceil_div(a.total, per_block), 1 << 20));
+    void* args[] = {&a};
+    const void* fn = rows == 1 ? reinterpret_cast<const void*>(&box_copy_kernel<V, true>)
+                               : reinterpret_cast<const void*>(&box_copy_kernel<V, false>);
+    return hipLaunchKernel(fn, dim3(unsigned(blocks)), dim3(kThreads), args, 0, s);
+}
+
+}  // namespace
+
+hipError_t launch_box_copy(const BoxCopy& b, CopyDir dir, const void* src, void* dst, hipStream_t s)
+{
+    const uintptr_t tile_ptr = reinterpret_cast<uintptr_t>(dir == TILE_TO_SLAB ? src : dst);
+    const uintptr_t slab_ptr = reinterpret_cast<uintptr_t>(dir == TILE_TO_SLAB ? dst : src);
+    auto ok = [&](int64_t v) {
+        return (b.base % v) == 0 && (b.run % v) == 0 && (b.tstride[0] % v) == 0 && (b.tstride[1] % v) == 0 &&
+               (b.tstride[2] % v) == 0 && (tile_ptr % v) == 0 && (dir == ZERO_TILE || (slab_ptr % v) == 0);
+    };
+    if (ok(16)) return launch_v<16>(b, dir, src, dst, s);
+    if (ok(4)) return launch_v<4>(b, dir, src, dst, s);
+    return launch_v<2>(b, dir, src, dst, s);
+}
+
+}  // namespace shardconv

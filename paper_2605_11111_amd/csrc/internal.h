@@ -1,0 +1,62 @@
+// Internal interfaces between the C-ABI layer (api.cpp) and the HIP kernels.
+// Every public call is normalised to three spatial axes: a 2D problem gets a
+// leading unit axis and a 1D problem two, with kernel 1, stride 1, pad 0 there.
+#pragma once
+
+#include <cstddef>
+#include <cstdint>
+
+#include <hip/hip_runtime.h>
+
+#include "shardconv.h"
+
+namespace shardconv {
+
+// A padded tile: dense [n][P0][P1][P2][c], all sizes in elements.
+struct Tile3 {
+    int64_t n, c;
+    int64_t P[3];                 // padded extents
+    int64_t lo[3], ext[3], hi[3]; // margins and interior
+    int esz;                      // bytes per element (2 or 4)
+};
+
+// A convolution read off a padded tile (see shard_conv_fwd).
+struct Conv3 {
+    int64_t cout;
+    int64_t K[3], S[3], pad[3], O[3];
+    int64_t taps() const { return K[0] * K[1] * K[2]; }
+    int64_t out_voxels() const { return O[0] * O[1] * O[2]; }
+};
+
+// A box copy between a tile and a dense slab (pack, unpack, zero fill).
+// After merging contiguous inner axes the box is `rows` = c0*c1*c2 runs of
+// `run` bytes; run r = (i0, i1, i2) starts at tile byte offset
+// base + i0*t0 + i1*t1 + i2*t2 and at slab byte offset r*run.
+struct BoxCopy {
+    int64_t base;
+    int64_t cnt[3];
+    int64_t tstride[3];
+    int64_t run;
+};
+
+enum CopyDir { TILE_TO_SLAB = 0, SLAB_TO_TILE = 1, ZERO_TILE = 2 };
+
+hipError_t launch_box_copy(const BoxCopy& b, CopyDir dir, const void* src, void* dst, hipStream_t s);
+
+// Convolution launchers. `ws` holds at least conv_*_workspace(...) bytes.
+size_t conv_fwd_workspace(const Tile3& t, const Conv3& cv, shard_dtype_t dt);
+size_t conv_wgrad_workspace(const Tile3& t, const Conv3& cv, shard_dtype_t dt);
+hipError_t launch_conv_fwd(const Tile3& t, const Conv3& cv, shard_dtype_t dt, const void* tile, const void* w,
+                           void* y, void* ws, hipStream_t s);
+hipError_t launch_conv_wgrad(const Tile3& t, const Conv3& cv, shard_dtype_t dt, const void* tile, const void* dy,
+                             float* dw, void* ws, hipStream_t s);
+
+// Which implementation a call takes. "generic" forces the plain direct kernels
+// (used by tests to cross-check the tiled MFMA kernels); read from the
+// environment variable SHARDCONV_ALGO at each call.
+bool force_generic();
+
+inline int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
+inline int64_t round_up(int64_t a, int64_t b) { return ceil_div(a, b) * b; }
+
+}  // namespace shardconv

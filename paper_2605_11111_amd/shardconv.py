@@ -1,0 +1,167 @@
+"""Python binding of libshardconv (the shard halo-convolution hot path on MI355X).
+
+Argument marshalling only: every function forwards to the C-ABI entry point of
+the same name in ``libshardconv.so`` (see ``include/shardconv.h`` for the
+semantics, layouts and error behaviour), passing raw device pointers of torch
+tensors and torch's current HIP stream. Every step of the hot path runs in the
+library's HIP kernels; there is no fallback: if the library is not built,
+importing this package raises.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libshardconv.so")
+
+SHARD_OK, SHARD_ERR_INVALID, SHARD_ERR_UNSUPPORTED, SHARD_ERR_HIP = 0, 1, 2, 3
+SHARD_F32, SHARD_BF16 = 0, 1
+
+if not os.path.exists(LIB_PATH):
+    raise ImportError(f"{LIB_PATH} is missing: build it first (python -m paper_2605_11111_amd.build)")
+
+_lib = ctypes.CDLL(LIB_PATH)
+_i64p = ctypes.POINTER(ctypes.c_int64)
+_vp = ctypes.c_void_p
+
+
+class shard_tile_t(ctypes.Structure):
+    _fields_ = [
+        ("ndim", ctypes.c_int32),
+        ("n", ctypes.c_int64),
+        ("c", ctypes.c_int64),
+        ("ext", ctypes.c_int64 * 3),
+        ("halo_lo", ctypes.c_int64 * 3),
+        ("halo_hi", ctypes.c_int64 * 3),
+    ]
+
+
+_tp = ctypes.POINTER(shard_tile_t)
+
+_SIGS = {
+    "shard_conv_geometry": (ctypes.c_int, [ctypes.c_int32] + [_i64p] * 11),
+    "shard_halo_slab_shape": (ctypes.c_int, [_tp, ctypes.c_int32, ctypes.c_int64, _i64p]),
+    "shard_halo_pack": (ctypes.c_int, [_tp, ctypes.c_int, _vp, ctypes.c_int32, ctypes.c_int32, ctypes.c_int64, _vp, _vp]),
+    "shard_halo_unpack": (ctypes.c_int, [_tp, ctypes.c_int, _vp, ctypes.c_int32, ctypes.c_int32, _vp, _vp]),
+    "shard_conv_fwd": (ctypes.c_int, [_tp, ctypes.c_int, _vp, _vp, ctypes.c_int64, _i64p, _i64p, _i64p, _i64p, _vp,
+                                      _vp, ctypes.c_size_t, _vp]),
+    "shard_conv_wgrad": (ctypes.c_int, [_tp, ctypes.c_int, _vp, _vp, ctypes.c_int64, _i64p, _i64p, _i64p, _i64p,
+                                        _vp, _vp, ctypes.c_size_t, _vp]),
+    "shard_conv_workspace_bytes": (ctypes.c_size_t, [ctypes.c_int32, _tp, ctypes.c_int, ctypes.c_int64, _i64p,
+                                                     _i64p, _i64p]),
+    "shard_status_string": (ctypes.c_char_p, [ctypes.c_int]),
+}
+for _name, (_res, _args) in _SIGS.items():
+    _f = getattr(_lib, _name)
+    _f.restype = _res
+    _f.argtypes = _args
+
+EXPORTED = tuple(_SIGS)
+
+
+class ShardError(RuntimeError):
+    def __init__(self, fn: str, status: int):
+        super().__init__(f"{fn}: {shard_status_string(status)} (status {status})")
+        self.status = status
+
+
+def _check(fn: str, status: int):
+    if status != SHARD_OK:
+        raise ShardError(fn, status)
+
+
+def _arr(vals, n=3):
+    v = [int(x) for x in vals] + [0] * (n - len(vals))
+    return (ctypes.c_int64 * n)(*v)
+
+
+def tile_desc(n, c, ext, halo_lo=None, halo_hi=None) -> shard_tile_t:
+    """Descriptor of a padded tile; ext/halo_lo/halo_hi are per spatial axis."""
+    nd = len(ext)
+    d = shard_tile_t()
+    d.ndim = nd
+    d.n, d.c = int(n), int(c)
+    for a in range(nd):
+        d.ext[a] = int(ext[a])
+        d.halo_lo[a] = int(halo_lo[a]) if halo_lo is not None else 0
+        d.halo_hi[a] = int(halo_hi[a]) if halo_hi is not None else 0
+    return d
+
+
+def _dtype_code(t) -> int:
+    import torch
+    if t.dtype == torch.float32:
+        return SHARD_F32
+    if t.dtype == torch.bfloat16:
+        return SHARD_BF16
+    raise TypeError(f"unsupported dtype {t.dtype}")
+
+
+def _ptr(t):
+    if t is None:
+        return None
+    if not t.is_cuda:
+        raise ValueError("device tensor required")
+    if not t.is_contiguous():
+        raise ValueError("contiguous tensor required")
+    return ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(stream):
+    if stream is not None:
+        return ctypes.c_void_p(int(stream))
+    import torch
+    return ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+
+
+def shard_status_string(status: int) -> str:
+    return _lib.shard_status_string(int(status)).decode()
+
+
+def shard_conv_geometry(global_ext, shard_off, shard_ext, kernel, stride, sharded_mask) -> dict:
+    nd = len(global_ext)
+    outs = [_arr([0] * nd) for _ in range(5)]
+    st = _lib.shard_conv_geometry(nd, _arr(global_ext), _arr(shard_off), _arr(shard_ext), _arr(kernel), _arr(stride),
+                                  _arr(sharded_mask), *outs)
+    _check("shard_conv_geometry", st)
+    keys = ("halo_lo", "halo_hi", "pad_lo", "out_off", "out_ext")
+    return {k: list(o)[:nd] for k, o in zip(keys, outs)}
+
+
+def shard_halo_slab_shape(desc: shard_tile_t, axis: int, width: int) -> list:
+    out = _arr([0] * 5, 5)
+    _check("shard_halo_slab_shape", _lib.shard_halo_slab_shape(ctypes.byref(desc), axis, width, out))
+    return list(out)
+
+
+def shard_halo_pack(desc, tile, axis, side, width, slab, stream=None):
+    _check("shard_halo_pack", _lib.shard_halo_pack(ctypes.byref(desc), _dtype_code(tile), _ptr(tile), axis, side,
+                                                   width, _ptr(slab), _stream(stream)))
+
+
+def shard_halo_unpack(desc, tile, axis, side, slab=None, stream=None):
+    _check("shard_halo_unpack", _lib.shard_halo_unpack(ctypes.byref(desc), _dtype_code(tile), _ptr(tile), axis, side,
+                                                       _ptr(slab), _stream(stream)))
+
+
+def shard_conv_workspace_bytes(op, desc, dtype_code, c_out, kernel, stride, out_ext) -> int:
+    n = _lib.shard_conv_workspace_bytes(op, ctypes.byref(desc), dtype_code, c_out, _arr(kernel), _arr(stride),
+                                        _arr(out_ext))
+    if n == ctypes.c_size_t(-1).value:
+        raise ShardError("shard_conv_workspace_bytes", SHARD_ERR_INVALID)
+    return int(n)
+
+
+def shard_conv_fwd(desc, tile, w, c_out, kernel, stride, pad_lo, out_ext, y, ws, stream=None):
+    nbytes = ws.numel() * ws.element_size() if ws is not None else 0
+    _check("shard_conv_fwd", _lib.shard_conv_fwd(ctypes.byref(desc), _dtype_code(tile), _ptr(tile), _ptr(w), c_out,
+                                                 _arr(kernel), _arr(stride), _arr(pad_lo), _arr(out_ext), _ptr(y),
+                                                 _ptr(ws), nbytes, _stream(stream)))
+
+
+def shard_conv_wgrad(desc, tile, dy, c_out, kernel, stride, pad_lo, out_ext, dw, ws, stream=None):
+    nbytes = ws.numel() * ws.element_size() if ws is not None else 0
+    _check("shard_conv_wgrad", _lib.shard_conv_wgrad(ctypes.byref(desc), _dtype_code(tile), _ptr(tile), _ptr(dy),
+                                                     c_out, _arr(kernel), _arr(stride), _arr(pad_lo), _arr(out_ext),
+                                                     _ptr(dw), _ptr(ws), nbytes, _stream(stream)))

@@ -1,0 +1,199 @@
+"""Host-side checks of the C-ABI library (no GPU needed, no kernel launched):
+it loads, exports every entry point the header declares, its closed-form
+geometry equals the oracle's enumeration, slab shapes match the oracle's
+exchange reading, and malformed calls are rejected before any launch."""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+from oracle import geometry as ogeo
+from oracle import halo as ohalo
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "shardconv.h")
+
+
+@pytest.fixture(scope="module")
+def sc():
+    from paper_2605_11111_amd import shardconv
+    return shardconv
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(shard_[a-z_0-9]+)\s*\(", text)))
+
+
+def test_library_exports_every_declared_symbol(sc):
+    names = declared_functions()
+    assert len(names) >= 8
+    lib = ctypes.CDLL(sc.LIB_PATH)
+    for n in names:
+        assert hasattr(lib, n), n
+    assert set(names) == set(sc.EXPORTED)
+
+
+def test_status_strings(sc):
+    assert sc.shard_status_string(0) == "ok"
+    assert "invalid" in sc.shard_status_string(1)
+    assert "unsupported" in sc.shard_status_string(2)
+    assert "HIP" in sc.shard_status_string(3)
+    assert sc.shard_status_string(99) == "unknown status"
+
+
+def test_geometry_equals_enumeration_on_small_grids(sc):
+    rng = np.random.default_rng(0)
+    checked = 0
+    for G in range(1, 41):
+        for K in (1, 3, 5, 7):
+            for S in (1, 2, 3):
+                for parts in range(1, min(G, 6) + 1):
+                    sizes = ogeo.chunk_sizes(G, parts)
+                    if G > parts and rng.random() < 0.5:
+                        cuts = np.sort(rng.choice(np.arange(1, G), size=parts - 1, replace=False))
+                        sizes = [int(v) for v in np.diff(np.concatenate([[0], cuts, [G]]))]
+                    for o, L in zip(ogeo.offsets(sizes), sizes):
+                        want = ogeo.axis_geometry(G, K, S, o, L, True)
+                        got = sc.shard_conv_geometry([G], [o], [L], [K], [S], [1])
+                        assert {k: v[0] for k, v in got.items()} == want, (G, K, S, o, L)
+                        checked += 1
+                want = ogeo.axis_geometry(G, K, S, 0, G, False)
+                got = sc.shard_conv_geometry([G], [0], [G], [K], [S], [0])
+                assert {k: v[0] for k, v in got.items()} == want
+    assert checked > 5000
+
+
+def test_geometry_of_the_workloads(sc):
+    import json
+    gold = json.load(open(os.path.join(ROOT, "tests", "golden", "worked_examples.json")))["workload_geometry"]
+    for name, c in gold.items():
+        if name.startswith("_"):
+            continue
+        got = sc.shard_conv_geometry(c["G"], c["o"], c["L"], c["K"], c["S"], c["sharded"])
+        for k in ("out_off", "out_ext", "halo_lo", "halo_hi", "pad_lo"):
+            assert got[k] == c[k], (name, k)
+
+
+@pytest.mark.parametrize("args", [
+    ([8], [0], [4], [2], [1], [1]),        # even kernel
+    ([8], [0], [4], [0], [1], [1]),        # kernel 0
+    ([8], [0], [4], [3], [0], [1]),        # stride 0
+    ([8], [6], [4], [3], [1], [1]),        # box beyond the domain
+    ([8], [-1], [4], [3], [1], [1]),       # negative offset
+    ([8], [0], [4], [3], [1], [0]),        # unsharded axis must be whole
+    ([0], [0], [0], [3], [1], [1]),        # empty domain
+])
+def test_geometry_rejects(sc, args):
+    with pytest.raises(sc.ShardError) as e:
+        sc.shard_conv_geometry(*args)
+    assert e.value.status == sc.SHARD_ERR_INVALID
+
+
+def test_slab_shapes_follow_the_exchange_order(sc):
+    lo, ext, hi = [2, 1, 0], [5, 4, 6], [1, 2, 3]
+    d = sc.tile_desc(2, 7, ext, lo, hi)
+    for axis in range(3):
+        for width in (0, 1, 3):
+            want = ohalo.slab_shape(2, 7, axis, width, lo, ext, hi)
+            got = sc.shard_halo_slab_shape(d, axis, width)
+            assert got == [want[0]] + want[2:] + [want[1]]
+    d2 = sc.tile_desc(1, 3, [5, 4], [1, 0], [2, 0])
+    assert sc.shard_halo_slab_shape(d2, 1, 2) == [1, 8, 2, 1, 3]
+    with pytest.raises(sc.ShardError):
+        sc.shard_halo_slab_shape(d2, 2, 1)
+    with pytest.raises(sc.ShardError):
+        sc.shard_halo_slab_shape(d2, 0, -1)
+
+
+def test_workspace_query(sc):
+    d = sc.tile_desc(1, 32, [8, 16, 40], [1, 0, 0], [1, 0, 0])
+    for op in (0, 1):
+        n = sc.shard_conv_workspace_bytes(op, d, sc.SHARD_BF16, 32, [3, 3, 3], [1, 1, 1], [8, 16, 40])
+        assert n >= 0
+    with pytest.raises(sc.ShardError):
+        sc.shard_conv_workspace_bytes(2, d, sc.SHARD_BF16, 32, [3, 3, 3], [1, 1, 1], [8, 16, 40])
+    with pytest.raises(sc.ShardError):
+        sc.shard_conv_workspace_bytes(0, d, sc.SHARD_BF16, 0, [3, 3, 3], [1, 1, 1], [8, 16, 40])
+    with pytest.raises(sc.ShardError):
+        sc.shard_conv_workspace_bytes(0, d, 7, 32, [3, 3, 3], [1, 1, 1], [8, 16, 40])
+
+
+# --- rejection before launch -------------------------------------------------
+# These calls use fake device addresses; every one must be refused by the host
+# checks. They are skipped where a GPU is visible, so that a missing check can
+# never turn into a launch on a real device.
+
+def _no_gpu():
+    try:
+        import torch
+        return not torch.cuda.is_available()
+    except Exception:
+        return True
+
+
+FAKE = ctypes.c_void_p(0x10000)
+pytestmark_host = pytest.mark.skipif(not _no_gpu(), reason="fake-pointer rejection tests run only without a GPU")
+
+
+def _raw(sc):
+    return sc._lib
+
+
+@pytestmark_host
+def test_pack_unpack_rejections(sc):
+    lib = _raw(sc)
+    d = sc.tile_desc(1, 4, [6, 5], [1, 0], [2, 0])
+    p = ctypes.byref(d)
+    assert lib.shard_halo_pack(p, 0, FAKE, 2, 0, 1, FAKE, None) == sc.SHARD_ERR_INVALID   # axis >= ndim
+    assert lib.shard_halo_pack(p, 0, FAKE, -1, 0, 1, FAKE, None) == sc.SHARD_ERR_INVALID
+    assert lib.shard_halo_pack(p, 0, FAKE, 0, 2, 1, FAKE, None) == sc.SHARD_ERR_INVALID   # side
+    assert lib.shard_halo_pack(p, 0, FAKE, 0, 0, -1, FAKE, None) == sc.SHARD_ERR_INVALID  # width < 0
+    assert lib.shard_halo_pack(p, 5, FAKE, 0, 0, 1, FAKE, None) == sc.SHARD_ERR_INVALID   # dtype
+    assert lib.shard_halo_pack(p, 0, FAKE, 0, 0, 7, FAKE, None) == sc.SHARD_ERR_UNSUPPORTED  # multi-hop
+    assert lib.shard_halo_pack(p, 0, None, 0, 0, 1, FAKE, None) == sc.SHARD_ERR_INVALID   # null tile
+    assert lib.shard_halo_pack(p, 0, FAKE, 0, 0, 1, None, None) == sc.SHARD_ERR_INVALID   # null slab
+    assert lib.shard_halo_pack(p, 0, None, 0, 0, 0, None, None) == sc.SHARD_OK            # width 0: no-op
+    assert lib.shard_halo_pack(p, 1, ctypes.c_void_p(0x10001), 0, 0, 1, FAKE, None) == sc.SHARD_ERR_INVALID
+    assert lib.shard_halo_unpack(p, 0, None, 0, 0, FAKE, None) == sc.SHARD_ERR_INVALID    # null tile
+    assert lib.shard_halo_unpack(p, 0, FAKE, 3, 0, FAKE, None) == sc.SHARD_ERR_INVALID
+    assert lib.shard_halo_unpack(p, 0, None, 1, 0, None, None) == sc.SHARD_OK             # zero-width margin
+    bad = sc.tile_desc(1, 4, [6, 5], [1, 0], [2, 0])
+    bad.ndim = 4
+    assert lib.shard_halo_pack(ctypes.byref(bad), 0, FAKE, 0, 0, 1, FAKE, None) == sc.SHARD_ERR_INVALID
+    bad2 = sc.tile_desc(1, 0, [6, 5])
+    assert lib.shard_halo_pack(ctypes.byref(bad2), 0, FAKE, 0, 0, 1, FAKE, None) == sc.SHARD_ERR_INVALID
+    bad3 = sc.tile_desc(1, 4, [6, -5])
+    assert lib.shard_halo_pack(ctypes.byref(bad3), 0, FAKE, 0, 0, 1, FAKE, None) == sc.SHARD_ERR_INVALID
+
+
+@pytestmark_host
+def test_conv_rejections(sc):
+    lib = _raw(sc)
+    A = lambda *v: (ctypes.c_int64 * 3)(*v)
+    d = sc.tile_desc(1, 16, [8, 8, 40], [1, 0, 0], [1, 0, 0])
+    p = ctypes.byref(d)
+    K, S, pad, O = A(3, 3, 3), A(1, 1, 1), A(0, 1, 1), A(8, 8, 40)
+    need = sc.shard_conv_workspace_bytes(0, d, sc.SHARD_BF16, 32, [3, 3, 3], [1, 1, 1], [8, 8, 40])
+    assert need > 0
+    f = lib.shard_conv_fwd
+    assert f(p, 1, FAKE, FAKE, 32, K, S, pad, O, FAKE, FAKE, need - 1, None) == sc.SHARD_ERR_INVALID  # short ws
+    assert f(p, 1, FAKE, FAKE, 32, K, S, pad, O, FAKE, None, need, None) == sc.SHARD_ERR_INVALID      # null ws
+    assert f(p, 1, FAKE, FAKE, 0, K, S, pad, O, FAKE, FAKE, need, None) == sc.SHARD_ERR_INVALID       # c_out 0
+    assert f(p, 1, FAKE, FAKE, 32, A(3, 0, 3), S, pad, O, FAKE, FAKE, need, None) == sc.SHARD_ERR_INVALID
+    assert f(p, 1, FAKE, FAKE, 32, K, A(1, 1, 0), pad, O, FAKE, FAKE, need, None) == sc.SHARD_ERR_INVALID
+    assert f(p, 1, FAKE, FAKE, 32, K, S, None, O, FAKE, FAKE, need, None) == sc.SHARD_ERR_INVALID     # null pad
+    assert f(p, 1, FAKE, FAKE, 32, K, S, pad, A(8, -1, 40), FAKE, FAKE, need, None) == sc.SHARD_ERR_INVALID
+    assert f(p, 1, FAKE, None, 32, K, S, pad, O, FAKE, FAKE, need, None) == sc.SHARD_ERR_INVALID      # null w
+    assert f(p, 1, FAKE, FAKE, 32, K, S, pad, O, None, FAKE, need, None) == sc.SHARD_ERR_INVALID      # null y
+    assert f(p, 1, FAKE, FAKE, 32, K, S, pad, O, FAKE, ctypes.c_void_p(0x10008), need, None) == sc.SHARD_ERR_INVALID
+    assert f(p, 1, FAKE, FAKE, 32, K, S, pad, A(0, 8, 40), None, None, 0, None) == sc.SHARD_OK        # empty: no-op
+    assert f(p, 1, FAKE, FAKE, 32, A(65, 3, 3), S, pad, O, FAKE, FAKE, need, None) == sc.SHARD_ERR_INVALID
+    wneed = sc.shard_conv_workspace_bytes(1, d, sc.SHARD_BF16, 32, [3, 3, 3], [1, 1, 1], [8, 8, 40])
+    g = lib.shard_conv_wgrad
+    assert g(p, 1, FAKE, FAKE, 32, K, S, pad, O, FAKE, FAKE, wneed - 1, None) == sc.SHARD_ERR_INVALID
+    assert g(p, 1, FAKE, FAKE, 32, K, S, pad, O, None, FAKE, wneed, None) == sc.SHARD_ERR_INVALID     # null dw
+    assert g(p, 1, FAKE, None, 32, K, S, pad, O, FAKE, FAKE, wneed, None) == sc.SHARD_ERR_INVALID     # null dy

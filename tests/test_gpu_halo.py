@@ -1,0 +1,143 @@
+"""GPU parity of halo pack / unpack: bit-exact against the oracle's padded tile
+and slabs, guard bands untouched, for every shard of the reduced workloads,
+the sequential exchange between all shards, and the measured shard of every
+full-size workload."""
+import numpy as np
+import pytest
+
+import synth
+import shard_cases as cases
+from gpu_util import build_tile, canary_for, dev, host, log
+from oracle import halo as ohalo
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def sc():
+    import torch
+    assert torch.cuda.is_available()
+    from paper_2605_11111_amd import shardconv
+    return shardconv
+
+
+def _bits_equal(a, b):
+    return a.shape == b.shape and np.array_equal(a.view(np.uint8), b.view(np.uint8))
+
+
+def _unpack_case(sc, w, idx):
+    log(f"unpack {w.name} shard {idx}")
+    desc, tile, sg, _ = build_tile(sc, w, idx)
+    got = host(tile)
+    want = cases.x_box(w, sg.tile_lo, sg.tile_hi, cases.out_code(w))
+    assert _bits_equal(got, want)
+
+
+@pytest.mark.parametrize("name", list(cases.REDUCED))
+def test_unpack_builds_padded_tile_every_shard(sc, name):
+    w = cases.REDUCED[name]
+    for idx in w.shards():
+        _unpack_case(sc, w, idx)
+
+
+@pytest.mark.parametrize("name", list(cases.REDUCED))
+def test_pack_every_face_with_guard_band(sc, name):
+    import torch
+    w = cases.REDUCED[name]
+    out = cases.out_code(w)
+    for idx in w.shards():
+        sg = cases.shard_geom(w, idx)
+        tile_h = cases.x_box(w, sg.tile_lo, sg.tile_hi, out)
+        tile = dev(tile_h)
+        desc = sc.tile_desc(w.N, w.cin, sg.ext, sg.g["halo_lo"], sg.g["halo_hi"])
+        logical = cases.to_ncdhw(cases.as_f64(tile_h, w))
+        for axis in range(w.nd):
+            for side in (0, 1):
+                if not cases.neighbour_exists(w, idx, axis, side):
+                    continue
+                nb = list(idx)
+                nb[axis] += 1 if side else -1
+                ng = cases.shard_geom(w, tuple(nb))
+                width = ng.g["halo_lo"][axis] if side == 1 else ng.g["halo_hi"][axis]
+                shape = sc.shard_halo_slab_shape(desc, axis, width)
+                n = int(np.prod(shape))
+                guard = 123
+                buf = torch.empty(n + 2 * guard, dtype=cases.torch_dtype(w), device="cuda")
+                fill = np.full(n + 2 * guard, canary_for(w))
+                buf.copy_(dev(fill))
+                sc.shard_halo_pack(desc, tile, axis, side, width, buf[guard:guard + n])
+                got = host(buf)
+                assert _bits_equal(got[:guard], fill[:guard]) and _bits_equal(got[guard + n:], fill[guard + n:])
+                want = ohalo.pack(logical, axis, side, width, sg.g["halo_lo"], sg.ext, sg.g["halo_hi"])
+                want_cl = cases.to_cl(want)
+                got_cl = cases.as_f64(got[guard:guard + n], w).reshape(want_cl.shape)
+                assert np.array_equal(got_cl, want_cl), (idx, axis, side)
+
+
+@pytest.mark.parametrize("name", ["c4r", "c5r", "c3r"])
+def test_sequential_exchange_between_all_shards(sc, name):
+    """Every shard starts from its interior only; axes are exchanged in order
+    with the library's pack into a slab and unpack on the neighbour; every tile
+    must end up equal to the zero-extended domain over its box (corners too)."""
+    import torch
+    w = cases.REDUCED[name]
+    out = cases.out_code(w)
+    tiles, geo = {}, {}
+    for idx in w.shards():
+        sg = cases.shard_geom(w, idx)
+        tiles[idx] = dev(cases.interior_tile_cl(w, sg, out, canary_for(w)))
+        geo[idx] = (sg, sc.tile_desc(w.N, w.cin, sg.ext, sg.g["halo_lo"], sg.g["halo_hi"]))
+    for axis in range(w.nd):
+        for idx in w.shards():
+            sg, desc = geo[idx]
+            for side in (0, 1):
+                width = sg.g["halo_lo"][axis] if side == 0 else sg.g["halo_hi"][axis]
+                if width == 0:
+                    continue
+                if not cases.neighbour_exists(w, idx, axis, side):
+                    sc.shard_halo_unpack(desc, tiles[idx], axis, side, None)
+                    continue
+                nb = list(idx)
+                nb[axis] += 1 if side else -1
+                nsg, ndesc = geo[tuple(nb)]
+                shape = sc.shard_halo_slab_shape(ndesc, axis, width)
+                slab = torch.empty(shape, dtype=cases.torch_dtype(w), device="cuda")
+                sc.shard_halo_pack(ndesc, tiles[tuple(nb)], axis, 1 - side, width, slab)
+                sc.shard_halo_unpack(desc, tiles[idx], axis, side, slab)
+    for idx in w.shards():
+        sg, _ = geo[idx]
+        assert _bits_equal(host(tiles[idx]), cases.x_box(w, sg.tile_lo, sg.tile_hi, out)), idx
+
+
+def test_unaligned_buffers_take_the_element_path(sc):
+    """Slab and tile at 2-byte (bf16) / 4-byte (fp32) offsets from 16-byte alignment."""
+    import torch
+    for name in ("c4r", "c1"):
+        w = cases.REDUCED[name]
+        out = cases.out_code(w)
+        idx = (0,) * w.nd
+        sg = cases.shard_geom(w, idx)
+        tile_h = cases.x_box(w, sg.tile_lo, sg.tile_hi, out)
+        big = torch.zeros(tile_h.size + 1, dtype=cases.torch_dtype(w), device="cuda")
+        tile = big[1:].view(tile_h.shape)
+        tile.copy_(dev(tile_h))
+        desc = sc.tile_desc(w.N, w.cin, sg.ext, sg.g["halo_lo"], sg.g["halo_hi"])
+        logical = cases.to_ncdhw(cases.as_f64(tile_h, w))
+        width = 1
+        shape = sc.shard_halo_slab_shape(desc, 0, width)
+        n = int(np.prod(shape))
+        sbig = torch.zeros(n + 1, dtype=cases.torch_dtype(w), device="cuda")
+        sc.shard_halo_pack(desc, tile, 0, 1, width, sbig[1:])
+        want = cases.to_cl(ohalo.pack(logical, 0, 1, width, sg.g["halo_lo"], sg.ext, sg.g["halo_hi"]))
+        assert np.array_equal(cases.as_f64(host(sbig[1:]), w).reshape(want.shape), want)
+
+
+@pytest.mark.parametrize("name", ["c1_2d_fp32", "c2_2d_bf16", "c4_3d_bf16_k5", "c5_3d_fp32_s2", "c3_3d_bf16"])
+def test_full_size_halos_of_the_measured_shard(sc, name):
+    w = cases.WORKLOADS[name]
+    idx = w.shard
+    log(f"full-size halo {name} shard {idx}")
+    desc, tile, sg, want = build_tile(sc, w, idx, keep_host=True)
+    got = host(tile)
+    del tile
+    assert _bits_equal(got, want)

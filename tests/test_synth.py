@@ -88,3 +88,15 @@ def test_bf16_output_is_rounded_f32_output():
     b = f.box(out=synth.OUT_BF16)
     assert np.array_equal(b, synth.round_bf16(f32))
     np.testing.assert_allclose(synth.bf16_to_f64(b), f32, rtol=2 ** -8)
+
+
+def test_oracle_output_rounding_matches_generator_rounding_and_ties():
+    """Two independent bf16 rounding implementations (oracle numpy, generator C)
+    agree on random values and on hand-picked ties."""
+    from oracle import conv
+    rng = np.random.default_rng(0)
+    v = np.concatenate([rng.normal(size=5000) * 10.0 ** rng.integers(-5, 6, size=5000),
+                        [1.0 + 2 ** -8, 1.0 + 3 * 2 ** -8, -(1.0 + 2 ** -8), 255.0, 257.0, 259.0]])
+    assert np.array_equal(conv.round_bf16(v), synth.round_bf16(v.astype(np.float32)))
+    got = conv.bf16_value(conv.round_bf16(np.array([257.0, 259.0, 1.0 + 2 ** -8])))
+    assert got.tolist() == [256.0, 260.0, 1.0]   # ties to even: 257 -> 256, 259 -> 260
