@@ -57,6 +57,7 @@ struct FwdArgs {
     int32_t nkc;       // K-chunks over all input channels
     int32_t nt;        // 32-wide N tiles over all output channels
     int32_t ng;        // N groups (workgroups along N)
+    int32_t vec;       // 16-byte loads allowed (tile base and channel rows aligned)
     int64_t nblocks;
 };
 
@@ -90,7 +91,7 @@ __device__ __forceinline__ void stage_brick(const FwdArgs& a, uint4* lds, int64_
     const int nq = a.nq;
     const int biv = a.BI[0] * a.BI[1] * a.BI[2];
     const int total = biv * nq;
-    const bool vec_ok = (a.cin * Traits<T>::esz) % 16 == 0;
+    const bool vec_ok = a.vec != 0;
     for (int u = threadIdx.x; u < total; u += kThreads) {
         const int q = u % nq;
         const int v = u / nq;
@@ -421,6 +422,7 @@ hipError_t run_fwd(const Tile3& t, const Conv3& cv, const void* tile, const void
     PlanF pl = plan_fwd_t<T>(t, cv);
     if (!pl.ok) return hipErrorInvalidValue;
     pl.a.tile = static_cast<const char*>(tile);
+    pl.a.vec = (reinterpret_cast<uintptr_t>(tile) % 16 == 0) && (t.c * Traits<T>::esz) % 16 == 0;
     pl.a.wfrag = static_cast<const uint4*>(ws);
     pl.a.y = static_cast<char*>(y);
     const int taps = int(cv.taps());

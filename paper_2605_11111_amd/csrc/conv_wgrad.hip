@@ -1,5 +1,24 @@
-// Weight gradient launcher.
+// Weight gradient of a shard on MFMA: dW[co][ci][t] = sum over the shard's
+// output voxels v of dy[v][co] * tile[v*S + t - pad][ci].
+//
+// GEMM view: M = output channels, N = input channels (per tap), K = output
+// voxels (millions). Split-K: the output bricks are cut into `nsplit`
+// contiguous ranges; a workgroup sweeps one range for one channel block and
+// tap group, keeps its dW tile in registers, and writes it once to the
+// workspace; a reduce kernel sums the ranges in a fixed order (bit-identical
+// results run to run, no atomics).
+//
+// bf16 (v_mfma_f32_16x16x32_bf16): each lane needs 8 consecutive K values
+// (voxels) of one channel, so both operands are staged in LDS transposed,
+// [channel][voxel]. Four waves own the 2x2 (or 4x1) 16x16 channel sub-tiles
+// of a 32x32 (or 64x16) block; every wave sweeps all taps of its group. For
+// tap (kd, kh, kw) a lane's 8 input voxels are 8 consecutive x positions
+// shifted by kw: it reads the two aligned 16-byte blocks covering them once
+// per (kd, kh) and derives every kw's operand with funnel shifts.
+// fp32 (v_mfma_f32_32x32x2_f32): one K value per lane, so both operands come
+// straight from channels-last LDS copies; the four waves split the taps.
 #include <algorithm>
+#include <cstdlib>
 
 #include "common.h"
 #include "internal.h"
@@ -10,16 +29,594 @@ size_t generic_wgrad_workspace(const Tile3& t, const Conv3& cv);
 hipError_t generic_conv_wgrad(const Tile3& t, const Conv3& cv, shard_dtype_t dt, const void* tile, const void* dy,
                               float* dw, void* ws, hipStream_t s);
 
+typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8_w;
+typedef __attribute__((ext_vector_type(4))) float f32x4_w;
+typedef __attribute__((ext_vector_type(16))) float f32x16_w;
+
+namespace {
+
+constexpr int kThreads = 256;
+constexpr int kTargetBlocks = 512;  // two resident workgroups per CU on 256 CUs
+
+struct WgArgs {
+    const char* tile;
+    const char* dy;
+    float* part;
+    float* dw;
+    int64_t n, cin, cout;
+    int64_t P[3], O[3];
+    int32_t K[3], S[3], pad[3];
+    int32_t BO[3];
+    int32_t NB[3];
+    int64_t nbricks;
+    int32_t nsplit, nmb, ncb, ntg;
+    int32_t kdg;          // bf16: kd planes per tap group; fp32: taps per group
+    int32_t biz, biy, bix, bixp;
+    int32_t cs, csd;      // LDS channel strides (bf16 layout, elements)
+    int32_t dy_off;       // byte offset of the dy copy in LDS
+    int32_t blk;          // floats of partial dW per workgroup
+    int32_t wco, wci;     // bf16: 16-wide sub-tiles per wave grid
+    int32_t xvec, dvec;   // 16-byte vector loads allowed (alignment of base and channel rows)
+    int64_t nblocks;
+};
+
+struct PlanW {
+    int kind;  // 0 generic, 1 bf16 tiled, 2 fp32 tiled
+    int kdg, k1, k2, wco;
+    WgArgs a;
+    size_t lds;
+};
+
+template <int S>
+__device__ __forceinline__ uint4 funnel(const uint4& b0, const uint4& b1)
+{
+    const uint32_t w[8] = {b0.x, b0.y, b0.z, b0.w, b1.x, b1.y, b1.z, b1.w};
+    constexpr int d = S / 2;
+    uint4 r;
+    if constexpr (S % 2 == 0) {
+        r.x = w[d];
+        r.y = w[d + 1];
+        r.z = w[d + 2];
+        r.w = w[d + 3];
+    } else {
+        r.x = __builtin_amdgcn_alignbit(w[d + 1], w[d], 16);
+        r.y = __builtin_amdgcn_alignbit(w[d + 2], w[d + 1], 16);
+        r.z = __builtin_amdgcn_alignbit(w[d + 3], w[d + 2], 16);
+        r.w = __builtin_amdgcn_alignbit(w[d + 4], w[d + 3], 16);
+    }
+    return r;
+}
+
+__device__ __forceinline__ void brick_origin(const WgArgs& a, int64_t br, int64_t& nn, int64_t ob[3])
+{
+    int64_t b = br;
+    const int bx = int(b % a.NB[2]);
+    b /= a.NB[2];
+    const int by = int(b % a.NB[1]);
+    b /= a.NB[1];
+    const int bz = int(b % a.NB[0]);
+    nn = b / a.NB[0];
+    ob[0] = int64_t(bz) * a.BO[0];
+    ob[1] = int64_t(by) * a.BO[1];
+    ob[2] = int64_t(bx) * a.BO[2];
+}
+
+// Load 8 consecutive channels [c, c + 8) of one voxel (zeros past `cend`).
+template <typename T>
+__device__ __forceinline__ void load8(const T* src, int64_t c, int64_t cend, bool vec_ok, T out[8])
+{
+    if (vec_ok && c + 8 <= cend) {
+        *reinterpret_cast<uint4*>(out) = *reinterpret_cast<const uint4*>(src);
+        if constexpr (sizeof(T) == 4) *reinterpret_cast<uint4*>(out + 4) = *reinterpret_cast<const uint4*>(src + 4);
+    } else {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) out[e] = (c + e < cend) ? src[e] : T(0);
+    }
+}
+
+template <int KDG, int K1, int K2, int WCO>
+__global__ __launch_bounds__(kThreads, 2) void wgrad_bf16_tiled(WgArgs a)
+{
+    constexpr int WCI = 4 / WCO;
+    constexpr int TG = KDG * K1 * K2;
+    constexpr int NCO = WCO * 16, NCI = WCI * 16;
+    extern __shared__ uint4 lds4[];
+    bf16_t* xs = reinterpret_cast<bf16_t*>(lds4);
+    bf16_t* ds = reinterpret_cast<bf16_t*>(reinterpret_cast<char*>(lds4) + a.dy_off);
+    const int lane = threadIdx.x & 63;
+    const int wave = threadIdx.x >> 6;
+    const int wco = wave / WCI, wci = wave % WCI;
+    const int g = lane >> 4;
+    const int l16 = lane & 15;
+
+    int64_t b = xcd_remap(blockIdx.x, a.nblocks);
+    const int tg = int(b % a.ntg);
+    b /= a.ntg;
+    const int cb = int(b % a.ncb);
+    b /= a.ncb;
+    const int mb = int(b % a.nmb);
+    const int64_t split = b / a.nmb;
+    const int64_t br0 = split * a.nbricks / a.nsplit, br1 = (split + 1) * a.nbricks / a.nsplit;
+    const int kd0 = tg * KDG;
+    const int64_t co0 = int64_t(mb) * NCO, ci0 = int64_t(cb) * NCI;
+    const int bov = a.BO[0] * a.BO[1] * a.BO[2];
+    const bool xvec = a.xvec != 0;
+    const bool dvec = a.dvec != 0;
+    const bf16_t* tile = reinterpret_cast<const bf16_t*>(a.tile);
+    const bf16_t* dy = reinterpret_cast<const bf16_t*>(a.dy);
+
+    f32x4_w acc[TG];
+#pragma unroll
+    for (int i = 0; i < TG; ++i) acc[i] = f32x4_w{0.f, 0.f, 0.f, 0.f};
+
+    for (int64_t br = br0; br < br1; ++br) {
+        int64_t nn, ob[3];
+        brick_origin(a, br, nn, ob);
+        const int64_t i0 = ob[0] * a.S[0] + kd0 - a.pad[0];
+        const int64_t i1 = ob[1] * a.S[1] - a.pad[1];
+        const int64_t i2 = ob[2] - a.pad[2];
+        __syncthreads();
+        // X^T: [ci][z][y][x], zero outside the tile and past cin
+        {
+            const int rows = a.biz * a.biy;
+            const int units = rows * a.bix * (NCI / 8);
+            for (int u = threadIdx.x; u < units; u += kThreads) {
+                const int q = u % (NCI / 8);
+                const int v = u / (NCI / 8);
+                const int x = v % a.bix;
+                const int row = v / a.bix;
+                const int y = row % a.biy;
+                const int z = row / a.biy;
+                const int64_t t0 = i0 + z, t1 = i1 + y, t2 = i2 + x;
+                const int64_t c = ci0 + 8 * q;
+                bf16_t val[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+                if (t0 >= 0 && t0 < a.P[0] && t1 >= 0 && t1 < a.P[1] && t2 >= 0 && t2 < a.P[2] && c < a.cin)
+                    load8(tile + (((nn * a.P[0] + t0) * a.P[1] + t1) * a.P[2] + t2) * a.cin + c, c, a.cin, xvec, val);
+                bf16_t* dst = xs + (8 * q) * a.cs + row * a.bixp + x;
+#pragma unroll
+                for (int e = 0; e < 8; ++e) dst[e * a.cs] = val[e];
+            }
+        }
+        // dy^T: [co][voxel of the output brick], zero past the output extent
+        {
+            const int units = bov * (NCO / 8);
+            for (int u = threadIdx.x; u < units; u += kThreads) {
+                const int q = u % (NCO / 8);
+                const int f = u / (NCO / 8);
+                const int ox = f % a.BO[2];
+                const int oy = (f / a.BO[2]) % a.BO[1];
+                const int oz = f / (a.BO[2] * a.BO[1]);
+                const int64_t o0 = ob[0] + oz, o1 = ob[1] + oy, o2 = ob[2] + ox;
+                const int64_t c = co0 + 8 * q;
+                bf16_t val[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+                if (o0 < a.O[0] && o1 < a.O[1] && o2 < a.O[2] && c < a.cout)
+                    load8(dy + (((nn * a.O[0] + o0) * a.O[1] + o1) * a.O[2] + o2) * a.cout + c, c, a.cout, dvec, val);
+                bf16_t* dst = ds + (8 * q) * a.csd + f;
+#pragma unroll
+                for (int e = 0; e < 8; ++e) dst[e * a.csd] = val[e];
+            }
+        }
+        __syncthreads();
+        const bf16_t* arow = ds + (wco * 16 + l16) * a.csd;
+        const bf16_t* xrow = xs + (wci * 16 + l16) * a.cs;
+        for (int ks = 0; ks < bov / 32; ++ks) {
+            const int f0 = ks * 32 + 8 * g;
+            const int ox0 = f0 % a.BO[2];
+            const int r = f0 / a.BO[2];
+            const int oy = r % a.BO[1];
+            const int oz = r / a.BO[1];
+            const uint4 av = *reinterpret_cast<const uint4*>(arow + f0);
+#pragma unroll
+            for (int kd = 0; kd < KDG; ++kd) {
+#pragma unroll
+                for (int kh = 0; kh < K1; ++kh) {
+                    const bf16_t* src = xrow + ((oz * a.S[0] + kd) * a.biy + oy * a.S[1] + kh) * a.bixp + ox0;
+                    const uint4 b0 = *reinterpret_cast<const uint4*>(src);
+                    const uint4 b1 = K2 > 1 ? *reinterpret_cast<const uint4*>(src + 8) : b0;
+#pragma unroll
+                    for (int kw = 0; kw < K2; ++kw) {
+                        uint4 bv;
+                        if (kw == 0) bv = funnel<0>(b0, b1);
+                        else if (kw == 1) bv = funnel<1>(b0, b1);
+                        else if (kw == 2) bv = funnel<2>(b0, b1);
+                        else if (kw == 3) bv = funnel<3>(b0, b1);
+                        else if (kw == 4) bv = funnel<4>(b0, b1);
+                        else if (kw == 5) bv = funnel<5>(b0, b1);
+                        else if (kw == 6) bv = funnel<6>(b0, b1);
+                        else bv = funnel<7>(b0, b1);
+                        const int ti = (kd * K1 + kh) * K2 + kw;
+                        acc[ti] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_w, av),
+                                                                          __builtin_bit_cast(bf16x8_w, bv), acc[ti],
+                                                                          0, 0, 0);
+                    }
+                }
+            }
+        }
+    }
+    float4* out = reinterpret_cast<float4*>(a.part +
+                                            ((((split * a.nmb + mb) * a.ncb + cb) * a.ntg + tg) * int64_t(a.blk)) +
+                                            int64_t(wave) * TG * 256);
+#pragma unroll
+    for (int i = 0; i < TG; ++i) out[i * 64 + lane] = make_float4(acc[i][0], acc[i][1], acc[i][2], acc[i][3]);
+}
+
+template <int TPW>
+__global__ __launch_bounds__(kThreads, 2) void wgrad_f32_tiled(WgArgs a)
+{
+    extern __shared__ uint4 lds4[];
+    float* xs = reinterpret_cast<float*>(lds4);
+    float* ds = reinterpret_cast<float*>(reinterpret_cast<char*>(lds4) + a.dy_off);
+    const int lane = threadIdx.x & 63;
+    const int wave = threadIdx.x >> 6;
+    const int g = lane >> 5;
+    const int l32 = lane & 31;
+
+    int64_t b = xcd_remap(blockIdx.x, a.nblocks);
+    const int tg = int(b % a.ntg);
+    b /= a.ntg;
+    const int cb = int(b % a.ncb);
+    b /= a.ncb;
+    const int mb = int(b % a.nmb);
+    const int64_t split = b / a.nmb;
+    const int64_t br0 = split * a.nbricks / a.nsplit, br1 = (split + 1) * a.nbricks / a.nsplit;
+    const int64_t co0 = int64_t(mb) * 32, ci0 = int64_t(cb) * 32;
+    const int taps = a.K[0] * a.K[1] * a.K[2];
+    const int bov = a.BO[0] * a.BO[1] * a.BO[2];
+    const int biv = a.biz * a.biy * a.bix;
+    const float* tile = reinterpret_cast<const float*>(a.tile);
+    const float* dy = reinterpret_cast<const float*>(a.dy);
+    const bool xvec = a.xvec != 0, dvec = a.dvec != 0;
+
+    // this wave's taps: t = tg * kdg + wave + 4 i
+    int toff[TPW];
+    bool tok[TPW];
+#pragma unroll
+    for (int i = 0; i < TPW; ++i) {
+        const int tl = wave + 4 * i;
+        const int t = tg * a.kdg + tl;
+        tok[i] = tl < a.kdg && t < taps;
+        const int tt = tok[i] ? t : 0;
+        const int kw = tt % a.K[2], kh = (tt / a.K[2]) % a.K[1], kd = tt / (a.K[2] * a.K[1]);
+        toff[i] = (kd * a.biy + kh) * a.bix + kw;
+    }
+    f32x16_w acc[TPW];
+#pragma unroll
+    for (int i = 0; i < TPW; ++i)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) acc[i][r] = 0.f;
+
+    for (int64_t br = br0; br < br1; ++br) {
+        int64_t nn, ob[3];
+        brick_origin(a, br, nn, ob);
+        const int64_t i0 = ob[0] * a.S[0] - a.pad[0];
+        const int64_t i1 = ob[1] * a.S[1] - a.pad[1];
+        const int64_t i2 = ob[2] * a.S[2] - a.pad[2];
+        __syncthreads();
+        for (int u = threadIdx.x; u < biv * 8; u += kThreads) {
+            const int q = u % 8;
+            const int v = u / 8;
+            const int x = v % a.bix;
+            const int y = (v / a.bix) % a.biy;
+            const int z = v / (a.bix * a.biy);
+            const int64_t t0 = i0 + z, t1 = i1 + y, t2 = i2 + x;
+            const int64_t c = ci0 + 4 * q;
+            float4 val = make_float4(0.f, 0.f, 0.f, 0.f);
+            if (t0 >= 0 && t0 < a.P[0] && t1 >= 0 && t1 < a.P[1] && t2 >= 0 && t2 < a.P[2] && c < a.cin) {
+                const float* src = tile + (((nn * a.P[0] + t0) * a.P[1] + t1) * a.P[2] + t2) * a.cin + c;
+                if (xvec && c + 4 <= a.cin) {
+                    val = *reinterpret_cast<const float4*>(src);
+                } else {
+                    float tmp[4];
+                    for (int e = 0; e < 4; ++e) tmp[e] = (c + e < a.cin) ? src[e] : 0.f;
+                    val = make_float4(tmp[0], tmp[1], tmp[2], tmp[3]);
+                }
+            }
+            reinterpret_cast<float4*>(xs)[v * 8 + q] = val;
+        }
+        const int bove = bov + (bov & 1);
+        for (int u = threadIdx.x; u < bove * 8; u += kThreads) {
+            const int q = u % 8;
+            const int f = u / 8;
+            const int ox = f % a.BO[2];
+            const int oy = (f / a.BO[2]) % a.BO[1];
+            const int oz = f / (a.BO[2] * a.BO[1]);
+            const int64_t o0 = ob[0] + oz, o1 = ob[1] + oy, o2 = ob[2] + ox;
+            const int64_t c = co0 + 4 * q;
+            float4 val = make_float4(0.f, 0.f, 0.f, 0.f);
+            if (f < bov && o0 < a.O[0] && o1 < a.O[1] && o2 < a.O[2] && c < a.cout) {
+                const float* src = dy + (((nn * a.O[0] + o0) * a.O[1] + o1) * a.O[2] + o2) * a.cout + c;
+                if (dvec && c + 4 <= a.cout) {
+                    val = *reinterpret_cast<const float4*>(src);
+                } else {
+                    float tmp[4];
+                    for (int e = 0; e < 4; ++e) tmp[e] = (c + e < a.cout) ? src[e] : 0.f;
+                    val = make_float4(tmp[0], tmp[1], tmp[2], tmp[3]);
+                }
+            }
+            reinterpret_cast<float4*>(ds)[f * 8 + q] = val;
+        }
+        __syncthreads();
+        for (int ks = 0; ks < bove / 2; ++ks) {
+            const int f = 2 * ks + g;
+            const int ff = f < bov ? f : 0;
+            const int ox = ff % a.BO[2];
+            const int oy = (ff / a.BO[2]) % a.BO[1];
+            const int oz = ff / (a.BO[2] * a.BO[1]);
+            const int vin = (oz * a.S[0] * a.biy + oy * a.S[1]) * a.bix + ox * a.S[2];
+            const float av = ds[f * 32 + l32];
+#pragma unroll
+            for (int i = 0; i < TPW; ++i) {
+                if (!tok[i]) continue;
+                const float bv = xs[(vin + toff[i]) * 32 + l32];
+                acc[i] = __builtin_amdgcn_mfma_f32_32x32x2f32(av, bv, acc[i], 0, 0, 0);
+            }
+        }
+    }
+    float4* out = reinterpret_cast<float4*>(a.part + (((split * a.nmb + mb) * a.ncb + cb) * a.ntg + tg) * int64_t(a.blk) +
+                                            int64_t(wave) * TPW * 1024);
+#pragma unroll
+    for (int i = 0; i < TPW; ++i)
+#pragma unroll
+        for (int r4 = 0; r4 < 4; ++r4)
+            out[(i * 64 + lane) * 4 + r4] =
+                make_float4(acc[i][4 * r4], acc[i][4 * r4 + 1], acc[i][4 * r4 + 2], acc[i][4 * r4 + 3]);
+}
+
+// Sum the split partials in split order and scatter into dw[co][ci][tap].
+// One thread per partial float of one (mb, cb, tg) block: reads are coalesced.
+__global__ __launch_bounds__(256) void wgrad_reduce(WgArgs a, int kind, int kdg, int k1, int k2, int wco)
+{
+    const int64_t groups = int64_t(a.nmb) * a.ncb * a.ntg;
+    const int64_t total = groups * a.blk;
+    const int taps = a.K[0] * a.K[1] * a.K[2];
+    for (int64_t e = int64_t(blockIdx.x) * 256 + threadIdx.x; e < total; e += int64_t(gridDim.x) * 256) {
+        const int64_t grp = e / a.blk;
+        const int p = int(e % a.blk);
+        const int tg = int(grp % a.ntg);
+        const int cb = int((grp / a.ntg) % a.ncb);
+        const int mb = int(grp / (int64_t(a.ntg) * a.ncb));
+        int64_t co, ci;
+        int tap;
+        if (kind == 1) {
+            const int wci_n = 4 / wco;
+            const int tgs = kdg * k1 * k2;
+            const int r = p % 4, lane = (p / 4) % 64, ti = (p / 256) % tgs, wave = p / (256 * tgs);
+            const int wc = wave / wci_n, wi = wave % wci_n;
+            co = int64_t(mb) * wco * 16 + wc * 16 + 4 * (lane / 16) + r;
+            ci = int64_t(cb) * wci_n * 16 + wi * 16 + (lane % 16);
+            const int kw = ti % k2, kh = (ti / k2) % k1, kdl = ti / (k2 * k1);
+            tap = ((tg * kdg + kdl) * a.K[1] + kh) * a.K[2] + kw;
+        } else {
+            const int tpw = a.blk / (4 * 1024);
+            const int r = p % 16, lane = (p / 16) % 64, i = (p / 1024) % tpw, wave = p / (1024 * tpw);
+            const int row = 8 * (r / 4) + 4 * (lane / 32) + (r % 4);
+            co = int64_t(mb) * 32 + row;
+            ci = int64_t(cb) * 32 + (lane % 32);
+            const int tl = wave + 4 * i;
+            tap = tg * kdg + tl;
+            if (tl >= kdg) continue;
+        }
+        if (co >= a.cout || ci >= a.cin || tap >= taps) continue;
+        float s = 0.f;
+        for (int64_t sp = 0; sp < a.nsplit; ++sp) s += a.part[sp * total + e];
+        a.dw[(co * a.cin + ci) * taps + tap] = s;
+    }
+}
+
+bool bf16_instance(int kdg, int k1, int k2)
+{
+    return (kdg == 3 && k1 == 3 && k2 == 3) || (kdg == 1 && k1 == 3 && k2 == 3) || (kdg == 1 && k1 == 5 && k2 == 5) ||
+           (kdg == 1 && k1 == 1 && (k2 == 1 || k2 == 3 || k2 == 5));
+}
+
+PlanW plan_wgrad(const Tile3& t, const Conv3& cv, shard_dtype_t dt)
+{
+    PlanW pl{};
+    pl.kind = 0;
+    if (force_generic()) return pl;
+    const int64_t taps = cv.taps();
+    for (int k = 0; k < 3; ++k)
+        if (cv.K[k] > 64 || cv.S[k] > 64 || cv.O[k] > (int64_t(1) << 30) || std::abs(cv.pad[k]) > (1 << 29)) return pl;
+    if (t.c > 4096 || cv.cout > 4096) return pl;
+    WgArgs a{};
+    a.n = t.n;
+    a.cin = t.c;
+    a.cout = cv.cout;
+    for (int k = 0; k < 3; ++k) {
+        a.P[k] = t.P[k];
+        a.O[k] = cv.O[k];
+        a.K[k] = int32_t(cv.K[k]);
+        a.S[k] = int32_t(cv.S[k]);
+        a.pad[k] = int32_t(cv.pad[k]);
+    }
+    const size_t kLds = 80 * 1024;
+    if (dt == SHARD_BF16) {
+        if (cv.S[2] != 1 || cv.K[2] > 8) return pl;
+        int kdg = (cv.K[0] * cv.K[1] * cv.K[2] <= 27) ? int(cv.K[0]) : 1;
+        if (!bf16_instance(kdg, int(cv.K[1]), int(cv.K[2]))) return pl;
+        const int wco = t.c <= 16 ? 4 : 2, wci = 4 / wco;
+        const int nco = wco * 16, nci = wci * 16;
+        // brick: W extent a multiple of 8 (an 8-voxel K group stays in one row)
+        double best = 1e300;
+        for (int b2 : {32, 64, 16, 8}) {
+            for (int b1 = 1; b1 <= 64; b1 *= 2) {
+                for (int b0 = 1; b0 <= 64; b0 *= 2) {
+                    const int bov = b0 * b1 * b2;
+                    if (bov % 32 != 0 || bov > 1024) continue;
+                    if (b0 > 1 && b0 > cv.O[0]) continue;
+                    if (b1 > 1 && b1 > cv.O[1]) continue;
+                    const int biz = int((b0 - 1) * cv.S[0] + kdg);
+                    const int biy = int((b1 - 1) * cv.S[1] + cv.K[1]);
+                    const int bix = int(b2 + cv.K[2] - 1);
+                    const int bixp = b2 + 8;
+                    int cs = biz * biy * bixp;
+                    cs = int(round_up(cs, 16) + 8);
+                    const int csd = int(round_up(bov, 16) + 8);
+                    const int dy_off = int(round_up(int64_t(nci) * cs * 2, 16));
+                    const size_t lds = size_t(dy_off) + size_t(nco) * csd * 2;
+                    if (lds > kLds) continue;
+                    double eff = 1.0;
+                    const int64_t bo[3] = {b0, b1, b2};
+                    for (int k = 0; k < 3; ++k) eff *= double(cv.O[k]) / double(ceil_div(cv.O[k], bo[k]) * bo[k]);
+                    const double cost = (double(biz * biy * bix) * nci / bov + double(nco)) / eff +
+                                        4096.0 / bov;  // staging bytes per output voxel, plus a per-brick overhead
+                    if (cost < best) {
+                        best = cost;
+                        a.BO[0] = b0;
+                        a.BO[1] = b1;
+                        a.BO[2] = b2;
+                        a.biz = biz;
+                        a.biy = biy;
+                        a.bix = bix;
+                        a.bixp = bixp;
+                        a.cs = cs;
+                        a.csd = csd;
+                        a.dy_off = dy_off;
+                        pl.lds = lds;
+                    }
+                }
+            }
+        }
+        if (best >= 1e299) return pl;
+        a.kdg = kdg;
+        a.nmb = int32_t(ceil_div(cv.cout, nco));
+        a.ncb = int32_t(ceil_div(t.c, nci));
+        a.ntg = int32_t(cv.K[0] / kdg);
+        a.blk = 4 * kdg * int(cv.K[1] * cv.K[2]) * 256;
+        a.wco = wco;
+        a.wci = wci;
+        pl.kind = 1;
+        pl.kdg = kdg;
+        pl.k1 = int(cv.K[1]);
+        pl.k2 = int(cv.K[2]);
+        pl.wco = wco;
+    } else {
+        const int tpw = 7;
+        const int tgs = 4 * tpw;
+        // brick: any shape with <= 64 outputs whose input footprint fits
+        double best = 1e300;
+        for (int b2 = 1; b2 <= 64; b2 *= 2)
+            for (int b1 = 1; b1 <= 64; b1 *= 2)
+                for (int b0 = 1; b0 <= 64; b0 *= 2) {
+                    const int bov = b0 * b1 * b2;
+                    if (bov > 64 || bov < 2) continue;
+                    if ((b0 > 1 && b0 > cv.O[0]) || (b1 > 1 && b1 > cv.O[1]) || (b2 > 1 && b2 > cv.O[2])) continue;
+                    const int biz = int((b0 - 1) * cv.S[0] + cv.K[0]);
+                    const int biy = int((b1 - 1) * cv.S[1] + cv.K[1]);
+                    const int bix = int((b2 - 1) * cv.S[2] + cv.K[2]);
+                    const int64_t biv = int64_t(biz) * biy * bix;
+                    const int dy_off = int(biv * 128);
+                    const size_t lds = size_t(dy_off) + size_t(bov + 1) * 128;
+                    if (lds > kLds) continue;
+                    double eff = 1.0;
+                    const int64_t bo[3] = {b0, b1, b2};
+                    for (int k = 0; k < 3; ++k) eff *= double(cv.O[k]) / double(ceil_div(cv.O[k], bo[k]) * bo[k]);
+                    const double cost = (double(biv) / bov + 1.0) / eff + 64.0 / bov;
+                    if (cost < best) {
+                        best = cost;
+                        a.BO[0] = b0;
+                        a.BO[1] = b1;
+                        a.BO[2] = b2;
+                        a.biz = biz;
+                        a.biy = biy;
+                        a.bix = bix;
+                        a.dy_off = dy_off;
+                        pl.lds = lds;
+                    }
+                }
+        if (best >= 1e299) return pl;
+        a.kdg = tgs;
+        a.nmb = int32_t(ceil_div(cv.cout, 32));
+        a.ncb = int32_t(ceil_div(t.c, 32));
+        a.ntg = int32_t(ceil_div(taps, tgs));
+        a.blk = 4 * tpw * 1024;
+        pl.kind = 2;
+    }
+    for (int k = 0; k < 3; ++k) a.NB[k] = int32_t(ceil_div(cv.O[k], a.BO[k]));
+    a.nbricks = t.n * int64_t(a.NB[0]) * a.NB[1] * a.NB[2];
+    const int64_t groups = int64_t(a.nmb) * a.ncb * a.ntg;
+    a.nsplit = int32_t(std::max<int64_t>(1, std::min<int64_t>(a.nbricks, ceil_div(kTargetBlocks, groups))));
+    a.nblocks = groups * a.nsplit;
+    if (a.nblocks >= (int64_t(1) << 31) || a.nbricks == 0) {
+        pl.kind = 0;
+        return pl;
+    }
+    pl.a = a;
+    return pl;
+}
+
+size_t tiled_workspace(const PlanW& pl)
+{
+    if (pl.kind == 0) return 0;
+    return size_t(pl.a.nblocks) * size_t(pl.a.blk) * sizeof(float);
+}
+
+template <typename K>
+hipError_t launch_with_lds(K fn, const PlanW& pl, hipStream_t s)
+{
+    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(fn), hipFuncAttributeMaxDynamicSharedMemorySize,
+                                       int(pl.lds));
+    if (e != hipSuccess) return e;
+    WgArgs a = pl.a;
+    void* args[] = {&a};
+    return hipLaunchKernel(reinterpret_cast<const void*>(fn), dim3(unsigned(a.nblocks)), dim3(kThreads), args, pl.lds,
+                           s);
+}
+
+hipError_t launch_bf16(const PlanW& pl, hipStream_t s)
+{
+    const int k = pl.kdg * 100 + pl.k1 * 10 + pl.k2;
+    if (pl.wco == 2) {
+        switch (k) {
+        case 333: return launch_with_lds(&wgrad_bf16_tiled<3, 3, 3, 2>, pl, s);
+        case 133: return launch_with_lds(&wgrad_bf16_tiled<1, 3, 3, 2>, pl, s);
+        case 155: return launch_with_lds(&wgrad_bf16_tiled<1, 5, 5, 2>, pl, s);
+        case 111: return launch_with_lds(&wgrad_bf16_tiled<1, 1, 1, 2>, pl, s);
+        case 113: return launch_with_lds(&wgrad_bf16_tiled<1, 1, 3, 2>, pl, s);
+        case 115: return launch_with_lds(&wgrad_bf16_tiled<1, 1, 5, 2>, pl, s);
+        default: break;
+        }
+    } else {
+        switch (k) {
+        case 333: return launch_with_lds(&wgrad_bf16_tiled<3, 3, 3, 4>, pl, s);
+        case 133: return launch_with_lds(&wgrad_bf16_tiled<1, 3, 3, 4>, pl, s);
+        case 155: return launch_with_lds(&wgrad_bf16_tiled<1, 5, 5, 4>, pl, s);
+        case 111: return launch_with_lds(&wgrad_bf16_tiled<1, 1, 1, 4>, pl, s);
+        case 113: return launch_with_lds(&wgrad_bf16_tiled<1, 1, 3, 4>, pl, s);
+        case 115: return launch_with_lds(&wgrad_bf16_tiled<1, 1, 5, 4>, pl, s);
+        default: break;
+        }
+    }
+    return hipErrorInvalidValue;
+}
+
+}  // namespace
+
 size_t conv_wgrad_workspace(const Tile3& t, const Conv3& cv, shard_dtype_t dt)
 {
-    (void)dt;
-    return generic_wgrad_workspace(t, cv);
+    return std::max(generic_wgrad_workspace(t, cv), tiled_workspace(plan_wgrad(t, cv, dt)));
 }
 
 hipError_t launch_conv_wgrad(const Tile3& t, const Conv3& cv, shard_dtype_t dt, const void* tile, const void* dy,
                              float* dw, void* ws, hipStream_t s)
 {
-    return generic_conv_wgrad(t, cv, dt, tile, dy, dw, ws, s);
+    PlanW pl = plan_wgrad(t, cv, dt);
+    if (pl.kind == 0) return generic_conv_wgrad(t, cv, dt, tile, dy, dw, ws, s);
+    pl.a.tile = static_cast<const char*>(tile);
+    pl.a.dy = static_cast<const char*>(dy);
+    const int64_t esz = dt == SHARD_BF16 ? 2 : 4;
+    pl.a.xvec = (reinterpret_cast<uintptr_t>(tile) % 16 == 0) && (t.c * esz) % 16 == 0;
+    pl.a.dvec = (reinterpret_cast<uintptr_t>(dy) % 16 == 0) && (cv.cout * esz) % 16 == 0;
+    pl.a.part = static_cast<float*>(ws);
+    pl.a.dw = dw;
+    hipError_t e = pl.kind == 1 ? launch_bf16(pl, s) : launch_with_lds(&wgrad_f32_tiled<7>, pl, s);
+    if (e != hipSuccess) return e;
+    const int64_t total = int64_t(pl.a.nmb) * pl.a.ncb * pl.a.ntg * pl.a.blk;
+    const unsigned grid = unsigned(std::max<int64_t>(1, std::min<int64_t>(ceil_div(total, 256), 1 << 16)));
+    WgArgs a = pl.a;
+    int kind = pl.kind, kdg = pl.a.kdg, k1 = pl.k1, k2 = pl.k2, wco = pl.wco;
+    void* args[] = {&a, &kind, &kdg, &k1, &k2, &wco};
+    return hipLaunchKernel(reinterpret_cast<const void*>(&wgrad_reduce), dim3(grid), dim3(256), args, 0, s);
 }
 
 }  // namespace shardconv
