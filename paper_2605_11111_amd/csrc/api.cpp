@@ -13,6 +13,12 @@ bool force_generic()
     return v && std::strcmp(v, "generic") == 0;
 }
 
+bool force_tiled()
+{
+    const char* v = std::getenv("SHARDCONV_ALGO");
+    return v && std::strcmp(v, "tiled") == 0;
+}
+
 size_t generic_wgrad_workspace(const Tile3& t, const Conv3& cv);
 hipError_t generic_conv_wgrad(const Tile3& t, const Conv3& cv, shard_dtype_t dt, const void* tile, const void* dy,
                               float* dw, void* ws, hipStream_t s);

@@ -432,6 +432,9 @@ hipError_t run_fwd(const Tile3& t, const Conv3& cv, const void* tile, const void
                        static_cast<uint4*>(ws), t.c, cv.cout, taps, pl.a.nkc, pl.a.nt);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
+    e = launch_conv_fwd_rows(t, cv, std::is_same<T, bf16_t>::value ? SHARD_BF16 : SHARD_F32, tile, ws, pl.a.nkc,
+                             pl.a.nt, y, s);
+    if (e != hipErrorNotSupported) return e;
     if (pl.rm == 4 && pl.rn == 1) return launch_tiled<T, 4, 1>(pl, s);
     if (pl.rm == 4 && pl.rn == 2) return launch_tiled<T, 4, 2>(pl, s);
     if (pl.rm == 2 && pl.rn == 2) return launch_tiled<T, 2, 2>(pl, s);

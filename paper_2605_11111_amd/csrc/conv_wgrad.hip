@@ -397,8 +397,16 @@ __global__ __launch_bounds__(256) void wgrad_reduce(WgArgs a, int kind, int kdg,
             if (tl >= kdg) continue;
         }
         if (co >= a.cout || ci >= a.cin || tap >= taps) continue;
-        float s = 0.f;
-        for (int64_t sp = 0; sp < a.nsplit; ++sp) s += a.part[sp * total + e];
+        // eight interleaved partial sums (split index mod 8), combined in a fixed
+        // tree: a fixed summation order with eight loads in flight
+        float s8[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+        int64_t sp = 0;
+        for (; sp + 8 <= a.nsplit; sp += 8) {
+#pragma unroll
+            for (int j = 0; j < 8; ++j) s8[j] += a.part[(sp + j) * total + e];
+        }
+        for (int j = 0; sp + j < a.nsplit; ++j) s8[j] += a.part[(sp + j) * total + e];
+        const float s = ((s8[0] + s8[1]) + (s8[2] + s8[3])) + ((s8[4] + s8[5]) + (s8[6] + s8[7]));
         a.dw[(co * a.cin + ci) * taps + tap] = s;
     }
 }
@@ -594,12 +602,37 @@ hipError_t launch_bf16(const PlanW& pl, hipStream_t s)
 
 size_t conv_wgrad_workspace(const Tile3& t, const Conv3& cv, shard_dtype_t dt)
 {
-    return std::max(generic_wgrad_workspace(t, cv), tiled_workspace(plan_wgrad(t, cv, dt)));
+    return std::max({generic_wgrad_workspace(t, cv), tiled_workspace(plan_wgrad(t, cv, dt)),
+                     wgrad_tr_workspace(t, cv, dt)});
 }
 
 hipError_t launch_conv_wgrad(const Tile3& t, const Conv3& cv, shard_dtype_t dt, const void* tile, const void* dy,
                              float* dw, void* ws, hipStream_t s)
 {
+    {
+        int32_t red[6];
+        hipError_t e = launch_wgrad_tr(t, cv, dt, tile, dy, static_cast<float*>(ws), red, s);
+        if (e != hipErrorNotSupported) {
+            if (e != hipSuccess) return e;
+            WgArgs a{};
+            a.part = static_cast<float*>(ws);
+            a.dw = dw;
+            a.cin = t.c;
+            a.cout = cv.cout;
+            for (int k = 0; k < 3; ++k) a.K[k] = int32_t(cv.K[k]);
+            a.nmb = red[0];
+            a.ncb = red[1];
+            a.ntg = red[2];
+            a.blk = red[3];
+            a.kdg = red[4];
+            a.nsplit = red[5];
+            const int64_t total = int64_t(a.nmb) * a.ncb * a.ntg * a.blk;
+            const unsigned grid = unsigned(std::max<int64_t>(1, std::min<int64_t>(ceil_div(total, 256), 1 << 16)));
+            int kind = 2, kdg = a.kdg, k1 = 0, k2 = 0, wco = 0;
+            void* args[] = {&a, &kind, &kdg, &k1, &k2, &wco};
+            return hipLaunchKernel(reinterpret_cast<const void*>(&wgrad_reduce), dim3(grid), dim3(256), args, 0, s);
+        }
+    }
     PlanW pl = plan_wgrad(t, cv, dt);
     if (pl.kind == 0) return generic_conv_wgrad(t, cv, dt, tile, dy, dw, ws, s);
     pl.a.tile = static_cast<const char*>(tile);

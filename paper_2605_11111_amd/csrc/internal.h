@@ -51,10 +51,20 @@ hipError_t launch_conv_fwd(const Tile3& t, const Conv3& cv, shard_dtype_t dt, co
 hipError_t launch_conv_wgrad(const Tile3& t, const Conv3& cv, shard_dtype_t dt, const void* tile, const void* dy,
                              float* dw, void* ws, hipStream_t s);
 
-// Which implementation a call takes. "generic" forces the plain direct kernels
-// (used by tests to cross-check the tiled MFMA kernels); read from the
-// environment variable SHARDCONV_ALGO at each call.
+// Specialised kernels; each returns hipErrorNotSupported when the shape is
+// outside what it handles (the caller then takes the general kernel).
+hipError_t launch_conv_fwd_rows(const Tile3& t, const Conv3& cv, shard_dtype_t dt, const void* tile,
+                                const void* wfrag, int nkc_frag, int nt_frag, void* y, hipStream_t s);
+size_t wgrad_tr_workspace(const Tile3& t, const Conv3& cv, shard_dtype_t dt);
+hipError_t launch_wgrad_tr(const Tile3& t, const Conv3& cv, shard_dtype_t dt, const void* tile, const void* dy,
+                           float* part, int32_t red[6], hipStream_t s);
+
+// Which implementation a call takes, read from the environment variable
+// SHARDCONV_ALGO at each call: unset picks the fastest applicable kernel,
+// "tiled" skips the shape-specialised kernels, "generic" forces the plain
+// direct kernels (tests use both to cross-check the kernels against each other).
 bool force_generic();
+bool force_tiled();
 
 inline int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
 inline int64_t round_up(int64_t a, int64_t b) { return ceil_div(a, b) * b; }

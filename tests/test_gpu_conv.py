@@ -104,27 +104,33 @@ def test_c1_concatenated_shards_equal_full_domain(sc):
     assert cases.norm_max_err(got, full) <= cases.TOL["f32"]
 
 
-def test_generic_and_tiled_kernels_agree(sc, monkeypatch):
-    """The untiled direct kernels and the tiled MFMA kernels give the same
-    result: bitwise on integer data, to the tolerance otherwise."""
-    for name in ("c3r", "c4r", "c5r", "c2r"):
-        w = cases.REDUCED[name]
-        idx = tuple(len(w.splits(a)) - 1 for a in range(w.nd))
-        for dist in (INT_DIST, None):
-            desc, tile, sg, _ = build_tile(sc, w, idx, dist)
-            w_host, _ = weights(w, dist)
-            dyh = dy_box(w, sg, dist)
-            y1 = host(run_fwd(sc, w, desc, tile, sg, dev(w_host)))
-            d1 = host(run_wgrad(sc, w, desc, tile, sg, dev(dyh)))
-            monkeypatch.setenv("SHARDCONV_ALGO", "generic")
-            y2 = host(run_fwd(sc, w, desc, tile, sg, dev(w_host)))
-            d2 = host(run_wgrad(sc, w, desc, tile, sg, dev(dyh)))
-            monkeypatch.delenv("SHARDCONV_ALGO")
-            if dist is INT_DIST:
-                assert np.array_equal(y1, y2) and np.array_equal(d1, d2), name
+@pytest.mark.parametrize("name", ["c3r", "c2r", "c4r", "c5r", "c1"])
+def test_kernel_variants_agree(sc, monkeypatch, name):
+    """The shape-specialised kernels (default), the general tiled MFMA kernels
+    (SHARDCONV_ALGO=tiled) and the direct kernels (SHARDCONV_ALGO=generic) give
+    the same result: bitwise on integer data, to the tolerance otherwise."""
+    w = cases.REDUCED[name]
+    idx = tuple(len(w.splits(a)) - 1 for a in range(w.nd))
+    for dist in (INT_DIST, None):
+        desc, tile, sg, _ = build_tile(sc, w, idx, dist)
+        w_host, _ = weights(w, dist)
+        wt, dyh = dev(w_host), dev(dy_box(w, sg, dist))
+        res = {}
+        for algo in ("", "tiled", "generic"):
+            if algo:
+                monkeypatch.setenv("SHARDCONV_ALGO", algo)
             else:
-                assert cases.norm_max_err(cases.as_f64(y1, w), cases.as_f64(y2, w)) <= cases.TOL[w.dtype]
-                assert cases.norm_max_err(d1.astype(np.float64), d2.astype(np.float64)) <= cases.TOL[w.dtype]
+                monkeypatch.delenv("SHARDCONV_ALGO", raising=False)
+            res[algo] = (host(run_fwd(sc, w, desc, tile, sg, wt)), host(run_wgrad(sc, w, desc, tile, sg, dyh)))
+        monkeypatch.delenv("SHARDCONV_ALGO", raising=False)
+        y0, d0 = res[""]
+        for algo in ("tiled", "generic"):
+            y1, d1 = res[algo]
+            if dist is INT_DIST:
+                assert np.array_equal(y0, y1) and np.array_equal(d0, d1), (name, algo)
+            else:
+                assert cases.norm_max_err(cases.as_f64(y1, w), cases.as_f64(y0, w)) <= cases.TOL[w.dtype]
+                assert cases.norm_max_err(d1.astype(np.float64), d0.astype(np.float64)) <= cases.TOL[w.dtype]
 
 
 def test_repeat_runs_are_bitwise_identical(sc):
