@@ -42,3 +42,70 @@ __device__ __forceinline__ int64_t xcd_remap(int64_t b, int64_t nblocks)
 }
 
 }  // namespace shardconv
+
+namespace shardconv {
+
+// Wait until at most N vector-memory operations of this wave are outstanding
+// and all its LDS operations are done, then barrier. Unlike __syncthreads(),
+// this does not wait for the wave's outstanding global stores (N of them may
+// still be in flight) - those need no ordering with the LDS data the barrier
+// publishes (direct global->LDS loads complete in issue order before them).
+template <int N>
+__device__ __forceinline__ void wait_vm_barrier()
+{
+    static_assert(N >= 0 && N < 64, "vmcnt range");
+    asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" ::"n"(N) : "memory");
+}
+
+// LDS accesses issued through inline asm. The compiler's wait insertion cannot
+// tell the buffers of direct global->LDS loads apart, so it would place an
+// s_waitcnt vmcnt(0) before any LDS access it sees after such a load - waiting
+// for every prefetch in flight. Accesses written as asm are invisible to it; the
+// caller orders them itself: lds_wait<N>() waits until at most N LDS operations
+// of the wave are outstanding (LDS operations complete in issue order), and
+// lds_ready() marks a register as produced at that point so that no use of it
+// is scheduled earlier.
+typedef __attribute__((ext_vector_type(4))) unsigned int lds_u32x4;
+
+__device__ __forceinline__ uint32_t lds_addr(const void* p)
+{
+    return static_cast<uint32_t>(reinterpret_cast<uintptr_t>((const __attribute__((address_space(3))) char*)(p)));
+}
+
+template <int OFF = 0>
+__device__ __forceinline__ lds_u32x4 lds_read_b128(uint32_t addr)
+{
+    static_assert(OFF >= 0 && OFF < 65536, "ds offset range");
+    lds_u32x4 r;
+    asm volatile("ds_read_b128 %0, %1 offset:%2" : "=v"(r) : "v"(addr), "n"(OFF));
+    return r;
+}
+
+template <int OFF = 0>
+__device__ __forceinline__ void lds_write_b16(uint32_t addr, uint32_t v)
+{
+    static_assert(OFF >= 0 && OFF < 65536, "ds offset range");
+    asm volatile("ds_write_b16 %0, %1 offset:%2" ::"v"(addr), "v"(v), "n"(OFF) : "memory");
+}
+
+template <int OFF = 0>
+__device__ __forceinline__ void lds_write_b16_hi(uint32_t addr, uint32_t v)
+{
+    static_assert(OFF >= 0 && OFF < 65536, "ds offset range");
+    asm volatile("ds_write_b16_d16_hi %0, %1 offset:%2" ::"v"(addr), "v"(v), "n"(OFF) : "memory");
+}
+
+template <int N>
+__device__ __forceinline__ void lds_wait()
+{
+    static_assert(N >= 0 && N < 16, "lgkmcnt range");
+    asm volatile("s_waitcnt lgkmcnt(%0)" ::"n"(N) : "memory");
+}
+
+template <typename T>
+__device__ __forceinline__ void lds_ready(T& v)
+{
+    asm volatile("" : "+v"(v));
+}
+
+}  // namespace shardconv

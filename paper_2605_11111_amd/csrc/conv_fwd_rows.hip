@@ -1,22 +1,33 @@
-// Forward convolution, bf16, for unit stride and small weight sets (the
-// halo-padded 3D/2D shard workloads): a persistent implicit GEMM whose operands
-// never leave the CU between reuses.
+// Forward convolution, bf16, unit stride, kernel width 3 along the innermost
+// axis (the halo-padded 3D/2D shard workloads): a persistent implicit GEMM with
+// M = 32 input voxels of one W row, N = 32 output channels, K = 16 input
+// channels per v_mfma_f32_32x32x16_bf16.
 //
-//  * One workgroup per CU (4 waves) sweeps output bricks of WZ x (WY*R) x 32
-//    voxels. The whole weight set, pre-arranged in MFMA B-fragment order, sits
-//    in LDS for the workgroup's lifetime.
-//  * The input footprint of a brick (the brick grown by the kernel reach; the
-//    halo rows arrive this way) is staged in 16-channel chunks by direct
-//    global->LDS buffer loads (no VGPR round trip), double buffered: the next
-//    chunk streams in while the current one feeds the MFMAs. Voxels outside the
-//    tile load as zero (out-of-range buffer offsets), which is the zero padding.
-//  * Each wave owns R consecutive output rows of one plane (32 voxels each, an
-//    M tile of v_mfma_f32_32x32x16_bf16). For a fixed (kd, kw) the A fragment of
-//    input row j serves output rows j - kh for every kh, so R + KH - 1 LDS reads
-//    feed R * KH MFMAs.
-//  * LDS addresses are per-lane constants plus compile-time immediates; the
-//    16-byte unit of a voxel is XOR-swizzled by bit 3 of its x position so the
-//    16 lanes of a ds_read_b128 phase hit 16 distinct bank groups.
+//  * The weights of a wave's 32 output channels sit in registers (B fragments)
+//    for the kernel's lifetime, so LDS carries input rows only.
+//  * A workgroup (4 waves) owns a brick of BZ x BY output rows and marches along
+//    W in 32-voxel input tiles. Each tile's footprint (BZ+KD-1 x BY+KH-1 input
+//    rows of 32 voxels, all channels) is staged by direct global->LDS buffer
+//    loads, NBUF deep; voxels outside the tile load as zero (out-of-range buffer
+//    offsets), which is the zero padding.
+//  * Taps along H/D are row choices: input row j of the stage serves the wave's
+//    output rows j - kh. Taps along W are not applied to the operand at all: input
+//    voxel u reaches output u - kw through tap kw, so each (output row, kw) keeps
+//    its own accumulator over the same A fragments and the three are summed with a
+//    shift of kw rows when the tile is done. Output rows that straddle the tile
+//    edge take their missing terms from the previous tile (a 3-value carry), so
+//    tile j completes the outputs [32j - 2, 32j + 30).
+//  * A-row m of the MFMA holds input voxel x(m) = 16*((m>>2)&1) + 4*(m>>3) + (m&3),
+//    so that accumulator register r of lane half g is voxel 16g + r: the W shift is
+//    a register shift except at r < kw, where the value comes from the other lane
+//    half (one ds_bpermute per value) or from the carry.
+//  * Staged rows are [x][16-byte unit], the unit XOR-swizzled by bits of x so the
+//    16 lanes of each ds_read_b128 phase hit distinct bank groups.
+//  * Results leave through a per-wave LDS transpose as 16-byte buffer stores;
+//    stores of outputs outside the tensor get an out-of-range offset and are
+//    dropped, so every wave issues the same number of memory operations per tile
+//    and the vmcnt waits are compile-time constants (vector memory operations
+//    complete in issue order).
 #include <algorithm>
 
 #include "common.h"
@@ -25,243 +36,419 @@
 namespace shardconv {
 
 typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8_r;
+typedef __attribute__((ext_vector_type(2))) __bf16 bf16x2_r;
 typedef __attribute__((ext_vector_type(16))) float f32x16_r;
+typedef __attribute__((ext_vector_type(4))) unsigned int u32x4_r;
 
 #define SC_LDS(p) ((__attribute__((address_space(3))) void*)(p))
 
 namespace {
 
-struct RowsArgs {
+struct XmArgs {
     const char* tile;
     const char* wfrag;
     char* y;
-    int64_t n;
-    int64_t P[3], O[3];
+    int32_t P[3], O[3];
     int32_t pad[3];
-    int32_t NB[3];
-    int64_t nbricks;
+    int32_t NBZ, NBY, NXT;  // bricks along D and H, input tiles along W
+    int32_t nseg, T;        // W segments per row and their length in tiles
+    uint32_t nbricks;       // n * NBZ * NBY * nseg
     uint32_t batch_bytes;   // tile bytes per batch item (< 2^32)
+    uint32_t ybatch_bytes;  // output bytes per batch item (< 2^32)
     int32_t cout;
 };
 
-template <int CIN, int NT, int KD, int KH, int KW, int WZ, int WY, int R>
-struct RowsCfg {
-    static constexpr int NKC = CIN / 16;          // 16-channel K chunks
-    static constexpr int BZ = WZ, BY = WY * R, BX = 32;
-    static constexpr int BIZ = BZ + KD - 1, BIY = BY + KH - 1, BIX = BX + KW - 1;
-    static constexpr int BIV = BIZ * BIY * BIX;
-    static constexpr int SLOTS = BIV * 2;          // 16-byte units per chunk
-    static constexpr int SLOTS_PAD = (SLOTS + 255) / 256 * 256;
-    static constexpr int NIT = SLOTS_PAD / 256;    // direct-load instructions per thread per chunk
-    static constexpr int CHUNK_BYTES = SLOTS_PAD * 16;
-    static constexpr int TAPS = KD * KH * KW;
-    static constexpr int W_BYTES = TAPS * NKC * NT * 1024;
-    static constexpr int W_SLOTS = W_BYTES / 16;
-    static constexpr int LDS_BYTES = W_BYTES + 2 * CHUNK_BYTES;
-    static constexpr int NROWS_IN = R + KH - 1;    // input rows a wave reads per (kd, kw)
+// 16-byte unit swizzle of voxel x for UPV units per voxel (see file comment).
+template <int UPV>
+__device__ __forceinline__ constexpr int xm_swz(int x)
+{
+    return UPV == 4 ? (((x >> 2) & 1) | (((x >> 4) & 1) << 1))
+                    : (((x >> 1) & 1) | (((x >> 2) & 1) << 1) | (((x >> 4) & 1) << 2));
+}
+
+template <int CIN, int KD, int KH, int WZ, int WY, int WC, int R, int NBUF>
+struct XmCfg {
+    static_assert(CIN == 32 || CIN == 64, "16-byte units per voxel: 4 or 8");
+    static_assert(WZ * WY * WC == 4, "four waves");
+    static_assert(NBUF >= 2 && NBUF <= 4, "stage depth");
+    static constexpr int KW = 3;
+    static constexpr int UPV = CIN / 8;
+    static constexpr int NKC = CIN / 16;
+    static constexpr int BZ = WZ, BY = WY * R;
+    static constexpr int IRZ = BZ + KD - 1, IRY = BY + KH - 1, IR = IRZ * IRY;
+    static constexpr int ROW_BYTES = 32 * UPV * 16;
+    static constexpr int STAGE_BYTES = IR * ROW_BYTES;
+    static constexpr int RPI = 256 / (32 * UPV);  // staged rows per direct-load instruction
+    static_assert(IRY % RPI == 0, "an instruction's rows share their D row");
+    static constexpr int NIT = IR / RPI;          // direct loads per thread per stage
+    static constexpr int NROWS_IN = R + KH - 1;
+    static_assert(NROWS_IN < 16, "lgkmcnt range");
+    static constexpr int EPI_BYTES = 2048;  // one 32 x 32 bf16 output tile per wave
+    static constexpr int EPI_STORES = R * 2;
+    static constexpr int LDS_BYTES = NBUF * STAGE_BYTES + 4 * EPI_BYTES;
+    static constexpr int VM_BASE = NIT * (NBUF - 2);
+    static_assert(VM_BASE + EPI_STORES * 3 < 64, "vmcnt range");
 };
 
-template <int CIN, int NT, int KD, int KH, int KW, int WZ, int WY, int R>
-__global__ __launch_bounds__(256, 1) void conv_fwd_rows(RowsArgs a)
+template <int CIN, int KD, int KH, int WZ, int WY, int WC, int R, int NBUF>
+__global__ __launch_bounds__(256, 1) void conv_fwd_xm(XmArgs a)
 {
-    using C = RowsCfg<CIN, NT, KD, KH, KW, WZ, WY, R>;
+    using C = XmCfg<CIN, KD, KH, WZ, WY, WC, R, NBUF>;
+    constexpr int KW = C::KW;
     extern __shared__ uint4 lds4[];
     char* lds = reinterpret_cast<char*>(lds4);
-    char* wl = lds;                       // weights
-    char* cb0 = lds + C::W_BYTES;         // chunk buffer 0 (buffer 1 follows)
-    const int tid = threadIdx.x;
-    const int lane = tid & 63;
-    const int wave = tid >> 6;
-    const int wz = wave / WY, wy = wave % WY;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int wc = wave % WC, wy = (wave / WC) % WY, wz = wave / (WC * WY);
     const int g = lane >> 5;
-    const int ox = lane & 31;
-    const int64_t nblk_grid = gridDim.x;
-    const int64_t L = xcd_remap(blockIdx.x, nblk_grid);
+    const uint32_t G = gridDim.x;
+    const uint32_t L = uint32_t(xcd_remap(blockIdx.x, G));
 
-    // weights -> LDS (once)
+    // weights of this wave's output-channel tile -> registers
+    uint4 wv[KD][KH][KW][C::NKC];
     {
-        __amdgpu_buffer_rsrc_t wr = __builtin_amdgcn_make_buffer_rsrc(const_cast<char*>(a.wfrag), short(0),
-                                                                      C::W_BYTES, 0x00020000);
-        for (int s0 = 0; s0 < C::W_SLOTS; s0 += 256) {
-            const int s = s0 + tid;
-            if (s < C::W_SLOTS)
-                __builtin_amdgcn_raw_ptr_buffer_load_lds(wr, SC_LDS(wl + (s0 + wave * 64) * 16), 16, s * 16, 0, 0, 0);
-        }
-    }
-
-    // per-thread staging slots: relative byte offset within a brick and its (z, y, x)
-    uint32_t srel[C::NIT];
-    uint32_t szyx[C::NIT];  // z << 20 | y << 10 | x, or 0xffffffff for padding slots
+        const uint4* wf = reinterpret_cast<const uint4*>(a.wfrag);
 #pragma unroll
-    for (int it = 0; it < C::NIT; ++it) {
-        const int s = it * 256 + tid;
-        if (s < C::SLOTS) {
-            const int v = s >> 1;
-            const int x = v % C::BIX;
-            const int yz = v / C::BIX;
-            const int y = yz % C::BIY;
-            const int z = yz / C::BIY;
-            const int u = (s & 1) ^ ((x >> 3) & 1);
-            srel[it] = uint32_t(((int64_t(z) * a.P[1] + y) * a.P[2] + x) * (CIN * 2) + u * 16);
-            szyx[it] = (uint32_t(z) << 20) | (uint32_t(y) << 10) | uint32_t(x);
-        } else {
-            srel[it] = 0;
-            szyx[it] = 0xffffffffu;
-        }
-    }
-
-    // per-lane A-read base (byte address within chunk buffer 0) for each kw
-    uint32_t abase[KW];
+        for (int kd = 0; kd < KD; ++kd)
 #pragma unroll
-    for (int kw = 0; kw < KW; ++kw) {
-        const int x = ox + kw;
-        abase[kw] = uint32_t((wz * C::BIY + wy * R) * C::BIX * 32 + x * 32 + ((g ^ ((x >> 3) & 1)) * 16)) +
-                    uint32_t(C::W_BYTES);
+            for (int kh = 0; kh < KH; ++kh)
+#pragma unroll
+                for (int kw = 0; kw < KW; ++kw)
+#pragma unroll
+                    for (int kc = 0; kc < C::NKC; ++kc) {
+                        const int tap = (kd * KH + kh) * KW + kw;
+                        wv[kd][kh][kw][kc] = wf[((tap * C::NKC + kc) * WC + wc) * 64 + lane];
+                    }
     }
-    const uint32_t bbase = uint32_t(lane * 16);
 
-    const int64_t per_b = (a.nbricks - L + nblk_grid - 1) / nblk_grid;  // bricks of this workgroup
-    const int64_t nchunks = per_b * C::NKC;
+    // staging: instruction it of a thread loads 16-byte unit su of voxel xs of
+    // staged row it * RPI + hs (rows D-major, then H)
+    const int hs = tid / (32 * C::UPV), xs = (tid % (32 * C::UPV)) / C::UPV, su = tid % C::UPV;
+    const uint32_t SY = uint32_t(a.P[2]) * (CIN * 2), SZ = uint32_t(a.P[1]) * SY;
+    const uint32_t tb = uint32_t(hs) * SY + uint32_t(xs * CIN * 2 + (su ^ xm_swz<C::UPV>(xs)) * 16);
 
-    // stage chunk q (brick index it_b = q / NKC, channel chunk kc = q % NKC) into buffer q & 1
-    auto stage = [&](int64_t q) {
-        const int64_t bi = L + (q / C::NKC) * nblk_grid;
-        const int kc = int(q % C::NKC);
-        int64_t b = bi;
-        const int bx = int(b % a.NB[2]);
-        b /= a.NB[2];
-        const int by = int(b % a.NB[1]);
-        b /= a.NB[1];
-        const int bz = int(b % a.NB[0]);
-        const int64_t nn = b / a.NB[0];
-        const int64_t i0 = int64_t(bz) * C::BZ - a.pad[0];
-        const int64_t i1 = int64_t(by) * C::BY - a.pad[1];
-        const int64_t i2 = int64_t(bx) * C::BX - a.pad[2];
-        const bool inner = i0 >= 0 && i0 + C::BIZ <= a.P[0] && i1 >= 0 && i1 + C::BIY <= a.P[1] && i2 >= 0 &&
-                           i2 + C::BIX <= a.P[2];
+    // A-read lane offsets within a staged row, per 16-channel chunk
+    const int m = lane & 31;
+    const int xa = 16 * ((m >> 2) & 1) + 4 * (m >> 3) + (m & 3);
+    const uint32_t lds0 = lds_addr(lds);
+    uint32_t abase[C::NKC];
+#pragma unroll
+    for (int kc = 0; kc < C::NKC; ++kc)
+        abase[kc] = lds0 + uint32_t((wz * C::IRY + wy * R) * C::ROW_BYTES + xa * C::UPV * 16 +
+                                    (((2 * kc) | g) ^ xm_swz<C::UPV>(xa)) * 16);
+
+    // bricks L, L + G, ... ; brick b is W segment b % nseg of output rows b / nseg.
+    // A segment after the first starts one tile early (its outputs are not stored)
+    // to build the carry.
+    struct Pos {
+        uint32_t brick;
+        int32_t j, jend, jstore;
+    };
+    auto seg_start = [&](Pos& p) {
+        if (p.brick >= a.nbricks) return;
+        const int32_t seg = int32_t(p.brick % uint32_t(a.nseg));
+        p.jstore = seg * a.T;
+        p.j = seg > 0 ? p.jstore - 1 : 0;
+        p.jend = min(p.jstore + a.T, a.NXT);
+    };
+    auto advance = [&](Pos& p) {
+        if (++p.j >= p.jend) {
+            p.brick += G;
+            seg_start(p);
+        }
+    };
+    auto rows_of = [&](uint32_t brick, int& bz, int& by, uint32_t& nn) {
+        uint32_t t = brick / uint32_t(a.nseg);
+        by = int(t % uint32_t(a.NBY));
+        t /= uint32_t(a.NBY);
+        bz = int(t % uint32_t(a.NBZ));
+        nn = t / uint32_t(a.NBZ);
+    };
+
+    auto stage = [&](const Pos& p, int buf) {
+        char* dst = lds + buf * C::STAGE_BYTES + wave * 64 * 16;
+        if (p.brick >= a.nbricks) {
+            // past the last unit: keep the per-thread load count uniform (zeros)
+            __amdgpu_buffer_rsrc_t r = __builtin_amdgcn_make_buffer_rsrc(const_cast<char*>(a.tile), short(0),
+                                                                         int(a.batch_bytes), 0x00020000);
+#pragma unroll
+            for (int it = 0; it < C::NIT; ++it)
+                __builtin_amdgcn_raw_ptr_buffer_load_lds(r, SC_LDS(dst + it * 4096), 16, a.batch_bytes, 0, 0, 0);
+            return;
+        }
+        int bz, by;
+        uint32_t nn;
+        rows_of(p.brick, bz, by, nn);
+        const int i0 = bz * C::BZ - a.pad[0];
+        const int i1 = by * C::BY - a.pad[1];
+        const int i2 = p.j * 32 - a.pad[2];
+        const bool inner = i0 >= 0 && i0 + C::IRZ <= a.P[0] && i1 >= 0 && i1 + C::IRY <= a.P[1] && i2 >= 0 &&
+                           i2 + 32 <= a.P[2];
+        const int64_t origin = ((int64_t(i0) * a.P[1] + i1) * a.P[2] + i2) * (CIN * 2);
         __amdgpu_buffer_rsrc_t r = __builtin_amdgcn_make_buffer_rsrc(
-            const_cast<char*>(a.tile) + nn * int64_t(a.batch_bytes), short(0), int(a.batch_bytes), 0x00020000);
-        const int64_t origin = ((i0 * a.P[1] + i1) * a.P[2] + i2) * (CIN * 2) + kc * 32;
-        char* dst = cb0 + (q & 1) * C::CHUNK_BYTES;
+            const_cast<char*>(a.tile) + int64_t(nn) * a.batch_bytes, short(0), int(a.batch_bytes), 0x00020000);
+        if (inner) {
+            const uint32_t org = uint32_t(origin);
 #pragma unroll
-        for (int it = 0; it < C::NIT; ++it) {
-            const uint32_t zyx = szyx[it];
-            if (zyx == 0xffffffffu) continue;
-            uint32_t off;
-            if (inner) {
-                off = uint32_t(origin + srel[it]);
-            } else {
-                const int64_t t0 = i0 + (zyx >> 20), t1 = i1 + ((zyx >> 10) & 1023), t2 = i2 + (zyx & 1023);
-                const bool ok = t0 >= 0 && t0 < a.P[0] && t1 >= 0 && t1 < a.P[1] && t2 >= 0 && t2 < a.P[2];
-                off = ok ? uint32_t(origin + int64_t(srel[it])) : a.batch_bytes;
+            for (int it = 0; it < C::NIT; ++it) {
+                const int row0 = it * C::RPI;
+                const uint32_t soff = org + uint32_t(row0 / C::IRY) * SZ + uint32_t(row0 % C::IRY) * SY;
+                __builtin_amdgcn_raw_ptr_buffer_load_lds(r, SC_LDS(dst + it * 4096), 16, tb, soff, 0, 0);
             }
-            __builtin_amdgcn_raw_ptr_buffer_load_lds(r, SC_LDS(dst + (it * 256 + wave * 64) * 16), 16, off, 0, 0, 0);
+        } else {
+#pragma unroll
+            for (int it = 0; it < C::NIT; ++it) {
+                const int row0 = it * C::RPI;
+                const int rz = row0 / C::IRY, ry = row0 % C::IRY + hs;
+                const int t0 = i0 + rz, t1 = i1 + ry, t2 = i2 + xs;
+                const bool ok = t0 >= 0 && t0 < a.P[0] && t1 >= 0 && t1 < a.P[1] && t2 >= 0 && t2 < a.P[2];
+                const uint32_t off =
+                    ok ? uint32_t(origin + int64_t(rz) * SZ + int64_t(row0 % C::IRY) * SY + tb) : a.batch_bytes;
+                __builtin_amdgcn_raw_ptr_buffer_load_lds(r, SC_LDS(dst + it * 4096), 16, off, 0, 0, 0);
+            }
         }
     };
 
-    f32x16_r acc[R][NT];
+    // epilogue LDS addresses: lane (g, co) writes voxel 16g + e of channel co at
+    // slot (16g + e) ^ g; the read-back gives lane U = it * 64 + lane the 16 bytes
+    // (voxel U / 4, channels 8 * (U % 4) ...)
+    const uint32_t epi = lds0 + uint32_t(NBUF * C::STAGE_BYTES + wave * C::EPI_BYTES);
+    const int co = lane & 31;
+    const uint32_t ew_even = epi + uint32_t(co * 2 + 1024 * g + 64 * g);
+    const uint32_t ew_odd = epi + uint32_t(co * 2 + 1024 * g - 64 * g);
+    uint32_t er[2];
 #pragma unroll
-    for (int r = 0; r < R; ++r)
-#pragma unroll
-        for (int t = 0; t < NT; ++t)
-#pragma unroll
-            for (int e = 0; e < 16; ++e) acc[r][t][e] = 0.f;
-
-    if (nchunks > 0) stage(0);
-    __builtin_amdgcn_s_waitcnt(0);
-    __syncthreads();
-
-    bf16_t* y = reinterpret_cast<bf16_t*>(a.y);
-    for (int64_t q = 0; q < nchunks; ++q) {
-        if (q + 1 < nchunks) stage(q + 1);
-        const int kc = int(q % C::NKC);
-        const uint32_t boff = uint32_t((q & 1) * C::CHUNK_BYTES);
-#pragma unroll
-        for (int kd = 0; kd < KD; ++kd) {
-#pragma unroll
-            for (int kw = 0; kw < KW; ++kw) {
-                uint4 av[C::NROWS_IN];
-#pragma unroll
-                for (int j = 0; j < C::NROWS_IN; ++j)
-                    av[j] = *reinterpret_cast<const uint4*>(lds + abase[kw] + boff +
-                                                            (kd * C::BIY + j) * C::BIX * 32);
-                uint4 bv[KH][NT];
-#pragma unroll
-                for (int kh = 0; kh < KH; ++kh)
-#pragma unroll
-                    for (int t = 0; t < NT; ++t) {
-                        const int tap = (kd * KH + kh) * KW + kw;
-                        bv[kh][t] = *reinterpret_cast<const uint4*>(wl + bbase + ((tap * C::NKC + kc) * NT + t) * 1024);
-                    }
-#pragma unroll
-                for (int kh = 0; kh < KH; ++kh)
-#pragma unroll
-                    for (int r = 0; r < R; ++r)
-#pragma unroll
-                        for (int t = 0; t < NT; ++t)
-                            acc[r][t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-                                __builtin_bit_cast(bf16x8_r, av[r + kh]), __builtin_bit_cast(bf16x8_r, bv[kh][t]),
-                                acc[r][t], 0, 0, 0);
-            }
-        }
-        if (kc == C::NKC - 1) {
-            // epilogue of brick q / NKC: rows 8*(e/4) + 4*g + (e%4) of each M tile, column = output channel
-            const int64_t bi = L + (q / C::NKC) * nblk_grid;
-            int64_t b = bi;
-            const int bx = int(b % a.NB[2]);
-            b /= a.NB[2];
-            const int by = int(b % a.NB[1]);
-            b /= a.NB[1];
-            const int bz = int(b % a.NB[0]);
-            const int64_t nn = b / a.NB[0];
-            const int64_t o0 = int64_t(bz) * C::BZ + wz;
-            const int64_t ox0 = int64_t(bx) * C::BX;
-#pragma unroll
-            for (int r = 0; r < R; ++r) {
-                const int64_t o1 = int64_t(by) * C::BY + wy * R + r;
-                const bool rok = o0 < a.O[0] && o1 < a.O[1];
-                bf16_t* row = y + (((nn * a.O[0] + o0) * a.O[1] + o1) * a.O[2] + ox0) * a.cout;
-#pragma unroll
-                for (int t = 0; t < NT; ++t) {
-                    const int co = t * 32 + ox;  // lane's column
-#pragma unroll
-                    for (int e = 0; e < 16; ++e) {
-                        const int xr = 8 * (e >> 2) + 4 * g + (e & 3);
-                        if (rok && ox0 + xr < a.O[2] && co < a.cout)
-                            row[xr * a.cout + co] = __builtin_bit_cast(bf16_t, __bf16(acc[r][t][e]));
-                        acc[r][t][e] = 0.f;
-                    }
-                }
-            }
-        }
-        __builtin_amdgcn_s_waitcnt(0);
-        __syncthreads();
+    for (int it = 0; it < 2; ++it) {
+        const int U = it * 64 + lane, v = U >> 2, uu = U & 3;
+        er[it] = epi + uint32_t((v ^ ((v >> 4) & 1)) * 64 + uu * 16);
     }
+
+    // output position of a computed tile: W tile j, output rows (o0, o1b + r)
+    struct TileOut {
+        int32_t j, o0, o1b;
+        uint32_t nn;
+        bool store;
+    };
+    auto tile_out = [&](const Pos& p) {
+        int bz, by;
+        uint32_t nn;
+        rows_of(p.brick, bz, by, nn);
+        return TileOut{p.j, bz * C::BZ + wz, by * C::BY + wy * R, nn, p.j >= p.jstore};
+    };
+
+    f32x16_r acc[R][KW];
+    float carry[R][3];
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+        carry[r][0] = carry[r][1] = carry[r][2] = 0.f;
+#pragma unroll
+        for (int kw = 0; kw < KW; ++kw)
+#pragma unroll
+            for (int e = 0; e < 16; ++e) acc[r][kw][e] = 0.f;
+    }
+
+    // The epilogue of output row rr of tile t, in five pieces that the main loop
+    // interleaves with the MFMAs of the next row:
+    //   0, 1: out[16g + e] = A2[e] + A1[e - 1] + A0[e - 2] for e < 8, e >= 8
+    //   2, 3: bf16 conversion and transpose writes to the wave's LDS buffer; 3 also
+    //         issues the two read-backs
+    //   4:    16-byte stores (the read-backs must have completed)
+    float eo[16];
+    lds_u32x4 ed[2];
+    auto epi_piece = [&](int rr, int k, const TileOut& t) {
+        if (k == 0) {
+            // values of voxels 14, 15 of the other lane half (v_permlane32_swap with
+            // itself gives lane l the row-0 value in [0] and the row-1 value in [1])
+            const uint32_t x1 = __float_as_uint(acc[rr][1][15]);
+            const uint32_t x2 = __float_as_uint(acc[rr][0][14]);
+            const uint32_t x3 = __float_as_uint(acc[rr][0][15]);
+            const auto p1 = __builtin_amdgcn_permlane32_swap(x1, x1, false, false);
+            const auto p2 = __builtin_amdgcn_permlane32_swap(x2, x2, false, false);
+            const auto p3 = __builtin_amdgcn_permlane32_swap(x3, x3, false, false);
+            const float s1 = __uint_as_float(g ? p1[0] : p1[1]);
+            const float t0 = __uint_as_float(g ? p2[0] : p2[1]);
+            const float v0 = __uint_as_float(g ? p3[0] : p3[1]);
+            const float c1 = g ? s1 : carry[rr][0];
+            const float c2 = g ? t0 : carry[rr][1];
+            const float c3 = g ? v0 : carry[rr][2];
+            carry[rr][0] = s1;
+            carry[rr][1] = t0;
+            carry[rr][2] = v0;
+            eo[0] = acc[rr][2][0] + c1 + c2;
+            eo[1] = acc[rr][2][1] + acc[rr][1][0] + c3;
+#pragma unroll
+            for (int e = 2; e < 8; ++e) eo[e] = acc[rr][2][e] + acc[rr][1][e - 1] + acc[rr][0][e - 2];
+        } else if (k == 1) {
+#pragma unroll
+            for (int e = 8; e < 16; ++e) eo[e] = acc[rr][2][e] + acc[rr][1][e - 1] + acc[rr][0][e - 2];
+        } else if (k == 2 || k == 3) {
+#pragma unroll
+            for (int e = 8 * (k - 2); e < 8 * (k - 1); e += 2) {
+                const bf16x2_r pk = {__bf16(eo[e]), __bf16(eo[e + 1])};
+                const uint32_t w = __builtin_bit_cast(uint32_t, pk);
+                lds_write_b16(ew_even + uint32_t(e * 64), w);
+                lds_write_b16_hi(ew_odd + uint32_t((e + 1) * 64), w);
+            }
+            if (k == 3) {
+                ed[0] = lds_read_b128(er[0]);
+                ed[1] = lds_read_b128(er[1]);
+            }
+        } else {
+            lds_ready(ed[0]);
+            lds_ready(ed[1]);
+            __amdgpu_buffer_rsrc_t yr = __builtin_amdgcn_make_buffer_rsrc(
+                a.y + int64_t(t.nn) * a.ybatch_bytes, short(0), int(a.ybatch_bytes), 0x00020000);
+            const int o1 = t.o1b + rr;
+            const bool rowok = t.store && t.o0 < a.O[0] && o1 < a.O[1];
+            const uint32_t rbase = uint32_t((int64_t(t.o0) * a.O[1] + o1) * a.O[2]);
+#pragma unroll
+            for (int it = 0; it < 2; ++it) {
+                const int v = (it * 64 + lane) >> 2, uu = lane & 3;
+                const int ox = t.j * 32 - (KW - 1) + v;
+                const bool ok = rowok && ox >= 0 && ox < a.O[2];
+                const uint32_t off =
+                    ok ? ((rbase + uint32_t(ox)) * uint32_t(a.cout) + uint32_t(wc * 32 + uu * 8)) * 2u
+                       : a.ybatch_bytes;
+                __builtin_amdgcn_raw_buffer_store_b128(ed[it], yr, off, 0, 0);
+            }
+        }
+    };
+    // which epilogue pieces run in group q of a row
+    constexpr int NG = KD * C::NKC;  // (kd, kc) groups per output row
+    static_assert(NG >= 4, "five epilogue pieces in at least four groups");
+    auto pieces_of = [&](int q, int rr, const TileOut& t) {
+        if (NG >= 5) {
+            if (q < 5) epi_piece(rr, q, t);
+        } else {
+            if (q == 0) epi_piece(rr, 0, t);
+            if (q == 1) epi_piece(rr, 1, t);
+            if (q == 2) {
+                epi_piece(rr, 2, t);
+                epi_piece(rr, 3, t);
+            }
+            if (q == 3) epi_piece(rr, 4, t);
+        }
+    };
+
+    Pos cp{L, 0, 0, 0}, sp{L, 0, 0, 0};
+    seg_start(cp);
+    seg_start(sp);
+#pragma unroll
+    for (int p = 0; p < NBUF - 1; ++p) {
+        stage(sp, p);
+        advance(sp);
+    }
+
+    // the row R - 1 of the previous tile is pending at the start of each tile; the
+    // first tile's predecessor stores nothing
+    TileOut prev{0, 0, 0, 0, false};
+    int cbuf = 0, sbuf = NBUF - 1;
+    for (uint32_t u = 0; cp.brick < a.nbricks; ++u) {
+        // Unit u's loads have landed and every wave is done with the buffer that
+        // is refilled next. Issued after unit u's loads: the loads of the next
+        // NBUF - 2 units and the stores of the last min(u, NBUF - 1) units.
+        const uint32_t ks = u < NBUF - 1 ? u : NBUF - 1;
+        if (ks == 0)
+            wait_vm_barrier<C::VM_BASE>();
+        else if (ks == 1)
+            wait_vm_barrier<C::VM_BASE + C::EPI_STORES>();
+        else if (ks == 2)
+            wait_vm_barrier<C::VM_BASE + 2 * C::EPI_STORES>();
+        else
+            wait_vm_barrier<C::VM_BASE + 3 * C::EPI_STORES>();
+        stage(sp, sbuf);
+        advance(sp);
+        sbuf = sbuf + 1 == NBUF ? 0 : sbuf + 1;
+        const TileOut cur = tile_out(cp);
+
+        // steps s = (row r, group q): the KH input rows of step s + 1 are read while
+        // step s multiplies
+        const uint32_t boff = uint32_t(cbuf * C::STAGE_BYTES);
+        constexpr int S = R * NG;
+        lds_u32x4 av[2][KH];
+        auto load_step = [&](int st, lds_u32x4 (&A)[KH]) {
+            const int r = st / NG, q = st % NG;
+            const int kd = q / C::NKC, kc = q % C::NKC;
+#pragma unroll
+            for (int kh = 0; kh < KH; ++kh)
+                A[kh] = lds_read_b128(abase[kc] + boff + uint32_t((kd * C::IRY + r + kh) * C::ROW_BYTES));
+        };
+        load_step(0, av[0]);
+#pragma unroll
+        for (int st = 0; st < S; ++st) {
+            const int cur_b = st & 1;
+            const int r = st / NG, q = st % NG;
+            const int kd = q / C::NKC, kc = q % C::NKC;
+            if (st + 1 < S) {
+                load_step(st + 1, av[cur_b ^ 1]);
+                lds_wait<KH>();
+            } else {
+                lds_wait<0>();
+            }
+#pragma unroll
+            for (int kh = 0; kh < KH; ++kh) lds_ready(av[cur_b][kh]);
+#pragma unroll
+            for (int kh = 0; kh < KH; ++kh)
+#pragma unroll
+                for (int kw = 0; kw < KW; ++kw) {
+                    const f32x16_r c0 = (q == 0 && kh == 0) ? f32x16_r{} : acc[r][kw];
+                    acc[r][kw] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+                        __builtin_bit_cast(bf16x8_r, av[cur_b][kh]),
+                        __builtin_bit_cast(bf16x8_r, wv[kd][kh][kw][kc]), c0, 0, 0, 0);
+                }
+            // the pending row: R - 1 of the previous tile while row 0 multiplies,
+            // else row r - 1 of this tile
+            if (r == 0)
+                pieces_of(q, R - 1, prev);
+            else
+                pieces_of(q, r - 1, cur);
+        }
+        cbuf = cbuf + 1 == NBUF ? 0 : cbuf + 1;
+        prev = cur;
+        advance(cp);
+    }
+    // the last tile's row R - 1
+#pragma unroll
+    for (int k = 0; k < 4; ++k) epi_piece(R - 1, k, prev);
+    lds_wait<0>();
+    epi_piece(R - 1, 4, prev);
+    // no direct loads may still target LDS when the workgroup retires
+    wait_vm_barrier<0>();
 }
 
-template <int CIN, int NT, int KD, int KH, int KW, int WZ, int WY, int R>
-hipError_t launch_rows(const Tile3& t, const Conv3& cv, const void* tile, const void* wfrag, void* y, hipStream_t s)
+template <int CIN, int KD, int KH, int WZ, int WY, int WC, int R, int NBUF>
+hipError_t launch_xm(const Tile3& t, const Conv3& cv, const void* tile, const void* wfrag, void* y, hipStream_t s)
 {
-    using C = RowsCfg<CIN, NT, KD, KH, KW, WZ, WY, R>;
-    RowsArgs a{};
+    using C = XmCfg<CIN, KD, KH, WZ, WY, WC, R, NBUF>;
+    static_assert(C::LDS_BYTES <= 160 * 1024, "LDS budget");
+    XmArgs a{};
     a.tile = static_cast<const char*>(tile);
     a.wfrag = static_cast<const char*>(wfrag);
     a.y = static_cast<char*>(y);
-    a.n = t.n;
     for (int k = 0; k < 3; ++k) {
-        a.P[k] = t.P[k];
-        a.O[k] = cv.O[k];
+        a.P[k] = int32_t(t.P[k]);
+        a.O[k] = int32_t(cv.O[k]);
         a.pad[k] = int32_t(cv.pad[k]);
     }
-    const int bo[3] = {C::BZ, C::BY, C::BX};
-    for (int k = 0; k < 3; ++k) a.NB[k] = int32_t(ceil_div(cv.O[k], bo[k]));
-    a.nbricks = t.n * int64_t(a.NB[0]) * a.NB[1] * a.NB[2];
-    a.batch_bytes = uint32_t(t.P[0] * t.P[1] * t.P[2] * t.c * 2);
-    a.cout = int32_t(cv.cout);
+    if (t.n == 0 || cv.O[0] == 0 || cv.O[1] == 0 || cv.O[2] == 0) return hipSuccess;
+    a.NBZ = int32_t(ceil_div(cv.O[0], C::BZ));
+    a.NBY = int32_t(ceil_div(cv.O[1], C::BY));
+    a.NXT = int32_t(ceil_div(cv.O[2] + C::KW - 1, 32));
     int dev = 0, cus = 256;
     if (hipGetDevice(&dev) == hipSuccess) hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
-    const int64_t grid = std::max<int64_t>(1, std::min<int64_t>(a.nbricks, cus));
-    auto fn = &conv_fwd_rows<CIN, NT, KD, KH, KW, WZ, WY, R>;
+    const int64_t rows = t.n * int64_t(a.NBZ) * a.NBY;
+    // split W rows into segments when there are too few bricks to fill the chip
+    int64_t nseg = 1;
+    while (rows * nseg < cus && (a.NXT / (nseg * 2)) >= 8) nseg *= 2;
+    a.nseg = int32_t(nseg);
+    a.T = int32_t(ceil_div(a.NXT, nseg));
+    const int64_t nb = rows * nseg;
+    if (nb >= (int64_t(1) << 31)) return hipErrorNotSupported;
+    a.nbricks = uint32_t(nb);
+    a.batch_bytes = uint32_t(t.P[0] * t.P[1] * t.P[2] * t.c * 2);
+    a.ybatch_bytes = uint32_t(cv.O[0] * cv.O[1] * cv.O[2] * cv.cout * 2);
+    a.cout = int32_t(cv.cout);
+    const int64_t grid = std::max<int64_t>(1, std::min<int64_t>(nb, cus));
+    auto fn = &conv_fwd_xm<CIN, KD, KH, WZ, WY, WC, R, NBUF>;
     hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(fn), hipFuncAttributeMaxDynamicSharedMemorySize,
                                        C::LDS_BYTES);
     if (e != hipSuccess) return e;
@@ -271,25 +458,29 @@ hipError_t launch_rows(const Tile3& t, const Conv3& cv, const void* tile, const 
 
 }  // namespace
 
-// The row-reuse kernel applies to bf16, unit stride, tiles of < 4 GiB per batch
-// item, 16-byte aligned tiles, and the (channel, kernel) shapes instantiated below.
+// The W-march kernel applies to bf16, unit stride, kernel width 3 along W,
+// tiles and outputs of < 4 GiB per batch item, 16-byte aligned buffers, extents
+// below 2^24, and the (channel, kernel) shapes instantiated below.
 // Returns hipErrorNotSupported when it does not apply.
 hipError_t launch_conv_fwd_rows(const Tile3& t, const Conv3& cv, shard_dtype_t dt, const void* tile,
                                 const void* wfrag, int nkc_frag, int nt_frag, void* y, hipStream_t s)
 {
     if (dt != SHARD_BF16 || force_tiled()) return hipErrorNotSupported;
-    if (cv.S[0] != 1 || cv.S[1] != 1 || cv.S[2] != 1) return hipErrorNotSupported;
-    if (reinterpret_cast<uintptr_t>(tile) % 16 != 0 || reinterpret_cast<uintptr_t>(wfrag) % 16 != 0)
+    if (cv.S[0] != 1 || cv.S[1] != 1 || cv.S[2] != 1 || cv.K[2] != 3) return hipErrorNotSupported;
+    if (reinterpret_cast<uintptr_t>(tile) % 16 != 0 || reinterpret_cast<uintptr_t>(wfrag) % 16 != 0 ||
+        reinterpret_cast<uintptr_t>(y) % 16 != 0)
         return hipErrorNotSupported;
     const int64_t bb = t.P[0] * t.P[1] * t.P[2] * t.c * 2;
-    if (bb >= (int64_t(1) << 32) - 64) return hipErrorNotSupported;
+    const int64_t yb = cv.O[0] * cv.O[1] * cv.O[2] * cv.cout * 2;
+    if (bb >= (int64_t(1) << 32) - 64 || yb >= (int64_t(1) << 32) - 64) return hipErrorNotSupported;
     for (int k = 0; k < 3; ++k)
-        if (std::abs(cv.pad[k]) > (1 << 20) || cv.O[k] > (int64_t(1) << 30)) return hipErrorNotSupported;
-    // fragment arrays laid out by wfrag_kernel with exactly CIN/16 chunks and NT tiles
-    if (t.c == 32 && cv.cout == 32 && cv.K[0] == 3 && cv.K[1] == 3 && cv.K[2] == 3 && nkc_frag == 2 && nt_frag == 1)
-        return launch_rows<32, 1, 3, 3, 3, 4, 1, 4>(t, cv, tile, wfrag, y, s);
-    if (t.c == 64 && cv.cout == 64 && cv.K[0] == 1 && cv.K[1] == 3 && cv.K[2] == 3 && nkc_frag == 4 && nt_frag == 2)
-        return launch_rows<64, 2, 1, 3, 3, 1, 4, 4>(t, cv, tile, wfrag, y, s);
+        if (std::abs(cv.pad[k]) > (1 << 20) || cv.O[k] >= (int64_t(1) << 24) || t.P[k] >= (int64_t(1) << 24))
+            return hipErrorNotSupported;
+    // fragment arrays laid out by wfrag_kernel with exactly CIN/16 chunks and cout/32 tiles
+    if (t.c == 32 && cv.cout == 32 && cv.K[0] == 3 && cv.K[1] == 3 && nkc_frag == 2 && nt_frag == 1)
+        return launch_xm<32, 3, 3, 4, 1, 1, 2, 3>(t, cv, tile, wfrag, y, s);
+    if (t.c == 64 && cv.cout == 64 && cv.K[0] == 1 && cv.K[1] == 3 && nkc_frag == 4 && nt_frag == 2)
+        return launch_xm<64, 1, 3, 1, 2, 2, 4, 3>(t, cv, tile, wfrag, y, s);
     return hipErrorNotSupported;
 }
 

@@ -41,7 +41,7 @@ struct TrArgs {
     int64_t nbricks;
     uint32_t tile_bytes, dy_bytes;  // per batch item (< 2^32)
     int32_t nmb, ncb, ntg, tgs;     // channel blocks, tap groups, taps per group
-    int32_t nsplit;
+    int32_t nsplit;                 // workgroups per group; split s takes bricks s, s + nsplit, ...
 };
 
 template <int BZ, int BY, int BX, int KD, int KH, int KW, int SD, int SH, int SW, int TPW>
@@ -75,14 +75,16 @@ __global__ __launch_bounds__(256, 1) void wgrad_tr(TrArgs a)
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int64_t G = gridDim.x;
 
-    int64_t b = xcd_remap(blockIdx.x, G);
+    // logical index: group innermost, so each XCD holds a contiguous range of splits per group
+    const int64_t Lg = xcd_remap(blockIdx.x, G);
+    const int64_t groups = int64_t(a.nmb) * a.ncb * a.ntg;
+    int64_t b = Lg % groups;
+    const int64_t split = Lg / groups;
     const int tg = int(b % a.ntg);
     b /= a.ntg;
     const int cb = int(b % a.ncb);
     b /= a.ncb;
-    const int mb = int(b % a.nmb);
-    const int64_t split = b / a.nmb;
-    const int64_t br0 = split * a.nbricks / a.nsplit, br1 = (split + 1) * a.nbricks / a.nsplit;
+    const int mb = int(b);
     const int64_t ci0 = int64_t(cb) * 32, co0 = int64_t(mb) * 32;
     constexpr int TAPS = KD * KH * KW;
 
@@ -182,41 +184,63 @@ __global__ __launch_bounds__(256, 1) void wgrad_tr(TrArgs a)
         }
     };
 
-    const int64_t nb = br1 - br0;
-    if (nb > 0) stage(br0, 0);
-    __builtin_amdgcn_s_waitcnt(0);
-    __syncthreads();
-    for (int64_t k = 0; k < nb; ++k) {
-        if (k + 1 < nb) stage(br0 + k + 1, int((k + 1) & 1));
-        const char* xs = lds + int(k & 1) * C::STAGE_BYTES;
-        const char* ds = xs + C::X_BYTES;
-#pragma unroll 2
-        for (int ks = 0; ks < C::BOV / 16; ++ks) {
-            // output voxel f = 16 ks + kl (the second read takes f + 4, same W row)
-            const int f = 16 * ks + kl;
-            const int xo = f % BX, yo = (f / BX) % BY, zo = f / (BX * BY);
-            const int vin = ((zo * SD) * C::BIY + yo * SH) * C::BIX + xo * SW;
-            const uint2 a0 = tr_read(ds + f * 64 + colb);
-            const uint2 a1 = tr_read(ds + (f + 4) * 64 + colb);
-            const uint4 av = make_uint4(a0.x, a0.y, a1.x, a1.y);
-            const char* xb0 = xs + vin * 64 + colb;
-            const char* xb1 = xb0 + 4 * SW * 64;
+    // operand reads of K step ks (16 output voxels) from stage buffer xs / ds
+    auto load_step = [&](const char* xs, const char* ds, int ks, uint4& av, uint4 (&bv)[TPW]) {
+        const int f = 16 * ks + kl;
+        const int xo = f % BX, yo = (f / BX) % BY, zo = f / (BX * BY);
+        const int vin = ((zo * SD) * C::BIY + yo * SH) * C::BIX + xo * SW;
+        const uint2 a0 = tr_read(ds + f * 64 + colb);
+        const uint2 a1 = tr_read(ds + (f + 4) * 64 + colb);
+        av = make_uint4(a0.x, a0.y, a1.x, a1.y);
+        const char* xb0 = xs + vin * 64 + colb;
+        const char* xb1 = xb0 + 4 * SW * 64;   // f + 4 stays in the same W row (BX % 16 == 0)
 #pragma unroll
-            for (int i = 0; i < TPW; ++i) {
-                if (!tok[i]) continue;
-                const uint2 b0 = tr_read(xb0 + toff[i]);
-                const uint2 b1 = tr_read(xb1 + toff[i]);
-                const uint4 bv = make_uint4(b0.x, b0.y, b1.x, b1.y);
-                acc[i] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8_t2, av),
-                                                                 __builtin_bit_cast(bf16x8_t2, bv), acc[i], 0, 0, 0);
-            }
+        for (int i = 0; i < TPW; ++i) {
+            if (!tok[i]) continue;
+            const uint2 b0 = tr_read(xb0 + toff[i]);
+            const uint2 b1 = tr_read(xb1 + toff[i]);
+            bv[i] = make_uint4(b0.x, b0.y, b1.x, b1.y);
         }
-        __builtin_amdgcn_s_waitcnt(0);
-        __syncthreads();
+    };
+    auto mfma_step = [&](const uint4& av, const uint4 (&bv)[TPW]) {
+#pragma unroll
+        for (int i = 0; i < TPW; ++i) {
+            if (!tok[i]) continue;
+            acc[i] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8_t2, av),
+                                                             __builtin_bit_cast(bf16x8_t2, bv[i]), acc[i], 0, 0, 0);
+        }
+    };
+
+    int64_t b_cur = split;
+    if (b_cur < a.nbricks) stage(b_cur, 0);
+    wait_vm_barrier<0>();
+    int buf = 0;
+    while (b_cur < a.nbricks) {
+        const int64_t b_next = b_cur + a.nsplit;
+        if (b_next < a.nbricks) stage(b_next, buf ^ 1);
+        const char* xs = lds + buf * C::STAGE_BYTES;
+        const char* ds = xs + C::X_BYTES;
+        // software pipeline: the operands of step ks + 1 are read while step ks multiplies
+        uint4 av0, av1, bv0[TPW], bv1[TPW];
+        load_step(xs, ds, 0, av0, bv0);
+#pragma unroll
+        for (int ks = 0; ks < C::BOV / 16; ks += 2) {
+            if (ks + 1 < C::BOV / 16) load_step(xs, ds, ks + 1, av1, bv1);
+            __builtin_amdgcn_sched_barrier(0);
+            mfma_step(av0, bv0);
+            __builtin_amdgcn_sched_barrier(0);
+            if (ks + 2 < C::BOV / 16) load_step(xs, ds, ks + 2, av0, bv0);
+            __builtin_amdgcn_sched_barrier(0);
+            if (ks + 1 < C::BOV / 16) mfma_step(av1, bv1);
+            __builtin_amdgcn_sched_barrier(0);
+        }
+        wait_vm_barrier<0>();
+        buf ^= 1;
+        b_cur = b_next;
     }
     // partial tile: [wave][tap i][lane][16]
     const int64_t grp = (int64_t(mb) * a.ncb + cb) * a.ntg + tg;
-    const int64_t groups = int64_t(a.nmb) * a.ncb * a.ntg;
+
     float4* out = reinterpret_cast<float4*>(a.part + (split * groups + grp) * int64_t(4 * TPW * 1024) +
                                             int64_t(wave) * TPW * 1024);
 #pragma unroll
@@ -289,6 +313,7 @@ static TrPlan plan_tr(const Tile3& t, const Conv3& cv, shard_dtype_t dt)
     a.ntg = int32_t(ceil_div(cv.taps(), a.tgs));
     const int64_t groups = int64_t(a.nmb) * a.ncb * a.ntg;
     a.nsplit = int32_t(std::max<int64_t>(1, std::min<int64_t>(a.nbricks, ceil_div(256, groups))));
+    if (a.nsplit >= 8) a.nsplit -= a.nsplit % 8;
     p.grid = groups * a.nsplit;
     p.lds = lds;
     p.ok = p.grid < (int64_t(1) << 31);

@@ -159,6 +159,9 @@ EDGE = [
     ("3d_s3_negative_pad", "f32", 1, 8, 16, (25, 9, 14), (2, 1, 1), (3, 3, 3), (3, 1, 2)),
     ("3d_wide_channels", "bf16", 1, 96, 80, (9, 10, 40), (2, 1, 1), (3, 3, 3), (1, 1, 1)),
     ("3d_thin_w", "bf16", 1, 32, 32, (10, 11, 3), (2, 1, 1), (3, 3, 3), (1, 1, 1)),
+    # few long rows: the W-march kernels split rows into segments
+    ("3d_long_rows", "bf16", 1, 32, 32, (6, 5, 700), (2, 1, 1), (3, 3, 3), (1, 1, 1)),
+    ("2d_long_rows", "bf16", 2, 64, 64, (9, 1100), (2, 1), (3, 3), (1, 1)),
 ]
 
 
