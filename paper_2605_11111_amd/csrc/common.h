@@ -81,6 +81,18 @@ __device__ __forceinline__ lds_u32x4 lds_read_b128(uint32_t addr)
     return r;
 }
 
+// ds_read_b64_tr_b16: within each 16-lane group, lane i addresses row i / 4,
+// columns 4 * (i % 4) .. + 3 of a row-major 16-bit matrix, and lane j receives
+// column j of the four rows.
+template <int OFF = 0>
+__device__ __forceinline__ uint2 lds_read_tr16_b64(uint32_t addr)
+{
+    static_assert(OFF >= 0 && OFF < 65536, "ds offset range");
+    uint2 r;
+    asm volatile("ds_read_b64_tr_b16 %0, %1 offset:%2" : "=v"(r) : "v"(addr), "n"(OFF));
+    return r;
+}
+
 template <int OFF = 0>
 __device__ __forceinline__ void lds_write_b16(uint32_t addr, uint32_t v)
 {

@@ -59,11 +59,6 @@ struct TrCfg {
     static constexpr int LDS_BYTES = 2 * STAGE_BYTES;
 };
 
-__device__ __forceinline__ uint2 tr_read(const char* p)
-{
-    const s16x4_t2 v = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) s16x4_t2*)SC_LDS2(p));
-    return __builtin_bit_cast(uint2, v);
-}
 
 template <int BZ, int BY, int BX, int KD, int KH, int KW, int SD, int SH, int SW, int TPW>
 __global__ __launch_bounds__(256, 1) void wgrad_tr(TrArgs a)
@@ -88,6 +83,7 @@ __global__ __launch_bounds__(256, 1) void wgrad_tr(TrArgs a)
     const int64_t ci0 = int64_t(cb) * 32, co0 = int64_t(mb) * 32;
     constexpr int TAPS = KD * KH * KW;
 
+    const uint32_t lds0 = lds_addr(lds);
     // this wave's taps (w, w + 4, ...) as byte offsets of their voxel shift in the input brick
     int toff[TPW];
     bool tok[TPW];
@@ -184,25 +180,34 @@ __global__ __launch_bounds__(256, 1) void wgrad_tr(TrArgs a)
         }
     };
 
-    // operand reads of K step ks (16 output voxels) from stage buffer xs / ds
-    auto load_step = [&](const char* xs, const char* ds, int ks, uint4& av, uint4 (&bv)[TPW]) {
+    // operand reads of K step ks (16 output voxels) from stage buffer xs / ds. Every
+    // wave issues 2 + 2 * TPW reads per step (a wave with fewer taps reads tap 0
+    // again) so that the lgkmcnt waits below are the same for all waves.
+    auto load_step = [&](uint32_t xs, uint32_t ds, int ks, lds_u32x4& av, lds_u32x4 (&bv)[TPW]) {
         const int f = 16 * ks + kl;
         const int xo = f % BX, yo = (f / BX) % BY, zo = f / (BX * BY);
         const int vin = ((zo * SD) * C::BIY + yo * SH) * C::BIX + xo * SW;
-        const uint2 a0 = tr_read(ds + f * 64 + colb);
-        const uint2 a1 = tr_read(ds + (f + 4) * 64 + colb);
-        av = make_uint4(a0.x, a0.y, a1.x, a1.y);
-        const char* xb0 = xs + vin * 64 + colb;
-        const char* xb1 = xb0 + 4 * SW * 64;   // f + 4 stays in the same W row (BX % 16 == 0)
+        const uint2 a0 = lds_read_tr16_b64(ds + uint32_t(f * 64 + colb));
+        const uint2 a1 = lds_read_tr16_b64(ds + uint32_t((f + 4) * 64 + colb));
+        av = lds_u32x4{a0.x, a0.y, a1.x, a1.y};
+        const uint32_t xb0 = xs + uint32_t(vin * 64 + colb);
+        const uint32_t xb1 = xb0 + uint32_t(4 * SW * 64);  // f + 4 stays in the same W row (BX % 16 == 0)
 #pragma unroll
         for (int i = 0; i < TPW; ++i) {
-            if (!tok[i]) continue;
-            const uint2 b0 = tr_read(xb0 + toff[i]);
-            const uint2 b1 = tr_read(xb1 + toff[i]);
-            bv[i] = make_uint4(b0.x, b0.y, b1.x, b1.y);
+            const uint2 b0 = lds_read_tr16_b64(xb0 + uint32_t(toff[i]));
+            const uint2 b1 = lds_read_tr16_b64(xb1 + uint32_t(toff[i]));
+            bv[i] = lds_u32x4{b0.x, b0.y, b1.x, b1.y};
         }
     };
-    auto mfma_step = [&](const uint4& av, const uint4 (&bv)[TPW]) {
+    // LDS operations per step (the wait allows at most 15 outstanding)
+    constexpr int RPS = 2 + 2 * TPW;
+    constexpr int WAIT_NEXT = RPS < 15 ? RPS : 15;
+    auto ready = [&](lds_u32x4& av, lds_u32x4 (&bv)[TPW]) {
+        lds_ready(av);
+#pragma unroll
+        for (int i = 0; i < TPW; ++i) lds_ready(bv[i]);
+    };
+    auto mfma_step = [&](const lds_u32x4& av, const lds_u32x4 (&bv)[TPW]) {
 #pragma unroll
         for (int i = 0; i < TPW; ++i) {
             if (!tok[i]) continue;
@@ -218,21 +223,23 @@ __global__ __launch_bounds__(256, 1) void wgrad_tr(TrArgs a)
     while (b_cur < a.nbricks) {
         const int64_t b_next = b_cur + a.nsplit;
         if (b_next < a.nbricks) stage(b_next, buf ^ 1);
-        const char* xs = lds + buf * C::STAGE_BYTES;
-        const char* ds = xs + C::X_BYTES;
+        const uint32_t xs = lds0 + uint32_t(buf * C::STAGE_BYTES);
+        const uint32_t ds = xs + uint32_t(C::X_BYTES);
         // software pipeline: the operands of step ks + 1 are read while step ks multiplies
-        uint4 av0, av1, bv0[TPW], bv1[TPW];
-        load_step(xs, ds, 0, av0, bv0);
+        constexpr int NKS = C::BOV / 16;
+        lds_u32x4 av[2], bv[2][TPW];
+        load_step(xs, ds, 0, av[0], bv[0]);
 #pragma unroll
-        for (int ks = 0; ks < C::BOV / 16; ks += 2) {
-            if (ks + 1 < C::BOV / 16) load_step(xs, ds, ks + 1, av1, bv1);
-            __builtin_amdgcn_sched_barrier(0);
-            mfma_step(av0, bv0);
-            __builtin_amdgcn_sched_barrier(0);
-            if (ks + 2 < C::BOV / 16) load_step(xs, ds, ks + 2, av0, bv0);
-            __builtin_amdgcn_sched_barrier(0);
-            if (ks + 1 < C::BOV / 16) mfma_step(av1, bv1);
-            __builtin_amdgcn_sched_barrier(0);
+        for (int ks = 0; ks < NKS; ++ks) {
+            const int cb = ks & 1;
+            if (ks + 1 < NKS) {
+                load_step(xs, ds, ks + 1, av[cb ^ 1], bv[cb ^ 1]);
+                lds_wait<WAIT_NEXT>();
+            } else {
+                lds_wait<0>();
+            }
+            ready(av[cb], bv[cb]);
+            mfma_step(av[cb], bv[cb]);
         }
         wait_vm_barrier<0>();
         buf ^= 1;
