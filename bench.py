@@ -7,11 +7,19 @@ before the timed region. Geometry and slab shapes come from the library
 itself; the CPU oracle is used only by the cpu_baseline leg. Prints ONE JSON
 line on stdout (progress goes to stderr).
 
-    python bench.py [--steps K] [--warmup W] [--workload c3] [--no-cpu-baseline]
+    python bench.py [--steps K] [--warmup W] [--workload c3] [--no-cpu-baseline] [--copy-calibration]
+
+The roofline's "traffic" field is the HBM traffic of the dominant kernel measured
+with rocprofv3 counters (FETCH_SIZE and WRITE_SIZE, each scaled by what it reads
+for a plain device copy of known size) and recorded in
+profiles/<op>_<workload>_traffic.txt together with a hash of the kernel sources;
+it is reported only while the sources still hash the same, else null.
 """
 from __future__ import annotations
 
 import argparse
+import glob
+import hashlib
 import json
 import os
 import sys
@@ -76,6 +84,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="c3", choices=sorted(DESCR))
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="run one 64 MiB device-to-device copy first (reference for counter scaling)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU's shard; --gpus {args.gpus} is not supported: this build has no "
@@ -162,6 +172,13 @@ def main():
             if events is not None:
                 events[i][1].record(stream)
 
+    if args.copy_calibration:
+        src = torch.empty(64 << 20, dtype=torch.uint8, device="cuda")
+        src.fill_(1)
+        torch.cuda.synchronize()
+        torch.empty_like(src).copy_(src)
+        torch.cuda.synchronize()
+        del src
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
@@ -196,7 +213,7 @@ def main():
     dom = max(("conv_fwd", "conv_wgrad"), key=lambda k: per_op[k][2])
     ach = per_op[dom][1] / (per_op[dom][2] * 1e-3) / 1e12
     roofline = {"kernel": dom, "bound": "mfma", "achieved": round(ach, 2), "peak": PEAK[dt], "unit": "TFLOP/s",
-                "frac": round(ach / PEAK[dt], 4), "traffic": None,
+                "frac": round(ach / PEAK[dt], 4), "traffic": measured_traffic(dom, args.workload),
                 "work_per_launch": f"{flops:.4e} flop: 2*Cout*Cin*prod(K) per output voxel x {int(np.prod(O))} voxels"}
 
     cpu = None if args.no_cpu_baseline else cpu_baseline(w, g, tile_lo)
@@ -214,6 +231,38 @@ def main():
     print(json.dumps(line), flush=True)
 
 
+def source_hash():
+    """sha256 over the library sources (any change invalidates recorded counters)."""
+    h = hashlib.sha256()
+    files = sorted(glob.glob(os.path.join(ROOT, "paper_2605_11111_amd", "csrc", "*")) +
+                   glob.glob(os.path.join(ROOT, "include", "*.h")))
+    for f in files:
+        h.update(os.path.basename(f).encode())
+        with open(f, "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()
+
+
+def measured_traffic(op, workload):
+    """HBM bytes per launch of `op` from the committed counter summary, or None
+    when there is none or the kernel sources changed since it was taken."""
+    path = os.path.join(ROOT, "profiles", f"{op}_{workload}_traffic.txt")
+    if not os.path.exists(path):
+        return None
+    rec = {}
+    with open(path) as fh:
+        for line in fh:
+            if ":" in line and not line.startswith("#"):
+                k, v = line.split(":", 1)
+                rec[k.strip()] = v.strip()
+    if rec.get("source_sha256") != source_hash():
+        return None
+    try:
+        return int(float(rec["traffic_bytes_per_launch"]))
+    except (KeyError, ValueError):
+        return None
+
+
 def cpu_baseline(w, g, tile_lo):
     """The oracle (float64 NumPy) timed on a bounded sample of the same shard:
     forward and weight gradient over a few output planes along axis 0."""
@@ -225,32 +274,38 @@ def cpu_baseline(w, g, tile_lo):
         cores = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
     except Exception:
         cores = os.cpu_count()
-    planes = 2
     L = g["out_ext"][0]
-    p0 = L // 2
-    r0 = p0 * w.S[0] - g["pad_lo"][0]
-    r1 = (p0 + planes - 1) * w.S[0] - g["pad_lo"][0] + w.K[0]
     sharded = [p > 1 for p in w.parts]
     pad = [0 if sharded[a] else (w.K[a] - 1) // 2 for a in range(w.nd)]
-    lo_t = [tile_lo[0] + r0] + [0 - pad[a] if not sharded[a] else tile_lo[a] for a in range(1, w.nd)]
-    hi_t = [tile_lo[0] + r1] + [w.G[a] + pad[a] if not sharded[a] else
-                                tile_lo[a] + g["halo_lo"][a] + g["ext"][a] + g["halo_hi"][a] for a in range(1, w.nd)]
-    xw = np.moveaxis(as_f64(w.x_box(lo_t, hi_t)), -1, 1)
-    w64 = as_f64(w.weights_host())
-    lo = list(g["out_off"])
-    hi = [o + e for o, e in zip(g["out_off"], g["out_ext"])]
-    lo[0], hi[0] = lo[0] + p0, lo[0] + p0 + planes
     full_out = [(G + 2 * ((K - 1) // 2) - K) // S + 1 for G, K, S in zip(w.G, w.K, w.S)]
-    dy64 = np.moveaxis(as_f64(w.dy_field(full_out).box((0, 0, *lo), (w.N, w.cout, *hi), out=w.out)), -1, 1)
-    t0 = time.time()
-    oconv.conv_forward_window(xw, lo_t, w.G, w64, w.S, lo, hi)
-    oconv.conv_wgrad_window(xw, lo_t, w.G, dy64, w.K, w.S, lo, hi)
-    sec = time.time() - t0
-    vox = w.N * int(np.prod([h - l for l, h in zip(lo, hi)]))
-    fl = 2 * 2.0 * vox * w.cout * w.cin * int(np.prod(w.K))
+    w64 = as_f64(w.weights_host())
+    dyf = w.dy_field(full_out)
+    budget = 12.0          # seconds of oracle time
+    sec, planes = 0.0, 0
+    p0 = L // 2
+    while sec < budget and planes < L:
+        p = (p0 + planes) % L
+        r0 = p * w.S[0] - g["pad_lo"][0]
+        r1 = p * w.S[0] - g["pad_lo"][0] + w.K[0]
+        lo_t = [tile_lo[0] + r0] + [0 - pad[a] if not sharded[a] else tile_lo[a] for a in range(1, w.nd)]
+        hi_t = [tile_lo[0] + r1] + [w.G[a] + pad[a] if not sharded[a] else
+                                    tile_lo[a] + g["halo_lo"][a] + g["ext"][a] + g["halo_hi"][a]
+                                    for a in range(1, w.nd)]
+        xw = np.moveaxis(as_f64(w.x_box(lo_t, hi_t)), -1, 1)
+        lo = list(g["out_off"])
+        hi = [o + e for o, e in zip(g["out_off"], g["out_ext"])]
+        lo[0], hi[0] = lo[0] + p, lo[0] + p + 1
+        dy64 = np.moveaxis(as_f64(dyf.box((0, 0, *lo), (w.N, w.cout, *hi), out=w.out)), -1, 1)
+        t0 = time.time()
+        oconv.conv_forward_window(xw, lo_t, w.G, w64, w.S, lo, hi)
+        oconv.conv_wgrad_window(xw, lo_t, w.G, dy64, w.K, w.S, lo, hi)
+        sec += time.time() - t0
+        planes += 1
+    plane_vox = w.N * int(np.prod(g["out_ext"][1:]))
+    fl = 2 * 2.0 * planes * plane_vox * w.cout * w.cin * int(np.prod(w.K))
     return {"value": round(fl / sec / 1e12, 6), "unit": "TFLOP/s", "cores": int(cores), "kind": "oracle",
-            "sample": f"fwd+wgrad over {planes} of {L} output planes along axis 0 of the same shard "
-                      f"({sec:.1f}s, float64 NumPy)"}
+            "sample": f"fwd+wgrad over {planes} of {L} output planes along axis 0 of the same shard, "
+                      f"one plane per call ({sec:.1f}s of oracle time, float64 NumPy; input generation excluded)"}
 
 
 if __name__ == "__main__":
