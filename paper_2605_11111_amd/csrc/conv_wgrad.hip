@@ -603,12 +603,16 @@ hipError_t launch_bf16(const PlanW& pl, hipStream_t s)
 size_t conv_wgrad_workspace(const Tile3& t, const Conv3& cv, shard_dtype_t dt)
 {
     return std::max({generic_wgrad_workspace(t, cv), tiled_workspace(plan_wgrad(t, cv, dt)),
-                     wgrad_tr_workspace(t, cv, dt)});
+                     wgrad_tr_workspace(t, cv, dt), wgrad_xm_workspace(t, cv, dt)});
 }
 
 hipError_t launch_conv_wgrad(const Tile3& t, const Conv3& cv, shard_dtype_t dt, const void* tile, const void* dy,
                              float* dw, void* ws, hipStream_t s)
 {
+    {
+        hipError_t e = launch_wgrad_xm(t, cv, dt, tile, dy, dw, ws, s);
+        if (e != hipErrorNotSupported) return e;
+    }
     {
         int32_t red[6];
         hipError_t e = launch_wgrad_tr(t, cv, dt, tile, dy, static_cast<float*>(ws), red, s);

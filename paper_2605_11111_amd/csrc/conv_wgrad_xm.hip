@@ -1,0 +1,523 @@
+// Weight gradient, bf16, unit stride, 3 x 3 taps in H and W (KD = 1 or 3):
+// dW[co][ci][kd][kh][kw] = sum over output voxels v of dy[v][co] * tile[v + t - pad][ci],
+// a split-K implicit GEMM with M = 32 output channels, N = 32 input channels and
+// K = output voxels along W, on v_mfma_f32_32x32x16_bf16.
+//
+//  * Wave roles: each role is one (Co tile, Ci tile, kd) and owns the nine
+//    (kh, kw) taps of that plane offset as nine 32 x 32 fp32 accumulators kept in
+//    registers over all the workgroup's bricks. With fewer than four roles the
+//    spare wave repeats role 0 without storing it. All four waves issue the
+//    staging loads, in the shadow of their first MFMAs of the previous tile.
+//  * A workgroup owns bricks of BZ x BY output rows and marches along W in
+//    32-voxel tiles. Each tile's inputs (dy rows and the BZ+KD-1 x BY+2 input rows:
+//    32 voxels in a main area, the next 4 in a halo area) are staged unchanged
+//    (channels-last) by direct global->LDS buffer loads, double buffered;
+//    out-of-range offsets load zeros.
+//  * Operands need 8 consecutive voxels per lane; they are read with
+//    ds_read_b64_tr_b16 (transpose on read). K step s of lane half g covers
+//    voxels 16g + 8s .. + 7, so a lane holds the contiguous run 16g .. 16g + 19
+//    of its channel after five reads, and the W taps are register selections:
+//    kw = 0 and 2 are dword-aligned windows, kw = 1 is one v_alignbit per dword.
+//    One row's five reads serve all three kw of both K steps.
+//  * Walking the brick's output rows along H, input row y + kh serves output
+//    rows y, y - 1, y - 2: each input row is read once per plane (a ring of four
+//    register slots per plane parity), so a wave issues about nine 512-byte
+//    transposed reads per eighteen MFMAs.
+//  * The partial of every workgroup is written once; wgrad_xm_reduce sums the
+//    partials in a fixed order (results are bitwise repeatable).
+#include <algorithm>
+
+#include "common.h"
+#include "internal.h"
+
+namespace shardconv {
+
+typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8_w;
+typedef __attribute__((ext_vector_type(16))) float f32x16_w;
+
+#define SC_LDSW(p) ((__attribute__((address_space(3))) void*)(p))
+
+namespace {
+
+struct WxArgs {
+    const char* tile;
+    const char* dy;
+    float* part;
+    int32_t P[3], O[3];
+    int32_t pad[3];
+    int32_t NBZ, NBY, NXT;  // bricks along D and H, 32-voxel tiles along W
+    int32_t nseg, T;        // W segments per brick row and their length in tiles
+    uint32_t nbricks;       // n * NBZ * NBY * nseg
+    uint32_t tile_bytes, dy_bytes;  // per batch item (< 2^32)
+    uint32_t xrow, xplane, yrow, yplane;  // byte strides of tile and dy rows and planes
+};
+
+// 16-byte unit swizzle of staged voxel v for UPV units per voxel: with 128-byte
+// voxels the four rows of a transposed read would fall on two bank windows, so
+// rows with bit 1 set move by 32 bytes.
+template <int UPV>
+__device__ __forceinline__ constexpr int wx_swz(int v)
+{
+    return UPV == 8 ? (((v >> 1) & 1) << 1) : 0;
+}
+
+template <int KD, int NCI, int NCO, int BZ, int BY>
+struct WxCfg {
+    static constexpr int CIN = 32 * NCI, COUT = 32 * NCO;
+    static constexpr int UPX = CIN / 8, UPY = COUT / 8;   // 16-byte units per voxel
+    static constexpr int NR = NCO * NCI * KD;             // wave roles
+    static_assert(NR >= 1 && NR <= 4, "at most four roles per workgroup");
+    static constexpr int XRZ = BZ + KD - 1, XRY = BY + 2, XR = XRZ * XRY;
+    // input row r: voxels 0..31 in the main area, voxels 32..35 in the halo area
+    static constexpr int XROW = 32 * UPX * 16;
+    static constexpr int IPR_X = 32 * UPX / 64;            // direct-load instructions per main row
+    static constexpr int XH_ROW = 4 * UPX * 16;
+    static constexpr int XH_SLOTS = XR * 4 * UPX;
+    static_assert(XH_SLOTS % 64 == 0, "whole halo instructions");
+    static constexpr int XH_INSTR = XH_SLOTS / 64;
+    static constexpr int X_BYTES = XR * XROW;
+    static constexpr int XH_BYTES = XH_SLOTS * 16;
+    static constexpr int YROW = 32 * UPY * 16;
+    static constexpr int IPR_Y = 32 * UPY / 64;
+    static constexpr int Y_BYTES = BZ * BY * YROW;
+    static constexpr int X_INSTR = XR * IPR_X, Y_INSTR = BZ * BY * IPR_Y;
+    static constexpr int N_INSTR = X_INSTR + XH_INSTR + Y_INSTR;
+    static constexpr int STAGE_BYTES = X_BYTES + XH_BYTES + Y_BYTES;
+    static constexpr int LDS_BYTES = 2 * STAGE_BYTES;
+    static constexpr int NQ = BZ * BY;                     // output rows per tile
+    static constexpr int PART_FLOATS = 4 * 9 * 1024;       // per workgroup: [wave][tap][lane][16]
+};
+
+template <int KD, int NCI, int NCO, int BZ, int BY>
+__global__ __launch_bounds__(256, 1) void wgrad_xm(WxArgs a)
+{
+    using C = WxCfg<KD, NCI, NCO, BZ, BY>;
+    extern __shared__ uint4 lds4[];
+    char* lds = reinterpret_cast<char*>(lds4);
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const uint32_t G = gridDim.x;
+    const uint32_t L = uint32_t(xcd_remap(blockIdx.x, G));
+    // every wave runs the compute path (a branch around it would make the compiler
+    // shuttle the accumulators between register files on every tile); a spare
+    // wave repeats role 0 and drops its result
+    const bool computes = wave < C::NR;
+    const int role = computes ? wave : 0;
+    const int kd = role % KD, cb = (role / KD) % NCI, mb = role / (KD * NCI);
+    const uint32_t lds0 = lds_addr(lds);
+
+    // ---- staging (loader waves) ----
+    struct Pos {
+        uint32_t brick;
+        int32_t j, jend;
+    };
+    auto seg_start = [&](Pos& p) {
+        if (p.brick >= a.nbricks) return;
+        const int32_t seg = int32_t(p.brick % uint32_t(a.nseg));
+        p.j = seg * a.T;
+        p.jend = min(p.j + a.T, a.NXT);
+    };
+    auto advance = [&](Pos& p) {
+        if (++p.j >= p.jend) {
+            p.brick += G;
+            seg_start(p);
+        }
+    };
+    // Staging: wave w loads the input rows r = w, w + 4, ... (IPR_X instructions
+    // each), the halo instructions h = w, w + 4, ... and the dy rows w, w + 4, ...
+    // Main and dy rows: lane l carries unit l % UPV of voxel piece * (64 / UPV) +
+    // l / UPV; halo area: 4 * UPX lanes per row, unit l % UPX of voxel 32 + (l / UPX) % 4.
+    // Byte offsets are 32-bit (a batch item is < 4 GiB; only in-range offsets are
+    // used, so wrap-around in the intermediate sums is harmless).
+    const int vx = lane / C::UPX, ux = lane % C::UPX;
+    const int vy = lane / C::UPY, uy = lane % C::UPY;
+    const int hrow = lane / (4 * C::UPX), hv = 32 + (lane / C::UPX) % 4;
+    static_assert((64 / C::UPX) % 4 == 0 && (64 / C::UPY) % 4 == 0, "swizzle bit is lane-constant");
+    const uint32_t lxm = uint32_t(vx * C::CIN * 2 + (ux ^ wx_swz<C::UPX>(vx)) * 16);
+    const uint32_t lym = uint32_t(vy * C::COUT * 2 + (uy ^ wx_swz<C::UPY>(vy)) * 16);
+    const uint32_t lxh = uint32_t(hv * C::CIN * 2 + (ux ^ wx_swz<C::UPX>(hv)) * 16);
+    constexpr int XPI = 64 / C::UPX, YPI = 64 / C::UPY;  // voxels per instruction
+    constexpr int HRPI = 64 / (4 * C::UPX);              // halo rows per instruction
+    auto stage = [&](const Pos& p, int buf) {
+        char* xdst = lds + buf * C::STAGE_BYTES;
+        char* hdst = xdst + C::X_BYTES;
+        char* ydst = hdst + C::XH_BYTES;
+        const bool live = p.brick < a.nbricks;
+        uint32_t t = live ? p.brick / uint32_t(a.nseg) : 0;
+        const int by = int(t % uint32_t(a.NBY));
+        t /= uint32_t(a.NBY);
+        const int bz = int(t % uint32_t(a.NBZ));
+        const uint32_t nn = live ? t / uint32_t(a.NBZ) : 0;
+        const int o0 = bz * BZ, o1 = by * BY, o2 = p.j * 32;
+        const int i0 = o0 - a.pad[0], i1 = o1 - a.pad[1], i2 = o2 - a.pad[2];
+        const uint32_t xorg = uint32_t(i0) * a.xplane + uint32_t(i1) * a.xrow + uint32_t(i2) * (C::CIN * 2);
+        const uint32_t yorg = uint32_t(o0) * a.yplane + uint32_t(o1) * a.yrow + uint32_t(o2) * (C::COUT * 2);
+        __amdgpu_buffer_rsrc_t rx = __builtin_amdgcn_make_buffer_rsrc(
+            const_cast<char*>(a.tile) + int64_t(nn) * a.tile_bytes, short(0), int(a.tile_bytes), 0x00020000);
+        __amdgpu_buffer_rsrc_t ry = __builtin_amdgcn_make_buffer_rsrc(
+            const_cast<char*>(a.dy) + int64_t(nn) * a.dy_bytes, short(0), int(a.dy_bytes), 0x00020000);
+        const bool inner = live && i0 >= 0 && i0 + C::XRZ <= a.P[0] && i1 >= 0 && i1 + C::XRY <= a.P[1] &&
+                           i2 >= 0 && i2 + 36 <= a.P[2] && o0 + BZ <= a.O[0] && o1 + BY <= a.O[1] &&
+                           o2 + 32 <= a.O[2];
+        if (inner) {
+#pragma unroll
+            for (int k = 0; k < (C::XR + 3) / 4; ++k) {
+                const int row = 4 * k + wave;
+                if (row < C::XR) {
+                    const uint32_t u = xorg + uint32_t(row / C::XRY) * a.xplane + uint32_t(row % C::XRY) * a.xrow + lxm;
+#pragma unroll
+                    for (int pc = 0; pc < C::IPR_X; ++pc)
+                        __builtin_amdgcn_raw_ptr_buffer_load_lds(rx, SC_LDSW(xdst + (row * C::IPR_X + pc) * 1024), 16,
+                                                                 u + uint32_t(pc * XPI * C::CIN * 2), 0, 0, 0);
+                }
+            }
+#pragma unroll
+            for (int k = 0; k < (C::XH_INSTR + 3) / 4; ++k) {
+                const int hi = 4 * k + wave;
+                if (hi < C::XH_INSTR) {
+                    const int row = hi * HRPI + hrow;
+                    const uint32_t u = xorg + uint32_t(row / C::XRY) * a.xplane + uint32_t(row % C::XRY) * a.xrow + lxh;
+                    __builtin_amdgcn_raw_ptr_buffer_load_lds(rx, SC_LDSW(hdst + hi * 1024), 16, u, 0, 0, 0);
+                }
+            }
+#pragma unroll
+            for (int k = 0; k < (C::NQ + 3) / 4; ++k) {
+                const int row = 4 * k + wave;
+                if (row < C::NQ) {
+                    const uint32_t u = yorg + uint32_t(row / BY) * a.yplane + uint32_t(row % BY) * a.yrow + lym;
+#pragma unroll
+                    for (int pc = 0; pc < C::IPR_Y; ++pc)
+                        __builtin_amdgcn_raw_ptr_buffer_load_lds(ry, SC_LDSW(ydst + (row * C::IPR_Y + pc) * 1024), 16,
+                                                                 u + uint32_t(pc * YPI * C::COUT * 2), 0, 0, 0);
+                }
+            }
+            return;
+        }
+        // edge tiles: per-lane range checks, out-of-range voxels load zeros
+        for (int row = wave; row < C::XR; row += 4) {
+            const int zr = row / C::XRY, yr = row % C::XRY;
+            const bool rok = live && i0 + zr >= 0 && i0 + zr < a.P[0] && i1 + yr >= 0 && i1 + yr < a.P[1];
+            const uint32_t u = xorg + uint32_t(zr) * a.xplane + uint32_t(yr) * a.xrow + lxm;
+            for (int pc = 0; pc < C::IPR_X; ++pc) {
+                const int t2 = i2 + pc * XPI + vx;
+                const bool ok = rok && t2 >= 0 && t2 < a.P[2];
+                __builtin_amdgcn_raw_ptr_buffer_load_lds(rx, SC_LDSW(xdst + (row * C::IPR_X + pc) * 1024), 16,
+                                                         ok ? u + uint32_t(pc * XPI * C::CIN * 2) : a.tile_bytes, 0,
+                                                         0, 0);
+            }
+        }
+        for (int hi = wave; hi < C::XH_INSTR; hi += 4) {
+            const int row = hi * HRPI + hrow;
+            const int zr = row / C::XRY, yr = row % C::XRY;
+            const bool ok = live && i0 + zr >= 0 && i0 + zr < a.P[0] && i1 + yr >= 0 && i1 + yr < a.P[1] &&
+                            i2 + hv >= 0 && i2 + hv < a.P[2];
+            const uint32_t u = xorg + uint32_t(zr) * a.xplane + uint32_t(yr) * a.xrow + lxh;
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(rx, SC_LDSW(hdst + hi * 1024), 16, ok ? u : a.tile_bytes, 0, 0,
+                                                     0);
+        }
+        for (int row = wave; row < C::NQ; row += 4) {
+            const int zb = row / BY, yb = row % BY;
+            const bool rok = live && o0 + zb < a.O[0] && o1 + yb < a.O[1];
+            const uint32_t u = yorg + uint32_t(zb) * a.yplane + uint32_t(yb) * a.yrow + lym;
+            for (int pc = 0; pc < C::IPR_Y; ++pc) {
+                const bool ok = rok && o2 + pc * YPI + vy < a.O[2];
+                __builtin_amdgcn_raw_ptr_buffer_load_lds(ry, SC_LDSW(ydst + (row * C::IPR_Y + pc) * 1024), 16,
+                                                         ok ? u + uint32_t(pc * YPI * C::COUT * 2) : a.dy_bytes, 0,
+                                                         0, 0);
+            }
+        }
+    };
+
+    // ---- operand reads (compute waves) ----
+    // transposed-read lane terms: 16-lane group G = lane / 16 reads voxels
+    // 16g + 4r + i/4 (g = lane / 32, read r) at channels c0 + 4 (i % 4) .. + 3,
+    // c0 = 32 * tile + 16 * (G % 2)
+    const int gi = lane & 15, gh = lane >> 5, gc = (lane >> 4) & 1;
+    const int vq = 16 * gh + gi / 4;  // voxel of read 0
+    auto lane_off = [&](int upv, int c) {
+        const int swz = upv == 8 ? (((vq >> 1) & 1) << 1) : 0;
+        return uint32_t(vq * upv * 16 + (((c >> 3) ^ swz) << 4) + (c & 7) * 2);
+    };
+    const uint32_t xl = lane_off(C::UPX, 32 * cb + 16 * gc + 4 * (gi & 3));
+    const uint32_t yl = lane_off(C::UPY, 32 * mb + 16 * gc + 4 * (gi & 3));
+
+    f32x16_w acc[3][3];
+#pragma unroll
+    for (int kh = 0; kh < 3; ++kh)
+#pragma unroll
+        for (int kw = 0; kw < 3; ++kw)
+#pragma unroll
+            for (int e = 0; e < 16; ++e) acc[kh][kw][e] = 0.f;
+
+    // register slots: input rows of plane parity p, row yr in slot p * 4 + yr % 4
+    uint32_t xr[8][10];
+    uint32_t xs[8][8];     // kw = 1 windows (both K steps) of the slot's row
+    uint32_t dyr[2][8];    // dy of output rows q (parity q % 2), both K steps
+
+    // read 4 (voxels 16g + 16 .. + 19): lane half 0 from the main row, lane half 1
+    // (voxels 32..35) from the halo area
+    const int vq4 = gh ? gi / 4 : 16 + gi / 4;
+    const uint32_t xl4 = uint32_t(gh ? C::X_BYTES : 0) +
+                         uint32_t(vq4 * C::UPX * 16 +
+                                  ((((32 * cb + 16 * gc + 4 * (gi & 3)) >> 3) ^ wx_swz<C::UPX>(vq4)) << 4) +
+                                  ((4 * (gi & 3)) & 7) * 2);
+    const uint32_t xrs4 = uint32_t(gh ? C::XH_ROW : C::XROW);
+    auto read_x_row = [&](uint32_t xbase, int zr, int yr, int slot) {
+        const int row = zr * C::XRY + yr;
+        const uint32_t base = xbase + uint32_t(row * C::XROW) + xl;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            const uint2 d = lds_read_tr16_b64(base + uint32_t(r * 4 * C::UPX * 16));
+            xr[slot][2 * r] = d.x;
+            xr[slot][2 * r + 1] = d.y;
+        }
+        const uint2 d = lds_read_tr16_b64(xbase + xl4 + uint32_t(row) * xrs4);
+        xr[slot][8] = d.x;
+        xr[slot][9] = d.y;
+    };
+    auto read_dy_row = [&](uint32_t ybase, int q, int slot) {
+        const uint32_t base = ybase + uint32_t(q * C::YROW) + yl;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            const uint2 d = lds_read_tr16_b64(base + uint32_t(r * 4 * C::UPY * 16));
+            dyr[slot][2 * r] = d.x;
+            dyr[slot][2 * r + 1] = d.y;
+        }
+    };
+    // reads for output row q: its dy row and the input rows it needs first
+    auto issue_row = [&](uint32_t xbase, uint32_t ybase, int q) {
+        const int zb = q / BY, yb = q % BY;
+        read_dy_row(ybase, q, q & 1);
+        if (yb == 0) {
+#pragma unroll
+            for (int kh = 0; kh < 3; ++kh) read_x_row(xbase, zb + kd, kh, (zb & 1) * 4 + kh);
+        } else {
+            read_x_row(xbase, zb + kd, yb + 2, (zb & 1) * 4 + (yb + 2) % 4);
+        }
+    };
+    auto ready_row = [&](int q) {
+        const int zb = q / BY, yb = q % BY;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) lds_ready(dyr[q & 1][e]);
+        const int k0 = yb == 0 ? 0 : 2;
+#pragma unroll
+        for (int kh = k0; kh < 3; ++kh) {
+            const int slot = (zb & 1) * 4 + (yb + kh) % 4;
+#pragma unroll
+            for (int e = 0; e < 10; ++e) lds_ready(xr[slot][e]);
+            // kw = 1: voxels shifted by one (the high half of dword i, the low of i + 1)
+#pragma unroll
+            for (int s = 0; s < 2; ++s)
+#pragma unroll
+                for (int e = 0; e < 4; ++e)
+                    xs[slot][4 * s + e] = __builtin_amdgcn_alignbit(xr[slot][4 * s + e + 1], xr[slot][4 * s + e], 16);
+        }
+    };
+    auto mfma_row = [&](int q) {
+        const int zb = q / BY, yb = q % BY;
+#pragma unroll
+        for (int s = 0; s < 2; ++s) {
+            const uint4 av = make_uint4(dyr[q & 1][4 * s], dyr[q & 1][4 * s + 1], dyr[q & 1][4 * s + 2],
+                                        dyr[q & 1][4 * s + 3]);
+#pragma unroll
+            for (int kh = 0; kh < 3; ++kh) {
+                const int slot = (zb & 1) * 4 + (yb + kh) % 4;
+                const uint32_t* x = xr[slot];
+                const uint4 b0 = make_uint4(x[4 * s], x[4 * s + 1], x[4 * s + 2], x[4 * s + 3]);
+                const uint4 b1 = make_uint4(xs[slot][4 * s], xs[slot][4 * s + 1], xs[slot][4 * s + 2],
+                                            xs[slot][4 * s + 3]);
+                const uint4 b2 = make_uint4(x[4 * s + 1], x[4 * s + 2], x[4 * s + 3], x[4 * s + 4]);
+                acc[kh][0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8_w, av),
+                                                                     __builtin_bit_cast(bf16x8_w, b0), acc[kh][0], 0,
+                                                                     0, 0);
+                acc[kh][1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8_w, av),
+                                                                     __builtin_bit_cast(bf16x8_w, b1), acc[kh][1], 0,
+                                                                     0, 0);
+                acc[kh][2] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8_w, av),
+                                                                     __builtin_bit_cast(bf16x8_w, b2), acc[kh][2], 0,
+                                                                     0, 0);
+            }
+        }
+    };
+
+    Pos cp{L, 0, 0}, sp{L, 0, 0};
+    seg_start(cp);
+    seg_start(sp);
+    stage(sp, 0);
+    advance(sp);
+    int buf = 0;
+    while (cp.brick < a.nbricks) {
+        // this tile's loads have landed; every wave is done with the other buffer
+        wait_vm_barrier<0>();
+        const uint32_t xbase = lds0 + uint32_t(buf * C::STAGE_BYTES);
+        const uint32_t ybase = xbase + uint32_t(C::X_BYTES + C::XH_BYTES);
+        issue_row(xbase, ybase, 0);
+#pragma unroll
+        for (int q = 0; q < C::NQ; ++q) {
+            const bool plane_break = (q + 1) % BY == 0;  // next row starts a new plane
+            if (q + 1 < C::NQ && !plane_break) {
+                issue_row(xbase, ybase, q + 1);
+                lds_wait<9>();
+            } else {
+                lds_wait<0>();
+            }
+            ready_row(q);
+            mfma_row(q);
+            // the next tile's loads go out in the shadow of the first row's MFMAs
+            if (q == 0) {
+                stage(sp, buf ^ 1);
+                advance(sp);
+            }
+            if (q + 1 < C::NQ && plane_break) issue_row(xbase, ybase, q + 1);
+        }
+        buf ^= 1;
+        advance(cp);
+    }
+    wait_vm_barrier<0>();
+    if (computes) {
+        // partial: [workgroup][wave][tap kh * 3 + kw][lane][16]
+        float4* out = reinterpret_cast<float4*>(a.part + int64_t(L) * C::PART_FLOATS + int64_t(wave) * 9 * 1024);
+#pragma unroll
+        for (int kh = 0; kh < 3; ++kh)
+#pragma unroll
+            for (int kw = 0; kw < 3; ++kw)
+#pragma unroll
+                for (int r4 = 0; r4 < 4; ++r4)
+                    out[((kh * 3 + kw) * 64 + lane) * 4 + r4] =
+                        make_float4(acc[kh][kw][4 * r4], acc[kh][kw][4 * r4 + 1], acc[kh][kw][4 * r4 + 2],
+                                    acc[kh][kw][4 * r4 + 3]);
+    }
+}
+
+// dw[co][ci][tap] = sum over workgroups (in order) of the partials. One thread per
+// partial float of one workgroup block.
+template <int KD, int NCI, int NCO>
+__global__ __launch_bounds__(256) void wgrad_xm_reduce(const float* part, float* dw, int nsplit)
+{
+    constexpr int NR = NCO * NCI * KD;
+    constexpr int CIN = 32 * NCI;
+    constexpr int TAPS = KD * 9;
+    constexpr int BLK = 4 * 9 * 1024;
+    const int e = int(blockIdx.x) * 256 + threadIdx.x;
+    if (e >= NR * 9 * 1024) return;
+    const int r = e % 16, lane = (e / 16) % 64, t9 = (e / 1024) % 9, wave = e / (9 * 1024);
+    const int kd = wave % KD, cb = (wave / KD) % NCI, mb = wave / (KD * NCI);
+    const int co = mb * 32 + 8 * (r / 4) + 4 * (lane / 32) + (r % 4);
+    const int ci = cb * 32 + (lane % 32);
+    const int tap = kd * 9 + t9;
+    float s8[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+    int sp = 0;
+    for (; sp + 8 <= nsplit; sp += 8) {
+#pragma unroll
+        for (int j = 0; j < 8; ++j) s8[j] += part[int64_t(sp + j) * BLK + e];
+    }
+    for (int j = 0; sp + j < nsplit; ++j) s8[j] += part[int64_t(sp + j) * BLK + e];
+    dw[(co * CIN + ci) * TAPS + tap] = ((s8[0] + s8[1]) + (s8[2] + s8[3])) + ((s8[4] + s8[5]) + (s8[6] + s8[7]));
+}
+
+struct WxPlan {
+    bool ok;
+    int cfg;  // 0: KD 3, 32 -> 32 channels, brick 2 x 4; 1: KD 1, 64 -> 64, brick 1 x 8
+    WxArgs a;
+    size_t lds;
+    int64_t grid;
+};
+
+WxPlan plan_wx(const Tile3& t, const Conv3& cv, shard_dtype_t dt)
+{
+    WxPlan p{};
+    p.ok = false;
+    if (force_generic() || force_tiled() || dt != SHARD_BF16) return p;
+    for (int k = 0; k < 3; ++k)
+        if (cv.S[k] != 1 || std::abs(cv.pad[k]) > (1 << 20) || cv.O[k] >= (int64_t(1) << 24) ||
+            t.P[k] >= (int64_t(1) << 24))
+            return p;
+    if (cv.K[1] != 3 || cv.K[2] != 3) return p;
+    int bz, by;
+    if (cv.K[0] == 3 && t.c == 32 && cv.cout == 32) {
+        p.cfg = 0;
+        bz = 2, by = 4;
+        p.lds = WxCfg<3, 1, 1, 2, 4>::LDS_BYTES;
+    } else if (cv.K[0] == 1 && t.c == 64 && cv.cout == 64) {
+        p.cfg = 1;
+        bz = 1, by = 8;
+        p.lds = WxCfg<1, 2, 2, 1, 8>::LDS_BYTES;
+    } else {
+        return p;
+    }
+    const int64_t tb = t.P[0] * t.P[1] * t.P[2] * t.c * 2;
+    const int64_t db = cv.O[0] * cv.O[1] * cv.O[2] * cv.cout * 2;
+    if (tb >= (int64_t(1) << 32) - 64 || db >= (int64_t(1) << 32) - 64) return p;
+    WxArgs& a = p.a;
+    for (int k = 0; k < 3; ++k) {
+        a.P[k] = int32_t(t.P[k]);
+        a.O[k] = int32_t(cv.O[k]);
+        a.pad[k] = int32_t(cv.pad[k]);
+    }
+    a.NBZ = int32_t(ceil_div(cv.O[0], bz));
+    a.NBY = int32_t(ceil_div(cv.O[1], by));
+    a.NXT = int32_t(ceil_div(cv.O[2], 32));
+    const int64_t rows = t.n * int64_t(a.NBZ) * a.NBY;
+    if (rows == 0 || a.NXT == 0) return p;
+    int64_t nseg = 1;
+    while (rows * nseg < 256 && a.NXT / (nseg * 2) >= 4) nseg *= 2;
+    a.nseg = int32_t(nseg);
+    a.T = int32_t(ceil_div(a.NXT, nseg));
+    const int64_t nb = rows * nseg;
+    if (nb >= (int64_t(1) << 31)) return p;
+    a.nbricks = uint32_t(nb);
+    a.tile_bytes = uint32_t(tb);
+    a.dy_bytes = uint32_t(db);
+    a.xrow = uint32_t(t.P[2] * t.c * 2);
+    a.xplane = uint32_t(t.P[1] * t.P[2] * t.c * 2);
+    a.yrow = uint32_t(cv.O[2] * cv.cout * 2);
+    a.yplane = uint32_t(cv.O[1] * cv.O[2] * cv.cout * 2);
+    p.grid = std::max<int64_t>(1, std::min<int64_t>(nb, 256));
+    p.ok = true;
+    return p;
+}
+
+template <int KD, int NCI, int NCO, int BZ, int BY>
+hipError_t run_wx(const WxPlan& p, float* dw, hipStream_t s)
+{
+    using C = WxCfg<KD, NCI, NCO, BZ, BY>;
+    auto fn = &wgrad_xm<KD, NCI, NCO, BZ, BY>;
+    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(fn), hipFuncAttributeMaxDynamicSharedMemorySize,
+                                       int(C::LDS_BYTES));
+    if (e != hipSuccess) return e;
+    WxArgs a = p.a;
+    void* args[] = {&a};
+    e = hipLaunchKernel(reinterpret_cast<const void*>(fn), dim3(unsigned(p.grid)), dim3(256), args, C::LDS_BYTES, s);
+    if (e != hipSuccess) return e;
+    const int total = C::NR * 9 * 1024;
+    hipLaunchKernelGGL((wgrad_xm_reduce<KD, NCI, NCO>), dim3(unsigned(ceil_div(total, 256))), dim3(256), 0, s,
+                       p.a.part, dw, int(p.grid));
+    return hipGetLastError();
+}
+
+}  // namespace
+
+size_t wgrad_xm_workspace(const Tile3& t, const Conv3& cv, shard_dtype_t dt)
+{
+    const WxPlan p = plan_wx(t, cv, dt);
+    return p.ok ? size_t(p.grid) * 4 * 9 * 1024 * sizeof(float) : 0;
+}
+
+// The W-march weight gradient applies to bf16, unit stride, 3 x 3 taps in H and
+// W with 3 (Ci = Co = 32) or 1 (Ci = Co = 64) taps in D, tiles and dy of < 4 GiB
+// per batch item, 16-byte aligned buffers. Launches the partial and the reduce
+// kernels; returns hipErrorNotSupported when it does not apply.
+hipError_t launch_wgrad_xm(const Tile3& t, const Conv3& cv, shard_dtype_t dt, const void* tile, const void* dy,
+                           float* dw, void* ws, hipStream_t s)
+{
+    WxPlan p = plan_wx(t, cv, dt);
+    if (!p.ok || reinterpret_cast<uintptr_t>(tile) % 16 != 0 || reinterpret_cast<uintptr_t>(dy) % 16 != 0 ||
+        reinterpret_cast<uintptr_t>(ws) % 16 != 0)
+        return hipErrorNotSupported;
+    p.a.tile = static_cast<const char*>(tile);
+    p.a.dy = static_cast<const char*>(dy);
+    p.a.part = static_cast<float*>(ws);
+    return p.cfg == 0 ? run_wx<3, 1, 1, 2, 4>(p, dw, s) : run_wx<1, 2, 2, 1, 8>(p, dw, s);
+}
+
+}  // namespace shardconv

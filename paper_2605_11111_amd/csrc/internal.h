@@ -55,6 +55,9 @@ hipError_t launch_conv_wgrad(const Tile3& t, const Conv3& cv, shard_dtype_t dt, 
 // outside what it handles (the caller then takes the general kernel).
 hipError_t launch_conv_fwd_rows(const Tile3& t, const Conv3& cv, shard_dtype_t dt, const void* tile,
                                 const void* wfrag, int nkc_frag, int nt_frag, void* y, hipStream_t s);
+size_t wgrad_xm_workspace(const Tile3& t, const Conv3& cv, shard_dtype_t dt);
+hipError_t launch_wgrad_xm(const Tile3& t, const Conv3& cv, shard_dtype_t dt, const void* tile, const void* dy,
+                           float* dw, void* ws, hipStream_t s);
 size_t wgrad_tr_workspace(const Tile3& t, const Conv3& cv, shard_dtype_t dt);
 hipError_t launch_wgrad_tr(const Tile3& t, const Conv3& cv, shard_dtype_t dt, const void* tile, const void* dy,
                            float* part, int32_t red[6], hipStream_t s);
