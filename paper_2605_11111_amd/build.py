@@ -28,9 +28,18 @@ FLAGS = [
 ]
 
 
+# Per-source code generation options. The forward W-march kernel keeps its
+# weight fragments in AGPRs for the kernel's lifetime; with the MFMA results in
+# VGPRs (VGPR form) the register allocator no longer shuffles those fragments
+# between AGPRs on every tile, and the epilogue reads the accumulators directly.
+SRC_FLAGS = {
+    "conv_fwd_rows.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"],
+}
+
+
 def _compile(src: str) -> str:
     obj = os.path.join(OBJ, os.path.basename(src) + ".o")
-    cmd = [HIPCC, *FLAGS, "-x", "hip", "-c", src, "-o", obj]
+    cmd = [HIPCC, *FLAGS, *SRC_FLAGS.get(os.path.basename(src), []), "-x", "hip", "-c", src, "-o", obj]
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         sys.stderr.write(r.stdout + r.stderr)

@@ -87,7 +87,7 @@ struct XmCfg {
     static constexpr int EPI_STORES = R * 2;
     static constexpr int LDS_BYTES = NBUF * STAGE_BYTES + 4 * EPI_BYTES;
     static constexpr int VM_BASE = NIT * (NBUF - 2);
-    static_assert(VM_BASE + EPI_STORES * 3 < 64, "vmcnt range");
+    static_assert(NBUF <= 4 && VM_BASE + EPI_STORES * 2 < 64, "vmcnt range");
 };
 
 template <int CIN, int KD, int KH, int WZ, int WY, int WC, int R, int NBUF>
@@ -104,9 +104,9 @@ __global__ __launch_bounds__(256, 1) void conv_fwd_xm(XmArgs a)
     const uint32_t L = uint32_t(xcd_remap(blockIdx.x, G));
 
     // weights of this wave's output-channel tile -> registers
-    uint4 wv[KD][KH][KW][C::NKC];
+    u32x4_r wv[KD][KH][KW][C::NKC];
     {
-        const uint4* wf = reinterpret_cast<const uint4*>(a.wfrag);
+        const u32x4_r* wf = reinterpret_cast<const u32x4_r*>(a.wfrag);
 #pragma unroll
         for (int kd = 0; kd < KD; ++kd)
 #pragma unroll
@@ -139,16 +139,24 @@ __global__ __launch_bounds__(256, 1) void conv_fwd_xm(XmArgs a)
     // bricks L, L + G, ... ; brick b is W segment b % nseg of output rows b / nseg.
     // A segment after the first starts one tile early (its outputs are not stored)
     // to build the carry.
+    // The brick's rows (bz, by) and batch item nn are decoded once per brick.
     struct Pos {
         uint32_t brick;
         int32_t j, jend, jstore;
+        int32_t bz, by;
+        uint32_t nn;
     };
     auto seg_start = [&](Pos& p) {
         if (p.brick >= a.nbricks) return;
-        const int32_t seg = int32_t(p.brick % uint32_t(a.nseg));
+        uint32_t t = p.brick / uint32_t(a.nseg);
+        const int32_t seg = int32_t(p.brick - t * uint32_t(a.nseg));
         p.jstore = seg * a.T;
         p.j = seg > 0 ? p.jstore - 1 : 0;
         p.jend = min(p.jstore + a.T, a.NXT);
+        const uint32_t t2 = t / uint32_t(a.NBY);
+        p.by = int32_t(t - t2 * uint32_t(a.NBY));
+        p.nn = t2 / uint32_t(a.NBZ);
+        p.bz = int32_t(t2 - p.nn * uint32_t(a.NBZ));
     };
     auto advance = [&](Pos& p) {
         if (++p.j >= p.jend) {
@@ -156,57 +164,46 @@ __global__ __launch_bounds__(256, 1) void conv_fwd_xm(XmArgs a)
             seg_start(p);
         }
     };
-    auto rows_of = [&](uint32_t brick, int& bz, int& by, uint32_t& nn) {
-        uint32_t t = brick / uint32_t(a.nseg);
-        by = int(t % uint32_t(a.NBY));
-        t /= uint32_t(a.NBY);
-        bz = int(t % uint32_t(a.NBZ));
-        nn = t / uint32_t(a.NBZ);
-    };
 
-    auto stage = [&](const Pos& p, int buf) {
-        char* dst = lds + buf * C::STAGE_BYTES + wave * 64 * 16;
-        if (p.brick >= a.nbricks) {
-            // past the last unit: keep the per-thread load count uniform (zeros)
-            __amdgpu_buffer_rsrc_t r = __builtin_amdgcn_make_buffer_rsrc(const_cast<char*>(a.tile), short(0),
-                                                                         int(a.batch_bytes), 0x00020000);
-#pragma unroll
-            for (int it = 0; it < C::NIT; ++it)
-                __builtin_amdgcn_raw_ptr_buffer_load_lds(r, SC_LDS(dst + it * 4096), 16, a.batch_bytes, 0, 0, 0);
-            return;
-        }
-        int bz, by;
-        uint32_t nn;
-        rows_of(p.brick, bz, by, nn);
-        const int i0 = bz * C::BZ - a.pad[0];
+    // Staging of one unit is split in a set-up (uniform values of the unit, once per
+    // tile) and NIT single loads that the main loop spreads over its MFMA steps:
+    // issued as a burst, the loads stall the wave at issue (the memory pipeline
+    // accepts them more slowly than four waves issue them), and with one wave per
+    // SIMD every stalled cycle is an idle matrix core. Offsets are 32-bit (a batch
+    // item is < 4 GiB); a voxel outside the tile, or a unit past the last, gets an
+    // out-of-range offset and loads as zero.
+    __amdgpu_buffer_rsrc_t st_r = __builtin_amdgcn_make_buffer_rsrc(const_cast<char*>(a.tile), short(0),
+                                                                    int(a.batch_bytes), 0x00020000);
+    char* st_dst = lds;
+    uint32_t st_vbase = 0;
+    int32_t st_i0 = 0, st_vy = 0;
+    bool st_okx = false;
+    auto stage_setup = [&](const Pos& p, int buf) {
+        const bool live = p.brick < a.nbricks;
+        const int bz = live ? p.bz : 0, by = live ? p.by : 0;
+        const uint32_t nn = live ? p.nn : 0;
+        st_i0 = bz * C::BZ - a.pad[0];
         const int i1 = by * C::BY - a.pad[1];
         const int i2 = p.j * 32 - a.pad[2];
-        const bool inner = i0 >= 0 && i0 + C::IRZ <= a.P[0] && i1 >= 0 && i1 + C::IRY <= a.P[1] && i2 >= 0 &&
-                           i2 + 32 <= a.P[2];
-        const int64_t origin = ((int64_t(i0) * a.P[1] + i1) * a.P[2] + i2) * (CIN * 2);
-        __amdgpu_buffer_rsrc_t r = __builtin_amdgcn_make_buffer_rsrc(
-            const_cast<char*>(a.tile) + int64_t(nn) * a.batch_bytes, short(0), int(a.batch_bytes), 0x00020000);
-        if (inner) {
-            const uint32_t org = uint32_t(origin);
-#pragma unroll
-            for (int it = 0; it < C::NIT; ++it) {
-                const int row0 = it * C::RPI;
-                const uint32_t soff = org + uint32_t(row0 / C::IRY) * SZ + uint32_t(row0 % C::IRY) * SY;
-                __builtin_amdgcn_raw_ptr_buffer_load_lds(r, SC_LDS(dst + it * 4096), 16, tb, soff, 0, 0);
-            }
-        } else {
-#pragma unroll
-            for (int it = 0; it < C::NIT; ++it) {
-                const int row0 = it * C::RPI;
-                const int rz = row0 / C::IRY, ry = row0 % C::IRY + hs;
-                const int t0 = i0 + rz, t1 = i1 + ry, t2 = i2 + xs;
-                const bool ok = t0 >= 0 && t0 < a.P[0] && t1 >= 0 && t1 < a.P[1] && t2 >= 0 && t2 < a.P[2];
-                const uint32_t off =
-                    ok ? uint32_t(origin + int64_t(rz) * SZ + int64_t(row0 % C::IRY) * SY + tb) : a.batch_bytes;
-                __builtin_amdgcn_raw_ptr_buffer_load_lds(r, SC_LDS(dst + it * 4096), 16, off, 0, 0, 0);
-            }
-        }
+        const int64_t origin = ((int64_t(st_i0) * a.P[1] + i1) * a.P[2] + i2) * (CIN * 2);
+        st_r = __builtin_amdgcn_make_buffer_rsrc(const_cast<char*>(a.tile) + int64_t(nn) * a.batch_bytes, short(0),
+                                                 int(a.batch_bytes), 0x00020000);
+        st_dst = lds + buf * C::STAGE_BYTES + wave * 64 * 16;
+        st_vbase = uint32_t(origin) + tb;
+        st_vy = i1 + hs;
+        st_okx = live && uint32_t(i2 + xs) < uint32_t(a.P[2]);
     };
+    auto stage_load = [&](int it) {
+        const int row0 = it * C::RPI;
+        const int rz = row0 / C::IRY, ry = row0 % C::IRY;
+        const bool ok = st_okx && uint32_t(st_i0 + rz) < uint32_t(a.P[0]) && uint32_t(st_vy + ry) < uint32_t(a.P[1]);
+        const uint32_t off = ok ? st_vbase + uint32_t(rz) * SZ + uint32_t(ry) * SY : a.batch_bytes;
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(st_r, SC_LDS(st_dst + it * 4096), 16, off, 0, 0, 0);
+    };
+    // load it of a unit goes out in MFMA step step_of(it) of the tile before; the
+    // last in the last step, after that step's stores
+    constexpr int S_STEPS = R * KD * C::NKC;
+    static_assert(S_STEPS >= C::NIT, "at most one staging load per MFMA step");
 
     // epilogue LDS addresses: lane (g, co) writes voxel 16g + e of channel co at
     // slot (16g + e) ^ g; the read-back gives lane U = it * 64 + lane the 16 bytes
@@ -229,10 +226,7 @@ __global__ __launch_bounds__(256, 1) void conv_fwd_xm(XmArgs a)
         bool store;
     };
     auto tile_out = [&](const Pos& p) {
-        int bz, by;
-        uint32_t nn;
-        rows_of(p.brick, bz, by, nn);
-        return TileOut{p.j, bz * C::BZ + wz, by * C::BY + wy * R, nn, p.j >= p.jstore};
+        return TileOut{p.j, p.bz * C::BZ + wz, p.by * C::BY + wy * R, p.nn, p.j >= p.jstore};
     };
 
     f32x16_r acc[R][KW];
@@ -329,12 +323,14 @@ __global__ __launch_bounds__(256, 1) void conv_fwd_xm(XmArgs a)
         }
     };
 
-    Pos cp{L, 0, 0, 0}, sp{L, 0, 0, 0};
+    Pos cp{L, 0, 0, 0, 0, 0, 0}, sp{L, 0, 0, 0, 0, 0, 0};
     seg_start(cp);
     seg_start(sp);
 #pragma unroll
     for (int p = 0; p < NBUF - 1; ++p) {
-        stage(sp, p);
+        stage_setup(sp, p);
+#pragma unroll
+        for (int it = 0; it < C::NIT; ++it) stage_load(it);
         advance(sp);
     }
 
@@ -344,18 +340,26 @@ __global__ __launch_bounds__(256, 1) void conv_fwd_xm(XmArgs a)
     int cbuf = 0, sbuf = NBUF - 1;
     for (uint32_t u = 0; cp.brick < a.nbricks; ++u) {
         // Unit u's loads have landed and every wave is done with the buffer that
-        // is refilled next. Issued after unit u's loads: the loads of the next
-        // NBUF - 2 units and the stores of the last min(u, NBUF - 1) units.
-        const uint32_t ks = u < NBUF - 1 ? u : NBUF - 1;
+        // is refilled next. Issued after unit u's last load: the loads of the next
+        // NBUF - 2 units and the stores of the last min(u, NBUF - 2) tiles (a tile
+        // body issues its staging loads last).
+        const uint32_t ks = u < NBUF - 2 ? u : NBUF - 2;
         if (ks == 0)
             wait_vm_barrier<C::VM_BASE>();
         else if (ks == 1)
             wait_vm_barrier<C::VM_BASE + C::EPI_STORES>();
-        else if (ks == 2)
-            wait_vm_barrier<C::VM_BASE + 2 * C::EPI_STORES>();
         else
-            wait_vm_barrier<C::VM_BASE + 3 * C::EPI_STORES>();
-        stage(sp, sbuf);
+            wait_vm_barrier<C::VM_BASE + 2 * C::EPI_STORES>();
+        // the weight fragments stay in AGPRs (MFMA reads its B operand from them)
+#pragma unroll
+        for (int kd = 0; kd < KD; ++kd)
+#pragma unroll
+            for (int kh = 0; kh < KH; ++kh)
+#pragma unroll
+                for (int kw = 0; kw < KW; ++kw)
+#pragma unroll
+                    for (int kc = 0; kc < C::NKC; ++kc) asm volatile("" : "+a"(wv[kd][kh][kw][kc]));
+        stage_setup(sp, sbuf);
         advance(sp);
         sbuf = sbuf + 1 == NBUF ? 0 : sbuf + 1;
         const TileOut cur = tile_out(cp);
@@ -401,6 +405,9 @@ __global__ __launch_bounds__(256, 1) void conv_fwd_xm(XmArgs a)
                 pieces_of(q, R - 1, prev);
             else
                 pieces_of(q, r - 1, cur);
+#pragma unroll
+            for (int it = 0; it < C::NIT; ++it)
+                if (((it + 1) * S_STEPS) / C::NIT - 1 == st) stage_load(it);
         }
         cbuf = cbuf + 1 == NBUF ? 0 : cbuf + 1;
         prev = cur;
