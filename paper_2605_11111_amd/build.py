@@ -10,6 +10,7 @@ from __future__ import annotations
 import concurrent.futures as cf
 import glob
 import os
+import re
 import subprocess
 import sys
 
@@ -39,12 +40,29 @@ SRC_FLAGS = {
 
 def _compile(src: str) -> str:
     obj = os.path.join(OBJ, os.path.basename(src) + ".o")
-    cmd = [HIPCC, *FLAGS, *SRC_FLAGS.get(os.path.basename(src), []), "-x", "hip", "-c", src, "-o", obj]
+    cmd = [HIPCC, *FLAGS, *SRC_FLAGS.get(os.path.basename(src), []), "-Rpass-analysis=kernel-resource-usage",
+           "-x", "hip", "-c", src, "-o", obj]
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         sys.stderr.write(r.stdout + r.stderr)
         raise RuntimeError(f"hipcc failed on {src}")
+    _check_no_scratch(src, r.stderr)
     return obj
+
+
+def _check_no_scratch(src: str, remarks: str) -> None:
+    """The kernels issue LDS reads through inline asm and wait for them with
+    explicit counters; that is only sound while the destination registers stay
+    registers. A kernel that spills to scratch could store such a register
+    before its data has arrived, so the build refuses any scratch use."""
+    name = None
+    for line in remarks.splitlines():
+        m = re.search(r"Function Name: (\S+)", line)
+        if m:
+            name = m.group(1)
+        m = re.search(r"ScratchSize \[bytes/lane\]: (\d+)", line)
+        if m and int(m.group(1)) != 0:
+            raise RuntimeError(f"{os.path.basename(src)}: kernel {name} uses {m.group(1)} bytes/lane of scratch")
 
 
 def build(verbose: bool = False) -> str:

@@ -98,24 +98,33 @@ __global__ __launch_bounds__(256, 1) void wgrad_xm(WxArgs a)
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const uint32_t G = gridDim.x;
     const uint32_t L = uint32_t(xcd_remap(blockIdx.x, G));
-    // every wave runs the compute path (a branch around it would make the compiler
-    // shuttle the accumulators between register files on every tile); a spare
-    // wave repeats role 0 and drops its result
-    const bool computes = wave < C::NR;
-    const int role = computes ? wave : 0;
+    // With four roles every wave computes and issues a quarter of the staging
+    // loads; with three, wave 3 is a dedicated loader that issues them all (its
+    // stalls at issue then never hold back a matrix core).
+    static_assert(C::NR == 3 || C::NR == 4, "three or four wave roles");
+    constexpr bool kLoader = C::NR == 3;
+    const int role = wave < C::NR ? wave : 0;
     const int kd = role % KD, cb = (role / KD) % NCI, mb = role / (KD * NCI);
     const uint32_t lds0 = lds_addr(lds);
 
     // ---- staging (loader waves) ----
+    // a brick's rows (bz, by) and batch item nn are decoded once per brick
     struct Pos {
         uint32_t brick;
         int32_t j, jend;
+        int32_t bz, by;
+        uint32_t nn;
     };
     auto seg_start = [&](Pos& p) {
         if (p.brick >= a.nbricks) return;
-        const int32_t seg = int32_t(p.brick % uint32_t(a.nseg));
+        const uint32_t t = p.brick / uint32_t(a.nseg);
+        const int32_t seg = int32_t(p.brick - t * uint32_t(a.nseg));
         p.j = seg * a.T;
         p.jend = min(p.j + a.T, a.NXT);
+        const uint32_t t2 = t / uint32_t(a.NBY);
+        p.by = int32_t(t - t2 * uint32_t(a.NBY));
+        p.nn = t2 / uint32_t(a.NBZ);
+        p.bz = int32_t(t2 - p.nn * uint32_t(a.NBZ));
     };
     auto advance = [&](Pos& p) {
         if (++p.j >= p.jend) {
@@ -138,17 +147,92 @@ __global__ __launch_bounds__(256, 1) void wgrad_xm(WxArgs a)
     const uint32_t lxh = uint32_t(hv * C::CIN * 2 + (ux ^ wx_swz<C::UPX>(hv)) * 16);
     constexpr int XPI = 64 / C::UPX, YPI = 64 / C::UPY;  // voxels per instruction
     constexpr int HRPI = 64 / (4 * C::UPX);              // halo rows per instruction
-    auto stage = [&](const Pos& p, int buf) {
-        char* xdst = lds + buf * C::STAGE_BYTES;
-        char* hdst = xdst + C::X_BYTES;
-        char* ydst = hdst + C::XH_BYTES;
+    // A unit's staging is a set-up (its uniform values, once per tile) and the
+    // wave's single loads k = 0 .. KLOADS - 1, which the main loop spreads over the
+    // first rows of the tile: issued as one burst they stall the wave at issue,
+    // idling its matrix core. Load k of wave w is instruction 4k + w of its area
+    // (input rows k < KX, halo rows KX <= k < KX + 2, dy rows after), so every
+    // load's area and staged row are known at compile time up to the wave's bits.
+    // A lane whose voxel lies outside the tile or the output, or a unit past the
+    // last, loads zeros (out-of-range offset).
+    static_assert(C::X_INSTR % 4 == 0 && C::Y_INSTR % 4 == 0 && C::XH_INSTR <= 8, "load slots");
+    static_assert(C::XRY % (4 / C::IPR_X) == 0 && BY % (4 / C::IPR_Y) == 0, "a slot's rows share a plane");
+    constexpr int KX = C::X_INSTR / 4, KH0 = KX, KY0 = KX + 2;
+    constexpr int KLOADS = KY0 + C::Y_INSTR / 4;
+    constexpr int RKX = 4 / C::IPR_X, RKY = 4 / C::IPR_Y;  // staged rows per slot
+    const int wrx = wave / C::IPR_X, pcx = wave % C::IPR_X;
+    const int wry = wave / C::IPR_Y, pcy = wave % C::IPR_Y;
+    const uint32_t lxw = lxm + uint32_t(pcx * XPI * C::CIN * 2);
+    const uint32_t lyw = lym + uint32_t(pcy * YPI * C::COUT * 2);
+    __amdgpu_buffer_rsrc_t st_rx = __builtin_amdgcn_make_buffer_rsrc(const_cast<char*>(a.tile), short(0),
+                                                                     int(a.tile_bytes), 0x00020000);
+    __amdgpu_buffer_rsrc_t st_ry = __builtin_amdgcn_make_buffer_rsrc(const_cast<char*>(a.dy), short(0),
+                                                                     int(a.dy_bytes), 0x00020000);
+    char* st_dst = lds;
+    uint32_t st_xorg = 0, st_yorg = 0;
+    int32_t st_i0 = 0, st_i1 = 0, st_i2 = 0, st_o0 = 0, st_o1 = 0;
+    bool st_live = false, st_okx = false, st_oky = false;
+    auto stage_setup = [&](const Pos& p, int buf) {
+        st_live = p.brick < a.nbricks;
+        const uint32_t nn = st_live ? p.nn : 0;
+        st_o0 = st_live ? p.bz * BZ : 0;
+        st_o1 = st_live ? p.by * BY : 0;
+        const int o2 = p.j * 32;
+        st_i0 = st_o0 - a.pad[0];
+        st_i1 = st_o1 - a.pad[1];
+        st_i2 = o2 - a.pad[2];
+        st_xorg = uint32_t(st_i0) * a.xplane + uint32_t(st_i1 + wrx) * a.xrow + uint32_t(st_i2) * (C::CIN * 2);
+        st_yorg = uint32_t(st_o0) * a.yplane + uint32_t(st_o1 + wry) * a.yrow + uint32_t(o2) * (C::COUT * 2);
+        st_okx = st_live && uint32_t(st_i2 + pcx * XPI + vx) < uint32_t(a.P[2]);
+        st_oky = st_live && o2 + pcy * YPI + vy < a.O[2];
+        st_rx = __builtin_amdgcn_make_buffer_rsrc(const_cast<char*>(a.tile) + int64_t(nn) * a.tile_bytes, short(0),
+                                                  int(a.tile_bytes), 0x00020000);
+        st_ry = __builtin_amdgcn_make_buffer_rsrc(const_cast<char*>(a.dy) + int64_t(nn) * a.dy_bytes, short(0),
+                                                  int(a.dy_bytes), 0x00020000);
+        st_dst = lds + buf * C::STAGE_BYTES + wave * 1024;
+    };
+    auto stage_load = [&](int k) {
+        if (k < KH0) {
+            const int zr = (RKX * k) / C::XRY, yr0 = (RKX * k) % C::XRY;
+            const bool ok = st_okx && uint32_t(st_i0 + zr) < uint32_t(a.P[0]) &&
+                            uint32_t(st_i1 + yr0 + wrx) < uint32_t(a.P[1]);
+            const uint32_t u = st_xorg + uint32_t(zr) * a.xplane + uint32_t(yr0) * a.xrow + lxw;
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(st_rx, SC_LDSW(st_dst + 4 * k * 1024), 16, ok ? u : a.tile_bytes,
+                                                     0, 0, 0);
+        } else if (k < KY0) {
+            const int hi = 4 * (k - KH0) + wave;
+            if (hi < C::XH_INSTR) {
+                const int row = hi * HRPI + hrow;
+                const int zr = row / C::XRY, yr = row % C::XRY;
+                const bool ok = st_live && uint32_t(st_i0 + zr) < uint32_t(a.P[0]) &&
+                                uint32_t(st_i1 + yr) < uint32_t(a.P[1]) && uint32_t(st_i2 + hv) < uint32_t(a.P[2]);
+                const uint32_t u = st_xorg - uint32_t(wrx) * a.xrow + uint32_t(zr) * a.xplane +
+                                   uint32_t(yr) * a.xrow + lxh;
+                __builtin_amdgcn_raw_ptr_buffer_load_lds(st_rx,
+                                                         SC_LDSW(st_dst + C::X_BYTES + 4 * (k - KH0) * 1024), 16,
+                                                         ok ? u : a.tile_bytes, 0, 0, 0);
+            }
+        } else {
+            const int kk = k - KY0;
+            const int zb = (RKY * kk) / BY, yb0 = (RKY * kk) % BY;
+            const bool ok = st_oky && st_o0 + zb < a.O[0] && st_o1 + yb0 + wry < a.O[1];
+            const uint32_t u = st_yorg + uint32_t(zb) * a.yplane + uint32_t(yb0) * a.yrow + lyw;
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(st_ry,
+                                                     SC_LDSW(st_dst + C::X_BYTES + C::XH_BYTES + 4 * kk * 1024), 16,
+                                                     ok ? u : a.dy_bytes, 0, 0, 0);
+        }
+    };
+    // rows of a tile over which the loads of the next unit are spread (the rest
+    // of the tile covers their latency)
+    constexpr int LOAD_ROWS = C::NQ > 4 ? C::NQ - 2 : 1;
+    static_assert((KLOADS + LOAD_ROWS - 1) / LOAD_ROWS <= 6, "at most one load per MFMA group");
+
+    // the dedicated loader issues every load of a unit (instruction index known at
+    // compile time)
+    auto loader_unit = [&](const Pos& p, int buf) {
         const bool live = p.brick < a.nbricks;
-        uint32_t t = live ? p.brick / uint32_t(a.nseg) : 0;
-        const int by = int(t % uint32_t(a.NBY));
-        t /= uint32_t(a.NBY);
-        const int bz = int(t % uint32_t(a.NBZ));
-        const uint32_t nn = live ? t / uint32_t(a.NBZ) : 0;
-        const int o0 = bz * BZ, o1 = by * BY, o2 = p.j * 32;
+        const uint32_t nn = live ? p.nn : 0;
+        const int o0 = live ? p.bz * BZ : 0, o1 = live ? p.by * BY : 0, o2 = p.j * 32;
         const int i0 = o0 - a.pad[0], i1 = o1 - a.pad[1], i2 = o2 - a.pad[2];
         const uint32_t xorg = uint32_t(i0) * a.xplane + uint32_t(i1) * a.xrow + uint32_t(i2) * (C::CIN * 2);
         const uint32_t yorg = uint32_t(o0) * a.yplane + uint32_t(o1) * a.yrow + uint32_t(o2) * (C::COUT * 2);
@@ -156,77 +240,57 @@ __global__ __launch_bounds__(256, 1) void wgrad_xm(WxArgs a)
             const_cast<char*>(a.tile) + int64_t(nn) * a.tile_bytes, short(0), int(a.tile_bytes), 0x00020000);
         __amdgpu_buffer_rsrc_t ry = __builtin_amdgcn_make_buffer_rsrc(
             const_cast<char*>(a.dy) + int64_t(nn) * a.dy_bytes, short(0), int(a.dy_bytes), 0x00020000);
-        const bool inner = live && i0 >= 0 && i0 + C::XRZ <= a.P[0] && i1 >= 0 && i1 + C::XRY <= a.P[1] &&
-                           i2 >= 0 && i2 + 36 <= a.P[2] && o0 + BZ <= a.O[0] && o1 + BY <= a.O[1] &&
-                           o2 + 32 <= a.O[2];
-        if (inner) {
+        char* dst = lds + buf * C::STAGE_BYTES;
 #pragma unroll
-            for (int k = 0; k < (C::XR + 3) / 4; ++k) {
-                const int row = 4 * k + wave;
-                if (row < C::XR) {
-                    const uint32_t u = xorg + uint32_t(row / C::XRY) * a.xplane + uint32_t(row % C::XRY) * a.xrow + lxm;
-#pragma unroll
-                    for (int pc = 0; pc < C::IPR_X; ++pc)
-                        __builtin_amdgcn_raw_ptr_buffer_load_lds(rx, SC_LDSW(xdst + (row * C::IPR_X + pc) * 1024), 16,
-                                                                 u + uint32_t(pc * XPI * C::CIN * 2), 0, 0, 0);
-                }
-            }
-#pragma unroll
-            for (int k = 0; k < (C::XH_INSTR + 3) / 4; ++k) {
-                const int hi = 4 * k + wave;
-                if (hi < C::XH_INSTR) {
-                    const int row = hi * HRPI + hrow;
-                    const uint32_t u = xorg + uint32_t(row / C::XRY) * a.xplane + uint32_t(row % C::XRY) * a.xrow + lxh;
-                    __builtin_amdgcn_raw_ptr_buffer_load_lds(rx, SC_LDSW(hdst + hi * 1024), 16, u, 0, 0, 0);
-                }
-            }
-#pragma unroll
-            for (int k = 0; k < (C::NQ + 3) / 4; ++k) {
-                const int row = 4 * k + wave;
-                if (row < C::NQ) {
-                    const uint32_t u = yorg + uint32_t(row / BY) * a.yplane + uint32_t(row % BY) * a.yrow + lym;
-#pragma unroll
-                    for (int pc = 0; pc < C::IPR_Y; ++pc)
-                        __builtin_amdgcn_raw_ptr_buffer_load_lds(ry, SC_LDSW(ydst + (row * C::IPR_Y + pc) * 1024), 16,
-                                                                 u + uint32_t(pc * YPI * C::COUT * 2), 0, 0, 0);
-                }
-            }
-            return;
-        }
-        // edge tiles: per-lane range checks, out-of-range voxels load zeros
-        for (int row = wave; row < C::XR; row += 4) {
+        for (int i = 0; i < C::X_INSTR; ++i) {
+            const int row = i / C::IPR_X, pc = i % C::IPR_X;
             const int zr = row / C::XRY, yr = row % C::XRY;
-            const bool rok = live && i0 + zr >= 0 && i0 + zr < a.P[0] && i1 + yr >= 0 && i1 + yr < a.P[1];
-            const uint32_t u = xorg + uint32_t(zr) * a.xplane + uint32_t(yr) * a.xrow + lxm;
-            for (int pc = 0; pc < C::IPR_X; ++pc) {
-                const int t2 = i2 + pc * XPI + vx;
-                const bool ok = rok && t2 >= 0 && t2 < a.P[2];
-                __builtin_amdgcn_raw_ptr_buffer_load_lds(rx, SC_LDSW(xdst + (row * C::IPR_X + pc) * 1024), 16,
-                                                         ok ? u + uint32_t(pc * XPI * C::CIN * 2) : a.tile_bytes, 0,
-                                                         0, 0);
-            }
+            const bool ok = live && uint32_t(i0 + zr) < uint32_t(a.P[0]) && uint32_t(i1 + yr) < uint32_t(a.P[1]) &&
+                            uint32_t(i2 + pc * XPI + vx) < uint32_t(a.P[2]);
+            const uint32_t u = xorg + uint32_t(zr) * a.xplane + uint32_t(yr) * a.xrow + lxm +
+                               uint32_t(pc * XPI * C::CIN * 2);
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(rx, SC_LDSW(dst + i * 1024), 16, ok ? u : a.tile_bytes, 0, 0, 0);
         }
-        for (int hi = wave; hi < C::XH_INSTR; hi += 4) {
+#pragma unroll
+        for (int hi = 0; hi < C::XH_INSTR; ++hi) {
             const int row = hi * HRPI + hrow;
             const int zr = row / C::XRY, yr = row % C::XRY;
-            const bool ok = live && i0 + zr >= 0 && i0 + zr < a.P[0] && i1 + yr >= 0 && i1 + yr < a.P[1] &&
-                            i2 + hv >= 0 && i2 + hv < a.P[2];
+            const bool ok = live && uint32_t(i0 + zr) < uint32_t(a.P[0]) && uint32_t(i1 + yr) < uint32_t(a.P[1]) &&
+                            uint32_t(i2 + hv) < uint32_t(a.P[2]);
             const uint32_t u = xorg + uint32_t(zr) * a.xplane + uint32_t(yr) * a.xrow + lxh;
-            __builtin_amdgcn_raw_ptr_buffer_load_lds(rx, SC_LDSW(hdst + hi * 1024), 16, ok ? u : a.tile_bytes, 0, 0,
-                                                     0);
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(rx, SC_LDSW(dst + C::X_BYTES + hi * 1024), 16,
+                                                     ok ? u : a.tile_bytes, 0, 0, 0);
         }
-        for (int row = wave; row < C::NQ; row += 4) {
+#pragma unroll
+        for (int j = 0; j < C::Y_INSTR; ++j) {
+            const int row = j / C::IPR_Y, pc = j % C::IPR_Y;
             const int zb = row / BY, yb = row % BY;
-            const bool rok = live && o0 + zb < a.O[0] && o1 + yb < a.O[1];
-            const uint32_t u = yorg + uint32_t(zb) * a.yplane + uint32_t(yb) * a.yrow + lym;
-            for (int pc = 0; pc < C::IPR_Y; ++pc) {
-                const bool ok = rok && o2 + pc * YPI + vy < a.O[2];
-                __builtin_amdgcn_raw_ptr_buffer_load_lds(ry, SC_LDSW(ydst + (row * C::IPR_Y + pc) * 1024), 16,
-                                                         ok ? u + uint32_t(pc * YPI * C::COUT * 2) : a.dy_bytes, 0,
-                                                         0, 0);
-            }
+            const bool ok = live && o0 + zb < a.O[0] && o1 + yb < a.O[1] && o2 + pc * YPI + vy < a.O[2];
+            const uint32_t u = yorg + uint32_t(zb) * a.yplane + uint32_t(yb) * a.yrow + lym +
+                               uint32_t(pc * YPI * C::COUT * 2);
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(ry, SC_LDSW(dst + C::X_BYTES + C::XH_BYTES + j * 1024), 16,
+                                                     ok ? u : a.dy_bytes, 0, 0, 0);
         }
     };
+    if (kLoader && wave == 3) {
+        Pos cp{L, 0, 0, 0, 0, 0}, sp{L, 0, 0, 0, 0, 0};
+        seg_start(cp);
+        seg_start(sp);
+        loader_unit(sp, 0);
+        advance(sp);
+        int buf = 0;
+        while (cp.brick < a.nbricks) {
+            // this tile's loads have landed and the compute waves are done with
+            // the other buffer: fill it with the next unit
+            wait_vm_barrier<0>();
+            loader_unit(sp, buf ^ 1);
+            advance(sp);
+            buf ^= 1;
+            advance(cp);
+        }
+        wait_vm_barrier<0>();
+        return;
+    }
 
     // ---- operand reads (compute waves) ----
     // transposed-read lane terms: 16-lane group G = lane / 16 reads voxels
@@ -313,7 +377,8 @@ __global__ __launch_bounds__(256, 1) void wgrad_xm(WxArgs a)
                     xs[slot][4 * s + e] = __builtin_amdgcn_alignbit(xr[slot][4 * s + e + 1], xr[slot][4 * s + e], 16);
         }
     };
-    auto mfma_row = [&](int q) {
+    // after_group(g) runs after MFMA group g = s * 3 + kh (three MFMAs) of the row
+    auto mfma_row = [&](int q, auto&& after_group) {
         const int zb = q / BY, yb = q % BY;
 #pragma unroll
         for (int s = 0; s < 2; ++s) {
@@ -336,21 +401,30 @@ __global__ __launch_bounds__(256, 1) void wgrad_xm(WxArgs a)
                 acc[kh][2] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8_w, av),
                                                                      __builtin_bit_cast(bf16x8_w, b2), acc[kh][2], 0,
                                                                      0, 0);
+                after_group(s * 3 + kh);
             }
         }
     };
 
-    Pos cp{L, 0, 0}, sp{L, 0, 0};
+    Pos cp{L, 0, 0, 0, 0, 0}, sp{L, 0, 0, 0, 0, 0};
     seg_start(cp);
     seg_start(sp);
-    stage(sp, 0);
-    advance(sp);
+    if (!kLoader) {
+        stage_setup(sp, 0);
+#pragma unroll
+        for (int k = 0; k < KLOADS; ++k) stage_load(k);
+        advance(sp);
+    }
     int buf = 0;
     while (cp.brick < a.nbricks) {
         // this tile's loads have landed; every wave is done with the other buffer
         wait_vm_barrier<0>();
         const uint32_t xbase = lds0 + uint32_t(buf * C::STAGE_BYTES);
         const uint32_t ybase = xbase + uint32_t(C::X_BYTES + C::XH_BYTES);
+        if (!kLoader) {
+            stage_setup(sp, buf ^ 1);
+            advance(sp);
+        }
         issue_row(xbase, ybase, 0);
 #pragma unroll
         for (int q = 0; q < C::NQ; ++q) {
@@ -362,19 +436,20 @@ __global__ __launch_bounds__(256, 1) void wgrad_xm(WxArgs a)
                 lds_wait<0>();
             }
             ready_row(q);
-            mfma_row(q);
-            // the next tile's loads go out in the shadow of the first row's MFMAs
-            if (q == 0) {
-                stage(sp, buf ^ 1);
-                advance(sp);
-            }
+            // the next unit's loads go out one per MFMA group, so that the memory
+            // pipeline never holds more than about one load per wave
+            const int kb = !kLoader && q < LOAD_ROWS ? (q * KLOADS + LOAD_ROWS - 1) / LOAD_ROWS : KLOADS;
+            const int ke = !kLoader && q < LOAD_ROWS ? ((q + 1) * KLOADS + LOAD_ROWS - 1) / LOAD_ROWS : KLOADS;
+            mfma_row(q, [&](int g) {
+                if (kb + g < ke) stage_load(kb + g);
+            });
             if (q + 1 < C::NQ && plane_break) issue_row(xbase, ybase, q + 1);
         }
         buf ^= 1;
         advance(cp);
     }
     wait_vm_barrier<0>();
-    if (computes) {
+    {
         // partial: [workgroup][wave][tap kh * 3 + kw][lane][16]
         float4* out = reinterpret_cast<float4*>(a.part + int64_t(L) * C::PART_FLOATS + int64_t(wave) * 9 * 1024);
 #pragma unroll
