@@ -41,6 +41,39 @@ __device__ __forceinline__ int64_t xcd_remap(int64_t b, int64_t nblocks)
     return x * q + (x < r ? x : r) + j;
 }
 
+// Brick raster of the persistent W-march kernels. Brick t (W segment already
+// removed) of a batch item's NBZ x NBY brick grid lies in raster block t / (TZ*TY)
+// (blocks row-major over the grid, each TZ x TY bricks, TZ | NBZ and TY | NBY) at
+// row-major position t % (TZ*TY) inside it. A workgroup handles bricks L, L + G,
+// ...; with xcd_remap the 32 workgroups of an XCD hold 32 consecutive bricks, so
+// a 32-brick block keeps the halo rows its bricks share in that XCD's L2, and the
+// eight XCDs work on adjacent blocks at the same time (shared halos meet in the
+// last-level cache). TZ = TY = 1 is the plain row-major order.
+__device__ __forceinline__ void brick_rows(uint32_t t, int32_t NBZ, int32_t NBY, int32_t TZ, int32_t TY, int32_t& bz,
+                                           int32_t& by, uint32_t& nn)
+{
+    const uint32_t per_item = uint32_t(NBZ) * uint32_t(NBY);
+    nn = t / per_item;
+    const uint32_t tt = t - nn * per_item;
+    const uint32_t bs = uint32_t(TZ) * uint32_t(TY);
+    const uint32_t blk = tt / bs, r = tt - blk * bs;
+    const uint32_t nty = uint32_t(NBY) / uint32_t(TY);
+    const uint32_t bzb = blk / nty, byb = blk - bzb * nty;
+    const uint32_t rz = r / uint32_t(TY);
+    bz = int32_t(bzb * uint32_t(TZ) + rz);
+    by = int32_t(byb * uint32_t(TY) + (r - rz * uint32_t(TY)));
+}
+
+// Largest raster block TZ x TY of at most `want_z` x (32 / TZ) bricks that
+// divides the NBZ x NBY grid (powers of two).
+inline void pick_raster(int64_t NBZ, int64_t NBY, int want_z, int32_t& TZ, int32_t& TY)
+{
+    TZ = 1;
+    while (TZ * 2 <= want_z && NBZ % (TZ * 2) == 0) TZ *= 2;
+    TY = 1;
+    while (TZ * TY * 2 <= 32 && NBY % (TY * 2) == 0) TY *= 2;
+}
+
 }  // namespace shardconv
 
 namespace shardconv {

@@ -51,6 +51,7 @@ struct XmArgs {
     int32_t P[3], O[3];
     int32_t pad[3];
     int32_t NBZ, NBY, NXT;  // bricks along D and H, input tiles along W
+    int32_t TZ, TY;         // raster block of TZ x TY bricks (divides NBZ x NBY)
     int32_t nseg, T;        // W segments per row and their length in tiles
     uint32_t nbricks;       // n * NBZ * NBY * nseg
     uint32_t batch_bytes;   // tile bytes per batch item (< 2^32)
@@ -153,10 +154,7 @@ __global__ __launch_bounds__(256, 1) void conv_fwd_xm(XmArgs a)
         p.jstore = seg * a.T;
         p.j = seg > 0 ? p.jstore - 1 : 0;
         p.jend = min(p.jstore + a.T, a.NXT);
-        const uint32_t t2 = t / uint32_t(a.NBY);
-        p.by = int32_t(t - t2 * uint32_t(a.NBY));
-        p.nn = t2 / uint32_t(a.NBZ);
-        p.bz = int32_t(t2 - p.nn * uint32_t(a.NBZ));
+        brick_rows(t, a.NBZ, a.NBY, a.TZ, a.TY, p.bz, p.by, p.nn);
     };
     auto advance = [&](Pos& p) {
         if (++p.j >= p.jend) {
@@ -439,6 +437,7 @@ hipError_t launch_xm(const Tile3& t, const Conv3& cv, const void* tile, const vo
     if (t.n == 0 || cv.O[0] == 0 || cv.O[1] == 0 || cv.O[2] == 0) return hipSuccess;
     a.NBZ = int32_t(ceil_div(cv.O[0], C::BZ));
     a.NBY = int32_t(ceil_div(cv.O[1], C::BY));
+    pick_raster(a.NBZ, a.NBY, 4, a.TZ, a.TY);
     a.NXT = int32_t(ceil_div(cv.O[2] + C::KW - 1, 32));
     int dev = 0, cus = 256;
     if (hipGetDevice(&dev) == hipSuccess) hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);

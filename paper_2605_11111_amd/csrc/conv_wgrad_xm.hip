@@ -46,6 +46,7 @@ struct WxArgs {
     int32_t P[3], O[3];
     int32_t pad[3];
     int32_t NBZ, NBY, NXT;  // bricks along D and H, 32-voxel tiles along W
+    int32_t TZ, TY;         // raster block of TZ x TY bricks (divides NBZ x NBY)
     int32_t nseg, T;        // W segments per brick row and their length in tiles
     uint32_t nbricks;       // n * NBZ * NBY * nseg
     uint32_t tile_bytes, dy_bytes;  // per batch item (< 2^32)
@@ -121,10 +122,7 @@ __global__ __launch_bounds__(256, 1) void wgrad_xm(WxArgs a)
         const int32_t seg = int32_t(p.brick - t * uint32_t(a.nseg));
         p.j = seg * a.T;
         p.jend = min(p.j + a.T, a.NXT);
-        const uint32_t t2 = t / uint32_t(a.NBY);
-        p.by = int32_t(t - t2 * uint32_t(a.NBY));
-        p.nn = t2 / uint32_t(a.NBZ);
-        p.bz = int32_t(t2 - p.nn * uint32_t(a.NBZ));
+        brick_rows(t, a.NBZ, a.NBY, a.TZ, a.TY, p.bz, p.by, p.nn);
     };
     auto advance = [&](Pos& p) {
         if (++p.j >= p.jend) {
@@ -245,8 +243,8 @@ __global__ __launch_bounds__(256, 1) void wgrad_xm(WxArgs a)
         for (int i = 0; i < C::X_INSTR; ++i) {
             const int row = i / C::IPR_X, pc = i % C::IPR_X;
             const int zr = row / C::XRY, yr = row % C::XRY;
-            const bool ok = live && uint32_t(i0 + zr) < uint32_t(a.P[0]) && uint32_t(i1 + yr) < uint32_t(a.P[1]) &&
-                            uint32_t(i2 + pc * XPI + vx) < uint32_t(a.P[2]);
+            const bool ok = live & (uint32_t(i0 + zr) < uint32_t(a.P[0])) & (uint32_t(i1 + yr) < uint32_t(a.P[1])) &
+                            (uint32_t(i2 + pc * XPI + vx) < uint32_t(a.P[2]));
             const uint32_t u = xorg + uint32_t(zr) * a.xplane + uint32_t(yr) * a.xrow + lxm +
                                uint32_t(pc * XPI * C::CIN * 2);
             __builtin_amdgcn_raw_ptr_buffer_load_lds(rx, SC_LDSW(dst + i * 1024), 16, ok ? u : a.tile_bytes, 0, 0, 0);
@@ -255,8 +253,8 @@ __global__ __launch_bounds__(256, 1) void wgrad_xm(WxArgs a)
         for (int hi = 0; hi < C::XH_INSTR; ++hi) {
             const int row = hi * HRPI + hrow;
             const int zr = row / C::XRY, yr = row % C::XRY;
-            const bool ok = live && uint32_t(i0 + zr) < uint32_t(a.P[0]) && uint32_t(i1 + yr) < uint32_t(a.P[1]) &&
-                            uint32_t(i2 + hv) < uint32_t(a.P[2]);
+            const bool ok = live & (uint32_t(i0 + zr) < uint32_t(a.P[0])) & (uint32_t(i1 + yr) < uint32_t(a.P[1])) &
+                            (uint32_t(i2 + hv) < uint32_t(a.P[2]));
             const uint32_t u = xorg + uint32_t(zr) * a.xplane + uint32_t(yr) * a.xrow + lxh;
             __builtin_amdgcn_raw_ptr_buffer_load_lds(rx, SC_LDSW(dst + C::X_BYTES + hi * 1024), 16,
                                                      ok ? u : a.tile_bytes, 0, 0, 0);
@@ -265,7 +263,7 @@ __global__ __launch_bounds__(256, 1) void wgrad_xm(WxArgs a)
         for (int j = 0; j < C::Y_INSTR; ++j) {
             const int row = j / C::IPR_Y, pc = j % C::IPR_Y;
             const int zb = row / BY, yb = row % BY;
-            const bool ok = live && o0 + zb < a.O[0] && o1 + yb < a.O[1] && o2 + pc * YPI + vy < a.O[2];
+            const bool ok = live & (o0 + zb < a.O[0]) & (o1 + yb < a.O[1]) & (o2 + pc * YPI + vy < a.O[2]);
             const uint32_t u = yorg + uint32_t(zb) * a.yplane + uint32_t(yb) * a.yrow + lym +
                                uint32_t(pc * YPI * C::COUT * 2);
             __builtin_amdgcn_raw_ptr_buffer_load_lds(ry, SC_LDSW(dst + C::X_BYTES + C::XH_BYTES + j * 1024), 16,
@@ -531,6 +529,7 @@ WxPlan plan_wx(const Tile3& t, const Conv3& cv, shard_dtype_t dt)
     }
     a.NBZ = int32_t(ceil_div(cv.O[0], bz));
     a.NBY = int32_t(ceil_div(cv.O[1], by));
+    pick_raster(a.NBZ, a.NBY, 8, a.TZ, a.TY);
     a.NXT = int32_t(ceil_div(cv.O[2], 32));
     const int64_t rows = t.n * int64_t(a.NBZ) * a.NBY;
     if (rows == 0 || a.NXT == 0) return p;
