@@ -3,11 +3,14 @@
 // convolution, ShardTensor section "PyTorch Dispatch").
 //
 // The box is `rows` runs of `run` contiguous bytes (contiguous inner axes are
-// merged on the host). Each thread moves U vectors of V bytes, all loads issued
-// before any store; consecutive lanes touch consecutive vectors, so every wave
-// instruction covers 64*V contiguous bytes. A single-run box (the common case
-// of a slab along the outermost sharded axis, which is one contiguous block of
-// the tile) takes a specialisation with no index arithmetic.
+// merged on the host). Each thread moves U vectors of V bytes (U = 8 for 16-byte
+// vectors), all loads issued before any store; consecutive lanes touch
+// consecutive vectors, so every wave instruction covers 64*V contiguous bytes.
+// Loads and stores are nontemporal: a slab is read or written once per exchange,
+// and streaming it past the caches measured faster than cached accesses for a
+// 16 MiB face. A single-run box (the common case of a slab along the outermost
+// sharded axis, which is one contiguous block of the tile) takes a
+// specialisation with no index arithmetic.
 #include <algorithm>
 
 #include "internal.h"
@@ -27,16 +30,24 @@ struct CopyArgs {
 };
 
 constexpr int kThreads = 256;
-constexpr int kUnroll = 4;
 
 template <int V>
 struct Vec;
 template <>
-struct Vec<16> { using T = uint4; };
+struct Vec<16> {
+    using T = __attribute__((ext_vector_type(4))) unsigned int;
+    static constexpr int U = 8;
+};
 template <>
-struct Vec<4> { using T = uint32_t; };
+struct Vec<4> {
+    using T = uint32_t;
+    static constexpr int U = 4;
+};
 template <>
-struct Vec<2> { using T = uint16_t; };
+struct Vec<2> {
+    using T = uint16_t;
+    static constexpr int U = 4;
+};
 
 template <int V, bool kSingleRun>
 __device__ __forceinline__ int64_t tile_offset(const CopyArgs& a, int64_t v)
@@ -55,6 +66,7 @@ template <int V, bool kSingleRun>
 __global__ __launch_bounds__(kThreads) void box_copy_kernel(CopyArgs a)
 {
     using T = typename Vec<V>::T;
+    constexpr int kUnroll = Vec<V>::U;
     const int64_t nthreads = int64_t(gridDim.x) * kThreads;
     const int64_t tid = int64_t(blockIdx.x) * kThreads + threadIdx.x;
     for (int64_t v0 = tid; v0 < a.total; v0 += nthreads * kUnroll) {
@@ -66,9 +78,9 @@ __global__ __launch_bounds__(kThreads) void box_copy_kernel(CopyArgs a)
             off[u] = v < a.total ? tile_offset<V, kSingleRun>(a, v) : 0;
             if (v < a.total) {
                 if (a.dir == TILE_TO_SLAB) {
-                    val[u] = *reinterpret_cast<const T*>(a.src + off[u]);
+                    val[u] = __builtin_nontemporal_load(reinterpret_cast<const T*>(a.src + off[u]));
                 } else if (a.dir == SLAB_TO_TILE) {
-                    val[u] = *reinterpret_cast<const T*>(a.src + v * V);
+                    val[u] = __builtin_nontemporal_load(reinterpret_cast<const T*>(a.src + v * V));
                 } else {
                     val[u] = T{};
                 }
@@ -79,9 +91,9 @@ __global__ __launch_bounds__(kThreads) void box_copy_kernel(CopyArgs a)
             const int64_t v = v0 + u * nthreads;
             if (v < a.total) {
                 if (a.dir == TILE_TO_SLAB) {
-                    *reinterpret_cast<T*>(a.dst + v * V) = val[u];
+                    __builtin_nontemporal_store(val[u], reinterpret_cast<T*>(a.dst + v * V));
                 } else {
-                    *reinterpret_cast<T*>(a.dst + off[u]) = val[u];
+                    __builtin_nontemporal_store(val[u], reinterpret_cast<T*>(a.dst + off[u]));
                 }
             }
         }
@@ -104,7 +116,7 @@ hipError_t launch_v(const BoxCopy& b, CopyDir dir, const void* src, void* dst, h
     const int64_t rows = b.cnt[0] * b.cnt[1] * b.cnt[2];
     a.total = rows * a.nvec_row;
     a.dir = dir;
-    const int64_t per_block = int64_t(kThreads) * kUnroll;
+    const int64_t per_block = int64_t(kThreads) * Vec<V>::U;
     const int64_t blocks = std::max<int64_t>(1, std::min<int64_t>(ceil_div(a.total, per_block), 1 << 20));
     void* args[] = {&a};
     const void* fn = rows == 1 ? reinterpret_cast<const void*>(&box_copy_kernel<V, true>)
