@@ -153,4 +153,19 @@ __device__ __forceinline__ void lds_ready(T& v)
     asm volatile("" : "+v"(v));
 }
 
+// A 32-bit LDS word read now (waits for it and every earlier LDS operation of
+// the wave), made wave-uniform: for polling counters that other waves raise.
+__device__ __forceinline__ uint32_t lds_read_u32_now(uint32_t addr)
+{
+    uint32_t v;
+    asm volatile("ds_read_b32 %0, %1\n\ts_waitcnt lgkmcnt(0)" : "=v"(v) : "v"(addr) : "memory");
+    return __builtin_amdgcn_readfirstlane(v);
+}
+
+// Atomic add to a 32-bit LDS word (no return value); callers issue it from one lane.
+__device__ __forceinline__ void lds_add_u32(uint32_t addr, uint32_t v)
+{
+    asm volatile("ds_add_u32 %0, %1" ::"v"(addr), "v"(v) : "memory");
+}
+
 }  // namespace shardconv

@@ -14,9 +14,13 @@
 //    output rows j - kh. Taps along W are not applied to the operand at all: input
 //    voxel u reaches output u - kw through tap kw, so each (output row, kw) keeps
 //    its own accumulator over the same A fragments and the three are summed with a
-//    shift of kw rows when the tile is done. Output rows that straddle the tile
-//    edge take their missing terms from the previous tile (a 3-value carry), so
-//    tile j completes the outputs [32j - 2, 32j + 30).
+//    shift of kw rows when the tile is done. Tile j stages tile voxels
+//    [32j, 32j + 32); output rows that straddle the tile edge take their missing
+//    terms from the previous tile (a 3-value carry, zero before the row's first
+//    tile), so tile j completes the outputs [32j + pad - 2, 32j + pad + 30). A row
+//    takes ceil(P2 / 32) tiles: the last two outputs of the last tile need only
+//    voxels past the row end (zero), so they are written from the carry (no
+//    extra tile of MFMAs for them).
 //  * A-row m of the MFMA holds input voxel x(m) = 16*((m>>2)&1) + 4*(m>>3) + (m&3),
 //    so that accumulator register r of lane half g is voxel 16g + r: the W shift is
 //    a register shift except at r < kw, where the value comes from the other lane
@@ -182,7 +186,7 @@ __global__ __launch_bounds__(256, 1) void conv_fwd_xm(XmArgs a)
         const uint32_t nn = live ? p.nn : 0;
         st_i0 = bz * C::BZ - a.pad[0];
         const int i1 = by * C::BY - a.pad[1];
-        const int i2 = p.j * 32 - a.pad[2];
+        const int i2 = p.j * 32;
         const int64_t origin = ((int64_t(st_i0) * a.P[1] + i1) * a.P[2] + i2) * (CIN * 2);
         st_r = __builtin_amdgcn_make_buffer_rsrc(const_cast<char*>(a.tile) + int64_t(nn) * a.batch_bytes, short(0),
                                                  int(a.batch_bytes), 0x00020000);
@@ -259,12 +263,35 @@ __global__ __launch_bounds__(256, 1) void conv_fwd_xm(XmArgs a)
             const float s1 = __uint_as_float(g ? p1[0] : p1[1]);
             const float t0 = __uint_as_float(g ? p2[0] : p2[1]);
             const float v0 = __uint_as_float(g ? p3[0] : p3[1]);
-            const float c1 = g ? s1 : carry[rr][0];
-            const float c2 = g ? t0 : carry[rr][1];
-            const float c3 = g ? v0 : carry[rr][2];
+            // no voxels precede a row's first tile
+            const bool row0 = t.j == 0;
+            const float c1 = g ? s1 : (row0 ? 0.f : carry[rr][0]);
+            const float c2 = g ? t0 : (row0 ? 0.f : carry[rr][1]);
+            const float c3 = g ? v0 : (row0 ? 0.f : carry[rr][2]);
             carry[rr][0] = s1;
             carry[rr][1] = t0;
             carry[rr][2] = v0;
+            if (t.j == a.NXT - 1) {
+                // the row's last tile: outputs 32j + pad + 30 and + 31 would be
+                // completed by a next tile whose voxels lie past the row end (zero),
+                // so they are the carry terms alone (lane half 0: s1 + t0 and v0)
+                const int o1 = t.o1b + rr;
+                const int ox = t.j * 32 + a.pad[2] + 30;
+                if (g == 0 && t.store && t.o0 < a.O[0] && o1 < a.O[1]) {
+                    __amdgpu_buffer_rsrc_t yr = __builtin_amdgcn_make_buffer_rsrc(
+                        a.y + int64_t(t.nn) * a.ybatch_bytes, short(0), int(a.ybatch_bytes), 0x00020000);
+                    const uint32_t rbase = uint32_t((int64_t(t.o0) * a.O[1] + o1) * a.O[2]);
+                    const uint32_t cof = uint32_t(wc * 32 + co);
+                    if (ox >= 0 && ox < a.O[2])
+                        __builtin_amdgcn_raw_buffer_store_b16(__builtin_bit_cast(uint16_t, __bf16(s1 + t0)), yr,
+                                                              ((rbase + uint32_t(ox)) * uint32_t(a.cout) + cof) * 2u,
+                                                              0, 0);
+                    if (ox + 1 >= 0 && ox + 1 < a.O[2])
+                        __builtin_amdgcn_raw_buffer_store_b16(__builtin_bit_cast(uint16_t, __bf16(v0)), yr,
+                                                              ((rbase + uint32_t(ox + 1)) * uint32_t(a.cout) + cof) * 2u,
+                                                              0, 0);
+                }
+            }
             eo[0] = acc[rr][2][0] + c1 + c2;
             eo[1] = acc[rr][2][1] + acc[rr][1][0] + c3;
 #pragma unroll
@@ -295,7 +322,7 @@ __global__ __launch_bounds__(256, 1) void conv_fwd_xm(XmArgs a)
 #pragma unroll
             for (int it = 0; it < 2; ++it) {
                 const int v = (it * 64 + lane) >> 2, uu = lane & 3;
-                const int ox = t.j * 32 - (KW - 1) + v;
+                const int ox = t.j * 32 + a.pad[2] - (KW - 1) + v;
                 const bool ok = rowok && ox >= 0 && ox < a.O[2];
                 const uint32_t off =
                     ok ? ((rbase + uint32_t(ox)) * uint32_t(a.cout) + uint32_t(wc * 32 + uu * 8)) * 2u
@@ -438,7 +465,7 @@ hipError_t launch_xm(const Tile3& t, const Conv3& cv, const void* tile, const vo
     a.NBZ = int32_t(ceil_div(cv.O[0], C::BZ));
     a.NBY = int32_t(ceil_div(cv.O[1], C::BY));
     pick_raster(a.NBZ, a.NBY, 4, a.TZ, a.TY);
-    a.NXT = int32_t(ceil_div(cv.O[2] + C::KW - 1, 32));
+    a.NXT = int32_t(ceil_div(t.P[2], 32));
     int dev = 0, cus = 256;
     if (hipGetDevice(&dev) == hipSuccess) hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
     const int64_t rows = t.n * int64_t(a.NBZ) * a.NBY;

@@ -5,9 +5,14 @@
 //
 //  * Wave roles: each role is one (Co tile, Ci tile, kd) and owns the nine
 //    (kh, kw) taps of that plane offset as nine 32 x 32 fp32 accumulators kept in
-//    registers over all the workgroup's bricks. With fewer than four roles the
-//    spare wave repeats role 0 without storing it. All four waves issue the
-//    staging loads, in the shadow of their first MFMAs of the previous tile.
+//    registers over all the workgroup's bricks. With four roles (one wave each)
+//    every wave also issues a quarter of the staging loads, one per MFMA group.
+//    With three roles the workgroup has eight waves, two per SIMD: the two waves
+//    of a role's SIMD split the tile's K (voxels) in halves - each keeps its own
+//    accumulators, summed later with the other partials - and the fourth SIMD's
+//    two waves only issue the staging loads. A direct global->LDS load stalls its
+//    wave at issue for tens of cycles; with two MFMA waves per SIMD the other one
+//    keeps the matrix core busy meanwhile, and no compute wave issues loads.
 //  * A workgroup owns bricks of BZ x BY output rows and marches along W in
 //    32-voxel tiles. Each tile's inputs (dy rows and the BZ+KD-1 x BY+2 input rows:
 //    32 voxels in a main area, the next 4 in a halo area) are staged unchanged
@@ -18,14 +23,16 @@
 //    voxels 16g + 8s .. + 7, so a lane holds the contiguous run 16g .. 16g + 19
 //    of its channel after five reads, and the W taps are register selections:
 //    kw = 0 and 2 are dword-aligned windows, kw = 1 is one v_alignbit per dword.
-//    One row's five reads serve all three kw of both K steps.
+//    One row's five reads serve all three kw of both K steps (a wave that owns
+//    one K step reads the three that cover its 10-voxel run).
 //  * Walking the brick's output rows along H, input row y + kh serves output
 //    rows y, y - 1, y - 2: each input row is read once per plane (a ring of four
 //    register slots per plane parity), so a wave issues about nine 512-byte
-//    transposed reads per eighteen MFMAs.
+//    transposed reads per eighteen MFMAs (five per nine with one K step).
 //  * The partial of every workgroup is written once; wgrad_xm_reduce sums the
 //    partials in a fixed order (results are bitwise repeatable).
 #include <algorithm>
+#include <type_traits>
 
 #include "common.h"
 #include "internal.h"
@@ -86,27 +93,65 @@ struct WxCfg {
     static constexpr int STAGE_BYTES = X_BYTES + XH_BYTES + Y_BYTES;
     static constexpr int LDS_BYTES = 2 * STAGE_BYTES;
     static constexpr int NQ = BZ * BY;                     // output rows per tile
-    static constexpr int PART_FLOATS = 4 * 9 * 1024;       // per workgroup: [wave][tap][lane][16]
+    static constexpr int PART_FLOATS = 4 * 9 * 1024;       // per K split of a workgroup: [role][tap][lane][16]
 };
 
-template <int KD, int NCI, int NCO, int BZ, int BY>
-__global__ __launch_bounds__(256, 1) void wgrad_xm(WxArgs a)
+// KS = 1: four waves, two stage buffers, a workgroup barrier per tile.
+// KS = 2: eight waves, K split in halves between the two waves of a SIMD (three
+// roles only), NB stage buffers handed between loaders and compute waves through
+// LDS counters instead of barriers (see the flag protocol below).
+template <int KD, int NCI, int NCO, int BZ, int BY, int KS, int NB>
+__global__ __launch_bounds__(256 * KS, 1) void wgrad_xm(WxArgs a)
 {
     using C = WxCfg<KD, NCI, NCO, BZ, BY>;
     extern __shared__ uint4 lds4[];
     char* lds = reinterpret_cast<char*>(lds4);
     const int tid = threadIdx.x, lane = tid & 63;
+    // wave w runs on SIMD w % 4; ks = w / 4 is its K half (KS = 2)
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int simd = wave & 3, ks = wave >> 2;
     const uint32_t G = gridDim.x;
     const uint32_t L = uint32_t(xcd_remap(blockIdx.x, G));
     // With four roles every wave computes and issues a quarter of the staging
-    // loads; with three, wave 3 is a dedicated loader that issues them all (its
-    // stalls at issue then never hold back a matrix core).
+    // loads; with three, the waves of SIMD 3 are dedicated loaders that issue
+    // them all (their stalls at issue then never hold back a matrix core).
     static_assert(C::NR == 3 || C::NR == 4, "three or four wave roles");
+    static_assert(KS == 1 || (KS == 2 && C::NR == 3), "K split only with three roles");
     constexpr bool kLoader = C::NR == 3;
-    const int role = wave < C::NR ? wave : 0;
+    const int role = simd < C::NR ? simd : 0;
     const int kd = role % KD, cb = (role / KD) % NCI, mb = role / (KD * NCI);
     const uint32_t lds0 = lds_addr(lds);
+    static_assert(KS == 1 ? NB == 2 : (NB >= 2 && NB <= 4), "stage buffers");
+
+    // Flag protocol (KS = 2). After the NB stage buffers LDS holds two counters
+    // per buffer b: full[b], raised by each of the two loader waves once the
+    // loads of a unit it issued into b have landed, and free[b], raised by each of
+    // the six compute waves once it has read a unit out of b. Unit u lives in
+    // buffer u % NB and is that buffer's (u / NB + 1)-th fill: a compute wave
+    // starts it when full[b] >= 2 (u / NB + 1), and a loader refills b for unit u
+    // when free[b] >= 6 (u / NB). Neither wait depends on a later signal of the
+    // waiting wave's own kind, so the pipeline cannot deadlock. Every wait is also
+    // bounded: a wait that gives up (2^20 polls, far beyond any real wait) raises
+    // an abort word that ends every later wait at once, so a broken hand-off
+    // shows as wrong results and never as a hung kernel.
+    constexpr int NCW = 3 * KS;  // compute waves (KS = 2)
+    const uint32_t flag_full0 = lds0 + uint32_t(NB * C::STAGE_BYTES);
+    const uint32_t flag_free0 = flag_full0 + uint32_t(4 * NB);
+    const uint32_t flag_abort = flag_free0 + uint32_t(4 * NB);
+    if (KS == 2) {
+        if (tid < 2 * NB + 1) reinterpret_cast<uint32_t*>(lds + NB * C::STAGE_BYTES)[tid] = 0u;
+        __syncthreads();
+    }
+    auto raise = [&](uint32_t addr) {
+        if (lane == 0) lds_add_u32(addr, 1u);
+    };
+    auto spin_until = [&](uint32_t addr, uint32_t target) {
+        for (uint32_t it = 0; it < (1u << 20); ++it) {
+            if (lds_read_u32_now(addr) >= target || lds_read_u32_now(flag_abort) != 0u) return;
+            __builtin_amdgcn_s_sleep(1);
+        }
+        raise(flag_abort);
+    };
 
     // ---- staging (loader waves) ----
     // a brick's rows (bz, by) and batch item nn are decoded once per brick
@@ -153,7 +198,7 @@ __global__ __launch_bounds__(256, 1) void wgrad_xm(WxArgs a)
     // load's area and staged row are known at compile time up to the wave's bits.
     // A lane whose voxel lies outside the tile or the output, or a unit past the
     // last, loads zeros (out-of-range offset).
-    static_assert(C::X_INSTR % 4 == 0 && C::Y_INSTR % 4 == 0 && C::XH_INSTR <= 8, "load slots");
+    static_assert(kLoader || (C::X_INSTR % 4 == 0 && C::Y_INSTR % 4 == 0 && C::XH_INSTR <= 8), "load slots");
     static_assert(C::XRY % (4 / C::IPR_X) == 0 && BY % (4 / C::IPR_Y) == 0, "a slot's rows share a plane");
     constexpr int KX = C::X_INSTR / 4, KH0 = KX, KY0 = KX + 2;
     constexpr int KLOADS = KY0 + C::Y_INSTR / 4;
@@ -223,11 +268,12 @@ __global__ __launch_bounds__(256, 1) void wgrad_xm(WxArgs a)
     // rows of a tile over which the loads of the next unit are spread (the rest
     // of the tile covers their latency)
     constexpr int LOAD_ROWS = C::NQ > 4 ? C::NQ - 2 : 1;
-    static_assert((KLOADS + LOAD_ROWS - 1) / LOAD_ROWS <= 6, "at most one load per MFMA group");
+    static_assert(kLoader || (KLOADS + LOAD_ROWS - 1) / LOAD_ROWS <= 6, "at most one load per MFMA group");
 
-    // the dedicated loader issues every load of a unit (instruction index known at
-    // compile time)
-    auto loader_unit = [&](const Pos& p, int buf) {
+    // the dedicated loaders issue every load of a unit: loader LI of KS issues the
+    // instructions i with i % KS == LI (instruction index known at compile time)
+    auto loader_unit = [&](const Pos& p, int buf, auto li_c) {
+        constexpr int LI = decltype(li_c)::value;
         const bool live = p.brick < a.nbricks;
         const uint32_t nn = live ? p.nn : 0;
         const int o0 = live ? p.bz * BZ : 0, o1 = live ? p.by * BY : 0, o2 = p.j * 32;
@@ -240,7 +286,7 @@ __global__ __launch_bounds__(256, 1) void wgrad_xm(WxArgs a)
             const_cast<char*>(a.dy) + int64_t(nn) * a.dy_bytes, short(0), int(a.dy_bytes), 0x00020000);
         char* dst = lds + buf * C::STAGE_BYTES;
 #pragma unroll
-        for (int i = 0; i < C::X_INSTR; ++i) {
+        for (int i = LI; i < C::X_INSTR; i += KS) {
             const int row = i / C::IPR_X, pc = i % C::IPR_X;
             const int zr = row / C::XRY, yr = row % C::XRY;
             const bool ok = live & (uint32_t(i0 + zr) < uint32_t(a.P[0])) & (uint32_t(i1 + yr) < uint32_t(a.P[1])) &
@@ -250,7 +296,7 @@ __global__ __launch_bounds__(256, 1) void wgrad_xm(WxArgs a)
             __builtin_amdgcn_raw_ptr_buffer_load_lds(rx, SC_LDSW(dst + i * 1024), 16, ok ? u : a.tile_bytes, 0, 0, 0);
         }
 #pragma unroll
-        for (int hi = 0; hi < C::XH_INSTR; ++hi) {
+        for (int hi = LI; hi < C::XH_INSTR; hi += KS) {
             const int row = hi * HRPI + hrow;
             const int zr = row / C::XRY, yr = row % C::XRY;
             const bool ok = live & (uint32_t(i0 + zr) < uint32_t(a.P[0])) & (uint32_t(i1 + yr) < uint32_t(a.P[1])) &
@@ -260,7 +306,7 @@ __global__ __launch_bounds__(256, 1) void wgrad_xm(WxArgs a)
                                                      ok ? u : a.tile_bytes, 0, 0, 0);
         }
 #pragma unroll
-        for (int j = 0; j < C::Y_INSTR; ++j) {
+        for (int j = LI; j < C::Y_INSTR; j += KS) {
             const int row = j / C::IPR_Y, pc = j % C::IPR_Y;
             const int zb = row / BY, yb = row % BY;
             const bool ok = live & (o0 + zb < a.O[0]) & (o1 + yb < a.O[1]) & (o2 + pc * YPI + vy < a.O[2]);
@@ -270,23 +316,48 @@ __global__ __launch_bounds__(256, 1) void wgrad_xm(WxArgs a)
                                                      ok ? u : a.dy_bytes, 0, 0, 0);
         }
     };
-    if (kLoader && wave == 3) {
-        Pos cp{L, 0, 0, 0, 0, 0}, sp{L, 0, 0, 0, 0, 0};
-        seg_start(cp);
-        seg_start(sp);
-        loader_unit(sp, 0);
-        advance(sp);
-        int buf = 0;
-        while (cp.brick < a.nbricks) {
-            // this tile's loads have landed and the compute waves are done with
-            // the other buffer: fill it with the next unit
-            wait_vm_barrier<0>();
-            loader_unit(sp, buf ^ 1);
+    if (KS == 2 && simd == 3) {
+        auto run_loader = [&](auto li_c) {
+            Pos sp{L, 0, 0, 0, 0, 0};
+            seg_start(sp);
+            uint32_t u = 0;
+            int b = 0;
+            while (sp.brick < a.nbricks) {
+                if (u >= uint32_t(NB)) spin_until(flag_free0 + uint32_t(4 * b), uint32_t(NCW) * (u / NB));
+                loader_unit(sp, b, li_c);
+                asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+                raise(flag_full0 + uint32_t(4 * b));
+                advance(sp);
+                ++u;
+                b = b + 1 == NB ? 0 : b + 1;
+            }
+        };
+        if (ks == 0)
+            run_loader(std::integral_constant<int, 0>{});
+        else
+            run_loader(std::integral_constant<int, KS - 1>{});
+        return;
+    }
+    if (KS == 1 && kLoader && simd == 3) {
+        auto run_loader = [&](auto li_c) {
+            Pos cp{L, 0, 0, 0, 0, 0}, sp{L, 0, 0, 0, 0, 0};
+            seg_start(cp);
+            seg_start(sp);
+            loader_unit(sp, 0, li_c);
             advance(sp);
-            buf ^= 1;
-            advance(cp);
-        }
-        wait_vm_barrier<0>();
+            int buf = 0;
+            while (cp.brick < a.nbricks) {
+                // this tile's loads have landed and the compute waves are done
+                // with the other buffer: fill it with the next unit
+                wait_vm_barrier<0>();
+                loader_unit(sp, buf ^ 1, li_c);
+                advance(sp);
+                buf ^= 1;
+                advance(cp);
+            }
+            wait_vm_barrier<0>();
+        };
+        run_loader(std::integral_constant<int, 0>{});
         return;
     }
 
@@ -303,6 +374,14 @@ __global__ __launch_bounds__(256, 1) void wgrad_xm(WxArgs a)
     const uint32_t xl = lane_off(C::UPX, 32 * cb + 16 * gc + 4 * (gi & 3));
     const uint32_t yl = lane_off(C::UPY, 32 * mb + 16 * gc + 4 * (gi & 3));
 
+    // K steps of 16 voxels per wave and row (both, or the wave's half), and the
+    // transposed reads they need: K step s of lane half g multiplies voxels
+    // 16g + 8s .. + 7 and, shifted by kw <= 2, needs voxels up to 16g + 8s + 9,
+    // which reads 2s .. 2s + 2 cover (read 4 of lane half 1 is the halo area).
+    constexpr int SW = 2 / KS;
+    constexpr int NXR = 2 * SW + 1, NYR = 2 * SW;
+    const int s0 = KS == 2 ? ks : 0;
+
     f32x16_w acc[3][3];
 #pragma unroll
     for (int kh = 0; kh < 3; ++kh)
@@ -312,9 +391,9 @@ __global__ __launch_bounds__(256, 1) void wgrad_xm(WxArgs a)
             for (int e = 0; e < 16; ++e) acc[kh][kw][e] = 0.f;
 
     // register slots: input rows of plane parity p, row yr in slot p * 4 + yr % 4
-    uint32_t xr[8][10];
-    uint32_t xs[8][8];     // kw = 1 windows (both K steps) of the slot's row
-    uint32_t dyr[2][8];    // dy of output rows q (parity q % 2), both K steps
+    uint32_t xr[8][2 * NXR];
+    uint32_t xs[8][4 * SW];     // kw = 1 windows (the wave's K steps) of the slot's row
+    uint32_t dyr[2][4 * SW];    // dy of output rows q (parity q % 2), the wave's K steps
 
     // read 4 (voxels 16g + 16 .. + 19): lane half 0 from the main row, lane half 1
     // (voxels 32..35) from the halo area
@@ -324,26 +403,34 @@ __global__ __launch_bounds__(256, 1) void wgrad_xm(WxArgs a)
                                   ((((32 * cb + 16 * gc + 4 * (gi & 3)) >> 3) ^ wx_swz<C::UPX>(vq4)) << 4) +
                                   ((4 * (gi & 3)) & 7) * 2);
     const uint32_t xrs4 = uint32_t(gh ? C::XH_ROW : C::XROW);
+    // reads j < NXR - 1 are main-row reads 2 s0 + j; the last one is read
+    // 2 s0 + NXR - 1, which is read 4 (halo form) unless it is the first half's read 2
+    constexpr uint32_t RSTEP_X = 4 * C::UPX * 16, RSTEP_Y = 4 * C::UPY * 16;
+    const uint32_t xl_s = xl + uint32_t(2 * s0) * RSTEP_X;
+    const bool last_halo = 2 * s0 + NXR - 1 == 4;
+    const uint32_t xl_last = last_halo ? xl4 : xl_s + uint32_t(NXR - 1) * RSTEP_X;
+    const uint32_t xst_last = last_halo ? xrs4 : uint32_t(C::XROW);
+    const uint32_t yl_s = yl + uint32_t(2 * s0) * RSTEP_Y;
     auto read_x_row = [&](uint32_t xbase, int zr, int yr, int slot) {
         const int row = zr * C::XRY + yr;
-        const uint32_t base = xbase + uint32_t(row * C::XROW) + xl;
+        const uint32_t base = xbase + uint32_t(row * C::XROW) + xl_s;
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-            const uint2 d = lds_read_tr16_b64(base + uint32_t(r * 4 * C::UPX * 16));
-            xr[slot][2 * r] = d.x;
-            xr[slot][2 * r + 1] = d.y;
+        for (int j = 0; j < NXR - 1; ++j) {
+            const uint2 d = lds_read_tr16_b64(base + uint32_t(j) * RSTEP_X);
+            xr[slot][2 * j] = d.x;
+            xr[slot][2 * j + 1] = d.y;
         }
-        const uint2 d = lds_read_tr16_b64(xbase + xl4 + uint32_t(row) * xrs4);
-        xr[slot][8] = d.x;
-        xr[slot][9] = d.y;
+        const uint2 d = lds_read_tr16_b64(xbase + xl_last + uint32_t(row) * xst_last);
+        xr[slot][2 * NXR - 2] = d.x;
+        xr[slot][2 * NXR - 1] = d.y;
     };
     auto read_dy_row = [&](uint32_t ybase, int q, int slot) {
-        const uint32_t base = ybase + uint32_t(q * C::YROW) + yl;
+        const uint32_t base = ybase + uint32_t(q * C::YROW) + yl_s;
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-            const uint2 d = lds_read_tr16_b64(base + uint32_t(r * 4 * C::UPY * 16));
-            dyr[slot][2 * r] = d.x;
-            dyr[slot][2 * r + 1] = d.y;
+        for (int j = 0; j < NYR; ++j) {
+            const uint2 d = lds_read_tr16_b64(base + uint32_t(j) * RSTEP_Y);
+            dyr[slot][2 * j] = d.x;
+            dyr[slot][2 * j + 1] = d.y;
         }
     };
     // reads for output row q: its dy row and the input rows it needs first
@@ -360,36 +447,37 @@ __global__ __launch_bounds__(256, 1) void wgrad_xm(WxArgs a)
     auto ready_row = [&](int q) {
         const int zb = q / BY, yb = q % BY;
 #pragma unroll
-        for (int e = 0; e < 8; ++e) lds_ready(dyr[q & 1][e]);
+        for (int e = 0; e < 4 * SW; ++e) lds_ready(dyr[q & 1][e]);
         const int k0 = yb == 0 ? 0 : 2;
 #pragma unroll
         for (int kh = k0; kh < 3; ++kh) {
             const int slot = (zb & 1) * 4 + (yb + kh) % 4;
 #pragma unroll
-            for (int e = 0; e < 10; ++e) lds_ready(xr[slot][e]);
+            for (int e = 0; e < 2 * NXR; ++e) lds_ready(xr[slot][e]);
             // kw = 1: voxels shifted by one (the high half of dword i, the low of i + 1)
 #pragma unroll
-            for (int s = 0; s < 2; ++s)
+            for (int sl = 0; sl < SW; ++sl)
 #pragma unroll
                 for (int e = 0; e < 4; ++e)
-                    xs[slot][4 * s + e] = __builtin_amdgcn_alignbit(xr[slot][4 * s + e + 1], xr[slot][4 * s + e], 16);
+                    xs[slot][4 * sl + e] =
+                        __builtin_amdgcn_alignbit(xr[slot][4 * sl + e + 1], xr[slot][4 * sl + e], 16);
         }
     };
-    // after_group(g) runs after MFMA group g = s * 3 + kh (three MFMAs) of the row
+    // after_group(g) runs after MFMA group g = sl * 3 + kh (three MFMAs) of the row
     auto mfma_row = [&](int q, auto&& after_group) {
         const int zb = q / BY, yb = q % BY;
 #pragma unroll
-        for (int s = 0; s < 2; ++s) {
-            const uint4 av = make_uint4(dyr[q & 1][4 * s], dyr[q & 1][4 * s + 1], dyr[q & 1][4 * s + 2],
-                                        dyr[q & 1][4 * s + 3]);
+        for (int sl = 0; sl < SW; ++sl) {
+            const uint4 av = make_uint4(dyr[q & 1][4 * sl], dyr[q & 1][4 * sl + 1], dyr[q & 1][4 * sl + 2],
+                                        dyr[q & 1][4 * sl + 3]);
 #pragma unroll
             for (int kh = 0; kh < 3; ++kh) {
                 const int slot = (zb & 1) * 4 + (yb + kh) % 4;
                 const uint32_t* x = xr[slot];
-                const uint4 b0 = make_uint4(x[4 * s], x[4 * s + 1], x[4 * s + 2], x[4 * s + 3]);
-                const uint4 b1 = make_uint4(xs[slot][4 * s], xs[slot][4 * s + 1], xs[slot][4 * s + 2],
-                                            xs[slot][4 * s + 3]);
-                const uint4 b2 = make_uint4(x[4 * s + 1], x[4 * s + 2], x[4 * s + 3], x[4 * s + 4]);
+                const uint4 b0 = make_uint4(x[4 * sl], x[4 * sl + 1], x[4 * sl + 2], x[4 * sl + 3]);
+                const uint4 b1 = make_uint4(xs[slot][4 * sl], xs[slot][4 * sl + 1], xs[slot][4 * sl + 2],
+                                            xs[slot][4 * sl + 3]);
+                const uint4 b2 = make_uint4(x[4 * sl + 1], x[4 * sl + 2], x[4 * sl + 3], x[4 * sl + 4]);
                 acc[kh][0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8_w, av),
                                                                      __builtin_bit_cast(bf16x8_w, b0), acc[kh][0], 0,
                                                                      0, 0);
@@ -399,7 +487,7 @@ __global__ __launch_bounds__(256, 1) void wgrad_xm(WxArgs a)
                 acc[kh][2] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8_w, av),
                                                                      __builtin_bit_cast(bf16x8_w, b2), acc[kh][2], 0,
                                                                      0, 0);
-                after_group(s * 3 + kh);
+                after_group(sl * 3 + kh);
             }
         }
     };
@@ -414,9 +502,14 @@ __global__ __launch_bounds__(256, 1) void wgrad_xm(WxArgs a)
         advance(sp);
     }
     int buf = 0;
+    uint32_t u = 0;
     while (cp.brick < a.nbricks) {
-        // this tile's loads have landed; every wave is done with the other buffer
-        wait_vm_barrier<0>();
+        // this tile's loads have landed (and, with barriers, every wave is done
+        // with the buffer that is refilled next)
+        if (KS == 2)
+            spin_until(flag_full0 + uint32_t(4 * buf), 2u * (u / NB + 1));
+        else
+            wait_vm_barrier<0>();
         const uint32_t xbase = lds0 + uint32_t(buf * C::STAGE_BYTES);
         const uint32_t ybase = xbase + uint32_t(C::X_BYTES + C::XH_BYTES);
         if (!kLoader) {
@@ -429,7 +522,7 @@ __global__ __launch_bounds__(256, 1) void wgrad_xm(WxArgs a)
             const bool plane_break = (q + 1) % BY == 0;  // next row starts a new plane
             if (q + 1 < C::NQ && !plane_break) {
                 issue_row(xbase, ybase, q + 1);
-                lds_wait<9>();
+                lds_wait<NXR + NYR>();
             } else {
                 lds_wait<0>();
             }
@@ -443,13 +536,17 @@ __global__ __launch_bounds__(256, 1) void wgrad_xm(WxArgs a)
             });
             if (q + 1 < C::NQ && plane_break) issue_row(xbase, ybase, q + 1);
         }
-        buf ^= 1;
+        // the last row waited for all of this wave's reads of the buffer
+        if (KS == 2) raise(flag_free0 + uint32_t(4 * buf));
+        buf = buf + 1 == NB ? 0 : buf + 1;
+        ++u;
         advance(cp);
     }
-    wait_vm_barrier<0>();
+    if (KS == 1) wait_vm_barrier<0>();
     {
-        // partial: [workgroup][wave][tap kh * 3 + kw][lane][16]
-        float4* out = reinterpret_cast<float4*>(a.part + int64_t(L) * C::PART_FLOATS + int64_t(wave) * 9 * 1024);
+        // partial: [workgroup][K half][role][tap kh * 3 + kw][lane][16]
+        float4* out = reinterpret_cast<float4*>(a.part + (int64_t(L) * KS + s0) * C::PART_FLOATS +
+                                                int64_t(role) * 9 * 1024);
 #pragma unroll
         for (int kh = 0; kh < 3; ++kh)
 #pragma unroll
@@ -490,11 +587,15 @@ __global__ __launch_bounds__(256) void wgrad_xm_reduce(const float* part, float*
 
 struct WxPlan {
     bool ok;
-    int cfg;  // 0: KD 3, 32 -> 32 channels, brick 2 x 4; 1: KD 1, 64 -> 64, brick 1 x 8
+    int cfg;  // 0: KD 3, 32 -> 32 channels, brick 2 x 4, K split in halves (8 waves); 1: KD 1, 64 -> 64, brick 1 x 8
+    int ks;   // K splits per workgroup (partials per workgroup)
     WxArgs a;
     size_t lds;
     int64_t grid;
 };
+
+// Brick and stage depth of the three-role (KD = 3, 32 -> 32 channels) kernel.
+constexpr int kC3BZ = 2, kC3BY = 4, kC3NB = 2;
 
 WxPlan plan_wx(const Tile3& t, const Conv3& cv, shard_dtype_t dt)
 {
@@ -509,10 +610,12 @@ WxPlan plan_wx(const Tile3& t, const Conv3& cv, shard_dtype_t dt)
     int bz, by;
     if (cv.K[0] == 3 && t.c == 32 && cv.cout == 32) {
         p.cfg = 0;
-        bz = 2, by = 4;
-        p.lds = WxCfg<3, 1, 1, 2, 4>::LDS_BYTES;
+        p.ks = 2;
+        bz = kC3BZ, by = kC3BY;
+        p.lds = 0;
     } else if (cv.K[0] == 1 && t.c == 64 && cv.cout == 64) {
         p.cfg = 1;
+        p.ks = 1;
         bz = 1, by = 8;
         p.lds = WxCfg<1, 2, 2, 1, 8>::LDS_BYTES;
     } else {
@@ -551,21 +654,23 @@ WxPlan plan_wx(const Tile3& t, const Conv3& cv, shard_dtype_t dt)
     return p;
 }
 
-template <int KD, int NCI, int NCO, int BZ, int BY>
+template <int KD, int NCI, int NCO, int BZ, int BY, int KS, int NB>
 hipError_t run_wx(const WxPlan& p, float* dw, hipStream_t s)
 {
     using C = WxCfg<KD, NCI, NCO, BZ, BY>;
-    auto fn = &wgrad_xm<KD, NCI, NCO, BZ, BY>;
+    constexpr int LDS = NB * C::STAGE_BYTES + (KS == 2 ? 8 * NB + 16 : 0);
+    static_assert(LDS <= 160 * 1024, "LDS budget");
+    auto fn = &wgrad_xm<KD, NCI, NCO, BZ, BY, KS, NB>;
     hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(fn), hipFuncAttributeMaxDynamicSharedMemorySize,
-                                       int(C::LDS_BYTES));
+                                       LDS);
     if (e != hipSuccess) return e;
     WxArgs a = p.a;
     void* args[] = {&a};
-    e = hipLaunchKernel(reinterpret_cast<const void*>(fn), dim3(unsigned(p.grid)), dim3(256), args, C::LDS_BYTES, s);
+    e = hipLaunchKernel(reinterpret_cast<const void*>(fn), dim3(unsigned(p.grid)), dim3(256 * KS), args, LDS, s);
     if (e != hipSuccess) return e;
     const int total = C::NR * 9 * 1024;
     hipLaunchKernelGGL((wgrad_xm_reduce<KD, NCI, NCO>), dim3(unsigned(ceil_div(total, 256))), dim3(256), 0, s,
-                       p.a.part, dw, int(p.grid));
+                       p.a.part, dw, int(p.grid * KS));
     return hipGetLastError();
 }
 
@@ -574,7 +679,7 @@ hipError_t run_wx(const WxPlan& p, float* dw, hipStream_t s)
 size_t wgrad_xm_workspace(const Tile3& t, const Conv3& cv, shard_dtype_t dt)
 {
     const WxPlan p = plan_wx(t, cv, dt);
-    return p.ok ? size_t(p.grid) * 4 * 9 * 1024 * sizeof(float) : 0;
+    return p.ok ? size_t(p.grid) * size_t(p.ks) * 4 * 9 * 1024 * sizeof(float) : 0;
 }
 
 // The W-march weight gradient applies to bf16, unit stride, 3 x 3 taps in H and
@@ -591,7 +696,7 @@ hipError_t launch_wgrad_xm(const Tile3& t, const Conv3& cv, shard_dtype_t dt, co
     p.a.tile = static_cast<const char*>(tile);
     p.a.dy = static_cast<const char*>(dy);
     p.a.part = static_cast<float*>(ws);
-    return p.cfg == 0 ? run_wx<3, 1, 1, 2, 4>(p, dw, s) : run_wx<1, 2, 2, 1, 8>(p, dw, s);
+    return p.cfg == 0 ? run_wx<3, 1, 1, kC3BZ, kC3BY, 2, kC3NB>(p, dw, s) : run_wx<1, 2, 2, 1, 8, 1, 2>(p, dw, s);
 }
 
 }  // namespace shardconv
