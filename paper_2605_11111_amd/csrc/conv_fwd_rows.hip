@@ -393,37 +393,66 @@ __global__ __launch_bounds__(256, 1) void conv_fwd_xm(XmArgs a)
         // step s multiplies
         const uint32_t boff = uint32_t(cbuf * C::STAGE_BYTES);
         constexpr int S = R * NG;
-        lds_u32x4 av[2][KH];
-        auto load_step = [&](int st, lds_u32x4 (&A)[KH]) {
+        // Step s = (row r, group q = (kd, kc)) multiplies input rows r .. r + KH - 1
+        // of plane kd. Rows r + 1 .. r + KH - 1 are also the first KH - 1 rows of
+        // row r + 1's step in the same group, so they stay in registers (cache[q])
+        // and that step reads only its last row: R * KH reads per group become
+        // KH + R - 1. Reads of step s + 1 go out while step s multiplies.
+        lds_u32x4 fresh[2][KH];
+        lds_u32x4 cache[NG][KH - 1];
+        auto reads_of = [](int st) { return st / NG == 0 ? KH : 1; };
+        auto load_step = [&](int st, lds_u32x4 (&F)[KH]) {
             const int r = st / NG, q = st % NG;
             const int kd = q / C::NKC, kc = q % C::NKC;
+            if (r == 0) {
 #pragma unroll
-            for (int kh = 0; kh < KH; ++kh)
-                A[kh] = lds_read_b128(abase[kc] + boff + uint32_t((kd * C::IRY + r + kh) * C::ROW_BYTES));
+                for (int kh = 0; kh < KH; ++kh)
+                    F[kh] = lds_read_b128(abase[kc] + boff + uint32_t((kd * C::IRY + kh) * C::ROW_BYTES));
+            } else {
+                F[0] = lds_read_b128(abase[kc] + boff + uint32_t((kd * C::IRY + r + KH - 1) * C::ROW_BYTES));
+            }
         };
-        load_step(0, av[0]);
+        load_step(0, fresh[0]);
 #pragma unroll
         for (int st = 0; st < S; ++st) {
             const int cur_b = st & 1;
             const int r = st / NG, q = st % NG;
             const int kd = q / C::NKC, kc = q % C::NKC;
             if (st + 1 < S) {
-                load_step(st + 1, av[cur_b ^ 1]);
-                lds_wait<KH>();
+                load_step(st + 1, fresh[cur_b ^ 1]);
+                if (reads_of(st + 1) == KH)
+                    lds_wait<KH>();
+                else
+                    lds_wait<1>();
             } else {
                 lds_wait<0>();
             }
+            lds_u32x4 A[KH];
 #pragma unroll
-            for (int kh = 0; kh < KH; ++kh) lds_ready(av[cur_b][kh]);
+            for (int kh = 0; kh < KH; ++kh) {
+                if (r == 0) {
+                    lds_ready(fresh[cur_b][kh]);
+                    A[kh] = fresh[cur_b][kh];
+                } else if (kh == KH - 1) {
+                    lds_ready(fresh[cur_b][0]);
+                    A[kh] = fresh[cur_b][0];
+                } else {
+                    A[kh] = cache[q][kh];
+                }
+            }
 #pragma unroll
             for (int kh = 0; kh < KH; ++kh)
 #pragma unroll
                 for (int kw = 0; kw < KW; ++kw) {
                     const f32x16_r c0 = (q == 0 && kh == 0) ? f32x16_r{} : acc[r][kw];
                     acc[r][kw] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-                        __builtin_bit_cast(bf16x8_r, av[cur_b][kh]),
-                        __builtin_bit_cast(bf16x8_r, wv[kd][kh][kw][kc]), c0, 0, 0, 0);
+                        __builtin_bit_cast(bf16x8_r, A[kh]), __builtin_bit_cast(bf16x8_r, wv[kd][kh][kw][kc]), c0,
+                        0, 0, 0);
                 }
+            if (r + 1 < R) {
+#pragma unroll
+                for (int kh = 0; kh + 1 < KH; ++kh) cache[q][kh] = A[kh + 1];
+            }
             // the pending row: R - 1 of the previous tile while row 0 multiplies,
             // else row r - 1 of this tile
             if (r == 0)
