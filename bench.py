@@ -8,6 +8,11 @@ itself; the CPU oracle is used only by the cpu_baseline leg. Prints ONE JSON
 line on stdout (progress goes to stderr).
 
     python bench.py [--steps K] [--warmup W] [--workload c3] [--no-cpu-baseline] [--copy-calibration]
+                    [--no-backward]
+
+The backward-pass ops of the same shard (input gradient onto the padded tile,
+reverse halo) are timed after the step and reported under "backward_ops"; they
+are not part of `value`.
 
 The roofline's "traffic" field is the HBM traffic of the dominant kernel measured
 with rocprofv3 counters (FETCH_SIZE and WRITE_SIZE, each scaled by what it reads
@@ -86,6 +91,8 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="run one 64 MiB device-to-device copy first (reference for counter scaling)")
+    ap.add_argument("--no-backward", action="store_true",
+                    help="skip the backward-pass ops (input gradient, reverse halo), timed after the step")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU's shard; --gpus {args.gpus} is not supported: this build has no "
@@ -199,6 +206,8 @@ def main():
                                                      for k in range(args.steps)])))
     log("timed region done")
 
+    backward = None if args.no_backward else time_backward(sc, w, g, desc, wt, dy, send, flops, args, stream)
+
     dt = w.dtype
     value = 2 * flops / (ms_step * 1e-3) / 1e12
     detail = {}
@@ -226,9 +235,66 @@ def main():
                    "tile_padded": [w.N] + [l + e + h for l, e, h in zip(lo, ext, hi)] + [w.cin],
                    "out": [w.N] + list(O) + [w.cout], "kernel": list(w.K), "stride": list(w.S),
                    "accumulate": "f32"},
-        "ops": detail, "roofline": roofline, "cpu_baseline": cpu,
+        "ops": detail, "roofline": roofline, "cpu_baseline": cpu, "backward_ops": backward,
     }
     print(json.dumps(line), flush=True)
+
+
+def time_backward(sc, w, g, desc, wt, dy, send, flops, args, stream):
+    """The backward-pass ops of the same shard, timed after the step (they are not
+    part of `value`): the input gradient onto the padded tile, then the reverse
+    halo - each margin's gradient packed for the neighbour it came from, and a
+    received gradient slab added onto each interior face (the slabs the forward
+    pack filled stand in for the neighbours' gradients: same shapes)."""
+    import numpy as np
+    import torch
+    tdt = torch.float32 if w.dtype == "f32" else torch.bfloat16
+    code = sc.SHARD_F32 if w.dtype == "f32" else sc.SHARD_BF16
+    O = g["out_ext"]
+    P = [l + e + h for l, e, h in zip(g["halo_lo"], g["ext"], g["halo_hi"])]
+    dtile = torch.empty([w.N] + P + [w.cin], dtype=tdt, device="cuda")
+    wsd = torch.empty(max(16, sc.shard_conv_workspace_bytes(2, desc, code, w.cout, w.K, w.S, O)),
+                      dtype=torch.uint8, device="cuda")
+    ops = [("conv_dgrad", "dgrad", flops,
+            lambda: sc.shard_conv_dgrad(desc, dy, wt, w.cout, w.K, w.S, g["pad_lo"], O, dtile, wsd))]
+    for axis in range(w.nd):
+        for side in (0, 1):
+            width = g["halo_lo"][axis] if side == 0 else g["halo_hi"][axis]
+            if width > 0 and w.neighbour_exists(w.shard, axis, side):
+                buf = torch.empty(sc.shard_halo_slab_shape(desc, axis, width), dtype=tdt, device="cuda")
+                nbytes = buf.numel() * buf.element_size()
+                ops.append((f"pack_margin_a{axis}s{side}", "halo", 2 * nbytes,
+                            lambda axis=axis, side=side, buf=buf: sc.shard_halo_pack_margin(desc, dtile, axis, side,
+                                                                                            buf)))
+    for (axis, side, nwidth, buf, nbytes) in send:
+        # read slab + read and write the face rows
+        ops.append((f"accumulate_a{axis}s{side}", "halo", 3 * nbytes,
+                    lambda axis=axis, side=side, nwidth=nwidth, buf=buf:
+                    sc.shard_halo_accumulate(desc, dtile, axis, side, nwidth, buf)))
+    for _ in range(args.warmup):
+        for op in ops:
+            op[3]()
+    torch.cuda.synchronize()
+    ev = [[[torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)] for _ in ops]
+          for _ in range(args.steps)]
+    for k in range(args.steps):
+        for i, op in enumerate(ops):
+            ev[k][i][0].record(stream)
+            op[3]()
+            ev[k][i][1].record(stream)
+    torch.cuda.synchronize()
+    out = {}
+    for i, (label, kind, work, _) in enumerate(ops):
+        ms = float(np.mean([ev[k][i][0].elapsed_time(ev[k][i][1]) for k in range(args.steps)]))
+        if kind == "dgrad":
+            tf = work / (ms * 1e-3) / 1e12
+            out[label] = {"ms": round(ms, 4), "tflops": round(tf, 2), "frac_mfma_peak": round(tf / PEAK[w.dtype], 4)}
+        else:
+            gbs = work / (ms * 1e-3) / 1e9
+            out[label] = {"ms": round(ms, 4), "gbs": round(gbs, 1), "frac_hbm_peak": round(gbs / HBM_PEAK, 4),
+                          "bytes": int(work)}
+    log("backward ops timed")
+    return out
 
 
 def source_hash():

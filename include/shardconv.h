@@ -17,6 +17,9 @@
  *   shard_halo_unpack     copy a received slab into a margin, or zero-fill it
  *   shard_conv_fwd        convolution read off the padded tile
  *   shard_conv_wgrad      the shard's partial weight gradient
+ *   shard_conv_dgrad      the input gradient read back onto the padded tile
+ *   shard_halo_pack_margin, shard_halo_accumulate
+ *                         the reverse halo exchange of the backward pass
  *
  * Convolution semantics are PyTorch's cross-correlation (no bias, dilation 1,
  * groups 1), which the paper's programming model keeps (section "Benchmarks
@@ -176,9 +179,64 @@ shard_status_t shard_conv_wgrad(const shard_tile_t* x, shard_dtype_t dtype, cons
                                 size_t ws_bytes, hipStream_t stream);
 
 /*
- * Workspace bytes shard_conv_fwd (op 0) or shard_conv_wgrad (op 1) needs for
- * these arguments. A pure function of its arguments (the launch plan does not
- * depend on the device); host only. Returns (size_t)-1 for malformed arguments.
+ * Input gradient read back onto the padded tile (the backward pass of the
+ * shard's convolution; the convolution analogue of the input gradient
+ * dL/dx = dL/dz W that the paper writes for a Linear layer, section "What
+ * Causes High GPU Memory Usage?", subsection "An Example of Memory Usage"):
+ *   dtile[n][p][ci] = sum over co, taps t and outputs j with j*S + t - pad_lo = p
+ *                     of w[co][ci][t] * dy[n][j][co]
+ * per axis, for every row p of the padded tile, margins included (same tile
+ * reading rule as shard_conv_fwd; taps that fall outside the tile drop out).
+ * The margin rows then hold gradient that belongs to the neighbours' interiors:
+ * shard_halo_pack_margin / shard_halo_accumulate return it, in descending axis
+ * order, after which the interior equals the shard's slice of the full-domain
+ * input gradient.
+ *   x      descriptor of the padded tile (its c is the input channel count Ci)
+ *   dy     [n][out_ext0][out_ext1][out_ext2][c_out], dtype
+ *   w      [c_out][x->c][kernel0][kernel1][kernel2], dtype (the forward weights)
+ *   dtile  the padded tile layout, dtype, every element overwritten (bf16 is
+ *          rounded to nearest-even from the binary32 sum; no owned outputs
+ *          gives zeros)
+ *   ws     device workspace of at least shard_conv_workspace_bytes(2, ...) bytes.
+ * Errors: as shard_conv_fwd.
+ */
+shard_status_t shard_conv_dgrad(const shard_tile_t* x, shard_dtype_t dtype, const void* dy, const void* w,
+                                int64_t c_out, const int64_t kernel[], const int64_t stride[],
+                                const int64_t pad_lo[], const int64_t out_ext[], void* dtile, void* ws,
+                                size_t ws_bytes, hipStream_t stream);
+
+/*
+ * Reverse halo, sending half: copy the margin on (axis, side) of a tile holding
+ * a gradient (the box shard_halo_unpack writes) into the dense slab
+ * (shape shard_halo_slab_shape(x, axis, margin width)), to be returned to the
+ * neighbour the margin came from. The halo exchange copies a neighbour's rows
+ * into the margin (section "PyTorch Dispatch"); its derivative adds the
+ * margin's gradient back onto those rows. Bit-exact copy; a zero-width margin
+ * is a no-op. Errors: SHARD_ERR_INVALID (bad descriptor, dtype, axis, side,
+ * null pointer).
+ */
+shard_status_t shard_halo_pack_margin(const shard_tile_t* x, shard_dtype_t dtype, const void* tile, int32_t axis,
+                                      int32_t side, void* slab, hipStream_t stream);
+
+/*
+ * Reverse halo, receiving half: add the slab to the `width` interior rows on
+ * (axis, side) (the box shard_halo_pack reads for that width), element-wise:
+ * each sum is formed in binary32 and, for SHARD_BF16, rounded to nearest-even.
+ * `width` is the neighbour's margin on the facing side. Axes are returned in
+ * descending order (the forward exchange runs ascending), so the slabs of later
+ * axes carry the corner gradients into earlier axes' margins, which the earlier
+ * axes then return. width == 0 is a no-op.
+ * Errors: SHARD_ERR_INVALID (bad descriptor, dtype, axis, side, width < 0, null
+ * pointer); SHARD_ERR_UNSUPPORTED when width > ext[axis].
+ */
+shard_status_t shard_halo_accumulate(const shard_tile_t* x, shard_dtype_t dtype, void* tile, int32_t axis,
+                                     int32_t side, int64_t width, const void* slab, hipStream_t stream);
+
+/*
+ * Workspace bytes shard_conv_fwd (op 0), shard_conv_wgrad (op 1) or
+ * shard_conv_dgrad (op 2) needs for these arguments. A pure function of its
+ * arguments (the launch plan does not depend on the device); host only.
+ * Returns (size_t)-1 for malformed arguments.
  */
 size_t shard_conv_workspace_bytes(int32_t op, const shard_tile_t* x, shard_dtype_t dtype, int64_t c_out,
                                   const int64_t kernel[], const int64_t stride[], const int64_t out_ext[]);

@@ -56,6 +56,27 @@ def wgrad_scalar(x, dy, kernel, stride, out_lo, out_hi):
     return dw
 
 
+def dgrad_scalar(dy, w, G, stride):
+    """dx[n][ci][i] = sum over co, t and outputs j with j*S - P + t = i of
+    w[co][ci][t] * dy[n][co][j]: every (output, tap) pair adds its term to the
+    input it was read from, inputs outside the domain dropped."""
+    N, Co = dy.shape[:2]
+    Ci = w.shape[1]
+    K = w.shape[2:]
+    nd = len(G)
+    n_out = dy.shape[2:]
+    dx = np.zeros([N, Ci] + list(G))
+    for n in range(N):
+        for co in range(Co):
+            for j in itertools.product(*[range(m) for m in n_out]):
+                for t in itertools.product(*[range(k) for k in K]):
+                    src = [j[a] * stride[a] - (K[a] - 1) // 2 + t[a] for a in range(nd)]
+                    if all(0 <= src[a] < G[a] for a in range(nd)):
+                        for ci in range(Ci):
+                            dx[(n, ci) + tuple(src)] += float(w[(co, ci) + t]) * float(dy[(n, co) + j])
+    return dx
+
+
 def toeplitz(w, G, stride):
     """Dense matrix T with vec(y[n]) = T @ vec(x[n]) for one batch item, built entry
     by entry: T[(co, j), (ci, i)] = w[co, ci, i - j*S + P] when that tap exists."""

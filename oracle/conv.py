@@ -150,6 +150,73 @@ def conv_wgrad(x, dy, kernel, stride, out_lo=None, out_hi=None) -> np.ndarray:
     return conv_wgrad_window(xw, origin, G, dy, kernel, stride, out_lo, out_hi)
 
 
+def conv_dgrad(dy, w, G, stride) -> np.ndarray:
+    """Full-domain input gradient: the derivative of sum(dy * conv_forward(x, w))
+    with respect to x over the domain [0, G),
+
+        dx[n, ci, i] = sum over co, t and outputs j with j*S - P + t = i of
+                       w[co, ci, t] * dy[n, co, j]
+
+    (the convolution analogue of dL/dx = dL/dz W for a Linear layer, section
+    "What Causes High GPU Memory Usage?", subsection "An Example of Memory
+    Usage"). dy covers the whole output. Written as a scatter: for every tap the
+    outputs' contributions are added to the input rows they were read from;
+    rows that fall in the zero padding are dropped."""
+    dy = np.asarray(dy, dtype=np.float64)
+    nd = len(G)
+    kernel = w.shape[2:]
+    n_out = [out_len(G[a], kernel[a], stride[a]) for a in range(nd)]
+    if list(dy.shape[2:]) != n_out or dy.shape[1] != w.shape[0]:
+        raise ValueError("dy does not match the full output")
+    P = [(k - 1) // 2 for k in kernel]
+    # accumulate into the zero-extended domain [-P, G + P), then cut the domain
+    ext = [G[a] + 2 * P[a] for a in range(nd)]
+    dxe = np.zeros([dy.shape[0], w.shape[1]] + ext)
+    if dy.size == 0:
+        return dxe[(slice(None), slice(None)) + tuple(slice(P[a], P[a] + G[a]) for a in range(nd))]
+    for tap in itertools.product(*[range(k) for k in kernel]):
+        wt = w[(slice(None), slice(None)) + tap]                              # [Co, Ci]
+        contrib = np.moveaxis(np.tensordot(wt, dy, axes=([0], [1])), 0, 1)   # [N, Ci, *out]
+        sl = [slice(None), slice(None)]
+        for a in range(nd):
+            # output j reads extended row j*S + t
+            sl.append(slice(tap[a], tap[a] + (n_out[a] - 1) * stride[a] + 1, stride[a]))
+        dxe[tuple(sl)] += contrib
+    return dxe[(slice(None), slice(None)) + tuple(slice(P[a], P[a] + G[a]) for a in range(nd))]
+
+
+def tile_dgrad(dy, w, stride, pad_lo, tile_ext) -> np.ndarray:
+    """Input gradient read back onto a padded tile: the adjoint of ``tile_conv``.
+    Output jj, tap t read tile row jj*S + t - pad_lo along each axis; its
+    contribution w[co, ci, t] * dy[jj] is added to that row when the row lies in
+    [0, tile_ext) and dropped otherwise (zero padding outside the tile). The
+    result covers every tile row, margins included: the margin rows hold the
+    gradient that belongs to the neighbours' interiors."""
+    dy = np.asarray(dy, dtype=np.float64)
+    nd = dy.ndim - 2
+    kernel = w.shape[2:]
+    out_ext = dy.shape[2:]
+    dt = np.zeros([dy.shape[0], w.shape[1]] + list(tile_ext))
+    if dy.size == 0:
+        return dt
+    for tap in itertools.product(*[range(k) for k in kernel]):
+        wt = w[(slice(None), slice(None)) + tap]
+        contrib = np.moveaxis(np.tensordot(wt, dy, axes=([0], [1])), 0, 1)  # [N, Ci, *out]
+        src, dst = [slice(None), slice(None)], [slice(None), slice(None)]
+        empty = False
+        for a in range(nd):
+            rows = np.arange(out_ext[a]) * stride[a] + tap[a] - pad_lo[a]
+            ok = np.nonzero((rows >= 0) & (rows < tile_ext[a]))[0]
+            if ok.size == 0:
+                empty = True
+                break
+            src.append(slice(ok[0], ok[-1] + 1))
+            dst.append(slice(rows[ok[0]], rows[ok[-1]] + 1, stride[a]))
+        if not empty:
+            dt[tuple(dst)] += contrib[tuple(src)]
+    return dt
+
+
 def shard_input_box(geom: dict, shard_off, shard_ext, global_ext) -> tuple:
     """Spatial box of the shard's padded tile: [o - halo_lo, o + L + halo_hi) on
     sharded axes (margins outside the domain are zero padding), the whole axis

@@ -90,3 +90,34 @@ def slab_shape(n, c, axis, width, halo_lo, ext, halo_hi):
             s0, s1 = _span(a, axis, halo_lo, ext, halo_hi)
             shp.append(s1 - s0)
     return shp
+
+
+# --- the reverse exchange of the backward pass -----------------------------
+#
+# The halo exchange copies a neighbour's interior rows into a shard's margin;
+# its derivative (the reading taken here of how gradients flow back through the
+# exchange) adds the gradient that lands on a margin back onto the rows it was
+# copied from. With the forward exchange in ascending axis order, the reverse
+# runs in descending axis order over the same boxes: a shard sends the gradient
+# on its margin (the box ``unpack`` wrote) and the neighbour adds the slab into
+# the interior face rows (the box ``pack`` read), which on later axes span the
+# padded extent of earlier axes and so carry the corner gradients onward.
+
+
+def pack_margin(tile, axis, side, halo_lo, ext, halo_hi) -> np.ndarray:
+    """Slab holding the gradient on the margin (axis, side), sent to the
+    neighbour it came from."""
+    lo, hi = face_box(axis, margin_rows(axis, side, halo_lo, ext, halo_hi), halo_lo, ext, halo_hi)
+    return np.array(_cut(tile, lo, hi), copy=True)
+
+
+def accumulate(tile, axis, side, width, slab, halo_lo, ext, halo_hi, rounding=None) -> np.ndarray:
+    """Copy of ``tile`` with ``slab`` added to the ``width`` interior face rows on
+    (axis, side) - the rows ``pack`` sends. ``rounding`` maps the float64 sum to
+    the stored values (None: exact)."""
+    lo, hi = face_box(axis, pack_rows(axis, side, width, halo_lo, ext), halo_lo, ext, halo_hi)
+    out = np.array(tile, dtype=np.float64, copy=True)
+    sl = (slice(None), slice(None)) + tuple(slice(l, h) for l, h in zip(lo, hi))
+    s = out[sl] + np.asarray(slab, dtype=np.float64)
+    out[sl] = s if rounding is None else rounding(s)
+    return out

@@ -236,15 +236,48 @@ shard_status_t shard_halo_unpack(const shard_tile_t* x, shard_dtype_t dtype, voi
     return map_hip(launch_box_copy(b, SLAB_TO_TILE, slab, tile, stream));
 }
 
+shard_status_t shard_halo_pack_margin(const shard_tile_t* x, shard_dtype_t dtype, const void* tile, int32_t axis,
+                                      int32_t side, void* slab, hipStream_t stream)
+{
+    Tile3 t;
+    if (!norm_tile(x, dtype, t) || axis < 0 || axis >= x->ndim || (side != 0 && side != 1))
+        return SHARD_ERR_INVALID;
+    const int k = 3 - x->ndim + axis;
+    const int64_t r0 = side == 0 ? 0 : t.lo[k] + t.ext[k];
+    const int64_t r1 = side == 0 ? t.lo[k] : t.P[k];
+    int64_t start[3], cnt[3];
+    slab_spans(t, k, r0, r1, start, cnt);
+    if (t.n * cnt[0] * cnt[1] * cnt[2] == 0) return SHARD_OK;
+    if (!tile || !slab || !aligned(tile, t.esz) || !aligned(slab, t.esz)) return SHARD_ERR_INVALID;
+    return map_hip(launch_box_copy(make_box(t, k, r0, r1), TILE_TO_SLAB, tile, slab, stream));
+}
+
+shard_status_t shard_halo_accumulate(const shard_tile_t* x, shard_dtype_t dtype, void* tile, int32_t axis,
+                                     int32_t side, int64_t width, const void* slab, hipStream_t stream)
+{
+    Tile3 t;
+    if (!norm_tile(x, dtype, t) || axis < 0 || axis >= x->ndim || (side != 0 && side != 1) || width < 0)
+        return SHARD_ERR_INVALID;
+    const int k = 3 - x->ndim + axis;
+    if (width > t.ext[k]) return SHARD_ERR_UNSUPPORTED;
+    const int64_t r0 = side == 0 ? t.lo[k] : t.lo[k] + t.ext[k] - width;
+    int64_t start[3], cnt[3];
+    slab_spans(t, k, r0, r0 + width, start, cnt);
+    if (t.n * cnt[0] * cnt[1] * cnt[2] == 0) return SHARD_OK;
+    if (!tile || !slab || !aligned(tile, t.esz) || !aligned(slab, t.esz)) return SHARD_ERR_INVALID;
+    return map_hip(launch_box_add(make_box(t, k, r0, r0 + width), t.esz, slab, tile, stream));
+}
+
 size_t shard_conv_workspace_bytes(int32_t op, const shard_tile_t* x, shard_dtype_t dtype, int64_t c_out,
                                   const int64_t kernel[], const int64_t stride[], const int64_t out_ext[])
 {
     Tile3 t;
     Conv3 cv;
-    if ((op != 0 && op != 1) || !norm_tile(x, dtype, t) || !norm_conv(x, t, c_out, kernel, stride, nullptr, out_ext, cv))
+    if (op < 0 || op > 2 || !norm_tile(x, dtype, t) || !norm_conv(x, t, c_out, kernel, stride, nullptr, out_ext, cv))
         return size_t(-1);
     if (op == 0) return conv_fwd_workspace(t, cv, dtype);
-    return conv_wgrad_workspace(t, cv, dtype);
+    if (op == 1) return conv_wgrad_workspace(t, cv, dtype);
+    return conv_dgrad_workspace(t, cv, dtype);
 }
 
 shard_status_t shard_conv_fwd(const shard_tile_t* x, shard_dtype_t dtype, const void* tile, const void* w,
@@ -280,6 +313,34 @@ shard_status_t shard_conv_wgrad(const shard_tile_t* x, shard_dtype_t dtype, cons
     if (!aligned(tile, t.esz) || !aligned(dy, t.esz)) return SHARD_ERR_INVALID;
     if (empty) return map_hip(generic_conv_wgrad(t, cv, dtype, tile, dy, dw, ws, stream));
     return map_hip(launch_conv_wgrad(t, cv, dtype, tile, dy, dw, ws, stream));
+}
+
+shard_status_t shard_conv_dgrad(const shard_tile_t* x, shard_dtype_t dtype, const void* dy, const void* w,
+                                int64_t c_out, const int64_t kernel[], const int64_t stride[], const int64_t pad_lo[],
+                                const int64_t out_ext[], void* dtile, void* ws, size_t ws_bytes, hipStream_t stream)
+{
+    Tile3 t;
+    Conv3 cv;
+    if (!norm_tile(x, dtype, t) || !pad_lo || !norm_conv(x, t, c_out, kernel, stride, pad_lo, out_ext, cv))
+        return SHARD_ERR_INVALID;
+    if (tile_elems(t) == 0) return SHARD_OK;
+    const size_t need = conv_dgrad_workspace(t, cv, dtype);
+    if (ws_bytes < need || (need > 0 && !ws)) return SHARD_ERR_INVALID;
+    if (!dtile || !w || !aligned(dtile, t.esz) || !aligned(w, t.esz) || !aligned(dy, t.esz) || !aligned(ws, 16))
+        return SHARD_ERR_INVALID;
+    if (t.n * cv.out_voxels() == 0) {
+        // no owned outputs: the tile's gradient is zero
+        BoxCopy b{};
+        b.base = 0;
+        b.run = tile_elems(t) * t.esz;
+        for (int i = 0; i < 3; ++i) {
+            b.cnt[i] = 1;
+            b.tstride[i] = 0;
+        }
+        return map_hip(launch_box_copy(b, ZERO_TILE, nullptr, dtile, stream));
+    }
+    if (!dy) return SHARD_ERR_INVALID;
+    return map_hip(launch_conv_dgrad(t, cv, dtype, dy, w, dtile, ws, stream));
 }
 
 }  // extern "C"

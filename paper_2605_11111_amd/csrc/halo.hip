@@ -13,6 +13,7 @@
 // specialisation with no index arithmetic.
 #include <algorithm>
 
+#include "common.h"
 #include "internal.h"
 
 namespace shardconv {
@@ -124,7 +125,94 @@ hipError_t launch_v(const BoxCopy& b, CopyDir dir, const void* src, void* dst, h
     return hipLaunchKernel(fn, dim3(unsigned(blocks)), dim3(kThreads), args, 0, s);
 }
 
+// tile[box] += slab, element-wise in binary32 (bf16 sums rounded to nearest
+// even): the receiving half of the reverse halo exchange.
+template <int V, typename E, bool kSingleRun>
+__global__ __launch_bounds__(kThreads) void box_add_kernel(CopyArgs a)
+{
+    using T = typename Vec<V>::T;
+    constexpr int kUnroll = Vec<V>::U;
+    constexpr int NE = V / int(sizeof(E));
+    const int64_t nthreads = int64_t(gridDim.x) * kThreads;
+    const int64_t tid = int64_t(blockIdx.x) * kThreads + threadIdx.x;
+    for (int64_t v0 = tid; v0 < a.total; v0 += nthreads * kUnroll) {
+        T sv[kUnroll], tv[kUnroll];
+        int64_t off[kUnroll];
+#pragma unroll
+        for (int u = 0; u < kUnroll; ++u) {
+            const int64_t v = v0 + u * nthreads;
+            off[u] = v < a.total ? tile_offset<V, kSingleRun>(a, v) : 0;
+            if (v < a.total) {
+                sv[u] = __builtin_nontemporal_load(reinterpret_cast<const T*>(a.src + v * V));
+                tv[u] = *reinterpret_cast<const T*>(a.dst + off[u]);
+            }
+        }
+#pragma unroll
+        for (int u = 0; u < kUnroll; ++u) {
+            const int64_t v = v0 + u * nthreads;
+            if (v < a.total) {
+                E es[NE], et[NE];
+                __builtin_memcpy(es, &sv[u], V);
+                __builtin_memcpy(et, &tv[u], V);
+#pragma unroll
+                for (int i = 0; i < NE; ++i) et[i] = from_f32<E>(to_f32(et[i]) + to_f32(es[i]));
+                T r;
+                __builtin_memcpy(&r, et, V);
+                *reinterpret_cast<T*>(a.dst + off[u]) = r;
+            }
+        }
+    }
+}
+
+template <int V>
+CopyArgs copy_args(const BoxCopy& b, CopyDir dir, const void* src, void* dst, int64_t& blocks, int64_t& rows)
+{
+    CopyArgs a;
+    a.src = static_cast<const char*>(src);
+    a.dst = static_cast<char*>(dst);
+    a.base = b.base;
+    a.cnt1 = b.cnt[1];
+    a.cnt2 = b.cnt[2];
+    a.t0 = b.tstride[0];
+    a.t1 = b.tstride[1];
+    a.t2 = b.tstride[2];
+    a.nvec_row = b.run / V;
+    rows = b.cnt[0] * b.cnt[1] * b.cnt[2];
+    a.total = rows * a.nvec_row;
+    a.dir = dir;
+    const int64_t per_block = int64_t(kThreads) * Vec<V>::U;
+    blocks = std::max<int64_t>(1, std::min<int64_t>(ceil_div(a.total, per_block), 1 << 20));
+    return a;
+}
+
+template <int V, typename E>
+hipError_t launch_add_v(const BoxCopy& b, const void* slab, void* tile, hipStream_t s)
+{
+    int64_t blocks, rows;
+    CopyArgs a = copy_args<V>(b, SLAB_TO_TILE, slab, tile, blocks, rows);
+    void* args[] = {&a};
+    const void* fn = rows == 1 ? reinterpret_cast<const void*>(&box_add_kernel<V, E, true>)
+                               : reinterpret_cast<const void*>(&box_add_kernel<V, E, false>);
+    return hipLaunchKernel(fn, dim3(unsigned(blocks)), dim3(kThreads), args, 0, s);
+}
+
 }  // namespace
+
+hipError_t launch_box_add(const BoxCopy& b, int esz, const void* slab, void* tile, hipStream_t s)
+{
+    auto ok = [&](int64_t v) {
+        return (b.base % v) == 0 && (b.run % v) == 0 && (b.tstride[0] % v) == 0 && (b.tstride[1] % v) == 0 &&
+               (b.tstride[2] % v) == 0 && (reinterpret_cast<uintptr_t>(tile) % v) == 0 &&
+               (reinterpret_cast<uintptr_t>(slab) % v) == 0;
+    };
+    if (esz == 2) {
+        if (ok(16)) return launch_add_v<16, bf16_t>(b, slab, tile, s);
+        if (ok(4)) return launch_add_v<4, bf16_t>(b, slab, tile, s);
+        return launch_add_v<2, bf16_t>(b, slab, tile, s);
+    }
+    if (ok(16)) return launch_add_v<16, float>(b, slab, tile, s);
+    return launch_add_v<4, float>(b, slab, tile, s);
+}
 
 hipError_t launch_box_copy(const BoxCopy& b, CopyDir dir, const void* src, void* dst, hipStream_t s)
 {

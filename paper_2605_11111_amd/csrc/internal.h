@@ -42,6 +42,8 @@ struct BoxCopy {
 enum CopyDir { TILE_TO_SLAB = 0, SLAB_TO_TILE = 1, ZERO_TILE = 2 };
 
 hipError_t launch_box_copy(const BoxCopy& b, CopyDir dir, const void* src, void* dst, hipStream_t s);
+// tile[box] += slab (dense), element-wise in binary32; esz 2 (bf16) or 4 (f32).
+hipError_t launch_box_add(const BoxCopy& b, int esz, const void* slab, void* tile, hipStream_t s);
 
 // Convolution launchers. `ws` holds at least conv_*_workspace(...) bytes.
 size_t conv_fwd_workspace(const Tile3& t, const Conv3& cv, shard_dtype_t dt);
@@ -50,6 +52,9 @@ hipError_t launch_conv_fwd(const Tile3& t, const Conv3& cv, shard_dtype_t dt, co
                            void* y, void* ws, hipStream_t s);
 hipError_t launch_conv_wgrad(const Tile3& t, const Conv3& cv, shard_dtype_t dt, const void* tile, const void* dy,
                              float* dw, void* ws, hipStream_t s);
+size_t conv_dgrad_workspace(const Tile3& t, const Conv3& cv, shard_dtype_t dt);
+hipError_t launch_conv_dgrad(const Tile3& t, const Conv3& cv, shard_dtype_t dt, const void* dy, const void* w,
+                             void* dtile, void* ws, hipStream_t s);
 
 // Specialised kernels; each returns hipErrorNotSupported when the shape is
 // outside what it handles (the caller then takes the general kernel).

@@ -48,6 +48,11 @@ _SIGS = {
                                       _vp, ctypes.c_size_t, _vp]),
     "shard_conv_wgrad": (ctypes.c_int, [_tp, ctypes.c_int, _vp, _vp, ctypes.c_int64, _i64p, _i64p, _i64p, _i64p,
                                         _vp, _vp, ctypes.c_size_t, _vp]),
+    "shard_conv_dgrad": (ctypes.c_int, [_tp, ctypes.c_int, _vp, _vp, ctypes.c_int64, _i64p, _i64p, _i64p, _i64p,
+                                        _vp, _vp, ctypes.c_size_t, _vp]),
+    "shard_halo_pack_margin": (ctypes.c_int, [_tp, ctypes.c_int, _vp, ctypes.c_int32, ctypes.c_int32, _vp, _vp]),
+    "shard_halo_accumulate": (ctypes.c_int, [_tp, ctypes.c_int, _vp, ctypes.c_int32, ctypes.c_int32, ctypes.c_int64,
+                                             _vp, _vp]),
     "shard_conv_workspace_bytes": (ctypes.c_size_t, [ctypes.c_int32, _tp, ctypes.c_int, ctypes.c_int64, _i64p,
                                                      _i64p, _i64p]),
     "shard_status_string": (ctypes.c_char_p, [ctypes.c_int]),
@@ -165,3 +170,20 @@ def shard_conv_wgrad(desc, tile, dy, c_out, kernel, stride, pad_lo, out_ext, dw,
     _check("shard_conv_wgrad", _lib.shard_conv_wgrad(ctypes.byref(desc), _dtype_code(tile), _ptr(tile), _ptr(dy),
                                                      c_out, _arr(kernel), _arr(stride), _arr(pad_lo), _arr(out_ext),
                                                      _ptr(dw), _ptr(ws), nbytes, _stream(stream)))
+
+
+def shard_conv_dgrad(desc, dy, w, c_out, kernel, stride, pad_lo, out_ext, dtile, ws, stream=None):
+    nbytes = ws.numel() * ws.element_size() if ws is not None else 0
+    _check("shard_conv_dgrad", _lib.shard_conv_dgrad(ctypes.byref(desc), _dtype_code(dtile), _ptr(dy), _ptr(w), c_out,
+                                                     _arr(kernel), _arr(stride), _arr(pad_lo), _arr(out_ext),
+                                                     _ptr(dtile), _ptr(ws), nbytes, _stream(stream)))
+
+
+def shard_halo_pack_margin(desc, tile, axis, side, slab, stream=None):
+    _check("shard_halo_pack_margin", _lib.shard_halo_pack_margin(ctypes.byref(desc), _dtype_code(tile), _ptr(tile),
+                                                                 axis, side, _ptr(slab), _stream(stream)))
+
+
+def shard_halo_accumulate(desc, tile, axis, side, width, slab, stream=None):
+    _check("shard_halo_accumulate", _lib.shard_halo_accumulate(ctypes.byref(desc), _dtype_code(tile), _ptr(tile),
+                                                               axis, side, width, _ptr(slab), _stream(stream)))

@@ -111,11 +111,13 @@ def test_slab_shapes_follow_the_exchange_order(sc):
 
 def test_workspace_query(sc):
     d = sc.tile_desc(1, 32, [8, 16, 40], [1, 0, 0], [1, 0, 0])
-    for op in (0, 1):
+    for op in (0, 1, 2):
         n = sc.shard_conv_workspace_bytes(op, d, sc.SHARD_BF16, 32, [3, 3, 3], [1, 1, 1], [8, 16, 40])
         assert n >= 0
+    # the input gradient of a strided convolution takes the direct kernel (no workspace)
+    assert sc.shard_conv_workspace_bytes(2, d, sc.SHARD_F32, 32, [3, 3, 3], [2, 2, 2], [4, 8, 20]) == 0
     with pytest.raises(sc.ShardError):
-        sc.shard_conv_workspace_bytes(2, d, sc.SHARD_BF16, 32, [3, 3, 3], [1, 1, 1], [8, 16, 40])
+        sc.shard_conv_workspace_bytes(3, d, sc.SHARD_BF16, 32, [3, 3, 3], [1, 1, 1], [8, 16, 40])
     with pytest.raises(sc.ShardError):
         sc.shard_conv_workspace_bytes(0, d, sc.SHARD_BF16, 0, [3, 3, 3], [1, 1, 1], [8, 16, 40])
     with pytest.raises(sc.ShardError):
@@ -197,3 +199,48 @@ def test_conv_rejections(sc):
     assert g(p, 1, FAKE, FAKE, 32, K, S, pad, O, FAKE, FAKE, wneed - 1, None) == sc.SHARD_ERR_INVALID
     assert g(p, 1, FAKE, FAKE, 32, K, S, pad, O, None, FAKE, wneed, None) == sc.SHARD_ERR_INVALID     # null dw
     assert g(p, 1, FAKE, None, 32, K, S, pad, O, FAKE, FAKE, wneed, None) == sc.SHARD_ERR_INVALID     # null dy
+
+
+@pytestmark_host
+def test_reverse_halo_rejections(sc):
+    lib = _raw(sc)
+    d = sc.tile_desc(1, 4, [6, 5], [1, 0], [2, 0])
+    p = ctypes.byref(d)
+    m, a = lib.shard_halo_pack_margin, lib.shard_halo_accumulate
+    assert m(p, 0, FAKE, 2, 0, FAKE, None) == sc.SHARD_ERR_INVALID       # axis >= ndim
+    assert m(p, 0, FAKE, 0, 2, FAKE, None) == sc.SHARD_ERR_INVALID       # side
+    assert m(p, 5, FAKE, 0, 0, FAKE, None) == sc.SHARD_ERR_INVALID       # dtype
+    assert m(p, 0, None, 0, 0, FAKE, None) == sc.SHARD_ERR_INVALID       # null tile
+    assert m(p, 0, FAKE, 0, 0, None, None) == sc.SHARD_ERR_INVALID       # null slab
+    assert m(p, 0, None, 1, 0, None, None) == sc.SHARD_OK                # zero-width margin: no-op
+    assert m(p, 1, ctypes.c_void_p(0x10001), 0, 0, FAKE, None) == sc.SHARD_ERR_INVALID  # misaligned
+    assert a(p, 0, FAKE, 0, 0, -1, FAKE, None) == sc.SHARD_ERR_INVALID   # width < 0
+    assert a(p, 0, FAKE, 0, 3, 1, FAKE, None) == sc.SHARD_ERR_INVALID    # side
+    assert a(p, 0, FAKE, -1, 0, 1, FAKE, None) == sc.SHARD_ERR_INVALID   # axis
+    assert a(p, 0, FAKE, 0, 0, 7, FAKE, None) == sc.SHARD_ERR_UNSUPPORTED  # wider than the interior
+    assert a(p, 0, None, 0, 0, 1, FAKE, None) == sc.SHARD_ERR_INVALID    # null tile
+    assert a(p, 0, FAKE, 0, 0, 1, None, None) == sc.SHARD_ERR_INVALID    # null slab
+    assert a(p, 0, None, 0, 0, 0, None, None) == sc.SHARD_OK             # width 0: no-op
+
+
+@pytestmark_host
+def test_dgrad_rejections(sc):
+    lib = _raw(sc)
+    A = lambda *v: (ctypes.c_int64 * 3)(*v)
+    d = sc.tile_desc(1, 16, [8, 8, 40], [1, 0, 0], [1, 0, 0])
+    p = ctypes.byref(d)
+    K, S, pad, O = A(3, 3, 3), A(1, 1, 1), A(0, 1, 1), A(8, 8, 40)
+    need = sc.shard_conv_workspace_bytes(2, d, sc.SHARD_BF16, 32, [3, 3, 3], [1, 1, 1], [8, 8, 40])
+    assert need > 0
+    f = lib.shard_conv_dgrad
+    assert f(p, 1, FAKE, FAKE, 32, K, S, pad, O, FAKE, FAKE, need - 1, None) == sc.SHARD_ERR_INVALID  # short ws
+    assert f(p, 1, FAKE, FAKE, 32, K, S, pad, O, FAKE, None, need, None) == sc.SHARD_ERR_INVALID      # null ws
+    assert f(p, 1, FAKE, FAKE, 0, K, S, pad, O, FAKE, FAKE, need, None) == sc.SHARD_ERR_INVALID       # c_out 0
+    assert f(p, 1, FAKE, FAKE, 32, K, S, None, O, FAKE, FAKE, need, None) == sc.SHARD_ERR_INVALID     # null pad
+    assert f(p, 1, FAKE, None, 32, K, S, pad, O, FAKE, FAKE, need, None) == sc.SHARD_ERR_INVALID      # null w
+    assert f(p, 1, FAKE, FAKE, 32, K, S, pad, O, None, FAKE, need, None) == sc.SHARD_ERR_INVALID      # null dtile
+    assert f(p, 1, None, FAKE, 32, K, S, pad, O, FAKE, FAKE, need, None) == sc.SHARD_ERR_INVALID      # null dy
+    assert f(p, 1, FAKE, FAKE, 32, K, S, pad, O, FAKE, ctypes.c_void_p(0x10008), need, None) == sc.SHARD_ERR_INVALID
+    assert f(p, 7, FAKE, FAKE, 32, K, S, pad, O, FAKE, FAKE, need, None) == sc.SHARD_ERR_INVALID      # dtype
+    empty = sc.tile_desc(0, 16, [8, 8, 40], [1, 0, 0], [1, 0, 0])
+    assert f(ctypes.byref(empty), 1, None, FAKE, 32, K, S, pad, O, None, None, 0, None) == sc.SHARD_OK  # no tile

@@ -1,0 +1,337 @@
+"""GPU parity of the backward pass on a shard: the input gradient read back
+onto the padded tile (shard_conv_dgrad) and the reverse halo exchange
+(shard_halo_pack_margin, shard_halo_accumulate), against the float64 oracle.
+
+Bars as for the forward pass: fp32 normalised max error <= 1e-5, bf16 (fp32
+accumulation) <= 2e-2, and integer-valued inputs bit for bit (a bf16 value is
+the oracle's nearest-even rounding of the exact sum; a bf16 accumulate rounds
+the binary32 sum of two bf16 values). The reverse exchange runs between every
+shard of the reduced domains on the one GPU; afterwards each interior must be
+the shard's slice of the full-domain input gradient.
+"""
+import numpy as np
+import pytest
+
+import synth
+import shard_cases as cases
+from gpu_util import dev, dy_box, empty_like_dtype, host, log, weights
+from oracle import conv as oconv
+from oracle import halo as ohalo
+
+pytestmark = pytest.mark.gpu
+
+INT_DIST = (synth.INT, (-2.0, 2.0))
+
+
+@pytest.fixture(scope="module")
+def sc():
+    import torch
+    assert torch.cuda.is_available()
+    from paper_2605_11111_amd import shardconv
+    return shardconv
+
+
+def _code(sc, w):
+    return sc.SHARD_F32 if w.dtype == "f32" else sc.SHARD_BF16
+
+
+def _padded(sg):
+    return [l + e + h for l, e, h in zip(sg.g["halo_lo"], sg.ext, sg.g["halo_hi"])]
+
+
+def run_dgrad(sc, w, sg, dy, wt, fill=None):
+    import torch
+    desc = sc.tile_desc(w.N, w.cin, sg.ext, sg.g["halo_lo"], sg.g["halo_hi"])
+    O = sg.g["out_ext"]
+    dtile = empty_like_dtype([w.N] + _padded(sg) + [w.cin], w)
+    if fill is not None:
+        dtile.fill_(fill)
+    n = sc.shard_conv_workspace_bytes(2, desc, _code(sc, w), w.cout, w.K, w.S, O)
+    ws = torch.empty(max(n, 16), dtype=torch.uint8, device="cuda")
+    sc.shard_conv_dgrad(desc, dy, wt, w.cout, w.K, w.S, sg.g["pad_lo"], O, dtile, ws)
+    return desc, dtile
+
+
+def expected_dgrad(w, sg, dyh, w64):
+    """Oracle input gradient over the whole padded tile (channels-last float64)."""
+    dy64 = cases.to_ncdhw(cases.as_f64(dyh, w))
+    return cases.to_cl(oconv.tile_dgrad(dy64, w64, w.S, sg.g["pad_lo"], _padded(sg)))
+
+
+def _exact_bits(w, ref):
+    return cases.bf16_rne_of_f64(ref) if w.dtype == "bf16" else ref.astype(np.float32)
+
+
+def _same(w, got, ref_exact):
+    if w.dtype == "bf16":
+        return np.array_equal(got, cases.bf16_rne_of_f64(ref_exact))
+    return np.array_equal(got.astype(np.float64), ref_exact)
+
+
+def _dgrad_case(sc, w, idx, dist=None):
+    sg = cases.shard_geom(w, idx)
+    w_host, w64 = weights(w, dist)
+    dyh = dy_box(w, sg, dist)
+    _, dtile = run_dgrad(sc, w, sg, dev(dyh), dev(w_host), fill=float("nan"))
+    return host(dtile), expected_dgrad(w, sg, dyh, w64)
+
+
+@pytest.mark.parametrize("name", list(cases.REDUCED))
+def test_dgrad_every_shard_reduced(sc, name):
+    w = cases.REDUCED[name]
+    for idx in w.shards():
+        log(f"dgrad {name} shard {idx}")
+        got, ref = _dgrad_case(sc, w, idx)
+        err = cases.norm_max_err(cases.as_f64(got, w), ref)
+        assert err <= cases.TOL[w.dtype], (idx, err)
+
+
+@pytest.mark.parametrize("name", list(cases.REDUCED))
+def test_dgrad_integer_exact_reduced(sc, name):
+    w = cases.REDUCED[name]
+    for idx in w.shards():
+        got, ref = _dgrad_case(sc, w, idx, INT_DIST)
+        assert np.max(np.abs(ref)) < 2 ** 24
+        assert _same(w, got, ref), idx
+
+
+@pytest.mark.parametrize("name", ["c3r", "c2r", "c4r", "c5r", "c1"])
+def test_dgrad_kernel_variants_agree(sc, monkeypatch, name):
+    """The forward-kernel route (default, and SHARDCONV_ALGO=tiled) and the direct
+    kernel (SHARDCONV_ALGO=generic) agree: bitwise on integer data."""
+    w = cases.REDUCED[name]
+    idx = tuple(len(w.splits(a)) - 1 for a in range(w.nd))
+    for dist in (INT_DIST, None):
+        sg = cases.shard_geom(w, idx)
+        w_host, _ = weights(w, dist)
+        wt, dyh = dev(w_host), dev(dy_box(w, sg, dist))
+        res = {}
+        for algo in ("", "tiled", "generic"):
+            if algo:
+                monkeypatch.setenv("SHARDCONV_ALGO", algo)
+            else:
+                monkeypatch.delenv("SHARDCONV_ALGO", raising=False)
+            res[algo] = host(run_dgrad(sc, w, sg, dyh, wt)[1])
+        monkeypatch.delenv("SHARDCONV_ALGO", raising=False)
+        for algo in ("tiled", "generic"):
+            if dist is INT_DIST:
+                assert np.array_equal(res[""], res[algo]), (name, algo)
+            else:
+                assert cases.norm_max_err(cases.as_f64(res[algo], w), cases.as_f64(res[""], w)) <= cases.TOL[w.dtype]
+
+
+def _exchange_on_gpu(sc, w, dist):
+    """dgrad on every shard, then the margins returned in descending axis order."""
+    tiles, meta = {}, {}
+    w_host, w64 = weights(w, dist)
+    wt = dev(w_host)
+    for idx in w.shards():
+        sg = cases.shard_geom(w, idx)
+        dyh = dy_box(w, sg, dist)
+        desc, dtile = run_dgrad(sc, w, sg, dev(dyh), wt)
+        tiles[idx], meta[idx] = dtile, (sg, desc)
+    for axis in reversed(range(w.nd)):
+        sends = []
+        for idx, dtile in tiles.items():
+            sg, desc = meta[idx]
+            for side in (0, 1):
+                width = sg.g["halo_lo"][axis] if side == 0 else sg.g["halo_hi"][axis]
+                if width == 0 or not cases.neighbour_exists(w, idx, axis, side):
+                    continue
+                nb = list(idx)
+                nb[axis] += -1 if side == 0 else 1
+                slab = empty_like_dtype(sc.shard_halo_slab_shape(desc, axis, width), w)
+                sc.shard_halo_pack_margin(desc, dtile, axis, side, slab)
+                sends.append((tuple(nb), 1 - side, width, slab))
+        for nb, side, width, slab in sends:
+            sc.shard_halo_accumulate(meta[nb][1], tiles[nb], axis, side, width, slab)
+    return tiles, meta, w64
+
+
+def _oracle_exchange(w, dist, w64, rounding):
+    """The same pipeline on the oracle (logical float64), with the device's rounding."""
+    tiles, meta = {}, {}
+    for idx in w.shards():
+        sg = cases.shard_geom(w, idx)
+        tiles[idx] = rounding(cases.to_ncdhw(expected_dgrad(w, sg, dy_box(w, sg, dist), w64)))
+        meta[idx] = sg
+    for axis in reversed(range(w.nd)):
+        sends = []
+        for idx, t in tiles.items():
+            sg = meta[idx]
+            for side in (0, 1):
+                width = sg.g["halo_lo"][axis] if side == 0 else sg.g["halo_hi"][axis]
+                if width == 0 or not cases.neighbour_exists(w, idx, axis, side):
+                    continue
+                nb = list(idx)
+                nb[axis] += -1 if side == 0 else 1
+                sends.append((tuple(nb), 1 - side, width,
+                              ohalo.pack_margin(t, axis, side, sg.g["halo_lo"], sg.ext, sg.g["halo_hi"])))
+        for nb, side, width, slab in sends:
+            s = meta[nb]
+            tiles[nb] = ohalo.accumulate(tiles[nb], axis, side, width, slab, s.g["halo_lo"], s.ext, s.g["halo_hi"],
+                                         rounding)
+    return tiles
+
+
+@pytest.mark.parametrize("name", list(cases.REDUCED))
+def test_reverse_exchange_gives_the_full_input_gradient(sc, name):
+    """fp data: every interior within the tolerance of the full-domain input
+    gradient. Integer data: every whole tile (margins included) bit for bit equal
+    to the oracle running the same pipeline with the device's roundings."""
+    w = cases.REDUCED[name]
+    if w.dtype == "bf16":
+        rounding = lambda v: oconv.bf16_value(oconv.round_bf16(v))
+    else:
+        rounding = lambda v: np.asarray(v, dtype=np.float64).astype(np.float32).astype(np.float64)
+    n_out = tuple(cases.ogeo.out_len(g, k, s) for g, k, s in zip(w.G, w.K, w.S))
+    for dist in (None, INT_DIST):
+        log(f"reverse exchange {name} {'int' if dist else 'fp'}")
+        tiles, meta, w64 = _exchange_on_gpu(sc, w, dist)
+        if dist is None:
+            dy_full = cases.field(w, "dy", dist).box((0, 0) + (0,) * w.nd, (w.N, w.cout) + n_out,
+                                                       out=cases.out_code(w))
+            full = oconv.conv_dgrad(cases.to_ncdhw(cases.as_f64(dy_full, w)), w64, w.G, w.S)
+            for idx, dtile in tiles.items():
+                sg, _ = meta[idx]
+                got = cases.to_ncdhw(cases.as_f64(host(dtile), w))
+                inner = (slice(None), slice(None)) + tuple(slice(l, l + e) for l, e in zip(sg.g["halo_lo"], sg.ext))
+                box = (slice(None), slice(None)) + tuple(slice(o, o + e) for o, e in zip(sg.off, sg.ext))
+                err = cases.norm_max_err(got[inner], full[box])
+                assert err <= cases.TOL[w.dtype], (idx, err)
+        else:
+            ref = _oracle_exchange(w, dist, w64, rounding)
+            for idx, dtile in tiles.items():
+                got = cases.to_ncdhw(cases.as_f64(host(dtile), w))
+                assert np.array_equal(got, ref[idx]), idx
+
+
+@pytest.mark.parametrize("dt", ["bf16", "f32"])
+@pytest.mark.parametrize("aligned", [True, False])
+def test_pack_margin_and_accumulate_bitwise(sc, dt, aligned):
+    """Random tiles (values chosen to hit rounding ties in bf16): pack_margin is
+    the oracle's margin cut and accumulate the oracle's rounded sum, bit for bit;
+    unaligned buffers take the element path."""
+    import torch
+    rng = np.random.default_rng(17)
+    lo, ext, hi = [2, 1, 0], [5, 4, 7], [1, 2, 0]
+    n, c = 2, 3
+    P = [a + b + d for a, b, d in zip(lo, ext, hi)]
+    tdt = torch.bfloat16 if dt == "bf16" else torch.float32
+    # bf16 values with few significant bits make sums land on ties
+    vals = rng.integers(-64, 65, size=[n] + P + [c]).astype(np.float64) * 2.0 ** rng.integers(-9, -2, size=[n] + P + [c])
+    base = torch.tensor(vals, dtype=torch.float64).to(tdt)
+    off = 0 if aligned else 1
+    store = torch.zeros(base.numel() + off, dtype=tdt, device="cuda")
+    tile = store[off:].view(base.shape)
+    tile.copy_(base.cuda())
+    desc = sc.tile_desc(n, c, ext, lo, hi)
+    rounding = (lambda v: oconv.bf16_value(oconv.round_bf16(v))) if dt == "bf16" else \
+        (lambda v: np.asarray(v).astype(np.float32).astype(np.float64))
+    t64 = cases.to_ncdhw(base.double().numpy())
+    for axis in range(3):
+        for side in (0, 1):
+            width = lo[axis] if side == 0 else hi[axis]
+            if width == 0:
+                continue
+            shp = sc.shard_halo_slab_shape(desc, axis, width)
+            sstore = torch.zeros(int(np.prod(shp)) + off, dtype=tdt, device="cuda")
+            slab = sstore[off:].view(shp)
+            sc.shard_halo_pack_margin(desc, tile, axis, side, slab)
+            ref_slab = ohalo.pack_margin(t64, axis, side, lo, ext, hi)
+            assert np.array_equal(cases.to_ncdhw(slab.double().cpu().numpy()), ref_slab)
+            # add that slab onto the face rows of the same side (a stand-in neighbour)
+            aw = min(width, ext[axis])
+            addend = slab.narrow(1 + axis, 0, aw).contiguous()
+            if not aligned:
+                astore = torch.zeros(addend.numel() + 1, dtype=tdt, device="cuda")
+                astore[1:].copy_(addend.reshape(-1))
+                addend = astore[1:].view(addend.shape)
+            sc.shard_halo_accumulate(desc, tile, axis, side, aw, addend)
+            t64 = ohalo.accumulate(t64, axis, side, aw, cases.to_ncdhw(addend.double().cpu().numpy()), lo, ext, hi,
+                                   rounding)
+            assert np.array_equal(cases.to_ncdhw(tile.double().cpu().numpy()), t64), (axis, side)
+
+
+def test_dgrad_without_owned_outputs_is_zero(sc):
+    import torch
+    w = cases.REDUCED["c4r"]
+    sg = cases.shard_geom(w, (0, 0, 0))
+    desc = sc.tile_desc(w.N, w.cin, sg.ext, sg.g["halo_lo"], sg.g["halo_hi"])
+    dtile = torch.full([w.N] + _padded(sg) + [w.cin], 3.0, dtype=torch.bfloat16, device="cuda")
+    O = [0, sg.g["out_ext"][1], sg.g["out_ext"][2]]
+    n = sc.shard_conv_workspace_bytes(2, desc, sc.SHARD_BF16, w.cout, w.K, w.S, O)
+    ws = torch.empty(max(n, 16), dtype=torch.uint8, device="cuda")
+    sc.shard_conv_dgrad(desc, None, torch.zeros(1, dtype=torch.bfloat16, device="cuda"), w.cout, w.K, w.S,
+                        sg.g["pad_lo"], O, dtile, ws)
+    assert float(dtile.abs().max()) == 0.0
+
+
+EDGE = [
+    # (name, dtype, N, cin, cout, G, parts, K, S)
+    ("1d_bf16", "bf16", 2, 16, 32, (301,), (3,), (5,), (1,)),
+    ("1d_f32_s3", "f32", 1, 8, 8, (97,), (4,), (3,), (3,)),
+    ("2d_k7_ragged_c", "bf16", 1, 24, 40, (29, 37), (3, 1), (7, 7), (1, 1)),
+    ("2d_f32_odd_channels", "f32", 2, 5, 7, (19, 21), (2, 2), (3, 3), (2, 1)),
+    ("3d_s3_negative_pad", "f32", 1, 8, 16, (25, 9, 14), (2, 1, 1), (3, 3, 3), (3, 1, 2)),
+    ("3d_thin_w", "bf16", 1, 32, 32, (10, 11, 3), (2, 1, 1), (3, 3, 3), (1, 1, 1)),
+    ("3d_long_rows", "bf16", 1, 32, 32, (6, 5, 700), (2, 1, 1), (3, 3, 3), (1, 1, 1)),
+]
+
+
+@pytest.mark.parametrize("case", EDGE, ids=lambda c: c[0])
+def test_dgrad_edge_shapes_every_shard(sc, case):
+    name, dt, N, cin, cout, G, parts, K, S = case
+    wl = cases.Workload(name, dt, N, cin, cout, G, parts, K, S, (0,) * len(G),
+                        x_dist=(synth.UNIFORM, (-1.0, 1.0)), w_dist=(synth.UNIFORM, (-0.5, 0.5)),
+                        dy_dist=(synth.UNIFORM, (-1.0, 1.0)))
+    for idx in wl.shards():
+        log(f"dgrad edge {name} shard {idx}")
+        got, ref = _dgrad_case(sc, wl, idx)
+        assert cases.norm_max_err(cases.as_f64(got, wl), ref) <= cases.TOL[dt], idx
+        goti, refi = _dgrad_case(sc, wl, idx, INT_DIST)
+        assert _same(wl, goti, refi), idx
+
+
+# --- full-size workloads ------------------------------------------------------
+
+FULL = ["c1_2d_fp32", "c2_2d_bf16", "c4_3d_bf16_k5", "c5_3d_fp32_s2", "c3_3d_bf16"]
+
+
+@pytest.mark.parametrize("name", FULL)
+@pytest.mark.parametrize("integer", [False, True])
+def test_full_size_dgrad_sampled_planes(sc, name, integer):
+    """The measured shard at full size; tile planes (margins included) checked
+    one by one: tile plane p receives dy planes j with j*S + t - pad = p."""
+    w = cases.WORKLOADS[name]
+    dist = INT_DIST if integer else None
+    sg = cases.shard_geom(w, w.shard)
+    w_host, w64 = weights(w, dist)
+    log(f"full dgrad {name}: generating dy")
+    dyh = dy_box(w, sg, dist)
+    _, dtile = run_dgrad(sc, w, sg, dev(dyh), dev(w_host))
+    P = _padded(sg)
+    rng = np.random.default_rng(4)
+    planes = sorted(set([0, 1, P[0] - 2, P[0] - 1] + [int(v) for v in rng.integers(2, max(3, P[0] - 2), size=2)]))
+    got = host(dtile[:, planes])
+    del dtile
+    S0, K0, pad0, O0 = w.S[0], w.K[0], sg.g["pad_lo"][0], sg.g["out_ext"][0]
+    for k, p in enumerate(planes):
+        j0 = max(0, -(-(p + pad0 - (K0 - 1)) // S0))
+        j1 = min(O0, (p + pad0) // S0 + 1)
+        pad = list(sg.g["pad_lo"])
+        pad[0] = pad0 - j0 * S0 + p
+        ext = [1] + P[1:]
+        if j1 > j0:
+            win = cases.to_ncdhw(cases.as_f64(dyh[:, j0:j1], w))
+            ref = cases.to_cl(oconv.tile_dgrad(win, w64, w.S, pad, ext))
+        else:
+            ref = np.zeros([w.N] + ext + [w.cin])
+        g = got[:, k:k + 1]
+        if integer:
+            assert np.max(np.abs(ref)) < 2 ** 24
+            assert _same(w, g, ref), p
+        else:
+            err = cases.norm_max_err(cases.as_f64(g, w), ref)
+            log(f"  plane {p}: normalised max err {err:.3e}")
+            assert err <= cases.TOL[w.dtype], (p, err)
