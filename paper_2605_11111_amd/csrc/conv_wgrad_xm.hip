@@ -29,7 +29,7 @@
 //    rows y, y - 1, y - 2: each input row is read once per plane (a ring of four
 //    register slots per plane parity), so a wave issues about nine 512-byte
 //    transposed reads per eighteen MFMAs (five per nine with one K step).
-//  * The partial of every workgroup is written once; wgrad_xm_reduce sums the
+//  * The partial of every workgroup is written once; wgrad_xm_reduce1/2 sum the
 //    partials in a fixed order (results are bitwise repeatable).
 #include <algorithm>
 #include <type_traits>
@@ -559,30 +559,53 @@ __global__ __launch_bounds__(256 * KS, 1) void wgrad_xm(WxArgs a)
     }
 }
 
-// dw[co][ci][tap] = sum over workgroups (in order) of the partials. One thread per
-// partial float of one workgroup block.
+// The partials are summed in two fixed-order passes: pass 1 gives each of
+// kChunks blocks of workgroup partials its own sum (one thread per partial float
+// and chunk, many independent chains instead of one chain of nsplit loads),
+// pass 2 adds the kChunks sums in order and scatters into dw. Bitwise
+// repeatable.
+constexpr int kChunks = 16;
+
 template <int KD, int NCI, int NCO>
-__global__ __launch_bounds__(256) void wgrad_xm_reduce(const float* part, float* dw, int nsplit)
+__global__ __launch_bounds__(256) void wgrad_xm_reduce1(const float* part, float* sums, int nsplit)
+{
+    constexpr int NR = NCO * NCI * KD;
+    constexpr int BLK = 4 * 9 * 1024;
+    constexpr int NE = NR * 9 * 1024;
+    const int e = int(blockIdx.x) * 256 + threadIdx.x;
+    const int ch = int(blockIdx.y);
+    if (e >= NE) return;
+    const int per = (nsplit + kChunks - 1) / kChunks;
+    const int s0 = ch * per, s1 = min(nsplit, s0 + per);
+    float s4[4] = {0.f, 0.f, 0.f, 0.f};
+    int sp = s0;
+    for (; sp + 4 <= s1; sp += 4) {
+#pragma unroll
+        for (int j = 0; j < 4; ++j) s4[j] += part[int64_t(sp + j) * BLK + e];
+    }
+    for (int j = 0; sp + j < s1; ++j) s4[j] += part[int64_t(sp + j) * BLK + e];
+    sums[int64_t(ch) * NE + e] = (s4[0] + s4[1]) + (s4[2] + s4[3]);
+}
+
+// dw[co][ci][tap] = sum over the chunk sums, in chunk order.
+template <int KD, int NCI, int NCO>
+__global__ __launch_bounds__(256) void wgrad_xm_reduce2(const float* sums, float* dw)
 {
     constexpr int NR = NCO * NCI * KD;
     constexpr int CIN = 32 * NCI;
     constexpr int TAPS = KD * 9;
-    constexpr int BLK = 4 * 9 * 1024;
+    constexpr int NE = NR * 9 * 1024;
     const int e = int(blockIdx.x) * 256 + threadIdx.x;
-    if (e >= NR * 9 * 1024) return;
+    if (e >= NE) return;
     const int r = e % 16, lane = (e / 16) % 64, t9 = (e / 1024) % 9, wave = e / (9 * 1024);
     const int kd = wave % KD, cb = (wave / KD) % NCI, mb = wave / (KD * NCI);
     const int co = mb * 32 + 8 * (r / 4) + 4 * (lane / 32) + (r % 4);
     const int ci = cb * 32 + (lane % 32);
     const int tap = kd * 9 + t9;
-    float s8[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
-    int sp = 0;
-    for (; sp + 8 <= nsplit; sp += 8) {
+    float acc = 0.f;
 #pragma unroll
-        for (int j = 0; j < 8; ++j) s8[j] += part[int64_t(sp + j) * BLK + e];
-    }
-    for (int j = 0; sp + j < nsplit; ++j) s8[j] += part[int64_t(sp + j) * BLK + e];
-    dw[(co * CIN + ci) * TAPS + tap] = ((s8[0] + s8[1]) + (s8[2] + s8[3])) + ((s8[4] + s8[5]) + (s8[6] + s8[7]));
+    for (int ch = 0; ch < kChunks; ++ch) acc += sums[int64_t(ch) * NE + e];
+    dw[(co * CIN + ci) * TAPS + tap] = acc;
 }
 
 struct WxPlan {
@@ -669,8 +692,11 @@ hipError_t run_wx(const WxPlan& p, float* dw, hipStream_t s)
     e = hipLaunchKernel(reinterpret_cast<const void*>(fn), dim3(unsigned(p.grid)), dim3(256 * KS), args, LDS, s);
     if (e != hipSuccess) return e;
     const int total = C::NR * 9 * 1024;
-    hipLaunchKernelGGL((wgrad_xm_reduce<KD, NCI, NCO>), dim3(unsigned(ceil_div(total, 256))), dim3(256), 0, s,
-                       p.a.part, dw, int(p.grid * KS));
+    float* sums = p.a.part + size_t(p.grid) * KS * C::PART_FLOATS;
+    hipLaunchKernelGGL((wgrad_xm_reduce1<KD, NCI, NCO>), dim3(unsigned(ceil_div(total, 256)), kChunks), dim3(256), 0,
+                       s, p.a.part, sums, int(p.grid * KS));
+    hipLaunchKernelGGL((wgrad_xm_reduce2<KD, NCI, NCO>), dim3(unsigned(ceil_div(total, 256))), dim3(256), 0, s, sums,
+                       dw);
     return hipGetLastError();
 }
 
@@ -679,7 +705,8 @@ hipError_t run_wx(const WxPlan& p, float* dw, hipStream_t s)
 size_t wgrad_xm_workspace(const Tile3& t, const Conv3& cv, shard_dtype_t dt)
 {
     const WxPlan p = plan_wx(t, cv, dt);
-    return p.ok ? size_t(p.grid) * size_t(p.ks) * 4 * 9 * 1024 * sizeof(float) : 0;
+    // partials, then kChunks chunk sums of at most four roles
+    return p.ok ? (size_t(p.grid) * size_t(p.ks) + kChunks) * 4 * 9 * 1024 * sizeof(float) : 0;
 }
 
 // The W-march weight gradient applies to bf16, unit stride, 3 x 3 taps in H and
