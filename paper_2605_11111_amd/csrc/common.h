@@ -74,6 +74,32 @@ inline void pick_raster(int64_t NBZ, int64_t NBY, int want_z, int32_t& TZ, int32
     while (TZ * TY * 2 <= 32 && NBY % (TY * 2) == 0) TY *= 2;
 }
 
+// W segments of the persistent W-march kernels. `rows` brick rows of `ntiles`
+// tiles each are cut into segments of T tiles that `cus` workgroups take in
+// rounds; a segment after a row's first pays `warm` extra tiles (the forward
+// kernel rebuilds its carry). Picks the segment count with the fewest tile-steps
+// per workgroup, ceil(rows * nseg / cus) * (T + warm), preferring fewer segments,
+// and segments of at least `min_t` tiles. Returns nseg (the segments actually
+// formed, ceil(ntiles / T)) and T.
+inline void pick_segments(int64_t rows, int64_t ntiles, int64_t cus, int64_t warm, int64_t min_t, int64_t& nseg,
+                          int64_t& T)
+{
+    nseg = 1;
+    T = ntiles;
+    int64_t best = ((rows + cus - 1) / cus) * ntiles;
+    for (int64_t k = 2; k <= 64; ++k) {
+        const int64_t t = (ntiles + k - 1) / k;
+        if (t < min_t) break;
+        const int64_t segs = (ntiles + t - 1) / t;
+        const int64_t cost = ((rows * segs + cus - 1) / cus) * (t + warm);
+        if (cost < best) {
+            best = cost;
+            nseg = segs;
+            T = t;
+        }
+    }
+}
+
 }  // namespace shardconv
 
 namespace shardconv {

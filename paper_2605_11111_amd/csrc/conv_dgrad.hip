@@ -10,12 +10,19 @@
 // that belongs to the neighbours' interiors; shard_halo_pack_margin and
 // shard_halo_accumulate return it).
 //
-// Unit stride: the sum is a forward convolution of dy (zero outside the owned
-// output box) with the flipped, channel-transposed kernel
-//   w'[ci][co][t'] = w[co][ci][K - 1 - t'],   pad' = K - 1 - pad,
-// over the output box P (the padded tile), so it runs on the forward MFMA
-// kernels (the W-march kernel for the 3x3(x3) bf16 shapes). Other strides take a
-// direct kernel: one thread per tile element, over the taps whose phase matches.
+// Stride phases. Per axis, tile row p = phi + S*m (phase phi in [0, S)) is
+// reached only by taps t = r + S*u with r = (phi + pad) mod S, and then
+// jj = m + c - u with c = (phi + pad - r) / S. So each phase is a unit-stride
+// forward convolution of dy (zero outside the owned box) with the sub-kernel
+// of its taps, flipped and channel-swapped,
+//   w_phi[ci][co][u'] = w[co][ci][r + S*(Ku - 1 - u')],   pad' = Ku - 1 - c,
+// over the M = ceil((P - phi) / S) rows of that phase, written to every S-th
+// tile row through an output map. Unit stride is the single phase phi = 0 with
+// the whole flipped kernel and a dense map, which runs on the W-march kernel
+// for the 3x3(x3) bf16 shapes. A phase without taps (S > K) is zero-filled.
+// SHARDCONV_ALGO=generic takes a direct kernel instead (one thread per tile
+// element, over the taps whose phase matches): a structurally different
+// cross-check.
 #include <algorithm>
 
 #include "common.h"
@@ -24,18 +31,41 @@
 namespace shardconv {
 namespace {
 
+// w_phi[ci][co][u0][u1][u2] = w[co][ci][r0 + S0 (Ku0-1-u0)][r1 + S1 (Ku1-1-u1)][r2 + S2 (Ku2-1-u2)]
+struct SubKernel {
+    int32_t K[3], Ku[3], r[3], S[3];
+};
+
 template <typename T>
 __global__ __launch_bounds__(256) void dgrad_weights(const T* __restrict__ w, T* __restrict__ wt, int64_t cin,
-                                                     int64_t cout, int K0, int K1, int K2)
+                                                     int64_t cout, SubKernel k)
 {
-    const int64_t taps = int64_t(K0) * K1 * K2;
+    const int64_t taps = int64_t(k.Ku[0]) * k.Ku[1] * k.Ku[2];
     const int64_t total = cin * cout * taps;
     for (int64_t e = int64_t(blockIdx.x) * 256 + threadIdx.x; e < total; e += int64_t(gridDim.x) * 256) {
-        // e indexes w'[ci][co][a][b][c]
-        const int64_t c = e % K2, b = (e / K2) % K1, a = (e / (int64_t(K1) * K2)) % K0;
+        const int64_t u2 = e % k.Ku[2], u1 = (e / k.Ku[2]) % k.Ku[1], u0 = (e / (int64_t(k.Ku[1]) * k.Ku[2])) % k.Ku[0];
         const int64_t co = (e / taps) % cout, ci = e / (taps * cout);
-        const int64_t src = (((co * cin + ci) * K0 + (K0 - 1 - a)) * K1 + (K1 - 1 - b)) * K2 + (K2 - 1 - c);
-        wt[e] = w[src];
+        const int64_t t0 = k.r[0] + int64_t(k.S[0]) * (k.Ku[0] - 1 - u0);
+        const int64_t t1 = k.r[1] + int64_t(k.S[1]) * (k.Ku[1] - 1 - u1);
+        const int64_t t2 = k.r[2] + int64_t(k.S[2]) * (k.Ku[2] - 1 - u2);
+        wt[e] = w[(((co * cin + ci) * k.K[0] + t0) * k.K[1] + t1) * k.K[2] + t2];
+    }
+}
+
+// zeros at the elements an output map addresses (a phase that no tap reaches)
+template <typename T>
+__global__ __launch_bounds__(256) void fill_zero_mapped(T* __restrict__ y, int64_t n, int64_t M0, int64_t M1,
+                                                        int64_t M2, int64_t c, OutMap om)
+{
+    const int64_t total = n * M0 * M1 * M2 * c;
+    for (int64_t e = int64_t(blockIdx.x) * 256 + threadIdx.x; e < total; e += int64_t(gridDim.x) * 256) {
+        int64_t r = e;
+        const int64_t ci = r % c; r /= c;
+        const int64_t m2 = r % M2; r /= M2;
+        const int64_t m1 = r % M1; r /= M1;
+        const int64_t m0 = r % M0;
+        const int64_t nn = r / M0;
+        y[om.base + nn * om.str[0] + m0 * om.str[1] + m1 * om.str[2] + m2 * om.str[3] + ci] = T(0);
     }
 }
 
@@ -86,58 +116,113 @@ __global__ __launch_bounds__(256) void dgrad_direct(DgArgs a)
     }
 }
 
-bool unit_stride(const Conv3& cv) { return cv.S[0] == 1 && cv.S[1] == 1 && cv.S[2] == 1; }
+// One stride phase of the input gradient as a forward problem on dy.
+struct Phase {
+    bool empty;     // no tile row has this phase
+    bool zero;      // rows of this phase, but no tap reaches them
+    SubKernel k;
+    Tile3 tf;       // dy as the input tile
+    Conv3 cf;       // the unit-stride sub-convolution; cf.O = M
+    OutMap om;      // where its rows sit in the tile
+};
 
-// dy as the input tile and the tile's extent as the output box of the
-// equivalent forward convolution (unit stride only).
-void as_forward(const Tile3& t, const Conv3& cv, Tile3& tf, Conv3& cf)
+Phase make_phase(const Tile3& t, const Conv3& cv, const int phi[3])
 {
-    tf.n = t.n;
-    tf.c = cv.cout;
-    tf.esz = t.esz;
-    cf.cout = t.c;
-    for (int k = 0; k < 3; ++k) {
-        tf.P[k] = tf.ext[k] = cv.O[k];
-        tf.lo[k] = tf.hi[k] = 0;
-        cf.K[k] = cv.K[k];
-        cf.S[k] = 1;
-        cf.pad[k] = cv.K[k] - 1 - cv.pad[k];
-        cf.O[k] = t.P[k];
+    Phase ph{};
+    ph.tf.n = t.n;
+    ph.tf.c = cv.cout;
+    ph.tf.esz = t.esz;
+    ph.cf.cout = t.c;
+    int64_t base = 0;
+    const int64_t str[3] = {t.P[1] * t.P[2] * t.c, t.P[2] * t.c, t.c};
+    for (int a = 0; a < 3; ++a) {
+        const int64_t S = cv.S[a], K = cv.K[a];
+        const int64_t M = phi[a] < t.P[a] ? ceil_div(t.P[a] - phi[a], S) : 0;
+        if (M == 0) ph.empty = true;
+        const int64_t r = ((phi[a] + cv.pad[a]) % S + S) % S;
+        const int64_t Ku = r < K ? ceil_div(K - r, S) : 0;
+        if (Ku == 0) ph.zero = true;
+        const int64_t c = (phi[a] + cv.pad[a] - r) / S;  // exact
+        ph.k.K[a] = int32_t(K);
+        ph.k.Ku[a] = int32_t(std::max<int64_t>(Ku, 1));
+        ph.k.r[a] = int32_t(r);
+        ph.k.S[a] = int32_t(S);
+        ph.tf.P[a] = ph.tf.ext[a] = cv.O[a];
+        ph.tf.lo[a] = ph.tf.hi[a] = 0;
+        ph.cf.K[a] = ph.k.Ku[a];
+        ph.cf.S[a] = 1;
+        ph.cf.pad[a] = Ku - 1 - c;
+        ph.cf.O[a] = M;
+        base += phi[a] * str[a];
+        ph.om.str[1 + a] = S * str[a];
     }
+    ph.om.base = base;
+    ph.om.str[0] = t.P[0] * t.P[1] * t.P[2] * t.c;
+    return ph;
 }
 
-size_t wt_bytes(const Tile3& t, const Conv3& cv) { return size_t(round_up(t.c * cv.cout * cv.taps() * t.esz, 256)); }
+template <typename F>
+void for_each_phase(const Tile3& t, const Conv3& cv, F&& f)
+{
+    int phi[3];
+    for (phi[0] = 0; phi[0] < cv.S[0]; ++phi[0])
+        for (phi[1] = 0; phi[1] < cv.S[1]; ++phi[1])
+            for (phi[2] = 0; phi[2] < cv.S[2]; ++phi[2]) f(make_phase(t, cv, phi));
+}
+
+size_t wt_bytes(const Phase& ph)
+{
+    return size_t(round_up(ph.cf.cout * ph.tf.c * ph.cf.taps() * ph.tf.esz, 256));
+}
 
 }  // namespace
 
 size_t conv_dgrad_workspace(const Tile3& t, const Conv3& cv, shard_dtype_t dt)
 {
-    if (!unit_stride(cv) || force_generic()) return 0;
-    Tile3 tf;
-    Conv3 cf;
-    as_forward(t, cv, tf, cf);
-    return wt_bytes(t, cv) + conv_fwd_workspace(tf, cf, dt);
+    if (force_generic()) return 0;
+    size_t need = 0;
+    for_each_phase(t, cv, [&](const Phase& ph) {
+        if (!ph.empty && !ph.zero) need = std::max(need, wt_bytes(ph) + conv_fwd_workspace(ph.tf, ph.cf, dt));
+    });
+    return need;
 }
 
 hipError_t launch_conv_dgrad(const Tile3& t, const Conv3& cv, shard_dtype_t dt, const void* dy, const void* w,
                              void* dtile, void* ws, hipStream_t s)
 {
-    if (unit_stride(cv) && !force_generic()) {
-        Tile3 tf;
-        Conv3 cf;
-        as_forward(t, cv, tf, cf);
-        char* wt = static_cast<char*>(ws);
-        const int64_t total = t.c * cv.cout * cv.taps();
-        const unsigned grid = unsigned(std::max<int64_t>(1, std::min<int64_t>(ceil_div(total, 256), 4096)));
-        if (dt == SHARD_BF16)
-            hipLaunchKernelGGL(dgrad_weights<bf16_t>, dim3(grid), dim3(256), 0, s, static_cast<const bf16_t*>(w),
-                               reinterpret_cast<bf16_t*>(wt), t.c, cv.cout, int(cv.K[0]), int(cv.K[1]), int(cv.K[2]));
-        else
-            hipLaunchKernelGGL(dgrad_weights<float>, dim3(grid), dim3(256), 0, s, static_cast<const float*>(w),
-                               reinterpret_cast<float*>(wt), t.c, cv.cout, int(cv.K[0]), int(cv.K[1]), int(cv.K[2]));
-        hipError_t e = hipGetLastError();
-        if (e != hipSuccess) return e;
-        return launch_conv_fwd(tf, cf, dt, dy, wt, dtile, wt + wt_bytes(t, cv), s);
+    if (!force_generic()) {
+        // phases run one after another on the stream and reuse the workspace
+        hipError_t err = hipSuccess;
+        for_each_phase(t, cv, [&](const Phase& ph) {
+            if (err != hipSuccess || ph.empty) return;
+            if (ph.zero) {
+                const int64_t total = t.n * ph.cf.O[0] * ph.cf.O[1] * ph.cf.O[2] * t.c;
+                const unsigned grid = unsigned(std::max<int64_t>(1, std::min<int64_t>(ceil_div(total, 256), 1 << 16)));
+                if (dt == SHARD_BF16)
+                    hipLaunchKernelGGL(fill_zero_mapped<bf16_t>, dim3(grid), dim3(256), 0, s,
+                                       static_cast<bf16_t*>(dtile), t.n, ph.cf.O[0], ph.cf.O[1], ph.cf.O[2], t.c,
+                                       ph.om);
+                else
+                    hipLaunchKernelGGL(fill_zero_mapped<float>, dim3(grid), dim3(256), 0, s,
+                                       static_cast<float*>(dtile), t.n, ph.cf.O[0], ph.cf.O[1], ph.cf.O[2], t.c,
+                                       ph.om);
+                err = hipGetLastError();
+                return;
+            }
+            char* wt = static_cast<char*>(ws);
+            const int64_t total = t.c * cv.cout * ph.cf.taps();
+            const unsigned grid = unsigned(std::max<int64_t>(1, std::min<int64_t>(ceil_div(total, 256), 4096)));
+            if (dt == SHARD_BF16)
+                hipLaunchKernelGGL(dgrad_weights<bf16_t>, dim3(grid), dim3(256), 0, s, static_cast<const bf16_t*>(w),
+                                   reinterpret_cast<bf16_t*>(wt), t.c, cv.cout, ph.k);
+            else
+                hipLaunchKernelGGL(dgrad_weights<float>, dim3(grid), dim3(256), 0, s, static_cast<const float*>(w),
+                                   reinterpret_cast<float*>(wt), t.c, cv.cout, ph.k);
+            err = hipGetLastError();
+            if (err == hipSuccess)
+                err = launch_conv_fwd_mapped(ph.tf, ph.cf, dt, dy, wt, dtile, ph.om, wt + wt_bytes(ph), s);
+        });
+        return err;
     }
     DgArgs a{};
     a.dy = dy;

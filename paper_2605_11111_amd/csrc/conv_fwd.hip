@@ -59,6 +59,7 @@ struct FwdArgs {
     int32_t ng;        // N groups (workgroups along N)
     int32_t vec;       // 16-byte loads allowed (tile base and channel rows aligned)
     int64_t nblocks;
+    int64_t ybase, ys[4];  // output map: element of (n, o0, o1, o2, co) = ybase + n*ys0 + ... + co
 };
 
 struct PlanF {
@@ -251,11 +252,11 @@ __global__ __launch_bounds__(kThreads, 2) void conv_fwd_tiled(FwdArgs a)
             const int oz = f / (a.BO[2] * a.BO[1]);
             const int64_t o0 = ob[0] + oz, o1 = ob[1] + oy, o2 = ob[2] + ox;
             if (o0 >= a.O[0] || o1 >= a.O[1] || o2 >= a.O[2]) continue;
-            const int64_t vox = ((nn * a.O[0] + o0) * a.O[1] + o1) * a.O[2] + o2;
+            const int64_t vox = a.ybase + nn * a.ys[0] + o0 * a.ys[1] + o1 * a.ys[2] + o2 * a.ys[3];
 #pragma unroll
             for (int j = 0; j < RN; ++j) {
                 const int64_t co = int64_t(nt0 + j) * 32 + row;
-                if (co < a.cout) y[vox * a.cout + co] = from_f32<T>(acc[i][j][r]);
+                if (co < a.cout) y[vox + co] = from_f32<T>(acc[i][j][r]);
             }
         }
     }
@@ -416,11 +417,16 @@ hipError_t launch_tiled(const PlanF& pl, hipStream_t s)
 }
 
 template <typename T>
-hipError_t run_fwd(const Tile3& t, const Conv3& cv, const void* tile, const void* w, void* y, void* ws,
-                   hipStream_t s)
+hipError_t run_fwd(const Tile3& t, const Conv3& cv, const void* tile, const void* w, void* y, const OutMap& om,
+                   void* ws, hipStream_t s)
 {
     PlanF pl = plan_fwd_t<T>(t, cv);
     if (!pl.ok) return hipErrorInvalidValue;
+    const OutMap dm = dense_out(cv);
+    const bool dense = om.base == 0 && om.str[0] == dm.str[0] && om.str[1] == dm.str[1] && om.str[2] == dm.str[2] &&
+                       om.str[3] == dm.str[3];
+    pl.a.ybase = om.base;
+    for (int k = 0; k < 4; ++k) pl.a.ys[k] = om.str[k];
     pl.a.tile = static_cast<const char*>(tile);
     pl.a.vec = (reinterpret_cast<uintptr_t>(tile) % 16 == 0) && (t.c * Traits<T>::esz) % 16 == 0;
     pl.a.wfrag = static_cast<const uint4*>(ws);
@@ -432,9 +438,11 @@ hipError_t run_fwd(const Tile3& t, const Conv3& cv, const void* tile, const void
                        static_cast<uint4*>(ws), t.c, cv.cout, taps, pl.a.nkc, pl.a.nt);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-    e = launch_conv_fwd_rows(t, cv, std::is_same<T, bf16_t>::value ? SHARD_BF16 : SHARD_F32, tile, ws, pl.a.nkc,
-                             pl.a.nt, y, s);
-    if (e != hipErrorNotSupported) return e;
+    if (dense) {
+        e = launch_conv_fwd_rows(t, cv, std::is_same<T, bf16_t>::value ? SHARD_BF16 : SHARD_F32, tile, ws,
+                                 pl.a.nkc, pl.a.nt, y, s);
+        if (e != hipErrorNotSupported) return e;
+    }
     if (pl.rm == 4 && pl.rn == 1) return launch_tiled<T, 4, 1>(pl, s);
     if (pl.rm == 4 && pl.rn == 2) return launch_tiled<T, 4, 2>(pl, s);
     if (pl.rm == 2 && pl.rn == 2) return launch_tiled<T, 2, 2>(pl, s);
@@ -446,20 +454,38 @@ hipError_t run_fwd(const Tile3& t, const Conv3& cv, const void* tile, const void
 
 size_t generic_wgrad_workspace(const Tile3& t, const Conv3& cv);
 hipError_t generic_conv_fwd(const Tile3& t, const Conv3& cv, shard_dtype_t dt, const void* tile, const void* w,
-                            void* y, hipStream_t s);
+                            void* y, const OutMap& om, hipStream_t s);
+
+OutMap dense_out(const Conv3& cv)
+{
+    OutMap m;
+    m.base = 0;
+    m.str[3] = cv.cout;
+    m.str[2] = cv.O[2] * m.str[3];
+    m.str[1] = cv.O[1] * m.str[2];
+    m.str[0] = cv.O[0] * m.str[1];
+    return m;
+}
 
 size_t conv_fwd_workspace(const Tile3& t, const Conv3& cv, shard_dtype_t dt)
 {
     return dt == SHARD_BF16 ? wfrag_bytes<bf16_t>(t, cv) : wfrag_bytes<float>(t, cv);
 }
 
-hipError_t launch_conv_fwd(const Tile3& t, const Conv3& cv, shard_dtype_t dt, const void* tile, const void* w,
-                           void* y, void* ws, hipStream_t s)
+hipError_t launch_conv_fwd_mapped(const Tile3& t, const Conv3& cv, shard_dtype_t dt, const void* tile,
+                                  const void* w, void* y, const OutMap& om, void* ws, hipStream_t s)
 {
     const bool tiled = !force_generic() && tiled_supported(t, cv) &&
                        (dt == SHARD_BF16 ? plan_fwd_t<bf16_t>(t, cv).ok : plan_fwd_t<float>(t, cv).ok);
-    if (!tiled) return generic_conv_fwd(t, cv, dt, tile, w, y, s);
-    return dt == SHARD_BF16 ? run_fwd<bf16_t>(t, cv, tile, w, y, ws, s) : run_fwd<float>(t, cv, tile, w, y, ws, s);
+    if (!tiled) return generic_conv_fwd(t, cv, dt, tile, w, y, om, s);
+    return dt == SHARD_BF16 ? run_fwd<bf16_t>(t, cv, tile, w, y, om, ws, s)
+                            : run_fwd<float>(t, cv, tile, w, y, om, ws, s);
+}
+
+hipError_t launch_conv_fwd(const Tile3& t, const Conv3& cv, shard_dtype_t dt, const void* tile, const void* w,
+                           void* y, void* ws, hipStream_t s)
+{
+    return launch_conv_fwd_mapped(t, cv, dt, tile, w, y, dense_out(cv), ws, s);
 }
 
 }  // namespace shardconv

@@ -498,11 +498,11 @@ hipError_t launch_xm(const Tile3& t, const Conv3& cv, const void* tile, const vo
     int dev = 0, cus = 256;
     if (hipGetDevice(&dev) == hipSuccess) hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
     const int64_t rows = t.n * int64_t(a.NBZ) * a.NBY;
-    // split W rows into segments when there are too few bricks to fill the chip
-    int64_t nseg = 1;
-    while (rows * nseg < cus && (a.NXT / (nseg * 2)) >= 8) nseg *= 2;
+    // split W rows into segments when the bricks do not fill the chip evenly
+    int64_t nseg, T;
+    pick_segments(rows, a.NXT, cus, 1, 4, nseg, T);
     a.nseg = int32_t(nseg);
-    a.T = int32_t(ceil_div(a.NXT, nseg));
+    a.T = int32_t(T);
     const int64_t nb = rows * nseg;
     if (nb >= (int64_t(1) << 31)) return hipErrorNotSupported;
     a.nbricks = uint32_t(nb);

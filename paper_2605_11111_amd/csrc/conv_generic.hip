@@ -18,6 +18,7 @@ struct GenArgs {
     int64_t n, cin, cout;
     int64_t P[3], K[3], S[3], pad[3], O[3];
     int64_t chunk, nchunks, ndw;
+    int64_t ybase, ys[4];  // forward output map (see OutMap)
 };
 
 template <typename T>
@@ -51,7 +52,7 @@ __global__ __launch_bounds__(256) void fwd_direct(GenArgs a)
                 }
             }
         }
-        y[e] = from_f32<T>(acc);
+        y[a.ybase + nn * a.ys[0] + o0 * a.ys[1] + o1 * a.ys[2] + o2 * a.ys[3] + co] = from_f32<T>(acc);
     }
 }
 
@@ -136,9 +137,11 @@ size_t generic_wgrad_workspace(const Tile3& t, const Conv3& cv)
 }
 
 hipError_t generic_conv_fwd(const Tile3& t, const Conv3& cv, shard_dtype_t dt, const void* tile, const void* w,
-                            void* y, hipStream_t s)
+                            void* y, const OutMap& om, hipStream_t s)
 {
     GenArgs a = make_args(t, cv);
+    a.ybase = om.base;
+    for (int k = 0; k < 4; ++k) a.ys[k] = om.str[k];
     a.tile = tile;
     a.w_or_dy = w;
     a.out = y;

@@ -659,10 +659,10 @@ WxPlan plan_wx(const Tile3& t, const Conv3& cv, shard_dtype_t dt)
     a.NXT = int32_t(ceil_div(cv.O[2], 32));
     const int64_t rows = t.n * int64_t(a.NBZ) * a.NBY;
     if (rows == 0 || a.NXT == 0) return p;
-    int64_t nseg = 1;
-    while (rows * nseg < 256 && a.NXT / (nseg * 2) >= 4) nseg *= 2;
+    int64_t nseg, T;
+    pick_segments(rows, a.NXT, 256, 0, 4, nseg, T);
     a.nseg = int32_t(nseg);
-    a.T = int32_t(ceil_div(a.NXT, nseg));
+    a.T = int32_t(T);
     const int64_t nb = rows * nseg;
     if (nb >= (int64_t(1) << 31)) return p;
     a.nbricks = uint32_t(nb);

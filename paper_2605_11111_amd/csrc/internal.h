@@ -45,11 +45,24 @@ hipError_t launch_box_copy(const BoxCopy& b, CopyDir dir, const void* src, void*
 // tile[box] += slab (dense), element-wise in binary32; esz 2 (bf16) or 4 (f32).
 hipError_t launch_box_add(const BoxCopy& b, int esz, const void* slab, void* tile, hipStream_t s);
 
+// Where a forward convolution writes output (n, o0, o1, o2, co): element
+// base + n*str[0] + o0*str[1] + o1*str[2] + o2*str[3] + co. The dense map of
+// Conv3 is y[n][O0][O1][O2][cout]; the input gradient of a strided convolution
+// writes each stride phase into every S-th row of the tile with a strided map.
+struct OutMap {
+    int64_t base;
+    int64_t str[4];
+};
+OutMap dense_out(const Conv3& cv);
+
 // Convolution launchers. `ws` holds at least conv_*_workspace(...) bytes.
 size_t conv_fwd_workspace(const Tile3& t, const Conv3& cv, shard_dtype_t dt);
 size_t conv_wgrad_workspace(const Tile3& t, const Conv3& cv, shard_dtype_t dt);
 hipError_t launch_conv_fwd(const Tile3& t, const Conv3& cv, shard_dtype_t dt, const void* tile, const void* w,
                            void* y, void* ws, hipStream_t s);
+// The same with an output map (a non-dense map takes the general kernels).
+hipError_t launch_conv_fwd_mapped(const Tile3& t, const Conv3& cv, shard_dtype_t dt, const void* tile,
+                                  const void* w, void* y, const OutMap& om, void* ws, hipStream_t s);
 hipError_t launch_conv_wgrad(const Tile3& t, const Conv3& cv, shard_dtype_t dt, const void* tile, const void* dy,
                              float* dw, void* ws, hipStream_t s);
 size_t conv_dgrad_workspace(const Tile3& t, const Conv3& cv, shard_dtype_t dt);
