@@ -17,11 +17,14 @@ shapes". The oracle is therefore the plain definition:
 * ``geometry``  - which outputs a shard owns and which input rows (halo) it
                   needs, found by enumeration;
 * ``conv``      - the full-domain zero-padded cross-correlation (PyTorch
-                  semantics) restricted to any output box, its weight gradient,
-                  and the zero-extended input box a shard's padded tile holds;
+                  semantics) restricted to any output box, its weight and input
+                  gradients, and the zero-extended input box a shard's padded
+                  tile holds;
 * ``halo``      - the face slabs exchanged along each sharded axis;
 * ``brute``     - scalar-loop and dense-matrix restatements used to pin the
-                  above on tiny inputs.
+                  above on tiny inputs;
+* ``norm``      - group normalisation of a sharded tensor: per-shard sums, their
+                  total over all shards, and the normalised interior.
 
 Everything is float64 NumPy (``numpy.tensordot`` is the only library step).
 
@@ -29,4 +32,4 @@ Parity status: every function here is pinned by tests marked ``not gpu``
 (brute force, dense Toeplitz matrices, torch's float64 CPU convolution,
 closed forms and invariants); none is "parity unpinned".
 """
-from . import geometry, conv, halo, brute  # noqa: F401
+from . import geometry, conv, halo, brute, norm  # noqa: F401
