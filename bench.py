@@ -10,9 +10,10 @@ line on stdout (progress goes to stderr).
     python bench.py [--steps K] [--warmup W] [--workload c3] [--no-cpu-baseline] [--copy-calibration]
                     [--no-backward]
 
-The backward-pass ops of the same shard (input gradient onto the padded tile,
-reverse halo) are timed after the step and reported under "backward_ops"; they
-are not part of `value`.
+The ops beyond the step on the same shard - the backward pass (input gradient
+onto the padded tile, reverse halo) and group normalisation with statistics over
+all shards (the shard's sums, then the interior normalised) - are timed after
+the step and reported under "next_rows"; they are not part of `value`.
 
 The roofline's "traffic" field is the HBM traffic of the dominant kernel measured
 with rocprofv3 counters (FETCH_SIZE and WRITE_SIZE, each scaled by what it reads
@@ -92,7 +93,7 @@ def main():
     ap.add_argument("--copy-calibration", action="store_true",
                     help="run one 64 MiB device-to-device copy first (reference for counter scaling)")
     ap.add_argument("--no-backward", action="store_true",
-                    help="skip the backward-pass ops (input gradient, reverse halo), timed after the step")
+                    help="skip the ops beyond the step (input gradient, reverse halo, group normalisation)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU's shard; --gpus {args.gpus} is not supported: this build has no "
@@ -206,7 +207,10 @@ def main():
                                                      for k in range(args.steps)])))
     log("timed region done")
 
-    backward = None if args.no_backward else time_backward(sc, w, g, desc, wt, dy, send, flops, args, stream)
+    next_rows = None
+    if not args.no_backward:
+        next_rows = time_backward(sc, w, g, desc, wt, dy, send, flops, args, stream)
+        next_rows.update(time_group_norm(sc, w, g, desc, tile, args, stream))
 
     dt = w.dtype
     value = 2 * flops / (ms_step * 1e-3) / 1e12
@@ -235,7 +239,7 @@ def main():
                    "tile_padded": [w.N] + [l + e + h for l, e, h in zip(lo, ext, hi)] + [w.cin],
                    "out": [w.N] + list(O) + [w.cout], "kernel": list(w.K), "stride": list(w.S),
                    "accumulate": "f32"},
-        "ops": detail, "roofline": roofline, "cpu_baseline": cpu, "backward_ops": backward,
+        "ops": detail, "roofline": roofline, "cpu_baseline": cpu, "next_rows": next_rows,
     }
     print(json.dumps(line), flush=True)
 
@@ -295,6 +299,55 @@ def time_backward(sc, w, g, desc, wt, dy, send, flops, args, stream):
                           "bytes": int(work)}
     log("backward ops timed")
     return out
+
+
+def _time_ops(ops, args, stream):
+    import numpy as np
+    import torch
+    for _ in range(args.warmup):
+        for op in ops:
+            op[3]()
+    torch.cuda.synchronize()
+    ev = [[[torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)] for _ in ops]
+          for _ in range(args.steps)]
+    for k in range(args.steps):
+        for i, op in enumerate(ops):
+            ev[k][i][0].record(stream)
+            op[3]()
+            ev[k][i][1].record(stream)
+    torch.cuda.synchronize()
+    out = {}
+    for i, (label, kind, work, _) in enumerate(ops):
+        ms = float(np.mean([ev[k][i][0].elapsed_time(ev[k][i][1]) for k in range(args.steps)]))
+        gbs = work / (ms * 1e-3) / 1e9
+        out[label] = {"ms": round(ms, 4), "gbs": round(gbs, 1), "frac_hbm_peak": round(gbs / HBM_PEAK, 4),
+                      "bytes": int(work)}
+    return out
+
+
+def time_group_norm(sc, w, g, desc, tile, args, stream):
+    """Group normalisation of the shard's interior (c / 8 groups): its sums (reads
+    the interior once) and the normalisation with those sums standing for the
+    totals over all shards (reads and writes the interior), into a second tile."""
+    import numpy as np
+    import torch
+    code = sc.SHARD_F32 if w.dtype == "f32" else sc.SHARD_BF16
+    groups = max(1, w.cin // 8)
+    ws = torch.empty(max(16, sc.shard_norm_workspace_bytes(desc, code, groups)), dtype=torch.uint8, device="cuda")
+    sums = torch.empty((w.N, groups, 2), dtype=torch.float64, device="cuda")
+    out = torch.empty_like(tile)
+    gamma = torch.ones(w.cin, device="cuda")
+    beta = torch.zeros(w.cin, device="cuda")
+    inner_bytes = w.N * int(np.prod(g["ext"])) * w.cin * tile.element_size()
+    count = int(np.prod(w.G)) * (w.cin // groups)
+    sc.shard_norm_stats(desc, tile, groups, sums, ws)
+    torch.cuda.synchronize()
+    ops = [("norm_stats", "norm", inner_bytes, lambda: sc.shard_norm_stats(desc, tile, groups, sums, ws)),
+           ("norm_apply", "norm", 2 * inner_bytes,
+            lambda: sc.shard_norm_apply(desc, tile, sums, count, 1e-5, groups, gamma, beta, out, ws))]
+    res = _time_ops(ops, args, stream)
+    log("group normalisation timed")
+    return res
 
 
 def source_hash():

@@ -20,6 +20,8 @@
  *   shard_conv_dgrad      the input gradient read back onto the padded tile
  *   shard_halo_pack_margin, shard_halo_accumulate
  *                         the reverse halo exchange of the backward pass
+ *   shard_norm_stats, shard_norm_apply
+ *                         group normalisation with statistics over all shards
  *
  * Convolution semantics are PyTorch's cross-correlation (no bias, dilation 1,
  * groups 1), which the paper's programming model keeps (section "Benchmarks
@@ -240,6 +242,47 @@ shard_status_t shard_halo_accumulate(const shard_tile_t* x, shard_dtype_t dtype,
  */
 size_t shard_conv_workspace_bytes(int32_t op, const shard_tile_t* x, shard_dtype_t dtype, int64_t c_out,
                                   const int64_t kernel[], const int64_t stride[], const int64_t out_ext[]);
+
+/*
+ * Group normalisation of a sharded tensor. A normalisation layer aggregates its
+ * statistics across all ranks before normalising (section "PyTorch Dispatch");
+ * this library reads it as group normalisation: per batch item n and group g
+ * of c / groups consecutive channels, mean and (biased) variance over the
+ * group's channels and the whole domain. A shard computes its sums, the sums of
+ * all shards are added (the all-reduce), and every shard normalises its
+ * interior. Margins are neither read nor written.
+ *
+ * shard_norm_workspace_bytes: device workspace either call below needs;
+ * (size_t)-1 for a bad descriptor, dtype or groups (groups must divide c).
+ */
+size_t shard_norm_workspace_bytes(const shard_tile_t* x, shard_dtype_t dtype, int64_t groups);
+
+/*
+ * The shard's sums over its interior: sums[n][g][0] = sum x, sums[n][g][1] =
+ * sum x^2 (float64, device, [x->n][groups][2], overwritten; an empty interior
+ * gives zeros). Elements are summed in binary32 within fixed blocks of rows and
+ * the blocks in float64, in a fixed order: repeated calls give bit-identical sums.
+ * Errors: SHARD_ERR_INVALID (bad descriptor, dtype, groups, null or misaligned
+ * pointer, short workspace); SHARD_ERR_HIP if a launch fails.
+ */
+shard_status_t shard_norm_stats(const shard_tile_t* x, shard_dtype_t dtype, const void* tile, int64_t groups,
+                                double* sums, void* ws, size_t ws_bytes, hipStream_t stream);
+
+/*
+ * Normalise the interior with the sums of all shards (`sums`, float64 device
+ * [x->n][groups][2]) over `count` elements per (n, group) of the whole domain:
+ *   mean = S1 / count, var = max(S2 / count - mean^2, 0),
+ *   out = (x - mean) / sqrt(var + eps) * gamma[c] + beta[c]
+ * evaluated as x * scale[c] + shift[c] with scale and shift formed in float64
+ * and rounded once to binary32; gamma and beta are binary32 device arrays of c
+ * values. `out` has the tile's layout (interior written, margins untouched)
+ * and may be `tile` itself. A bf16 out is rounded to nearest-even.
+ * Errors: SHARD_ERR_INVALID (bad descriptor, dtype, groups, count <= 0,
+ * eps < 0, null or misaligned pointer, short workspace); SHARD_ERR_HIP.
+ */
+shard_status_t shard_norm_apply(const shard_tile_t* x, shard_dtype_t dtype, const void* tile, const double* sums,
+                                double count, double eps, int64_t groups, const float* gamma, const float* beta,
+                                void* out, void* ws, size_t ws_bytes, hipStream_t stream);
 
 /* Static, human-readable text for a status code. Never NULL. */
 const char* shard_status_string(shard_status_t status);

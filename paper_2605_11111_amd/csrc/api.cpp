@@ -343,4 +343,39 @@ shard_status_t shard_conv_dgrad(const shard_tile_t* x, shard_dtype_t dtype, cons
     return map_hip(launch_conv_dgrad(t, cv, dtype, dy, w, dtile, ws, stream));
 }
 
+size_t shard_norm_workspace_bytes(const shard_tile_t* x, shard_dtype_t dtype, int64_t groups)
+{
+    Tile3 t;
+    if (!norm_tile(x, dtype, t) || groups < 1 || groups > t.c || t.c % groups != 0) return size_t(-1);
+    return norm_workspace(t, groups);
+}
+
+shard_status_t shard_norm_stats(const shard_tile_t* x, shard_dtype_t dtype, const void* tile, int64_t groups,
+                                double* sums, void* ws, size_t ws_bytes, hipStream_t stream)
+{
+    Tile3 t;
+    if (!norm_tile(x, dtype, t) || groups < 1 || groups > t.c || t.c % groups != 0) return SHARD_ERR_INVALID;
+    if (t.n == 0) return SHARD_OK;
+    const size_t need = norm_workspace(t, groups);
+    if (!sums || !ws || ws_bytes < need || !aligned(sums, 8) || !aligned(ws, 16)) return SHARD_ERR_INVALID;
+    if (tile_elems(t) > 0 && (!tile || !aligned(tile, t.esz))) return SHARD_ERR_INVALID;
+    return map_hip(launch_norm_stats(t, dtype, tile, groups, sums, ws, stream));
+}
+
+shard_status_t shard_norm_apply(const shard_tile_t* x, shard_dtype_t dtype, const void* tile, const double* sums,
+                                double count, double eps, int64_t groups, const float* gamma, const float* beta,
+                                void* out, void* ws, size_t ws_bytes, hipStream_t stream)
+{
+    Tile3 t;
+    if (!norm_tile(x, dtype, t) || groups < 1 || groups > t.c || t.c % groups != 0) return SHARD_ERR_INVALID;
+    if (!(count > 0.0) || !(count < 1e300) || !(eps >= 0.0) || !(eps < 1e300)) return SHARD_ERR_INVALID;
+    if (t.n * t.ext[0] * t.ext[1] * t.ext[2] == 0) return SHARD_OK;
+    const size_t need = norm_workspace(t, groups);
+    if (!tile || !out || !sums || !gamma || !beta || !ws || ws_bytes < need) return SHARD_ERR_INVALID;
+    if (!aligned(tile, t.esz) || !aligned(out, t.esz) || !aligned(sums, 8) || !aligned(gamma, 4) ||
+        !aligned(beta, 4) || !aligned(ws, 16))
+        return SHARD_ERR_INVALID;
+    return map_hip(launch_norm_apply(t, dtype, tile, sums, count, eps, groups, gamma, beta, out, ws, stream));
+}
+
 }  // extern "C"

@@ -69,6 +69,14 @@ size_t conv_dgrad_workspace(const Tile3& t, const Conv3& cv, shard_dtype_t dt);
 hipError_t launch_conv_dgrad(const Tile3& t, const Conv3& cv, shard_dtype_t dt, const void* dy, const void* w,
                              void* dtile, void* ws, hipStream_t s);
 
+// Group normalisation of a shard's interior (see norm.hip).
+size_t norm_workspace(const Tile3& t, int64_t groups);
+hipError_t launch_norm_stats(const Tile3& t, shard_dtype_t dt, const void* tile, int64_t groups, double* sums,
+                             void* ws, hipStream_t s);
+hipError_t launch_norm_apply(const Tile3& t, shard_dtype_t dt, const void* tile, const double* sums, double count,
+                             double eps, int64_t groups, const float* gamma, const float* beta, void* out, void* ws,
+                             hipStream_t s);
+
 // Specialised kernels; each returns hipErrorNotSupported when the shape is
 // outside what it handles (the caller then takes the general kernel).
 hipError_t launch_conv_fwd_rows(const Tile3& t, const Conv3& cv, shard_dtype_t dt, const void* tile,

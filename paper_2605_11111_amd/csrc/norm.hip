@@ -1,0 +1,340 @@
+// Domain-parallel group normalisation on a shard (ShardTensor section "PyTorch
+// Dispatch": a normalisation layer aggregates its statistics across all ranks
+// before it normalises). Per batch item n and group g of C / G consecutive
+// channels, a shard contributes S1 = sum x and S2 = sum x^2 over its interior;
+// the totals over all shards give mean = S1 / cnt and var = S2 / cnt - mean^2,
+// and every shard then writes y = (x - mean) / sqrt(var + eps) * gamma + beta
+// over its interior.
+//
+// Both passes stream the interior once (HBM-bound). The interior is a set of
+// W runs of ext2 * C contiguous elements. On the vector path (C * esz a
+// multiple of 16, 16-byte aligned tile, 256 vectors span whole channel sets) a
+// thread reads 16-byte vectors whose channels never change, so it keeps its
+// channels' sums, scales and shifts in registers; other shapes take an
+// element-wise path.
+//
+// Statistics: pass 1 gives every block (a fixed range of rows of one batch
+// item) fp32 per-channel sums, reduced across its threads through LDS in a fixed
+// order; pass 2 adds, per (n, g), the blocks' sums of the group's channels in
+// float64 (a fixed-order tree over 256 threads). Results are bitwise repeatable.
+#include <algorithm>
+
+#include "common.h"
+#include "internal.h"
+
+namespace shardconv {
+namespace {
+
+constexpr int kT = 256;
+constexpr int kU = 4;  // 16-byte loads in flight per thread
+typedef __attribute__((ext_vector_type(4))) unsigned int u32x4_n;
+
+struct NormArgs {
+    const char* x;
+    char* y;
+    float* part;            // stats: [n * B][c][2]; apply: [n][c][2] scale, shift
+    const double* sums;     // [n][G][2]
+    const float* gamma;
+    const float* beta;
+    double* out;            // [n][G][2]
+    int64_t n, c, G;
+    int64_t P[3], lo[3], ext[3];
+    int64_t rows;           // interior rows per batch item: ext0 * ext1
+    int64_t B;              // stats blocks per batch item
+    double count, eps;
+};
+
+__device__ __forceinline__ int64_t run_offset(const NormArgs& a, int64_t nn, int64_t row)
+{
+    const int64_t i0 = a.lo[0] + row / a.ext[1], i1 = a.lo[1] + row % a.ext[1];
+    return (((nn * a.P[0] + i0) * a.P[1] + i1) * a.P[2] + a.lo[2]) * a.c;
+}
+
+template <typename T>
+struct Vec16 {
+    static constexpr int N = 16 / int(sizeof(T));
+};
+
+// pass 1, vector path: block (nn, b) sums rows [b * rows / B, (b + 1) * rows / B)
+template <typename T>
+__global__ __launch_bounds__(kT) void norm_stats_vec(NormArgs a)
+{
+    constexpr int VE = Vec16<T>::N;
+    __shared__ float red[2][kT][VE];
+    const int64_t nn = blockIdx.x / a.B, b = blockIdx.x % a.B;
+    const int64_t r0 = b * a.rows / a.B, r1 = (b + 1) * a.rows / a.B;
+    const int64_t nvec = a.ext[2] * a.c / VE;
+    const int tid = threadIdx.x;
+    float s1[VE], s2[VE];
+#pragma unroll
+    for (int i = 0; i < VE; ++i) s1[i] = s2[i] = 0.f;
+    for (int64_t row = r0; row < r1; ++row) {
+        const uint4* src = reinterpret_cast<const uint4*>(reinterpret_cast<const T*>(a.x) + run_offset(a, nn, row));
+        // kU loads in flight per thread before the arithmetic
+        for (int64_t v0 = tid; v0 < nvec; v0 += kU * kT) {
+            uint4 u[kU];
+#pragma unroll
+            for (int j = 0; j < kU; ++j) {
+                const int64_t v = v0 + j * kT;
+                u[j] = v < nvec ? src[v] : make_uint4(0u, 0u, 0u, 0u);
+            }
+#pragma unroll
+            for (int j = 0; j < kU; ++j) {
+                T e[VE];
+                __builtin_memcpy(e, &u[j], 16);
+#pragma unroll
+                for (int i = 0; i < VE; ++i) {
+                    const float f = to_f32(e[i]);
+                    s1[i] += f;
+                    s2[i] = fmaf(f, f, s2[i]);
+                }
+            }
+        }
+    }
+#pragma unroll
+    for (int i = 0; i < VE; ++i) {
+        red[0][tid][i] = s1[i];
+        red[1][tid][i] = s2[i];
+    }
+    __syncthreads();
+    // threads tid and tid + k * (C / VE) hold the same channels: fold in a fixed tree
+    const int per = int(a.c / VE);
+    for (int step = kT / 2; step >= per; step /= 2) {
+        if (tid < step) {
+#pragma unroll
+            for (int i = 0; i < VE; ++i) {
+                red[0][tid][i] += red[0][tid + step][i];
+                red[1][tid][i] += red[1][tid + step][i];
+            }
+        }
+        __syncthreads();
+    }
+    if (tid < per) {
+        float* out = a.part + (nn * a.B + b) * a.c * 2;
+#pragma unroll
+        for (int i = 0; i < VE; ++i) {
+            out[(tid * VE + i) * 2] = red[0][tid][i];
+            out[(tid * VE + i) * 2 + 1] = red[1][tid][i];
+        }
+    }
+}
+
+// pass 1, element path: thread t owns channels t, t + kT, ... and sums them over
+// the block's rows, one element at a time
+template <typename T>
+__global__ __launch_bounds__(kT) void norm_stats_elem(NormArgs a)
+{
+    const int64_t nn = blockIdx.x / a.B, b = blockIdx.x % a.B;
+    const int64_t r0 = b * a.rows / a.B, r1 = (b + 1) * a.rows / a.B;
+    const int64_t run = a.ext[2] * a.c;
+    float* out = a.part + (nn * a.B + b) * a.c * 2;
+    for (int64_t ch = threadIdx.x; ch < a.c; ch += kT) {
+        float s1 = 0.f, s2 = 0.f;
+        for (int64_t row = r0; row < r1; ++row) {
+            const T* src = reinterpret_cast<const T*>(a.x) + run_offset(a, nn, row);
+            for (int64_t e = ch; e < run; e += a.c) {
+                const float f = to_f32(src[e]);
+                s1 += f;
+                s2 = fmaf(f, f, s2);
+            }
+        }
+        out[ch * 2] = s1;
+        out[ch * 2 + 1] = s2;
+    }
+}
+
+// pass 2: block (nn, g) adds the B blocks' sums of the group's channels in float64
+__global__ __launch_bounds__(kT) void norm_stats_final(NormArgs a)
+{
+    __shared__ double red[2][kT];
+    const int64_t nn = blockIdx.x / a.G, g = blockIdx.x % a.G;
+    const int64_t cpg = a.c / a.G;
+    const int64_t items = a.B * cpg;
+    double s1 = 0.0, s2 = 0.0;
+    for (int64_t k = threadIdx.x; k < items; k += kT) {
+        const int64_t b = k / cpg, ch = g * cpg + k % cpg;
+        const float* p = a.part + ((nn * a.B + b) * a.c + ch) * 2;
+        s1 += double(p[0]);
+        s2 += double(p[1]);
+    }
+    red[0][threadIdx.x] = s1;
+    red[1][threadIdx.x] = s2;
+    __syncthreads();
+    for (int step = kT / 2; step >= 1; step /= 2) {
+        if (int(threadIdx.x) < step) {
+            red[0][threadIdx.x] += red[0][threadIdx.x + step];
+            red[1][threadIdx.x] += red[1][threadIdx.x + step];
+        }
+        __syncthreads();
+    }
+    if (threadIdx.x == 0) {
+        a.out[(nn * a.G + g) * 2] = red[0][0];
+        a.out[(nn * a.G + g) * 2 + 1] = red[1][0];
+    }
+}
+
+// scale[n][c] = gamma[c] * rstd[n][g], shift[n][c] = beta[c] - mean[n][g] * scale, from
+// the totals over all shards (float64, rounded once to binary32)
+__global__ __launch_bounds__(kT) void norm_affine(NormArgs a)
+{
+    const int64_t total = a.n * a.c;
+    for (int64_t e = int64_t(blockIdx.x) * kT + threadIdx.x; e < total; e += int64_t(gridDim.x) * kT) {
+        const int64_t nn = e / a.c, ch = e % a.c, g = ch / (a.c / a.G);
+        const double mean = a.sums[(nn * a.G + g) * 2] / a.count;
+        const double var = fmax(a.sums[(nn * a.G + g) * 2 + 1] / a.count - mean * mean, 0.0);
+        const double rstd = 1.0 / sqrt(var + a.eps);
+        const double sc = double(a.gamma[ch]) * rstd;
+        a.part[e * 2] = float(sc);
+        a.part[e * 2 + 1] = float(double(a.beta[ch]) - mean * sc);
+    }
+}
+
+template <typename T>
+__global__ __launch_bounds__(kT) void norm_apply_vec(NormArgs a)
+{
+    constexpr int VE = Vec16<T>::N;
+    const int64_t nvec = a.ext[2] * a.c / VE;
+    const int per = int(a.c / VE);
+    const int tid = threadIdx.x;
+    const int cb = (tid % per) * VE;  // first channel of this thread's vectors
+    // grid: blockIdx.x runs over (n, row chunk)
+    const int64_t chunks = gridDim.x / a.n;
+    const int64_t nn = blockIdx.x / chunks, b = blockIdx.x % chunks;
+    const int64_t r0 = b * a.rows / chunks, r1 = (b + 1) * a.rows / chunks;
+    float sc[VE], sh[VE];
+#pragma unroll
+    for (int i = 0; i < VE; ++i) {
+        sc[i] = a.part[(nn * a.c + cb + i) * 2];
+        sh[i] = a.part[(nn * a.c + cb + i) * 2 + 1];
+    }
+    for (int64_t row = r0; row < r1; ++row) {
+        const int64_t off = run_offset(a, nn, row);
+        const uint4* src = reinterpret_cast<const uint4*>(reinterpret_cast<const T*>(a.x) + off);
+        u32x4_n* dst = reinterpret_cast<u32x4_n*>(reinterpret_cast<T*>(a.y) + off);
+        for (int64_t v0 = tid; v0 < nvec; v0 += kU * kT) {
+            uint4 u[kU];
+#pragma unroll
+            for (int j = 0; j < kU; ++j) {
+                const int64_t v = v0 + j * kT;
+                if (v < nvec) u[j] = src[v];
+            }
+#pragma unroll
+            for (int j = 0; j < kU; ++j) {
+                const int64_t v = v0 + j * kT;
+                if (v >= nvec) continue;
+                T e[VE];
+                __builtin_memcpy(e, &u[j], 16);
+#pragma unroll
+                for (int i = 0; i < VE; ++i) e[i] = from_f32<T>(fmaf(to_f32(e[i]), sc[i], sh[i]));
+                u32x4_n r;
+                __builtin_memcpy(&r, e, 16);
+                // the normalised tile is consumed by the next layer, not by this kernel
+                __builtin_nontemporal_store(r, dst + v);
+            }
+        }
+    }
+}
+
+template <typename T>
+__global__ __launch_bounds__(kT) void norm_apply_elem(NormArgs a)
+{
+    const int64_t run = a.ext[2] * a.c;
+    const int64_t total = a.n * a.rows * run;
+    for (int64_t e = int64_t(blockIdx.x) * kT + threadIdx.x; e < total; e += int64_t(gridDim.x) * kT) {
+        const int64_t k = e % run, r = e / run;
+        const int64_t nn = r / a.rows, row = r % a.rows;
+        const int64_t ch = k % a.c;
+        const int64_t off = run_offset(a, nn, row) + k;
+        const float v = to_f32(reinterpret_cast<const T*>(a.x)[off]);
+        reinterpret_cast<T*>(a.y)[off] =
+            from_f32<T>(fmaf(v, a.part[(nn * a.c + ch) * 2], a.part[(nn * a.c + ch) * 2 + 1]));
+    }
+}
+
+NormArgs make_norm(const Tile3& t, int64_t groups)
+{
+    NormArgs a{};
+    a.n = t.n;
+    a.c = t.c;
+    a.G = groups;
+    for (int k = 0; k < 3; ++k) {
+        a.P[k] = t.P[k];
+        a.lo[k] = t.lo[k];
+        a.ext[k] = t.ext[k];
+    }
+    a.rows = t.ext[0] * t.ext[1];
+    // about 1024 stats blocks in all, at most one per row
+    a.B = std::max<int64_t>(1, std::min<int64_t>(a.rows, ceil_div(1024, std::max<int64_t>(t.n, 1))));
+    return a;
+}
+
+bool vec_path(const Tile3& t, const void* x, const void* y)
+{
+    const int64_t ve = 16 / t.esz;
+    return (t.c * t.esz) % 16 == 0 && (int64_t(kT) * ve) % t.c == 0 && reinterpret_cast<uintptr_t>(x) % 16 == 0 &&
+           (y == nullptr || reinterpret_cast<uintptr_t>(y) % 16 == 0);
+}
+
+unsigned grid_of(int64_t total) { return unsigned(std::max<int64_t>(1, std::min<int64_t>(ceil_div(total, kT), 1 << 16))); }
+
+}  // namespace
+
+size_t norm_workspace(const Tile3& t, int64_t groups)
+{
+    const NormArgs a = make_norm(t, groups);
+    return size_t(std::max(a.n * a.B * a.c * 2, a.n * a.c * 2)) * sizeof(float);
+}
+
+hipError_t launch_norm_stats(const Tile3& t, shard_dtype_t dt, const void* tile, int64_t groups, double* sums,
+                             void* ws, hipStream_t s)
+{
+    NormArgs a = make_norm(t, groups);
+    a.x = static_cast<const char*>(tile);
+    a.part = static_cast<float*>(ws);
+    a.out = sums;
+    void* args[] = {&a};
+    const unsigned blocks = unsigned(a.n * a.B);
+    const bool vec = vec_path(t, tile, nullptr);
+    const void* fn;
+    if (dt == SHARD_BF16)
+        fn = vec ? reinterpret_cast<const void*>(&norm_stats_vec<bf16_t>)
+                 : reinterpret_cast<const void*>(&norm_stats_elem<bf16_t>);
+    else
+        fn = vec ? reinterpret_cast<const void*>(&norm_stats_vec<float>)
+                 : reinterpret_cast<const void*>(&norm_stats_elem<float>);
+    hipError_t e = hipLaunchKernel(fn, dim3(blocks), dim3(kT), args, 0, s);
+    if (e != hipSuccess) return e;
+    return hipLaunchKernel(reinterpret_cast<const void*>(&norm_stats_final), dim3(unsigned(a.n * a.G)), dim3(kT),
+                           args, 0, s);
+}
+
+hipError_t launch_norm_apply(const Tile3& t, shard_dtype_t dt, const void* tile, const double* sums, double count,
+                             double eps, int64_t groups, const float* gamma, const float* beta, void* out, void* ws,
+                             hipStream_t s)
+{
+    NormArgs a = make_norm(t, groups);
+    a.x = static_cast<const char*>(tile);
+    a.y = static_cast<char*>(out);
+    a.part = static_cast<float*>(ws);
+    a.sums = sums;
+    a.gamma = gamma;
+    a.beta = beta;
+    a.count = count;
+    a.eps = eps;
+    void* args[] = {&a};
+    hipError_t e = hipLaunchKernel(reinterpret_cast<const void*>(&norm_affine), dim3(grid_of(a.n * a.c)), dim3(kT),
+                                   args, 0, s);
+    if (e != hipSuccess) return e;
+    if (vec_path(t, tile, out)) {
+        // about 2048 blocks in all, at most one per row
+        const int64_t chunks = std::max<int64_t>(1, std::min<int64_t>(a.rows, ceil_div(2048, a.n)));
+        const void* fn = dt == SHARD_BF16 ? reinterpret_cast<const void*>(&norm_apply_vec<bf16_t>)
+                                          : reinterpret_cast<const void*>(&norm_apply_vec<float>);
+        return hipLaunchKernel(fn, dim3(unsigned(a.n * chunks)), dim3(kT), args, 0, s);
+    }
+    const void* fn = dt == SHARD_BF16 ? reinterpret_cast<const void*>(&norm_apply_elem<bf16_t>)
+                                      : reinterpret_cast<const void*>(&norm_apply_elem<float>);
+    return hipLaunchKernel(fn, dim3(grid_of(a.n * a.rows * a.ext[2] * a.c)), dim3(kT), args, 0, s);
+}
+
+}  // namespace shardconv

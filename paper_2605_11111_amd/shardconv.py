@@ -53,6 +53,10 @@ _SIGS = {
     "shard_halo_pack_margin": (ctypes.c_int, [_tp, ctypes.c_int, _vp, ctypes.c_int32, ctypes.c_int32, _vp, _vp]),
     "shard_halo_accumulate": (ctypes.c_int, [_tp, ctypes.c_int, _vp, ctypes.c_int32, ctypes.c_int32, ctypes.c_int64,
                                              _vp, _vp]),
+    "shard_norm_workspace_bytes": (ctypes.c_size_t, [_tp, ctypes.c_int, ctypes.c_int64]),
+    "shard_norm_stats": (ctypes.c_int, [_tp, ctypes.c_int, _vp, ctypes.c_int64, _vp, _vp, ctypes.c_size_t, _vp]),
+    "shard_norm_apply": (ctypes.c_int, [_tp, ctypes.c_int, _vp, _vp, ctypes.c_double, ctypes.c_double, ctypes.c_int64,
+                                        _vp, _vp, _vp, _vp, ctypes.c_size_t, _vp]),
     "shard_conv_workspace_bytes": (ctypes.c_size_t, [ctypes.c_int32, _tp, ctypes.c_int, ctypes.c_int64, _i64p,
                                                      _i64p, _i64p]),
     "shard_status_string": (ctypes.c_char_p, [ctypes.c_int]),
@@ -187,3 +191,23 @@ def shard_halo_pack_margin(desc, tile, axis, side, slab, stream=None):
 def shard_halo_accumulate(desc, tile, axis, side, width, slab, stream=None):
     _check("shard_halo_accumulate", _lib.shard_halo_accumulate(ctypes.byref(desc), _dtype_code(tile), _ptr(tile),
                                                                axis, side, width, _ptr(slab), _stream(stream)))
+
+
+def shard_norm_workspace_bytes(desc, dtype_code, groups) -> int:
+    n = _lib.shard_norm_workspace_bytes(ctypes.byref(desc), dtype_code, groups)
+    if n == ctypes.c_size_t(-1).value:
+        raise ShardError("shard_norm_workspace_bytes", SHARD_ERR_INVALID)
+    return int(n)
+
+
+def shard_norm_stats(desc, tile, groups, sums, ws, stream=None):
+    nbytes = ws.numel() * ws.element_size() if ws is not None else 0
+    _check("shard_norm_stats", _lib.shard_norm_stats(ctypes.byref(desc), _dtype_code(tile), _ptr(tile), groups,
+                                                     _ptr(sums), _ptr(ws), nbytes, _stream(stream)))
+
+
+def shard_norm_apply(desc, tile, sums, count, eps, groups, gamma, beta, out, ws, stream=None):
+    nbytes = ws.numel() * ws.element_size() if ws is not None else 0
+    _check("shard_norm_apply", _lib.shard_norm_apply(ctypes.byref(desc), _dtype_code(tile), _ptr(tile), _ptr(sums),
+                                                     float(count), float(eps), groups, _ptr(gamma), _ptr(beta),
+                                                     _ptr(out), _ptr(ws), nbytes, _stream(stream)))

@@ -244,3 +244,44 @@ def test_dgrad_rejections(sc):
     assert f(p, 7, FAKE, FAKE, 32, K, S, pad, O, FAKE, FAKE, need, None) == sc.SHARD_ERR_INVALID      # dtype
     empty = sc.tile_desc(0, 16, [8, 8, 40], [1, 0, 0], [1, 0, 0])
     assert f(ctypes.byref(empty), 1, None, FAKE, 32, K, S, pad, O, None, None, 0, None) == sc.SHARD_OK  # no tile
+
+
+def test_norm_workspace_query(sc):
+    d = sc.tile_desc(1, 32, [8, 16, 40], [1, 0, 0], [1, 0, 0])
+    assert sc.shard_norm_workspace_bytes(d, sc.SHARD_BF16, 4) > 0
+    for bad in (0, 3, 64, -1):
+        with pytest.raises(sc.ShardError):
+            sc.shard_norm_workspace_bytes(d, sc.SHARD_BF16, bad)
+
+
+@pytestmark_host
+def test_norm_rejections(sc):
+    lib = _raw(sc)
+    d = sc.tile_desc(1, 32, [8, 16, 40], [1, 0, 0], [1, 0, 0])
+    p = ctypes.byref(d)
+    need = sc.shard_norm_workspace_bytes(d, sc.SHARD_BF16, 4)
+    st, ap = lib.shard_norm_stats, lib.shard_norm_apply
+    assert st(p, 1, FAKE, 3, FAKE, FAKE, need, None) == sc.SHARD_ERR_INVALID        # groups does not divide c
+    assert st(p, 1, FAKE, 4, None, FAKE, need, None) == sc.SHARD_ERR_INVALID       # null sums
+    assert st(p, 1, FAKE, 4, FAKE, FAKE, need - 1, None) == sc.SHARD_ERR_INVALID   # short workspace
+    assert st(p, 1, None, 4, FAKE, FAKE, need, None) == sc.SHARD_ERR_INVALID       # null tile
+    assert st(p, 1, FAKE, 4, ctypes.c_void_p(0x10004), FAKE, need, None) == sc.SHARD_ERR_INVALID  # misaligned
+    assert st(p, 9, FAKE, 4, FAKE, FAKE, need, None) == sc.SHARD_ERR_INVALID       # dtype
+    empty = sc.tile_desc(0, 32, [8, 16, 40])
+    assert st(ctypes.byref(empty), 1, None, 4, None, None, 0, None) == sc.SHARD_OK  # no batch items
+    args = lambda **k: [k.get(n, v) for n, v in [("tile", FAKE), ("sums", FAKE), ("count", 100.0), ("eps", 1e-5),
+                                                  ("groups", 4), ("gamma", FAKE), ("beta", FAKE), ("out", FAKE),
+                                                  ("ws", FAKE), ("nb", need)]]
+    ok = lambda **k: ap(p, 1, *args(**k), None)
+    assert ok(count=0.0) == sc.SHARD_ERR_INVALID
+    assert ok(count=float("nan")) == sc.SHARD_ERR_INVALID
+    assert ok(eps=-1.0) == sc.SHARD_ERR_INVALID
+    assert ok(groups=5) == sc.SHARD_ERR_INVALID
+    assert ok(gamma=None) == sc.SHARD_ERR_INVALID
+    assert ok(beta=None) == sc.SHARD_ERR_INVALID
+    assert ok(out=None) == sc.SHARD_ERR_INVALID
+    assert ok(sums=None) == sc.SHARD_ERR_INVALID
+    assert ok(nb=need - 1) == sc.SHARD_ERR_INVALID
+    assert ok(gamma=ctypes.c_void_p(0x10002)) == sc.SHARD_ERR_INVALID
+    flat = sc.tile_desc(1, 32, [0, 16, 40])
+    assert ap(ctypes.byref(flat), 1, None, None, 100.0, 1e-5, 4, None, None, None, None, 0, None) == sc.SHARD_OK

@@ -1,0 +1,204 @@
+"""GPU parity of domain-parallel group normalisation (shard_norm_stats,
+shard_norm_apply) against the float64 oracle.
+
+Every shard's tile carries NaN canaries in its margins, so a kernel that read a
+margin would poison its sums. Sums: integer-valued inputs bit for bit (every
+partial sum is an exact integer), fp inputs within 1e-5 of the sum of absolute
+values (S1) or of S2. Normalised interiors: after adding all shards' sums (the
+all-reduce) every shard normalises its interior, which must equal the oracle's
+whole-domain group normalisation to the fp32 / bf16 tolerance; margins keep
+their canaries.
+"""
+import numpy as np
+import pytest
+
+import synth
+import shard_cases as cases
+from gpu_util import canary_for, dev, host, log
+from oracle import norm as onorm
+
+pytestmark = pytest.mark.gpu
+
+INT_DIST = (synth.INT, (-2.0, 2.0))
+EPS = 1e-5
+
+
+@pytest.fixture(scope="module")
+def sc():
+    import torch
+    assert torch.cuda.is_available()
+    from paper_2605_11111_amd import shardconv
+    return shardconv
+
+
+def _code(sc, w):
+    return sc.SHARD_F32 if w.dtype == "f32" else sc.SHARD_BF16
+
+
+def _shard(sc, w, idx, dist):
+    sg = cases.shard_geom(w, idx)
+    tile_h = cases.interior_tile_cl(w, sg, cases.out_code(w), canary_for(w), dist)
+    desc = sc.tile_desc(w.N, w.cin, sg.ext, sg.g["halo_lo"], sg.g["halo_hi"])
+    inner = (slice(None),) + tuple(slice(l, l + e) for l, e in zip(sg.g["halo_lo"], sg.ext)) + (slice(None),)
+    return sg, desc, tile_h, inner
+
+
+def _stats(sc, w, desc, tile, groups):
+    import torch
+    n = sc.shard_norm_workspace_bytes(desc, _code(sc, w), groups)
+    ws = torch.empty(max(n, 16), dtype=torch.uint8, device="cuda")
+    sums = torch.full((w.N, groups, 2), float("nan"), dtype=torch.float64, device="cuda")
+    sc.shard_norm_stats(desc, tile, groups, sums, ws)
+    return sums
+
+
+def _groups(c):
+    return sorted(set(g for g in (1, max(1, c // 8), c) if c % g == 0))
+
+
+def _check_sums(got, x64, groups, integer):
+    ref = onorm.sums(x64, groups)
+    if integer:
+        assert np.array_equal(got, ref)
+    else:
+        absum = onorm.sums(np.abs(x64), groups)[..., 0]
+        assert np.all(np.abs(got[..., 0] - ref[..., 0]) <= 1e-5 * absum + 1e-6)
+        assert np.all(np.abs(got[..., 1] - ref[..., 1]) <= 1e-5 * ref[..., 1] + 1e-6)
+
+
+@pytest.mark.parametrize("name", list(cases.REDUCED))
+@pytest.mark.parametrize("integer", [False, True])
+def test_stats_every_shard_reduced(sc, name, integer):
+    w = cases.REDUCED[name]
+    dist = INT_DIST if integer else None
+    for idx in w.shards():
+        sg, desc, tile_h, inner = _shard(sc, w, idx, dist)
+        tile = dev(tile_h)
+        x64 = cases.to_ncdhw(cases.as_f64(tile_h[inner], w))
+        for groups in _groups(w.cin):
+            log(f"norm stats {name} shard {idx} groups {groups}")
+            got = _stats(sc, w, desc, tile, groups).cpu().numpy()
+            _check_sums(got, x64, groups, integer)
+
+
+@pytest.mark.parametrize("name", list(cases.REDUCED))
+def test_sharded_group_norm_equals_the_whole_domain(sc, name):
+    """Sums of every shard added in shard order, then every interior normalised
+    (out of place and in place, which must agree bitwise)."""
+    import torch
+    w = cases.REDUCED[name]
+    rng = np.random.default_rng(3)
+    gamma = rng.uniform(0.5, 2.0, w.cin).astype(np.float32)
+    beta = rng.uniform(-1.0, 1.0, w.cin).astype(np.float32)
+    x_full = cases.to_ncdhw(cases.as_f64(w.x_box([0] * w.nd, list(w.G)), w))
+    for groups in _groups(w.cin):
+        log(f"group norm {name} groups {groups}")
+        shards = [_shard(sc, w, idx, None) for idx in w.shards()]
+        tiles = [dev(t[2]) for t in shards]
+        total = torch.zeros((w.N, groups, 2), dtype=torch.float64, device="cuda")
+        for (sg, desc, _, _), tile in zip(shards, tiles):
+            total += _stats(sc, w, desc, tile, groups)
+        count = int(np.prod(w.G)) * (w.cin // groups)
+        ref = onorm.group_norm(x_full, groups, EPS, gamma.astype(np.float64), beta.astype(np.float64))
+        g_d, b_d = torch.from_numpy(gamma).cuda(), torch.from_numpy(beta).cuda()
+        for (sg, desc, tile_h, inner), tile in zip(shards, tiles):
+            n = sc.shard_norm_workspace_bytes(desc, _code(sc, w), groups)
+            ws = torch.empty(max(n, 16), dtype=torch.uint8, device="cuda")
+            out = dev(np.full_like(tile_h, canary_for(w)))
+            sc.shard_norm_apply(desc, tile, total, count, EPS, groups, g_d, b_d, out, ws)
+            got = host(out)
+            margin = np.ones(got.shape, dtype=bool)
+            margin[inner] = False
+            assert np.array_equal(got[margin].view(np.uint8), tile_h[margin].view(np.uint8))  # canaries kept
+            box = (slice(None), slice(None)) + tuple(slice(o, o + e) for o, e in zip(sg.off, sg.ext))
+            err = cases.norm_max_err(cases.to_ncdhw(cases.as_f64(got[inner], w)), ref[box])
+            assert err <= cases.TOL[w.dtype], (sg.off, groups, err)
+            sc.shard_norm_apply(desc, tile, total, count, EPS, groups, g_d, b_d, tile, ws)   # in place
+            assert np.array_equal(host(tile)[inner].view(np.uint8), got[inner].view(np.uint8))
+
+
+def test_stats_are_bitwise_repeatable(sc):
+    w = cases.REDUCED["c3r"]
+    sg, desc, tile_h, _ = _shard(sc, w, w.shards()[1], None)
+    tile = dev(tile_h)
+    a = _stats(sc, w, desc, tile, 4).cpu().numpy()
+    b = _stats(sc, w, desc, tile, 4).cpu().numpy()
+    assert np.array_equal(a.view(np.uint64), b.view(np.uint64))
+
+
+@pytest.mark.parametrize("dt,c,groups,aligned", [("bf16", 3, 1, True), ("f32", 5, 5, True), ("bf16", 24, 3, True),
+                                                 ("bf16", 32, 4, False), ("f32", 8, 2, False)])
+def test_element_path_shapes(sc, dt, c, groups, aligned):
+    """Channel counts or alignments outside the vector path."""
+    import torch
+    wl = cases.Workload(f"norm_{dt}_{c}", dt, 2, c, c, (9, 7, 11), (2, 1, 1), (3, 3, 3), (1, 1, 1), (1, 0, 0),
+                        x_dist=(synth.UNIFORM, (-1.0, 1.0)))
+    sg, desc, tile_h, inner = _shard(sc, wl, wl.shard, None)
+    tdt = cases.torch_dtype(wl)
+    off = 0 if aligned else 1
+    store = torch.zeros(tile_h.size + off, dtype=tdt, device="cuda")
+    tile = store[off:].view(tile_h.shape)
+    tile.copy_(dev(tile_h))
+    x64 = cases.to_ncdhw(cases.as_f64(tile_h[inner], wl))
+    sums = _stats(sc, wl, desc, tile, groups)
+    _check_sums(sums.cpu().numpy(), x64, groups, False)
+    count = x64.size // (x64.shape[0] * groups)
+    gamma = torch.linspace(0.5, 1.5, c, device="cuda")
+    beta = torch.linspace(-0.5, 0.5, c, device="cuda")
+    n = sc.shard_norm_workspace_bytes(desc, _code(sc, wl), groups)
+    ws = torch.empty(max(n, 16), dtype=torch.uint8, device="cuda")
+    ostore = torch.zeros(tile_h.size + off, dtype=tdt, device="cuda")
+    out = ostore[off:].view(tile_h.shape)
+    sc.shard_norm_apply(desc, tile, sums, count, EPS, groups, gamma, beta, out, ws)
+    ref = onorm.normalise(x64, onorm.sums(x64, groups), count, EPS, gamma.cpu().double().numpy(),
+                          beta.cpu().double().numpy(), groups)
+    err = cases.norm_max_err(cases.to_ncdhw(cases.as_f64(host(out)[inner], wl)), ref)
+    assert err <= cases.TOL[dt], err
+
+
+FULL = ["c1_2d_fp32", "c2_2d_bf16", "c5_3d_fp32_s2", "c3_3d_bf16"]
+
+
+@pytest.mark.parametrize("name", FULL)
+def test_full_size_stats_and_sampled_planes(sc, name):
+    """The measured shard at full size: its sums against the oracle's (summed
+    plane by plane), then the interior normalised with those sums as the totals
+    (one shard standing for all) and checked on sampled interior planes."""
+    import torch
+    w = cases.WORKLOADS[name]
+    groups = max(1, w.cin // 8)
+    sg = cases.shard_geom(w, w.shard)
+    log(f"full norm {name}: generating the interior")
+    inner_h = w.x_box(sg.off, [o + e for o, e in zip(sg.off, sg.ext)])
+    lo, hi = sg.g["halo_lo"], sg.g["halo_hi"]
+    P = [l + e + h for l, e, h in zip(lo, sg.ext, hi)]
+    tile = torch.empty([w.N] + P + [w.cin], dtype=cases.torch_dtype(w), device="cuda")
+    tile.fill_(float("nan"))
+    inner = (slice(None),) + tuple(slice(l, l + e) for l, e in zip(lo, sg.ext)) + (slice(None),)
+    tile[inner] = dev(inner_h)
+    desc = sc.tile_desc(w.N, w.cin, sg.ext, lo, hi)
+    sums = _stats(sc, w, desc, tile, groups).cpu().numpy()
+    ref = np.zeros((w.N, groups, 2))
+    absum = np.zeros((w.N, groups))
+    for p in range(sg.ext[0]):
+        x64 = cases.to_ncdhw(cases.as_f64(inner_h[:, p:p + 1], w))
+        ref += onorm.sums(x64, groups)
+        absum += onorm.sums(np.abs(x64), groups)[..., 0]
+    assert np.all(np.abs(sums[..., 0] - ref[..., 0]) <= 1e-5 * absum)
+    assert np.all(np.abs(sums[..., 1] - ref[..., 1]) <= 1e-5 * ref[..., 1])
+    count = int(np.prod(sg.ext)) * (w.cin // groups)
+    gamma = torch.linspace(0.5, 1.5, w.cin, device="cuda")
+    beta = torch.linspace(-0.5, 0.5, w.cin, device="cuda")
+    n = sc.shard_norm_workspace_bytes(desc, _code(sc, w), groups)
+    ws = torch.empty(max(n, 16), dtype=torch.uint8, device="cuda")
+    sc.shard_norm_apply(desc, tile, torch.from_numpy(ref).cuda(), count, EPS, groups, gamma, beta, tile, ws)
+    L = sg.ext[0]
+    for p in sorted(set([0, L // 2, L - 1])):
+        got = cases.to_ncdhw(cases.as_f64(host(tile[:, lo[0] + p:lo[0] + p + 1])[(slice(None), slice(None)) +
+                                                                              inner[2:]], w))
+        x64 = cases.to_ncdhw(cases.as_f64(inner_h[:, p:p + 1], w))
+        exp = onorm.normalise(x64, ref, count, EPS, gamma.cpu().double().numpy(), beta.cpu().double().numpy(),
+                              groups)
+        err = cases.norm_max_err(got, exp)
+        log(f"  plane {p}: normalised max err {err:.3e}")
+        assert err <= cases.TOL[w.dtype], (p, err)
