@@ -18,13 +18,12 @@ the step and reported under "next_rows"; they are not part of `value`.
 The roofline's "traffic" field is the HBM traffic of the dominant kernel measured
 with rocprofv3 counters (FETCH_SIZE and WRITE_SIZE, each scaled by what it reads
 for a plain device copy of known size) and recorded in
-profiles/<op>_<workload>_traffic.txt together with a hash of the kernel sources;
+profiles/<op>_<workload>_traffic.txt together with a hash of that kernel's sources;
 it is reported only while the sources still hash the same, else null.
 """
 from __future__ import annotations
 
 import argparse
-import glob
 import hashlib
 import json
 import os
@@ -211,6 +210,7 @@ def main():
     if not args.no_backward:
         next_rows = time_backward(sc, w, g, desc, wt, dy, send, flops, args, stream)
         next_rows.update(time_group_norm(sc, w, g, desc, tile, args, stream))
+        next_rows.update(time_folded(sc, w, g, desc, tile, wt, recv, args, stream))
 
     dt = w.dtype
     value = 2 * flops / (ms_step * 1e-3) / 1e12
@@ -319,10 +319,44 @@ def _time_ops(ops, args, stream):
     out = {}
     for i, (label, kind, work, _) in enumerate(ops):
         ms = float(np.mean([ev[k][i][0].elapsed_time(ev[k][i][1]) for k in range(args.steps)]))
-        gbs = work / (ms * 1e-3) / 1e9
-        out[label] = {"ms": round(ms, 4), "gbs": round(gbs, 1), "frac_hbm_peak": round(gbs / HBM_PEAK, 4),
-                      "bytes": int(work)}
+        if kind.startswith("mfma:"):
+            tf = work / (ms * 1e-3) / 1e12
+            out[label] = {"ms": round(ms, 4), "tflops": round(tf, 2),
+                          "frac_mfma_peak": round(tf / PEAK[kind[5:]], 4)}
+        else:
+            gbs = work / (ms * 1e-3) / 1e9
+            out[label] = {"ms": round(ms, 4), "gbs": round(gbs, 1), "frac_hbm_peak": round(gbs / HBM_PEAK, 4),
+                          "bytes": int(work)}
     return out
+
+
+def time_folded(sc, w, g, desc, tile, wt, recv, args, stream):
+    """The forward with the halo folded into its loads (margins never read; the
+    received slabs serve the margin rows), whole and as the interior / boundary
+    pair that lets the exchange overlap the interior (timed after the step, not
+    part of `value`; flops of each part are those of its outputs)."""
+    import numpy as np
+    import torch
+    tdt = torch.float32 if w.dtype == "f32" else torch.bfloat16
+    code = sc.SHARD_F32 if w.dtype == "f32" else sc.SHARD_BF16
+    O = g["out_ext"]
+    y = torch.empty([w.N] + list(O) + [w.cout], dtype=tdt, device="cuda")
+    ws = torch.empty(max(16, sc.shard_conv_workspace_bytes(0, desc, code, w.cout, w.K, w.S, O)),
+                     dtype=torch.uint8, device="cuda")
+    slabs = {(axis, side): slab for (axis, side, slab, _) in recv}
+    lo, hi = sc.shard_conv_interior(desc, w.K, w.S, g["pad_lo"], O)
+    per_vox = 2.0 * w.N * w.cout * w.cin * int(np.prod(w.K))
+    n_all = int(np.prod(O))
+    n_int = int(np.prod([b - a for a, b in zip(lo, hi)]))
+
+    def call(region, sl):
+        return lambda: sc.shard_conv_fwd_folded(desc, tile, sl, region, wt, w.cout, w.K, w.S, g["pad_lo"], O, y, ws)
+    ops = [("conv_fwd_folded", "mfma:" + w.dtype, per_vox * n_all, call(sc.SHARD_REGION_ALL, slabs)),
+           ("conv_fwd_interior", "mfma:" + w.dtype, per_vox * n_int, call(sc.SHARD_REGION_INTERIOR, None)),
+           ("conv_fwd_boundary", "mfma:" + w.dtype, per_vox * (n_all - n_int), call(sc.SHARD_REGION_BOUNDARY, slabs))]
+    res = _time_ops(ops, args, stream)
+    log("folded forward timed")
+    return res
 
 
 def time_group_norm(sc, w, g, desc, tile, args, stream):
@@ -350,11 +384,19 @@ def time_group_norm(sc, w, g, desc, tile, args, stream):
     return res
 
 
-def source_hash():
-    """sha256 over the library sources (any change invalidates recorded counters)."""
+# The source files each measured kernel is built and launched from: the kernel
+# itself, its host-side launcher and the shared headers.
+KERNEL_SOURCES = {
+    "conv_fwd": ["conv_fwd.hip", "conv_fwd_rows.hip", "common.h", "internal.h"],
+    "conv_wgrad": ["conv_wgrad.hip", "conv_wgrad_xm.hip", "common.h", "internal.h"],
+}
+
+
+def source_hash(op):
+    """sha256 over the sources of `op`'s kernel (any change to them invalidates
+    the recorded counters)."""
     h = hashlib.sha256()
-    files = sorted(glob.glob(os.path.join(ROOT, "paper_2605_11111_amd", "csrc", "*")) +
-                   glob.glob(os.path.join(ROOT, "include", "*.h")))
+    files = [os.path.join(ROOT, "paper_2605_11111_amd", "csrc", f) for f in KERNEL_SOURCES[op]]
     for f in files:
         h.update(os.path.basename(f).encode())
         with open(f, "rb") as fh:
@@ -374,7 +416,7 @@ def measured_traffic(op, workload):
             if ":" in line and not line.startswith("#"):
                 k, v = line.split(":", 1)
                 rec[k.strip()] = v.strip()
-    if rec.get("source_sha256") != source_hash():
+    if rec.get("source_sha256") != source_hash(op):
         return None
     try:
         return int(float(rec["traffic_bytes_per_launch"]))

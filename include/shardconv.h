@@ -17,6 +17,9 @@
  *   shard_halo_unpack     copy a received slab into a margin, or zero-fill it
  *   shard_conv_fwd        convolution read off the padded tile
  *   shard_conv_wgrad      the shard's partial weight gradient
+ *   shard_conv_interior   outputs that need no halo (host only)
+ *   shard_conv_fwd_folded forward reading the halo from the received slabs,
+ *                         all outputs or the interior / boundary part
  *   shard_conv_dgrad      the input gradient read back onto the padded tile
  *   shard_halo_pack_margin, shard_halo_accumulate
  *                         the reverse halo exchange of the backward pass
@@ -162,6 +165,61 @@ shard_status_t shard_conv_fwd(const shard_tile_t* x, shard_dtype_t dtype, const 
                               int64_t c_out, const int64_t kernel[], const int64_t stride[],
                               const int64_t pad_lo[], const int64_t out_ext[], void* y, void* ws,
                               size_t ws_bytes, hipStream_t stream);
+
+/*
+ * Received halo slabs for the folded entry points: slab[a][side] is the slab
+ * the neighbour on (axis a, side 0 = lo / 1 = hi) sent, laid out as
+ * shard_halo_slab_shape(x, a, that margin's width) gives, in the tile's dtype,
+ * aligned to the element size (16-byte alignment keeps the fast loads); NULL
+ * where the side is a global boundary (zeros).
+ * Entries of sides whose margin width is 0 are ignored.
+ */
+typedef struct {
+    const void* slab[3][2];
+} shard_halo_src_t;
+
+typedef enum {
+    SHARD_REGION_ALL = 0,      /* every owned output */
+    SHARD_REGION_INTERIOR = 1, /* outputs whose input rows avoid every margin */
+    SHARD_REGION_BOUNDARY = 2  /* the other outputs */
+} shard_region_t;
+
+/*
+ * The interior outputs of a convolution read off the padded tile: per axis,
+ * outputs j in [int_lo[a], int_hi[a]) whose input rows j*S - pad_lo + t,
+ * t < kernel[a], all lie in the interior [halo_lo[a], halo_lo[a] + ext[a])
+ * (all outputs on an axis without margins). They depend on no halo, so they can
+ * be computed while the halo exchange (section "PyTorch Dispatch") is in
+ * flight; the paper lists such communication/computation overlap as missing
+ * (section "Limitations"). An empty interior has int_lo == int_hi. Host only.
+ * Errors: SHARD_ERR_INVALID for malformed arguments.
+ */
+shard_status_t shard_conv_interior(const shard_tile_t* x, const int64_t kernel[], const int64_t stride[],
+                                   const int64_t pad_lo[], const int64_t out_ext[], int64_t int_lo[],
+                                   int64_t int_hi[]);
+
+/*
+ * shard_conv_fwd with the halo folded into the tile loads: the contents of the
+ * tile's margins never affect the result and are never written; the
+ * convolution reads each margin voxel from the received slab of its margin
+ * (`halo`, NULL = no slabs: every margin zero), a corner voxel from the slab of
+ * the later axis. The result equals shard_halo_unpack of every slab in
+ * ascending axis order followed by shard_conv_fwd, without the copies into the
+ * margins: bit for bit when both calls select the same kernel (margins on one
+ * axis, 16-byte aligned slabs) and on integer-valued data, otherwise up to the
+ * order of the floating-point sums.
+ *   region  SHARD_REGION_ALL, _INTERIOR or _BOUNDARY (shard_region_t): which
+ *           outputs are written; the others in y are left untouched. INTERIOR
+ *           reads no slab; INTERIOR then BOUNDARY writes what ALL writes.
+ * Other arguments, workspace and errors: as shard_conv_fwd (the same workspace
+ * size serves every region); SHARD_ERR_INVALID also for an unknown region or a
+ * slab not aligned to the element size.
+ */
+shard_status_t shard_conv_fwd_folded(const shard_tile_t* x, shard_dtype_t dtype, const void* tile,
+                                     const shard_halo_src_t* halo, int32_t region, const void* w, int64_t c_out,
+                                     const int64_t kernel[], const int64_t stride[], const int64_t pad_lo[],
+                                     const int64_t out_ext[], void* y, void* ws, size_t ws_bytes,
+                                     hipStream_t stream);
 
 /*
  * Weight gradient of the shard (its partial; summing the partials of all

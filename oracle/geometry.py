@@ -81,3 +81,22 @@ def offsets(sizes) -> list:
         out.append(acc)
         acc += s
     return out
+
+
+def interior_outputs(lo: int, ext: int, hi: int, K: int, S: int, pad_lo: int, n_out: int) -> list:
+    """Outputs j along one axis of a padded tile (margins lo and hi around ext
+    interior rows) that read no margin row: every input row j*S - pad_lo + t,
+    t < K, lies in the interior [lo, lo + ext) on each side that has a margin
+    (an axis without margins: every output). They depend on no halo, so they can
+    be computed while the exchange (section "PyTorch Dispatch") is in flight,
+    the communication/computation overlap the paper lists as missing (section
+    "Limitations"). Listed one by one."""
+    out = []
+    for j in range(n_out):
+        rows = [j * S - pad_lo + t for t in range(K)]
+        if lo > 0 and min(rows) < lo:
+            continue
+        if hi > 0 and max(rows) >= lo + ext:
+            continue
+        out.append(j)
+    return out

@@ -1,5 +1,6 @@
 // C-ABI entry points: argument validation on the host (before any launch, so
 // an error writes nothing), normalisation to three spatial axes, dispatch.
+#include <algorithm>
 #include <cstdlib>
 #include <cstring>
 
@@ -162,6 +163,63 @@ BoxCopy make_box(const Tile3& t, int k, int64_t r0, int64_t r1)
 
 shard_status_t map_hip(hipError_t e) { return e == hipSuccess ? SHARD_OK : SHARD_ERR_HIP; }
 
+// Interior outputs per internal axis: [jlo, jhi) of the outputs whose input rows
+// j*S - pad + t (t < K) lie in [lo, lo + ext); every output on an axis without
+// margins. jhi >= jlo.
+void interior_box(const Tile3& t, const Conv3& cv, int64_t jlo[3], int64_t jhi[3])
+{
+    for (int k = 0; k < 3; ++k) {
+        jlo[k] = 0;
+        jhi[k] = cv.O[k];
+        if (t.lo[k] > 0) {
+            const int64_t a = t.lo[k] + cv.pad[k];  // first j with j*S - pad >= lo
+            jlo[k] = a <= 0 ? 0 : std::min(cv.O[k], ceil_div(a, cv.S[k]));
+        }
+        if (t.hi[k] > 0) {
+            const int64_t b = t.lo[k] + t.ext[k] - cv.K[k] + cv.pad[k];  // last j has j*S <= b
+            jhi[k] = b < 0 ? 0 : std::min(cv.O[k], b / cv.S[k] + 1);
+        }
+        if (jhi[k] < jlo[k]) jhi[k] = jlo[k];
+    }
+}
+
+// The output boxes of a region: ALL is the owned box, INTERIOR the interior box,
+// BOUNDARY the owned box minus the interior, peeled axis by axis (axis k's two
+// slabs span the interior on earlier axes and everything on later ones).
+int region_boxes(const Tile3& t, const Conv3& cv, int32_t region, Region out[6])
+{
+    int nb = 0;
+    int64_t jlo[3], jhi[3];
+    interior_box(t, cv, jlo, jhi);
+    if (region == SHARD_REGION_ALL || region == SHARD_REGION_INTERIOR) {
+        Region r{};
+        for (int k = 0; k < 3; ++k) {
+            r.org[k] = region == SHARD_REGION_ALL ? 0 : jlo[k];
+            r.ext[k] = region == SHARD_REGION_ALL ? cv.O[k] : jhi[k] - jlo[k];
+        }
+        out[nb++] = r;
+        return nb;
+    }
+    for (int k = 0; k < 3; ++k) {
+        for (int sd = 0; sd < 2; ++sd) {
+            Region r{};
+            for (int b = 0; b < 3; ++b) {
+                if (b < k) {
+                    r.org[b] = jlo[b];
+                    r.ext[b] = jhi[b] - jlo[b];
+                } else if (b > k) {
+                    r.org[b] = 0;
+                    r.ext[b] = cv.O[b];
+                }
+            }
+            r.org[k] = sd == 0 ? 0 : jhi[k];
+            r.ext[k] = sd == 0 ? jlo[k] : cv.O[k] - jhi[k];
+            if (r.ext[0] * r.ext[1] * r.ext[2] > 0) out[nb++] = r;
+        }
+    }
+    return nb;
+}
+
 }  // namespace
 
 extern "C" {
@@ -295,6 +353,85 @@ shard_status_t shard_conv_fwd(const shard_tile_t* x, shard_dtype_t dtype, const 
     if (!aligned(tile, t.esz) || !aligned(w, t.esz) || !aligned(y, t.esz) || !aligned(ws, 16))
         return SHARD_ERR_INVALID;
     return map_hip(launch_conv_fwd(t, cv, dtype, tile, w, y, ws, stream));
+}
+
+shard_status_t shard_conv_interior(const shard_tile_t* x, const int64_t kernel[], const int64_t stride[],
+                                   const int64_t pad_lo[], const int64_t out_ext[], int64_t int_lo[],
+                                   int64_t int_hi[])
+{
+    Tile3 t;
+    Conv3 cv;
+    if (!norm_tile(x, SHARD_F32, t) || !pad_lo || !int_lo || !int_hi ||
+        !norm_conv(x, t, 1, kernel, stride, pad_lo, out_ext, cv))
+        return SHARD_ERR_INVALID;
+    int64_t jlo[3], jhi[3];
+    interior_box(t, cv, jlo, jhi);
+    const int off = 3 - x->ndim;
+    for (int a = 0; a < x->ndim; ++a) {
+        int_lo[a] = jlo[off + a];
+        int_hi[a] = jhi[off + a];
+    }
+    return SHARD_OK;
+}
+
+shard_status_t shard_conv_fwd_folded(const shard_tile_t* x, shard_dtype_t dtype, const void* tile,
+                                     const shard_halo_src_t* halo, int32_t region, const void* w, int64_t c_out,
+                                     const int64_t kernel[], const int64_t stride[], const int64_t pad_lo[],
+                                     const int64_t out_ext[], void* y, void* ws, size_t ws_bytes,
+                                     hipStream_t stream)
+{
+    Tile3 t;
+    Conv3 cv;
+    if (!norm_tile(x, dtype, t) || !pad_lo || !norm_conv(x, t, c_out, kernel, stride, pad_lo, out_ext, cv))
+        return SHARD_ERR_INVALID;
+    if (region != SHARD_REGION_ALL && region != SHARD_REGION_INTERIOR && region != SHARD_REGION_BOUNDARY)
+        return SHARD_ERR_INVALID;
+    if (t.n * cv.out_voxels() == 0) return SHARD_OK;
+    const size_t need = conv_fwd_workspace(t, cv, dtype);
+    if (ws_bytes < need || (need > 0 && !ws)) return SHARD_ERR_INVALID;
+    if ((tile_elems(t) > 0 && !tile) || !w || !y) return SHARD_ERR_INVALID;
+    if (!aligned(tile, t.esz) || !aligned(w, t.esz) || !aligned(y, t.esz) || !aligned(ws, 16))
+        return SHARD_ERR_INVALID;
+    Fold f{};
+    const int off = 3 - x->ndim;
+    for (int k = 0; k < 3; ++k) {
+        f.lo[k] = t.lo[k];
+        f.ext[k] = t.ext[k];
+        f.P[k] = t.P[k];
+        if (t.lo[k] > 0 || t.hi[k] > 0) f.mask |= 1u << k;
+        for (int sd = 0; sd < 2; ++sd) {
+            const int64_t width = sd == 0 ? t.lo[k] : t.hi[k];
+            const void* p = (halo && k >= off && width > 0) ? halo->slab[k - off][sd] : nullptr;
+            if (!aligned(p, t.esz)) return SHARD_ERR_INVALID;
+            f.slab[k][sd] = static_cast<const char*>(p);
+        }
+    }
+    const OutMap om = dense_out(cv);
+    const Fold* fold = f.mask ? &f : nullptr;
+    const FwdFamily fam = fwd_family(t, cv, dtype, tile, y, om, fold, ws);
+    // The interior outputs read no margin, so the plain kernels serve them (rows
+    // a brick stages past the region feed only outputs that are not written).
+    // On the W-march kernel the folded loads cost more than a separate launch
+    // over the boundary, so the whole box runs as interior + boundary there.
+    Region boxes[7];
+    bool folded[7];
+    int nb = 0;
+    if (region == SHARD_REGION_ALL && fold && fam == FWD_ROWS) {
+        nb = region_boxes(t, cv, SHARD_REGION_INTERIOR, boxes);
+        for (int i = 0; i < nb; ++i) folded[i] = false;
+        const int nbb = region_boxes(t, cv, SHARD_REGION_BOUNDARY, boxes + nb);
+        for (int i = nb; i < nb + nbb; ++i) folded[i] = true;
+        nb += nbb;
+    } else {
+        nb = region_boxes(t, cv, region, boxes);
+        for (int i = 0; i < nb; ++i) folded[i] = fold && region != SHARD_REGION_INTERIOR;
+    }
+    for (int i = 0; i < nb; ++i) {
+        const hipError_t e = launch_conv_fwd_region(t, cv, dtype, tile, w, y, om, boxes[i], folded[i] ? fold : nullptr,
+                                                    fam, ws, stream);
+        if (e != hipSuccess) return SHARD_ERR_HIP;
+    }
+    return SHARD_OK;
 }
 
 shard_status_t shard_conv_wgrad(const shard_tile_t* x, shard_dtype_t dtype, const void* tile, const void* dy,

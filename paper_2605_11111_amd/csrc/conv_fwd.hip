@@ -60,6 +60,8 @@ struct FwdArgs {
     int32_t vec;       // 16-byte loads allowed (tile base and channel rows aligned)
     int64_t nblocks;
     int64_t ybase, ys[4];  // output map: element of (n, o0, o1, o2, co) = ybase + n*ys0 + ... + co
+    int64_t org[3];        // origin of the computed region of outputs (O is its extent)
+    Fold fold;             // halo folded into the loads when fold.mask != 0
 };
 
 struct PlanF {
@@ -93,6 +95,36 @@ __device__ __forceinline__ void stage_brick(const FwdArgs& a, uint4* lds, int64_
     const int biv = a.BI[0] * a.BI[1] * a.BI[2];
     const int total = biv * nq;
     const bool vec_ok = a.vec != 0;
+    if (a.fold.mask) {
+        // margin voxels come from the received slabs (or are zero)
+        for (int u = threadIdx.x; u < total; u += kThreads) {
+            const int q = u % nq;
+            const int v = u / nq;
+            const int x = v % a.BI[2];
+            const int yz = v / a.BI[2];
+            const int y = yz % a.BI[1];
+            const int z = yz / a.BI[1];
+            const int64_t t0 = i0[0] + z, t1 = i0[1] + y, t2 = i0[2] + x;
+            const int c = c0 + q * kPerUnit;
+            uint4 val = make_uint4(0, 0, 0, 0);
+            if (t0 >= 0 && t0 < a.P[0] && t1 >= 0 && t1 < a.P[1] && t2 >= 0 && t2 < a.P[2] && c < a.cin) {
+                const char* vox = fold_voxel(a.fold, a.tile, nn, t0, t1, t2, a.cin * Traits<T>::esz);
+                if (vox) {
+                    const T* src = reinterpret_cast<const T*>(vox) + c;
+                    if (vec_ok && c + kPerUnit <= a.cin) {
+                        val = *reinterpret_cast<const uint4*>(src);
+                    } else {
+                        T tmp[kPerUnit];
+#pragma unroll
+                        for (int e = 0; e < kPerUnit; ++e) tmp[e] = (c + e < a.cin) ? src[e] : T(0);
+                        val = *reinterpret_cast<const uint4*>(tmp);
+                    }
+                }
+            }
+            lds[v * nq + (q ^ swz(v, a.vpl_s, a.qmask))] = val;
+        }
+        return;
+    }
     for (int u = threadIdx.x; u < total; u += kThreads) {
         const int q = u % nq;
         const int v = u / nq;
@@ -158,7 +190,8 @@ __global__ __launch_bounds__(kThreads, 2) void conv_fwd_tiled(FwdArgs a)
     const int bz = int(b % a.NB[0]);
     const int64_t nn = b / a.NB[0];
     const int64_t ob[3] = {int64_t(bz) * a.BO[0], int64_t(by) * a.BO[1], int64_t(bx) * a.BO[2]};
-    const int64_t i0[3] = {ob[0] * a.S[0] - a.pad[0], ob[1] * a.S[1] - a.pad[1], ob[2] * a.S[2] - a.pad[2]};
+    const int64_t i0[3] = {(a.org[0] + ob[0]) * a.S[0] - a.pad[0], (a.org[1] + ob[1]) * a.S[1] - a.pad[1],
+                           (a.org[2] + ob[2]) * a.S[2] - a.pad[2]};
     const int nt0 = ngi * RN;
     const int bov = a.BO[0] * a.BO[1] * a.BO[2];
 
@@ -252,7 +285,8 @@ __global__ __launch_bounds__(kThreads, 2) void conv_fwd_tiled(FwdArgs a)
             const int oz = f / (a.BO[2] * a.BO[1]);
             const int64_t o0 = ob[0] + oz, o1 = ob[1] + oy, o2 = ob[2] + ox;
             if (o0 >= a.O[0] || o1 >= a.O[1] || o2 >= a.O[2]) continue;
-            const int64_t vox = a.ybase + nn * a.ys[0] + o0 * a.ys[1] + o1 * a.ys[2] + o2 * a.ys[3];
+            const int64_t vox = a.ybase + nn * a.ys[0] + (a.org[0] + o0) * a.ys[1] + (a.org[1] + o1) * a.ys[2] +
+                                (a.org[2] + o2) * a.ys[3];
 #pragma unroll
             for (int j = 0; j < RN; ++j) {
                 const int64_t co = int64_t(nt0 + j) * 32 + row;
@@ -416,19 +450,45 @@ hipError_t launch_tiled(const PlanF& pl, hipStream_t s)
                            pl.lds, s);
 }
 
+// Whether every buffer the loads may read is 16-byte aligned.
+bool loads_aligned(const void* tile, const Fold* fold)
+{
+    if (reinterpret_cast<uintptr_t>(tile) % 16 != 0) return false;
+    if (fold)
+        for (int k = 0; k < 3; ++k)
+            for (int sd = 0; sd < 2; ++sd)
+                if (reinterpret_cast<uintptr_t>(fold->slab[k][sd]) % 16 != 0) return false;
+    return true;
+}
+
+bool dense_map(const Conv3& cv, const OutMap& om)
+{
+    const OutMap dm = dense_out(cv);
+    return om.base == 0 && om.str[0] == dm.str[0] && om.str[1] == dm.str[1] && om.str[2] == dm.str[2] &&
+           om.str[3] == dm.str[3];
+}
+
 template <typename T>
 hipError_t run_fwd(const Tile3& t, const Conv3& cv, const void* tile, const void* w, void* y, const OutMap& om,
-                   void* ws, hipStream_t s)
+                   const Region& rg, const Fold* fold, bool rows, void* ws, hipStream_t s)
 {
+    // the plan of the whole output box, its brick grid cut to the region: every
+    // output is summed in the same order whatever region computes it
     PlanF pl = plan_fwd_t<T>(t, cv);
     if (!pl.ok) return hipErrorInvalidValue;
-    const OutMap dm = dense_out(cv);
-    const bool dense = om.base == 0 && om.str[0] == dm.str[0] && om.str[1] == dm.str[1] && om.str[2] == dm.str[2] &&
-                       om.str[3] == dm.str[3];
+    for (int k = 0; k < 3; ++k) {
+        pl.a.O[k] = rg.ext[k];
+        pl.a.NB[k] = int32_t(ceil_div(rg.ext[k], pl.a.BO[k]));
+    }
+    pl.a.nblocks = t.n * int64_t(pl.a.NB[0]) * pl.a.NB[1] * pl.a.NB[2] * pl.a.ng;
     pl.a.ybase = om.base;
-    for (int k = 0; k < 4; ++k) pl.a.ys[k] = om.str[k];
+    for (int k = 0; k < 4; ++k) {
+        pl.a.ys[k] = om.str[k];
+        if (k < 3) pl.a.org[k] = rg.org[k];
+    }
+    if (fold) pl.a.fold = *fold;
     pl.a.tile = static_cast<const char*>(tile);
-    pl.a.vec = (reinterpret_cast<uintptr_t>(tile) % 16 == 0) && (t.c * Traits<T>::esz) % 16 == 0;
+    pl.a.vec = loads_aligned(tile, fold) && (t.c * Traits<T>::esz) % 16 == 0;
     pl.a.wfrag = static_cast<const uint4*>(ws);
     pl.a.y = static_cast<char*>(y);
     const int taps = int(cv.taps());
@@ -438,11 +498,9 @@ hipError_t run_fwd(const Tile3& t, const Conv3& cv, const void* tile, const void
                        static_cast<uint4*>(ws), t.c, cv.cout, taps, pl.a.nkc, pl.a.nt);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-    if (dense) {
-        e = launch_conv_fwd_rows(t, cv, std::is_same<T, bf16_t>::value ? SHARD_BF16 : SHARD_F32, tile, ws,
-                                 pl.a.nkc, pl.a.nt, y, s);
-        if (e != hipErrorNotSupported) return e;
-    }
+    if (rows)
+        return launch_conv_fwd_rows(t, cv, std::is_same<T, bf16_t>::value ? SHARD_BF16 : SHARD_F32, tile, ws,
+                                    pl.a.nkc, pl.a.nt, y, rg, fold, s);
     if (pl.rm == 4 && pl.rn == 1) return launch_tiled<T, 4, 1>(pl, s);
     if (pl.rm == 4 && pl.rn == 2) return launch_tiled<T, 4, 2>(pl, s);
     if (pl.rm == 2 && pl.rn == 2) return launch_tiled<T, 2, 2>(pl, s);
@@ -454,7 +512,7 @@ hipError_t run_fwd(const Tile3& t, const Conv3& cv, const void* tile, const void
 
 size_t generic_wgrad_workspace(const Tile3& t, const Conv3& cv);
 hipError_t generic_conv_fwd(const Tile3& t, const Conv3& cv, shard_dtype_t dt, const void* tile, const void* w,
-                            void* y, const OutMap& om, hipStream_t s);
+                            void* y, const OutMap& om, const Region& rg, const Fold* fold, hipStream_t s);
 
 OutMap dense_out(const Conv3& cv)
 {
@@ -472,14 +530,35 @@ size_t conv_fwd_workspace(const Tile3& t, const Conv3& cv, shard_dtype_t dt)
     return dt == SHARD_BF16 ? wfrag_bytes<bf16_t>(t, cv) : wfrag_bytes<float>(t, cv);
 }
 
+FwdFamily fwd_family(const Tile3& t, const Conv3& cv, shard_dtype_t dt, const void* tile, const void* y,
+                     const OutMap& om, const Fold* fold, const void* ws)
+{
+    if (force_generic() || !tiled_supported(t, cv)) return FWD_GENERIC;
+    const PlanF pl = dt == SHARD_BF16 ? plan_fwd_t<bf16_t>(t, cv) : plan_fwd_t<float>(t, cv);
+    if (!pl.ok) return FWD_GENERIC;
+    if (dense_map(cv, om) && conv_fwd_rows_supported(t, cv, dt, tile, ws, pl.a.nkc, pl.a.nt, y, fold))
+        return FWD_ROWS;
+    return FWD_TILED;
+}
+
+hipError_t launch_conv_fwd_region(const Tile3& t, const Conv3& cv, shard_dtype_t dt, const void* tile,
+                                  const void* w, void* y, const OutMap& om, const Region& rg, const Fold* fold,
+                                  FwdFamily fam, void* ws, hipStream_t s)
+{
+    if (t.n * rg.ext[0] * rg.ext[1] * rg.ext[2] == 0) return hipSuccess;
+    if (fam == FWD_GENERIC) return generic_conv_fwd(t, cv, dt, tile, w, y, om, rg, fold, s);
+    const bool rows = fam == FWD_ROWS;
+    return dt == SHARD_BF16 ? run_fwd<bf16_t>(t, cv, tile, w, y, om, rg, fold, rows, ws, s)
+                            : run_fwd<float>(t, cv, tile, w, y, om, rg, fold, rows, ws, s);
+}
+
 hipError_t launch_conv_fwd_mapped(const Tile3& t, const Conv3& cv, shard_dtype_t dt, const void* tile,
                                   const void* w, void* y, const OutMap& om, void* ws, hipStream_t s)
 {
-    const bool tiled = !force_generic() && tiled_supported(t, cv) &&
-                       (dt == SHARD_BF16 ? plan_fwd_t<bf16_t>(t, cv).ok : plan_fwd_t<float>(t, cv).ok);
-    if (!tiled) return generic_conv_fwd(t, cv, dt, tile, w, y, om, s);
-    return dt == SHARD_BF16 ? run_fwd<bf16_t>(t, cv, tile, w, y, om, ws, s)
-                            : run_fwd<float>(t, cv, tile, w, y, om, ws, s);
+    Region all{};
+    for (int k = 0; k < 3; ++k) all.ext[k] = cv.O[k];
+    const FwdFamily fam = fwd_family(t, cv, dt, tile, y, om, nullptr, ws);
+    return launch_conv_fwd_region(t, cv, dt, tile, w, y, om, all, nullptr, fam, ws, s);
 }
 
 hipError_t launch_conv_fwd(const Tile3& t, const Conv3& cv, shard_dtype_t dt, const void* tile, const void* w,

@@ -61,6 +61,13 @@ struct XmArgs {
     uint32_t batch_bytes;   // tile bytes per batch item (< 2^32)
     uint32_t ybatch_bytes;  // output bytes per batch item (< 2^32)
     int32_t cout;
+    int32_t org[2], oend[2];  // computed outputs along axes 0, 1: [org, oend) (O gives the strides)
+    // halo folded into the loads along axis fa (0 or 1): padded rows c < flo come
+    // from fslab[0], rows c >= fhi from fslab[1] (null: zero), the rest from the tile
+    const char* fslab[2];
+    uint32_t fbatch[2];  // slab bytes per batch item
+    uint32_t fSZ[2];     // slab stride along axis 0, bytes
+    int32_t fa, flo, fhi;
 };
 
 // 16-byte unit swizzle of voxel x for UPV units per voxel (see file comment).
@@ -76,6 +83,9 @@ struct XmCfg {
     static_assert(CIN == 32 || CIN == 64, "16-byte units per voxel: 4 or 8");
     static_assert(WZ * WY * WC == 4, "four waves");
     static_assert(NBUF >= 2 && NBUF <= 4, "stage depth");
+    // a tile's last row is finished while the next tile's first row multiplies:
+    // they need distinct accumulators
+    static_assert(R >= 2, "two or more output rows per wave");
     static constexpr int KW = 3;
     static constexpr int UPV = CIN / 8;
     static constexpr int NKC = CIN / 16;
@@ -95,7 +105,7 @@ struct XmCfg {
     static_assert(NBUF <= 4 && VM_BASE + EPI_STORES * 2 < 64, "vmcnt range");
 };
 
-template <int CIN, int KD, int KH, int WZ, int WY, int WC, int R, int NBUF>
+template <int CIN, int KD, int KH, int WZ, int WY, int WC, int R, int NBUF, bool FOLD>
 __global__ __launch_bounds__(256, 1) void conv_fwd_xm(XmArgs a)
 {
     using C = XmCfg<CIN, KD, KH, WZ, WY, WC, R, NBUF>;
@@ -176,31 +186,65 @@ __global__ __launch_bounds__(256, 1) void conv_fwd_xm(XmArgs a)
     // out-of-range offset and loads as zero.
     __amdgpu_buffer_rsrc_t st_r = __builtin_amdgcn_make_buffer_rsrc(const_cast<char*>(a.tile), short(0),
                                                                     int(a.batch_bytes), 0x00020000);
+    // folded halo: the received slabs of this batch item (a missing slab is a
+    // zero-length buffer, so its rows load as zero)
+    __amdgpu_buffer_rsrc_t st_rl = st_r, st_rh = st_r;
     char* st_dst = lds;
     uint32_t st_vbase = 0;
-    int32_t st_i0 = 0, st_vy = 0;
+    int32_t st_i0 = 0, st_i1 = 0, st_vy = 0;
     bool st_okx = false;
     auto stage_setup = [&](const Pos& p, int buf) {
         const bool live = p.brick < a.nbricks;
         const int bz = live ? p.bz : 0, by = live ? p.by : 0;
         const uint32_t nn = live ? p.nn : 0;
-        st_i0 = bz * C::BZ - a.pad[0];
-        const int i1 = by * C::BY - a.pad[1];
+        st_i0 = a.org[0] + bz * C::BZ - a.pad[0];
+        st_i1 = a.org[1] + by * C::BY - a.pad[1];
         const int i2 = p.j * 32;
-        const int64_t origin = ((int64_t(st_i0) * a.P[1] + i1) * a.P[2] + i2) * (CIN * 2);
+        const int64_t origin = ((int64_t(st_i0) * a.P[1] + st_i1) * a.P[2] + i2) * (CIN * 2);
         st_r = __builtin_amdgcn_make_buffer_rsrc(const_cast<char*>(a.tile) + int64_t(nn) * a.batch_bytes, short(0),
                                                  int(a.batch_bytes), 0x00020000);
+        if (FOLD) {
+            st_rl = __builtin_amdgcn_make_buffer_rsrc(
+                const_cast<char*>(a.fslab[0] ? a.fslab[0] + int64_t(nn) * a.fbatch[0] : a.tile), short(0),
+                a.fslab[0] ? int(a.fbatch[0]) : 0, 0x00020000);
+            st_rh = __builtin_amdgcn_make_buffer_rsrc(
+                const_cast<char*>(a.fslab[1] ? a.fslab[1] + int64_t(nn) * a.fbatch[1] : a.tile), short(0),
+                a.fslab[1] ? int(a.fbatch[1]) : 0, 0x00020000);
+        }
         st_dst = lds + buf * C::STAGE_BYTES + wave * 64 * 16;
         st_vbase = uint32_t(origin) + tb;
-        st_vy = i1 + hs;
+        st_vy = st_i1 + hs;
         st_okx = live && uint32_t(i2 + xs) < uint32_t(a.P[2]);
     };
     auto stage_load = [&](int it) {
         const int row0 = it * C::RPI;
         const int rz = row0 / C::IRY, ry = row0 % C::IRY;
         const bool ok = st_okx && uint32_t(st_i0 + rz) < uint32_t(a.P[0]) && uint32_t(st_vy + ry) < uint32_t(a.P[1]);
-        const uint32_t off = ok ? st_vbase + uint32_t(rz) * SZ + uint32_t(ry) * SY : a.batch_bytes;
-        __builtin_amdgcn_raw_ptr_buffer_load_lds(st_r, SC_LDS(st_dst + it * 4096), 16, off, 0, 0, 0);
+        uint32_t off = st_vbase + uint32_t(rz) * SZ + uint32_t(ry) * SY;
+        if (FOLD) {
+            // the row's coordinate along the fold axis is uniform over the
+            // instruction (one D row per instruction; one H row when fa == 1)
+            const int32_t z = st_i0 + rz;
+            const int32_t c = a.fa == 0 ? z : st_i1 + ry;
+            const uint32_t sfa = a.fa == 0 ? SZ : SY;
+            // one load per branch: the buffer descriptor stays scalar (a select of
+            // descriptors compiles to a per-lane loop)
+            if (c < a.flo) {
+                off -= uint32_t(z) * (SZ - a.fSZ[0]);
+                __builtin_amdgcn_raw_ptr_buffer_load_lds(st_rl, SC_LDS(st_dst + it * 4096), 16,
+                                                         ok ? off : 0xFFFFFFC0u, 0, 0, 0);
+            } else if (c >= a.fhi) {
+                off -= uint32_t(z) * (SZ - a.fSZ[1]) + uint32_t(a.fhi) * sfa;
+                __builtin_amdgcn_raw_ptr_buffer_load_lds(st_rh, SC_LDS(st_dst + it * 4096), 16,
+                                                         ok ? off : 0xFFFFFFC0u, 0, 0, 0);
+            } else {
+                __builtin_amdgcn_raw_ptr_buffer_load_lds(st_r, SC_LDS(st_dst + it * 4096), 16,
+                                                         ok ? off : 0xFFFFFFC0u, 0, 0, 0);
+            }
+        } else {
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(st_r, SC_LDS(st_dst + it * 4096), 16, ok ? off : a.batch_bytes,
+                                                     0, 0, 0);
+        }
     };
     // load it of a unit goes out in MFMA step step_of(it) of the tile before; the
     // last in the last step, after that step's stores
@@ -228,7 +272,7 @@ __global__ __launch_bounds__(256, 1) void conv_fwd_xm(XmArgs a)
         bool store;
     };
     auto tile_out = [&](const Pos& p) {
-        return TileOut{p.j, p.bz * C::BZ + wz, p.by * C::BY + wy * R, p.nn, p.j >= p.jstore};
+        return TileOut{p.j, a.org[0] + p.bz * C::BZ + wz, a.org[1] + p.by * C::BY + wy * R, p.nn, p.j >= p.jstore};
     };
 
     f32x16_r acc[R][KW];
@@ -277,7 +321,7 @@ __global__ __launch_bounds__(256, 1) void conv_fwd_xm(XmArgs a)
                 // so they are the carry terms alone (lane half 0: s1 + t0 and v0)
                 const int o1 = t.o1b + rr;
                 const int ox = t.j * 32 + a.pad[2] + 30;
-                if (g == 0 && t.store && t.o0 < a.O[0] && o1 < a.O[1]) {
+                if (g == 0 && t.store && t.o0 < a.oend[0] && o1 < a.oend[1]) {
                     __amdgpu_buffer_rsrc_t yr = __builtin_amdgcn_make_buffer_rsrc(
                         a.y + int64_t(t.nn) * a.ybatch_bytes, short(0), int(a.ybatch_bytes), 0x00020000);
                     const uint32_t rbase = uint32_t((int64_t(t.o0) * a.O[1] + o1) * a.O[2]);
@@ -317,7 +361,7 @@ __global__ __launch_bounds__(256, 1) void conv_fwd_xm(XmArgs a)
             __amdgpu_buffer_rsrc_t yr = __builtin_amdgcn_make_buffer_rsrc(
                 a.y + int64_t(t.nn) * a.ybatch_bytes, short(0), int(a.ybatch_bytes), 0x00020000);
             const int o1 = t.o1b + rr;
-            const bool rowok = t.store && t.o0 < a.O[0] && o1 < a.O[1];
+            const bool rowok = t.store && t.o0 < a.oend[0] && o1 < a.oend[1];
             const uint32_t rbase = uint32_t((int64_t(t.o0) * a.O[1] + o1) * a.O[2]);
 #pragma unroll
             for (int it = 0; it < 2; ++it) {
@@ -476,12 +520,49 @@ __global__ __launch_bounds__(256, 1) void conv_fwd_xm(XmArgs a)
     wait_vm_barrier<0>();
 }
 
+// A folded halo the staging loads can take: margins on one axis, 0 or 1, whose
+// rows are uniform over a load instruction (rpi staged rows per instruction
+// share their D row, so axis 1 needs rpi == 1), 16-byte aligned slabs of < 4 GiB
+// per batch item.
+bool fold_fits(const Tile3& t, const Fold& f, int rpi)
+{
+    if (f.mask != 1u && f.mask != 2u) return false;
+    const int k = f.mask == 1u ? 0 : 1;
+    if (k == 1 && rpi != 1) return false;
+    const int64_t SY = t.P[2] * t.c * 2;
+    for (int sd = 0; sd < 2; ++sd) {
+        const int64_t w = sd == 0 ? t.lo[k] : t.hi[k];
+        if (reinterpret_cast<uintptr_t>(f.slab[k][sd]) % 16 != 0) return false;
+        const int64_t bb = (k == 0 ? w * t.P[1] : t.P[0] * w) * SY;
+        if (bb >= (int64_t(1) << 32) - 64) return false;
+    }
+    return true;
+}
+
 template <int CIN, int KD, int KH, int WZ, int WY, int WC, int R, int NBUF>
-hipError_t launch_xm(const Tile3& t, const Conv3& cv, const void* tile, const void* wfrag, void* y, hipStream_t s)
+hipError_t launch_xm(const Tile3& t, const Conv3& cv, const void* tile, const void* wfrag, void* y, const Region& rg,
+                     const Fold* fold, hipStream_t s)
 {
     using C = XmCfg<CIN, KD, KH, WZ, WY, WC, R, NBUF>;
     static_assert(C::LDS_BYTES <= 160 * 1024, "LDS budget");
     XmArgs a{};
+    a.fa = -1;
+    if (fold) {
+        if (!fold_fits(t, *fold, C::RPI)) return hipErrorNotSupported;
+        a.fa = fold->mask == 1u ? 0 : 1;
+        const int k = a.fa;
+        a.flo = int32_t(t.lo[k]);
+        a.fhi = int32_t(t.lo[k] + t.ext[k]);
+        const int64_t SY = t.P[2] * t.c * 2;
+        for (int sd = 0; sd < 2; ++sd) {
+            const int64_t w = sd == 0 ? t.lo[k] : t.hi[k];
+            // slab [P0 or w][w or P1][P2][c]: no margins on the other axes
+            const int64_t sz = k == 0 ? t.P[1] * SY : w * SY;
+            a.fslab[sd] = w > 0 ? fold->slab[k][sd] : nullptr;
+            a.fbatch[sd] = uint32_t((k == 0 ? w : t.P[0]) * sz);
+            a.fSZ[sd] = uint32_t(sz);
+        }
+    }
     a.tile = static_cast<const char*>(tile);
     a.wfrag = static_cast<const char*>(wfrag);
     a.y = static_cast<char*>(y);
@@ -490,9 +571,13 @@ hipError_t launch_xm(const Tile3& t, const Conv3& cv, const void* tile, const vo
         a.O[k] = int32_t(cv.O[k]);
         a.pad[k] = int32_t(cv.pad[k]);
     }
-    if (t.n == 0 || cv.O[0] == 0 || cv.O[1] == 0 || cv.O[2] == 0) return hipSuccess;
-    a.NBZ = int32_t(ceil_div(cv.O[0], C::BZ));
-    a.NBY = int32_t(ceil_div(cv.O[1], C::BY));
+    if (t.n == 0 || rg.ext[0] == 0 || rg.ext[1] == 0 || rg.ext[2] == 0) return hipSuccess;
+    for (int k = 0; k < 2; ++k) {
+        a.org[k] = int32_t(rg.org[k]);
+        a.oend[k] = int32_t(rg.org[k] + rg.ext[k]);
+    }
+    a.NBZ = int32_t(ceil_div(rg.ext[0], C::BZ));
+    a.NBY = int32_t(ceil_div(rg.ext[1], C::BY));
     pick_raster(a.NBZ, a.NBY, 4, a.TZ, a.TY);
     a.NXT = int32_t(ceil_div(t.P[2], 32));
     int dev = 0, cus = 256;
@@ -510,7 +595,8 @@ hipError_t launch_xm(const Tile3& t, const Conv3& cv, const void* tile, const vo
     a.ybatch_bytes = uint32_t(cv.O[0] * cv.O[1] * cv.O[2] * cv.cout * 2);
     a.cout = int32_t(cv.cout);
     const int64_t grid = std::max<int64_t>(1, std::min<int64_t>(nb, cus));
-    auto fn = &conv_fwd_xm<CIN, KD, KH, WZ, WY, WC, R, NBUF>;
+    auto fn = fold ? &conv_fwd_xm<CIN, KD, KH, WZ, WY, WC, R, NBUF, true>
+                   : &conv_fwd_xm<CIN, KD, KH, WZ, WY, WC, R, NBUF, false>;
     hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(fn), hipFuncAttributeMaxDynamicSharedMemorySize,
                                        C::LDS_BYTES);
     if (e != hipSuccess) return e;
@@ -522,28 +608,47 @@ hipError_t launch_xm(const Tile3& t, const Conv3& cv, const void* tile, const vo
 
 // The W-march kernel applies to bf16, unit stride, kernel width 3 along W,
 // tiles and outputs of < 4 GiB per batch item, 16-byte aligned buffers, extents
-// below 2^24, and the (channel, kernel) shapes instantiated below.
-// Returns hipErrorNotSupported when it does not apply.
-hipError_t launch_conv_fwd_rows(const Tile3& t, const Conv3& cv, shard_dtype_t dt, const void* tile,
-                                const void* wfrag, int nkc_frag, int nt_frag, void* y, hipStream_t s)
+// below 2^24, the (channel, kernel) shapes instantiated below with the weight
+// fragments laid out by wfrag_kernel with exactly CIN/16 chunks and cout/32
+// tiles, and a folded halo that fold_fits.
+bool conv_fwd_rows_supported(const Tile3& t, const Conv3& cv, shard_dtype_t dt, const void* tile,
+                             const void* wfrag, int nkc_frag, int nt_frag, const void* y, const Fold* fold)
 {
-    if (dt != SHARD_BF16 || force_tiled()) return hipErrorNotSupported;
-    if (cv.S[0] != 1 || cv.S[1] != 1 || cv.S[2] != 1 || cv.K[2] != 3) return hipErrorNotSupported;
+    if (dt != SHARD_BF16 || force_tiled()) return false;
+    if (cv.S[0] != 1 || cv.S[1] != 1 || cv.S[2] != 1 || cv.K[2] != 3) return false;
     if (reinterpret_cast<uintptr_t>(tile) % 16 != 0 || reinterpret_cast<uintptr_t>(wfrag) % 16 != 0 ||
         reinterpret_cast<uintptr_t>(y) % 16 != 0)
-        return hipErrorNotSupported;
+        return false;
     const int64_t bb = t.P[0] * t.P[1] * t.P[2] * t.c * 2;
     const int64_t yb = cv.O[0] * cv.O[1] * cv.O[2] * cv.cout * 2;
-    if (bb >= (int64_t(1) << 32) - 64 || yb >= (int64_t(1) << 32) - 64) return hipErrorNotSupported;
+    if (bb >= (int64_t(1) << 32) - 64 || yb >= (int64_t(1) << 32) - 64) return false;
     for (int k = 0; k < 3; ++k)
         if (std::abs(cv.pad[k]) > (1 << 20) || cv.O[k] >= (int64_t(1) << 24) || t.P[k] >= (int64_t(1) << 24))
-            return hipErrorNotSupported;
-    // fragment arrays laid out by wfrag_kernel with exactly CIN/16 chunks and cout/32 tiles
-    if (t.c == 32 && cv.cout == 32 && cv.K[0] == 3 && cv.K[1] == 3 && nkc_frag == 2 && nt_frag == 1)
-        return launch_xm<32, 3, 3, 4, 1, 1, 2, 3>(t, cv, tile, wfrag, y, s);
-    if (t.c == 64 && cv.cout == 64 && cv.K[0] == 1 && cv.K[1] == 3 && nkc_frag == 4 && nt_frag == 2)
-        return launch_xm<64, 1, 3, 1, 2, 2, 4, 3>(t, cv, tile, wfrag, y, s);
-    return hipErrorNotSupported;
+            return false;
+    int rpi = 0;
+    if (t.c == 32 && cv.cout == 32 && cv.K[0] == 3 && cv.K[1] == 3 && nkc_frag == 2 && nt_frag == 1) rpi = 2;
+    if (t.c == 64 && cv.cout == 64 && cv.K[0] == 1 && cv.K[1] == 3 && nkc_frag == 4 && nt_frag == 2) rpi = 1;
+    if (rpi == 0) return false;
+    return !fold || fold_fits(t, *fold, rpi);
+}
+
+// Launches a region of a call conv_fwd_rows_supported accepts (regions cut axes
+// 0 and 1 only: the W march covers whole rows); hipErrorNotSupported otherwise.
+hipError_t launch_conv_fwd_rows(const Tile3& t, const Conv3& cv, shard_dtype_t dt, const void* tile,
+                                const void* wfrag, int nkc_frag, int nt_frag, void* y, const Region& rg,
+                                const Fold* fold, hipStream_t s)
+{
+    if (!conv_fwd_rows_supported(t, cv, dt, tile, wfrag, nkc_frag, nt_frag, y, fold)) return hipErrorNotSupported;
+    if (rg.org[2] != 0 || rg.ext[2] != cv.O[2]) return hipErrorNotSupported;
+    if (t.c == 32) {
+        // thin regions along axis 0 (the boundary planes of a D-sharded tile) take
+        // bricks two rows deep; per-output arithmetic is the same in both
+        if (rg.ext[0] <= 2) return launch_xm<32, 3, 3, 2, 2, 1, 2, 3>(t, cv, tile, wfrag, y, rg, fold, s);
+        return launch_xm<32, 3, 3, 4, 1, 1, 2, 3>(t, cv, tile, wfrag, y, rg, fold, s);
+    }
+    // thin regions along axis 1 (the boundary rows of an H-sharded 2D tile)
+    if (rg.ext[1] <= 2) return launch_xm<64, 1, 3, 1, 2, 2, 2, 3>(t, cv, tile, wfrag, y, rg, fold, s);
+    return launch_xm<64, 1, 3, 1, 2, 2, 4, 3>(t, cv, tile, wfrag, y, rg, fold, s);
 }
 
 }  // namespace shardconv

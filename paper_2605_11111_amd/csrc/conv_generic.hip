@@ -19,6 +19,8 @@ struct GenArgs {
     int64_t P[3], K[3], S[3], pad[3], O[3];
     int64_t chunk, nchunks, ndw;
     int64_t ybase, ys[4];  // forward output map (see OutMap)
+    int64_t org[3];        // forward: origin of the computed region (O is its extent)
+    Fold fold;             // forward: halo folded into the loads when fold.mask != 0
 };
 
 template <typename T>
@@ -31,9 +33,9 @@ __global__ __launch_bounds__(256) void fwd_direct(GenArgs a)
     for (int64_t e = int64_t(blockIdx.x) * 256 + threadIdx.x; e < total; e += int64_t(gridDim.x) * 256) {
         int64_t r = e;
         const int64_t co = r % a.cout; r /= a.cout;
-        const int64_t o2 = r % a.O[2]; r /= a.O[2];
-        const int64_t o1 = r % a.O[1]; r /= a.O[1];
-        const int64_t o0 = r % a.O[0];
+        const int64_t o2 = r % a.O[2] + a.org[2]; r /= a.O[2];
+        const int64_t o1 = r % a.O[1] + a.org[1]; r /= a.O[1];
+        const int64_t o0 = r % a.O[0] + a.org[0];
         const int64_t nn = r / a.O[0];
         float acc = 0.f;
         for (int64_t k0 = 0; k0 < a.K[0]; ++k0) {
@@ -45,7 +47,11 @@ __global__ __launch_bounds__(256) void fwd_direct(GenArgs a)
                 for (int64_t k2 = 0; k2 < a.K[2]; ++k2) {
                     const int64_t i2 = o2 * a.S[2] + k2 - a.pad[2];
                     if (i2 < 0 || i2 >= a.P[2]) continue;
-                    const T* src = tile + (((nn * a.P[0] + i0) * a.P[1] + i1) * a.P[2] + i2) * a.cin;
+                    const T* src = a.fold.mask
+                        ? reinterpret_cast<const T*>(fold_voxel(a.fold, static_cast<const char*>(a.tile), nn, i0, i1,
+                                                                i2, a.cin * int64_t(sizeof(T))))
+                        : tile + (((nn * a.P[0] + i0) * a.P[1] + i1) * a.P[2] + i2) * a.cin;
+                    if (!src) continue;
                     const T* wk = w + co * a.cin * a.K[0] * a.K[1] * a.K[2] + (k0 * a.K[1] + k1) * a.K[2] + k2;
                     const int64_t wstride = a.K[0] * a.K[1] * a.K[2];
                     for (int64_t ci = 0; ci < a.cin; ++ci) acc += to_f32(src[ci]) * to_f32(wk[ci * wstride]);
@@ -137,16 +143,22 @@ size_t generic_wgrad_workspace(const Tile3& t, const Conv3& cv)
 }
 
 hipError_t generic_conv_fwd(const Tile3& t, const Conv3& cv, shard_dtype_t dt, const void* tile, const void* w,
-                            void* y, const OutMap& om, hipStream_t s)
+                            void* y, const OutMap& om, const Region& rg, const Fold* fold, hipStream_t s)
 {
     GenArgs a = make_args(t, cv);
+    for (int k = 0; k < 3; ++k) {
+        a.O[k] = rg.ext[k];
+        a.org[k] = rg.org[k];
+    }
+    if (fold) a.fold = *fold;
     a.ybase = om.base;
     for (int k = 0; k < 4; ++k) a.ys[k] = om.str[k];
     a.tile = tile;
     a.w_or_dy = w;
     a.out = y;
     void* args[] = {&a};
-    const int64_t total = t.n * cv.out_voxels() * cv.cout;
+    const int64_t total = t.n * rg.ext[0] * rg.ext[1] * rg.ext[2] * cv.cout;
+    if (total == 0) return hipSuccess;
     const void* fn = dt == SHARD_BF16 ? reinterpret_cast<const void*>(&fwd_direct<bf16_t>)
                                       : reinterpret_cast<const void*>(&fwd_direct<float>);
     return hipLaunchKernel(fn, dim3(grid_for(total)), dim3(256), args, 0, s);

@@ -55,6 +55,57 @@ struct OutMap {
 };
 OutMap dense_out(const Conv3& cv);
 
+// A convolution whose halo is folded into its tile loads: the margin rows of
+// the padded tile are not read; a voxel in a margin comes from the slab received
+// for that margin (laid out as shard_halo_slab_shape gives: padded extents on
+// earlier axes, the margin width on its own axis, the interior on later axes) or
+// is zero where no slab is given (a global boundary). Axes are resolved from the
+// last to the first, so a corner voxel comes from the later axis's slab, as
+// after unpacking the slabs in ascending axis order. `mask` has bit k set for
+// every axis with a margin.
+struct Fold {
+    const char* slab[3][2];
+    int64_t lo[3], ext[3], P[3];
+    uint32_t mask;
+};
+
+// Byte offset of voxel (nn, t0, t1, t2) of a padded tile of `vox_bytes` bytes
+// per voxel, and the buffer it lies in (the tile, a slab, or null for zero).
+__host__ __device__ inline const char* fold_voxel(const Fold& f, const char* tile, int64_t nn, int64_t t0, int64_t t1,
+                                                  int64_t t2, int64_t vox_bytes)
+{
+    const int64_t tc[3] = {t0, t1, t2};
+    for (int a = 2; a >= 0; --a) {
+        if (!((f.mask >> a) & 1u)) continue;
+        const bool in_lo = tc[a] < f.lo[a];
+        const bool in_hi = tc[a] >= f.lo[a] + f.ext[a];
+        if (!in_lo && !in_hi) continue;
+        const char* slab = f.slab[a][in_hi ? 1 : 0];
+        if (!slab) return nullptr;
+        int64_t e[3], c[3];
+        for (int b = 0; b < 3; ++b) {
+            if (b < a) {
+                e[b] = f.P[b];
+                c[b] = tc[b];
+            } else if (b == a) {
+                e[b] = in_hi ? f.P[a] - f.lo[a] - f.ext[a] : f.lo[a];
+                c[b] = in_hi ? tc[a] - f.lo[a] - f.ext[a] : tc[a];
+            } else {
+                e[b] = f.ext[b];
+                c[b] = tc[b] - f.lo[b];
+            }
+        }
+        return slab + (((nn * e[0] + c[0]) * e[1] + c[1]) * e[2] + c[2]) * vox_bytes;
+    }
+    return tile + (((nn * f.P[0] + t0) * f.P[1] + t1) * f.P[2] + t2) * vox_bytes;
+}
+
+// The outputs a call computes: the box [org, org + ext) of the owned outputs
+// (Conv3::O); the output map stays that of the whole owned box.
+struct Region {
+    int64_t org[3], ext[3];
+};
+
 // Convolution launchers. `ws` holds at least conv_*_workspace(...) bytes.
 size_t conv_fwd_workspace(const Tile3& t, const Conv3& cv, shard_dtype_t dt);
 size_t conv_wgrad_workspace(const Tile3& t, const Conv3& cv, shard_dtype_t dt);
@@ -63,6 +114,17 @@ hipError_t launch_conv_fwd(const Tile3& t, const Conv3& cv, shard_dtype_t dt, co
 // The same with an output map (a non-dense map takes the general kernels).
 hipError_t launch_conv_fwd_mapped(const Tile3& t, const Conv3& cv, shard_dtype_t dt, const void* tile,
                                   const void* w, void* y, const OutMap& om, void* ws, hipStream_t s);
+// The kernel family a forward call takes. Every region of one call takes the
+// same family, so an output is summed in the same order whichever region
+// computes it.
+enum FwdFamily { FWD_GENERIC = 0, FWD_TILED = 1, FWD_ROWS = 2 };
+FwdFamily fwd_family(const Tile3& t, const Conv3& cv, shard_dtype_t dt, const void* tile, const void* y,
+                     const OutMap& om, const Fold* fold, const void* ws);
+// A region of the outputs on a chosen family, with the halo folded into the
+// loads when `fold` is given.
+hipError_t launch_conv_fwd_region(const Tile3& t, const Conv3& cv, shard_dtype_t dt, const void* tile,
+                                  const void* w, void* y, const OutMap& om, const Region& rg, const Fold* fold,
+                                  FwdFamily fam, void* ws, hipStream_t s);
 hipError_t launch_conv_wgrad(const Tile3& t, const Conv3& cv, shard_dtype_t dt, const void* tile, const void* dy,
                              float* dw, void* ws, hipStream_t s);
 size_t conv_dgrad_workspace(const Tile3& t, const Conv3& cv, shard_dtype_t dt);
@@ -79,8 +141,11 @@ hipError_t launch_norm_apply(const Tile3& t, shard_dtype_t dt, const void* tile,
 
 // Specialised kernels; each returns hipErrorNotSupported when the shape is
 // outside what it handles (the caller then takes the general kernel).
+bool conv_fwd_rows_supported(const Tile3& t, const Conv3& cv, shard_dtype_t dt, const void* tile,
+                             const void* wfrag, int nkc_frag, int nt_frag, const void* y, const Fold* fold);
 hipError_t launch_conv_fwd_rows(const Tile3& t, const Conv3& cv, shard_dtype_t dt, const void* tile,
-                                const void* wfrag, int nkc_frag, int nt_frag, void* y, hipStream_t s);
+                                const void* wfrag, int nkc_frag, int nt_frag, void* y, const Region& rg,
+                                const Fold* fold, hipStream_t s);
 size_t wgrad_xm_workspace(const Tile3& t, const Conv3& cv, shard_dtype_t dt);
 hipError_t launch_wgrad_xm(const Tile3& t, const Conv3& cv, shard_dtype_t dt, const void* tile, const void* dy,
                            float* dw, void* ws, hipStream_t s);

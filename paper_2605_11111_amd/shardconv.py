@@ -26,6 +26,13 @@ _i64p = ctypes.POINTER(ctypes.c_int64)
 _vp = ctypes.c_void_p
 
 
+SHARD_REGION_ALL, SHARD_REGION_INTERIOR, SHARD_REGION_BOUNDARY = 0, 1, 2
+
+
+class shard_halo_src_t(ctypes.Structure):
+    _fields_ = [("slab", (ctypes.c_void_p * 2) * 3)]
+
+
 class shard_tile_t(ctypes.Structure):
     _fields_ = [
         ("ndim", ctypes.c_int32),
@@ -59,6 +66,10 @@ _SIGS = {
                                         _vp, _vp, _vp, _vp, ctypes.c_size_t, _vp]),
     "shard_conv_workspace_bytes": (ctypes.c_size_t, [ctypes.c_int32, _tp, ctypes.c_int, ctypes.c_int64, _i64p,
                                                      _i64p, _i64p]),
+    "shard_conv_interior": (ctypes.c_int, [_tp, _i64p, _i64p, _i64p, _i64p, _i64p, _i64p]),
+    "shard_conv_fwd_folded": (ctypes.c_int, [_tp, ctypes.c_int, _vp, ctypes.c_void_p, ctypes.c_int32, _vp,
+                                             ctypes.c_int64, _i64p, _i64p, _i64p, _i64p, _vp, _vp, ctypes.c_size_t,
+                                             _vp]),
     "shard_status_string": (ctypes.c_char_p, [ctypes.c_int]),
 }
 for _name, (_res, _args) in _SIGS.items():
@@ -211,3 +222,34 @@ def shard_norm_apply(desc, tile, sums, count, eps, groups, gamma, beta, out, ws,
     _check("shard_norm_apply", _lib.shard_norm_apply(ctypes.byref(desc), _dtype_code(tile), _ptr(tile), _ptr(sums),
                                                      float(count), float(eps), groups, _ptr(gamma), _ptr(beta),
                                                      _ptr(out), _ptr(ws), nbytes, _stream(stream)))
+
+
+def shard_conv_interior(desc, kernel, stride, pad_lo, out_ext) -> tuple:
+    """(int_lo, int_hi): per axis, the outputs that read no margin."""
+    nd = desc.ndim
+    lo, hi = _arr([0] * nd), _arr([0] * nd)
+    _check("shard_conv_interior", _lib.shard_conv_interior(ctypes.byref(desc), _arr(kernel), _arr(stride),
+                                                           _arr(pad_lo), _arr(out_ext), lo, hi))
+    return list(lo)[:nd], list(hi)[:nd]
+
+
+def halo_src(slabs) -> shard_halo_src_t:
+    """shard_halo_src_t from {(axis, side): tensor or None}."""
+    h = shard_halo_src_t()
+    for (axis, side), t in slabs.items():
+        p = _ptr(t)
+        h.slab[axis][side] = None if p is None else p.value
+    return h
+
+
+def shard_conv_fwd_folded(desc, tile, slabs, region, w, c_out, kernel, stride, pad_lo, out_ext, y, ws,
+                          stream=None):
+    """Forward with the halo read from the received slabs ({(axis, side): tensor
+    or None}, or None for no slabs) for the outputs of `region`."""
+    h = None if slabs is None else halo_src(slabs)
+    st = _lib.shard_conv_fwd_folded(ctypes.byref(desc), _dtype_code(tile), _ptr(tile),
+                                    None if h is None else ctypes.cast(ctypes.byref(h), ctypes.c_void_p),
+                                    region, _ptr(w), c_out, _arr(kernel), _arr(stride), _arr(pad_lo), _arr(out_ext),
+                                    _ptr(y), _ptr(ws), ws.numel() * ws.element_size() if ws is not None else 0,
+                                    _stream(stream))
+    _check("shard_conv_fwd_folded", st)

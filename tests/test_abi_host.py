@@ -285,3 +285,58 @@ def test_norm_rejections(sc):
     assert ok(gamma=ctypes.c_void_p(0x10002)) == sc.SHARD_ERR_INVALID
     flat = sc.tile_desc(1, 32, [0, 16, 40])
     assert ap(ctypes.byref(flat), 1, None, None, 100.0, 1e-5, 4, None, None, None, None, 0, None) == sc.SHARD_OK
+
+
+def test_interior_query_equals_enumeration(sc):
+    """shard_conv_interior against the oracle's one-by-one listing, per axis, on
+    every shard of small 1-D splits and on the workloads' 3-D shards."""
+    checked = 0
+    for G in range(2, 33):
+        for K in (1, 3, 5, 7):
+            for S in (1, 2, 3):
+                for parts in range(1, min(G, 5) + 1):
+                    sizes = ogeo.chunk_sizes(G, parts)
+                    for o, L in zip(ogeo.offsets(sizes), sizes):
+                        g = ogeo.axis_geometry(G, K, S, o, L, parts > 1)
+                        d = sc.tile_desc(1, 4, [L], [g["halo_lo"]], [g["halo_hi"]])
+                        lo, hi = sc.shard_conv_interior(d, [K], [S], [g["pad_lo"]], [g["out_ext"]])
+                        want = ogeo.interior_outputs(g["halo_lo"], L, g["halo_hi"], K, S, g["pad_lo"], g["out_ext"])
+                        if want:
+                            assert (lo[0], hi[0]) == (want[0], want[-1] + 1), (G, K, S, o, L)
+                        else:
+                            assert lo[0] == hi[0], (G, K, S, o, L)
+                        checked += 1
+    assert checked > 2000
+    # 3-D: the C3 shard (D split in 4) and the corner shard of the 2x2 split
+    d = sc.tile_desc(1, 32, [128, 512, 512], [1, 0, 0], [1, 0, 0])
+    assert sc.shard_conv_interior(d, [3, 3, 3], [1, 1, 1], [0, 1, 1], [128, 512, 512]) == \
+        ([1, 0, 0], [127, 512, 512])
+    d = sc.tile_desc(1, 16, [128, 128, 256], [2, 2, 0], [2, 2, 0])
+    assert sc.shard_conv_interior(d, [5, 5, 5], [1, 1, 1], [0, 0, 2], [128, 128, 256]) == \
+        ([2, 2, 0], [126, 126, 256])
+
+
+@pytestmark_host
+def test_folded_rejections(sc):
+    lib = _raw(sc)
+    A = lambda *v: (ctypes.c_int64 * 3)(*v)
+    d = sc.tile_desc(1, 16, [8, 8, 40], [1, 0, 0], [1, 0, 0])
+    p = ctypes.byref(d)
+    K, S, pad, O = A(3, 3, 3), A(1, 1, 1), A(0, 1, 1), A(8, 8, 40)
+    need = sc.shard_conv_workspace_bytes(0, d, sc.SHARD_BF16, 32, [3, 3, 3], [1, 1, 1], [8, 8, 40])
+    f = lib.shard_conv_fwd_folded
+    h = sc.shard_halo_src_t()
+    hp = ctypes.cast(ctypes.byref(h), ctypes.c_void_p)
+    for region in (-1, 3):
+        assert f(p, 1, FAKE, hp, region, FAKE, 32, K, S, pad, O, FAKE, FAKE, need, None) == sc.SHARD_ERR_INVALID
+    assert f(p, 1, FAKE, hp, 0, FAKE, 32, K, S, pad, O, FAKE, FAKE, need - 1, None) == sc.SHARD_ERR_INVALID
+    assert f(p, 1, FAKE, hp, 0, None, 32, K, S, pad, O, FAKE, FAKE, need, None) == sc.SHARD_ERR_INVALID  # null w
+    assert f(p, 1, FAKE, hp, 0, FAKE, 32, K, S, None, O, FAKE, FAKE, need, None) == sc.SHARD_ERR_INVALID  # null pad
+    h.slab[0][1] = 0x10001                                                                          # misaligned slab
+    assert f(p, 1, FAKE, hp, 0, FAKE, 32, K, S, pad, O, FAKE, FAKE, need, None) == sc.SHARD_ERR_INVALID
+    assert f(p, 1, FAKE, hp, 0, FAKE, 32, K, S, pad, A(0, 8, 40), None, None, 0, None) == sc.SHARD_OK  # empty
+    il, ih = A(0, 0, 0), A(0, 0, 0)
+    q = lib.shard_conv_interior
+    assert q(p, K, S, None, O, il, ih) == sc.SHARD_ERR_INVALID
+    assert q(p, K, S, pad, O, None, ih) == sc.SHARD_ERR_INVALID
+    assert q(p, A(0, 3, 3), S, pad, O, il, ih) == sc.SHARD_ERR_INVALID
