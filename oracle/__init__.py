@@ -24,12 +24,16 @@ shapes". The oracle is therefore the plain definition:
 * ``brute``     - scalar-loop and dense-matrix restatements used to pin the
                   above on tiny inputs;
 * ``norm``      - group normalisation of a sharded tensor: per-shard sums, their
-                  total over all shards, and the normalised interior.
+                  total over all shards, and the normalised interior;
+* ``attention`` - one block step of ring attention: scaled dot-product
+                  attention against one key/value block and the log-space merge
+                  into the running result.
 
-Everything is float64 NumPy (``numpy.tensordot`` is the only library step).
+Everything is float64 NumPy (``numpy.tensordot`` and ``numpy.matmul`` are the
+only library steps).
 
 Parity status: every function here is pinned by tests marked ``not gpu``
 (brute force, dense Toeplitz matrices, torch's float64 CPU convolution,
 closed forms and invariants); none is "parity unpinned".
 """
-from . import geometry, conv, halo, brute, norm  # noqa: F401
+from . import geometry, conv, halo, brute, norm, attention  # noqa: F401
