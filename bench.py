@@ -211,6 +211,7 @@ def main():
         next_rows = time_backward(sc, w, g, desc, wt, dy, send, flops, args, stream)
         next_rows.update(time_group_norm(sc, w, g, desc, tile, args, stream))
         next_rows.update(time_folded(sc, w, g, desc, tile, wt, recv, args, stream))
+        next_rows.update(time_attention(sc, args, stream))
 
     dt = w.dtype
     value = 2 * flops / (ms_step * 1e-3) / 1e12
@@ -356,6 +357,28 @@ def time_folded(sc, w, g, desc, tile, wt, recv, args, stream):
            ("conv_fwd_boundary", "mfma:" + w.dtype, per_vox * (n_all - n_int), call(sc.SHARD_REGION_BOUNDARY, slabs))]
     res = _time_ops(ops, args, stream)
     log("folded forward timed")
+    return res
+
+
+def time_attention(sc, args, stream):
+    """One ring-attention block step on a sequence shard: 16 heads of dim 128,
+    16384 local queries against a 16384-key block (a 131072-token sequence over
+    8 devices), merged into a running state (4 * heads * Sq * Sk * D flops)."""
+    import torch
+    B, H, S, D = 1, 16, 16384, 128
+    g = torch.Generator(device="cuda").manual_seed(0)
+    q = torch.randn((B, H, S, D), generator=g, device="cuda").to(torch.bfloat16)
+    k = torch.randn((B, H, S, D), generator=g, device="cuda").to(torch.bfloat16)
+    v = torch.randn((B, H, S, D), generator=g, device="cuda").to(torch.bfloat16)
+    o = torch.zeros((B, H, S, D), device="cuda")
+    lse = torch.zeros((B, H, S), device="cuda")
+    scale = D ** -0.5
+    sc.shard_attn_block(q, k, v, o, lse, scale, True)
+    flops = 4.0 * B * H * S * S * D
+    ops = [("attn_block", "mfma:bf16", flops, lambda: sc.shard_attn_block(q, k, v, o, lse, scale, False))]
+    res = _time_ops(ops, args, stream)
+    res["attn_block"]["shape"] = f"B{B} H{H} Sq{S} Sk{S} D{D}"
+    log("attention block step timed")
     return res
 
 

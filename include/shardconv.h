@@ -25,6 +25,7 @@
  *                         the reverse halo exchange of the backward pass
  *   shard_norm_stats, shard_norm_apply
  *                         group normalisation with statistics over all shards
+ *   shard_attn_block      one block step of ring attention (log-space merge)
  *
  * Convolution semantics are PyTorch's cross-correlation (no bias, dilation 1,
  * groups 1), which the paper's programming model keeps (section "Benchmarks
@@ -343,6 +344,34 @@ shard_status_t shard_norm_apply(const shard_tile_t* x, shard_dtype_t dtype, cons
                                 void* out, void* ws, size_t ws_bytes, hipStream_t stream);
 
 /* Static, human-readable text for a status code. Never NULL. */
+/*
+ * One block step of ring attention (section "Performance Benchmarks",
+ * subsection "Ring Attention": each device attends its local queries to the
+ * key/value block it holds while K and V travel around the ring, accumulating
+ * the softmax in log space). Per batch item, head and query row i:
+ *   s[i][j]  = scale * q[i] . k[j]              over the block's sk keys
+ *   lse_b[i] = log sum_j exp(s[i][j]),  o_b[i] = sum_j exp(s[i][j] - lse_b[i]) v[j]
+ * merged into the running state (natural log):
+ *   lse[i] <- log(exp(lse[i]) + exp(lse_b[i]))
+ *   o[i]   <- exp(old lse[i] - lse[i]) o[i] + exp(lse_b[i] - lse[i]) o_b[i]
+ * `first` != 0 starts from the empty state (o = 0, lse = -inf) whatever o and
+ * lse hold. After every block of the sequence has been merged, o is
+ * softmax(scale q k^T) v over the whole sequence.
+ *   q      [batch][heads][sq][head_dim], dtype SHARD_BF16
+ *   k, v   [batch][heads][sk][head_dim], SHARD_BF16 (sk = 0: an empty block)
+ *   o      [batch][heads][sq][head_dim], binary32, read (unless first) and written
+ *   lse    [batch][heads][sq], binary32, read (unless first) and written
+ * head_dim 64 or 128; q, k, v and o 16-byte aligned; sk * head_dim * 2 < 2^32.
+ * Scores and sums are binary32; the probabilities enter the second product
+ * rounded to bf16 (to nearest even).
+ * Errors: SHARD_ERR_UNSUPPORTED for another dtype or head_dim or sizes past the
+ * limits; SHARD_ERR_INVALID for negative sizes, null or misaligned buffers, a
+ * non-finite scale; SHARD_ERR_HIP if a launch fails.
+ */
+shard_status_t shard_attn_block(int64_t batch, int64_t heads, int64_t sq, int64_t sk, int64_t head_dim,
+                                shard_dtype_t dtype, float scale, const void* q, const void* k, const void* v,
+                                float* o, float* lse, int32_t first, hipStream_t stream);
+
 const char* shard_status_string(shard_status_t status);
 
 #ifdef __cplusplus

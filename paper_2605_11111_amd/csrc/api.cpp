@@ -1,9 +1,11 @@
 // C-ABI entry points: argument validation on the host (before any launch, so
 // an error writes nothing), normalisation to three spatial axes, dispatch.
 #include <algorithm>
+#include <cmath>
 #include <cstdlib>
 #include <cstring>
 
+#include "attention.h"
 #include "internal.h"
 
 namespace shardconv {
@@ -432,6 +434,25 @@ shard_status_t shard_conv_fwd_folded(const shard_tile_t* x, shard_dtype_t dtype,
         if (e != hipSuccess) return SHARD_ERR_HIP;
     }
     return SHARD_OK;
+}
+
+shard_status_t shard_attn_block(int64_t batch, int64_t heads, int64_t sq, int64_t sk, int64_t head_dim,
+                                shard_dtype_t dtype, float scale, const void* q, const void* k, const void* v,
+                                float* o, float* lse, int32_t first, hipStream_t stream)
+{
+    if (batch < 0 || heads < 0 || sq < 0 || sk < 0 || head_dim < 1 || !valid_dtype(dtype) || !std::isfinite(scale))
+        return SHARD_ERR_INVALID;
+    if (dtype != SHARD_BF16 || (head_dim != 64 && head_dim != 128)) return SHARD_ERR_UNSUPPORTED;
+    if (batch > kMaxDim || heads > kMaxDim || sq > kMaxDim || sk > kMaxDim) return SHARD_ERR_UNSUPPORTED;
+    int64_t bh = batch;
+    if (!safe_mul(bh, heads)) return SHARD_ERR_UNSUPPORTED;
+    if (bh * sq == 0) return SHARD_OK;
+    if (!q || !o || !lse || !aligned(q, 16) || !aligned(o, 16) || !aligned(lse, 4)) return SHARD_ERR_INVALID;
+    if (sk > 0 && (!k || !v || !aligned(k, 16) || !aligned(v, 16))) return SHARD_ERR_INVALID;
+    const hipError_t e = launch_attn_block(bh, sq, sk, head_dim, scale, q, k ? k : q, v ? v : q, o, lse, first != 0,
+                                           stream);
+    if (e == hipErrorNotSupported) return SHARD_ERR_UNSUPPORTED;
+    return map_hip(e);
 }
 
 shard_status_t shard_conv_wgrad(const shard_tile_t* x, shard_dtype_t dtype, const void* tile, const void* dy,

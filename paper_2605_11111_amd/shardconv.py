@@ -70,6 +70,8 @@ _SIGS = {
     "shard_conv_fwd_folded": (ctypes.c_int, [_tp, ctypes.c_int, _vp, ctypes.c_void_p, ctypes.c_int32, _vp,
                                              ctypes.c_int64, _i64p, _i64p, _i64p, _i64p, _vp, _vp, ctypes.c_size_t,
                                              _vp]),
+    "shard_attn_block": (ctypes.c_int, [ctypes.c_int64] * 5 + [ctypes.c_int, ctypes.c_float, _vp, _vp, _vp, _vp, _vp,
+                                                                 ctypes.c_int32, _vp]),
     "shard_status_string": (ctypes.c_char_p, [ctypes.c_int]),
 }
 for _name, (_res, _args) in _SIGS.items():
@@ -253,3 +255,13 @@ def shard_conv_fwd_folded(desc, tile, slabs, region, w, c_out, kernel, stride, p
                                     _ptr(y), _ptr(ws), ws.numel() * ws.element_size() if ws is not None else 0,
                                     _stream(stream))
     _check("shard_conv_fwd_folded", st)
+
+
+def shard_attn_block(q, k, v, o, lse, scale, first, stream=None):
+    """One ring-attention block step: q [B][H][Sq][D], k/v [B][H][Sk][D] (bf16),
+    merged into o [B][H][Sq][D] and lse [B][H][Sq] (float32)."""
+    B, H, Sq, D = q.shape
+    Sk = k.shape[2]
+    st = _lib.shard_attn_block(B, H, Sq, Sk, D, _dtype_code(q), float(scale), _ptr(q), _ptr(k), _ptr(v), _ptr(o),
+                               _ptr(lse), 1 if first else 0, _stream(stream))
+    _check("shard_attn_block", st)

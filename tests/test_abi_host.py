@@ -340,3 +340,26 @@ def test_folded_rejections(sc):
     assert q(p, K, S, None, O, il, ih) == sc.SHARD_ERR_INVALID
     assert q(p, K, S, pad, O, None, ih) == sc.SHARD_ERR_INVALID
     assert q(p, A(0, 3, 3), S, pad, O, il, ih) == sc.SHARD_ERR_INVALID
+
+
+@pytestmark_host
+def test_attention_rejections(sc):
+    lib = _raw(sc)
+    f = lib.shard_attn_block
+    ok = (1, 2, 64, 64, 128, 1, 0.1, FAKE, FAKE, FAKE, FAKE, FAKE, 1, None)
+
+    def call(**kw):
+        names = ["b", "h", "sq", "sk", "d", "dt", "scale", "q", "k", "v", "o", "lse", "first", "s"]
+        args = dict(zip(names, ok))
+        args.update(kw)
+        return f(*[args[n] for n in names])
+    assert call(dt=0) == sc.SHARD_ERR_UNSUPPORTED                 # binary32 inputs
+    assert call(d=96) == sc.SHARD_ERR_UNSUPPORTED                 # head dim
+    assert call(sq=-1) == sc.SHARD_ERR_INVALID
+    assert call(sk=-1) == sc.SHARD_ERR_INVALID
+    assert call(scale=float("inf")) == sc.SHARD_ERR_INVALID
+    assert call(q=None) == sc.SHARD_ERR_INVALID
+    assert call(o=ctypes.c_void_p(0x10008)) == sc.SHARD_ERR_INVALID  # misaligned output
+    assert call(k=None) == sc.SHARD_ERR_INVALID
+    assert call(sk=1 << 30) == sc.SHARD_ERR_UNSUPPORTED           # 32-bit key offsets
+    assert call(sq=0, q=None, o=None, lse=None) == sc.SHARD_OK    # nothing to do
