@@ -23,9 +23,11 @@
 //    free of bank conflicts; keys past the block end load as zero and are
 //    masked to -inf in the scores, queries past the end load as zero and are
 //    not stored.
-//  * Softmax runs in base 2 on fp32 (scores scaled by scale * log2 e); the
-//    block's log-normaliser is m + log2(l), converted to natural log for the
-//    state. The merge with the stored state happens in the epilogue.
+//  * Softmax runs in base 2 on fp32 (scores scaled by scale * log2 e) against a
+//    reference max that moves only when a block's scores exceed it by more than
+//    2^8 (the rescale of O and l is then a rare wave-uniform branch); the
+//    log-normaliser is m + log2(l), converted to natural log for the state. The
+//    merge with the stored state happens in the epilogue.
 #include <algorithm>
 
 #include "attention.h"
@@ -43,6 +45,7 @@ namespace {
 
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLn2 = 0.6931471805599453f;
+constexpr float kSlack = 8.f;  // log2 headroom of the lazily updated reference max
 
 struct AttnArgs {
     const char* q;
@@ -206,43 +209,58 @@ __global__ __launch_bounds__(256, 1) void attn_block(AttnArgs a)
 #pragma unroll
             for (int dt = 0; dt < C::NDT; ++dt) vr[h][dt] = lds_read_tr16_b64(base + va[0][h][dt]);
 
-        // online softmax (base 2); element r of lane half g is key 8(r/4) + 4g + r%4
+        // online softmax in base 2 on raw scores s (x = s * c2); element r of lane
+        // half g is key 8(r/4) + 4g + r%4. The reference max m only moves when a
+        // block's max exceeds it by more than kSlack (then O and l are rescaled,
+        // a wave-uniform branch that is rare after the first blocks); otherwise
+        // p = 2^(x - m) <= 2^kSlack, exact in binary32 and in bf16's range, and
+        // l uses the same m, so the normalised result is unchanged.
         uint32_t pf[C::QT][2][4];
         const int kleft = a.sk - kb * C::KB;
+        if (kleft < C::KB) {
+#pragma unroll
+            for (int t = 0; t < C::QT; ++t)
+#pragma unroll
+                for (int r = 0; r < 16; ++r)
+                    if (8 * (r >> 2) + 4 * g + (r & 3) >= kleft) s[t][r] = -__builtin_inff();
+        }
+        float mx[C::QT];
+        bool need = false;
+#pragma unroll
+        for (int t = 0; t < C::QT; ++t) {
+            float v = s[t][0];
+#pragma unroll
+            for (int r = 1; r < 16; ++r) v = fmaxf(v, s[t][r]);
+            const uint32_t u = __float_as_uint(v);
+            const auto p = __builtin_amdgcn_permlane32_swap(u, u, false, false);
+            mx[t] = fmaxf(v, __uint_as_float(g ? p[0] : p[1])) * a.c2;
+            need |= mx[t] > m[t] + kSlack;
+        }
+        if (__builtin_amdgcn_ballot_w64(need) != 0) {
+#pragma unroll
+            for (int t = 0; t < C::QT; ++t) {
+                const float mn = fmaxf(m[t], mx[t]);
+                const float alpha = __builtin_amdgcn_exp2f(m[t] - mn);
+                l[t] *= alpha;
+                m[t] = mn;
+#pragma unroll
+                for (int dt = 0; dt < C::NDT; ++dt)
+#pragma unroll
+                    for (int r = 0; r < 16; ++r) o[t][dt][r] *= alpha;
+            }
+        }
 #pragma unroll
         for (int t = 0; t < C::QT; ++t) {
             float x[16];
-            float mx = -__builtin_inff();
-#pragma unroll
-            for (int r = 0; r < 16; ++r) {
-                const int key = 8 * (r >> 2) + 4 * g + (r & 3);
-                x[r] = key < kleft ? s[t][r] * a.c2 : -__builtin_inff();
-                mx = fmaxf(mx, x[r]);
-            }
-            {
-                const uint32_t u = __float_as_uint(mx);
-                const auto p = __builtin_amdgcn_permlane32_swap(u, u, false, false);
-                mx = fmaxf(mx, __uint_as_float(g ? p[0] : p[1]));
-            }
-            const float mn = fmaxf(m[t], mx);
-            const float alpha = __builtin_amdgcn_exp2f(m[t] - mn);
             float sum = 0.f;
 #pragma unroll
             for (int r = 0; r < 16; ++r) {
-                x[r] = __builtin_amdgcn_exp2f(x[r] - mn);
+                x[r] = __builtin_amdgcn_exp2f(__builtin_fmaf(s[t][r], a.c2, -m[t]));
                 sum += x[r];
             }
-            {
-                const uint32_t u = __float_as_uint(sum);
-                const auto p = __builtin_amdgcn_permlane32_swap(u, u, false, false);
-                sum += __uint_as_float(g ? p[0] : p[1]);
-            }
-            l[t] = l[t] * alpha + sum;
-            m[t] = mn;
-#pragma unroll
-            for (int dt = 0; dt < C::NDT; ++dt)
-#pragma unroll
-                for (int r = 0; r < 16; ++r) o[t][dt][r] *= alpha;
+            const uint32_t u = __float_as_uint(sum);
+            const auto p = __builtin_amdgcn_permlane32_swap(u, u, false, false);
+            l[t] += sum + __uint_as_float(g ? p[0] : p[1]);
 #pragma unroll
             for (int c = 0; c < 2; ++c)
 #pragma unroll
