@@ -35,6 +35,9 @@ FLAGS = [
 # between AGPRs on every tile, and the epilogue reads the accumulators directly.
 SRC_FLAGS = {
     "conv_fwd_rows.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"],
+    # the attention step holds scores, probabilities and V^T fragments for VALU
+    # work next to the MFMA operands; in AGPR form the allocator spills
+    "attention.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"],
 }
 
 

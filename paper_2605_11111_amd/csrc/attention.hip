@@ -29,6 +29,7 @@
 //    log-normaliser is m + log2(l), converted to natural log for the state. The
 //    merge with the stored state happens in the epilogue.
 #include <algorithm>
+#include <type_traits>
 
 #include "attention.h"
 #include "common.h"
@@ -85,6 +86,16 @@ __device__ __forceinline__ constexpr int k_slot(int key, int u)
 }
 __device__ __forceinline__ constexpr int v_slot(int key, int u) { return u ^ (2 * (key & 3)); }
 
+// f(integral_constant<int, i>) for i = 0 .. N - 1 (compile-time indices)
+template <int N, int I = 0, typename F>
+__device__ __forceinline__ void static_for(F&& f)
+{
+    if constexpr (I < N) {
+        f(std::integral_constant<int, I>{});
+        static_for<N, I + 1>(f);
+    }
+}
+
 template <int D>
 __global__ __launch_bounds__(256, 1) void attn_block(AttnArgs a)
 {
@@ -111,26 +122,28 @@ __global__ __launch_bounds__(256, 1) void attn_block(AttnArgs a)
     }
 
     // staging: load i of thread tid fills LDS bytes i*4096 + tid*16 of a block,
-    // i.e. key row r, slot s; it reads unit k_slot/v_slot^-1 of that key
+    // i.e. key row r, slot s; it reads unit k_slot/v_slot^-1 of that key. Step kb
+    // stages K of block kb + 1 and V of block kb (V runs one block behind: step kb
+    // multiplies the probabilities of block kb - 1); blocks past the end load as
+    // zero, so every step issues the same loads.
     const int64_t kv_bytes = int64_t(a.sk) * C::ROWB;
     const __amdgpu_buffer_rsrc_t rk = __builtin_amdgcn_make_buffer_rsrc(
         const_cast<char*>(a.k) + int64_t(bh) * kv_bytes, short(0), int(uint32_t(kv_bytes)), 0x00020000);
     const __amdgpu_buffer_rsrc_t rv = __builtin_amdgcn_make_buffer_rsrc(
         const_cast<char*>(a.v) + int64_t(bh) * kv_bytes, short(0), int(uint32_t(kv_bytes)), 0x00020000);
-    auto stage = [&](int kb, int buf) {
+    auto stage = [&](int kbk, int kbv, int buf) {
         char* dst = lds + buf * C::STAGE + wave * 1024;
 #pragma unroll
         for (int i = 0; i < C::NLD; ++i) {
             const int byte = i * 4096 + tid * 16;
-            const int r = byte / C::ROWB, s = (byte % C::ROWB) / 16;
-            const int key = kb * C::KB + r;
-            const bool ok = key < a.sk;
-            const uint32_t ok_ = ok ? 0u : 0xFFFFFFC0u;
-            const uint32_t ku = uint32_t(key) * C::ROWB + uint32_t(k_slot<D>(r, s)) * 16;
-            const uint32_t vu = uint32_t(key) * C::ROWB + uint32_t(v_slot(r, s)) * 16;
-            __builtin_amdgcn_raw_ptr_buffer_load_lds(rk, SC_LDSA(dst + i * 4096), 16, ok ? ku : ok_, 0, 0, 0);
-            __builtin_amdgcn_raw_ptr_buffer_load_lds(rv, SC_LDSA(dst + C::KV_BYTES + i * 4096), 16, ok ? vu : ok_,
-                                                     0, 0, 0);
+            const int r = byte / C::ROWB, sl = (byte % C::ROWB) / 16;
+            const int kk = kbk * C::KB + r, kv = kbv * C::KB + r;
+            const uint32_t ku = uint32_t(kk) * C::ROWB + uint32_t(k_slot<D>(r, sl)) * 16;
+            const uint32_t vu = uint32_t(kv) * C::ROWB + uint32_t(v_slot(r, sl)) * 16;
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(rk, SC_LDSA(dst + i * 4096), 16,
+                                                     kbk >= 0 && kk < a.sk ? ku : 0xFFFFFFC0u, 0, 0, 0);
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(rv, SC_LDSA(dst + C::KV_BYTES + i * 4096), 16,
+                                                     kbv >= 0 && kv < a.sk ? vu : 0xFFFFFFC0u, 0, 0, 0);
         }
     };
 
@@ -146,163 +159,206 @@ __global__ __launch_bounds__(256, 1) void attn_block(AttnArgs a)
             for (int r = 0; r < 16; ++r) o[t][dt][r] = 0.f;
     }
 
-    // fragment read addresses (bytes within a staged block)
+    // fragment read addresses (bytes within a staged block). K: lane (g, key n)
+    // reads unit 2c + g of its key, slot (2c + g) ^ (n % UPR) = 2 (c ^ zh) + (g ^ zl)
+    // with zh = (n % UPR) / 2, zl = n % 2.
     const uint32_t lds0 = lds_addr(lds);
-    uint32_t ka[C::NC];
-#pragma unroll
-    for (int c = 0; c < C::NC; ++c) ka[c] = uint32_t(ln * C::ROWB + k_slot<D>(ln, 2 * c + g) * 16);
-    // V^T: within a 16-lane group G, lane i addresses key row 16c + 4(G/2) + i/4
-    // (+ 8 for the second read) at head-dim columns 32dt + 16(G%2) + 4(i%4)
+    const int zk = ln & (C::UPR - 1);
+    const uint32_t kl = uint32_t(ln * C::ROWB + 16 * (g ^ (zk & 1)));
+    const uint32_t kzh = uint32_t(zk >> 1);
+    // V^T: within a 16-lane group G, lane i addresses key row 16c + 8h + 4(G/2) + i/4
+    // at head-dim columns 32dt + 16(G%2) + 4(i%4): unit 4dt + x (x < 4), slot
+    // (4dt + x) ^ 2(i/4) = 4 (dt ^ yb) + (x ^ 2 y1) with yb = i/8, y1 = (i/4) % 2.
+    // The dt part is an immediate offset; yb moves even dt by +64 B, odd dt by -64.
     const int G = lane >> 4, ii = lane & 15;
-    uint32_t va[2][2][C::NDT];
-#pragma unroll
-    for (int c = 0; c < 2; ++c)
-#pragma unroll
-        for (int h = 0; h < 2; ++h)
-#pragma unroll
-            for (int dt = 0; dt < C::NDT; ++dt) {
-                const int key = 16 * c + 8 * h + 4 * (G >> 1) + (ii >> 2);
-                const int col = 32 * dt + 16 * (G & 1) + 4 * (ii & 3);
-                va[c][h][dt] = uint32_t(C::KV_BYTES + key * C::ROWB + v_slot(key, col / 8) * 16 + (col % 8) * 2);
-            }
-
+    const int vx = 2 * (G & 1) + ((ii & 3) >> 1), vy1 = (ii >> 2) & 1, vyb = ii >> 3;
+    const uint32_t vcom = uint32_t((4 * (G >> 1) + (ii >> 2)) * C::ROWB + 16 * (vx ^ (2 * vy1)) + 8 * (ii & 1));
+    const uint32_t vbe = vcom + 64u * uint32_t(vyb), vbo = vcom - 64u * uint32_t(vyb);
     const int nkb = (a.sk + C::KB - 1) / C::KB;
-    stage(0, 0);
-    for (int kb = 0; kb < nkb; ++kb) {
+    // Step kb (software pipelined over key blocks): the score MFMAs of block kb,
+    // then the O^T MFMAs of block kb - 1 with the masking, row max and
+    // exponentials of block kb between them - a wave issues in order, so VALU
+    // work has to sit between MFMAs to run in their shadow (sched_group_barrier
+    // lays the streams out so). The probabilities alternate between two register
+    // sets (pA, pB). When block kb moves the reference max, l is rescaled at once
+    // and O at the start of step kb + 1, after the O^T MFMAs of block kb - 1.
+    f32x16_a sc[C::QT];
+    uint32_t pA[C::QT][2][4], pB[C::QT][2][4];
+    float alpha[C::QT];
+    bool resc = false;
+    auto step = [&](int kb, uint32_t (&pn)[C::QT][2][4], const uint32_t (&pp)[C::QT][2][4], auto do_s_c,
+                    auto do_pv_c) {
+        constexpr bool DO_S = decltype(do_s_c)::value, DO_PV = decltype(do_pv_c)::value;
         const int buf = kb & 1;
-        if (kb + 1 < nkb) {
-            stage(kb + 1, buf ^ 1);
-            wait_vm_barrier<2 * C::NLD>();
-        } else {
-            wait_vm_barrier<0>();
-        }
+        stage(kb + 1 < nkb ? kb + 1 : -1, kb < nkb ? kb : -1, buf ^ 1);
+        wait_vm_barrier<2 * C::NLD>();
         const uint32_t base = lds0 + uint32_t(buf * C::STAGE);
-
-        // S^T = K Q^T, K fragments read one step ahead
-        f32x16_a s[C::QT];
+        uint2 vr[2][2][C::NDT];
+        const uint32_t ve = base + vbe, vo = base + vbo;
+        auto vread = [&](auto c_c, auto h_c, auto dt_c) {
+            constexpr int c = decltype(c_c)::value, h = decltype(h_c)::value, dt = decltype(dt_c)::value;
+            constexpr int off = C::KV_BYTES + (16 * c + 8 * h) * C::ROWB + 64 * dt;
+            return lds_read_tr16_b64<off>((dt & 1) ? vo : ve);
+        };
+        auto vreads = [&](auto c_c) {
+            constexpr int c = decltype(c_c)::value;
+            static_for<2>([&](auto h_c) {
+                static_for<C::NDT>([&](auto dt_c) {
+                    vr[c][decltype(h_c)::value][decltype(dt_c)::value] = vread(c_c, h_c, dt_c);
+                });
+            });
+        };
+        if (DO_PV) {
+            vreads(std::integral_constant<int, 0>{});
+            if (resc) {
 #pragma unroll
-        for (int t = 0; t < C::QT; ++t)
+                for (int t = 0; t < C::QT; ++t)
 #pragma unroll
-            for (int r = 0; r < 16; ++r) s[t][r] = 0.f;
-        lds_u32x4 kf[2];
-        kf[0] = lds_read_b128(base + ka[0]);
+                    for (int dt = 0; dt < C::NDT; ++dt)
 #pragma unroll
-        for (int c = 0; c < C::NC; ++c) {
-            if (c + 1 < C::NC) {
-                kf[(c + 1) & 1] = lds_read_b128(base + ka[c + 1]);
-                lds_wait<1>();
-            } else {
-                lds_wait<0>();
+                        for (int r = 0; r < 16; ++r) o[t][dt][r] *= alpha[t];
             }
-            lds_ready(kf[c & 1]);
-#pragma unroll
-            for (int t = 0; t < C::QT; ++t)
-                s[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8_a, kf[c & 1]),
-                                                               __builtin_bit_cast(bf16x8_a, qf[t][c]), s[t], 0, 0,
-                                                               0);
         }
-
-        // V^T reads of the first step go out while the softmax runs
-        uint2 vr[2][C::NDT];
-#pragma unroll
-        for (int h = 0; h < 2; ++h)
-#pragma unroll
-            for (int dt = 0; dt < C::NDT; ++dt) vr[h][dt] = lds_read_tr16_b64(base + va[0][h][dt]);
-
-        // online softmax in base 2 on raw scores s (x = s * c2); element r of lane
-        // half g is key 8(r/4) + 4g + r%4. The reference max m only moves when a
-        // block's max exceeds it by more than kSlack (then O and l are rescaled,
-        // a wave-uniform branch that is rare after the first blocks); otherwise
-        // p = 2^(x - m) <= 2^kSlack, exact in binary32 and in bf16's range, and
-        // l uses the same m, so the normalised result is unchanged.
-        uint32_t pf[C::QT][2][4];
-        const int kleft = a.sk - kb * C::KB;
-        if (kleft < C::KB) {
+        if (DO_S) {
 #pragma unroll
             for (int t = 0; t < C::QT; ++t)
 #pragma unroll
-                for (int r = 0; r < 16; ++r)
-                    if (8 * (r >> 2) + 4 * g + (r & 3) >= kleft) s[t][r] = -__builtin_inff();
-        }
-        float mx[C::QT];
-        bool need = false;
+                for (int r = 0; r < 16; ++r) sc[t][r] = 0.f;
+            const uint32_t kb0 = base + kl;
+            auto kaddr = [&](int c) { return kb0 + 32u * (uint32_t(c) ^ kzh); };
+            lds_u32x4 kf[2];
+            kf[0] = lds_read_b128(kaddr(0));
 #pragma unroll
-        for (int t = 0; t < C::QT; ++t) {
-            float v = s[t][0];
-#pragma unroll
-            for (int r = 1; r < 16; ++r) v = fmaxf(v, s[t][r]);
-            const uint32_t u = __float_as_uint(v);
-            const auto p = __builtin_amdgcn_permlane32_swap(u, u, false, false);
-            mx[t] = fmaxf(v, __uint_as_float(g ? p[0] : p[1])) * a.c2;
-            need |= mx[t] > m[t] + kSlack;
-        }
-        if (__builtin_amdgcn_ballot_w64(need) != 0) {
-#pragma unroll
-            for (int t = 0; t < C::QT; ++t) {
-                const float mn = fmaxf(m[t], mx[t]);
-                const float alpha = __builtin_amdgcn_exp2f(m[t] - mn);
-                l[t] *= alpha;
-                m[t] = mn;
-#pragma unroll
-                for (int dt = 0; dt < C::NDT; ++dt)
-#pragma unroll
-                    for (int r = 0; r < 16; ++r) o[t][dt][r] *= alpha;
-            }
-        }
-#pragma unroll
-        for (int t = 0; t < C::QT; ++t) {
-            float x[16];
-            float sum = 0.f;
-#pragma unroll
-            for (int r = 0; r < 16; ++r) {
-                x[r] = __builtin_amdgcn_exp2f(__builtin_fmaf(s[t][r], a.c2, -m[t]));
-                sum += x[r];
-            }
-            const uint32_t u = __float_as_uint(sum);
-            const auto p = __builtin_amdgcn_permlane32_swap(u, u, false, false);
-            l[t] += sum + __uint_as_float(g ? p[0] : p[1]);
-#pragma unroll
-            for (int c = 0; c < 2; ++c)
-#pragma unroll
-                for (int e = 0; e < 4; ++e) {
-                    const bf16x2_a pk = {__bf16(x[8 * c + 2 * e]), __bf16(x[8 * c + 2 * e + 1])};
-                    pf[t][c][e] = __builtin_bit_cast(uint32_t, pk);
+            for (int c = 0; c < C::NC; ++c) {
+                if (c + 1 < C::NC) {
+                    kf[(c + 1) & 1] = lds_read_b128(kaddr(c + 1));
+                    lds_wait<1>();
+                } else {
+                    lds_wait<0>();
                 }
-        }
-
-        // O^T += V^T P^T over the block's two 16-key steps
+                lds_ready(kf[c & 1]);
 #pragma unroll
-        for (int c = 0; c < 2; ++c) {
-            uint2 cur[2][C::NDT];
+                for (int t = 0; t < C::QT; ++t)
+                    sc[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8_a, kf[c & 1]),
+                                                                    __builtin_bit_cast(bf16x8_a, qf[t][c]), sc[t], 0,
+                                                                    0, 0);
+            }
+        }
+        if (DO_PV) {
+            lds_wait<0>();
 #pragma unroll
             for (int h = 0; h < 2; ++h)
 #pragma unroll
-                for (int dt = 0; dt < C::NDT; ++dt) cur[h][dt] = vr[h][dt];
-            if (c == 0) {
-#pragma unroll
-                for (int h = 0; h < 2; ++h)
-#pragma unroll
-                    for (int dt = 0; dt < C::NDT; ++dt) vr[h][dt] = lds_read_tr16_b64(base + va[1][h][dt]);
-                lds_wait<2 * C::NDT>();
-            } else {
-                lds_wait<0>();
-            }
+                for (int dt = 0; dt < C::NDT; ++dt) lds_ready(vr[0][h][dt]);
+            vreads(std::integral_constant<int, 1>{});
+        }
+        auto pv = [&](int c) {
 #pragma unroll
             for (int dt = 0; dt < C::NDT; ++dt) {
-                lds_ready(cur[0][dt]);
-                lds_ready(cur[1][dt]);
-                const uint4 af = make_uint4(cur[0][dt].x, cur[0][dt].y, cur[1][dt].x, cur[1][dt].y);
+                const uint4 af = make_uint4(vr[c][0][dt].x, vr[c][0][dt].y, vr[c][1][dt].x, vr[c][1][dt].y);
 #pragma unroll
                 for (int t = 0; t < C::QT; ++t) {
-                    const uint4 bf = make_uint4(pf[t][c][0], pf[t][c][1], pf[t][c][2], pf[t][c][3]);
+                    const uint4 bf = make_uint4(pp[t][c][0], pp[t][c][1], pp[t][c][2], pp[t][c][3]);
                     o[t][dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8_a, af),
-                                                                       __builtin_bit_cast(bf16x8_a, bf), o[t][dt], 0,
-                                                                       0, 0);
+                                                                       __builtin_bit_cast(bf16x8_a, bf), o[t][dt],
+                                                                       0, 0, 0);
                 }
             }
+        };
+        // O^T MFMAs of block kb - 1, first half | mask and row max of block kb
+        if (DO_PV) pv(0);
+        float mx[C::QT];
+        if (DO_S) {
+            const int kleft = a.sk - kb * C::KB;
+            if (kleft < C::KB) {
+#pragma unroll
+                for (int t = 0; t < C::QT; ++t)
+#pragma unroll
+                    for (int r = 0; r < 16; ++r)
+                        if (8 * (r >> 2) + 4 * g + (r & 3) >= kleft) sc[t][r] = -__builtin_inff();
+            }
+            bool need = false;
+#pragma unroll
+            for (int t = 0; t < C::QT; ++t) {
+                float v = sc[t][0];
+#pragma unroll
+                for (int r = 1; r < 16; ++r) v = fmaxf(v, sc[t][r]);
+                const uint32_t u = __float_as_uint(v);
+                const auto p = __builtin_amdgcn_permlane32_swap(u, u, false, false);
+                mx[t] = fmaxf(v, __uint_as_float(g ? p[0] : p[1])) * a.c2;
+                need |= mx[t] > m[t] + kSlack;
+            }
+            // the reference max moves for every lane when any lane needs it to
+            resc = __builtin_amdgcn_ballot_w64(need) != 0;
+#pragma unroll
+            for (int t = 0; t < C::QT; ++t) {
+                const float mn = resc ? fmaxf(m[t], mx[t]) : m[t];
+                alpha[t] = __builtin_amdgcn_exp2f(m[t] - mn);
+                m[t] = mn;
+            }
         }
-        // every wave is done with this buffer before the next stage refills it
+        if (DO_PV && DO_S) {
+#pragma unroll
+            for (int i = 0; i < C::NDT * C::QT; ++i) {
+                __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+                __builtin_amdgcn_sched_group_barrier(0x002, 5, 0);
+            }
+        }
+        if (DO_PV) {
+            lds_wait<0>();
+#pragma unroll
+            for (int h = 0; h < 2; ++h)
+#pragma unroll
+                for (int dt = 0; dt < C::NDT; ++dt) lds_ready(vr[1][h][dt]);
+        }
+        // O^T MFMAs of block kb - 1, second half | exponentials of block kb
+        if (DO_PV) pv(1);
+        if (DO_S) {
+#pragma unroll
+            for (int t = 0; t < C::QT; ++t) {
+                float x[16];
+                float sum = 0.f;
+#pragma unroll
+                for (int r = 0; r < 16; ++r) {
+                    x[r] = __builtin_amdgcn_exp2f(__builtin_fmaf(sc[t][r], a.c2, -m[t]));
+                    sum += x[r];
+                }
+                const uint32_t u = __float_as_uint(sum);
+                const auto p = __builtin_amdgcn_permlane32_swap(u, u, false, false);
+                l[t] = l[t] * alpha[t] + sum + __uint_as_float(g ? p[0] : p[1]);
+#pragma unroll
+                for (int c = 0; c < 2; ++c)
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) {
+                        const bf16x2_a pk = {__bf16(x[8 * c + 2 * e]), __bf16(x[8 * c + 2 * e + 1])};
+                        pn[t][c][e] = __builtin_bit_cast(uint32_t, pk);
+                    }
+            }
+        }
+        if (DO_PV && DO_S) {
+#pragma unroll
+            for (int i = 0; i < C::NDT * C::QT; ++i) {
+                __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+                __builtin_amdgcn_sched_group_barrier(0x002, 10, 0);
+            }
+        }
+        // every wave is done with this buffer before the next step refills it
         __syncthreads();
+    };
+    using T_ = std::true_type;
+    using F_ = std::false_type;
+    stage(0, -1, 0);
+    step(0, pA, pB, T_{}, F_{});
+    int kb = 1;
+    for (; kb + 1 < nkb; kb += 2) {
+        step(kb, pB, pA, T_{}, T_{});
+        step(kb + 1, pA, pB, T_{}, T_{});
+    }
+    if (kb < nkb) {
+        step(kb, pB, pA, T_{}, T_{});
+        step(kb + 1, pA, pB, F_{}, T_{});
+    } else {
+        step(kb, pB, pA, F_{}, T_{});
     }
 
     // epilogue: lane (g, n) holds head-dim rows 32dt + 8j + 4g + e (e < 4) of
