@@ -1,8 +1,9 @@
 """Benchmark of the shard halo-convolution hot path on one MI355X.
 
 One step = one pass of the whole per-shard hot path over one synthetic shard:
-pack the boundary faces this shard sends, unpack the received slabs into its
-margins, forward convolution, weight gradient. All inputs are resident in HBM
+pack the boundary faces this shard sends (both faces of an axis in one launch),
+unpack the received slabs into its margins (both margins of an axis in one
+launch), forward convolution, weight gradient. All inputs are resident in HBM
 before the timed region. Geometry and slab shapes come from the library
 itself; the CPU oracle is used only by the cpu_baseline leg. Prints ONE JSON
 line on stdout (progress goes to stderr).
@@ -11,9 +12,11 @@ line on stdout (progress goes to stderr).
                     [--no-backward]
 
 The ops beyond the step on the same shard - the backward pass (input gradient
-onto the padded tile, reverse halo) and group normalisation with statistics over
-all shards (the shard's sums, then the interior normalised) - are timed after
-the step and reported under "next_rows"; they are not part of `value`.
+onto the padded tile, reverse halo), group normalisation with statistics over
+all shards (the shard's sums, then the interior normalised), the forward with
+the halo folded into its loads (whole, interior, boundary) and one ring-attention
+block step - are timed after the step and reported under "next_rows"; they are
+not part of `value`.
 
 The roofline's "traffic" field is the HBM traffic of the dominant kernel measured
 with rocprofv3 counters (FETCH_SIZE and WRITE_SIZE, each scaled by what it reads
@@ -156,15 +159,24 @@ def main():
                       dtype=torch.uint8, device="cuda")
     stream = torch.cuda.current_stream()
 
+    # the exchange along an axis: both faces packed by one launch before the
+    # sends, both margins filled by one launch after the receives
     ops = []
-    for (axis, side, nwidth, buf, nbytes) in send:
-        ops.append((f"pack_a{axis}s{side}", "pack", 2 * nbytes,
-                    lambda axis=axis, side=side, nwidth=nwidth, buf=buf:
-                    sc.shard_halo_pack(desc, tile, axis, side, nwidth, buf)))
-    for (axis, side, slab, nbytes) in recv:
-        moved = 2 * nbytes if slab is not None else nbytes
-        ops.append((f"unpack_a{axis}s{side}", "unpack", moved,
-                    lambda axis=axis, side=side, slab=slab: sc.shard_halo_unpack(desc, tile, axis, side, slab)))
+    for axis in range(w.nd):
+        sends = {side: (nwidth, buf, nbytes) for (a_, side, nwidth, buf, nbytes) in send if a_ == axis}
+        if sends:
+            wl, bl, nl = sends.get(0, (0, None, 0))
+            wh, bh, nh = sends.get(1, (0, None, 0))
+            ops.append((f"pack_a{axis}", "pack", 2 * (nl + nh),
+                        lambda axis=axis, wl=wl, bl=bl, wh=wh, bh=bh:
+                        sc.shard_halo_pack_pair(desc, tile, axis, wl, bl, wh, bh)))
+        recvs = {side: (slab, nbytes) for (a_, side, slab, nbytes) in recv if a_ == axis}
+        if recvs:
+            sl, nl = recvs.get(0, (None, 0))
+            sh, nh = recvs.get(1, (None, 0))
+            moved = (2 if sl is not None else 1) * nl + (2 if sh is not None else 1) * nh
+            ops.append((f"unpack_a{axis}", "unpack", moved,
+                        lambda axis=axis, sl=sl, sh=sh: sc.shard_halo_unpack_pair(desc, tile, axis, sl, sh)))
     flops = 2.0 * w.N * int(np.prod(O)) * w.cout * w.cin * int(np.prod(w.K))
     ops.append(("conv_fwd", "fwd", flops,
                 lambda: sc.shard_conv_fwd(desc, tile, wt, w.cout, w.K, w.S, g["pad_lo"], O, y, wsf)))

@@ -15,6 +15,8 @@
  *   shard_conv_geometry   which outputs a shard owns and the halo it needs (host)
  *   shard_halo_pack       copy a boundary face of the tile into a dense slab
  *   shard_halo_unpack     copy a received slab into a margin, or zero-fill it
+ *   shard_halo_pack_pair, shard_halo_unpack_pair
+ *                         both faces / both margins of an axis in one launch
  *   shard_conv_fwd        convolution read off the padded tile
  *   shard_conv_wgrad      the shard's partial weight gradient
  *   shard_conv_interior   outputs that need no halo (host only)
@@ -146,6 +148,21 @@ shard_status_t shard_halo_pack(const shard_tile_t* x, shard_dtype_t dtype, const
  */
 shard_status_t shard_halo_unpack(const shard_tile_t* x, shard_dtype_t dtype, void* tile, int32_t axis,
                                  int32_t side, const void* slab, hipStream_t stream);
+
+/*
+ * Both halves of an axis's exchange in one launch each (the faces of an axis are
+ * packed together before the sends and its margins filled together after the
+ * receives, section "PyTorch Dispatch"): shard_halo_pack_pair equals
+ * shard_halo_pack of side 0 with width_lo into slab_lo and of side 1 with
+ * width_hi into slab_hi; shard_halo_unpack_pair equals shard_halo_unpack of
+ * side 0 from slab_lo and side 1 from slab_hi (NULL: zero-fill that margin).
+ * A side of width 0 is skipped. Arguments and errors: as the single calls.
+ */
+shard_status_t shard_halo_pack_pair(const shard_tile_t* x, shard_dtype_t dtype, const void* tile, int32_t axis,
+                                    int64_t width_lo, void* slab_lo, int64_t width_hi, void* slab_hi,
+                                    hipStream_t stream);
+shard_status_t shard_halo_unpack_pair(const shard_tile_t* x, shard_dtype_t dtype, void* tile, int32_t axis,
+                                      const void* slab_lo, const void* slab_hi, hipStream_t stream);
 
 /*
  * Forward convolution over a padded tile:

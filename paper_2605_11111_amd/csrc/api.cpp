@@ -296,6 +296,68 @@ shard_status_t shard_halo_unpack(const shard_tile_t* x, shard_dtype_t dtype, voi
     return map_hip(launch_box_copy(b, SLAB_TO_TILE, slab, tile, stream));
 }
 
+shard_status_t shard_halo_pack_pair(const shard_tile_t* x, shard_dtype_t dtype, const void* tile, int32_t axis,
+                                    int64_t width_lo, void* slab_lo, int64_t width_hi, void* slab_hi,
+                                    hipStream_t stream)
+{
+    Tile3 t;
+    if (!norm_tile(x, dtype, t) || axis < 0 || axis >= x->ndim || width_lo < 0 || width_hi < 0)
+        return SHARD_ERR_INVALID;
+    const int k = 3 - x->ndim + axis;
+    if (width_lo > t.ext[k] || width_hi > t.ext[k]) return SHARD_ERR_UNSUPPORTED;
+    BoxCopy boxes[2];
+    const BoxCopy* bp[2];
+    CopyDir dirs[2] = {TILE_TO_SLAB, TILE_TO_SLAB};
+    const void* srcs[2] = {tile, tile};
+    void* dsts[2];
+    int n = 0;
+    for (int sd = 0; sd < 2; ++sd) {
+        const int64_t width = sd == 0 ? width_lo : width_hi;
+        void* slab = sd == 0 ? slab_lo : slab_hi;
+        const int64_t r0 = sd == 0 ? t.lo[k] : t.lo[k] + t.ext[k] - width;
+        int64_t start[3], cnt[3];
+        slab_spans(t, k, r0, r0 + width, start, cnt);
+        if (t.n * cnt[0] * cnt[1] * cnt[2] == 0) continue;
+        if (!tile || !slab || !aligned(tile, t.esz) || !aligned(slab, t.esz)) return SHARD_ERR_INVALID;
+        boxes[n] = make_box(t, k, r0, r0 + width);
+        bp[n] = &boxes[n];
+        dsts[n] = slab;
+        ++n;
+    }
+    if (n == 0) return SHARD_OK;
+    return map_hip(launch_box_copies(bp, dirs, srcs, dsts, n, stream));
+}
+
+shard_status_t shard_halo_unpack_pair(const shard_tile_t* x, shard_dtype_t dtype, void* tile, int32_t axis,
+                                      const void* slab_lo, const void* slab_hi, hipStream_t stream)
+{
+    Tile3 t;
+    if (!norm_tile(x, dtype, t) || axis < 0 || axis >= x->ndim) return SHARD_ERR_INVALID;
+    const int k = 3 - x->ndim + axis;
+    BoxCopy boxes[2];
+    const BoxCopy* bp[2];
+    CopyDir dirs[2];
+    const void* srcs[2];
+    void* dsts[2] = {tile, tile};
+    int n = 0;
+    for (int sd = 0; sd < 2; ++sd) {
+        const void* slab = sd == 0 ? slab_lo : slab_hi;
+        const int64_t r0 = sd == 0 ? 0 : t.lo[k] + t.ext[k];
+        const int64_t r1 = sd == 0 ? t.lo[k] : t.P[k];
+        int64_t start[3], cnt[3];
+        slab_spans(t, k, r0, r1, start, cnt);
+        if (t.n * cnt[0] * cnt[1] * cnt[2] == 0) continue;
+        if (!tile || !aligned(tile, t.esz) || (slab && !aligned(slab, t.esz))) return SHARD_ERR_INVALID;
+        boxes[n] = make_box(t, k, r0, r1);
+        bp[n] = &boxes[n];
+        dirs[n] = slab ? SLAB_TO_TILE : ZERO_TILE;
+        srcs[n] = slab;
+        ++n;
+    }
+    if (n == 0) return SHARD_OK;
+    return map_hip(launch_box_copies(bp, dirs, srcs, dsts, n, stream));
+}
+
 shard_status_t shard_halo_pack_margin(const shard_tile_t* x, shard_dtype_t dtype, const void* tile, int32_t axis,
                                       int32_t side, void* slab, hipStream_t stream)
 {

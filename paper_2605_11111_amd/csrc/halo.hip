@@ -63,13 +63,43 @@ __device__ __forceinline__ int64_t tile_offset(const CopyArgs& a, int64_t v)
     return a.base + i0 * a.t0 + i1 * a.t1 + i2 * a.t2 + col * V;
 }
 
+// One launch copies one or two boxes (both faces of an axis): blocks below
+// nblk0 take box 0, the rest box 1. The fields of a block's box are picked by
+// scalar selects (a dynamic index into the kernel arguments would copy them to
+// private memory).
+struct CopyArgs2 {
+    CopyArgs b0, b1;
+    int64_t nblk0;
+};
+
+__device__ __forceinline__ CopyArgs pick_box(const CopyArgs2& aa, bool second)
+{
+    CopyArgs a;
+    a.src = second ? aa.b1.src : aa.b0.src;
+    a.dst = second ? aa.b1.dst : aa.b0.dst;
+    a.base = second ? aa.b1.base : aa.b0.base;
+    a.cnt1 = second ? aa.b1.cnt1 : aa.b0.cnt1;
+    a.cnt2 = second ? aa.b1.cnt2 : aa.b0.cnt2;
+    a.t0 = second ? aa.b1.t0 : aa.b0.t0;
+    a.t1 = second ? aa.b1.t1 : aa.b0.t1;
+    a.t2 = second ? aa.b1.t2 : aa.b0.t2;
+    a.nvec_row = second ? aa.b1.nvec_row : aa.b0.nvec_row;
+    a.total = second ? aa.b1.total : aa.b0.total;
+    a.dir = second ? aa.b1.dir : aa.b0.dir;
+    return a;
+}
+
 template <int V, bool kSingleRun>
-__global__ __launch_bounds__(kThreads) void box_copy_kernel(CopyArgs a)
+__global__ __launch_bounds__(kThreads) void box_copy_kernel(CopyArgs2 aa)
 {
     using T = typename Vec<V>::T;
     constexpr int kUnroll = Vec<V>::U;
-    const int64_t nthreads = int64_t(gridDim.x) * kThreads;
-    const int64_t tid = int64_t(blockIdx.x) * kThreads + threadIdx.x;
+    const bool second = int64_t(blockIdx.x) >= aa.nblk0;
+    const CopyArgs a = pick_box(aa, second);
+    const int64_t nblk = second ? int64_t(gridDim.x) - aa.nblk0 : aa.nblk0;
+    const int64_t blk = second ? int64_t(blockIdx.x) - aa.nblk0 : int64_t(blockIdx.x);
+    const int64_t nthreads = nblk * kThreads;
+    const int64_t tid = blk * kThreads + threadIdx.x;
     for (int64_t v0 = tid; v0 < a.total; v0 += nthreads * kUnroll) {
         T val[kUnroll];
         int64_t off[kUnroll];
@@ -102,7 +132,7 @@ __global__ __launch_bounds__(kThreads) void box_copy_kernel(CopyArgs a)
 }
 
 template <int V>
-hipError_t launch_v(const BoxCopy& b, CopyDir dir, const void* src, void* dst, hipStream_t s)
+CopyArgs copy_args_v(const BoxCopy& b, CopyDir dir, const void* src, void* dst)
 {
     CopyArgs a;
     a.src = static_cast<const char*>(src);
@@ -114,14 +144,33 @@ hipError_t launch_v(const BoxCopy& b, CopyDir dir, const void* src, void* dst, h
     a.t1 = b.tstride[1];
     a.t2 = b.tstride[2];
     a.nvec_row = b.run / V;
-    const int64_t rows = b.cnt[0] * b.cnt[1] * b.cnt[2];
-    a.total = rows * a.nvec_row;
+    a.total = b.cnt[0] * b.cnt[1] * b.cnt[2] * a.nvec_row;
     a.dir = dir;
+    return a;
+}
+
+template <int V>
+int64_t copy_blocks(const CopyArgs& a)
+{
     const int64_t per_block = int64_t(kThreads) * Vec<V>::U;
-    const int64_t blocks = std::max<int64_t>(1, std::min<int64_t>(ceil_div(a.total, per_block), 1 << 20));
-    void* args[] = {&a};
-    const void* fn = rows == 1 ? reinterpret_cast<const void*>(&box_copy_kernel<V, true>)
-                               : reinterpret_cast<const void*>(&box_copy_kernel<V, false>);
+    return std::max<int64_t>(1, std::min<int64_t>(ceil_div(a.total, per_block), 1 << 20));
+}
+
+// boxes n (1 or 2) in one launch
+template <int V>
+hipError_t launch_v(const BoxCopy* const* b, const CopyDir* dir, const void* const* src, void* const* dst, int n,
+                    hipStream_t s)
+{
+    CopyArgs2 aa{};
+    aa.b0 = copy_args_v<V>(*b[0], dir[0], src[0], dst[0]);
+    aa.b1 = n > 1 ? copy_args_v<V>(*b[1], dir[1], src[1], dst[1]) : aa.b0;
+    aa.nblk0 = copy_blocks<V>(aa.b0);
+    const int64_t blocks = aa.nblk0 + (n > 1 ? copy_blocks<V>(aa.b1) : 0);
+    bool single = true;
+    for (int i = 0; i < n; ++i) single = single && b[i]->cnt[0] * b[i]->cnt[1] * b[i]->cnt[2] == 1;
+    void* args[] = {&aa};
+    const void* fn = single ? reinterpret_cast<const void*>(&box_copy_kernel<V, true>)
+                            : reinterpret_cast<const void*>(&box_copy_kernel<V, false>);
     return hipLaunchKernel(fn, dim3(unsigned(blocks)), dim3(kThreads), args, 0, s);
 }
 
@@ -214,17 +263,30 @@ hipError_t launch_box_add(const BoxCopy& b, int esz, const void* slab, void* til
     return launch_add_v<4, float>(b, slab, tile, s);
 }
 
+hipError_t launch_box_copies(const BoxCopy* const* b, const CopyDir* dir, const void* const* src, void* const* dst,
+                             int n, hipStream_t s)
+{
+    // the widest vector every box, tile and slab of the launch allows
+    auto ok = [&](int64_t v) {
+        for (int i = 0; i < n; ++i) {
+            const uintptr_t tile_ptr = reinterpret_cast<uintptr_t>(dir[i] == TILE_TO_SLAB ? src[i] : dst[i]);
+            const uintptr_t slab_ptr = reinterpret_cast<uintptr_t>(dir[i] == TILE_TO_SLAB ? dst[i] : src[i]);
+            const BoxCopy& x = *b[i];
+            if ((x.base % v) != 0 || (x.run % v) != 0 || (x.tstride[0] % v) != 0 || (x.tstride[1] % v) != 0 ||
+                (x.tstride[2] % v) != 0 || (tile_ptr % v) != 0 || (dir[i] != ZERO_TILE && (slab_ptr % v) != 0))
+                return false;
+        }
+        return true;
+    };
+    if (ok(16)) return launch_v<16>(b, dir, src, dst, n, s);
+    if (ok(4)) return launch_v<4>(b, dir, src, dst, n, s);
+    return launch_v<2>(b, dir, src, dst, n, s);
+}
+
 hipError_t launch_box_copy(const BoxCopy& b, CopyDir dir, const void* src, void* dst, hipStream_t s)
 {
-    const uintptr_t tile_ptr = reinterpret_cast<uintptr_t>(dir == TILE_TO_SLAB ? src : dst);
-    const uintptr_t slab_ptr = reinterpret_cast<uintptr_t>(dir == TILE_TO_SLAB ? dst : src);
-    auto ok = [&](int64_t v) {
-        return (b.base % v) == 0 && (b.run % v) == 0 && (b.tstride[0] % v) == 0 && (b.tstride[1] % v) == 0 &&
-               (b.tstride[2] % v) == 0 && (tile_ptr % v) == 0 && (dir == ZERO_TILE || (slab_ptr % v) == 0);
-    };
-    if (ok(16)) return launch_v<16>(b, dir, src, dst, s);
-    if (ok(4)) return launch_v<4>(b, dir, src, dst, s);
-    return launch_v<2>(b, dir, src, dst, s);
+    const BoxCopy* bp = &b;
+    return launch_box_copies(&bp, &dir, &src, &dst, 1, s);
 }
 
 }  // namespace shardconv

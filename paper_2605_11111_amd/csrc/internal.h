@@ -42,6 +42,9 @@ struct BoxCopy {
 enum CopyDir { TILE_TO_SLAB = 0, SLAB_TO_TILE = 1, ZERO_TILE = 2 };
 
 hipError_t launch_box_copy(const BoxCopy& b, CopyDir dir, const void* src, void* dst, hipStream_t s);
+// n (1 or 2) box copies in one launch (both faces or margins of an axis).
+hipError_t launch_box_copies(const BoxCopy* const* b, const CopyDir* dir, const void* const* src, void* const* dst,
+                             int n, hipStream_t s);
 // tile[box] += slab (dense), element-wise in binary32; esz 2 (bf16) or 4 (f32).
 hipError_t launch_box_add(const BoxCopy& b, int esz, const void* slab, void* tile, hipStream_t s);
 

@@ -72,6 +72,9 @@ _SIGS = {
                                              _vp]),
     "shard_attn_block": (ctypes.c_int, [ctypes.c_int64] * 5 + [ctypes.c_int, ctypes.c_float, _vp, _vp, _vp, _vp, _vp,
                                                                  ctypes.c_int32, _vp]),
+    "shard_halo_pack_pair": (ctypes.c_int, [_tp, ctypes.c_int, _vp, ctypes.c_int32, ctypes.c_int64, _vp,
+                                            ctypes.c_int64, _vp, _vp]),
+    "shard_halo_unpack_pair": (ctypes.c_int, [_tp, ctypes.c_int, _vp, ctypes.c_int32, _vp, _vp, _vp]),
     "shard_status_string": (ctypes.c_char_p, [ctypes.c_int]),
 }
 for _name, (_res, _args) in _SIGS.items():
@@ -265,3 +268,15 @@ def shard_attn_block(q, k, v, o, lse, scale, first, stream=None):
     st = _lib.shard_attn_block(B, H, Sq, Sk, D, _dtype_code(q), float(scale), _ptr(q), _ptr(k), _ptr(v), _ptr(o),
                                _ptr(lse), 1 if first else 0, _stream(stream))
     _check("shard_attn_block", st)
+
+
+def shard_halo_pack_pair(desc, tile, axis, width_lo, slab_lo, width_hi, slab_hi, stream=None):
+    _check("shard_halo_pack_pair", _lib.shard_halo_pack_pair(ctypes.byref(desc), _dtype_code(tile), _ptr(tile), axis,
+                                                             width_lo, _ptr(slab_lo), width_hi, _ptr(slab_hi),
+                                                             _stream(stream)))
+
+
+def shard_halo_unpack_pair(desc, tile, axis, slab_lo=None, slab_hi=None, stream=None):
+    _check("shard_halo_unpack_pair", _lib.shard_halo_unpack_pair(ctypes.byref(desc), _dtype_code(tile), _ptr(tile),
+                                                                 axis, _ptr(slab_lo), _ptr(slab_hi),
+                                                                 _stream(stream)))

@@ -141,3 +141,60 @@ def test_full_size_halos_of_the_measured_shard(sc, name):
     got = host(tile)
     del tile
     assert _bits_equal(got, want)
+
+
+def _pair_case(sc, w, idx):
+    """Both faces of every axis packed by one call, and both margins filled by
+    one call, bit for bit equal to the oracle's slabs and padded tile (the
+    margins start as canaries; global-boundary margins are zero-filled)."""
+    import torch
+    sg = cases.shard_geom(w, idx)
+    full_h = cases.x_box(w, sg.tile_lo, sg.tile_hi, cases.out_code(w))
+    lo, hi = sg.g["halo_lo"], sg.g["halo_hi"]
+    desc = sc.tile_desc(w.N, w.cin, sg.ext, lo, hi)
+    tile = dev(full_h)
+    for axis in range(w.nd):
+        widths = [min(lo[axis], sg.ext[axis]), min(hi[axis], sg.ext[axis])]
+        slabs = [torch.full(sc.shard_halo_slab_shape(desc, axis, wd), float("nan"), dtype=cases.torch_dtype(w),
+                            device="cuda") if wd else None for wd in widths]
+        sc.shard_halo_pack_pair(desc, tile, axis, widths[0], slabs[0], widths[1], slabs[1])
+        for side in (0, 1):
+            if not widths[side]:
+                continue
+            rows = ohalo.pack_rows(axis, side, widths[side], lo, sg.ext)
+            b0, b1 = ohalo.face_box(axis, rows, lo, sg.ext, hi)
+            box = (slice(None),) + tuple(slice(a, b) for a, b in zip(b0, b1)) + (slice(None),)
+            want = np.ascontiguousarray(full_h[box])
+            assert _bits_equal(host(slabs[side]).reshape(want.shape), want), (idx, axis, side)
+    # margins from canaries: received slabs where a neighbour exists, zero at a boundary
+    tile_h = np.full_like(full_h, canary_for(w))
+    inner = (slice(None),) + tuple(slice(l, l + e) for l, e in zip(lo, sg.ext)) + (slice(None),)
+    tile_h[inner] = full_h[inner]
+    t2 = dev(tile_h)
+    for axis in range(w.nd):
+        recv = []
+        for side in (0, 1):
+            width = lo[axis] if side == 0 else hi[axis]
+            if width and cases.neighbour_exists(w, idx, axis, side):
+                b0, b1 = ohalo.face_box(axis, ohalo.margin_rows(axis, side, lo, sg.ext, hi), lo, sg.ext, hi)
+                box = (slice(None),) + tuple(slice(a, b) for a, b in zip(b0, b1)) + (slice(None),)
+                recv.append(dev(np.ascontiguousarray(full_h[box])))
+            else:
+                recv.append(None)
+        sc.shard_halo_unpack_pair(desc, t2, axis, recv[0], recv[1])
+    assert _bits_equal(host(t2), full_h), idx
+
+
+@pytest.mark.parametrize("name", list(cases.REDUCED))
+def test_pair_calls_every_shard(sc, name):
+    w = cases.REDUCED[name]
+    for idx in w.shards():
+        log(f"pair {name} shard {idx}")
+        _pair_case(sc, w, idx)
+
+
+@pytest.mark.parametrize("name", ["c3_3d_bf16", "c4_3d_bf16_k5", "c5_3d_fp32_s2"])
+def test_pair_calls_full_size(sc, name):
+    w = cases.WORKLOADS[name]
+    log(f"pair full {name}")
+    _pair_case(sc, w, w.shard)
