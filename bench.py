@@ -242,6 +242,8 @@ def main():
                 "frac": round(ach / PEAK[dt], 4), "traffic": measured_traffic(dom, args.workload),
                 "work_per_launch": f"{flops:.4e} flop: 2*Cout*Cin*prod(K) per output voxel x {int(np.prod(O))} voxels"}
 
+    halo_bytes = max((work for (label, kind, work, _) in ops if kind in ("pack", "unpack")), default=0)
+    ceiling = measured_ceiling(args, stream, int(halo_bytes)) if halo_bytes else None
     cpu = None if args.no_cpu_baseline else cpu_baseline(w, g, tile_lo)
     line = {
         "metric": "shard conv fwd+wgrad TFLOP/s (% MFMA peak); halo pack/unpack GB/s (% HBM)",
@@ -252,7 +254,8 @@ def main():
                    "tile_padded": [w.N] + [l + e + h for l, e, h in zip(lo, ext, hi)] + [w.cin],
                    "out": [w.N] + list(O) + [w.cout], "kernel": list(w.K), "stride": list(w.S),
                    "accumulate": "f32"},
-        "ops": detail, "roofline": roofline, "cpu_baseline": cpu, "next_rows": next_rows,
+        "ops": detail, "roofline": roofline, "measured_copy_ceiling": ceiling, "cpu_baseline": cpu,
+        "next_rows": next_rows,
     }
     print(json.dumps(line), flush=True)
 
@@ -370,6 +373,33 @@ def time_folded(sc, w, g, desc, tile, wt, recv, args, stream):
     res = _time_ops(ops, args, stream)
     log("folded forward timed")
     return res
+
+
+def measured_ceiling(args, stream, nbytes):
+    """The part's own copy rate at the halo's size: a device-to-device copy
+    (torch's copy_, the runtime's blit kernel) of nbytes / 2 read + nbytes / 2
+    written, over 8 buffer pairs in turn, event-timed like the halo launches."""
+    import numpy as np
+    import torch
+    half = nbytes // 2
+    pairs = [(torch.empty(half, dtype=torch.uint8, device="cuda").fill_(1),
+              torch.empty(half, dtype=torch.uint8, device="cuda")) for _ in range(8)]
+    flush = torch.empty(512 << 20, dtype=torch.uint8, device="cuda")
+    times = []
+    for k in range(max(8, args.steps)):
+        src, dst = pairs[k % 8]
+        flush.fill_(k & 255)      # evict the last-level cache between copies
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        dst.copy_(src)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        times.append(e0.elapsed_time(e1))
+    ms = float(np.median(times))
+    gbs = nbytes / (ms * 1e-3) / 1e9
+    del pairs, flush
+    return {"ms": round(ms, 4), "gbs": round(gbs, 1), "frac_hbm_peak": round(gbs / HBM_PEAK, 4), "bytes": int(nbytes),
+            "what": "device-to-device copy of the same bytes (torch copy_), median of event-timed launches"}
 
 
 def time_attention(sc, args, stream):
