@@ -222,7 +222,7 @@ def main():
     if not args.no_backward:
         next_rows = time_backward(sc, w, g, desc, wt, dy, send, flops, args, stream)
         next_rows.update(time_group_norm(sc, w, g, desc, tile, args, stream))
-        next_rows.update(time_folded(sc, w, g, desc, tile, wt, recv, args, stream))
+        next_rows.update(time_folded(sc, w, g, desc, tile, wt, dy, recv, args, stream))
         next_rows.update(time_attention(sc, args, stream))
 
     dt = w.dtype
@@ -346,7 +346,7 @@ def _time_ops(ops, args, stream):
     return out
 
 
-def time_folded(sc, w, g, desc, tile, wt, recv, args, stream):
+def time_folded(sc, w, g, desc, tile, wt, dy, recv, args, stream):
     """The forward with the halo folded into its loads (margins never read; the
     received slabs serve the margin rows), whole and as the interior / boundary
     pair that lets the exchange overlap the interior (timed after the step, not
@@ -367,7 +367,12 @@ def time_folded(sc, w, g, desc, tile, wt, recv, args, stream):
 
     def call(region, sl):
         return lambda: sc.shard_conv_fwd_folded(desc, tile, sl, region, wt, w.cout, w.K, w.S, g["pad_lo"], O, y, ws)
+    dw = torch.empty((w.cout, w.cin) + tuple(w.K), dtype=torch.float32, device="cuda")
+    wsw = torch.empty(max(16, sc.shard_conv_workspace_bytes(1, desc, code, w.cout, w.K, w.S, O)), dtype=torch.uint8,
+                      device="cuda")
     ops = [("conv_fwd_folded", "mfma:" + w.dtype, per_vox * n_all, call(sc.SHARD_REGION_ALL, slabs)),
+           ("conv_wgrad_folded", "mfma:" + w.dtype, per_vox * n_all,
+            lambda: sc.shard_conv_wgrad_folded(desc, tile, slabs, dy, w.cout, w.K, w.S, g["pad_lo"], O, dw, wsw)),
            ("conv_fwd_interior", "mfma:" + w.dtype, per_vox * n_int, call(sc.SHARD_REGION_INTERIOR, None)),
            ("conv_fwd_boundary", "mfma:" + w.dtype, per_vox * (n_all - n_int), call(sc.SHARD_REGION_BOUNDARY, slabs))]
     res = _time_ops(ops, args, stream)

@@ -22,6 +22,8 @@
  *   shard_conv_interior   outputs that need no halo (host only)
  *   shard_conv_fwd_folded forward reading the halo from the received slabs,
  *                         all outputs or the interior / boundary part
+ *   shard_conv_wgrad_folded
+ *                         weight gradient reading the halo from the slabs
  *   shard_conv_dgrad      the input gradient read back onto the padded tile
  *   shard_halo_pack_margin, shard_halo_accumulate
  *                         the reverse halo exchange of the backward pass
@@ -255,6 +257,26 @@ shard_status_t shard_conv_wgrad(const shard_tile_t* x, shard_dtype_t dtype, cons
                                 int64_t c_out, const int64_t kernel[], const int64_t stride[],
                                 const int64_t pad_lo[], const int64_t out_ext[], float* dw, void* ws,
                                 size_t ws_bytes, hipStream_t stream);
+
+/*
+ * shard_conv_wgrad with the halo folded into the tile loads, the weight
+ * gradient's counterpart of shard_conv_fwd_folded (after a folded forward the
+ * margins hold nothing; the received slabs kept from the forward serve the
+ * backward pass): the tile's margin rows are never read, each margin voxel
+ * comes from the slab of its margin (`halo`, NULL = every margin zero), a
+ * corner voxel from the later axis's slab. dw equals shard_halo_unpack of every
+ * slab followed by shard_conv_wgrad: bit for bit when both select the same
+ * kernel (margins on one axis, 16-byte aligned slabs, shapes outside the
+ * transposed-read kernel's) and on integer-valued data, otherwise up to the
+ * order of the binary32 sums. Other arguments, workspace and errors: as
+ * shard_conv_wgrad; SHARD_ERR_INVALID also for a slab not aligned to the
+ * element size.
+ */
+shard_status_t shard_conv_wgrad_folded(const shard_tile_t* x, shard_dtype_t dtype, const void* tile,
+                                       const shard_halo_src_t* halo, const void* dy, int64_t c_out,
+                                       const int64_t kernel[], const int64_t stride[], const int64_t pad_lo[],
+                                       const int64_t out_ext[], float* dw, void* ws, size_t ws_bytes,
+                                       hipStream_t stream);
 
 /*
  * Input gradient read back onto the padded tile (the backward pass of the

@@ -24,7 +24,7 @@ bool force_tiled()
 
 size_t generic_wgrad_workspace(const Tile3& t, const Conv3& cv);
 hipError_t generic_conv_wgrad(const Tile3& t, const Conv3& cv, shard_dtype_t dt, const void* tile, const void* dy,
-                              float* dw, void* ws, hipStream_t s);
+                              float* dw, void* ws, const Fold* fold, hipStream_t s);
 
 }  // namespace shardconv
 
@@ -164,6 +164,27 @@ BoxCopy make_box(const Tile3& t, int k, int64_t r0, int64_t r1)
 }
 
 shard_status_t map_hip(hipError_t e) { return e == hipSuccess ? SHARD_OK : SHARD_ERR_HIP; }
+
+// The Fold of a call: every axis with a margin reads it from the received slab
+// (null: zero). False for a slab not aligned to the element size.
+bool make_fold(const shard_tile_t* x, const Tile3& t, const shard_halo_src_t* halo, Fold& f)
+{
+    f = Fold{};
+    const int off = 3 - x->ndim;
+    for (int k = 0; k < 3; ++k) {
+        f.lo[k] = t.lo[k];
+        f.ext[k] = t.ext[k];
+        f.P[k] = t.P[k];
+        if (t.lo[k] > 0 || t.hi[k] > 0) f.mask |= 1u << k;
+        for (int sd = 0; sd < 2; ++sd) {
+            const int64_t width = sd == 0 ? t.lo[k] : t.hi[k];
+            const void* p = (halo && k >= off && width > 0) ? halo->slab[k - off][sd] : nullptr;
+            if (!aligned(p, t.esz)) return false;
+            f.slab[k][sd] = static_cast<const char*>(p);
+        }
+    }
+    return true;
+}
 
 // Interior outputs per internal axis: [jlo, jhi) of the outputs whose input rows
 // j*S - pad + t (t < K) lie in [lo, lo + ext); every output on an axis without
@@ -456,20 +477,8 @@ shard_status_t shard_conv_fwd_folded(const shard_tile_t* x, shard_dtype_t dtype,
     if ((tile_elems(t) > 0 && !tile) || !w || !y) return SHARD_ERR_INVALID;
     if (!aligned(tile, t.esz) || !aligned(w, t.esz) || !aligned(y, t.esz) || !aligned(ws, 16))
         return SHARD_ERR_INVALID;
-    Fold f{};
-    const int off = 3 - x->ndim;
-    for (int k = 0; k < 3; ++k) {
-        f.lo[k] = t.lo[k];
-        f.ext[k] = t.ext[k];
-        f.P[k] = t.P[k];
-        if (t.lo[k] > 0 || t.hi[k] > 0) f.mask |= 1u << k;
-        for (int sd = 0; sd < 2; ++sd) {
-            const int64_t width = sd == 0 ? t.lo[k] : t.hi[k];
-            const void* p = (halo && k >= off && width > 0) ? halo->slab[k - off][sd] : nullptr;
-            if (!aligned(p, t.esz)) return SHARD_ERR_INVALID;
-            f.slab[k][sd] = static_cast<const char*>(p);
-        }
-    }
+    Fold f;
+    if (!make_fold(x, t, halo, f)) return SHARD_ERR_INVALID;
     const OutMap om = dense_out(cv);
     const Fold* fold = f.mask ? &f : nullptr;
     const FwdFamily fam = fwd_family(t, cv, dtype, tile, y, om, fold, ws);
@@ -531,8 +540,31 @@ shard_status_t shard_conv_wgrad(const shard_tile_t* x, shard_dtype_t dtype, cons
     const bool empty = t.n * cv.out_voxels() == 0;
     if (!empty && ((tile_elems(t) > 0 && !tile) || !dy)) return SHARD_ERR_INVALID;
     if (!aligned(tile, t.esz) || !aligned(dy, t.esz)) return SHARD_ERR_INVALID;
-    if (empty) return map_hip(generic_conv_wgrad(t, cv, dtype, tile, dy, dw, ws, stream));
+    if (empty) return map_hip(generic_conv_wgrad(t, cv, dtype, tile, dy, dw, ws, nullptr, stream));
     return map_hip(launch_conv_wgrad(t, cv, dtype, tile, dy, dw, ws, stream));
+}
+
+shard_status_t shard_conv_wgrad_folded(const shard_tile_t* x, shard_dtype_t dtype, const void* tile,
+                                       const shard_halo_src_t* halo, const void* dy, int64_t c_out,
+                                       const int64_t kernel[], const int64_t stride[], const int64_t pad_lo[],
+                                       const int64_t out_ext[], float* dw, void* ws, size_t ws_bytes,
+                                       hipStream_t stream)
+{
+    Tile3 t;
+    Conv3 cv;
+    if (!norm_tile(x, dtype, t) || !pad_lo || !norm_conv(x, t, c_out, kernel, stride, pad_lo, out_ext, cv))
+        return SHARD_ERR_INVALID;
+    const size_t need = conv_wgrad_workspace(t, cv, dtype);
+    if (ws_bytes < need || (need > 0 && !ws)) return SHARD_ERR_INVALID;
+    if (!dw || !aligned(dw, 4) || !aligned(ws, 16)) return SHARD_ERR_INVALID;
+    const bool empty = t.n * cv.out_voxels() == 0;
+    if (!empty && ((tile_elems(t) > 0 && !tile) || !dy)) return SHARD_ERR_INVALID;
+    if (!aligned(tile, t.esz) || !aligned(dy, t.esz)) return SHARD_ERR_INVALID;
+    Fold f;
+    if (!make_fold(x, t, halo, f)) return SHARD_ERR_INVALID;
+    if (empty) return map_hip(generic_conv_wgrad(t, cv, dtype, tile, dy, dw, ws, nullptr, stream));
+    if (!f.mask) return map_hip(launch_conv_wgrad(t, cv, dtype, tile, dy, dw, ws, stream));
+    return map_hip(launch_conv_wgrad_folded(t, cv, dtype, tile, dy, dw, ws, f, stream));
 }
 
 shard_status_t shard_conv_dgrad(const shard_tile_t* x, shard_dtype_t dtype, const void* dy, const void* w,

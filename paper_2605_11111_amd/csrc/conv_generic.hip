@@ -90,7 +90,12 @@ __global__ __launch_bounds__(256) void wgrad_direct(GenArgs a)
             const int64_t i1 = o1 * a.S[1] + k1 - a.pad[1];
             const int64_t i2 = o2 * a.S[2] + k2 - a.pad[2];
             if (i0 < 0 || i0 >= a.P[0] || i1 < 0 || i1 >= a.P[1] || i2 < 0 || i2 >= a.P[2]) continue;
-            const float xv = to_f32(tile[(((nn * a.P[0] + i0) * a.P[1] + i1) * a.P[2] + i2) * a.cin + ci]);
+            const T* vox = a.fold.mask
+                               ? reinterpret_cast<const T*>(fold_voxel(a.fold, static_cast<const char*>(a.tile), nn,
+                                                                       i0, i1, i2, a.cin * int64_t(sizeof(T))))
+                               : tile + (((nn * a.P[0] + i0) * a.P[1] + i1) * a.P[2] + i2) * a.cin;
+            if (!vox) continue;
+            const float xv = to_f32(vox[ci]);
             acc += to_f32(dy[v * a.cout + co]) * xv;
         }
         a.part[e] = acc;
@@ -165,9 +170,10 @@ hipError_t generic_conv_fwd(const Tile3& t, const Conv3& cv, shard_dtype_t dt, c
 }
 
 hipError_t generic_conv_wgrad(const Tile3& t, const Conv3& cv, shard_dtype_t dt, const void* tile, const void* dy,
-                              float* dw, void* ws, hipStream_t s)
+                              float* dw, void* ws, const Fold* fold, hipStream_t s)
 {
     GenArgs a = make_args(t, cv);
+    if (fold) a.fold = *fold;
     a.tile = tile;
     a.w_or_dy = dy;
     a.out = dw;

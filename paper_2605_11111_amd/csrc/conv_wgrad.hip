@@ -27,7 +27,7 @@ namespace shardconv {
 
 size_t generic_wgrad_workspace(const Tile3& t, const Conv3& cv);
 hipError_t generic_conv_wgrad(const Tile3& t, const Conv3& cv, shard_dtype_t dt, const void* tile, const void* dy,
-                              float* dw, void* ws, hipStream_t s);
+                              float* dw, void* ws, const Fold* fold, hipStream_t s);
 
 typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8_w;
 typedef __attribute__((ext_vector_type(4))) float f32x4_w;
@@ -58,6 +58,7 @@ struct WgArgs {
     int32_t wco, wci;     // bf16: 16-wide sub-tiles per wave grid
     int32_t xvec, dvec;   // 16-byte vector loads allowed (alignment of base and channel rows)
     int64_t nblocks;
+    Fold fold;            // halo folded into the loads when fold.mask != 0
 };
 
 struct PlanW {
@@ -170,8 +171,13 @@ __global__ __launch_bounds__(kThreads, 2) void wgrad_bf16_tiled(WgArgs a)
                 const int64_t t0 = i0 + z, t1 = i1 + y, t2 = i2 + x;
                 const int64_t c = ci0 + 8 * q;
                 bf16_t val[8] = {0, 0, 0, 0, 0, 0, 0, 0};
-                if (t0 >= 0 && t0 < a.P[0] && t1 >= 0 && t1 < a.P[1] && t2 >= 0 && t2 < a.P[2] && c < a.cin)
-                    load8(tile + (((nn * a.P[0] + t0) * a.P[1] + t1) * a.P[2] + t2) * a.cin + c, c, a.cin, xvec, val);
+                if (t0 >= 0 && t0 < a.P[0] && t1 >= 0 && t1 < a.P[1] && t2 >= 0 && t2 < a.P[2] && c < a.cin) {
+                    const bf16_t* vox =
+                        a.fold.mask ? reinterpret_cast<const bf16_t*>(fold_voxel(a.fold, a.tile, nn, t0, t1, t2,
+                                                                                 a.cin * 2))
+                                    : tile + (((nn * a.P[0] + t0) * a.P[1] + t1) * a.P[2] + t2) * a.cin;
+                    if (vox) load8(vox + c, c, a.cin, xvec, val);
+                }
                 bf16_t* dst = xs + (8 * q) * a.cs + row * a.bixp + x;
 #pragma unroll
                 for (int e = 0; e < 8; ++e) dst[e * a.cs] = val[e];
@@ -301,8 +307,13 @@ __global__ __launch_bounds__(kThreads, 2) void wgrad_f32_tiled(WgArgs a)
             const int64_t t0 = i0 + z, t1 = i1 + y, t2 = i2 + x;
             const int64_t c = ci0 + 4 * q;
             float4 val = make_float4(0.f, 0.f, 0.f, 0.f);
-            if (t0 >= 0 && t0 < a.P[0] && t1 >= 0 && t1 < a.P[1] && t2 >= 0 && t2 < a.P[2] && c < a.cin) {
-                const float* src = tile + (((nn * a.P[0] + t0) * a.P[1] + t1) * a.P[2] + t2) * a.cin + c;
+            const float* vox = nullptr;
+            if (t0 >= 0 && t0 < a.P[0] && t1 >= 0 && t1 < a.P[1] && t2 >= 0 && t2 < a.P[2] && c < a.cin)
+                vox = a.fold.mask
+                          ? reinterpret_cast<const float*>(fold_voxel(a.fold, a.tile, nn, t0, t1, t2, a.cin * 4))
+                          : tile + (((nn * a.P[0] + t0) * a.P[1] + t1) * a.P[2] + t2) * a.cin;
+            if (vox) {
+                const float* src = vox + c;
                 if (xvec && c + 4 <= a.cin) {
                     val = *reinterpret_cast<const float4*>(src);
                 } else {
@@ -606,14 +617,16 @@ size_t conv_wgrad_workspace(const Tile3& t, const Conv3& cv, shard_dtype_t dt)
                      wgrad_tr_workspace(t, cv, dt), wgrad_xm_workspace(t, cv, dt)});
 }
 
-hipError_t launch_conv_wgrad(const Tile3& t, const Conv3& cv, shard_dtype_t dt, const void* tile, const void* dy,
-                             float* dw, void* ws, hipStream_t s)
+namespace {
+
+hipError_t run_wgrad(const Tile3& t, const Conv3& cv, shard_dtype_t dt, const void* tile, const void* dy, float* dw,
+                     void* ws, const Fold* fold, hipStream_t s)
 {
     {
-        hipError_t e = launch_wgrad_xm(t, cv, dt, tile, dy, dw, ws, s);
+        hipError_t e = launch_wgrad_xm(t, cv, dt, tile, dy, dw, ws, fold, s);
         if (e != hipErrorNotSupported) return e;
     }
-    {
+    if (!fold) {
         int32_t red[6];
         hipError_t e = launch_wgrad_tr(t, cv, dt, tile, dy, static_cast<float*>(ws), red, s);
         if (e != hipErrorNotSupported) {
@@ -638,11 +651,17 @@ hipError_t launch_conv_wgrad(const Tile3& t, const Conv3& cv, shard_dtype_t dt, 
         }
     }
     PlanW pl = plan_wgrad(t, cv, dt);
-    if (pl.kind == 0) return generic_conv_wgrad(t, cv, dt, tile, dy, dw, ws, s);
+    if (pl.kind == 0) return generic_conv_wgrad(t, cv, dt, tile, dy, dw, ws, fold, s);
     pl.a.tile = static_cast<const char*>(tile);
     pl.a.dy = static_cast<const char*>(dy);
     const int64_t esz = dt == SHARD_BF16 ? 2 : 4;
-    pl.a.xvec = (reinterpret_cast<uintptr_t>(tile) % 16 == 0) && (t.c * esz) % 16 == 0;
+    bool xal = reinterpret_cast<uintptr_t>(tile) % 16 == 0;
+    if (fold) {
+        pl.a.fold = *fold;
+        for (int k = 0; k < 3; ++k)
+            for (int sd = 0; sd < 2; ++sd) xal = xal && reinterpret_cast<uintptr_t>(fold->slab[k][sd]) % 16 == 0;
+    }
+    pl.a.xvec = xal && (t.c * esz) % 16 == 0;
     pl.a.dvec = (reinterpret_cast<uintptr_t>(dy) % 16 == 0) && (cv.cout * esz) % 16 == 0;
     pl.a.part = static_cast<float*>(ws);
     pl.a.dw = dw;
@@ -654,6 +673,20 @@ hipError_t launch_conv_wgrad(const Tile3& t, const Conv3& cv, shard_dtype_t dt, 
     int kind = pl.kind, kdg = pl.a.kdg, k1 = pl.k1, k2 = pl.k2, wco = pl.wco;
     void* args[] = {&a, &kind, &kdg, &k1, &k2, &wco};
     return hipLaunchKernel(reinterpret_cast<const void*>(&wgrad_reduce), dim3(grid), dim3(256), args, 0, s);
+}
+
+}  // namespace
+
+hipError_t launch_conv_wgrad(const Tile3& t, const Conv3& cv, shard_dtype_t dt, const void* tile, const void* dy,
+                             float* dw, void* ws, hipStream_t s)
+{
+    return run_wgrad(t, cv, dt, tile, dy, dw, ws, nullptr, s);
+}
+
+hipError_t launch_conv_wgrad_folded(const Tile3& t, const Conv3& cv, shard_dtype_t dt, const void* tile,
+                                    const void* dy, float* dw, void* ws, const Fold& fold, hipStream_t s)
+{
+    return run_wgrad(t, cv, dt, tile, dy, dw, ws, &fold, s);
 }
 
 }  // namespace shardconv

@@ -58,6 +58,12 @@ struct WxArgs {
     uint32_t nbricks;       // n * NBZ * NBY * nseg
     uint32_t tile_bytes, dy_bytes;  // per batch item (< 2^32)
     uint32_t xrow, xplane, yrow, yplane;  // byte strides of tile and dy rows and planes
+    // halo folded into the loads along axis fa (0 or 1): padded rows c < flo come
+    // from fslab[0], rows c >= fhi from fslab[1] (null: zero), the rest from the tile
+    const char* fslab[2];
+    uint32_t fbatch[2];  // slab bytes per batch item
+    uint32_t fSZ[2];     // slab stride along axis 0, bytes
+    int32_t fa, flo, fhi;
 };
 
 // 16-byte unit swizzle of staged voxel v for UPV units per voxel: with 128-byte
@@ -100,7 +106,7 @@ struct WxCfg {
 // KS = 2: eight waves, K split in halves between the two waves of a SIMD (three
 // roles only), NB stage buffers handed between loaders and compute waves through
 // LDS counters instead of barriers (see the flag protocol below).
-template <int KD, int NCI, int NCO, int BZ, int BY, int KS, int NB>
+template <int KD, int NCI, int NCO, int BZ, int BY, int KS, int NB, bool FOLD>
 __global__ __launch_bounds__(256 * KS, 1) void wgrad_xm(WxArgs a)
 {
     using C = WxCfg<KD, NCI, NCO, BZ, BY>;
@@ -175,6 +181,42 @@ __global__ __launch_bounds__(256 * KS, 1) void wgrad_xm(WxArgs a)
             seg_start(p);
         }
     };
+    // One 16-byte x load of padded voxel row (z, y) at tile offset `off` (the
+    // offset of that row in the padded tile): with the halo folded, a row in a
+    // margin along the fold axis comes from its slab (the offset moved to the
+    // slab's layout), zero past the data. (z, y) may differ between lanes (the
+    // halo area packs several rows per instruction): the branch then diverges
+    // and each lane's load runs under its own source, writing only its own slot.
+    auto slab_rsrc = [&](int sd, uint32_t nn) {
+        return __builtin_amdgcn_make_buffer_rsrc(
+            const_cast<char*>(a.fslab[sd] ? a.fslab[sd] + int64_t(nn) * a.fbatch[sd] : a.tile), short(0),
+            a.fslab[sd] ? int(a.fbatch[sd]) : 0, 0x00020000);
+    };
+    // A unit whose staged rows all lie inside [flo, fhi) along the fold axis takes
+    // the plain loads (`touch` false, uniform over the unit).
+    auto touches = [&](int32_t z0, int32_t y0) {
+        const int32_t c0 = a.fa == 0 ? z0 : y0, n = a.fa == 0 ? C::XRZ : C::XRY;
+        return FOLD && (c0 < a.flo || c0 + n > a.fhi);
+    };
+    auto xload = [&](__amdgpu_buffer_rsrc_t rt, __amdgpu_buffer_rsrc_t rl, __amdgpu_buffer_rsrc_t rh, char* dst,
+                     uint32_t off, bool ok, int32_t z, int32_t y, bool touch) {
+        if (!FOLD || !touch) {
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(rt, SC_LDSW(dst), 16, ok ? off : 0xFFFFFFC0u, 0, 0, 0);
+            return;
+        }
+        const int32_t c = a.fa == 0 ? z : y;
+        if (c < a.flo) {
+            const uint32_t o = off - uint32_t(z) * (a.xplane - a.fSZ[0]);
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(rl, SC_LDSW(dst), 16, ok ? o : 0xFFFFFFC0u, 0, 0, 0);
+        } else if (c >= a.fhi) {
+            const uint32_t o = off - uint32_t(z) * (a.xplane - a.fSZ[1]) -
+                               uint32_t(a.fhi) * (a.fa == 0 ? a.xplane : a.xrow);
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(rh, SC_LDSW(dst), 16, ok ? o : 0xFFFFFFC0u, 0, 0, 0);
+        } else {
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(rt, SC_LDSW(dst), 16, ok ? off : 0xFFFFFFC0u, 0, 0, 0);
+        }
+    };
+
     // Staging: wave w loads the input rows r = w, w + 4, ... (IPR_X instructions
     // each), the halo instructions h = w, w + 4, ... and the dy rows w, w + 4, ...
     // Main and dy rows: lane l carries unit l % UPV of voxel piece * (64 / UPV) +
@@ -211,6 +253,8 @@ __global__ __launch_bounds__(256 * KS, 1) void wgrad_xm(WxArgs a)
                                                                      int(a.tile_bytes), 0x00020000);
     __amdgpu_buffer_rsrc_t st_ry = __builtin_amdgcn_make_buffer_rsrc(const_cast<char*>(a.dy), short(0),
                                                                      int(a.dy_bytes), 0x00020000);
+    __amdgpu_buffer_rsrc_t st_rl = st_rx, st_rh = st_rx;
+    bool st_touch = false;
     char* st_dst = lds;
     uint32_t st_xorg = 0, st_yorg = 0;
     int32_t st_i0 = 0, st_i1 = 0, st_i2 = 0, st_o0 = 0, st_o1 = 0;
@@ -232,6 +276,11 @@ __global__ __launch_bounds__(256 * KS, 1) void wgrad_xm(WxArgs a)
                                                   int(a.tile_bytes), 0x00020000);
         st_ry = __builtin_amdgcn_make_buffer_rsrc(const_cast<char*>(a.dy) + int64_t(nn) * a.dy_bytes, short(0),
                                                   int(a.dy_bytes), 0x00020000);
+        if (FOLD) {
+            st_rl = slab_rsrc(0, nn);
+            st_rh = slab_rsrc(1, nn);
+            st_touch = touches(st_i0, st_i1);
+        }
         st_dst = lds + buf * C::STAGE_BYTES + wave * 1024;
     };
     auto stage_load = [&](int k) {
@@ -240,8 +289,7 @@ __global__ __launch_bounds__(256 * KS, 1) void wgrad_xm(WxArgs a)
             const bool ok = st_okx && uint32_t(st_i0 + zr) < uint32_t(a.P[0]) &&
                             uint32_t(st_i1 + yr0 + wrx) < uint32_t(a.P[1]);
             const uint32_t u = st_xorg + uint32_t(zr) * a.xplane + uint32_t(yr0) * a.xrow + lxw;
-            __builtin_amdgcn_raw_ptr_buffer_load_lds(st_rx, SC_LDSW(st_dst + 4 * k * 1024), 16, ok ? u : a.tile_bytes,
-                                                     0, 0, 0);
+            xload(st_rx, st_rl, st_rh, st_dst + 4 * k * 1024, u, ok, st_i0 + zr, st_i1 + yr0 + wrx, st_touch);
         } else if (k < KY0) {
             const int hi = 4 * (k - KH0) + wave;
             if (hi < C::XH_INSTR) {
@@ -251,9 +299,8 @@ __global__ __launch_bounds__(256 * KS, 1) void wgrad_xm(WxArgs a)
                                 uint32_t(st_i1 + yr) < uint32_t(a.P[1]) && uint32_t(st_i2 + hv) < uint32_t(a.P[2]);
                 const uint32_t u = st_xorg - uint32_t(wrx) * a.xrow + uint32_t(zr) * a.xplane +
                                    uint32_t(yr) * a.xrow + lxh;
-                __builtin_amdgcn_raw_ptr_buffer_load_lds(st_rx,
-                                                         SC_LDSW(st_dst + C::X_BYTES + 4 * (k - KH0) * 1024), 16,
-                                                         ok ? u : a.tile_bytes, 0, 0, 0);
+                xload(st_rx, st_rl, st_rh, st_dst + C::X_BYTES + 4 * (k - KH0) * 1024, u, ok, st_i0 + zr, st_i1 + yr,
+                      st_touch);
             }
         } else {
             const int kk = k - KY0;
@@ -284,6 +331,8 @@ __global__ __launch_bounds__(256 * KS, 1) void wgrad_xm(WxArgs a)
             const_cast<char*>(a.tile) + int64_t(nn) * a.tile_bytes, short(0), int(a.tile_bytes), 0x00020000);
         __amdgpu_buffer_rsrc_t ry = __builtin_amdgcn_make_buffer_rsrc(
             const_cast<char*>(a.dy) + int64_t(nn) * a.dy_bytes, short(0), int(a.dy_bytes), 0x00020000);
+        const __amdgpu_buffer_rsrc_t rl = FOLD ? slab_rsrc(0, nn) : rx, rh = FOLD ? slab_rsrc(1, nn) : rx;
+        const bool touch = touches(i0, i1);
         char* dst = lds + buf * C::STAGE_BYTES;
 #pragma unroll
         for (int i = LI; i < C::X_INSTR; i += KS) {
@@ -293,7 +342,7 @@ __global__ __launch_bounds__(256 * KS, 1) void wgrad_xm(WxArgs a)
                             (uint32_t(i2 + pc * XPI + vx) < uint32_t(a.P[2]));
             const uint32_t u = xorg + uint32_t(zr) * a.xplane + uint32_t(yr) * a.xrow + lxm +
                                uint32_t(pc * XPI * C::CIN * 2);
-            __builtin_amdgcn_raw_ptr_buffer_load_lds(rx, SC_LDSW(dst + i * 1024), 16, ok ? u : a.tile_bytes, 0, 0, 0);
+            xload(rx, rl, rh, dst + i * 1024, u, ok, i0 + zr, i1 + yr, touch);
         }
 #pragma unroll
         for (int hi = LI; hi < C::XH_INSTR; hi += KS) {
@@ -302,8 +351,7 @@ __global__ __launch_bounds__(256 * KS, 1) void wgrad_xm(WxArgs a)
             const bool ok = live & (uint32_t(i0 + zr) < uint32_t(a.P[0])) & (uint32_t(i1 + yr) < uint32_t(a.P[1])) &
                             (uint32_t(i2 + hv) < uint32_t(a.P[2]));
             const uint32_t u = xorg + uint32_t(zr) * a.xplane + uint32_t(yr) * a.xrow + lxh;
-            __builtin_amdgcn_raw_ptr_buffer_load_lds(rx, SC_LDSW(dst + C::X_BYTES + hi * 1024), 16,
-                                                     ok ? u : a.tile_bytes, 0, 0, 0);
+            xload(rx, rl, rh, dst + C::X_BYTES + hi * 1024, u, ok, i0 + zr, i1 + yr, touch);
         }
 #pragma unroll
         for (int j = LI; j < C::Y_INSTR; j += KS) {
@@ -678,12 +726,12 @@ WxPlan plan_wx(const Tile3& t, const Conv3& cv, shard_dtype_t dt)
 }
 
 template <int KD, int NCI, int NCO, int BZ, int BY, int KS, int NB>
-hipError_t run_wx(const WxPlan& p, float* dw, hipStream_t s)
+hipError_t run_wx(const WxPlan& p, float* dw, bool fold, hipStream_t s)
 {
     using C = WxCfg<KD, NCI, NCO, BZ, BY>;
     constexpr int LDS = NB * C::STAGE_BYTES + (KS == 2 ? 8 * NB + 16 : 0);
     static_assert(LDS <= 160 * 1024, "LDS budget");
-    auto fn = &wgrad_xm<KD, NCI, NCO, BZ, BY, KS, NB>;
+    auto fn = fold ? &wgrad_xm<KD, NCI, NCO, BZ, BY, KS, NB, true> : &wgrad_xm<KD, NCI, NCO, BZ, BY, KS, NB, false>;
     hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(fn), hipFuncAttributeMaxDynamicSharedMemorySize,
                                        LDS);
     if (e != hipSuccess) return e;
@@ -713,17 +761,40 @@ size_t wgrad_xm_workspace(const Tile3& t, const Conv3& cv, shard_dtype_t dt)
 // W with 3 (Ci = Co = 32) or 1 (Ci = Co = 64) taps in D, tiles and dy of < 4 GiB
 // per batch item, 16-byte aligned buffers. Launches the partial and the reduce
 // kernels; returns hipErrorNotSupported when it does not apply.
+// With a folded halo the margins must lie on one axis, 0 or 1, the slabs be
+// 16-byte aligned and below 4 GiB per batch item.
 hipError_t launch_wgrad_xm(const Tile3& t, const Conv3& cv, shard_dtype_t dt, const void* tile, const void* dy,
-                           float* dw, void* ws, hipStream_t s)
+                           float* dw, void* ws, const Fold* fold, hipStream_t s)
 {
     WxPlan p = plan_wx(t, cv, dt);
     if (!p.ok || reinterpret_cast<uintptr_t>(tile) % 16 != 0 || reinterpret_cast<uintptr_t>(dy) % 16 != 0 ||
         reinterpret_cast<uintptr_t>(ws) % 16 != 0)
         return hipErrorNotSupported;
+    p.a.fa = -1;
+    if (fold) {
+        if (fold->mask != 1u && fold->mask != 2u) return hipErrorNotSupported;
+        const int k = fold->mask == 1u ? 0 : 1;
+        p.a.fa = k;
+        p.a.flo = int32_t(t.lo[k]);
+        p.a.fhi = int32_t(t.lo[k] + t.ext[k]);
+        for (int sd = 0; sd < 2; ++sd) {
+            const int64_t w = sd == 0 ? t.lo[k] : t.hi[k];
+            const char* sp = fold->slab[k][sd];
+            if (reinterpret_cast<uintptr_t>(sp) % 16 != 0) return hipErrorNotSupported;
+            // slab [P0 or w][w or P1][P2][c]: no margins on the other axes
+            const int64_t sz = k == 0 ? int64_t(p.a.xplane) : w * int64_t(p.a.xrow);
+            const int64_t bb = (k == 0 ? w : t.P[0]) * sz;
+            if (bb >= (int64_t(1) << 32) - 64) return hipErrorNotSupported;
+            p.a.fslab[sd] = w > 0 ? sp : nullptr;
+            p.a.fbatch[sd] = uint32_t(bb);
+            p.a.fSZ[sd] = uint32_t(sz);
+        }
+    }
     p.a.tile = static_cast<const char*>(tile);
     p.a.dy = static_cast<const char*>(dy);
     p.a.part = static_cast<float*>(ws);
-    return p.cfg == 0 ? run_wx<3, 1, 1, kC3BZ, kC3BY, 2, kC3NB>(p, dw, s) : run_wx<1, 2, 2, 1, 8, 1, 2>(p, dw, s);
+    return p.cfg == 0 ? run_wx<3, 1, 1, kC3BZ, kC3BY, 2, kC3NB>(p, dw, fold != nullptr, s)
+                      : run_wx<1, 2, 2, 1, 8, 1, 2>(p, dw, fold != nullptr, s);
 }
 
 }  // namespace shardconv

@@ -130,6 +130,10 @@ hipError_t launch_conv_fwd_region(const Tile3& t, const Conv3& cv, shard_dtype_t
                                   FwdFamily fam, void* ws, hipStream_t s);
 hipError_t launch_conv_wgrad(const Tile3& t, const Conv3& cv, shard_dtype_t dt, const void* tile, const void* dy,
                              float* dw, void* ws, hipStream_t s);
+// The same with the halo folded into the loads (the kernels that cannot fold
+// are passed over).
+hipError_t launch_conv_wgrad_folded(const Tile3& t, const Conv3& cv, shard_dtype_t dt, const void* tile,
+                                    const void* dy, float* dw, void* ws, const Fold& fold, hipStream_t s);
 size_t conv_dgrad_workspace(const Tile3& t, const Conv3& cv, shard_dtype_t dt);
 hipError_t launch_conv_dgrad(const Tile3& t, const Conv3& cv, shard_dtype_t dt, const void* dy, const void* w,
                              void* dtile, void* ws, hipStream_t s);
@@ -151,7 +155,7 @@ hipError_t launch_conv_fwd_rows(const Tile3& t, const Conv3& cv, shard_dtype_t d
                                 const Fold* fold, hipStream_t s);
 size_t wgrad_xm_workspace(const Tile3& t, const Conv3& cv, shard_dtype_t dt);
 hipError_t launch_wgrad_xm(const Tile3& t, const Conv3& cv, shard_dtype_t dt, const void* tile, const void* dy,
-                           float* dw, void* ws, hipStream_t s);
+                           float* dw, void* ws, const Fold* fold, hipStream_t s);
 size_t wgrad_tr_workspace(const Tile3& t, const Conv3& cv, shard_dtype_t dt);
 hipError_t launch_wgrad_tr(const Tile3& t, const Conv3& cv, shard_dtype_t dt, const void* tile, const void* dy,
                            float* part, int32_t red[6], hipStream_t s);

@@ -75,6 +75,8 @@ _SIGS = {
     "shard_halo_pack_pair": (ctypes.c_int, [_tp, ctypes.c_int, _vp, ctypes.c_int32, ctypes.c_int64, _vp,
                                             ctypes.c_int64, _vp, _vp]),
     "shard_halo_unpack_pair": (ctypes.c_int, [_tp, ctypes.c_int, _vp, ctypes.c_int32, _vp, _vp, _vp]),
+    "shard_conv_wgrad_folded": (ctypes.c_int, [_tp, ctypes.c_int, _vp, ctypes.c_void_p, _vp, ctypes.c_int64, _i64p,
+                                               _i64p, _i64p, _i64p, _vp, _vp, ctypes.c_size_t, _vp]),
     "shard_status_string": (ctypes.c_char_p, [ctypes.c_int]),
 }
 for _name, (_res, _args) in _SIGS.items():
@@ -280,3 +282,15 @@ def shard_halo_unpack_pair(desc, tile, axis, slab_lo=None, slab_hi=None, stream=
     _check("shard_halo_unpack_pair", _lib.shard_halo_unpack_pair(ctypes.byref(desc), _dtype_code(tile), _ptr(tile),
                                                                  axis, _ptr(slab_lo), _ptr(slab_hi),
                                                                  _stream(stream)))
+
+
+def shard_conv_wgrad_folded(desc, tile, slabs, dy, c_out, kernel, stride, pad_lo, out_ext, dw, ws, stream=None):
+    """Weight gradient with the halo read from the received slabs ({(axis, side):
+    tensor or None}, or None for no slabs)."""
+    h = None if slabs is None else halo_src(slabs)
+    st = _lib.shard_conv_wgrad_folded(ctypes.byref(desc), _dtype_code(tile), _ptr(tile),
+                                      None if h is None else ctypes.cast(ctypes.byref(h), ctypes.c_void_p), _ptr(dy),
+                                      c_out, _arr(kernel), _arr(stride), _arr(pad_lo), _arr(out_ext), _ptr(dw),
+                                      _ptr(ws), ws.numel() * ws.element_size() if ws is not None else 0,
+                                      _stream(stream))
+    _check("shard_conv_wgrad_folded", st)

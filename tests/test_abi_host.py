@@ -363,3 +363,21 @@ def test_attention_rejections(sc):
     assert call(k=None) == sc.SHARD_ERR_INVALID
     assert call(sk=1 << 30) == sc.SHARD_ERR_UNSUPPORTED           # 32-bit key offsets
     assert call(sq=0, q=None, o=None, lse=None) == sc.SHARD_OK    # nothing to do
+
+
+@pytestmark_host
+def test_folded_wgrad_rejections(sc):
+    lib = _raw(sc)
+    A = lambda *v: (ctypes.c_int64 * 3)(*v)
+    d = sc.tile_desc(1, 16, [8, 8, 40], [1, 0, 0], [1, 0, 0])
+    p = ctypes.byref(d)
+    K, S, pad, O = A(3, 3, 3), A(1, 1, 1), A(0, 1, 1), A(8, 8, 40)
+    need = sc.shard_conv_workspace_bytes(1, d, sc.SHARD_BF16, 32, [3, 3, 3], [1, 1, 1], [8, 8, 40])
+    f = lib.shard_conv_wgrad_folded
+    h = sc.shard_halo_src_t()
+    hp = ctypes.cast(ctypes.byref(h), ctypes.c_void_p)
+    assert f(p, 1, FAKE, hp, FAKE, 32, K, S, pad, O, FAKE, FAKE, need - 1, None) == sc.SHARD_ERR_INVALID  # short ws
+    assert f(p, 1, FAKE, hp, FAKE, 32, K, S, pad, O, None, FAKE, need, None) == sc.SHARD_ERR_INVALID      # null dw
+    assert f(p, 1, FAKE, hp, None, 32, K, S, pad, O, FAKE, FAKE, need, None) == sc.SHARD_ERR_INVALID      # null dy
+    h.slab[0][0] = 0x10001                                                                            # misaligned
+    assert f(p, 1, FAKE, hp, FAKE, 32, K, S, pad, O, FAKE, FAKE, need, None) == sc.SHARD_ERR_INVALID

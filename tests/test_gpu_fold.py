@@ -173,3 +173,68 @@ def test_full_size_folded_and_split_equal_unpacked(sc, name):
     assert torch.equal(y.view(torch.int16 if w.dtype == "bf16" else torch.int32),
                        want.view(torch.int16 if w.dtype == "bf16" else torch.int32))
     log(f"full folded {name}: ok")
+
+
+def _wgrad_folded(sc, w, desc, tile, slabs, sg, dy):
+    import torch
+    O = sg.g["out_ext"]
+    dw = torch.full((w.cout, w.cin) + tuple(w.K), float("nan"), device="cuda")
+    code = sc.SHARD_F32 if w.dtype == "f32" else sc.SHARD_BF16
+    n = sc.shard_conv_workspace_bytes(1, desc, code, w.cout, w.K, w.S, O)
+    ws = torch.empty(max(n, 16), dtype=torch.uint8, device="cuda")
+    sc.shard_conv_wgrad_folded(desc, tile, slabs, dy, w.cout, w.K, w.S, sg.g["pad_lo"], O, dw, ws)
+    return dw
+
+
+@pytest.mark.parametrize("name", list(cases.REDUCED))
+def test_folded_wgrad_equals_unpacked_every_shard_reduced(sc, name):
+    """The weight gradient reading the halo from the slabs (NaN canaries in every
+    margin) equals unpack + shard_conv_wgrad bit for bit, and the oracle."""
+    from gpu_util import dy_box, run_wgrad
+    w = cases.REDUCED[name]
+    for idx in w.shards():
+        log(f"folded wgrad {name} shard {idx}")
+        desc, tile, slabs, sg, full_h = _canary_tile_and_slabs(sc, w, idx)
+        dyh = dy_box(w, sg)
+        dy = dev(dyh)
+        got = _wgrad_folded(sc, w, desc, tile, slabs, sg, dy).cpu().numpy()
+        d2, t2, _, _ = build_tile(sc, w, idx)
+        want = run_wgrad(sc, w, d2, t2, sg, dy).cpu().numpy()
+        assert np.array_equal(got.view(np.uint32), want.view(np.uint32)), idx
+        xw, origin = window_from_tile(w, sg, full_h)
+        ref = cases.expected_wgrad(w, sg, xw, origin, cases.to_ncdhw(cases.as_f64(dyh, w)))
+        assert cases.norm_max_err(got.astype(np.float64), ref) <= cases.TOL[w.dtype], idx
+
+
+@pytest.mark.parametrize("name", ["c3r", "c2r", "c4r", "c5r", "c1"])
+@pytest.mark.parametrize("algo", ["", "tiled", "generic"])
+def test_folded_wgrad_kernel_variants_integer_exact(sc, monkeypatch, name, algo):
+    from gpu_util import dy_box
+    if algo:
+        monkeypatch.setenv("SHARDCONV_ALGO", algo)
+    w = cases.REDUCED[name]
+    idx = tuple(min(1, len(w.splits(a)) - 1) for a in range(w.nd))
+    desc, tile, slabs, sg, full_h = _canary_tile_and_slabs(sc, w, idx, INT_DIST)
+    dyh = dy_box(w, sg, INT_DIST)
+    got = _wgrad_folded(sc, w, desc, tile, slabs, sg, dev(dyh)).cpu().numpy().astype(np.float64)
+    xw, origin = window_from_tile(w, sg, full_h)
+    ref = cases.expected_wgrad(w, sg, xw, origin, cases.to_ncdhw(cases.as_f64(dyh, w)))
+    assert np.max(np.abs(ref)) < 2 ** 24
+    assert np.array_equal(got, ref)
+
+
+@pytest.mark.parametrize("name", ["c3_3d_bf16", "c2_2d_bf16"])
+def test_full_size_folded_wgrad_equals_unpacked(sc, name):
+    import torch
+    from gpu_util import dy_box, run_wgrad
+    w = cases.WORKLOADS[name]
+    log(f"full folded wgrad {name}: building tiles")
+    desc, tile, slabs, sg, full_h = _canary_tile_and_slabs(sc, w, w.shard)
+    del full_h
+    dy = dev(dy_box(w, sg))
+    d2, t2, _, _ = build_tile(sc, w, w.shard)
+    want = run_wgrad(sc, w, d2, t2, sg, dy)
+    del t2
+    got = _wgrad_folded(sc, w, desc, tile, slabs, sg, dy)
+    assert torch.equal(got.view(torch.int32), want.view(torch.int32))
+    log(f"full folded wgrad {name}: ok")
