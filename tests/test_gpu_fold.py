@@ -238,3 +238,53 @@ def test_full_size_folded_wgrad_equals_unpacked(sc, name):
     got = _wgrad_folded(sc, w, desc, tile, slabs, sg, dy)
     assert torch.equal(got.view(torch.int32), want.view(torch.int32))
     log(f"full folded wgrad {name}: ok")
+
+
+EDGE = [
+    # (name, dtype, N, cin, cout, G, parts, K, S)
+    ("1d_bf16", "bf16", 2, 16, 32, (301,), (3,), (5,), (1,)),
+    ("1d_f32_s3", "f32", 1, 8, 8, (97,), (4,), (3,), (3,)),
+    ("2d_k7_ragged_c", "bf16", 1, 24, 40, (29, 37), (3, 1), (7, 7), (1, 1)),
+    ("2d_f32_two_axes", "f32", 2, 5, 7, (19, 21), (2, 2), (3, 3), (2, 1)),
+    ("3d_s3_negative_pad", "f32", 1, 8, 16, (25, 9, 14), (2, 1, 1), (3, 3, 3), (3, 1, 2)),
+    ("3d_thin_w", "bf16", 1, 32, 32, (10, 11, 3), (2, 1, 1), (3, 3, 3), (1, 1, 1)),
+    ("3d_long_rows", "bf16", 1, 32, 32, (6, 5, 700), (2, 1, 1), (3, 3, 3), (1, 1, 1)),
+    ("3d_three_axes", "bf16", 1, 16, 16, (12, 10, 40), (2, 2, 2), (3, 3, 3), (1, 1, 1)),
+    ("2d_long_rows_h_split", "bf16", 2, 64, 64, (9, 1100), (2, 1), (3, 3), (1, 1)),
+]
+
+
+@pytest.mark.parametrize("case", EDGE, ids=lambda c: c[0])
+def test_folded_edge_shapes_every_shard_integer_exact(sc, case):
+    """Folded forward (whole, and interior then boundary) and folded weight
+    gradient on edge shapes - 1D, strides 2 and 3, negative pads, margins on two
+    and three axes (corners from the later axis's slab), odd channel counts, long
+    rows - bit for bit against the oracle on integer data, every shard."""
+    from gpu_util import dy_box
+    name, dt, N, cin, cout, G, parts, K, S = case
+    wl = cases.Workload(name, dt, N, cin, cout, G, parts, K, S, (0,) * len(G),
+                        x_dist=(synth.UNIFORM, (-1.0, 1.0)), w_dist=(synth.UNIFORM, (-0.5, 0.5)),
+                        dy_dist=(synth.UNIFORM, (-1.0, 1.0)))
+    w_host, w64 = weights(wl, INT_DIST)
+    wt = dev(w_host)
+    for idx in wl.shards():
+        log(f"folded edge {name} shard {idx}")
+        desc, tile, slabs, sg, full_h = _canary_tile_and_slabs(sc, wl, idx, INT_DIST)
+        xw, origin = window_from_tile(wl, sg, full_h)
+        ref = cases.expected_fwd(wl, sg, xw, origin, w64)
+        want = cases.bf16_rne_of_f64(ref) if dt == "bf16" else ref
+        for parts_ in ((sc.SHARD_REGION_ALL,), (sc.SHARD_REGION_INTERIOR, sc.SHARD_REGION_BOUNDARY)):
+            y = None
+            for region in parts_:
+                y = _folded(sc, wl, desc, tile, None if region == sc.SHARD_REGION_INTERIOR else slabs, sg, wt,
+                            region, y)
+            got = host(y)
+            if dt == "bf16":
+                assert np.array_equal(got, want), (idx, parts_)
+            else:
+                assert np.array_equal(got.astype(np.float64), want), (idx, parts_)
+        dyh = dy_box(wl, sg, INT_DIST)
+        dref = cases.expected_wgrad(wl, sg, xw, origin, cases.to_ncdhw(cases.as_f64(dyh, wl)))
+        assert np.max(np.abs(dref)) < 2 ** 24
+        dw = _wgrad_folded(sc, wl, desc, tile, slabs, sg, dev(dyh)).cpu().numpy().astype(np.float64)
+        assert np.array_equal(dw, dref), idx
