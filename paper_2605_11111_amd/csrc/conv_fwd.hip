@@ -50,7 +50,7 @@ struct FwdArgs {
     int32_t BI[3];     // input brick
     int32_t NB[3];     // bricks per axis
     int32_t nq;        // 16-byte units per voxel in LDS (per pass)
-    int32_t vpl_s;     // swizzle divisor (voxels per 256 B line, times W stride)
+    int32_t vpl_sh;    // swizzle period, log2 (voxels per 256 B line times the W stride, rounded down to 2^k)
     int32_t qmask;     // swizzle mask
     int32_t cc;        // channels per pass
     int32_t npass;
@@ -84,26 +84,48 @@ struct Traits<float> {
     static constexpr int esz = 4;
 };
 
-__device__ __forceinline__ int swz(int v, int vpl_s, int qmask) { return (v / vpl_s) & qmask; }
+__device__ __forceinline__ int swz(int v, int vpl_sh, int qmask) { return (v >> vpl_sh) & qmask; }
+
+// Visit every 16-byte unit (voxel v = (z, y, x) of the brick, channel unit q)
+// once across the block. When a (z, y) row of units fits the block, a thread
+// keeps its column (x, q) and steps over rows: one division per row instead of
+// three per unit.
+template <typename F>
+__device__ __forceinline__ void for_each_unit(const FwdArgs& a, F&& fn)
+{
+    const int nq = a.nq;
+    const int rowlen = a.BI[2] * nq;
+    if (rowlen <= kThreads) {
+        const int rpp = kThreads / rowlen;
+        const int r0 = int(threadIdx.x) / rowlen, cu = int(threadIdx.x) - r0 * rowlen;
+        if (r0 >= rpp) return;
+        const int x = cu / nq, q = cu - x * nq;
+        const int rows = a.BI[0] * a.BI[1];
+        for (int r = r0; r < rows; r += rpp) {
+            const int z = r / a.BI[1], y = r - z * a.BI[1];
+            fn(r * a.BI[2] + x, q, z, y, x);
+        }
+        return;
+    }
+    const int total = a.BI[0] * a.BI[1] * a.BI[2] * nq;
+    for (int u = threadIdx.x; u < total; u += kThreads) {
+        const int q = u % nq;
+        const int v = u / nq;
+        const int x = v % a.BI[2];
+        const int yz = v / a.BI[2];
+        fn(v, q, yz / a.BI[1], yz % a.BI[1], x);
+    }
+}
 
 // Stage the input brick channels [c0, c0 + cc) into LDS.
 template <typename T>
 __device__ __forceinline__ void stage_brick(const FwdArgs& a, uint4* lds, int64_t nn, const int64_t i0[3], int c0)
 {
     constexpr int kPerUnit = 16 / Traits<T>::esz;
-    const int nq = a.nq;
-    const int biv = a.BI[0] * a.BI[1] * a.BI[2];
-    const int total = biv * nq;
     const bool vec_ok = a.vec != 0;
     if (a.fold.mask) {
         // margin voxels come from the received slabs (or are zero)
-        for (int u = threadIdx.x; u < total; u += kThreads) {
-            const int q = u % nq;
-            const int v = u / nq;
-            const int x = v % a.BI[2];
-            const int yz = v / a.BI[2];
-            const int y = yz % a.BI[1];
-            const int z = yz / a.BI[1];
+        for_each_unit(a, [&](int v, int q, int z, int y, int x) {
             const int64_t t0 = i0[0] + z, t1 = i0[1] + y, t2 = i0[2] + x;
             const int c = c0 + q * kPerUnit;
             uint4 val = make_uint4(0, 0, 0, 0);
@@ -121,17 +143,11 @@ __device__ __forceinline__ void stage_brick(const FwdArgs& a, uint4* lds, int64_
                     }
                 }
             }
-            lds[v * nq + (q ^ swz(v, a.vpl_s, a.qmask))] = val;
-        }
+            lds[v * a.nq + (q ^ swz(v, a.vpl_sh, a.qmask))] = val;
+        });
         return;
     }
-    for (int u = threadIdx.x; u < total; u += kThreads) {
-        const int q = u % nq;
-        const int v = u / nq;
-        const int x = v % a.BI[2];
-        const int yz = v / a.BI[2];
-        const int y = yz % a.BI[1];
-        const int z = yz / a.BI[1];
+    for_each_unit(a, [&](int v, int q, int z, int y, int x) {
         const int64_t t0 = i0[0] + z, t1 = i0[1] + y, t2 = i0[2] + x;
         const int c = c0 + q * kPerUnit;
         uint4 val = make_uint4(0, 0, 0, 0);
@@ -147,8 +163,8 @@ __device__ __forceinline__ void stage_brick(const FwdArgs& a, uint4* lds, int64_
                 val = *reinterpret_cast<const uint4*>(tmp);
             }
         }
-        lds[v * nq + (q ^ swz(v, a.vpl_s, a.qmask))] = val;
-    }
+        lds[v * a.nq + (q ^ swz(v, a.vpl_sh, a.qmask))] = val;
+    });
 }
 
 template <typename T>
@@ -231,6 +247,18 @@ __global__ __launch_bounds__(kThreads, 2) void conv_fwd_tiled(FwdArgs a)
             for (int j = 0; j < RN; ++j) bcur[j] = a.wfrag[(fb + j) * 64 + lane];
         }
         int t0 = 0, t1 = 0, t2 = 0, kc = 0;
+        // A fragments (LDS) of the next iteration are read while this one multiplies
+        auto read_a = [&](int tt0, int tt1, int tt2, int kkc, uint4 (&av)[RM]) {
+            const int toff = tt0 * plane + tt1 * a.BI[2] + tt2;
+            const int q = 2 * kkc + g;
+#pragma unroll
+            for (int i = 0; i < RM; ++i) {
+                const int v = vbase[i] + toff;
+                av[i] = lds[v * a.nq + (q ^ swz(v, a.vpl_sh, a.qmask))];
+            }
+        };
+        uint4 acur[RM];
+        read_a(0, 0, 0, 0, acur);
         for (int it = 0; it < iters; ++it) {
             // next (tap, kc)
             int nkc_ = kc + 1, n2 = t2, n1 = t1, n0 = t0;
@@ -245,26 +273,22 @@ __global__ __launch_bounds__(kThreads, 2) void conv_fwd_tiled(FwdArgs a)
                 }
             }
             uint4 bnext[RN];
+            uint4 anext[RM];
             if (it + 1 < iters) {
                 const int ntap = (n0 * a.K[1] + n1) * a.K[2] + n2;
                 const int64_t fb = (int64_t(ntap) * a.nkc + p * kcp + nkc_) * a.nt + nt0;
 #pragma unroll
                 for (int j = 0; j < RN; ++j) bnext[j] = a.wfrag[(fb + j) * 64 + lane];
-            }
-            const int toff = t0 * plane + t1 * a.BI[2] + t2;
-            const int q = 2 * kc + g;
-            uint4 av[RM];
-#pragma unroll
-            for (int i = 0; i < RM; ++i) {
-                const int v = vbase[i] + toff;
-                av[i] = lds[v * a.nq + (q ^ swz(v, a.vpl_s, a.qmask))];
+                read_a(n0, n1, n2, nkc_, anext);
             }
 #pragma unroll
             for (int i = 0; i < RM; ++i)
 #pragma unroll
-                for (int j = 0; j < RN; ++j) mfma_step<T>(acc[i][j], av[i], bcur[j]);
+                for (int j = 0; j < RN; ++j) mfma_step<T>(acc[i][j], acur[i], bcur[j]);
 #pragma unroll
             for (int j = 0; j < RN; ++j) bcur[j] = bnext[j];
+#pragma unroll
+            for (int i = 0; i < RM; ++i) acur[i] = anext[i];
             kc = nkc_;
             t0 = n0;
             t1 = n1;
@@ -272,17 +296,30 @@ __global__ __launch_bounds__(kThreads, 2) void conv_fwd_tiled(FwdArgs a)
         }
     }
 
-    // epilogue: lane holds column lane%32, rows 8*(r/4) + 4*g + (r%4)
+    // epilogue: lane holds column lane%32, rows 8*(r/4) + 4*g + (r%4); the
+    // brick coordinates of a row are advanced from the previous row's (carries
+    // instead of divisions)
     T* y = reinterpret_cast<T*>(a.y);
 #pragma unroll
     for (int i = 0; i < RM; ++i) {
+        const int fb = (wave * RM + i) * 32 + 4 * g;
+        int ox = fb % a.BO[2];
+        int oy = (fb / a.BO[2]) % a.BO[1];
+        int oz = fb / (a.BO[2] * a.BO[1]);
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
-            const int f = (wave * RM + i) * 32 + 8 * (r >> 2) + 4 * g + (r & 3);
+            if (r > 0) {
+                ox += (r & 3) == 0 ? 5 : 1;
+                while (ox >= a.BO[2]) {
+                    ox -= a.BO[2];
+                    if (++oy == a.BO[1]) {
+                        oy = 0;
+                        ++oz;
+                    }
+                }
+            }
+            const int f = fb + 8 * (r >> 2) + (r & 3);
             if (f >= bov) continue;
-            const int ox = f % a.BO[2];
-            const int oy = (f / a.BO[2]) % a.BO[1];
-            const int oz = f / (a.BO[2] * a.BO[1]);
             const int64_t o0 = ob[0] + oz, o1 = ob[1] + oy, o2 = ob[2] + ox;
             if (o0 >= a.O[0] || o1 >= a.O[1] || o2 >= a.O[2]) continue;
             const int64_t vox = a.ybase + nn * a.ys[0] + (a.org[0] + o0) * a.ys[1] + (a.org[1] + o1) * a.ys[2] +
@@ -402,7 +439,8 @@ PlanF plan_fwd_t(const Tile3& t, const Conv3& cv)
     }
     a.nq = int32_t(a.cc * esz / 16);
     const int vpl = std::max(1, 16 / a.nq);
-    a.vpl_s = int32_t(vpl * a.S[2]);
+    a.vpl_sh = 0;
+    while ((int64_t(2) << a.vpl_sh) <= int64_t(vpl) * a.S[2]) ++a.vpl_sh;
     // XOR swizzle only when the unit count is a power of two (stays inside the voxel)
     a.qmask = (a.nq & (a.nq - 1)) == 0 ? int32_t(std::min(a.nq, 16) - 1) : 0;
     a.npass = int32_t(ceil_div(cfull, a.cc));
