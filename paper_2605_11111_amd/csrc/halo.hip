@@ -3,9 +3,12 @@
 // convolution, ShardTensor section "PyTorch Dispatch").
 //
 // The box is `rows` runs of `run` contiguous bytes (contiguous inner axes are
-// merged on the host). Each thread moves U vectors of V bytes (U = 8 for 16-byte
-// vectors), all loads issued before any store; consecutive lanes touch
-// consecutive vectors, so every wave instruction covers 64*V contiguous bytes.
+// merged on the host), seen as a sequence of V-byte vectors cut into chunks of
+// kThreads * U vectors (64 KiB for 16-byte vectors). A workgroup moves whole
+// chunks, each thread U vectors of it, all loads issued before any store;
+// consecutive lanes touch consecutive vectors, so every wave instruction covers
+// 64*V contiguous bytes and a workgroup's accesses stay within one chunk (this
+// measured faster than spreading a thread's vectors over the whole box).
 // Loads and stores are nontemporal: a slab is read or written once per exchange,
 // and streaming it past the caches measured faster than cached accesses for a
 // 16 MiB face. A single-run box (the common case of a slab along the outermost
@@ -30,7 +33,7 @@ struct CopyArgs {
     int dir;             // CopyDir
 };
 
-constexpr int kThreads = 256;
+constexpr int kThreads = 512;
 
 template <int V>
 struct Vec;
@@ -98,14 +101,13 @@ __global__ __launch_bounds__(kThreads) void box_copy_kernel(CopyArgs2 aa)
     const CopyArgs a = pick_box(aa, second);
     const int64_t nblk = second ? int64_t(gridDim.x) - aa.nblk0 : aa.nblk0;
     const int64_t blk = second ? int64_t(blockIdx.x) - aa.nblk0 : int64_t(blockIdx.x);
-    const int64_t nthreads = nblk * kThreads;
-    const int64_t tid = blk * kThreads + threadIdx.x;
-    for (int64_t v0 = tid; v0 < a.total; v0 += nthreads * kUnroll) {
+    constexpr int64_t kChunk = int64_t(kThreads) * kUnroll;
+    for (int64_t v0 = blk * kChunk + threadIdx.x; v0 < a.total; v0 += nblk * kChunk) {
         T val[kUnroll];
         int64_t off[kUnroll];
 #pragma unroll
         for (int u = 0; u < kUnroll; ++u) {
-            const int64_t v = v0 + u * nthreads;
+            const int64_t v = v0 + u * kThreads;
             off[u] = v < a.total ? tile_offset<V, kSingleRun>(a, v) : 0;
             if (v < a.total) {
                 if (a.dir == TILE_TO_SLAB) {
@@ -119,7 +121,7 @@ __global__ __launch_bounds__(kThreads) void box_copy_kernel(CopyArgs2 aa)
         }
 #pragma unroll
         for (int u = 0; u < kUnroll; ++u) {
-            const int64_t v = v0 + u * nthreads;
+            const int64_t v = v0 + u * kThreads;
             if (v < a.total) {
                 if (a.dir == TILE_TO_SLAB) {
                     __builtin_nontemporal_store(val[u], reinterpret_cast<T*>(a.dst + v * V));
@@ -182,14 +184,13 @@ __global__ __launch_bounds__(kThreads) void box_add_kernel(CopyArgs a)
     using T = typename Vec<V>::T;
     constexpr int kUnroll = Vec<V>::U;
     constexpr int NE = V / int(sizeof(E));
-    const int64_t nthreads = int64_t(gridDim.x) * kThreads;
-    const int64_t tid = int64_t(blockIdx.x) * kThreads + threadIdx.x;
-    for (int64_t v0 = tid; v0 < a.total; v0 += nthreads * kUnroll) {
+    constexpr int64_t kChunk = int64_t(kThreads) * kUnroll;
+    for (int64_t v0 = int64_t(blockIdx.x) * kChunk + threadIdx.x; v0 < a.total; v0 += int64_t(gridDim.x) * kChunk) {
         T sv[kUnroll], tv[kUnroll];
         int64_t off[kUnroll];
 #pragma unroll
         for (int u = 0; u < kUnroll; ++u) {
-            const int64_t v = v0 + u * nthreads;
+            const int64_t v = v0 + u * kThreads;
             off[u] = v < a.total ? tile_offset<V, kSingleRun>(a, v) : 0;
             if (v < a.total) {
                 sv[u] = __builtin_nontemporal_load(reinterpret_cast<const T*>(a.src + v * V));
@@ -198,7 +199,7 @@ __global__ __launch_bounds__(kThreads) void box_add_kernel(CopyArgs a)
         }
 #pragma unroll
         for (int u = 0; u < kUnroll; ++u) {
-            const int64_t v = v0 + u * nthreads;
+            const int64_t v = v0 + u * kThreads;
             if (v < a.total) {
                 E es[NE], et[NE];
                 __builtin_memcpy(es, &sv[u], V);
