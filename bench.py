@@ -18,6 +18,12 @@ the halo folded into its loads (whole, interior, boundary) and one ring-attentio
 block step - are timed after the step and reported under "next_rows"; they are
 not part of `value`.
 
+Beside the published peaks the line carries the part's measured ceilings: a
+device-to-device copy of the halo launch's bytes ("measured_copy_ceiling"), and a
+matrix-instruction-only kernel with the shader clock it ran at plus hipBLASLt on
+a large square bf16 GEMM ("measured_mfma_ceiling"; bf16 workloads, skipped with
+--no-backward).
+
 The roofline's "traffic" field is the HBM traffic of the dominant kernel measured
 with rocprofv3 counters (FETCH_SIZE and WRITE_SIZE, each scaled by what it reads
 for a plain device copy of known size) and recorded in
@@ -95,7 +101,8 @@ def main():
     ap.add_argument("--copy-calibration", action="store_true",
                     help="run one 64 MiB device-to-device copy first (reference for counter scaling)")
     ap.add_argument("--no-backward", action="store_true",
-                    help="skip the ops beyond the step (input gradient, reverse halo, group normalisation)")
+                    help="skip the ops beyond the step (input gradient, reverse halo, group normalisation, "
+                         "folded forward, attention) and the measured MFMA ceiling")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU's shard; --gpus {args.gpus} is not supported: this build has no "
@@ -244,6 +251,7 @@ def main():
 
     halo_bytes = max((work for (label, kind, work, _) in ops if kind in ("pack", "unpack")), default=0)
     ceiling = measured_ceiling(args, stream, int(halo_bytes)) if halo_bytes else None
+    mfma_ceiling = measured_mfma_ceiling(stream) if dt == "bf16" and not args.no_backward else None
     cpu = None if args.no_cpu_baseline else cpu_baseline(w, g, tile_lo)
     line = {
         "metric": "shard conv fwd+wgrad TFLOP/s (% MFMA peak); halo pack/unpack GB/s (% HBM)",
@@ -254,7 +262,8 @@ def main():
                    "tile_padded": [w.N] + [l + e + h for l, e, h in zip(lo, ext, hi)] + [w.cin],
                    "out": [w.N] + list(O) + [w.cout], "kernel": list(w.K), "stride": list(w.S),
                    "accumulate": "f32"},
-        "ops": detail, "roofline": roofline, "measured_copy_ceiling": ceiling, "cpu_baseline": cpu,
+        "ops": detail, "roofline": roofline, "measured_copy_ceiling": ceiling,
+        "measured_mfma_ceiling": mfma_ceiling, "cpu_baseline": cpu,
         "next_rows": next_rows,
     }
     print(json.dumps(line), flush=True)
@@ -405,6 +414,55 @@ def measured_ceiling(args, stream, nbytes):
     del pairs, flush
     return {"ms": round(ms, 4), "gbs": round(gbs, 1), "frac_hbm_peak": round(gbs / HBM_PEAK, 4), "bytes": int(nbytes),
             "what": "device-to-device copy of the same bytes (torch copy_), median of event-timed launches"}
+
+
+def measured_mfma_ceiling(stream):
+    """The part's sustained bf16 matrix rate and shader clock: a kernel of
+    nothing but v_mfma_f32_32x32x16_bf16 (one 4-wave workgroup per compute unit,
+    4 independent chains per wave, libshardprobe.so), median of 3 launches; and
+    the rate hipBLASLt reaches on a large square bf16 GEMM (torch.matmul), the
+    vendor library's own ceiling for a plain contraction. Context beside the
+    published peak, not a bound of the path."""
+    import numpy as np
+    import torch
+    from paper_2605_11111_amd import probe
+    cus = torch.cuda.get_device_properties(0).multi_processor_count
+    iters = 20000
+    out = torch.empty(cus * 256, dtype=torch.float32, device="cuda")
+    clk = torch.empty(2 * cus, dtype=torch.int64, device="cuda")
+    res = []
+    for k in range(4):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        probe.shard_probe_mfma_bf16(iters, cus, out, clk)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        c = clk.cpu().numpy().reshape(-1, 2).astype(np.float64)
+        mhz = float(np.mean(c[:, 0] / (c[:, 1] / 100.0)))
+        if k > 0:
+            res.append((e0.elapsed_time(e1), mhz))
+    ms, mhz = sorted(res)[len(res) // 2]
+    tf = 2.0 * 32 * 32 * 16 * 4 * iters * cus * 4 / (ms * 1e-3) / 1e12
+    n = 8192
+    a = torch.randn(n, n, device="cuda", dtype=torch.bfloat16)
+    b = torch.randn(n, n, device="cuda", dtype=torch.bfloat16)
+    for _ in range(3):
+        torch.matmul(a, b)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(10):
+        torch.matmul(a, b)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    gms = e0.elapsed_time(e1) / 10
+    gtf = 2.0 * n ** 3 / (gms * 1e-3) / 1e12
+    del a, b
+    return {"mfma_only": {"tflops": round(tf, 1), "frac_mfma_peak": round(tf / PEAK["bf16"], 4),
+                          "shader_clock_mhz": round(mhz), "ms": round(ms, 4),
+                          "what": "v_mfma_f32_32x32x16_bf16 only, 4 chains per wave, 1 wave per SIMD"},
+            "gemm": {"tflops": round(gtf, 1), "frac_mfma_peak": round(gtf / PEAK["bf16"], 4), "ms": round(gms, 4),
+                     "what": "torch.matmul bf16 8192x8192x8192 (hipBLASLt)"}}
 
 
 def time_attention(sc, args, stream):

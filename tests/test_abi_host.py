@@ -37,6 +37,19 @@ def test_library_exports_every_declared_symbol(sc):
     assert set(names) == set(sc.EXPORTED)
 
 
+def test_probe_library_exports_its_header():
+    from paper_2605_11111_amd import probe
+    text = re.sub(r"/\*.*?\*/", "", open(os.path.join(ROOT, "include", "shardprobe.h")).read(), flags=re.S)
+    names = sorted(set(re.findall(r"\b(shard_[a-z_0-9]+)\s*\(", text)))
+    assert names == sorted(probe.EXPORTED)
+    lib = ctypes.CDLL(probe.LIB_PATH)
+    for n in names:
+        assert hasattr(lib, n), n
+    # argument checks happen before any launch
+    assert lib.shard_probe_mfma_bf16(ctypes.c_int64(0), 1, ctypes.c_void_p(8), ctypes.c_void_p(8), None) == 1
+    assert lib.shard_probe_mfma_bf16(ctypes.c_int64(1), 1, None, ctypes.c_void_p(8), None) == 1
+
+
 def test_status_strings(sc):
     assert sc.shard_status_string(0) == "ok"
     assert "invalid" in sc.shard_status_string(1)
