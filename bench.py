@@ -419,10 +419,12 @@ def measured_ceiling(args, stream, nbytes):
 def measured_mfma_ceiling(stream):
     """The part's sustained bf16 matrix rate and shader clock: a kernel of
     nothing but v_mfma_f32_32x32x16_bf16 (one 4-wave workgroup per compute unit,
-    4 independent chains per wave, libshardprobe.so), median of 3 launches; and
-    the rate hipBLASLt reaches on a large square bf16 GEMM (torch.matmul), the
-    vendor library's own ceiling for a plain contraction. Context beside the
-    published peak, not a bound of the path."""
+    4 independent chains per wave, libshardprobe.so), on constant operands and
+    on random ones that change every instruction (the part is power-limited and
+    toggling operands lower its clock), median of 3 launches each; and the rate
+    hipBLASLt reaches on a large square bf16 GEMM of N(0, 1) operands
+    (torch.matmul), the vendor library's own figure for a plain contraction.
+    Context beside the published peak, not a bound of the path."""
     import numpy as np
     import torch
     from paper_2605_11111_amd import probe
@@ -430,19 +432,26 @@ def measured_mfma_ceiling(stream):
     iters = 20000
     out = torch.empty(cus * 256, dtype=torch.float32, device="cuda")
     clk = torch.empty(2 * cus, dtype=torch.int64, device="cuda")
-    res = []
-    for k in range(4):
-        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        e0.record(stream)
-        probe.shard_probe_mfma_bf16(iters, cus, out, clk)
-        e1.record(stream)
-        torch.cuda.synchronize()
-        c = clk.cpu().numpy().reshape(-1, 2).astype(np.float64)
-        mhz = float(np.mean(c[:, 0] / (c[:, 1] / 100.0)))
-        if k > 0:
-            res.append((e0.elapsed_time(e1), mhz))
-    ms, mhz = sorted(res)[len(res) // 2]
-    tf = 2.0 * 32 * 32 * 16 * 4 * iters * cus * 4 / (ms * 1e-3) / 1e12
+    res = {}
+    for random in (False, True):
+        runs = []
+        for k in range(4):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            probe.shard_probe_mfma_bf16(iters, cus, random, out, clk)
+            e1.record(stream)
+            torch.cuda.synchronize()
+            c = clk.cpu().numpy().reshape(-1, 2).astype(np.float64)
+            mhz = float(np.mean(c[:, 0] / (c[:, 1] / 100.0)))
+            if k > 0:
+                runs.append((e0.elapsed_time(e1), mhz))
+        ms, mhz = sorted(runs)[len(runs) // 2]
+        tf = 2.0 * 32 * 32 * 16 * 4 * iters * cus * 4 / (ms * 1e-3) / 1e12
+        res["mfma_only_random" if random else "mfma_only_constant"] = {
+            "tflops": round(tf, 1), "frac_mfma_peak": round(tf / PEAK["bf16"], 4), "shader_clock_mhz": round(mhz),
+            "ms": round(ms, 4),
+            "what": "v_mfma_f32_32x32x16_bf16 only, 4 chains per wave, 1 wave per SIMD, "
+                    + ("random N(0,1) operands changing every instruction" if random else "constant operands")}
     n = 8192
     a = torch.randn(n, n, device="cuda", dtype=torch.bfloat16)
     b = torch.randn(n, n, device="cuda", dtype=torch.bfloat16)
@@ -458,11 +467,9 @@ def measured_mfma_ceiling(stream):
     gms = e0.elapsed_time(e1) / 10
     gtf = 2.0 * n ** 3 / (gms * 1e-3) / 1e12
     del a, b
-    return {"mfma_only": {"tflops": round(tf, 1), "frac_mfma_peak": round(tf / PEAK["bf16"], 4),
-                          "shader_clock_mhz": round(mhz), "ms": round(ms, 4),
-                          "what": "v_mfma_f32_32x32x16_bf16 only, 4 chains per wave, 1 wave per SIMD"},
-            "gemm": {"tflops": round(gtf, 1), "frac_mfma_peak": round(gtf / PEAK["bf16"], 4), "ms": round(gms, 4),
-                     "what": "torch.matmul bf16 8192x8192x8192 (hipBLASLt)"}}
+    res["gemm"] = {"tflops": round(gtf, 1), "frac_mfma_peak": round(gtf / PEAK["bf16"], 4), "ms": round(gms, 4),
+                   "what": "torch.matmul bf16 8192x8192x8192, N(0,1) operands (hipBLASLt)"}
+    return res
 
 
 def time_attention(sc, args, stream):

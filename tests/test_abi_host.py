@@ -46,8 +46,9 @@ def test_probe_library_exports_its_header():
     for n in names:
         assert hasattr(lib, n), n
     # argument checks happen before any launch
-    assert lib.shard_probe_mfma_bf16(ctypes.c_int64(0), 1, ctypes.c_void_p(8), ctypes.c_void_p(8), None) == 1
-    assert lib.shard_probe_mfma_bf16(ctypes.c_int64(1), 1, None, ctypes.c_void_p(8), None) == 1
+    assert lib.shard_probe_mfma_bf16(ctypes.c_int64(0), 1, 0, ctypes.c_void_p(8), ctypes.c_void_p(8), None) == 1
+    assert lib.shard_probe_mfma_bf16(ctypes.c_int64(6), 1, 0, ctypes.c_void_p(8), ctypes.c_void_p(8), None) == 1
+    assert lib.shard_probe_mfma_bf16(ctypes.c_int64(4), 1, 1, None, ctypes.c_void_p(8), None) == 1
 
 
 def test_status_strings(sc):
