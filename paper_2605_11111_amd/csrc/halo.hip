@@ -194,7 +194,7 @@ __global__ __launch_bounds__(kThreads) void box_add_kernel(CopyArgs a)
             off[u] = v < a.total ? tile_offset<V, kSingleRun>(a, v) : 0;
             if (v < a.total) {
                 sv[u] = __builtin_nontemporal_load(reinterpret_cast<const T*>(a.src + v * V));
-                tv[u] = *reinterpret_cast<const T*>(a.dst + off[u]);
+                tv[u] = __builtin_nontemporal_load(reinterpret_cast<const T*>(a.dst + off[u]));
             }
         }
 #pragma unroll
@@ -208,7 +208,7 @@ __global__ __launch_bounds__(kThreads) void box_add_kernel(CopyArgs a)
                 for (int i = 0; i < NE; ++i) et[i] = from_f32<E>(to_f32(et[i]) + to_f32(es[i]));
                 T r;
                 __builtin_memcpy(&r, et, V);
-                *reinterpret_cast<T*>(a.dst + off[u]) = r;
+                __builtin_nontemporal_store(r, reinterpret_cast<T*>(a.dst + off[u]));
             }
         }
     }
