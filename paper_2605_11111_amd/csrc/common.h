@@ -13,14 +13,10 @@ using bf16_t = uint16_t;
 __device__ __forceinline__ float to_f32(float v) { return v; }
 __device__ __forceinline__ float to_f32(bf16_t v) { return __uint_as_float(uint32_t(v) << 16); }
 
-// binary32 -> bfloat16, round to nearest even (NaN stays a quiet NaN).
-__device__ __forceinline__ bf16_t f32_to_bf16(float f)
-{
-    uint32_t b = __float_as_uint(f);
-    if ((b & 0x7f800000u) == 0x7f800000u) return bf16_t((b >> 16) | ((b & 0xffffu) ? 0x40u : 0u));
-    b += 0x7fffu + ((b >> 16) & 1u);
-    return bf16_t(b >> 16);
-}
+// binary32 -> bfloat16, round to nearest even (NaN stays a NaN): the hardware
+// conversion (v_cvt_pk_bf16_f32), one instruction instead of the integer
+// rounding sequence.
+__device__ __forceinline__ bf16_t f32_to_bf16(float f) { return __builtin_bit_cast(bf16_t, __bf16(f)); }
 
 template <typename T>
 __device__ __forceinline__ T from_f32(float v);
