@@ -272,9 +272,10 @@ def main():
 def time_backward(sc, w, g, desc, wt, dy, send, flops, args, stream):
     """The backward-pass ops of the same shard, timed after the step (they are not
     part of `value`): the input gradient onto the padded tile, then the reverse
-    halo - each margin's gradient packed for the neighbour it came from, and a
-    received gradient slab added onto each interior face (the slabs the forward
-    pack filled stand in for the neighbours' gradients: same shapes)."""
+    halo per axis - the margins' gradients packed for the neighbours they came
+    from (both sides in one launch), and the received gradient slabs added onto
+    the interior faces (one launch; the slabs the forward pack filled stand in
+    for the neighbours' gradients: same shapes)."""
     import numpy as np
     import torch
     tdt = torch.float32 if w.dtype == "f32" else torch.bfloat16
@@ -286,20 +287,26 @@ def time_backward(sc, w, g, desc, wt, dy, send, flops, args, stream):
                       dtype=torch.uint8, device="cuda")
     ops = [("conv_dgrad", "dgrad", flops,
             lambda: sc.shard_conv_dgrad(desc, dy, wt, w.cout, w.K, w.S, g["pad_lo"], O, dtile, wsd))]
-    for axis in range(w.nd):
+    # the reverse exchange runs the axes in descending order; both sides of an
+    # axis go out in one launch and come back in one launch
+    for axis in reversed(range(w.nd)):
+        bufs, moved = [None, None], 0
         for side in (0, 1):
             width = g["halo_lo"][axis] if side == 0 else g["halo_hi"][axis]
             if width > 0 and w.neighbour_exists(w.shard, axis, side):
-                buf = torch.empty(sc.shard_halo_slab_shape(desc, axis, width), dtype=tdt, device="cuda")
-                nbytes = buf.numel() * buf.element_size()
-                ops.append((f"pack_margin_a{axis}s{side}", "halo", 2 * nbytes,
-                            lambda axis=axis, side=side, buf=buf: sc.shard_halo_pack_margin(desc, dtile, axis, side,
-                                                                                            buf)))
-    for (axis, side, nwidth, buf, nbytes) in send:
-        # read slab + read and write the face rows
-        ops.append((f"accumulate_a{axis}s{side}", "halo", 3 * nbytes,
-                    lambda axis=axis, side=side, nwidth=nwidth, buf=buf:
-                    sc.shard_halo_accumulate(desc, dtile, axis, side, nwidth, buf)))
+                bufs[side] = torch.empty(sc.shard_halo_slab_shape(desc, axis, width), dtype=tdt, device="cuda")
+                moved += 2 * bufs[side].numel() * bufs[side].element_size()
+        if moved:
+            ops.append((f"pack_margin_a{axis}", "halo", moved,
+                        lambda axis=axis, b=bufs: sc.shard_halo_pack_margin_pair(desc, dtile, axis, b[0], b[1])))
+        recv = {side: (nwidth, buf, nbytes) for (a_, side, nwidth, buf, nbytes) in send if a_ == axis}
+        if recv:
+            wl, bl, nl = recv.get(0, (0, None, 0))
+            wh, bh, nh = recv.get(1, (0, None, 0))
+            # read slab + read and write the face rows
+            ops.append((f"accumulate_a{axis}", "halo", 3 * (nl + nh),
+                        lambda axis=axis, wl=wl, bl=bl, wh=wh, bh=bh:
+                        sc.shard_halo_accumulate_pair(desc, dtile, axis, wl, bl, wh, bh)))
     for _ in range(args.warmup):
         for op in ops:
             op[3]()

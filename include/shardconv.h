@@ -27,6 +27,8 @@
  *   shard_conv_dgrad      the input gradient read back onto the padded tile
  *   shard_halo_pack_margin, shard_halo_accumulate
  *                         the reverse halo exchange of the backward pass
+ *   shard_halo_pack_margin_pair, shard_halo_accumulate_pair
+ *                         both sides of an axis's reverse exchange in one launch
  *   shard_norm_stats, shard_norm_apply
  *                         group normalisation with statistics over all shards
  *   shard_attn_block      one block step of ring attention (log-space merge)
@@ -331,6 +333,23 @@ shard_status_t shard_halo_pack_margin(const shard_tile_t* x, shard_dtype_t dtype
  */
 shard_status_t shard_halo_accumulate(const shard_tile_t* x, shard_dtype_t dtype, void* tile, int32_t axis,
                                      int32_t side, int64_t width, const void* slab, hipStream_t stream);
+
+/*
+ * Both sides of an axis's reverse exchange in one launch each (the adjoint of
+ * shard_halo_pack_pair / shard_halo_unpack_pair): shard_halo_pack_margin_pair
+ * equals shard_halo_pack_margin of side 0 into slab_lo and of side 1 into
+ * slab_hi (a NULL slab skips that side; a zero-width margin is a no-op);
+ * shard_halo_accumulate_pair equals shard_halo_accumulate of side 0 with
+ * width_lo from slab_lo followed by side 1 with width_hi from slab_hi (width 0
+ * skips a side). When the two faces overlap (width_lo + width_hi > ext[axis])
+ * the sides are added by two launches in that order, so the result is the
+ * single calls' in every case. Arguments and errors: as the single calls.
+ */
+shard_status_t shard_halo_pack_margin_pair(const shard_tile_t* x, shard_dtype_t dtype, const void* tile,
+                                           int32_t axis, void* slab_lo, void* slab_hi, hipStream_t stream);
+shard_status_t shard_halo_accumulate_pair(const shard_tile_t* x, shard_dtype_t dtype, void* tile, int32_t axis,
+                                          int64_t width_lo, const void* slab_lo, int64_t width_hi,
+                                          const void* slab_hi, hipStream_t stream);
 
 /*
  * Workspace bytes shard_conv_fwd (op 0), shard_conv_wgrad (op 1) or

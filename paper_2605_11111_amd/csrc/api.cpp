@@ -411,6 +411,72 @@ shard_status_t shard_halo_accumulate(const shard_tile_t* x, shard_dtype_t dtype,
     return map_hip(launch_box_add(make_box(t, k, r0, r0 + width), t.esz, slab, tile, stream));
 }
 
+shard_status_t shard_halo_pack_margin_pair(const shard_tile_t* x, shard_dtype_t dtype, const void* tile,
+                                           int32_t axis, void* slab_lo, void* slab_hi, hipStream_t stream)
+{
+    Tile3 t;
+    if (!norm_tile(x, dtype, t) || axis < 0 || axis >= x->ndim) return SHARD_ERR_INVALID;
+    const int k = 3 - x->ndim + axis;
+    BoxCopy boxes[2];
+    const BoxCopy* bp[2];
+    CopyDir dirs[2] = {TILE_TO_SLAB, TILE_TO_SLAB};
+    const void* srcs[2] = {tile, tile};
+    void* dsts[2];
+    int n = 0;
+    for (int sd = 0; sd < 2; ++sd) {
+        void* slab = sd == 0 ? slab_lo : slab_hi;
+        if (!slab) continue;
+        const int64_t r0 = sd == 0 ? 0 : t.lo[k] + t.ext[k];
+        const int64_t r1 = sd == 0 ? t.lo[k] : t.P[k];
+        int64_t start[3], cnt[3];
+        slab_spans(t, k, r0, r1, start, cnt);
+        if (t.n * cnt[0] * cnt[1] * cnt[2] == 0) continue;
+        if (!tile || !aligned(tile, t.esz) || !aligned(slab, t.esz)) return SHARD_ERR_INVALID;
+        boxes[n] = make_box(t, k, r0, r1);
+        bp[n] = &boxes[n];
+        dsts[n] = slab;
+        ++n;
+    }
+    if (n == 0) return SHARD_OK;
+    return map_hip(launch_box_copies(bp, dirs, srcs, dsts, n, stream));
+}
+
+shard_status_t shard_halo_accumulate_pair(const shard_tile_t* x, shard_dtype_t dtype, void* tile, int32_t axis,
+                                          int64_t width_lo, const void* slab_lo, int64_t width_hi,
+                                          const void* slab_hi, hipStream_t stream)
+{
+    Tile3 t;
+    if (!norm_tile(x, dtype, t) || axis < 0 || axis >= x->ndim || width_lo < 0 || width_hi < 0)
+        return SHARD_ERR_INVALID;
+    const int k = 3 - x->ndim + axis;
+    if (width_lo > t.ext[k] || width_hi > t.ext[k]) return SHARD_ERR_UNSUPPORTED;
+    BoxCopy boxes[2];
+    const BoxCopy* bp[2];
+    const void* slabs[2];
+    int n = 0;
+    for (int sd = 0; sd < 2; ++sd) {
+        const int64_t width = sd == 0 ? width_lo : width_hi;
+        const void* slab = sd == 0 ? slab_lo : slab_hi;
+        const int64_t r0 = sd == 0 ? t.lo[k] : t.lo[k] + t.ext[k] - width;
+        int64_t start[3], cnt[3];
+        slab_spans(t, k, r0, r0 + width, start, cnt);
+        if (t.n * cnt[0] * cnt[1] * cnt[2] == 0) continue;
+        if (!tile || !slab || !aligned(tile, t.esz) || !aligned(slab, t.esz)) return SHARD_ERR_INVALID;
+        boxes[n] = make_box(t, k, r0, r0 + width);
+        bp[n] = &boxes[n];
+        slabs[n] = slab;
+        ++n;
+    }
+    if (n == 0) return SHARD_OK;
+    if (n == 2 && width_lo + width_hi > t.ext[k]) {
+        // overlapping faces: one launch per side, in order
+        hipError_t e = launch_box_adds(bp, t.esz, slabs, tile, 1, stream);
+        if (e != hipSuccess) return map_hip(e);
+        return map_hip(launch_box_adds(bp + 1, t.esz, slabs + 1, tile, 1, stream));
+    }
+    return map_hip(launch_box_adds(bp, t.esz, slabs, tile, n, stream));
+}
+
 size_t shard_conv_workspace_bytes(int32_t op, const shard_tile_t* x, shard_dtype_t dtype, int64_t c_out,
                                   const int64_t kernel[], const int64_t stride[], const int64_t out_ext[])
 {

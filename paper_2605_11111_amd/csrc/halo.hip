@@ -177,15 +177,21 @@ hipError_t launch_v(const BoxCopy* const* b, const CopyDir* dir, const void* con
 }
 
 // tile[box] += slab, element-wise in binary32 (bf16 sums rounded to nearest
-// even): the receiving half of the reverse halo exchange.
+// even): the receiving half of the reverse halo exchange. One launch adds one
+// or two boxes (both faces of an axis; they never overlap in one launch), split
+// over the blocks like box_copy_kernel.
 template <int V, typename E, bool kSingleRun>
-__global__ __launch_bounds__(kThreads) void box_add_kernel(CopyArgs a)
+__global__ __launch_bounds__(kThreads) void box_add_kernel(CopyArgs2 aa)
 {
     using T = typename Vec<V>::T;
     constexpr int kUnroll = Vec<V>::U;
     constexpr int NE = V / int(sizeof(E));
+    const bool second = int64_t(blockIdx.x) >= aa.nblk0;
+    const CopyArgs a = pick_box(aa, second);
+    const int64_t nblk = second ? int64_t(gridDim.x) - aa.nblk0 : aa.nblk0;
+    const int64_t blk = second ? int64_t(blockIdx.x) - aa.nblk0 : int64_t(blockIdx.x);
     constexpr int64_t kChunk = int64_t(kThreads) * kUnroll;
-    for (int64_t v0 = int64_t(blockIdx.x) * kChunk + threadIdx.x; v0 < a.total; v0 += int64_t(gridDim.x) * kChunk) {
+    for (int64_t v0 = blk * kChunk + threadIdx.x; v0 < a.total; v0 += nblk * kChunk) {
         T sv[kUnroll], tv[kUnroll];
         int64_t off[kUnroll];
 #pragma unroll
@@ -214,54 +220,51 @@ __global__ __launch_bounds__(kThreads) void box_add_kernel(CopyArgs a)
     }
 }
 
-template <int V>
-CopyArgs copy_args(const BoxCopy& b, CopyDir dir, const void* src, void* dst, int64_t& blocks, int64_t& rows)
-{
-    CopyArgs a;
-    a.src = static_cast<const char*>(src);
-    a.dst = static_cast<char*>(dst);
-    a.base = b.base;
-    a.cnt1 = b.cnt[1];
-    a.cnt2 = b.cnt[2];
-    a.t0 = b.tstride[0];
-    a.t1 = b.tstride[1];
-    a.t2 = b.tstride[2];
-    a.nvec_row = b.run / V;
-    rows = b.cnt[0] * b.cnt[1] * b.cnt[2];
-    a.total = rows * a.nvec_row;
-    a.dir = dir;
-    const int64_t per_block = int64_t(kThreads) * Vec<V>::U;
-    blocks = std::max<int64_t>(1, std::min<int64_t>(ceil_div(a.total, per_block), 1 << 20));
-    return a;
-}
-
 template <int V, typename E>
-hipError_t launch_add_v(const BoxCopy& b, const void* slab, void* tile, hipStream_t s)
+hipError_t launch_add_v(const BoxCopy* const* b, const void* const* slab, void* tile, int n, hipStream_t s)
 {
-    int64_t blocks, rows;
-    CopyArgs a = copy_args<V>(b, SLAB_TO_TILE, slab, tile, blocks, rows);
-    void* args[] = {&a};
-    const void* fn = rows == 1 ? reinterpret_cast<const void*>(&box_add_kernel<V, E, true>)
-                               : reinterpret_cast<const void*>(&box_add_kernel<V, E, false>);
+    CopyArgs2 aa{};
+    aa.b0 = copy_args_v<V>(*b[0], SLAB_TO_TILE, slab[0], tile);
+    aa.b1 = n > 1 ? copy_args_v<V>(*b[1], SLAB_TO_TILE, slab[1], tile) : aa.b0;
+    aa.nblk0 = copy_blocks<V>(aa.b0);
+    const int64_t blocks = aa.nblk0 + (n > 1 ? copy_blocks<V>(aa.b1) : 0);
+    bool single = true;
+    for (int i = 0; i < n; ++i) single = single && b[i]->cnt[0] * b[i]->cnt[1] * b[i]->cnt[2] == 1;
+    void* args[] = {&aa};
+    const void* fn = single ? reinterpret_cast<const void*>(&box_add_kernel<V, E, true>)
+                            : reinterpret_cast<const void*>(&box_add_kernel<V, E, false>);
     return hipLaunchKernel(fn, dim3(unsigned(blocks)), dim3(kThreads), args, 0, s);
 }
 
 }  // namespace
 
-hipError_t launch_box_add(const BoxCopy& b, int esz, const void* slab, void* tile, hipStream_t s)
+hipError_t launch_box_adds(const BoxCopy* const* b, int esz, const void* const* slab, void* tile, int n,
+                           hipStream_t s)
 {
+    // the widest vector every box, the tile and the slabs allow
     auto ok = [&](int64_t v) {
-        return (b.base % v) == 0 && (b.run % v) == 0 && (b.tstride[0] % v) == 0 && (b.tstride[1] % v) == 0 &&
-               (b.tstride[2] % v) == 0 && (reinterpret_cast<uintptr_t>(tile) % v) == 0 &&
-               (reinterpret_cast<uintptr_t>(slab) % v) == 0;
+        if ((reinterpret_cast<uintptr_t>(tile) % v) != 0) return false;
+        for (int i = 0; i < n; ++i) {
+            const BoxCopy& x = *b[i];
+            if ((x.base % v) != 0 || (x.run % v) != 0 || (x.tstride[0] % v) != 0 || (x.tstride[1] % v) != 0 ||
+                (x.tstride[2] % v) != 0 || (reinterpret_cast<uintptr_t>(slab[i]) % v) != 0)
+                return false;
+        }
+        return true;
     };
     if (esz == 2) {
-        if (ok(16)) return launch_add_v<16, bf16_t>(b, slab, tile, s);
-        if (ok(4)) return launch_add_v<4, bf16_t>(b, slab, tile, s);
-        return launch_add_v<2, bf16_t>(b, slab, tile, s);
+        if (ok(16)) return launch_add_v<16, bf16_t>(b, slab, tile, n, s);
+        if (ok(4)) return launch_add_v<4, bf16_t>(b, slab, tile, n, s);
+        return launch_add_v<2, bf16_t>(b, slab, tile, n, s);
     }
-    if (ok(16)) return launch_add_v<16, float>(b, slab, tile, s);
-    return launch_add_v<4, float>(b, slab, tile, s);
+    if (ok(16)) return launch_add_v<16, float>(b, slab, tile, n, s);
+    return launch_add_v<4, float>(b, slab, tile, n, s);
+}
+
+hipError_t launch_box_add(const BoxCopy& b, int esz, const void* slab, void* tile, hipStream_t s)
+{
+    const BoxCopy* bp = &b;
+    return launch_box_adds(&bp, esz, &slab, tile, 1, s);
 }
 
 hipError_t launch_box_copies(const BoxCopy* const* b, const CopyDir* dir, const void* const* src, void* const* dst,

@@ -47,6 +47,9 @@ hipError_t launch_box_copies(const BoxCopy* const* b, const CopyDir* dir, const 
                              int n, hipStream_t s);
 // tile[box] += slab (dense), element-wise in binary32; esz 2 (bf16) or 4 (f32).
 hipError_t launch_box_add(const BoxCopy& b, int esz, const void* slab, void* tile, hipStream_t s);
+// n (1 or 2) non-overlapping box adds in one launch (both faces of an axis).
+hipError_t launch_box_adds(const BoxCopy* const* b, int esz, const void* const* slab, void* tile, int n,
+                           hipStream_t s);
 
 // Where a forward convolution writes output (n, o0, o1, o2, co): element
 // base + n*str[0] + o0*str[1] + o1*str[2] + o2*str[3] + co. The dense map of

@@ -77,6 +77,9 @@ _SIGS = {
     "shard_halo_unpack_pair": (ctypes.c_int, [_tp, ctypes.c_int, _vp, ctypes.c_int32, _vp, _vp, _vp]),
     "shard_conv_wgrad_folded": (ctypes.c_int, [_tp, ctypes.c_int, _vp, ctypes.c_void_p, _vp, ctypes.c_int64, _i64p,
                                                _i64p, _i64p, _i64p, _vp, _vp, ctypes.c_size_t, _vp]),
+    "shard_halo_pack_margin_pair": (ctypes.c_int, [_tp, ctypes.c_int, _vp, ctypes.c_int32, _vp, _vp, _vp]),
+    "shard_halo_accumulate_pair": (ctypes.c_int, [_tp, ctypes.c_int, _vp, ctypes.c_int32, ctypes.c_int64, _vp,
+                                                  ctypes.c_int64, _vp, _vp]),
     "shard_status_string": (ctypes.c_char_p, [ctypes.c_int]),
 }
 for _name, (_res, _args) in _SIGS.items():
@@ -209,6 +212,18 @@ def shard_halo_pack_margin(desc, tile, axis, side, slab, stream=None):
 def shard_halo_accumulate(desc, tile, axis, side, width, slab, stream=None):
     _check("shard_halo_accumulate", _lib.shard_halo_accumulate(ctypes.byref(desc), _dtype_code(tile), _ptr(tile),
                                                                axis, side, width, _ptr(slab), _stream(stream)))
+
+
+def shard_halo_pack_margin_pair(desc, tile, axis, slab_lo=None, slab_hi=None, stream=None):
+    _check("shard_halo_pack_margin_pair",
+           _lib.shard_halo_pack_margin_pair(ctypes.byref(desc), _dtype_code(tile), _ptr(tile), axis, _ptr(slab_lo),
+                                            _ptr(slab_hi), _stream(stream)))
+
+
+def shard_halo_accumulate_pair(desc, tile, axis, width_lo, slab_lo, width_hi, slab_hi, stream=None):
+    _check("shard_halo_accumulate_pair",
+           _lib.shard_halo_accumulate_pair(ctypes.byref(desc), _dtype_code(tile), _ptr(tile), axis, width_lo,
+                                           _ptr(slab_lo), width_hi, _ptr(slab_hi), _stream(stream)))
 
 
 def shard_norm_workspace_bytes(desc, dtype_code, groups) -> int:

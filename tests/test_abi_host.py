@@ -238,6 +238,32 @@ def test_reverse_halo_rejections(sc):
 
 
 @pytestmark_host
+def test_reverse_halo_pair_rejections(sc):
+    lib = _raw(sc)
+    d = sc.tile_desc(1, 4, [6, 5], [1, 0], [2, 0])
+    p = ctypes.byref(d)
+    m, a = lib.shard_halo_pack_margin_pair, lib.shard_halo_accumulate_pair
+    assert m(p, 0, FAKE, 2, FAKE, FAKE, None) == sc.SHARD_ERR_INVALID    # axis >= ndim
+    assert m(p, 0, FAKE, -1, FAKE, FAKE, None) == sc.SHARD_ERR_INVALID   # axis < 0
+    assert m(p, 5, FAKE, 0, FAKE, FAKE, None) == sc.SHARD_ERR_INVALID    # dtype
+    assert m(p, 0, None, 0, FAKE, None, None) == sc.SHARD_ERR_INVALID    # null tile, margin lo of width 1
+    assert m(p, 0, None, 0, None, FAKE, None) == sc.SHARD_ERR_INVALID    # null tile, margin hi of width 2
+    assert m(p, 0, None, 0, None, None, None) == sc.SHARD_OK             # both sides skipped
+    assert m(p, 0, None, 1, FAKE, FAKE, None) == sc.SHARD_OK             # zero-width margins: no-op
+    assert m(p, 1, ctypes.c_void_p(0x10001), 0, FAKE, None, None) == sc.SHARD_ERR_INVALID  # misaligned tile
+    assert m(p, 1, FAKE, 0, None, ctypes.c_void_p(0x10001), None) == sc.SHARD_ERR_INVALID  # misaligned slab
+    assert a(p, 0, FAKE, 0, -1, FAKE, 1, FAKE, None) == sc.SHARD_ERR_INVALID   # width_lo < 0
+    assert a(p, 0, FAKE, 0, 1, FAKE, -1, FAKE, None) == sc.SHARD_ERR_INVALID   # width_hi < 0
+    assert a(p, 0, FAKE, 2, 1, FAKE, 1, FAKE, None) == sc.SHARD_ERR_INVALID    # axis
+    assert a(p, 0, FAKE, 0, 7, FAKE, 1, FAKE, None) == sc.SHARD_ERR_UNSUPPORTED  # wider than the interior
+    assert a(p, 0, FAKE, 0, 1, FAKE, 7, FAKE, None) == sc.SHARD_ERR_UNSUPPORTED
+    assert a(p, 0, None, 0, 1, FAKE, 0, None, None) == sc.SHARD_ERR_INVALID    # null tile
+    assert a(p, 0, FAKE, 0, 1, None, 0, None, None) == sc.SHARD_ERR_INVALID    # null slab lo
+    assert a(p, 0, FAKE, 0, 0, None, 2, None, None) == sc.SHARD_ERR_INVALID    # null slab hi
+    assert a(p, 0, None, 0, 0, None, 0, None, None) == sc.SHARD_OK             # both widths 0: no-op
+
+
+@pytestmark_host
 def test_dgrad_rejections(sc):
     lib = _raw(sc)
     A = lambda *v: (ctypes.c_int64 * 3)(*v)

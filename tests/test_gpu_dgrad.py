@@ -253,6 +253,63 @@ def test_pack_margin_and_accumulate_bitwise(sc, dt, aligned):
             assert np.array_equal(cases.to_ncdhw(tile.double().cpu().numpy()), t64), (axis, side)
 
 
+@pytest.mark.parametrize("dt", ["bf16", "f32"])
+@pytest.mark.parametrize("aligned", [True, False])
+def test_reverse_halo_pair_calls(sc, dt, aligned):
+    """Both margins of an axis packed by one call equal the oracle's margin cuts
+    and the single calls, bit for bit; both faces accumulated by one call equal
+    the oracle's rounded sums taken side 0 then side 1 (faces that overlap
+    included: axis 0 is accumulated with widths summing past its extent)."""
+    import torch
+    rng = np.random.default_rng(23)
+    lo, ext, hi = [2, 1, 0], [5, 4, 7], [1, 2, 0]
+    n, c = 2, 3
+    P = [a + b + d for a, b, d in zip(lo, ext, hi)]
+    tdt = torch.bfloat16 if dt == "bf16" else torch.float32
+    off = 0 if aligned else 1
+
+    def dev_buf(shape, values=None):
+        store = torch.zeros(int(np.prod(shape)) + off, dtype=tdt, device="cuda")
+        t = store[off:].view(shape)
+        if values is not None:
+            t.copy_(torch.tensor(values, dtype=torch.float64).to(tdt).cuda())
+        return t
+
+    def tie_values(shape):
+        return rng.integers(-64, 65, size=shape).astype(np.float64) * 2.0 ** rng.integers(-9, -2, size=shape)
+
+    tile = dev_buf([n] + P + [c], tie_values([n] + P + [c]))
+    desc = sc.tile_desc(n, c, ext, lo, hi)
+    rounding = (lambda v: oconv.bf16_value(oconv.round_bf16(v))) if dt == "bf16" else \
+        (lambda v: np.asarray(v).astype(np.float32).astype(np.float64))
+    t64 = cases.to_ncdhw(tile.double().cpu().numpy())
+    single = tile.clone()
+    for axis in range(3):
+        margins = [lo[axis], hi[axis]]
+        pair = [dev_buf(sc.shard_halo_slab_shape(desc, axis, m)) if m else None for m in margins]
+        sc.shard_halo_pack_margin_pair(desc, tile, axis, pair[0], pair[1])
+        for side in (0, 1):
+            if not margins[side]:
+                continue
+            one = dev_buf(sc.shard_halo_slab_shape(desc, axis, margins[side]))
+            sc.shard_halo_pack_margin(desc, tile, axis, side, one)
+            assert torch.equal(pair[side].view(torch.int16 if dt == "bf16" else torch.int32),
+                               one.view(torch.int16 if dt == "bf16" else torch.int32)), (axis, side)
+            ref = ohalo.pack_margin(t64, axis, side, lo, ext, hi)
+            assert np.array_equal(cases.to_ncdhw(pair[side].double().cpu().numpy()), ref), (axis, side)
+        widths = [3, 3] if axis == 0 else [min(m, ext[axis]) for m in margins]
+        addends = [dev_buf(sc.shard_halo_slab_shape(desc, axis, wd), tie_values(sc.shard_halo_slab_shape(desc, axis, wd)))
+                   if wd else None for wd in widths]
+        sc.shard_halo_accumulate_pair(desc, tile, axis, widths[0], addends[0], widths[1], addends[1])
+        for side in (0, 1):
+            if widths[side]:
+                sc.shard_halo_accumulate(desc, single, axis, side, widths[side], addends[side])
+                t64 = ohalo.accumulate(t64, axis, side, widths[side],
+                                       cases.to_ncdhw(addends[side].double().cpu().numpy()), lo, ext, hi, rounding)
+        assert np.array_equal(cases.to_ncdhw(tile.double().cpu().numpy()), t64), axis
+        assert np.array_equal(cases.to_ncdhw(single.double().cpu().numpy()), t64), axis
+
+
 def test_dgrad_without_owned_outputs_is_zero(sc):
     import torch
     w = cases.REDUCED["c4r"]
