@@ -239,61 +239,59 @@ __global__ __launch_bounds__(kThreads, 2) void conv_fwd_tiled(FwdArgs a)
         stage_brick<T>(a, lds, nn, i0, p * a.cc);
         __syncthreads();
         const int iters = taps * kcp;
-        // software pipeline: fetch the B fragments of the next iteration early
-        uint4 bcur[RN];
-        {
-            const int64_t fb = (int64_t(0) * a.nkc + p * kcp) * a.nt + nt0;
+        // Iteration = (tap, channel chunk). Software pipeline over two operand
+        // sets that alternate (no register copies): the A fragments (LDS) and B
+        // fragments (weights, L2) of iteration it + 1 are in flight while
+        // iteration it multiplies; every load is unconditional (the one past the
+        // last iteration re-reads the last, in bounds), so the waits before each
+        // set's MFMAs cover exactly that set's loads.
+        struct TapIt {
+            int t0, t1, t2, kc;
+        };
+        auto step_tap = [&](TapIt& s) {
+            if (++s.kc == kcp) {
+                s.kc = 0;
+                if (++s.t2 == a.K[2]) {
+                    s.t2 = 0;
+                    if (++s.t1 == a.K[1]) {
+                        s.t1 = 0;
+                        ++s.t0;
+                    }
+                }
+            }
+        };
+        auto load = [&](const TapIt& s, uint4 (&av)[RM], uint4 (&bv)[RN]) {
+            const int tap = (s.t0 * a.K[1] + s.t1) * a.K[2] + s.t2;
+            const int64_t fb = (int64_t(tap) * a.nkc + p * kcp + s.kc) * a.nt + nt0;
 #pragma unroll
-            for (int j = 0; j < RN; ++j) bcur[j] = a.wfrag[(fb + j) * 64 + lane];
-        }
-        int t0 = 0, t1 = 0, t2 = 0, kc = 0;
-        // A fragments (LDS) of the next iteration are read while this one multiplies
-        auto read_a = [&](int tt0, int tt1, int tt2, int kkc, uint4 (&av)[RM]) {
-            const int toff = tt0 * plane + tt1 * a.BI[2] + tt2;
-            const int q = 2 * kkc + g;
+            for (int j = 0; j < RN; ++j) bv[j] = a.wfrag[(fb + j) * 64 + lane];
+            const int toff = s.t0 * plane + s.t1 * a.BI[2] + s.t2;
+            const int q = 2 * s.kc + g;
 #pragma unroll
             for (int i = 0; i < RM; ++i) {
                 const int v = vbase[i] + toff;
                 av[i] = lds[v * a.nq + (q ^ swz(v, a.vpl_sh, a.qmask))];
             }
         };
-        uint4 acur[RM];
-        read_a(0, 0, 0, 0, acur);
-        for (int it = 0; it < iters; ++it) {
-            // next (tap, kc)
-            int nkc_ = kc + 1, n2 = t2, n1 = t1, n0 = t0;
-            if (nkc_ == kcp) {
-                nkc_ = 0;
-                if (++n2 == a.K[2]) {
-                    n2 = 0;
-                    if (++n1 == a.K[1]) {
-                        n1 = 0;
-                        ++n0;
-                    }
-                }
-            }
-            uint4 bnext[RN];
-            uint4 anext[RM];
-            if (it + 1 < iters) {
-                const int ntap = (n0 * a.K[1] + n1) * a.K[2] + n2;
-                const int64_t fb = (int64_t(ntap) * a.nkc + p * kcp + nkc_) * a.nt + nt0;
-#pragma unroll
-                for (int j = 0; j < RN; ++j) bnext[j] = a.wfrag[(fb + j) * 64 + lane];
-                read_a(n0, n1, n2, nkc_, anext);
-            }
+        auto mma = [&](const uint4 (&av)[RM], const uint4 (&bv)[RN]) {
 #pragma unroll
             for (int i = 0; i < RM; ++i)
 #pragma unroll
-                for (int j = 0; j < RN; ++j) mfma_step<T>(acc[i][j], acur[i], bcur[j]);
-#pragma unroll
-            for (int j = 0; j < RN; ++j) bcur[j] = bnext[j];
-#pragma unroll
-            for (int i = 0; i < RM; ++i) acur[i] = anext[i];
-            kc = nkc_;
-            t0 = n0;
-            t1 = n1;
-            t2 = n2;
+                for (int j = 0; j < RN; ++j) mfma_step<T>(acc[i][j], av[i], bv[j]);
+        };
+        TapIt nx{0, 0, 0, 0};
+        uint4 a0[RM], b0[RN], a1[RM], b1[RN];
+        load(nx, a0, b0);
+        int it = 0;
+        for (; it + 1 < iters; it += 2) {
+            step_tap(nx);
+            load(nx, a1, b1);  // iteration it + 1
+            mma(a0, b0);
+            if (it + 2 < iters) step_tap(nx);
+            load(nx, a0, b0);  // iteration it + 2 (past the end: it + 1 again)
+            mma(a1, b1);
         }
+        if (it < iters) mma(a0, b0);
     }
 
     // epilogue: lane holds column lane%32, rows 8*(r/4) + 4*g + (r%4); the
