@@ -157,15 +157,12 @@ __global__ __launch_bounds__(kThreads, 2) void wgrad_bf16_tiled(WgArgs a)
         const int64_t i1 = ob[1] * a.S[1] - a.pad[1];
         const int64_t i2 = ob[2] - a.pad[2];
         __syncthreads();
-        // X^T: [ci][z][y][x], zero outside the tile and past cin
+        // X^T: [ci][z][y][x], zero outside the tile and past cin. A thread keeps
+        // its (x, 8-channel unit) column and steps over (z, y) rows (one division
+        // per row, none per unit) when a row of units fits the block.
         {
             const int rows = a.biz * a.biy;
-            const int units = rows * a.bix * (NCI / 8);
-            for (int u = threadIdx.x; u < units; u += kThreads) {
-                const int q = u % (NCI / 8);
-                const int v = u / (NCI / 8);
-                const int x = v % a.bix;
-                const int row = v / a.bix;
+            auto stage_x = [&](int q, int x, int row) {
                 const int y = row % a.biy;
                 const int z = row / a.biy;
                 const int64_t t0 = i0 + z, t1 = i1 + y, t2 = i2 + x;
@@ -181,17 +178,29 @@ __global__ __launch_bounds__(kThreads, 2) void wgrad_bf16_tiled(WgArgs a)
                 bf16_t* dst = xs + (8 * q) * a.cs + row * a.bixp + x;
 #pragma unroll
                 for (int e = 0; e < 8; ++e) dst[e * a.cs] = val[e];
+            };
+            constexpr int NQ = NCI / 8;
+            const int rowlen = a.bix * NQ;
+            if (rowlen <= kThreads) {
+                const int rpp = kThreads / rowlen;
+                const int r0 = int(threadIdx.x) / rowlen, cu = int(threadIdx.x) - r0 * rowlen;
+                if (r0 < rpp)
+                    for (int row = r0; row < rows; row += rpp) stage_x(cu % NQ, cu / NQ, row);
+            } else {
+                const int units = rows * rowlen;
+                for (int u = threadIdx.x; u < units; u += kThreads) {
+                    const int v = u / NQ;
+                    stage_x(u % NQ, v % a.bix, v / a.bix);
+                }
             }
         }
-        // dy^T: [co][voxel of the output brick], zero past the output extent
+        // dy^T: [co][voxel of the output brick], zero past the output extent;
+        // rows stepped as for X^T
         {
-            const int units = bov * (NCO / 8);
-            for (int u = threadIdx.x; u < units; u += kThreads) {
-                const int q = u % (NCO / 8);
-                const int f = u / (NCO / 8);
-                const int ox = f % a.BO[2];
-                const int oy = (f / a.BO[2]) % a.BO[1];
-                const int oz = f / (a.BO[2] * a.BO[1]);
+            auto stage_dy = [&](int q, int ox, int orow) {
+                const int oy = orow % a.BO[1];
+                const int oz = orow / a.BO[1];
+                const int f = orow * a.BO[2] + ox;
                 const int64_t o0 = ob[0] + oz, o1 = ob[1] + oy, o2 = ob[2] + ox;
                 const int64_t c = co0 + 8 * q;
                 bf16_t val[8] = {0, 0, 0, 0, 0, 0, 0, 0};
@@ -200,17 +209,41 @@ __global__ __launch_bounds__(kThreads, 2) void wgrad_bf16_tiled(WgArgs a)
                 bf16_t* dst = ds + (8 * q) * a.csd + f;
 #pragma unroll
                 for (int e = 0; e < 8; ++e) dst[e * a.csd] = val[e];
+            };
+            constexpr int NQ = NCO / 8;
+            const int rowlen = a.BO[2] * NQ;
+            const int orows = a.BO[0] * a.BO[1];
+            if (rowlen <= kThreads) {
+                const int rpp = kThreads / rowlen;
+                const int r0 = int(threadIdx.x) / rowlen, cu = int(threadIdx.x) - r0 * rowlen;
+                if (r0 < rpp)
+                    for (int orow = r0; orow < orows; orow += rpp) stage_dy(cu % NQ, cu / NQ, orow);
+            } else {
+                const int units = orows * rowlen;
+                for (int u = threadIdx.x; u < units; u += kThreads) {
+                    const int f = u / NQ;
+                    stage_dy(u % NQ, f % a.BO[2], f / a.BO[2]);
+                }
             }
         }
         __syncthreads();
         const bf16_t* arow = ds + (wco * 16 + l16) * a.csd;
         const bf16_t* xrow = xs + (wci * 16 + l16) * a.cs;
+        // the lane's 8 voxels [f0, f0 + 8) lie in one W row (BO[2] % 8 == 0);
+        // their brick coordinates advance by carries as f0 steps by 32
+        int ox0 = (8 * g) % a.BO[2], oy = ((8 * g) / a.BO[2]) % a.BO[1], oz = (8 * g) / (a.BO[2] * a.BO[1]);
         for (int ks = 0; ks < bov / 32; ++ks) {
             const int f0 = ks * 32 + 8 * g;
-            const int ox0 = f0 % a.BO[2];
-            const int r = f0 / a.BO[2];
-            const int oy = r % a.BO[1];
-            const int oz = r / a.BO[1];
+            if (ks > 0) {
+                ox0 += 32;
+                while (ox0 >= a.BO[2]) {
+                    ox0 -= a.BO[2];
+                    if (++oy == a.BO[1]) {
+                        oy = 0;
+                        ++oz;
+                    }
+                }
+            }
             const uint4 av = *reinterpret_cast<const uint4*>(arow + f0);
 #pragma unroll
             for (int kd = 0; kd < KDG; ++kd) {
