@@ -331,12 +331,11 @@ __global__ __launch_bounds__(kThreads, 2) void wgrad_f32_tiled(WgArgs a)
         const int64_t i1 = ob[1] * a.S[1] - a.pad[1];
         const int64_t i2 = ob[2] * a.S[2] - a.pad[2];
         __syncthreads();
-        for (int u = threadIdx.x; u < biv * 8; u += kThreads) {
-            const int q = u % 8;
-            const int v = u / 8;
-            const int x = v % a.bix;
-            const int y = (v / a.bix) % a.biy;
-            const int z = v / (a.bix * a.biy);
+        // staging: a thread keeps its (x, 4-channel unit) column and steps over
+        // rows (one division per row) when a row of units fits the block
+        auto stage_x = [&](int q, int x, int row) {
+            const int y = row % a.biy;
+            const int z = row / a.biy;
             const int64_t t0 = i0 + z, t1 = i1 + y, t2 = i2 + x;
             const int64_t c = ci0 + 4 * q;
             float4 val = make_float4(0.f, 0.f, 0.f, 0.f);
@@ -355,12 +354,24 @@ __global__ __launch_bounds__(kThreads, 2) void wgrad_f32_tiled(WgArgs a)
                     val = make_float4(tmp[0], tmp[1], tmp[2], tmp[3]);
                 }
             }
-            reinterpret_cast<float4*>(xs)[v * 8 + q] = val;
+            reinterpret_cast<float4*>(xs)[(row * a.bix + x) * 8 + q] = val;
+        };
+        {
+            const int rowlen = a.bix * 8, rows = a.biz * a.biy;
+            if (rowlen <= kThreads) {
+                const int rpp = kThreads / rowlen;
+                const int r0 = int(threadIdx.x) / rowlen, cu = int(threadIdx.x) - r0 * rowlen;
+                if (r0 < rpp)
+                    for (int row = r0; row < rows; row += rpp) stage_x(cu % 8, cu / 8, row);
+            } else {
+                for (int u = threadIdx.x; u < biv * 8; u += kThreads) {
+                    const int v = u / 8;
+                    stage_x(u % 8, v % a.bix, v / a.bix);
+                }
+            }
         }
         const int bove = bov + (bov & 1);
-        for (int u = threadIdx.x; u < bove * 8; u += kThreads) {
-            const int q = u % 8;
-            const int f = u / 8;
+        auto stage_dy = [&](int q, int f) {
             const int ox = f % a.BO[2];
             const int oy = (f / a.BO[2]) % a.BO[1];
             const int oz = f / (a.BO[2] * a.BO[1]);
@@ -378,15 +389,27 @@ __global__ __launch_bounds__(kThreads, 2) void wgrad_f32_tiled(WgArgs a)
                 }
             }
             reinterpret_cast<float4*>(ds)[f * 8 + q] = val;
-        }
+        };
+        for (int u = threadIdx.x; u < bove * 8; u += kThreads) stage_dy(u % 8, u / 8);
         __syncthreads();
+        // output voxel f = 2 ks + g of the brick; its coordinates advance by
+        // carries (a lane past the brick's end uses voxel 0: its dy row is zero)
+        int ox = g % a.BO[2], oy = (g / a.BO[2]) % a.BO[1], oz = g / (a.BO[2] * a.BO[1]);
         for (int ks = 0; ks < bove / 2; ++ks) {
             const int f = 2 * ks + g;
-            const int ff = f < bov ? f : 0;
-            const int ox = ff % a.BO[2];
-            const int oy = (ff / a.BO[2]) % a.BO[1];
-            const int oz = ff / (a.BO[2] * a.BO[1]);
-            const int vin = (oz * a.S[0] * a.biy + oy * a.S[1]) * a.bix + ox * a.S[2];
+            if (ks > 0) {
+                ox += 2;
+                while (ox >= a.BO[2]) {
+                    ox -= a.BO[2];
+                    if (++oy == a.BO[1]) {
+                        oy = 0;
+                        ++oz;
+                    }
+                }
+            }
+            const bool live = f < bov;
+            const int vin =
+                live ? (oz * a.S[0] * a.biy + oy * a.S[1]) * a.bix + ox * a.S[2] : 0;
             const float av = ds[f * 32 + l32];
 #pragma unroll
             for (int i = 0; i < TPW; ++i) {
