@@ -246,10 +246,15 @@ __global__ __launch_bounds__(256, 1) void conv_fwd_xm(XmArgs a)
                                                      0, 0, 0);
         }
     };
-    // load it of a unit goes out in MFMA step step_of(it) of the tile before; the
-    // last in the last step, after that step's stores
+    // load it of a unit goes out in MFMA step step_of(it) of the tile before (the
+    // last in the last step), behind that step's first MFMA
     constexpr int S_STEPS = R * KD * C::NKC;
     static_assert(S_STEPS >= C::NIT, "at most one staging load per MFMA step");
+    auto step_of = [](int it) { return ((it + 1) * S_STEPS) / C::NIT - 1; };
+    // Where a group count leaves the tile's last step without epilogue stores
+    // (six or more groups), a step's load goes out behind its first MFMA; else
+    // after the step's epilogue piece, so that a tile's last staging load
+    // follows its stores (the vmcnt waits count the stores issued after it).
 
     // epilogue LDS addresses: lane (g, co) writes voxel 16g + e of channel co at
     // slot (16g + e) ^ g; the read-back gives lane U = it * 64 + lane the 16 bytes
@@ -377,6 +382,7 @@ __global__ __launch_bounds__(256, 1) void conv_fwd_xm(XmArgs a)
     };
     // which epilogue pieces run in group q of a row
     constexpr int NG = KD * C::NKC;  // (kd, kc) groups per output row
+    constexpr bool kEarlyLoad = NG >= 6;
     static_assert(NG >= 4, "five epilogue pieces in at least four groups");
     auto pieces_of = [&](int q, int rr, const TileOut& t) {
         if (NG >= 5) {
@@ -492,7 +498,23 @@ __global__ __launch_bounds__(256, 1) void conv_fwd_xm(XmArgs a)
                     acc[r][kw] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
                         __builtin_bit_cast(bf16x8_r, A[kh]), __builtin_bit_cast(bf16x8_r, wv[kd][kh][kw][kc]), c0,
                         0, 0, 0);
+                    // the step's staging load goes out right behind its first MFMA, so
+                    // its issue stall overlaps that MFMA
+                    if (kEarlyLoad && kh == 0 && kw == 0) {
+#pragma unroll
+                        for (int it = 0; it < C::NIT; ++it)
+                            if (step_of(it) == st) stage_load(it);
+                    }
                 }
+            if constexpr (kEarlyLoad) {
+                // keep that order through scheduling: one MFMA, the load, the rest
+                bool has_load = false;
+#pragma unroll
+                for (int it = 0; it < C::NIT; ++it) has_load = has_load || step_of(it) == st;
+                __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // MFMA
+                if (has_load) __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);  // VMEM read
+                __builtin_amdgcn_sched_group_barrier(0x008, KH * KW - 1, 0);
+            }
             if (r + 1 < R) {
 #pragma unroll
                 for (int kh = 0; kh + 1 < KH; ++kh) cache[q][kh] = A[kh + 1];
@@ -503,9 +525,11 @@ __global__ __launch_bounds__(256, 1) void conv_fwd_xm(XmArgs a)
                 pieces_of(q, R - 1, prev);
             else
                 pieces_of(q, r - 1, cur);
+            if constexpr (!kEarlyLoad) {
 #pragma unroll
-            for (int it = 0; it < C::NIT; ++it)
-                if (((it + 1) * S_STEPS) / C::NIT - 1 == st) stage_load(it);
+                for (int it = 0; it < C::NIT; ++it)
+                    if (step_of(it) == st) stage_load(it);
+            }
         }
         cbuf = cbuf + 1 == NBUF ? 0 : cbuf + 1;
         prev = cur;
