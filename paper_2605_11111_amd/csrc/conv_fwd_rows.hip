@@ -386,7 +386,9 @@ __global__ __launch_bounds__(256, 1) void conv_fwd_xm(XmArgs a)
     static_assert(NG >= 4, "five epilogue pieces in at least four groups");
     auto pieces_of = [&](int q, int rr, const TileOut& t) {
         if (NG >= 5) {
-            if (q < 5) epi_piece(rr, q, t);
+            // with six or more groups piece 4 (the stores) goes out in the MFMA
+            // sequence of group 4 (see the main loop)
+            if (q < (kEarlyLoad ? 4 : 5)) epi_piece(rr, q, t);
         } else {
             if (q == 0) epi_piece(rr, 0, t);
             if (q == 1) epi_piece(rr, 1, t);
@@ -498,21 +500,30 @@ __global__ __launch_bounds__(256, 1) void conv_fwd_xm(XmArgs a)
                     acc[r][kw] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
                         __builtin_bit_cast(bf16x8_r, A[kh]), __builtin_bit_cast(bf16x8_r, wv[kd][kh][kw][kc]), c0,
                         0, 0, 0);
-                    // the step's staging load goes out right behind its first MFMA, so
-                    // its issue stall overlaps that MFMA
+                    // the step's staging load, and in group 4 the pending row's
+                    // stores, go out right behind its first MFMA, so that their issue
+                    // stalls overlap that MFMA
                     if (kEarlyLoad && kh == 0 && kw == 0) {
 #pragma unroll
                         for (int it = 0; it < C::NIT; ++it)
                             if (step_of(it) == st) stage_load(it);
+                        if (q == 4) {
+                            if (r == 0)
+                                epi_piece(R - 1, 4, prev);
+                            else
+                                epi_piece(r - 1, 4, cur);
+                        }
                     }
                 }
             if constexpr (kEarlyLoad) {
-                // keep that order through scheduling: one MFMA, the load, the rest
+                // keep that order through scheduling: one MFMA, the load, the stores,
+                // the rest
                 bool has_load = false;
 #pragma unroll
                 for (int it = 0; it < C::NIT; ++it) has_load = has_load || step_of(it) == st;
                 __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // MFMA
                 if (has_load) __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);  // VMEM read
+                if (q == 4) __builtin_amdgcn_sched_group_barrier(0x040, 2, 0);    // VMEM write
                 __builtin_amdgcn_sched_group_barrier(0x008, KH * KW - 1, 0);
             }
             if (r + 1 < R) {
