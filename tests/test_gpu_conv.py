@@ -162,6 +162,10 @@ EDGE = [
     # few long rows: the W-march kernels split rows into segments
     ("3d_long_rows", "bf16", 1, 32, 32, (6, 5, 700), (2, 1, 1), (3, 3, 3), (1, 1, 1)),
     ("2d_long_rows", "bf16", 2, 64, 64, (9, 1100), (2, 1), (3, 3), (1, 1)),
+    # 16 or fewer output channels: 16 x 16 output tiles (cin not a multiple of
+    # the 32-channel K chunk in the second)
+    ("3d_narrow_out", "bf16", 1, 64, 16, (10, 12, 40), (2, 1, 1), (3, 3, 3), (1, 1, 1)),
+    ("2d_narrow_out_k5", "bf16", 2, 48, 12, (21, 33), (2, 1), (5, 5), (1, 1)),
 ]
 
 
