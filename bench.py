@@ -105,7 +105,7 @@ def main():
                          "folded forward, attention) and the measured MFMA ceiling")
     args = ap.parse_args()
     if args.gpus != 1:
-        print(f"bench.py measures one GPU's shard; --gpus {args.gpus} is not supported: this build has no "
+        print(f"bench.py measures one GPU's shard; --gpus {args.gpus} is not supported: shardconv has no "
               "multi-GPU path (no collectives or sharding across devices)", file=sys.stderr)
         sys.exit(2)
 
