@@ -565,10 +565,12 @@ shard_status_t shard_conv_fwd_folded(const shard_tile_t* x, shard_dtype_t dtype,
         nb = region_boxes(t, cv, region, boxes);
         for (int i = 0; i < nb; ++i) folded[i] = fold && region != SHARD_REGION_INTERIOR;
     }
+    bool laid = false;  // weight fragments in ws (the first non-empty region lays them out)
     for (int i = 0; i < nb; ++i) {
         const hipError_t e = launch_conv_fwd_region(t, cv, dtype, tile, w, y, om, boxes[i], folded[i] ? fold : nullptr,
-                                                    fam, ws, stream);
+                                                    fam, ws, stream, laid);
         if (e != hipSuccess) return SHARD_ERR_HIP;
+        laid = laid || t.n * boxes[i].ext[0] * boxes[i].ext[1] * boxes[i].ext[2] > 0;
     }
     return SHARD_OK;
 }

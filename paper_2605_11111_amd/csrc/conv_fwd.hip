@@ -506,7 +506,7 @@ bool dense_map(const Conv3& cv, const OutMap& om)
 
 template <typename T>
 hipError_t run_fwd(const Tile3& t, const Conv3& cv, const void* tile, const void* w, void* y, const OutMap& om,
-                   const Region& rg, const Fold* fold, bool rows, void* ws, hipStream_t s)
+                   const Region& rg, const Fold* fold, bool rows, void* ws, bool frags_ready, hipStream_t s)
 {
     // the plan of the whole output box, its brick grid cut to the region: every
     // output is summed in the same order whatever region computes it
@@ -527,13 +527,17 @@ hipError_t run_fwd(const Tile3& t, const Conv3& cv, const void* tile, const void
     pl.a.vec = loads_aligned(tile, fold) && (t.c * Traits<T>::esz) % 16 == 0;
     pl.a.wfrag = static_cast<const uint4*>(ws);
     pl.a.y = static_cast<char*>(y);
-    const int taps = int(cv.taps());
-    const int64_t frag_total = int64_t(taps) * pl.a.nkc * pl.a.nt * 64;
-    const unsigned fg = unsigned(std::max<int64_t>(1, std::min<int64_t>(ceil_div(frag_total, 256), 4096)));
-    hipLaunchKernelGGL(wfrag_kernel<T>, dim3(fg), dim3(256), 0, s, static_cast<const T*>(w),
-                       static_cast<uint4*>(ws), t.c, cv.cout, taps, pl.a.nkc, pl.a.nt);
-    hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return e;
+    // the weight fragments depend on (t, cv) only: a call over several regions
+    // lays them out once
+    if (!frags_ready) {
+        const int taps = int(cv.taps());
+        const int64_t frag_total = int64_t(taps) * pl.a.nkc * pl.a.nt * 64;
+        const unsigned fg = unsigned(std::max<int64_t>(1, std::min<int64_t>(ceil_div(frag_total, 256), 4096)));
+        hipLaunchKernelGGL(wfrag_kernel<T>, dim3(fg), dim3(256), 0, s, static_cast<const T*>(w),
+                           static_cast<uint4*>(ws), t.c, cv.cout, taps, pl.a.nkc, pl.a.nt);
+        const hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
+    }
     if (rows)
         return launch_conv_fwd_rows(t, cv, std::is_same<T, bf16_t>::value ? SHARD_BF16 : SHARD_F32, tile, ws,
                                     pl.a.nkc, pl.a.nt, y, rg, fold, s);
@@ -579,13 +583,13 @@ FwdFamily fwd_family(const Tile3& t, const Conv3& cv, shard_dtype_t dt, const vo
 
 hipError_t launch_conv_fwd_region(const Tile3& t, const Conv3& cv, shard_dtype_t dt, const void* tile,
                                   const void* w, void* y, const OutMap& om, const Region& rg, const Fold* fold,
-                                  FwdFamily fam, void* ws, hipStream_t s)
+                                  FwdFamily fam, void* ws, hipStream_t s, bool frags_ready)
 {
     if (t.n * rg.ext[0] * rg.ext[1] * rg.ext[2] == 0) return hipSuccess;
     if (fam == FWD_GENERIC) return generic_conv_fwd(t, cv, dt, tile, w, y, om, rg, fold, s);
     const bool rows = fam == FWD_ROWS;
-    return dt == SHARD_BF16 ? run_fwd<bf16_t>(t, cv, tile, w, y, om, rg, fold, rows, ws, s)
-                            : run_fwd<float>(t, cv, tile, w, y, om, rg, fold, rows, ws, s);
+    return dt == SHARD_BF16 ? run_fwd<bf16_t>(t, cv, tile, w, y, om, rg, fold, rows, ws, frags_ready, s)
+                            : run_fwd<float>(t, cv, tile, w, y, om, rg, fold, rows, ws, frags_ready, s);
 }
 
 hipError_t launch_conv_fwd_mapped(const Tile3& t, const Conv3& cv, shard_dtype_t dt, const void* tile,

@@ -127,10 +127,13 @@ enum FwdFamily { FWD_GENERIC = 0, FWD_TILED = 1, FWD_ROWS = 2 };
 FwdFamily fwd_family(const Tile3& t, const Conv3& cv, shard_dtype_t dt, const void* tile, const void* y,
                      const OutMap& om, const Fold* fold, const void* ws);
 // A region of the outputs on a chosen family, with the halo folded into the
-// loads when `fold` is given.
+// loads when `fold` is given. `frags_ready`: ws already holds the weight
+// fragments (an earlier region of the same call with the same weights laid
+// them out), so they are not laid out again.
 hipError_t launch_conv_fwd_region(const Tile3& t, const Conv3& cv, shard_dtype_t dt, const void* tile,
                                   const void* w, void* y, const OutMap& om, const Region& rg, const Fold* fold,
-                                  FwdFamily fam, void* ws, hipStream_t s);
+                                  FwdFamily fam, void* ws, hipStream_t s,
+                                  bool frags_ready = false);
 hipError_t launch_conv_wgrad(const Tile3& t, const Conv3& cv, shard_dtype_t dt, const void* tile, const void* dy,
                              float* dw, void* ws, hipStream_t s);
 // The same with the halo folded into the loads (the kernels that cannot fold
