@@ -566,11 +566,25 @@ shard_status_t shard_conv_fwd_folded(const shard_tile_t* x, shard_dtype_t dtype,
         for (int i = 0; i < nb; ++i) folded[i] = fold && region != SHARD_REGION_INTERIOR;
     }
     bool laid = false;  // weight fragments in ws (the first non-empty region lays them out)
+    auto nonempty = [&](const Region& r) { return t.n * r.ext[0] * r.ext[1] * r.ext[2] > 0; };
     for (int i = 0; i < nb; ++i) {
+        // two regions of the W-march kernel that differ along axis 0 only (the
+        // boundary planes of a tile sharded along axis 0) go in one launch
+        if (fam == FWD_ROWS && i + 1 < nb && folded[i] == folded[i + 1] && nonempty(boxes[i]) &&
+            nonempty(boxes[i + 1])) {
+            const hipError_t e = launch_conv_fwd_region_pair(t, cv, dtype, tile, w, y, boxes[i], boxes[i + 1],
+                                                             folded[i] ? fold : nullptr, ws, stream, laid);
+            if (e == hipSuccess) {
+                laid = true;
+                ++i;
+                continue;
+            }
+            if (e != hipErrorNotSupported) return SHARD_ERR_HIP;
+        }
         const hipError_t e = launch_conv_fwd_region(t, cv, dtype, tile, w, y, om, boxes[i], folded[i] ? fold : nullptr,
                                                     fam, ws, stream, laid);
         if (e != hipSuccess) return SHARD_ERR_HIP;
-        laid = laid || t.n * boxes[i].ext[0] * boxes[i].ext[1] * boxes[i].ext[2] > 0;
+        laid = laid || nonempty(boxes[i]);
     }
     return SHARD_OK;
 }

@@ -592,6 +592,32 @@ hipError_t launch_conv_fwd_region(const Tile3& t, const Conv3& cv, shard_dtype_t
                             : run_fwd<float>(t, cv, tile, w, y, om, rg, fold, rows, ws, frags_ready, s);
 }
 
+hipError_t launch_conv_fwd_region_pair(const Tile3& t, const Conv3& cv, shard_dtype_t dt, const void* tile,
+                                       const void* w, void* y, const Region& ra, const Region& rb, const Fold* fold,
+                                       void* ws, hipStream_t s, bool frags_ready)
+{
+    if (dt != SHARD_BF16) return hipErrorNotSupported;
+    const PlanF pl = plan_fwd_t<bf16_t>(t, cv);
+    if (!pl.ok || !conv_fwd_rows_supported(t, cv, dt, tile, ws, pl.a.nkc, pl.a.nt, y, fold))
+        return hipErrorNotSupported;
+    // the pair's own checks before anything is launched (the weight layout
+    // included), so that a refusal leaves the stream untouched
+    if (ra.org[2] != 0 || ra.ext[2] != cv.O[2] || rb.org[1] != ra.org[1] || rb.ext[1] != ra.ext[1] ||
+        rb.org[2] != ra.org[2] || rb.ext[2] != ra.ext[2] ||
+        (rb.org[0] < ra.org[0] + ra.ext[0] && ra.org[0] < rb.org[0] + rb.ext[0]) || t.c != 32)
+        return hipErrorNotSupported;
+    if (!frags_ready) {
+        const int taps = int(cv.taps());
+        const int64_t frag_total = int64_t(taps) * pl.a.nkc * pl.a.nt * 64;
+        const unsigned fg = unsigned(std::max<int64_t>(1, std::min<int64_t>(ceil_div(frag_total, 256), 4096)));
+        hipLaunchKernelGGL(wfrag_kernel<bf16_t>, dim3(fg), dim3(256), 0, s, static_cast<const bf16_t*>(w),
+                           static_cast<uint4*>(ws), t.c, cv.cout, taps, pl.a.nkc, pl.a.nt);
+        const hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
+    }
+    return launch_conv_fwd_rows(t, cv, dt, tile, ws, pl.a.nkc, pl.a.nt, y, ra, fold, s, &rb);
+}
+
 hipError_t launch_conv_fwd_mapped(const Tile3& t, const Conv3& cv, shard_dtype_t dt, const void* tile,
                                   const void* w, void* y, const OutMap& om, void* ws, hipStream_t s)
 {

@@ -62,6 +62,9 @@ struct XmArgs {
     uint32_t ybatch_bytes;  // output bytes per batch item (< 2^32)
     int32_t cout;
     int32_t org[2], oend[2];  // computed outputs along axes 0, 1: [org, oend) (O gives the strides)
+    // a second region along axis 0 in the same launch: bricks bz >= nbz_a cover
+    // axis-0 rows [org0b, oend0b) (same axes 1 and 2)
+    int32_t nbz_a, org0b, oend0b;
     // halo folded into the loads along axis fa (0 or 1): padded rows c < flo come
     // from fslab[0], rows c >= fhi from fslab[1] (null: zero), the rest from the tile
     const char* fslab[2];
@@ -184,6 +187,9 @@ __global__ __launch_bounds__(256, 1) void conv_fwd_xm(XmArgs a)
     // SIMD every stalled cycle is an idle matrix core. Offsets are 32-bit (a batch
     // item is < 4 GiB); a voxel outside the tile, or a unit past the last, gets an
     // out-of-range offset and loads as zero.
+    // first output row along axis 0 of brick row bz, and the end of its region
+    auto org0_of = [&](int bz) { return bz < a.nbz_a ? a.org[0] + bz * C::BZ : a.org0b + (bz - a.nbz_a) * C::BZ; };
+    auto end0_of = [&](int bz) { return bz < a.nbz_a ? a.oend[0] : a.oend0b; };
     __amdgpu_buffer_rsrc_t st_r = __builtin_amdgcn_make_buffer_rsrc(const_cast<char*>(a.tile), short(0),
                                                                     int(a.batch_bytes), 0x00020000);
     // folded halo: the received slabs of this batch item (a missing slab is a
@@ -197,7 +203,7 @@ __global__ __launch_bounds__(256, 1) void conv_fwd_xm(XmArgs a)
         const bool live = p.brick < a.nbricks;
         const int bz = live ? p.bz : 0, by = live ? p.by : 0;
         const uint32_t nn = live ? p.nn : 0;
-        st_i0 = a.org[0] + bz * C::BZ - a.pad[0];
+        st_i0 = org0_of(bz) - a.pad[0];
         st_i1 = a.org[1] + by * C::BY - a.pad[1];
         const int i2 = p.j * 32;
         const int64_t origin = ((int64_t(st_i0) * a.P[1] + st_i1) * a.P[2] + i2) * (CIN * 2);
@@ -272,12 +278,13 @@ __global__ __launch_bounds__(256, 1) void conv_fwd_xm(XmArgs a)
 
     // output position of a computed tile: W tile j, output rows (o0, o1b + r)
     struct TileOut {
-        int32_t j, o0, o1b;
+        int32_t j, o0, o1b, oe0;
         uint32_t nn;
         bool store;
     };
     auto tile_out = [&](const Pos& p) {
-        return TileOut{p.j, a.org[0] + p.bz * C::BZ + wz, a.org[1] + p.by * C::BY + wy * R, p.nn, p.j >= p.jstore};
+        return TileOut{p.j, org0_of(p.bz) + wz, a.org[1] + p.by * C::BY + wy * R, end0_of(p.bz), p.nn,
+                       p.j >= p.jstore};
     };
 
     f32x16_r acc[R][KW];
@@ -326,7 +333,7 @@ __global__ __launch_bounds__(256, 1) void conv_fwd_xm(XmArgs a)
                 // so they are the carry terms alone (lane half 0: s1 + t0 and v0)
                 const int o1 = t.o1b + rr;
                 const int ox = t.j * 32 + a.pad[2] + 30;
-                if (g == 0 && t.store && t.o0 < a.oend[0] && o1 < a.oend[1]) {
+                if (g == 0 && t.store && t.o0 < t.oe0 && o1 < a.oend[1]) {
                     __amdgpu_buffer_rsrc_t yr = __builtin_amdgcn_make_buffer_rsrc(
                         a.y + int64_t(t.nn) * a.ybatch_bytes, short(0), int(a.ybatch_bytes), 0x00020000);
                     const uint32_t rbase = uint32_t((int64_t(t.o0) * a.O[1] + o1) * a.O[2]);
@@ -366,7 +373,7 @@ __global__ __launch_bounds__(256, 1) void conv_fwd_xm(XmArgs a)
             __amdgpu_buffer_rsrc_t yr = __builtin_amdgcn_make_buffer_rsrc(
                 a.y + int64_t(t.nn) * a.ybatch_bytes, short(0), int(a.ybatch_bytes), 0x00020000);
             const int o1 = t.o1b + rr;
-            const bool rowok = t.store && t.o0 < a.oend[0] && o1 < a.oend[1];
+            const bool rowok = t.store && t.o0 < t.oe0 && o1 < a.oend[1];
             const uint32_t rbase = uint32_t((int64_t(t.o0) * a.O[1] + o1) * a.O[2]);
 #pragma unroll
             for (int it = 0; it < 2; ++it) {
@@ -413,7 +420,7 @@ __global__ __launch_bounds__(256, 1) void conv_fwd_xm(XmArgs a)
 
     // the row R - 1 of the previous tile is pending at the start of each tile; the
     // first tile's predecessor stores nothing
-    TileOut prev{0, 0, 0, 0, false};
+    TileOut prev{0, 0, 0, 0, 0, false};
     int cbuf = 0, sbuf = NBUF - 1;
     for (uint32_t u = 0; cp.brick < a.nbricks; ++u) {
         // Unit u's loads have landed and every wave is done with the buffer that
@@ -576,7 +583,7 @@ bool fold_fits(const Tile3& t, const Fold& f, int rpi)
 
 template <int CIN, int KD, int KH, int WZ, int WY, int WC, int R, int NBUF>
 hipError_t launch_xm(const Tile3& t, const Conv3& cv, const void* tile, const void* wfrag, void* y, const Region& rg,
-                     const Fold* fold, hipStream_t s)
+                     const Region* rg2, const Fold* fold, hipStream_t s)
 {
     using C = XmCfg<CIN, KD, KH, WZ, WY, WC, R, NBUF>;
     static_assert(C::LDS_BYTES <= 160 * 1024, "LDS budget");
@@ -612,6 +619,13 @@ hipError_t launch_xm(const Tile3& t, const Conv3& cv, const void* tile, const vo
         a.oend[k] = int32_t(rg.org[k] + rg.ext[k]);
     }
     a.NBZ = int32_t(ceil_div(rg.ext[0], C::BZ));
+    a.nbz_a = a.NBZ;
+    a.org0b = a.oend0b = 0;
+    if (rg2 && rg2->ext[0] > 0) {
+        a.org0b = int32_t(rg2->org[0]);
+        a.oend0b = int32_t(rg2->org[0] + rg2->ext[0]);
+        a.NBZ += int32_t(ceil_div(rg2->ext[0], C::BZ));
+    }
     a.NBY = int32_t(ceil_div(rg.ext[1], C::BY));
     pick_raster(a.NBZ, a.NBY, 4, a.TZ, a.TY);
     a.NXT = int32_t(ceil_div(t.P[2], 32));
@@ -671,19 +685,26 @@ bool conv_fwd_rows_supported(const Tile3& t, const Conv3& cv, shard_dtype_t dt, 
 // 0 and 1 only: the W march covers whole rows); hipErrorNotSupported otherwise.
 hipError_t launch_conv_fwd_rows(const Tile3& t, const Conv3& cv, shard_dtype_t dt, const void* tile,
                                 const void* wfrag, int nkc_frag, int nt_frag, void* y, const Region& rg,
-                                const Fold* fold, hipStream_t s)
+                                const Fold* fold, hipStream_t s, const Region* rg2)
 {
     if (!conv_fwd_rows_supported(t, cv, dt, tile, wfrag, nkc_frag, nt_frag, y, fold)) return hipErrorNotSupported;
     if (rg.org[2] != 0 || rg.ext[2] != cv.O[2]) return hipErrorNotSupported;
+    if (rg2) {
+        // a second region must differ from the first along axis 0 only, and not overlap it
+        if (rg2->org[1] != rg.org[1] || rg2->ext[1] != rg.ext[1] || rg2->org[2] != rg.org[2] ||
+            rg2->ext[2] != rg.ext[2] || (rg2->org[0] < rg.org[0] + rg.ext[0] && rg.org[0] < rg2->org[0] + rg2->ext[0]))
+            return hipErrorNotSupported;
+    }
+    const int64_t ext0 = std::max<int64_t>(rg.ext[0], rg2 ? rg2->ext[0] : 0);
     if (t.c == 32) {
         // thin regions along axis 0 (the boundary planes of a D-sharded tile) take
         // bricks two rows deep; per-output arithmetic is the same in both
-        if (rg.ext[0] <= 2) return launch_xm<32, 3, 3, 2, 2, 1, 2, 3>(t, cv, tile, wfrag, y, rg, fold, s);
-        return launch_xm<32, 3, 3, 4, 1, 1, 2, 3>(t, cv, tile, wfrag, y, rg, fold, s);
+        if (ext0 <= 2) return launch_xm<32, 3, 3, 2, 2, 1, 2, 3>(t, cv, tile, wfrag, y, rg, rg2, fold, s);
+        return launch_xm<32, 3, 3, 4, 1, 1, 2, 3>(t, cv, tile, wfrag, y, rg, rg2, fold, s);
     }
     // thin regions along axis 1 (the boundary rows of an H-sharded 2D tile)
-    if (rg.ext[1] <= 2) return launch_xm<64, 1, 3, 1, 2, 2, 2, 3>(t, cv, tile, wfrag, y, rg, fold, s);
-    return launch_xm<64, 1, 3, 1, 2, 2, 4, 3>(t, cv, tile, wfrag, y, rg, fold, s);
+    if (rg.ext[1] <= 2) return launch_xm<64, 1, 3, 1, 2, 2, 2, 3>(t, cv, tile, wfrag, y, rg, rg2, fold, s);
+    return launch_xm<64, 1, 3, 1, 2, 2, 4, 3>(t, cv, tile, wfrag, y, rg, rg2, fold, s);
 }
 
 }  // namespace shardconv

@@ -134,6 +134,12 @@ hipError_t launch_conv_fwd_region(const Tile3& t, const Conv3& cv, shard_dtype_t
                                   const void* w, void* y, const OutMap& om, const Region& rg, const Fold* fold,
                                   FwdFamily fam, void* ws, hipStream_t s,
                                   bool frags_ready = false);
+// Two regions that differ along axis 0 only, in one launch of the W-march
+// kernel (FWD_ROWS); hipErrorNotSupported when that kernel cannot take them
+// together (nothing launched).
+hipError_t launch_conv_fwd_region_pair(const Tile3& t, const Conv3& cv, shard_dtype_t dt, const void* tile,
+                                       const void* w, void* y, const Region& ra, const Region& rb, const Fold* fold,
+                                       void* ws, hipStream_t s, bool frags_ready);
 hipError_t launch_conv_wgrad(const Tile3& t, const Conv3& cv, shard_dtype_t dt, const void* tile, const void* dy,
                              float* dw, void* ws, hipStream_t s);
 // The same with the halo folded into the loads (the kernels that cannot fold
@@ -156,9 +162,11 @@ hipError_t launch_norm_apply(const Tile3& t, shard_dtype_t dt, const void* tile,
 // outside what it handles (the caller then takes the general kernel).
 bool conv_fwd_rows_supported(const Tile3& t, const Conv3& cv, shard_dtype_t dt, const void* tile,
                              const void* wfrag, int nkc_frag, int nt_frag, const void* y, const Fold* fold);
+// rg2 (optional): a second region in the same launch, differing from rg along
+// axis 0 only and not overlapping it; hipErrorNotSupported otherwise.
 hipError_t launch_conv_fwd_rows(const Tile3& t, const Conv3& cv, shard_dtype_t dt, const void* tile,
                                 const void* wfrag, int nkc_frag, int nt_frag, void* y, const Region& rg,
-                                const Fold* fold, hipStream_t s);
+                                const Fold* fold, hipStream_t s, const Region* rg2 = nullptr);
 size_t wgrad_xm_workspace(const Tile3& t, const Conv3& cv, shard_dtype_t dt);
 hipError_t launch_wgrad_xm(const Tile3& t, const Conv3& cv, shard_dtype_t dt, const void* tile, const void* dy,
                            float* dw, void* ws, const Fold* fold, hipStream_t s);
