@@ -251,6 +251,9 @@ EDGE = [
     ("3d_long_rows", "bf16", 1, 32, 32, (6, 5, 700), (2, 1, 1), (3, 3, 3), (1, 1, 1)),
     ("3d_three_axes", "bf16", 1, 16, 16, (12, 10, 40), (2, 2, 2), (3, 3, 3), (1, 1, 1)),
     ("2d_long_rows_h_split", "bf16", 2, 64, 64, (9, 1100), (2, 1), (3, 3), (1, 1)),
+    # two batch items, three shards along D: both boundary planes of the middle
+    # shard go in one W-march launch
+    ("3d_batch2_split_d", "bf16", 2, 32, 32, (12, 10, 40), (3, 1, 1), (3, 3, 3), (1, 1, 1)),
 ]
 
 
