@@ -219,6 +219,11 @@ def main():
     stop.record(stream)
     torch.cuda.synchronize()
     ms_step = start.elapsed_time(stop) / args.steps
+    # the weight gradient's status word (0 unless a bounded wait inside the
+    # kernel gave up, which would also have made dw NaN)
+    if int(wsw[:4].view(torch.int32).item()) != 0 or not bool(torch.isfinite(dw).all()):
+        log("weight gradient reported a failed hand-off wait")
+        sys.exit(3)
     per_op = {}
     for i, (label, kind, work, _) in enumerate(ops):
         per_op[label] = (kind, work, float(np.mean([ev[k][i][0].elapsed_time(ev[k][i][1])

@@ -54,7 +54,9 @@
  *    returns immediately. Buffers must not overlap.
  *  - Every argument is checked on the host before any launch; on an error
  *    nothing is written. No exception crosses this interface, and the library
- *    keeps no mutable global state (calls from several host threads are safe).
+ *    keeps no mutable global state: the only state is the calling host thread's
+ *    own options (shard_set_call_opts), so calls from several host threads are
+ *    safe.
  *  - Device pointers must be aligned to their element size (2 or 4 bytes);
  *    16-byte aligned buffers take the vectorised paths.
  */
@@ -110,9 +112,10 @@ typedef struct {
  *   pad_lo            the value to pass to shard_conv_fwd/wgrad: P on unsharded
  *                     axes; on sharded axes <= 0, negative when the first owned
  *                     output's window starts inside the interior (stride > P+1).
- * Errors: SHARD_ERR_INVALID for null pointers, ndim outside 1..3, even or
+ * Errors: SHARD_ERR_INVALID for null pointers, ndim outside 1..3,
  * non-positive kernel, stride < 1, global_ext < 1, or an interior box outside
- * the domain (or not the whole axis when unsharded).
+ * the domain (or not the whole axis when unsharded); SHARD_ERR_UNSUPPORTED for
+ * an even kernel (no symmetric "same" padding) when the rest is well formed.
  */
 shard_status_t shard_conv_geometry(int32_t ndim, const int64_t global_ext[], const int64_t shard_off[],
                                    const int64_t shard_ext[], const int64_t kernel[], const int64_t stride[],
@@ -178,9 +181,11 @@ shard_status_t shard_halo_unpack_pair(const shard_tile_t* x, shard_dtype_t dtype
  *   y     [n][out_ext0][out_ext1][out_ext2][c_out], dtype (overwritten)
  *   ws    device workspace of at least shard_conv_workspace_bytes(0, ...) bytes
  *         (may be NULL when that is 0); contents are scratch.
- * kernel[a] in 1..64, stride[a] in 1..64, out_ext[a] >= 0, |pad_lo[a]| < 2^30.
- * Empty output (n or any out_ext 0) is a no-op.
- * Errors: SHARD_ERR_INVALID for malformed arguments or a short workspace;
+ * kernel[a] odd in 1..63, stride[a] in 1..64, out_ext[a] >= 0,
+ * |pad_lo[a]| < 2^30. Empty output (n or any out_ext 0) is a no-op.
+ * Errors: SHARD_ERR_INVALID for malformed arguments (kernel or stride outside
+ * 1..64, ...) or a short workspace; SHARD_ERR_UNSUPPORTED for an even kernel
+ * (the method's convolutions pad symmetrically, which needs an odd kernel);
  * SHARD_ERR_HIP if a launch fails.
  */
 shard_status_t shard_conv_fwd(const shard_tile_t* x, shard_dtype_t dtype, const void* tile, const void* w,
@@ -251,6 +256,12 @@ shard_status_t shard_conv_fwd_folded(const shard_tile_t* x, shard_dtype_t dtype,
  *   dy    [n][out_ext0][out_ext1][out_ext2][c_out], dtype
  *   dw    [c_out][x->c][kernel0][kernel1][kernel2], binary32 (overwritten)
  *   ws    device workspace of at least shard_conv_workspace_bytes(1, ...) bytes.
+ *         Its first 32-bit word is the call's device-side status once the call
+ *         has completed on the stream: 0 normally; nonzero when a bounded wait
+ *         between the waves of a workgroup gave up (possible only if the GPU
+ *         stalled a workgroup's waves far beyond any normal schedule), in which
+ *         case every dw element is NaN. The caller may read it after
+ *         synchronising; the rest of ws is scratch.
  * The summation order is fixed: repeated calls give bit-identical dw.
  * An empty output box writes dw = 0.
  * Errors: as shard_conv_fwd.
@@ -355,7 +366,7 @@ shard_status_t shard_halo_accumulate_pair(const shard_tile_t* x, shard_dtype_t d
  * Workspace bytes shard_conv_fwd (op 0), shard_conv_wgrad (op 1) or
  * shard_conv_dgrad (op 2) needs for these arguments. A pure function of its
  * arguments (the launch plan does not depend on the device); host only.
- * Returns (size_t)-1 for malformed arguments.
+ * Returns (size_t)-1 for malformed arguments or an even kernel.
  */
 size_t shard_conv_workspace_bytes(int32_t op, const shard_tile_t* x, shard_dtype_t dtype, int64_t c_out,
                                   const int64_t kernel[], const int64_t stride[], const int64_t out_ext[]);
@@ -401,7 +412,6 @@ shard_status_t shard_norm_apply(const shard_tile_t* x, shard_dtype_t dtype, cons
                                 double count, double eps, int64_t groups, const float* gamma, const float* beta,
                                 void* out, void* ws, size_t ws_bytes, hipStream_t stream);
 
-/* Static, human-readable text for a status code. Never NULL. */
 /*
  * One block step of ring attention (section "Performance Benchmarks",
  * subsection "Ring Attention": each device attends its local queries to the
@@ -430,7 +440,32 @@ shard_status_t shard_attn_block(int64_t batch, int64_t heads, int64_t sq, int64_
                                 shard_dtype_t dtype, float scale, const void* q, const void* k, const void* v,
                                 float* o, float* lse, int32_t first, hipStream_t stream);
 
+/* Static, human-readable text for a status code. Never NULL. */
 const char* shard_status_string(shard_status_t status);
+
+/*
+ * Options of the calling host thread, applied to its later calls (other
+ * threads keep their own; a new thread starts from the defaults):
+ *   kernels     which kernel family the convolutions (fwd, wgrad, dgrad and
+ *               the folded calls) take: SHARD_KERNELS_FASTEST (default) the
+ *               fastest applicable one, SHARD_KERNELS_TILED the general tiled
+ *               MFMA kernels (no shape-specialised kernel), SHARD_KERNELS_DIRECT
+ *               the plain direct kernels. All compute the same function; the
+ *               families exist to cross-check one another (the MFMA families
+ *               agree bit for bit on integer-valued data).
+ *   wait_polls  the poll bound of the weight gradient's hand-off waits between
+ *               the waves of a workgroup; 0 keeps the default (2^20 polls).
+ *               A small bound makes the waits give up, which the status word
+ *               of shard_conv_wgrad reports: the way to check that report.
+ * opts == NULL restores the defaults.
+ * Errors: SHARD_ERR_INVALID for an unknown kernel family.
+ */
+typedef enum { SHARD_KERNELS_FASTEST = 0, SHARD_KERNELS_TILED = 1, SHARD_KERNELS_DIRECT = 2 } shard_kernels_t;
+typedef struct {
+    int32_t kernels;
+    uint32_t wait_polls;
+} shard_call_opts_t;
+shard_status_t shard_set_call_opts(const shard_call_opts_t* opts);
 
 #ifdef __cplusplus
 }

@@ -2,25 +2,20 @@
 // an error writes nothing), normalisation to three spatial axes, dispatch.
 #include <algorithm>
 #include <cmath>
-#include <cstdlib>
-#include <cstring>
 
 #include "attention.h"
 #include "internal.h"
 
 namespace shardconv {
 
-bool force_generic()
-{
-    const char* v = std::getenv("SHARDCONV_ALGO");
-    return v && std::strcmp(v, "generic") == 0;
-}
+namespace {
+// per host thread: calls from other threads never see another thread's options
+thread_local CallOpts tl_opts{SHARD_KERNELS_FASTEST, 0u};
+}  // namespace
 
-bool force_tiled()
-{
-    const char* v = std::getenv("SHARDCONV_ALGO");
-    return v && std::strcmp(v, "tiled") == 0;
-}
+const CallOpts& call_opts() { return tl_opts; }
+bool force_generic() { return tl_opts.kernels == SHARD_KERNELS_DIRECT; }
+bool force_tiled() { return tl_opts.kernels == SHARD_KERNELS_TILED; }
 
 size_t generic_wgrad_workspace(const Tile3& t, const Conv3& cv);
 hipError_t generic_conv_wgrad(const Tile3& t, const Conv3& cv, shard_dtype_t dt, const void* tile, const void* dy,
@@ -112,6 +107,15 @@ bool norm_conv(const shard_tile_t* x, const Tile3& t, int64_t c_out, const int64
     return safe_mul(total, cv.cout);
 }
 
+// The convolutions this library implements pad symmetrically ("same"
+// padding, P = (K - 1) / 2 per side), which needs an odd kernel on every axis.
+bool odd_kernel(const shard_tile_t* x, const int64_t kernel[])
+{
+    for (int a = 0; a < x->ndim; ++a)
+        if (kernel[a] % 2 == 0) return false;
+    return true;
+}
+
 // The box a slab covers on internal axis k: rows [r0, r1) on k, the padded
 // extent on earlier axes, the interior on later ones.
 void slab_spans(const Tile3& t, int k, int64_t r0, int64_t r1, int64_t start[3], int64_t cnt[3])
@@ -164,6 +168,15 @@ BoxCopy make_box(const Tile3& t, int k, int64_t r0, int64_t r1)
 }
 
 shard_status_t map_hip(hipError_t e) { return e == hipSuccess ? SHARD_OK : SHARD_ERR_HIP; }
+
+// A weight gradient over no outputs: dw = 0 (the direct kernel's empty sum) and
+// a cleared status word.
+hipError_t empty_wgrad(const Tile3& t, const Conv3& cv, shard_dtype_t dt, float* dw, void* ws, hipStream_t s)
+{
+    hipError_t e = launch_wgrad_status_clear(static_cast<uint32_t*>(ws), s);
+    if (e != hipSuccess) return e;
+    return generic_conv_wgrad(t, cv, dt, nullptr, nullptr, dw, static_cast<char*>(ws) + kWgradStatusBytes, nullptr, s);
+}
 
 // The Fold of a call: every axis with a margin reads it from the received slab
 // (null: zero). False for a slab not aligned to the element size.
@@ -246,6 +259,19 @@ int region_boxes(const Tile3& t, const Conv3& cv, int32_t region, Region out[6])
 }  // namespace
 
 extern "C" {
+
+shard_status_t shard_set_call_opts(const shard_call_opts_t* opts)
+{
+    if (!opts) {
+        tl_opts = CallOpts{SHARD_KERNELS_FASTEST, 0u};
+        return SHARD_OK;
+    }
+    if (opts->kernels != SHARD_KERNELS_FASTEST && opts->kernels != SHARD_KERNELS_TILED &&
+        opts->kernels != SHARD_KERNELS_DIRECT)
+        return SHARD_ERR_INVALID;
+    tl_opts = CallOpts{opts->kernels, opts->wait_polls};
+    return SHARD_OK;
+}
 
 const char* shard_status_string(shard_status_t s)
 {
@@ -482,7 +508,8 @@ size_t shard_conv_workspace_bytes(int32_t op, const shard_tile_t* x, shard_dtype
 {
     Tile3 t;
     Conv3 cv;
-    if (op < 0 || op > 2 || !norm_tile(x, dtype, t) || !norm_conv(x, t, c_out, kernel, stride, nullptr, out_ext, cv))
+    if (op < 0 || op > 2 || !norm_tile(x, dtype, t) || !norm_conv(x, t, c_out, kernel, stride, nullptr, out_ext, cv) ||
+        !odd_kernel(x, kernel))
         return size_t(-1);
     if (op == 0) return conv_fwd_workspace(t, cv, dtype);
     if (op == 1) return conv_wgrad_workspace(t, cv, dtype);
@@ -497,6 +524,7 @@ shard_status_t shard_conv_fwd(const shard_tile_t* x, shard_dtype_t dtype, const 
     Conv3 cv;
     if (!norm_tile(x, dtype, t) || !pad_lo || !norm_conv(x, t, c_out, kernel, stride, pad_lo, out_ext, cv))
         return SHARD_ERR_INVALID;
+    if (!odd_kernel(x, kernel)) return SHARD_ERR_UNSUPPORTED;
     if (t.n * cv.out_voxels() == 0) return SHARD_OK;
     const size_t need = conv_fwd_workspace(t, cv, dtype);
     if (ws_bytes < need || (need > 0 && !ws)) return SHARD_ERR_INVALID;
@@ -535,6 +563,7 @@ shard_status_t shard_conv_fwd_folded(const shard_tile_t* x, shard_dtype_t dtype,
     Conv3 cv;
     if (!norm_tile(x, dtype, t) || !pad_lo || !norm_conv(x, t, c_out, kernel, stride, pad_lo, out_ext, cv))
         return SHARD_ERR_INVALID;
+    if (!odd_kernel(x, kernel)) return SHARD_ERR_UNSUPPORTED;
     if (region != SHARD_REGION_ALL && region != SHARD_REGION_INTERIOR && region != SHARD_REGION_BOUNDARY)
         return SHARD_ERR_INVALID;
     if (t.n * cv.out_voxels() == 0) return SHARD_OK;
@@ -616,13 +645,14 @@ shard_status_t shard_conv_wgrad(const shard_tile_t* x, shard_dtype_t dtype, cons
     Conv3 cv;
     if (!norm_tile(x, dtype, t) || !pad_lo || !norm_conv(x, t, c_out, kernel, stride, pad_lo, out_ext, cv))
         return SHARD_ERR_INVALID;
+    if (!odd_kernel(x, kernel)) return SHARD_ERR_UNSUPPORTED;
     const size_t need = conv_wgrad_workspace(t, cv, dtype);
     if (ws_bytes < need || (need > 0 && !ws)) return SHARD_ERR_INVALID;
     if (!dw || !aligned(dw, 4) || !aligned(ws, 16)) return SHARD_ERR_INVALID;
     const bool empty = t.n * cv.out_voxels() == 0;
     if (!empty && ((tile_elems(t) > 0 && !tile) || !dy)) return SHARD_ERR_INVALID;
     if (!aligned(tile, t.esz) || !aligned(dy, t.esz)) return SHARD_ERR_INVALID;
-    if (empty) return map_hip(generic_conv_wgrad(t, cv, dtype, tile, dy, dw, ws, nullptr, stream));
+    if (empty) return map_hip(empty_wgrad(t, cv, dtype, dw, ws, stream));
     return map_hip(launch_conv_wgrad(t, cv, dtype, tile, dy, dw, ws, stream));
 }
 
@@ -636,6 +666,7 @@ shard_status_t shard_conv_wgrad_folded(const shard_tile_t* x, shard_dtype_t dtyp
     Conv3 cv;
     if (!norm_tile(x, dtype, t) || !pad_lo || !norm_conv(x, t, c_out, kernel, stride, pad_lo, out_ext, cv))
         return SHARD_ERR_INVALID;
+    if (!odd_kernel(x, kernel)) return SHARD_ERR_UNSUPPORTED;
     const size_t need = conv_wgrad_workspace(t, cv, dtype);
     if (ws_bytes < need || (need > 0 && !ws)) return SHARD_ERR_INVALID;
     if (!dw || !aligned(dw, 4) || !aligned(ws, 16)) return SHARD_ERR_INVALID;
@@ -644,7 +675,7 @@ shard_status_t shard_conv_wgrad_folded(const shard_tile_t* x, shard_dtype_t dtyp
     if (!aligned(tile, t.esz) || !aligned(dy, t.esz)) return SHARD_ERR_INVALID;
     Fold f;
     if (!make_fold(x, t, halo, f)) return SHARD_ERR_INVALID;
-    if (empty) return map_hip(generic_conv_wgrad(t, cv, dtype, tile, dy, dw, ws, nullptr, stream));
+    if (empty) return map_hip(empty_wgrad(t, cv, dtype, dw, ws, stream));
     if (!f.mask) return map_hip(launch_conv_wgrad(t, cv, dtype, tile, dy, dw, ws, stream));
     return map_hip(launch_conv_wgrad_folded(t, cv, dtype, tile, dy, dw, ws, f, stream));
 }
@@ -657,6 +688,7 @@ shard_status_t shard_conv_dgrad(const shard_tile_t* x, shard_dtype_t dtype, cons
     Conv3 cv;
     if (!norm_tile(x, dtype, t) || !pad_lo || !norm_conv(x, t, c_out, kernel, stride, pad_lo, out_ext, cv))
         return SHARD_ERR_INVALID;
+    if (!odd_kernel(x, kernel)) return SHARD_ERR_UNSUPPORTED;
     if (tile_elems(t) == 0) return SHARD_OK;
     const size_t need = conv_dgrad_workspace(t, cv, dtype);
     if (ws_bytes < need || (need > 0 && !ws)) return SHARD_ERR_INVALID;

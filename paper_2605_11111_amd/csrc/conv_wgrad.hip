@@ -669,17 +669,37 @@ hipError_t launch_bf16(const PlanW& pl, hipStream_t s)
 
 size_t conv_wgrad_workspace(const Tile3& t, const Conv3& cv, shard_dtype_t dt)
 {
-    return std::max({generic_wgrad_workspace(t, cv), tiled_workspace(plan_wgrad(t, cv, dt)),
-                     wgrad_tr_workspace(t, cv, dt), wgrad_xm_workspace(t, cv, dt)});
+    return kWgradStatusBytes + std::max({generic_wgrad_workspace(t, cv), tiled_workspace(plan_wgrad(t, cv, dt)),
+                                         wgrad_tr_workspace(t, cv, dt), wgrad_xm_workspace(t, cv, dt)});
 }
 
 namespace {
 
-hipError_t run_wgrad(const Tile3& t, const Conv3& cv, shard_dtype_t dt, const void* tile, const void* dy, float* dw,
-                     void* ws, const Fold* fold, hipStream_t s)
+__global__ void wgrad_status_clear(uint32_t* status)
 {
+    if (threadIdx.x == 0) status[0] = 0u;
+}
+
+}  // namespace
+
+hipError_t launch_wgrad_status_clear(uint32_t* status, hipStream_t s)
+{
+    hipLaunchKernelGGL(wgrad_status_clear, dim3(1), dim3(64), 0, s, status);
+    return hipGetLastError();
+}
+
+namespace {
+
+// ws: the call's workspace (status block first, see kWgradStatusBytes)
+hipError_t run_wgrad(const Tile3& t, const Conv3& cv, shard_dtype_t dt, const void* tile, const void* dy, float* dw,
+                     void* ws_all, const Fold* fold, hipStream_t s)
+{
+    uint32_t* status = static_cast<uint32_t*>(ws_all);
+    void* ws = static_cast<char*>(ws_all) + kWgradStatusBytes;
     {
-        hipError_t e = launch_wgrad_xm(t, cv, dt, tile, dy, dw, ws, fold, s);
+        hipError_t e = launch_wgrad_status_clear(status, s);
+        if (e != hipSuccess) return e;
+        e = launch_wgrad_xm(t, cv, dt, tile, dy, dw, ws, fold, status, s);
         if (e != hipErrorNotSupported) return e;
     }
     if (!fold) {

@@ -64,6 +64,8 @@ struct WxArgs {
     uint32_t fbatch[2];  // slab bytes per batch item
     uint32_t fSZ[2];     // slab stride along axis 0, bytes
     int32_t fa, flo, fhi;
+    uint32_t* status;     // the call's status word (nonzero: a hand-off wait gave up)
+    uint32_t wait_polls;  // poll bound of a hand-off wait
 };
 
 // 16-byte unit swizzle of staged voxel v for UPV units per voxel: with 128-byte
@@ -137,9 +139,11 @@ __global__ __launch_bounds__(256 * KS, 1) void wgrad_xm(WxArgs a)
     // starts it when full[b] >= 2 (u / NB + 1), and a loader refills b for unit u
     // when free[b] >= 6 (u / NB). Neither wait depends on a later signal of the
     // waiting wave's own kind, so the pipeline cannot deadlock. Every wait is also
-    // bounded: a wait that gives up (2^20 polls, far beyond any real wait) raises
-    // an abort word that ends every later wait at once, so a broken hand-off
-    // shows as wrong results and never as a hung kernel.
+    // bounded: a wait that gives up (a.wait_polls polls, by default 2^20, far
+    // beyond any real wait) raises an abort word that ends every later wait at
+    // once, so a broken hand-off never hangs the kernel; it also sets the call's
+    // status word in global memory, and the reduction then writes NaN into every
+    // dw element, so the broken result cannot pass for a correct one.
     constexpr int NCW = 3 * KS;  // compute waves (KS = 2)
     const uint32_t flag_full0 = lds0 + uint32_t(NB * C::STAGE_BYTES);
     const uint32_t flag_free0 = flag_full0 + uint32_t(4 * NB);
@@ -152,11 +156,13 @@ __global__ __launch_bounds__(256 * KS, 1) void wgrad_xm(WxArgs a)
         if (lane == 0) lds_add_u32(addr, 1u);
     };
     auto spin_until = [&](uint32_t addr, uint32_t target) {
-        for (uint32_t it = 0; it < (1u << 20); ++it) {
+        for (uint32_t it = 0; it < a.wait_polls; ++it) {
             if (lds_read_u32_now(addr) >= target || lds_read_u32_now(flag_abort) != 0u) return;
             __builtin_amdgcn_s_sleep(1);
         }
         raise(flag_abort);
+        // a vector atomic from one lane (the status word is read after the kernel)
+        if (lane == 0) __hip_atomic_fetch_or(a.status, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     };
 
     // ---- staging (loader waves) ----
@@ -635,9 +641,10 @@ __global__ __launch_bounds__(256) void wgrad_xm_reduce1(const float* part, float
     sums[int64_t(ch) * NE + e] = (s4[0] + s4[1]) + (s4[2] + s4[3]);
 }
 
-// dw[co][ci][tap] = sum over the chunk sums, in chunk order.
+// dw[co][ci][tap] = sum over the chunk sums, in chunk order; NaN everywhere when
+// the partial kernel reported a hand-off wait that gave up.
 template <int KD, int NCI, int NCO>
-__global__ __launch_bounds__(256) void wgrad_xm_reduce2(const float* sums, float* dw)
+__global__ __launch_bounds__(256) void wgrad_xm_reduce2(const float* sums, float* dw, const uint32_t* status)
 {
     constexpr int NR = NCO * NCI * KD;
     constexpr int CIN = 32 * NCI;
@@ -653,7 +660,7 @@ __global__ __launch_bounds__(256) void wgrad_xm_reduce2(const float* sums, float
     float acc = 0.f;
 #pragma unroll
     for (int ch = 0; ch < kChunks; ++ch) acc += sums[int64_t(ch) * NE + e];
-    dw[(co * CIN + ci) * TAPS + tap] = acc;
+    dw[(co * CIN + ci) * TAPS + tap] = status[0] == 0u ? acc : __builtin_nanf("");
 }
 
 struct WxPlan {
@@ -726,7 +733,7 @@ WxPlan plan_wx(const Tile3& t, const Conv3& cv, shard_dtype_t dt)
 }
 
 template <int KD, int NCI, int NCO, int BZ, int BY, int KS, int NB>
-hipError_t run_wx(const WxPlan& p, float* dw, bool fold, hipStream_t s)
+hipError_t run_wx(const WxPlan& p, float* dw, bool fold, uint32_t* status, hipStream_t s)
 {
     using C = WxCfg<KD, NCI, NCO, BZ, BY>;
     constexpr int LDS = NB * C::STAGE_BYTES + (KS == 2 ? 8 * NB + 16 : 0);
@@ -744,7 +751,7 @@ hipError_t run_wx(const WxPlan& p, float* dw, bool fold, hipStream_t s)
     hipLaunchKernelGGL((wgrad_xm_reduce1<KD, NCI, NCO>), dim3(unsigned(ceil_div(total, 256)), kChunks), dim3(256), 0,
                        s, p.a.part, sums, int(p.grid * KS));
     hipLaunchKernelGGL((wgrad_xm_reduce2<KD, NCI, NCO>), dim3(unsigned(ceil_div(total, 256))), dim3(256), 0, s, sums,
-                       dw);
+                       dw, static_cast<const uint32_t*>(status));
     return hipGetLastError();
 }
 
@@ -764,7 +771,7 @@ size_t wgrad_xm_workspace(const Tile3& t, const Conv3& cv, shard_dtype_t dt)
 // With a folded halo the margins must lie on one axis, 0 or 1, the slabs be
 // 16-byte aligned and below 4 GiB per batch item.
 hipError_t launch_wgrad_xm(const Tile3& t, const Conv3& cv, shard_dtype_t dt, const void* tile, const void* dy,
-                           float* dw, void* ws, const Fold* fold, hipStream_t s)
+                           float* dw, void* ws, const Fold* fold, uint32_t* status, hipStream_t s)
 {
     WxPlan p = plan_wx(t, cv, dt);
     if (!p.ok || reinterpret_cast<uintptr_t>(tile) % 16 != 0 || reinterpret_cast<uintptr_t>(dy) % 16 != 0 ||
@@ -793,8 +800,10 @@ hipError_t launch_wgrad_xm(const Tile3& t, const Conv3& cv, shard_dtype_t dt, co
     p.a.tile = static_cast<const char*>(tile);
     p.a.dy = static_cast<const char*>(dy);
     p.a.part = static_cast<float*>(ws);
-    return p.cfg == 0 ? run_wx<3, 1, 1, kC3BZ, kC3BY, 2, kC3NB>(p, dw, fold != nullptr, s)
-                      : run_wx<1, 2, 2, 1, 8, 1, 2>(p, dw, fold != nullptr, s);
+    p.a.status = status;
+    p.a.wait_polls = call_opts().wait_polls ? call_opts().wait_polls : kDefaultWaitPolls;
+    return p.cfg == 0 ? run_wx<3, 1, 1, kC3BZ, kC3BY, 2, kC3NB>(p, dw, fold != nullptr, status, s)
+                      : run_wx<1, 2, 2, 1, 8, 1, 2>(p, dw, fold != nullptr, status, s);
 }
 
 }  // namespace shardconv

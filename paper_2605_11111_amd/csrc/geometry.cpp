@@ -34,13 +34,16 @@ extern "C" shard_status_t shard_conv_geometry(int32_t ndim, const int64_t global
     const int64_t kLimit = int64_t(1) << 40;
     for (int a = 0; a < ndim; ++a) {
         const int64_t G = global_ext[a], K = kernel[a], S = stride[a], o = shard_off[a], L = shard_ext[a];
-        if (G < 1 || G > kLimit || K < 1 || K % 2 == 0 || K > kLimit || S < 1 || S > kLimit) return SHARD_ERR_INVALID;
+        if (G < 1 || G > kLimit || K < 1 || K > kLimit || S < 1 || S > kLimit) return SHARD_ERR_INVALID;
         if (sharded_mask[a]) {
             if (o < 0 || L < 0 || o + L > G) return SHARD_ERR_INVALID;
         } else if (o != 0 || L != G) {
             return SHARD_ERR_INVALID;
         }
     }
+    // "same" padding P = (K - 1) / 2 per side needs an odd kernel
+    for (int a = 0; a < ndim; ++a)
+        if (kernel[a] % 2 == 0) return SHARD_ERR_UNSUPPORTED;
     for (int a = 0; a < ndim; ++a) {
         const int64_t G = global_ext[a], K = kernel[a], S = stride[a], o = shard_off[a], L = shard_ext[a];
         const int64_t P = (K - 1) / 2;

@@ -168,18 +168,32 @@ hipError_t launch_conv_fwd_rows(const Tile3& t, const Conv3& cv, shard_dtype_t d
                                 const void* wfrag, int nkc_frag, int nt_frag, void* y, const Region& rg,
                                 const Fold* fold, hipStream_t s, const Region* rg2 = nullptr);
 size_t wgrad_xm_workspace(const Tile3& t, const Conv3& cv, shard_dtype_t dt);
+// `status`: the call's status word (see kWgradStatusBytes).
 hipError_t launch_wgrad_xm(const Tile3& t, const Conv3& cv, shard_dtype_t dt, const void* tile, const void* dy,
-                           float* dw, void* ws, const Fold* fold, hipStream_t s);
+                           float* dw, void* ws, const Fold* fold, uint32_t* status, hipStream_t s);
 size_t wgrad_tr_workspace(const Tile3& t, const Conv3& cv, shard_dtype_t dt);
 hipError_t launch_wgrad_tr(const Tile3& t, const Conv3& cv, shard_dtype_t dt, const void* tile, const void* dy,
                            float* part, int32_t red[6], hipStream_t s);
 
-// Which implementation a call takes, read from the environment variable
-// SHARDCONV_ALGO at each call: unset picks the fastest applicable kernel,
-// "tiled" skips the shape-specialised kernels, "generic" forces the plain
-// direct kernels (tests use both to cross-check the kernels against each other).
+// Options of the calling host thread (shard_set_call_opts): which kernel family
+// a convolution takes - the fastest applicable (default), the general tiled MFMA
+// kernels past the shape-specialised ones, or the plain direct kernels (tests
+// cross-check the families against each other) - and the poll bound of the
+// weight gradient's inter-wave hand-off waits (0: the default).
+struct CallOpts {
+    int32_t kernels;
+    uint32_t wait_polls;
+};
+const CallOpts& call_opts();
 bool force_generic();
 bool force_tiled();
+
+// The weight-gradient workspace starts with a status block: its first 32-bit
+// word is 0 after a call completed normally and nonzero when a bounded wait of
+// the kernel gave up (dw then holds NaN). Cleared by every call.
+constexpr size_t kWgradStatusBytes = 256;
+constexpr uint32_t kDefaultWaitPolls = 1u << 20;
+hipError_t launch_wgrad_status_clear(uint32_t* status, hipStream_t s);
 
 inline int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
 inline int64_t round_up(int64_t a, int64_t b) { return ceil_div(a, b) * b; }

@@ -27,6 +27,11 @@ _vp = ctypes.c_void_p
 
 
 SHARD_REGION_ALL, SHARD_REGION_INTERIOR, SHARD_REGION_BOUNDARY = 0, 1, 2
+SHARD_KERNELS_FASTEST, SHARD_KERNELS_TILED, SHARD_KERNELS_DIRECT = 0, 1, 2
+
+
+class shard_call_opts_t(ctypes.Structure):
+    _fields_ = [("kernels", ctypes.c_int32), ("wait_polls", ctypes.c_uint32)]
 
 
 class shard_halo_src_t(ctypes.Structure):
@@ -81,6 +86,7 @@ _SIGS = {
     "shard_halo_accumulate_pair": (ctypes.c_int, [_tp, ctypes.c_int, _vp, ctypes.c_int32, ctypes.c_int64, _vp,
                                                   ctypes.c_int64, _vp, _vp]),
     "shard_status_string": (ctypes.c_char_p, [ctypes.c_int]),
+    "shard_set_call_opts": (ctypes.c_int, [ctypes.c_void_p]),
 }
 for _name, (_res, _args) in _SIGS.items():
     _f = getattr(_lib, _name)
@@ -147,6 +153,28 @@ def _stream(stream):
 
 def shard_status_string(status: int) -> str:
     return _lib.shard_status_string(int(status)).decode()
+
+
+def shard_set_call_opts(kernels=SHARD_KERNELS_FASTEST, wait_polls=0):
+    """Options of the calling host thread (None-like defaults restore them)."""
+    o = shard_call_opts_t(int(kernels), int(wait_polls))
+    _check("shard_set_call_opts", _lib.shard_set_call_opts(ctypes.byref(o)))
+
+
+class call_opts:
+    """Context manager: the calling thread's options inside the block, the
+    defaults after it."""
+
+    def __init__(self, kernels=SHARD_KERNELS_FASTEST, wait_polls=0):
+        self.kernels, self.wait_polls = kernels, wait_polls
+
+    def __enter__(self):
+        shard_set_call_opts(self.kernels, self.wait_polls)
+        return self
+
+    def __exit__(self, *exc):
+        _check("shard_set_call_opts", _lib.shard_set_call_opts(None))
+        return False
 
 
 def shard_conv_geometry(global_ext, shard_off, shard_ext, kernel, stride, sharded_mask) -> dict:

@@ -94,6 +94,9 @@ def run_wgrad(sc, w, desc, tile, sg, dy):
     nbytes = sc.shard_conv_workspace_bytes(1, desc, code, w.cout, w.K, w.S, O)
     ws = torch.empty(max(nbytes, 16), dtype=torch.uint8, device="cuda")
     sc.shard_conv_wgrad(desc, tile, dy, w.cout, w.K, w.S, sg.g["pad_lo"], O, dw, ws)
+    # the call's status word (first word of the workspace): 0 unless a bounded
+    # wait inside the kernel gave up
+    assert int(ws[:4].view(torch.int32).item()) == 0, "weight gradient reported a wait that gave up"
     return dw
 
 

@@ -19,6 +19,10 @@ from oracle import conv as oconv
 from oracle import geometry as ogeo
 
 
+# kernel family names of the cross-check tests -> shard_kernels_t
+KERNELS = {"": 0, "tiled": 1, "generic": 2}
+
+
 def torch_dtype(w: Workload):
     import torch
     return torch.float32 if w.dtype == "f32" else torch.bfloat16

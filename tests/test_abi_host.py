@@ -92,8 +92,18 @@ def test_geometry_of_the_workloads(sc):
             assert got[k] == c[k], (name, k)
 
 
+def test_geometry_even_kernel_is_unsupported(sc):
+    for args in (([8], [0], [4], [2], [1], [1]), ([8, 6], [0, 0], [4, 6], [3, 4], [1, 1], [1, 0])):
+        with pytest.raises(sc.ShardError) as e:
+            sc.shard_conv_geometry(*args)
+        assert e.value.status == sc.SHARD_ERR_UNSUPPORTED
+    # a malformed argument is reported as such even beside an even kernel
+    with pytest.raises(sc.ShardError) as e:
+        sc.shard_conv_geometry([8], [0], [4], [2], [0], [1])
+    assert e.value.status == sc.SHARD_ERR_INVALID
+
+
 @pytest.mark.parametrize("args", [
-    ([8], [0], [4], [2], [1], [1]),        # even kernel
     ([8], [0], [4], [0], [1], [1]),        # kernel 0
     ([8], [0], [4], [3], [0], [1]),        # stride 0
     ([8], [6], [4], [3], [1], [1]),        # box beyond the domain
@@ -208,11 +218,15 @@ def test_conv_rejections(sc):
     assert f(p, 1, FAKE, FAKE, 32, K, S, pad, O, FAKE, ctypes.c_void_p(0x10008), need, None) == sc.SHARD_ERR_INVALID
     assert f(p, 1, FAKE, FAKE, 32, K, S, pad, A(0, 8, 40), None, None, 0, None) == sc.SHARD_OK        # empty: no-op
     assert f(p, 1, FAKE, FAKE, 32, A(65, 3, 3), S, pad, O, FAKE, FAKE, need, None) == sc.SHARD_ERR_INVALID
+    # even kernels: well formed, but outside the symmetric padding the method uses
+    assert f(p, 1, FAKE, FAKE, 32, A(3, 2, 3), S, pad, O, FAKE, FAKE, need, None) == sc.SHARD_ERR_UNSUPPORTED
+    assert lib.shard_conv_workspace_bytes(0, p, 1, 32, A(3, 3, 4), S, O) == ctypes.c_size_t(-1).value
     wneed = sc.shard_conv_workspace_bytes(1, d, sc.SHARD_BF16, 32, [3, 3, 3], [1, 1, 1], [8, 8, 40])
     g = lib.shard_conv_wgrad
     assert g(p, 1, FAKE, FAKE, 32, K, S, pad, O, FAKE, FAKE, wneed - 1, None) == sc.SHARD_ERR_INVALID
     assert g(p, 1, FAKE, FAKE, 32, K, S, pad, O, None, FAKE, wneed, None) == sc.SHARD_ERR_INVALID     # null dw
     assert g(p, 1, FAKE, None, 32, K, S, pad, O, FAKE, FAKE, wneed, None) == sc.SHARD_ERR_INVALID     # null dy
+    assert g(p, 1, FAKE, FAKE, 32, A(4, 3, 3), S, pad, O, FAKE, FAKE, wneed, None) == sc.SHARD_ERR_UNSUPPORTED
 
 
 @pytestmark_host
@@ -282,6 +296,7 @@ def test_dgrad_rejections(sc):
     assert f(p, 1, None, FAKE, 32, K, S, pad, O, FAKE, FAKE, need, None) == sc.SHARD_ERR_INVALID      # null dy
     assert f(p, 1, FAKE, FAKE, 32, K, S, pad, O, FAKE, ctypes.c_void_p(0x10008), need, None) == sc.SHARD_ERR_INVALID
     assert f(p, 7, FAKE, FAKE, 32, K, S, pad, O, FAKE, FAKE, need, None) == sc.SHARD_ERR_INVALID      # dtype
+    assert f(p, 1, FAKE, FAKE, 32, A(3, 3, 2), S, pad, O, FAKE, FAKE, need, None) == sc.SHARD_ERR_UNSUPPORTED
     empty = sc.tile_desc(0, 16, [8, 8, 40], [1, 0, 0], [1, 0, 0])
     assert f(ctypes.byref(empty), 1, None, FAKE, 32, K, S, pad, O, None, None, 0, None) == sc.SHARD_OK  # no tile
 
@@ -375,6 +390,12 @@ def test_folded_rejections(sc):
     h.slab[0][1] = 0x10001                                                                          # misaligned slab
     assert f(p, 1, FAKE, hp, 0, FAKE, 32, K, S, pad, O, FAKE, FAKE, need, None) == sc.SHARD_ERR_INVALID
     assert f(p, 1, FAKE, hp, 0, FAKE, 32, K, S, pad, A(0, 8, 40), None, None, 0, None) == sc.SHARD_OK  # empty
+    h.slab[0][1] = None
+    assert f(p, 1, FAKE, hp, 0, FAKE, 32, A(2, 3, 3), S, pad, O, FAKE, FAKE, need, None) == \
+        sc.SHARD_ERR_UNSUPPORTED                                                                    # even kernel
+    wneed = sc.shard_conv_workspace_bytes(1, d, sc.SHARD_BF16, 32, [3, 3, 3], [1, 1, 1], [8, 8, 40])
+    assert lib.shard_conv_wgrad_folded(p, 1, FAKE, hp, FAKE, 32, A(3, 6, 3), S, pad, O, FAKE, FAKE, wneed,
+                                       None) == sc.SHARD_ERR_UNSUPPORTED
     il, ih = A(0, 0, 0), A(0, 0, 0)
     q = lib.shard_conv_interior
     assert q(p, K, S, None, O, il, ih) == sc.SHARD_ERR_INVALID

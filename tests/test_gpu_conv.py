@@ -105,9 +105,9 @@ def test_c1_concatenated_shards_equal_full_domain(sc):
 
 
 @pytest.mark.parametrize("name", ["c3r", "c2r", "c4r", "c5r", "c1"])
-def test_kernel_variants_agree(sc, monkeypatch, name):
+def test_kernel_variants_agree(sc, name):
     """The shape-specialised kernels (default), the general tiled MFMA kernels
-    (SHARDCONV_ALGO=tiled) and the direct kernels (SHARDCONV_ALGO=generic) give
+    (SHARD_KERNELS_TILED) and the direct kernels (SHARD_KERNELS_DIRECT) give
     the same result: bitwise on integer data, to the tolerance otherwise."""
     w = cases.REDUCED[name]
     idx = tuple(len(w.splits(a)) - 1 for a in range(w.nd))
@@ -117,12 +117,8 @@ def test_kernel_variants_agree(sc, monkeypatch, name):
         wt, dyh = dev(w_host), dev(dy_box(w, sg, dist))
         res = {}
         for algo in ("", "tiled", "generic"):
-            if algo:
-                monkeypatch.setenv("SHARDCONV_ALGO", algo)
-            else:
-                monkeypatch.delenv("SHARDCONV_ALGO", raising=False)
-            res[algo] = (host(run_fwd(sc, w, desc, tile, sg, wt)), host(run_wgrad(sc, w, desc, tile, sg, dyh)))
-        monkeypatch.delenv("SHARDCONV_ALGO", raising=False)
+            with sc.call_opts(kernels=cases.KERNELS[algo]):
+                res[algo] = (host(run_fwd(sc, w, desc, tile, sg, wt)), host(run_wgrad(sc, w, desc, tile, sg, dyh)))
         y0, d0 = res[""]
         for algo in ("tiled", "generic"):
             y1, d1 = res[algo]
@@ -294,3 +290,74 @@ def test_full_size_wgrad_with_plane_supported_dy(sc, name, integer):
         err = cases.norm_max_err(dw, ref)
         log(f"  wgrad {name}: normalised max err {err:.3e}")
         assert err <= cases.TOL[w.dtype]
+
+
+# the shapes of the three weight-gradient kernel families at full size: the
+# W-march kernel (C3), the tiled bf16 kernel (C4) and the tiled fp32 kernel (C5)
+DENSE_WGRAD = ["c3_3d_bf16", "c4_3d_bf16_k5", "c5_3d_fp32_s2"]
+
+
+@pytest.mark.parametrize("name", DENSE_WGRAD)
+@pytest.mark.timeout(900)
+def test_full_size_wgrad_dense_dy(sc, name):
+    """The weight gradient of the whole shard on the full seeded dy (every owned
+    output voxel contributes: the full split-K accumulation), against the oracle
+    summed over chunks of output planes on the host (the oracle's sum over the
+    owned box, taken chunk by chunk, is the same sum)."""
+    w = cases.WORKLOADS[name]
+    log(f"dense wgrad {name}: building tile")
+    desc, tile, sg, full_h = build_tile(sc, w, w.shard, keep_host=True)
+    dyh = dy_box(w, sg)
+    log(f"dense wgrad {name}: running")
+    dw = host(run_wgrad(sc, w, desc, tile, sg, dev(dyh))).astype(np.float64)
+    del tile
+    lo, hi = cases.owned_box(sg)
+    L = sg.g["out_ext"][0]
+    ref = np.zeros((w.cout, w.cin) + tuple(w.K))
+    CH = 8
+    for p0 in range(0, L, CH):
+        p1 = min(L, p0 + CH)
+        l2, h2 = list(lo), list(hi)
+        l2[0], h2[0] = lo[0] + p0, lo[0] + p1
+        r0 = p0 * w.S[0] - sg.g["pad_lo"][0]
+        r1 = (p1 - 1) * w.S[0] - sg.g["pad_lo"][0] + w.K[0]
+        xw, origin = window_from_tile(w, sg, full_h, (r0, r1))
+        ref += oconv.conv_wgrad_window(xw, origin, w.G, cases.to_ncdhw(cases.as_f64(dyh[:, p0:p1], w)), w.K, w.S,
+                                       l2, h2)
+        if p0 % (8 * CH) == 0:
+            log(f"  oracle planes {p0}..{p1} of {L}")
+    err = cases.norm_max_err(dw, ref)
+    log(f"  dense wgrad {name}: normalised max err {err:.3e}")
+    assert err <= cases.TOL[w.dtype]
+
+
+def test_wgrad_status_word_reports_a_wait_that_gave_up(sc):
+    """The W-march weight gradient hands stage buffers between its waves through
+    bounded waits. With the bound forced down to one poll the waits give up at
+    once (every kernel still runs to its end): the status word at the start of
+    the workspace must say so and every dw element must be NaN. With the default
+    bound the same call is clean and matches the first result."""
+    import torch
+    w = cases.REDUCED["c3r"]
+    idx = w.shards()[1]
+    desc, tile, sg, _ = build_tile(sc, w, idx)
+    dyh = dev(dy_box(w, sg))
+    O = sg.g["out_ext"]
+    dw = torch.empty((w.cout, w.cin) + tuple(w.K), dtype=torch.float32, device="cuda")
+    nbytes = sc.shard_conv_workspace_bytes(1, desc, sc.SHARD_BF16, w.cout, w.K, w.S, O)
+    ws = torch.empty(nbytes, dtype=torch.uint8, device="cuda")
+
+    def call():
+        ws[:4].fill_(0xA5)
+        sc.shard_conv_wgrad(desc, tile, dyh, w.cout, w.K, w.S, sg.g["pad_lo"], O, dw, ws)
+        torch.cuda.synchronize()
+        return int(ws[:4].view(torch.int32).item()), dw.clone()
+
+    s0, d0 = call()
+    assert s0 == 0 and bool(torch.isfinite(d0).all())
+    with sc.call_opts(wait_polls=1):
+        s1, d1 = call()
+    assert s1 != 0
+    assert bool(torch.isnan(d1).all())
+    s2, d2 = call()
+    assert s2 == 0 and torch.equal(d2, d0)

@@ -96,9 +96,9 @@ def test_dgrad_integer_exact_reduced(sc, name):
 
 
 @pytest.mark.parametrize("name", ["c3r", "c2r", "c4r", "c5r", "c1"])
-def test_dgrad_kernel_variants_agree(sc, monkeypatch, name):
-    """The forward-kernel route (default, and SHARDCONV_ALGO=tiled) and the direct
-    kernel (SHARDCONV_ALGO=generic) agree: bitwise on integer data."""
+def test_dgrad_kernel_variants_agree(sc, name):
+    """The forward-kernel route (default, and SHARD_KERNELS_TILED) and the direct
+    kernel (SHARD_KERNELS_DIRECT) agree: bitwise on integer data."""
     w = cases.REDUCED[name]
     idx = tuple(len(w.splits(a)) - 1 for a in range(w.nd))
     for dist in (INT_DIST, None):
@@ -107,12 +107,8 @@ def test_dgrad_kernel_variants_agree(sc, monkeypatch, name):
         wt, dyh = dev(w_host), dev(dy_box(w, sg, dist))
         res = {}
         for algo in ("", "tiled", "generic"):
-            if algo:
-                monkeypatch.setenv("SHARDCONV_ALGO", algo)
-            else:
-                monkeypatch.delenv("SHARDCONV_ALGO", raising=False)
-            res[algo] = host(run_dgrad(sc, w, sg, dyh, wt)[1])
-        monkeypatch.delenv("SHARDCONV_ALGO", raising=False)
+            with sc.call_opts(kernels=cases.KERNELS[algo]):
+                res[algo] = host(run_dgrad(sc, w, sg, dyh, wt)[1])
         for algo in ("tiled", "generic"):
             if dist is INT_DIST:
                 assert np.array_equal(res[""], res[algo]), (name, algo)

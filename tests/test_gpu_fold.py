@@ -126,11 +126,10 @@ def test_interior_then_boundary(sc, name):
 
 @pytest.mark.parametrize("name", ["c3r", "c2r", "c4r", "c5r", "c1"])
 @pytest.mark.parametrize("algo", ["", "tiled", "generic"])
-def test_folded_kernel_variants_integer_exact(sc, monkeypatch, name, algo):
+def test_folded_kernel_variants_integer_exact(sc, name, algo):
     """Every kernel family folds the halo: integer data bit for bit against the
     oracle on the last shard along every axis (two neighbours where there are)."""
-    if algo:
-        monkeypatch.setenv("SHARDCONV_ALGO", algo)
+    sc.shard_set_call_opts(kernels=cases.KERNELS[algo])
     w = cases.REDUCED[name]
     idx = tuple(min(1, len(w.splits(a)) - 1) for a in range(w.nd))
     w_host, w64 = weights(w, INT_DIST)
@@ -208,10 +207,9 @@ def test_folded_wgrad_equals_unpacked_every_shard_reduced(sc, name):
 
 @pytest.mark.parametrize("name", ["c3r", "c2r", "c4r", "c5r", "c1"])
 @pytest.mark.parametrize("algo", ["", "tiled", "generic"])
-def test_folded_wgrad_kernel_variants_integer_exact(sc, monkeypatch, name, algo):
+def test_folded_wgrad_kernel_variants_integer_exact(sc, name, algo):
     from gpu_util import dy_box
-    if algo:
-        monkeypatch.setenv("SHARDCONV_ALGO", algo)
+    sc.shard_set_call_opts(kernels=cases.KERNELS[algo])
     w = cases.REDUCED[name]
     idx = tuple(min(1, len(w.splits(a)) - 1) for a in range(w.nd))
     desc, tile, slabs, sg, full_h = _canary_tile_and_slabs(sc, w, idx, INT_DIST)
