@@ -8,6 +8,7 @@ import pytest
 import synth
 import shard_cases as cases
 from gpu_util import build_tile, canary_for, dev, host, log
+from oracle import conv as oconv
 from oracle import halo as ohalo
 
 pytestmark = pytest.mark.gpu
@@ -25,12 +26,42 @@ def _bits_equal(a, b):
     return a.shape == b.shape and np.array_equal(a.view(np.uint8), b.view(np.uint8))
 
 
+def _oracle_box(w, lo, hi):
+    """The zero-extended domain over the global box [lo, hi), channels-last
+    float64, by the oracle's definition: the generator supplies only the values
+    inside the domain, and oracle.conv.zero_extend places them and zero-fills
+    everything outside it."""
+    c0 = [max(0, l) for l in lo]
+    c1 = [min(g, h) for g, h in zip(w.G, hi)]
+    shape = [w.N, w.cin] + [h - l for l, h in zip(lo, hi)]
+    if any(b <= a for a, b in zip(c0, c1)):
+        return cases.to_cl(np.zeros(shape))
+    inner = cases.to_ncdhw(cases.as_f64(cases.x_box(w, c0, c1, cases.out_code(w)), w))
+    return cases.to_cl(oconv.zero_extend(inner, [l - c for l, c in zip(lo, c0)], [h - c for h, c in zip(hi, c0)]))
+
+
 def _unpack_case(sc, w, idx):
     log(f"unpack {w.name} shard {idx}")
     desc, tile, sg, _ = build_tile(sc, w, idx)
     got = host(tile)
-    want = cases.x_box(w, sg.tile_lo, sg.tile_hi, cases.out_code(w))
-    assert _bits_equal(got, want)
+    # the oracle's padded tile (the definition: the zero-extended domain over the
+    # shard's input box), and the oracle's exchange: interior only, then every
+    # margin written by oracle.halo.unpack from the slab the neighbour sends
+    x = cases.to_ncdhw(cases.as_f64(cases.x_box(w, [0] * w.nd, list(w.G), cases.out_code(w)), w))
+    want = oconv.padded_tile(x, sg.g, sg.off, sg.ext)
+    assert np.array_equal(cases.as_f64(got, w), cases.to_cl(want))
+    lo, hi = sg.g["halo_lo"], sg.g["halo_hi"]
+    t = np.full(want.shape, np.nan)
+    inner = (slice(None), slice(None)) + tuple(slice(l, l + e) for l, e in zip(lo, sg.ext))
+    t[inner] = want[inner]
+    for axis in range(w.nd):
+        for side in (0, 1):
+            if (lo[axis] if side == 0 else hi[axis]) == 0:
+                continue
+            slab = (ohalo.received_slab(x, axis, side, sg.off, lo, sg.ext, hi)
+                    if cases.neighbour_exists(w, idx, axis, side) else None)
+            t = ohalo.unpack(t, axis, side, slab, lo, sg.ext, hi)
+    assert np.array_equal(cases.as_f64(got, w), cases.to_cl(t))
 
 
 @pytest.mark.parametrize("name", list(cases.REDUCED))
@@ -141,6 +172,17 @@ def test_full_size_halos_of_the_measured_shard(sc, name):
     got = host(tile)
     del tile
     assert _bits_equal(got, want)
+    # every margin (what the unpack calls wrote) against the oracle's zero-extended
+    # domain over the same global box
+    lo, hi = sg.g["halo_lo"], sg.g["halo_hi"]
+    for axis in range(w.nd):
+        for side in (0, 1):
+            if (lo[axis] if side == 0 else hi[axis]) == 0:
+                continue
+            b0, b1 = ohalo.face_box(axis, ohalo.margin_rows(axis, side, lo, sg.ext, hi), lo, sg.ext, hi)
+            ref = _oracle_box(w, [t + a for t, a in zip(sg.tile_lo, b0)], [t + b for t, b in zip(sg.tile_lo, b1)])
+            box = (slice(None),) + tuple(slice(a, b) for a, b in zip(b0, b1)) + (slice(None),)
+            assert np.array_equal(cases.as_f64(got[box], w), ref), (axis, side)
 
 
 def _pair_case(sc, w, idx):
