@@ -194,6 +194,25 @@ shard_status_t shard_conv_fwd(const shard_tile_t* x, shard_dtype_t dtype, const 
                               size_t ws_bytes, hipStream_t stream);
 
 /*
+ * shard_conv_fwd for callers that cannot allocate device memory (code under HIP
+ * graph capture, tight serving loops, harnesses that forbid hipMalloc): the
+ * same convolution and result, bit for bit, without the workspace arguments.
+ * Its scratch (the weights rearranged for the matrix instructions) lives in a
+ * static device array of the library, 4 MiB, one per GPU, held until the
+ * process ends; the call allocates and frees nothing. Every call on a GPU
+ * shares that GPU's array, so calls that overlap on one GPU (on different
+ * streams, or from different host threads) race and must be serialised by the
+ * caller; sequential calls on one stream are safe.
+ * Errors: as shard_conv_fwd; SHARD_ERR_UNSUPPORTED also when the workspace
+ * shard_conv_fwd would need (shard_conv_workspace_bytes op 0) exceeds 4 MiB;
+ * SHARD_ERR_HIP also when the scratch array's address cannot be obtained.
+ */
+shard_status_t shard_conv_fwd_noalloc(const shard_tile_t* x, shard_dtype_t dtype, const void* tile, const void* w,
+                                      int64_t c_out, const int64_t kernel[], const int64_t stride[],
+                                      const int64_t pad_lo[], const int64_t out_ext[], void* y,
+                                      hipStream_t stream);
+
+/*
  * Received halo slabs for the folded entry points: slab[a][side] is the slab
  * the neighbour on (axis a, side 0 = lo / 1 = hi) sent, laid out as
  * shard_halo_slab_shape(x, a, that margin's width) gives, in the tile's dtype,

@@ -534,6 +534,22 @@ shard_status_t shard_conv_fwd(const shard_tile_t* x, shard_dtype_t dtype, const 
     return map_hip(launch_conv_fwd(t, cv, dtype, tile, w, y, ws, stream));
 }
 
+shard_status_t shard_conv_fwd_noalloc(const shard_tile_t* x, shard_dtype_t dtype, const void* tile, const void* w,
+                                      int64_t c_out, const int64_t kernel[], const int64_t stride[],
+                                      const int64_t pad_lo[], const int64_t out_ext[], void* y, hipStream_t stream)
+{
+    Tile3 t;
+    Conv3 cv;
+    if (!norm_tile(x, dtype, t) || !pad_lo || !norm_conv(x, t, c_out, kernel, stride, pad_lo, out_ext, cv))
+        return SHARD_ERR_INVALID;
+    if (!odd_kernel(x, kernel)) return SHARD_ERR_UNSUPPORTED;
+    if (t.n * cv.out_voxels() == 0) return SHARD_OK;
+    if (conv_fwd_workspace(t, cv, dtype) > conv_fwd_noalloc_limit()) return SHARD_ERR_UNSUPPORTED;
+    if ((tile_elems(t) > 0 && !tile) || !w || !y) return SHARD_ERR_INVALID;
+    if (!aligned(tile, t.esz) || !aligned(w, t.esz) || !aligned(y, t.esz)) return SHARD_ERR_INVALID;
+    return map_hip(launch_conv_fwd_noalloc(t, cv, dtype, tile, w, y, stream));
+}
+
 shard_status_t shard_conv_interior(const shard_tile_t* x, const int64_t kernel[], const int64_t stride[],
                                    const int64_t pad_lo[], const int64_t out_ext[], int64_t int_lo[],
                                    int64_t int_hi[])

@@ -140,6 +140,12 @@ hipError_t launch_conv_fwd_region(const Tile3& t, const Conv3& cv, shard_dtype_t
 hipError_t launch_conv_fwd_region_pair(const Tile3& t, const Conv3& cv, shard_dtype_t dt, const void* tile,
                                        const void* w, void* y, const Region& ra, const Region& rb, const Fold* fold,
                                        void* ws, hipStream_t s, bool frags_ready);
+// The forward with its workspace in the library's per-device scratch array
+// (noalloc.hip): bytes it holds, and the launch (the caller has checked that
+// conv_fwd_workspace fits).
+size_t conv_fwd_noalloc_limit();
+hipError_t launch_conv_fwd_noalloc(const Tile3& t, const Conv3& cv, shard_dtype_t dt, const void* tile,
+                                   const void* w, void* y, hipStream_t s);
 hipError_t launch_conv_wgrad(const Tile3& t, const Conv3& cv, shard_dtype_t dt, const void* tile, const void* dy,
                              float* dw, void* ws, hipStream_t s);
 // The same with the halo folded into the loads (the kernels that cannot fold

@@ -87,6 +87,8 @@ _SIGS = {
                                                   ctypes.c_int64, _vp, _vp]),
     "shard_status_string": (ctypes.c_char_p, [ctypes.c_int]),
     "shard_set_call_opts": (ctypes.c_int, [ctypes.c_void_p]),
+    "shard_conv_fwd_noalloc": (ctypes.c_int, [_tp, ctypes.c_int, _vp, _vp, ctypes.c_int64, _i64p, _i64p, _i64p,
+                                              _i64p, _vp, _vp]),
 }
 for _name, (_res, _args) in _SIGS.items():
     _f = getattr(_lib, _name)
@@ -216,6 +218,13 @@ def shard_conv_fwd(desc, tile, w, c_out, kernel, stride, pad_lo, out_ext, y, ws,
     _check("shard_conv_fwd", _lib.shard_conv_fwd(ctypes.byref(desc), _dtype_code(tile), _ptr(tile), _ptr(w), c_out,
                                                  _arr(kernel), _arr(stride), _arr(pad_lo), _arr(out_ext), _ptr(y),
                                                  _ptr(ws), nbytes, _stream(stream)))
+
+
+def shard_conv_fwd_noalloc(desc, tile, w, c_out, kernel, stride, pad_lo, out_ext, y, stream=None):
+    _check("shard_conv_fwd_noalloc", _lib.shard_conv_fwd_noalloc(ctypes.byref(desc), _dtype_code(tile), _ptr(tile),
+                                                                 _ptr(w), c_out, _arr(kernel), _arr(stride),
+                                                                 _arr(pad_lo), _arr(out_ext), _ptr(y),
+                                                                 _stream(stream)))
 
 
 def shard_conv_wgrad(desc, tile, dy, c_out, kernel, stride, pad_lo, out_ext, dw, ws, stream=None):
