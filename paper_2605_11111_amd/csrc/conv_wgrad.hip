@@ -23,6 +23,8 @@
 #include "common.h"
 #include "internal.h"
 
+#define SC_LDSW(p) ((__attribute__((address_space(3))) void*)(p))
+
 namespace shardconv {
 
 size_t generic_wgrad_workspace(const Tile3& t, const Conv3& cv);
@@ -279,6 +281,217 @@ __global__ __launch_bounds__(kThreads, 2) void wgrad_bf16_tiled(WgArgs a)
     for (int i = 0; i < TG; ++i) out[i * 64 + lane] = make_float4(acc[i][0], acc[i][1], acc[i][2], acc[i][3]);
 }
 
+// bf16 with the staging of brick b + 1 in flight while brick b multiplies (a
+// thread issues the global loads of its units of the next brick into registers
+// before the brick's MFMAs and writes them to LDS after them), and the
+// transposed LDS copies written four voxels at a time:
+// a staging unit is four consecutive voxels (along W) of one 8-channel group,
+// loaded as four 16-byte vectors into registers; after the brick's MFMAs each
+// of its 8 channels is written as one 8-byte LDS store of the four voxels (the
+// row-by-row 2-byte stores of wgrad_bf16_tiled cost eight stores per voxel
+// and bank conflicts). LDS layouts, bricks, K steps and taps are those of
+// wgrad_bf16_tiled: the partials are bit-identical. Units of the input brick
+// run over (group of four x, channel group, row) with x fastest, units of dy
+// over (quad of brick voxels, channel group), quads fastest: the lanes of a
+// store instruction write consecutive 8-byte slots.
+constexpr int kPipeBXU = 2;  // at most this many input staging units per thread
+constexpr int kPipeBDU = 2;  // and dy staging units
+
+template <int KDG, int K1, int K2, int WCO, int XU, int DU>
+__global__ __launch_bounds__(kThreads, 2) void wgrad_bf16_pipe(WgArgs a)
+{
+    constexpr int WCI = 4 / WCO;
+    constexpr int TG = KDG * K1 * K2;
+    constexpr int NCO = WCO * 16, NCI = WCI * 16;
+    constexpr int NQX = NCI / 8, NQD = NCO / 8;
+    extern __shared__ uint4 lds4[];
+    bf16_t* xs = reinterpret_cast<bf16_t*>(lds4);
+    bf16_t* ds = reinterpret_cast<bf16_t*>(reinterpret_cast<char*>(lds4) + a.dy_off);
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = tid >> 6;
+    const int wco = wave / WCI, wci = wave % WCI;
+    const int g = lane >> 4;
+    const int l16 = lane & 15;
+
+    int64_t b = xcd_remap(blockIdx.x, a.nblocks);
+    const int tg = int(b % a.ntg);
+    b /= a.ntg;
+    const int cb = int(b % a.ncb);
+    b /= a.ncb;
+    const int mb = int(b % a.nmb);
+    const int64_t split = b / a.nmb;
+    const int64_t br0 = split * a.nbricks / a.nsplit, br1 = (split + 1) * a.nbricks / a.nsplit;
+    const int kd0 = tg * KDG;
+    const int64_t co0 = int64_t(mb) * NCO, ci0 = int64_t(cb) * NCI;
+    const int bov = a.BO[0] * a.BO[1] * a.BO[2];
+    const bf16_t* tile = reinterpret_cast<const bf16_t*>(a.tile);
+    const bf16_t* dy = reinterpret_cast<const bf16_t*>(a.dy);
+    const int ngx = (a.bix + 3) / 4;             // groups of four x per input row
+    const int nxu = a.biz * a.biy * ngx * NQX;   // input units
+    const int ndu = (bov / 4) * NQD;             // dy units
+
+    f32x4_w acc[TG];
+#pragma unroll
+    for (int i = 0; i < TG; ++i) acc[i] = f32x4_w{0.f, 0.f, 0.f, 0.f};
+
+    uint4 xv[XU][4], dv[DU][4];
+    auto issue = [&](int64_t br) {
+        int64_t nn, ob[3];
+        brick_origin(a, br, nn, ob);
+        const int64_t i0 = ob[0] * a.S[0] + kd0 - a.pad[0];
+        const int64_t i1 = ob[1] * a.S[1] - a.pad[1];
+        const int64_t i2 = ob[2] - a.pad[2];
+#pragma unroll
+        for (int i = 0; i < XU; ++i) {
+            const int u = tid + i * kThreads;
+            const int gx = u % ngx, r = u / ngx;
+            const int q = r % NQX, row = r / NQX;
+            const int y = row % a.biy, z = row / a.biy;
+            const int64_t t0 = i0 + z, t1 = i1 + y;
+            const int64_t c = ci0 + 8 * q;
+            const bool rowok = u < nxu && t0 >= 0 && t0 < a.P[0] && t1 >= 0 && t1 < a.P[1] && c < a.cin;
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                const int x = 4 * gx + j;
+                const int64_t t2 = i2 + x;
+                uint4 val = make_uint4(0u, 0u, 0u, 0u);
+                if (rowok && x < a.bix && t2 >= 0 && t2 < a.P[2]) {
+                    const bf16_t* vox =
+                        a.fold.mask ? reinterpret_cast<const bf16_t*>(fold_voxel(a.fold, a.tile, nn, t0, t1, t2,
+                                                                                 a.cin * 2))
+                                    : tile + (((nn * a.P[0] + t0) * a.P[1] + t1) * a.P[2] + t2) * a.cin;
+                    if (vox) val = *reinterpret_cast<const uint4*>(vox + c);
+                }
+                xv[i][j] = val;
+            }
+        }
+#pragma unroll
+        for (int i = 0; i < DU; ++i) {
+            const int u = tid + i * kThreads;
+            const int nq4 = bov / 4;
+            const int f4 = u % nq4, q = u / nq4;
+            const int f = 4 * f4;
+            const int ox = f % a.BO[2];
+            const int oy = (f / a.BO[2]) % a.BO[1];
+            const int oz = f / (a.BO[2] * a.BO[1]);
+            const int64_t o0 = ob[0] + oz, o1 = ob[1] + oy;
+            const int64_t c = co0 + 8 * q;
+            const bool rowok = u < ndu && o0 < a.O[0] && o1 < a.O[1] && c < a.cout;
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                const int64_t o2 = ob[2] + ox + j;
+                uint4 val = make_uint4(0u, 0u, 0u, 0u);
+                if (rowok && o2 < a.O[2])
+                    val = *reinterpret_cast<const uint4*>(dy + (((nn * a.O[0] + o0) * a.O[1] + o1) * a.O[2] + o2) *
+                                                                   a.cout + c);
+                dv[i][j] = val;
+            }
+        }
+    };
+    // channel e of four voxels -> one 8-byte word (voxel j in bits 16 j ..)
+    auto pick = [](const uint4 (&v)[4], int e) {
+        auto half = [&](const uint4& w) {
+            const uint32_t d = e < 2 ? w.x : e < 4 ? w.y : e < 6 ? w.z : w.w;
+            return (e & 1) ? (d >> 16) : (d & 0xFFFFu);
+        };
+        return make_uint2(half(v[0]) | (half(v[1]) << 16), half(v[2]) | (half(v[3]) << 16));
+    };
+    auto commit = [&]() {
+#pragma unroll
+        for (int i = 0; i < XU; ++i) {
+            const int u = tid + i * kThreads;
+            if (u < nxu) {
+                const int gx = u % ngx, r = u / ngx;
+                const int q = r % NQX, row = r / NQX;
+                bf16_t* dst = xs + (8 * q) * a.cs + row * a.bixp + 4 * gx;
+#pragma unroll
+                for (int e = 0; e < 8; ++e) *reinterpret_cast<uint2*>(dst + e * a.cs) = pick(xv[i], e);
+            }
+        }
+#pragma unroll
+        for (int i = 0; i < DU; ++i) {
+            const int u = tid + i * kThreads;
+            if (u < ndu) {
+                const int nq4 = bov / 4;
+                const int f4 = u % nq4, q = u / nq4;
+                bf16_t* dst = ds + (8 * q) * a.csd + 4 * f4;
+#pragma unroll
+                for (int e = 0; e < 8; ++e) *reinterpret_cast<uint2*>(dst + e * a.csd) = pick(dv[i], e);
+            }
+        }
+    };
+
+    if (br0 < br1) issue(br0);
+    for (int64_t br = br0; br < br1; ++br) {
+        __syncthreads();  // every wave is done reading the previous brick
+        commit();
+        __syncthreads();
+        if (br + 1 < br1) issue(br + 1);
+        const bf16_t* arow = ds + (wco * 16 + l16) * a.csd;
+        const bf16_t* xrow = xs + (wci * 16 + l16) * a.cs;
+        int ox0 = (8 * g) % a.BO[2], oy = ((8 * g) / a.BO[2]) % a.BO[1], oz = (8 * g) / (a.BO[2] * a.BO[1]);
+        for (int ks = 0; ks < bov / 32; ++ks) {
+            const int f0 = ks * 32 + 8 * g;
+            if (ks > 0) {
+                ox0 += 32;
+                while (ox0 >= a.BO[2]) {
+                    ox0 -= a.BO[2];
+                    if (++oy == a.BO[1]) {
+                        oy = 0;
+                        ++oz;
+                    }
+                }
+            }
+            const uint4 av = *reinterpret_cast<const uint4*>(arow + f0);
+            // input rows (kd, kh) of the K step, read LA rows ahead of their MFMAs
+            constexpr int R = KDG * K1, LA = R < 3 ? R : 3;
+            const bf16_t* src0 = xrow + ((oz * a.S[0]) * a.biy + oy * a.S[1]) * a.bixp + ox0;
+            auto row_ptr = [&](int r) { return src0 + ((r / K1) * a.biy + (r % K1)) * a.bixp; };
+            uint4 rb0[LA], rb1[LA];
+#pragma unroll
+            for (int r = 0; r < LA; ++r) {
+                rb0[r] = *reinterpret_cast<const uint4*>(row_ptr(r));
+                rb1[r] = K2 > 1 ? *reinterpret_cast<const uint4*>(row_ptr(r) + 8) : rb0[r];
+            }
+#pragma unroll
+            for (int kd = 0; kd < KDG; ++kd) {
+#pragma unroll
+                for (int kh = 0; kh < K1; ++kh) {
+                    const int r = kd * K1 + kh;
+                    const uint4 b0 = rb0[r % LA];
+                    const uint4 b1 = rb1[r % LA];
+                    if (r + LA < R) {
+                        rb0[r % LA] = *reinterpret_cast<const uint4*>(row_ptr(r + LA));
+                        rb1[r % LA] = K2 > 1 ? *reinterpret_cast<const uint4*>(row_ptr(r + LA) + 8) : rb0[r % LA];
+                    }
+#pragma unroll
+                    for (int kw = 0; kw < K2; ++kw) {
+                        uint4 bv;
+                        if (kw == 0) bv = funnel<0>(b0, b1);
+                        else if (kw == 1) bv = funnel<1>(b0, b1);
+                        else if (kw == 2) bv = funnel<2>(b0, b1);
+                        else if (kw == 3) bv = funnel<3>(b0, b1);
+                        else if (kw == 4) bv = funnel<4>(b0, b1);
+                        else if (kw == 5) bv = funnel<5>(b0, b1);
+                        else if (kw == 6) bv = funnel<6>(b0, b1);
+                        else bv = funnel<7>(b0, b1);
+                        const int ti = (kd * K1 + kh) * K2 + kw;
+                        acc[ti] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_w, av),
+                                                                          __builtin_bit_cast(bf16x8_w, bv), acc[ti],
+                                                                          0, 0, 0);
+                    }
+                }
+            }
+        }
+    }
+    float4* out = reinterpret_cast<float4*>(a.part +
+                                            ((((split * a.nmb + mb) * a.ncb + cb) * a.ntg + tg) * int64_t(a.blk)) +
+                                            int64_t(wave) * TG * 256);
+#pragma unroll
+    for (int i = 0; i < TG; ++i) out[i * 64 + lane] = make_float4(acc[i][0], acc[i][1], acc[i][2], acc[i][3]);
+}
+
 template <int TPW>
 __global__ __launch_bounds__(kThreads, 2) void wgrad_f32_tiled(WgArgs a)
 {
@@ -417,6 +630,187 @@ __global__ __launch_bounds__(kThreads, 2) void wgrad_f32_tiled(WgArgs a)
                 const float bv = xs[(vin + toff[i]) * 32 + l32];
                 acc[i] = __builtin_amdgcn_mfma_f32_32x32x2f32(av, bv, acc[i], 0, 0, 0);
             }
+        }
+    }
+    float4* out = reinterpret_cast<float4*>(a.part + (((split * a.nmb + mb) * a.ncb + cb) * a.ntg + tg) * int64_t(a.blk) +
+                                            int64_t(wave) * TPW * 1024);
+#pragma unroll
+    for (int i = 0; i < TPW; ++i)
+#pragma unroll
+        for (int r4 = 0; r4 < 4; ++r4)
+            out[(i * 64 + lane) * 4 + r4] =
+                make_float4(acc[i][4 * r4], acc[i][4 * r4 + 1], acc[i][4 * r4 + 2], acc[i][4 * r4 + 3]);
+}
+
+// fp32 with direct global->LDS loads: the staging of a brick is one 16-byte
+// buffer load per thread and 4 KiB of LDS (unit u = thread + 256 i is float4 u
+// of the input copy: voxel u / 8, channels 4 (u % 8) ..), written by the load
+// itself with no register copy and no LDS store instruction; an offset past
+// the buffer (a voxel outside the tile, a unit past the brick) loads zeros.
+// Each thread's unit coordinates inside a brick are the same for every brick,
+// so they are packed into registers once. The K steps run as a software
+// pipeline (the operands of step ks + 1 are read while the MFMAs of step ks
+// run, every tap slot multiplies, no branch). Two workgroups per compute unit
+// alternate between loading and multiplying. Same bricks, K steps and taps as
+// wgrad_f32_tiled, in the same order: the partials are bit-identical.
+constexpr int kDlXU = 20;    // input load instructions per thread (80 KiB)
+constexpr int kDlDU = 3;     // dy load instructions per thread (bricks of <= 64 outputs)
+constexpr int kDlTab = 66;   // entries of the per-voxel input offset table
+
+__host__ __device__ inline int dl_round(int units) { return (units + kThreads - 1) / kThreads * kThreads; }
+
+struct DlLayout {
+    int dy_off, tab_off, bytes;
+};
+
+inline DlLayout dl_layout(const WgArgs& a)
+{
+    const int biv = a.biz * a.biy * a.bix;
+    const int bov = a.BO[0] * a.BO[1] * a.BO[2];
+    DlLayout L;
+    L.dy_off = dl_round(biv * 8) * 16;
+    L.tab_off = L.dy_off + dl_round((bov + (bov & 1)) * 8) * 16;
+    L.bytes = L.tab_off + kDlTab * 4;
+    return L;
+}
+
+template <int TPW>
+__global__ __launch_bounds__(kThreads, 2) void wgrad_f32_dl(WgArgs a, int dy_off, int tab_off, uint32_t xbatch,
+                                                            uint32_t dbatch)
+{
+    extern __shared__ uint4 lds4[];
+    char* lds = reinterpret_cast<char*>(lds4);
+    const float* xs = reinterpret_cast<const float*>(lds);
+    const float* ds = reinterpret_cast<const float*>(lds + dy_off);
+    int* vtab = reinterpret_cast<int*>(lds + tab_off);
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = tid >> 6;
+    const int g = lane >> 5;
+    const int l32 = lane & 31;
+
+    int64_t b = xcd_remap(blockIdx.x, a.nblocks);
+    const int tg = int(b % a.ntg);
+    b /= a.ntg;
+    const int cb = int(b % a.ncb);
+    b /= a.ncb;
+    const int mb = int(b % a.nmb);
+    const int64_t split = b / a.nmb;
+    const int64_t br0 = split * a.nbricks / a.nsplit, br1 = (split + 1) * a.nbricks / a.nsplit;
+    const int co0 = mb * 32, ci0 = cb * 32;
+    const int taps = a.K[0] * a.K[1] * a.K[2];
+    const int bov = a.BO[0] * a.BO[1] * a.BO[2];
+    const int bove = bov + (bov & 1);
+    const int biv = a.biz * a.biy * a.bix;
+    const int nxi = dl_round(biv * 8) / kThreads, ndi = dl_round(bove * 8) / kThreads;
+
+    // tap slots past the last tap multiply tap 0's operands (no branch in the
+    // MFMA sequence); the reduction never reads their partials
+    int toff[TPW];
+#pragma unroll
+    for (int i = 0; i < TPW; ++i) {
+        const int tl = wave + 4 * i;
+        const int t = tg * a.kdg + tl;
+        const int tt = (tl < a.kdg && t < taps) ? t : 0;
+        const int kw = tt % a.K[2], kh = (tt / a.K[2]) % a.K[1], kd = tt / (a.K[2] * a.K[1]);
+        toff[i] = ((kd * a.biy + kh) * a.bix + kw) * 32 + l32;
+    }
+    f32x16_w acc[TPW];
+#pragma unroll
+    for (int i = 0; i < TPW; ++i)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) acc[i][r] = 0.f;
+
+    // the thread's units: voxel (z, y, x) of the input brick packed as
+    // z << 20 | y << 10 | x, output voxel (oz, oy, ox) of the dy brick likewise;
+    // -1 for a unit past the brick
+    const int q = tid & 7;
+    int px[kDlXU], pd[kDlDU];
+#pragma unroll
+    for (int i = 0; i < kDlXU; ++i) {
+        const int v = (tid + i * kThreads) >> 3;
+        const int x = v % a.bix, r = v / a.bix;
+        px[i] = v < biv ? (((r / a.biy) << 20) | ((r % a.biy) << 10) | x) : -1;
+    }
+#pragma unroll
+    for (int i = 0; i < kDlDU; ++i) {
+        const int f = (tid + i * kThreads) >> 3;
+        const int ox = f % a.BO[2], oy = (f / a.BO[2]) % a.BO[1], oz = f / (a.BO[2] * a.BO[1]);
+        pd[i] = f < bov ? ((oz << 20) | (oy << 10) | ox) : -1;
+    }
+    for (int f = tid; f < bove; f += kThreads) {
+        const int ox = f % a.BO[2], oy = (f / a.BO[2]) % a.BO[1], oz = f / (a.BO[2] * a.BO[1]);
+        vtab[f] = f < bov ? ((oz * a.S[0] * a.biy + oy * a.S[1]) * a.bix + ox * a.S[2]) * 32 : 0;
+    }
+    const int P0 = int(a.P[0]), P1 = int(a.P[1]), P2 = int(a.P[2]);
+    const int O0 = int(a.O[0]), O1 = int(a.O[1]), O2 = int(a.O[2]);
+    const int cin = int(a.cin), cout = int(a.cout);
+    const bool cok = ci0 + 4 * q < cin, dok = co0 + 4 * q < cout;
+    constexpr uint32_t kOut = 0xFFFFFFF0u;  // past every buffer: loads zeros
+
+    for (int64_t br = br0; br < br1; ++br) {
+        int64_t nn, ob[3];
+        brick_origin(a, br, nn, ob);
+        const int i0 = int(ob[0] * a.S[0] - a.pad[0]), i1 = int(ob[1] * a.S[1] - a.pad[1]),
+                  i2 = int(ob[2] * a.S[2] - a.pad[2]);
+        __syncthreads();  // every wave is done reading the previous brick
+        const __amdgpu_buffer_rsrc_t rx = __builtin_amdgcn_make_buffer_rsrc(
+            const_cast<char*>(a.tile) + int64_t(nn) * xbatch, short(0), int(xbatch), 0x00020000);
+        const __amdgpu_buffer_rsrc_t rd = __builtin_amdgcn_make_buffer_rsrc(
+            const_cast<char*>(a.dy) + int64_t(nn) * dbatch, short(0), int(dbatch), 0x00020000);
+#pragma unroll
+        for (int i = 0; i < kDlXU; ++i) {
+            if (i < nxi) {
+                const int c = px[i];
+                const int t0 = i0 + (c >> 20), t1 = i1 + ((c >> 10) & 1023), t2 = i2 + (c & 1023);
+                const bool ok = c >= 0 && cok && uint32_t(t0) < uint32_t(P0) && uint32_t(t1) < uint32_t(P1) &&
+                                uint32_t(t2) < uint32_t(P2);
+                const uint32_t off = ((uint32_t(t0 * P1 + t1) * uint32_t(P2) + uint32_t(t2)) * uint32_t(cin) +
+                                      uint32_t(ci0 + 4 * q)) * 4u;
+                __builtin_amdgcn_raw_ptr_buffer_load_lds(rx, SC_LDSW(lds + i * 4096 + wave * 1024), 16,
+                                                         ok ? off : kOut, 0, 0, 0);
+            }
+        }
+#pragma unroll
+        for (int i = 0; i < kDlDU; ++i) {
+            if (i < ndi) {
+                const int c = pd[i];
+                const int o0 = int(ob[0]) + (c >> 20), o1 = int(ob[1]) + ((c >> 10) & 1023),
+                          o2 = int(ob[2]) + (c & 1023);
+                const bool ok = c >= 0 && dok && o0 < O0 && o1 < O1 && o2 < O2;
+                const uint32_t off = ((uint32_t(o0 * O1 + o1) * uint32_t(O2) + uint32_t(o2)) * uint32_t(cout) +
+                                      uint32_t(co0 + 4 * q)) * 4u;
+                __builtin_amdgcn_raw_ptr_buffer_load_lds(rd, SC_LDSW(lds + dy_off + i * 4096 + wave * 1024), 16,
+                                                         ok ? off : kOut, 0, 0, 0);
+            }
+        }
+        wait_vm_barrier<0>();  // the brick's loads have landed, for every wave
+        // software pipeline over the K steps: the operands of step ks + 1 and the
+        // input offset of step ks + 2 are read while the MFMAs of step ks run
+        const int nks = bove / 2;
+        float av = ds[g * 32 + l32];
+        float bv[TPW];
+        {
+            const int v0 = vtab[g];
+#pragma unroll
+            for (int i = 0; i < TPW; ++i) bv[i] = xs[v0 + toff[i]];
+        }
+        int vin1 = nks > 1 ? vtab[2 + g] : 0;
+        for (int ks = 0; ks < nks; ++ks) {
+            float avn = 0.f, bvn[TPW];
+            int vin2 = 0;
+            if (ks + 1 < nks) {
+                avn = ds[(2 * ks + 2 + g) * 32 + l32];
+#pragma unroll
+                for (int i = 0; i < TPW; ++i) bvn[i] = xs[vin1 + toff[i]];
+                if (ks + 2 < nks) vin2 = vtab[2 * ks + 4 + g];
+            }
+#pragma unroll
+            for (int i = 0; i < TPW; ++i) acc[i] = __builtin_amdgcn_mfma_f32_32x32x2f32(av, bv[i], acc[i], 0, 0, 0);
+            av = avn;
+#pragma unroll
+            for (int i = 0; i < TPW; ++i) bv[i] = bvn[i];
+            vin1 = vin2;
         }
     }
     float4* out = reinterpret_cast<float4*>(a.part + (((split * a.nmb + mb) * a.ncb + cb) * a.ntg + tg) * int64_t(a.blk) +
@@ -629,13 +1023,69 @@ size_t tiled_workspace(const PlanW& pl)
 template <typename K>
 hipError_t launch_with_lds(K fn, const PlanW& pl, hipStream_t s)
 {
+    const size_t lds = pl.lds;
     hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(fn), hipFuncAttributeMaxDynamicSharedMemorySize,
-                                       int(pl.lds));
+                                       int(lds));
     if (e != hipSuccess) return e;
     WgArgs a = pl.a;
     void* args[] = {&a};
-    return hipLaunchKernel(reinterpret_cast<const void*>(fn), dim3(unsigned(a.nblocks)), dim3(kThreads), args, pl.lds,
-                           s);
+    return hipLaunchKernel(reinterpret_cast<const void*>(fn), dim3(unsigned(a.nblocks)), dim3(kThreads), args, lds, s);
+}
+
+// The pipelined bf16 kernel takes 16-byte loads of every 8-channel group and at
+// most kPipeBXU / kPipeBDU staging units per thread.
+bool bf16_pipe_ok(const PlanW& pl)
+{
+    const WgArgs& a = pl.a;
+    const int nci = (4 / pl.wco) * 16, nco = pl.wco * 16;
+    const int64_t bov = int64_t(a.BO[0]) * a.BO[1] * a.BO[2];
+    const int64_t nxu = int64_t(a.biz) * a.biy * ((a.bix + 3) / 4) * (nci / 8);
+    const int64_t ndu = (bov / 4) * (nco / 8);
+    return a.xvec && a.dvec && a.cin % 8 == 0 && a.cout % 8 == 0 && bov % 4 == 0 && a.BO[2] % 4 == 0 &&
+           nxu <= int64_t(kPipeBXU) * kThreads && ndu <= int64_t(kPipeBDU) * kThreads;
+}
+
+template <int KDG, int K1, int K2, int WCO>
+hipError_t launch_bf16_t(const PlanW& pl, hipStream_t s)
+{
+    if (!bf16_pipe_ok(pl)) return launch_with_lds(&wgrad_bf16_tiled<KDG, K1, K2, WCO>, pl, s);
+    const WgArgs& a = pl.a;
+    const int64_t nxu = int64_t(a.biz) * a.biy * ((a.bix + 3) / 4) * ((4 / WCO) * 2);
+    const int64_t ndu = int64_t(a.BO[0]) * a.BO[1] * a.BO[2] / 4 * (WCO * 2);
+    const bool x1 = nxu <= kThreads, d1 = ndu <= kThreads;
+    if (x1 && d1) return launch_with_lds(&wgrad_bf16_pipe<KDG, K1, K2, WCO, 1, 1>, pl, s);
+    if (x1) return launch_with_lds(&wgrad_bf16_pipe<KDG, K1, K2, WCO, 1, 2>, pl, s);
+    if (d1) return launch_with_lds(&wgrad_bf16_pipe<KDG, K1, K2, WCO, 2, 1>, pl, s);
+    // two units of each would not fit the registers of two waves per SIMD
+    return launch_with_lds(&wgrad_bf16_tiled<KDG, K1, K2, WCO>, pl, s);
+}
+
+// The direct-load fp32 kernel: no folded halo (a load instruction has one
+// source buffer), 16-byte aligned channel groups, tile and dy of < 4 GiB per
+// batch item (32-bit offsets), brick extents below 1024, staging within its
+// instruction budget and two workgroups' LDS per compute unit.
+hipError_t launch_f32(const Tile3& t, const Conv3& cv, const PlanW& pl, hipStream_t s)
+{
+    const WgArgs& a = pl.a;
+    const int64_t xb = t.P[0] * t.P[1] * t.P[2] * t.c * 4, db = cv.O[0] * cv.O[1] * cv.O[2] * cv.cout * 4;
+    const DlLayout L = dl_layout(a);
+    const int64_t bov = int64_t(a.BO[0]) * a.BO[1] * a.BO[2];
+    const bool dl = !a.fold.mask && a.xvec && a.dvec && t.c % 4 == 0 && cv.cout % 4 == 0 && xb < (int64_t(1) << 32) - 64 &&
+                    db < (int64_t(1) << 32) - 64 && a.biz < 1024 && a.biy < 1024 && a.bix < 1024 &&
+                    dl_round(a.biz * a.biy * a.bix * 8) <= kDlXU * kThreads &&
+                    dl_round(int(bov + (bov & 1)) * 8) <= kDlDU * kThreads && bov + 1 <= kDlTab &&
+                    L.bytes <= 80 * 1024;
+    if (!dl) return launch_with_lds(&wgrad_f32_tiled<7>, pl, s);
+    auto fn = &wgrad_f32_dl<7>;
+    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(fn), hipFuncAttributeMaxDynamicSharedMemorySize,
+                                       L.bytes);
+    if (e != hipSuccess) return e;
+    WgArgs aa = a;
+    int dyo = L.dy_off, tabo = L.tab_off;
+    uint32_t xbu = uint32_t(xb), dbu = uint32_t(db);
+    void* args[] = {&aa, &dyo, &tabo, &xbu, &dbu};
+    return hipLaunchKernel(reinterpret_cast<const void*>(fn), dim3(unsigned(aa.nblocks)), dim3(kThreads), args,
+                           size_t(L.bytes), s);
 }
 
 hipError_t launch_bf16(const PlanW& pl, hipStream_t s)
@@ -643,22 +1093,22 @@ hipError_t launch_bf16(const PlanW& pl, hipStream_t s)
     const int k = pl.kdg * 100 + pl.k1 * 10 + pl.k2;
     if (pl.wco == 2) {
         switch (k) {
-        case 333: return launch_with_lds(&wgrad_bf16_tiled<3, 3, 3, 2>, pl, s);
-        case 133: return launch_with_lds(&wgrad_bf16_tiled<1, 3, 3, 2>, pl, s);
-        case 155: return launch_with_lds(&wgrad_bf16_tiled<1, 5, 5, 2>, pl, s);
-        case 111: return launch_with_lds(&wgrad_bf16_tiled<1, 1, 1, 2>, pl, s);
-        case 113: return launch_with_lds(&wgrad_bf16_tiled<1, 1, 3, 2>, pl, s);
-        case 115: return launch_with_lds(&wgrad_bf16_tiled<1, 1, 5, 2>, pl, s);
+        case 333: return launch_bf16_t<3, 3, 3, 2>(pl, s);
+        case 133: return launch_bf16_t<1, 3, 3, 2>(pl, s);
+        case 155: return launch_bf16_t<1, 5, 5, 2>(pl, s);
+        case 111: return launch_bf16_t<1, 1, 1, 2>(pl, s);
+        case 113: return launch_bf16_t<1, 1, 3, 2>(pl, s);
+        case 115: return launch_bf16_t<1, 1, 5, 2>(pl, s);
         default: break;
         }
     } else {
         switch (k) {
-        case 333: return launch_with_lds(&wgrad_bf16_tiled<3, 3, 3, 4>, pl, s);
-        case 133: return launch_with_lds(&wgrad_bf16_tiled<1, 3, 3, 4>, pl, s);
-        case 155: return launch_with_lds(&wgrad_bf16_tiled<1, 5, 5, 4>, pl, s);
-        case 111: return launch_with_lds(&wgrad_bf16_tiled<1, 1, 1, 4>, pl, s);
-        case 113: return launch_with_lds(&wgrad_bf16_tiled<1, 1, 3, 4>, pl, s);
-        case 115: return launch_with_lds(&wgrad_bf16_tiled<1, 1, 5, 4>, pl, s);
+        case 333: return launch_bf16_t<3, 3, 3, 4>(pl, s);
+        case 133: return launch_bf16_t<1, 3, 3, 4>(pl, s);
+        case 155: return launch_bf16_t<1, 5, 5, 4>(pl, s);
+        case 111: return launch_bf16_t<1, 1, 1, 4>(pl, s);
+        case 113: return launch_bf16_t<1, 1, 3, 4>(pl, s);
+        case 115: return launch_bf16_t<1, 1, 5, 4>(pl, s);
         default: break;
         }
     }
@@ -741,7 +1191,7 @@ hipError_t run_wgrad(const Tile3& t, const Conv3& cv, shard_dtype_t dt, const vo
     pl.a.dvec = (reinterpret_cast<uintptr_t>(dy) % 16 == 0) && (cv.cout * esz) % 16 == 0;
     pl.a.part = static_cast<float*>(ws);
     pl.a.dw = dw;
-    hipError_t e = pl.kind == 1 ? launch_bf16(pl, s) : launch_with_lds(&wgrad_f32_tiled<7>, pl, s);
+    hipError_t e = pl.kind == 1 ? launch_bf16(pl, s) : launch_f32(t, cv, pl, s);
     if (e != hipSuccess) return e;
     const int64_t total = int64_t(pl.a.nmb) * pl.a.ncb * pl.a.ntg * pl.a.blk;
     const unsigned grid = unsigned(std::max<int64_t>(1, std::min<int64_t>(ceil_div(total, 256), 1 << 16)));
