@@ -230,6 +230,9 @@ def main():
                                                      for k in range(args.steps)])))
     log("timed region done")
 
+    # the halo launches again, cold: 8 launches on 8 rotating buffer sets
+    cold = time_halo_cold(sc, w, desc, tile, ops, send, recv, args, stream)
+
     next_rows = None
     if not args.no_backward:
         next_rows = time_backward(sc, w, g, desc, wt, dy, send, flops, args, stream)
@@ -244,10 +247,20 @@ def main():
         if kind in ("fwd", "wgrad"):
             tf = work / (ms * 1e-3) / 1e12
             detail[label] = {"ms": round(ms, 4), "tflops": round(tf, 2), "frac_mfma_peak": round(tf / PEAK[dt], 4)}
+            ctr = measured_counters(label, args.workload)
+            if ctr:
+                detail[label]["mfma_busy_frac"] = ctr["mfma_busy_frac"]
+                detail[label]["counters"] = ctr
         else:
-            gbs = work / (ms * 1e-3) / 1e9
-            detail[label] = {"ms": round(ms, 4), "gbs": round(gbs, 1), "frac_hbm_peak": round(gbs / HBM_PEAK, 4),
-                             "bytes": int(work)}
+            # the gated figures are the cold ones; the launch inside the step
+            # (event pair around one launch, caches as the step left them) beside them
+            cms = cold[label]
+            gbs = work / (cms * 1e-3) / 1e9
+            detail[label] = {"ms": round(cms, 4), "gbs": round(gbs, 1), "frac_hbm_peak": round(gbs / HBM_PEAK, 4),
+                             "bytes": int(work), "in_step_ms": round(ms, 4),
+                             "protocol": "cold: 8 consecutive launches on 8 buffer sets (tile and slabs, 8 x the bytes "
+                                         "> the 256 MB last-level cache) between one event pair, per launch; "
+                                         "median of the repeats"}
     dom = max(("conv_fwd", "conv_wgrad"), key=lambda k: per_op[k][2])
     ach = per_op[dom][1] / (per_op[dom][2] * 1e-3) / 1e12
     roofline = {"kernel": dom, "bound": "mfma", "achieved": round(ach, 2), "peak": PEAK[dt], "unit": "TFLOP/s",
@@ -272,6 +285,60 @@ def main():
         "next_rows": next_rows,
     }
     print(json.dumps(line), flush=True)
+
+
+def time_halo_cold(sc, w, desc, tile, ops, send, recv, args, stream):
+    """Per-launch time of every halo op of the step on cold data: 8 copies of
+    the tile and of every slab, used in turn by 8 consecutive launches between
+    one event pair (each set was last touched 7 launches earlier, 7 x its bytes
+    ago: more than the last-level cache holds at the workloads' sizes), median
+    over `steps` repeats. One event pair over 8 launches also amortises the
+    event overhead, so the figure is close to the kernel time."""
+    import numpy as np
+    import torch
+    NS = 8
+    halo = [(label, kind) for (label, kind, _, _) in ops if kind in ("pack", "unpack")]
+    if not halo:
+        return {}
+    tiles = [tile] + [tile.clone() for _ in range(NS - 1)]
+    out = {}
+    for label, kind in halo:
+        axis = int(label.split("_a")[1])
+        calls = []
+        for k in range(NS):
+            if kind == "pack":
+                sends = {side: (nwidth, buf) for (a_, side, nwidth, buf, _) in send if a_ == axis}
+                wl, bl = sends.get(0, (0, None))
+                wh, bh = sends.get(1, (0, None))
+                bl = torch.empty_like(bl) if bl is not None else None
+                bh = torch.empty_like(bh) if bh is not None else None
+                calls.append(lambda t=tiles[k], wl=wl, bl=bl, wh=wh, bh=bh:
+                             sc.shard_halo_pack_pair(desc, t, axis, wl, bl, wh, bh))
+            else:
+                rv = {side: slab for (a_, side, slab, _) in recv if a_ == axis}
+                sl = rv.get(0)
+                sh = rv.get(1)
+                sl = sl.clone() if sl is not None else None
+                sh = sh.clone() if sh is not None else None
+                calls.append(lambda t=tiles[k], sl=sl, sh=sh: sc.shard_halo_unpack_pair(desc, t, axis, sl, sh))
+        for c in calls:
+            c()
+        torch.cuda.synchronize()
+        times = []
+        for _ in range(max(3, args.steps)):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            for c in calls:
+                c()
+            e1.record(stream)
+            torch.cuda.synchronize()
+            times.append(e0.elapsed_time(e1) / NS)
+        out[label] = float(np.median(times))
+        del calls
+    del tiles
+    torch.cuda.empty_cache()
+    log("cold halo launches timed")
+    return out
 
 
 def time_backward(sc, w, g, desc, wt, dy, send, flops, args, stream):
@@ -549,6 +616,35 @@ def source_hash(op):
         with open(f, "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()
+
+
+def measured_counters(op, workload):
+    """Matrix-core utilisation of `op`'s main kernel from the committed counter
+    summary (rocprofv3 --pmc: SQ_VALU_MFMA_BUSY_CYCLES over the SIMD cycles the
+    kernel ran, at the clock it ran at), or None when there is none or the
+    kernel sources changed since it was taken."""
+    path = os.path.join(ROOT, "profiles", f"{op}_{workload}_counters.txt")
+    if not os.path.exists(path):
+        return None
+    rec = {}
+    with open(path) as fh:
+        for line in fh:
+            if ":" in line and not line.startswith("#"):
+                k, v = line.split(":", 1)
+                rec[k.strip()] = v.strip()
+    if rec.get("source_sha256") != source_hash(op):
+        return None
+    out = {}
+    for k in ("mfma_busy_frac", "valu_per_mfma", "salu_per_mfma", "lds_bank_conflict_per_lds_cycle", "clock_mhz"):
+        try:
+            out[k] = float(rec[k])
+        except (KeyError, ValueError):
+            pass
+    if "mfma_busy_frac" not in out:
+        return None
+    out["kernel"] = rec.get("kernel")
+    out["source"] = f"profiles/{op}_{workload}_counters.txt"
+    return out
 
 
 def measured_traffic(op, workload):
