@@ -40,6 +40,9 @@ namespace {
 constexpr int kThreads = 256;
 constexpr int kTargetBlocks = 512;  // two resident workgroups per CU on 256 CUs
 
+// staging units rounded up to whole load instructions of the workgroup
+__host__ __device__ inline int dl_round(int units) { return (units + kThreads - 1) / kThreads * kThreads; }
+
 struct WgArgs {
     const char* tile;
     const char* dy;
@@ -492,6 +495,212 @@ __global__ __launch_bounds__(kThreads, 2) void wgrad_bf16_pipe(WgArgs a)
     for (int i = 0; i < TG; ++i) out[i * 64 + lane] = make_float4(acc[i][0], acc[i][1], acc[i][2], acc[i][3]);
 }
 
+// bf16, 16 input channels, one kd plane of taps per workgroup (the general
+// kernel's decomposition for large 3D kernels such as 5 x 5 x 5), without any
+// transposition while staging: the brick's input rows and dy are copied to LDS
+// channels-last by direct global->LDS loads, and every operand is read with
+// ds_read_b64_tr_b16 (within each 16-lane group, lane i addresses voxel
+// row k0 + i/4 at channels 4 (i % 4) ..; lane j receives channel j of voxels
+// k0 .. k0 + 3). v_mfma_f32_16x16x32_bf16: M = 16 output channels (wave w owns
+// channels 16 w ..), N = the 16 input channels, K = 32 output voxels, lane
+// group g = lane / 16 holding voxels 8 g .. 8 g + 7 of the K step.
+//  * A (dy): two reads of four voxels.
+//  * B (input row (kd, kh)): three reads give the lane 12 consecutive voxels
+//    8 g .. 8 g + 11 of its channel; the operand of tap kw is the window
+//    kw .. kw + 7 (dword aligned for even kw, one v_alignbit per dword for odd).
+// LDS layouts (16-byte units written by the loads, swizzled through the
+// lane -> source mapping so that the reads hit distinct banks):
+//  * input: voxel v of the brick (row pitch bixp8, a multiple of 8) at 32-byte
+//    slot v ^ (((v >> 3) & 1) << 2);
+//  * dy: voxel f at 128 f, its 32-byte channel chunk k at chunk
+//    k ^ (((f >> 1) & 1) | (((f >> 3) & 1) << 1)).
+// Bricks, K steps, taps and the partial layout are those of wgrad_bf16_tiled
+// with 4 waves of 16 output channels: the partials are bit-identical.
+constexpr int kTrXU = 8;   // input load instructions per thread
+constexpr int kTrDU = 8;   // dy load instructions per thread
+
+struct TrLayout {
+    int bixp8, dy_off, bytes;
+};
+
+inline TrLayout tr_layout(const WgArgs& a)
+{
+    TrLayout L;
+    L.bixp8 = (a.bix + 7) / 8 * 8;
+    const int xunits = a.biz * a.biy * L.bixp8 * 2;
+    const int bov = a.BO[0] * a.BO[1] * a.BO[2];
+    L.dy_off = dl_round(xunits) * 16;
+    L.bytes = L.dy_off + dl_round(bov * 8) * 16;
+    return L;
+}
+
+__device__ __forceinline__ int tr_xslot(int v) { return v ^ (((v >> 3) & 1) << 2); }
+__device__ __forceinline__ int tr_dswz(int f) { return ((f >> 1) & 1) | (((f >> 3) & 1) << 1); }
+
+template <int K1, int K2>
+__global__ __launch_bounds__(kThreads, 2) void wgrad_bf16_dl(WgArgs a, int bixp8, int dy_off, uint32_t xbatch,
+                                                             uint32_t dbatch)
+{
+    static_assert(K2 <= 5, "a 12-voxel run covers five W taps");
+    constexpr int TG = K1 * K2;
+    extern __shared__ uint4 lds4[];
+    char* lds = reinterpret_cast<char*>(lds4);
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = tid >> 6;
+    const int g = lane >> 4;
+    const int li = lane & 15;
+
+    int64_t b = xcd_remap(blockIdx.x, a.nblocks);
+    const int tg = int(b % a.ntg);
+    b /= a.ntg;
+    b /= a.ncb;  // a single block of 16 input channels
+    const int mb = int(b % a.nmb);
+    const int64_t split = b / a.nmb;
+    const int64_t br0 = split * a.nbricks / a.nsplit, br1 = (split + 1) * a.nbricks / a.nsplit;
+    const int kd0 = tg;
+    const int co0 = mb * 64;
+    const int bov = a.BO[0] * a.BO[1] * a.BO[2];
+    const int nxv = a.biz * a.biy * bixp8;
+    const int nxi = dl_round(nxv * 2) / kThreads, ndi = dl_round(bov * 8) / kThreads;
+
+    // the thread's load units, brick invariant. Input: slot s = 32-byte voxel
+    // slot s >> 1 (voxel v = its swizzle inverse), half h = s & 1 (channels
+    // 8 h ..); packed z << 20 | y << 10 | x << 1 | h, -1 past the row or brick.
+    // dy: slot s = voxel f = s >> 3, 16-byte unit p = s & 7 of its 128 bytes,
+    // holding global unit q = p ^ 2 swz(f) (channels 8 q ..); packed
+    // oz << 22 | oy << 12 | ox << 3 | q.
+    int px[kTrXU], pd[kTrDU];
+#pragma unroll
+    for (int i = 0; i < kTrXU; ++i) {
+        const int sl = tid + i * kThreads;
+        const int v = tr_xslot(sl >> 1), h = sl & 1;
+        const int x = v % bixp8, r = v / bixp8;
+        px[i] = (v < nxv && x < a.bix) ? (((r / a.biy) << 20) | ((r % a.biy) << 10) | (x << 1) | h) : -1;
+    }
+#pragma unroll
+    for (int i = 0; i < kTrDU; ++i) {
+        const int sl = tid + i * kThreads;
+        const int f = sl >> 3, q = (sl & 7) ^ (2 * tr_dswz(f));
+        const int ox = f % a.BO[2], oy = (f / a.BO[2]) % a.BO[1], oz = f / (a.BO[2] * a.BO[1]);
+        pd[i] = f < bov ? ((oz << 22) | (oy << 12) | (ox << 3) | q) : -1;
+    }
+    const int P0 = int(a.P[0]), P1 = int(a.P[1]), P2 = int(a.P[2]);
+    const int O0 = int(a.O[0]), O1 = int(a.O[1]), O2 = int(a.O[2]);
+    const int cout = int(a.cout);
+    constexpr uint32_t kOut = 0xFFFFFFF0u;
+
+    f32x4_w acc[TG];
+#pragma unroll
+    for (int i = 0; i < TG; ++i) acc[i] = f32x4_w{0.f, 0.f, 0.f, 0.f};
+
+    const uint32_t lds0 = lds_addr(lds);
+    const uint32_t colb = uint32_t((li & 3) * 8);
+    for (int64_t br = br0; br < br1; ++br) {
+        int64_t nn, ob[3];
+        brick_origin(a, br, nn, ob);
+        const int i0 = int(ob[0]) * a.S[0] + kd0 - a.pad[0], i1 = int(ob[1]) * a.S[1] - a.pad[1],
+                  i2 = int(ob[2]) - a.pad[2];
+        __syncthreads();  // every wave is done reading the previous brick
+        const __amdgpu_buffer_rsrc_t rx = __builtin_amdgcn_make_buffer_rsrc(
+            const_cast<char*>(a.tile) + int64_t(nn) * xbatch, short(0), int(xbatch), 0x00020000);
+        const __amdgpu_buffer_rsrc_t rd = __builtin_amdgcn_make_buffer_rsrc(
+            const_cast<char*>(a.dy) + int64_t(nn) * dbatch, short(0), int(dbatch), 0x00020000);
+#pragma unroll
+        for (int i = 0; i < kTrXU; ++i) {
+            if (i < nxi) {
+                const int c = px[i];
+                const int t0 = i0 + (c >> 20), t1 = i1 + ((c >> 10) & 1023), t2 = i2 + ((c >> 1) & 511);
+                const bool ok = c >= 0 && uint32_t(t0) < uint32_t(P0) && uint32_t(t1) < uint32_t(P1) &&
+                                uint32_t(t2) < uint32_t(P2);
+                const uint32_t off = ((uint32_t(t0 * P1 + t1) * uint32_t(P2) + uint32_t(t2)) * 16u +
+                                      uint32_t(8 * (c & 1))) * 2u;
+                __builtin_amdgcn_raw_ptr_buffer_load_lds(rx, SC_LDSW(lds + i * 4096 + wave * 1024), 16,
+                                                         ok ? off : kOut, 0, 0, 0);
+            }
+        }
+#pragma unroll
+        for (int i = 0; i < kTrDU; ++i) {
+            if (i < ndi) {
+                const int c = pd[i];
+                const int o0 = int(ob[0]) + (c >> 22), o1 = int(ob[1]) + ((c >> 12) & 1023),
+                          o2 = int(ob[2]) + ((c >> 3) & 511);
+                const bool ok = c >= 0 && o0 < O0 && o1 < O1 && o2 < O2;
+                const uint32_t off = ((uint32_t(o0 * O1 + o1) * uint32_t(O2) + uint32_t(o2)) * uint32_t(cout) +
+                                      uint32_t(co0 + 8 * (c & 7))) * 2u;
+                __builtin_amdgcn_raw_ptr_buffer_load_lds(rd, SC_LDSW(lds + dy_off + i * 4096 + wave * 1024), 16,
+                                                         ok ? off : kOut, 0, 0, 0);
+            }
+        }
+        wait_vm_barrier<0>();  // the brick's loads have landed, for every wave
+
+        int ox0 = (8 * g) % a.BO[2], oy = ((8 * g) / a.BO[2]) % a.BO[1], oz = (8 * g) / (a.BO[2] * a.BO[1]);
+        for (int ks = 0; ks < bov / 32; ++ks) {
+            const int f0 = ks * 32 + 8 * g;
+            if (ks > 0) {
+                ox0 += 32;
+                while (ox0 >= a.BO[2]) {
+                    ox0 -= a.BO[2];
+                    if (++oy == a.BO[1]) {
+                        oy = 0;
+                        ++oz;
+                    }
+                }
+            }
+            // A: dy voxels f0 .. f0 + 7, channels 16 wave ..
+            uint2 ar[2];
+#pragma unroll
+            for (int r = 0; r < 2; ++r) {
+                const int f = f0 + 4 * r + (li >> 2);
+                ar[r] = lds_read_tr16_b64(lds0 + uint32_t(dy_off + f * 128 + ((wave ^ tr_dswz(f)) * 32)) + colb);
+            }
+            // B rows: input plane oz * S0 (the tap group's kd is in the brick
+            // origin), rows oy + kh, voxels ox0 .. ox0 + 11 of the row
+            // a run starts at a multiple of 8, vb: its blocks vb, vb + 4, vb + 8 sit
+            // at slots vb + 4 B, vb + 4 (1 - B), vb + 8 + 4 (1 - B), B = bit 3 of vb
+            const int vrow = (oz * a.S[0] * a.biy + oy) * bixp8 + ox0;
+            uint2 xr[K1][3];
+#pragma unroll
+            for (int kh = 0; kh < K1; ++kh) {
+                const int vb = vrow + kh * bixp8;
+                const uint32_t hb = uint32_t((vb >> 3) & 1) * 128u;
+                const uint32_t rb = lds0 + uint32_t((vb + (li >> 2)) * 32) + colb;
+                xr[kh][0] = lds_read_tr16_b64(rb + hb);
+                xr[kh][1] = lds_read_tr16_b64(rb + (128u - hb));
+                xr[kh][2] = lds_read_tr16_b64(rb + 256u + (128u - hb));
+            }
+            lds_wait<0>();
+            const uint4 av = make_uint4(ar[0].x, ar[0].y, ar[1].x, ar[1].y);
+#pragma unroll
+            for (int kh = 0; kh < K1; ++kh) {
+                lds_ready(xr[kh][0]);
+                lds_ready(xr[kh][1]);
+                lds_ready(xr[kh][2]);
+                const uint32_t d[6] = {xr[kh][0].x, xr[kh][0].y, xr[kh][1].x, xr[kh][1].y, xr[kh][2].x, xr[kh][2].y};
+#pragma unroll
+                for (int kw = 0; kw < K2; ++kw) {
+                    uint4 bv;
+                    if (kw % 2 == 0) {
+                        bv = make_uint4(d[kw / 2], d[kw / 2 + 1], d[kw / 2 + 2], d[kw / 2 + 3]);
+                    } else {
+                        const int h = kw / 2;
+                        bv = make_uint4(__builtin_amdgcn_alignbit(d[h + 1], d[h], 16),
+                                        __builtin_amdgcn_alignbit(d[h + 2], d[h + 1], 16),
+                                        __builtin_amdgcn_alignbit(d[h + 3], d[h + 2], 16),
+                                        __builtin_amdgcn_alignbit(d[h + 4], d[h + 3], 16));
+                    }
+                    acc[kh * K2 + kw] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                        __builtin_bit_cast(bf16x8_w, av), __builtin_bit_cast(bf16x8_w, bv), acc[kh * K2 + kw], 0, 0, 0);
+                }
+            }
+        }
+    }
+    float4* out = reinterpret_cast<float4*>(a.part + ((((split * a.nmb + mb) * a.ncb) * a.ntg + tg) * int64_t(a.blk)) +
+                                            int64_t(wave) * TG * 256);
+#pragma unroll
+    for (int i = 0; i < TG; ++i) out[i * 64 + lane] = make_float4(acc[i][0], acc[i][1], acc[i][2], acc[i][3]);
+}
+
 template <int TPW>
 __global__ __launch_bounds__(kThreads, 2) void wgrad_f32_tiled(WgArgs a)
 {
@@ -656,8 +865,6 @@ __global__ __launch_bounds__(kThreads, 2) void wgrad_f32_tiled(WgArgs a)
 constexpr int kDlXU = 20;    // input load instructions per thread (80 KiB)
 constexpr int kDlDU = 3;     // dy load instructions per thread (bricks of <= 64 outputs)
 constexpr int kDlTab = 66;   // entries of the per-voxel input offset table
-
-__host__ __device__ inline int dl_round(int units) { return (units + kThreads - 1) / kThreads * kThreads; }
 
 struct DlLayout {
     int dy_off, tab_off, bytes;
@@ -1045,9 +1252,47 @@ bool bf16_pipe_ok(const PlanW& pl)
            nxu <= int64_t(kPipeBXU) * kThreads && ndu <= int64_t(kPipeBDU) * kThreads;
 }
 
+// The direct-load transposed-read kernel: 16 input channels, output channels
+// in whole blocks of 64, unit stride, one kd plane per tap group, no folded
+// halo, tile and dy of < 4 GiB per batch item, packed coordinates in range and
+// staging within its instruction budget and two workgroups' LDS per CU.
+template <int K1, int K2>
+hipError_t launch_bf16_dl(const PlanW& pl, hipStream_t s)
+{
+    const WgArgs& a = pl.a;
+    const TrLayout L = tr_layout(a);
+    auto fn = &wgrad_bf16_dl<K1, K2>;
+    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(fn), hipFuncAttributeMaxDynamicSharedMemorySize,
+                                       L.bytes);
+    if (e != hipSuccess) return e;
+    WgArgs aa = a;
+    int bx = L.bixp8, dyo = L.dy_off;
+    uint32_t xbu = uint32_t(a.P[0] * a.P[1] * a.P[2] * a.cin * 2);
+    uint32_t dbu = uint32_t(a.O[0] * a.O[1] * a.O[2] * a.cout * 2);
+    void* args[] = {&aa, &bx, &dyo, &xbu, &dbu};
+    return hipLaunchKernel(reinterpret_cast<const void*>(fn), dim3(unsigned(aa.nblocks)), dim3(kThreads), args,
+                           size_t(L.bytes), s);
+}
+
+bool bf16_dl_ok(const PlanW& pl)
+{
+    const WgArgs& a = pl.a;
+    const TrLayout L = tr_layout(a);
+    const int64_t bov = int64_t(a.BO[0]) * a.BO[1] * a.BO[2];
+    const int64_t xb = a.P[0] * a.P[1] * a.P[2] * a.cin * 2, db = a.O[0] * a.O[1] * a.O[2] * a.cout * 2;
+    return pl.kdg == 1 && pl.wco == 4 && a.cin == 16 && a.cout % 64 == 0 && a.S[0] == 1 && a.S[1] == 1 &&
+           a.S[2] == 1 && !a.fold.mask && a.xvec && a.dvec && a.K[2] <= 5 && xb < (int64_t(1) << 32) - 64 &&
+           db < (int64_t(1) << 32) - 64 && a.BO[2] % 8 == 0 && bov % 32 == 0 && L.bixp8 < 512 && a.biy < 1024 &&
+           a.biz < 1024 && a.BO[2] < 512 && a.BO[1] < 1024 && a.BO[0] < 512 &&
+           dl_round(a.biz * a.biy * L.bixp8 * 2) <= kTrXU * kThreads && dl_round(int(bov) * 8) <= kTrDU * kThreads &&
+           L.bytes <= 80 * 1024;
+}
+
 template <int KDG, int K1, int K2, int WCO>
 hipError_t launch_bf16_t(const PlanW& pl, hipStream_t s)
 {
+    if constexpr (KDG == 1 && WCO == 4 && K2 <= 5)
+        if (bf16_dl_ok(pl)) return launch_bf16_dl<K1, K2>(pl, s);
     if (!bf16_pipe_ok(pl)) return launch_with_lds(&wgrad_bf16_tiled<KDG, K1, K2, WCO>, pl, s);
     const WgArgs& a = pl.a;
     const int64_t nxu = int64_t(a.biz) * a.biy * ((a.bix + 3) / 4) * ((4 / WCO) * 2);
