@@ -17,9 +17,13 @@
 // element-wise path.
 //
 // Statistics: pass 1 gives every block (a fixed range of rows of one batch
-// item) fp32 per-channel sums, reduced across its threads through LDS in a fixed
-// order; pass 2 adds, per (n, g), the blocks' sums of the group's channels in
-// float64 (a fixed-order tree over 256 threads). Results are bitwise repeatable.
+// item) fp32 per-channel sums of the values shifted by a pivot (the channel's
+// value at the block's first voxel), reduced across its threads through LDS in
+// a fixed order; pass 2 turns each block's shifted sums back into sums of x in
+// float64 (S1 += d1 + cnt p, S2 += d2 + 2 p d1 + cnt p^2) and adds, per (n, g),
+// the blocks of the group's channels (a fixed-order tree over 256 threads).
+// The shift keeps the binary32 partials of offset data (mean large against the
+// spread) from cancelling. Results are bitwise repeatable.
 #include <algorithm>
 
 #include "common.h"
@@ -35,7 +39,7 @@ typedef __attribute__((ext_vector_type(4))) unsigned int u32x4_n;
 struct NormArgs {
     const char* x;
     char* y;
-    float* part;            // stats: [n * B][c][2]; apply: [n][c][2] scale, shift
+    float* part;            // stats: [n * B][c][3] shifted sums d1, d2 and pivot; apply: [n][c][2] scale, shift
     const double* sums;     // [n][G][2]
     const float* gamma;
     const float* beta;
@@ -68,6 +72,19 @@ __global__ __launch_bounds__(kT) void norm_stats_vec(NormArgs a)
     const int64_t r0 = b * a.rows / a.B, r1 = (b + 1) * a.rows / a.B;
     const int64_t nvec = a.ext[2] * a.c / VE;
     const int tid = threadIdx.x;
+    // pivot: the block's first voxel, the thread's channels (a thread's vectors
+    // always hold the same channels)
+    const int per = int(a.c / VE);
+    float piv[VE];
+    {
+        uint4 u0 = make_uint4(0u, 0u, 0u, 0u);
+        if (r0 < r1)
+            u0 = reinterpret_cast<const uint4*>(reinterpret_cast<const T*>(a.x) + run_offset(a, nn, r0))[tid % per];
+        T e[VE];
+        __builtin_memcpy(e, &u0, 16);
+#pragma unroll
+        for (int i = 0; i < VE; ++i) piv[i] = to_f32(e[i]);
+    }
     float s1[VE], s2[VE];
 #pragma unroll
     for (int i = 0; i < VE; ++i) s1[i] = s2[i] = 0.f;
@@ -92,7 +109,8 @@ __global__ __launch_bounds__(kT) void norm_stats_vec(NormArgs a)
                 __builtin_memcpy(e, &u[j], 16);
 #pragma unroll
                 for (int i = 0; i < VE; ++i) {
-                    const float f = to_f32(e[i]);
+                    // a vector past the row end holds zeros: it adds nothing
+                    const float f = v0 + j * kT < nvec ? to_f32(e[i]) - piv[i] : 0.f;
                     s1[i] += f;
                     s2[i] = fmaf(f, f, s2[i]);
                 }
@@ -106,7 +124,6 @@ __global__ __launch_bounds__(kT) void norm_stats_vec(NormArgs a)
     }
     __syncthreads();
     // threads tid and tid + k * (C / VE) hold the same channels: fold in a fixed tree
-    const int per = int(a.c / VE);
     for (int step = kT / 2; step >= per; step /= 2) {
         if (tid < step) {
 #pragma unroll
@@ -118,11 +135,12 @@ __global__ __launch_bounds__(kT) void norm_stats_vec(NormArgs a)
         __syncthreads();
     }
     if (tid < per) {
-        float* out = a.part + (nn * a.B + b) * a.c * 2;
+        float* out = a.part + (nn * a.B + b) * a.c * 3;
 #pragma unroll
         for (int i = 0; i < VE; ++i) {
-            out[(tid * VE + i) * 2] = red[0][tid][i];
-            out[(tid * VE + i) * 2 + 1] = red[1][tid][i];
+            out[(tid * VE + i) * 3] = red[0][tid][i];
+            out[(tid * VE + i) * 3 + 1] = red[1][tid][i];
+            out[(tid * VE + i) * 3 + 2] = piv[i];
         }
     }
 }
@@ -135,19 +153,21 @@ __global__ __launch_bounds__(kT) void norm_stats_elem(NormArgs a)
     const int64_t nn = blockIdx.x / a.B, b = blockIdx.x % a.B;
     const int64_t r0 = b * a.rows / a.B, r1 = (b + 1) * a.rows / a.B;
     const int64_t run = a.ext[2] * a.c;
-    float* out = a.part + (nn * a.B + b) * a.c * 2;
+    float* out = a.part + (nn * a.B + b) * a.c * 3;
     for (int64_t ch = threadIdx.x; ch < a.c; ch += kT) {
+        const float piv = r0 < r1 ? to_f32(reinterpret_cast<const T*>(a.x)[run_offset(a, nn, r0) + ch]) : 0.f;
         float s1 = 0.f, s2 = 0.f;
         for (int64_t row = r0; row < r1; ++row) {
             const T* src = reinterpret_cast<const T*>(a.x) + run_offset(a, nn, row);
             for (int64_t e = ch; e < run; e += a.c) {
-                const float f = to_f32(src[e]);
+                const float f = to_f32(src[e]) - piv;
                 s1 += f;
                 s2 = fmaf(f, f, s2);
             }
         }
-        out[ch * 2] = s1;
-        out[ch * 2 + 1] = s2;
+        out[ch * 3] = s1;
+        out[ch * 3 + 1] = s2;
+        out[ch * 3 + 2] = piv;
     }
 }
 
@@ -161,9 +181,12 @@ __global__ __launch_bounds__(kT) void norm_stats_final(NormArgs a)
     double s1 = 0.0, s2 = 0.0;
     for (int64_t k = threadIdx.x; k < items; k += kT) {
         const int64_t b = k / cpg, ch = g * cpg + k % cpg;
-        const float* p = a.part + ((nn * a.B + b) * a.c + ch) * 2;
-        s1 += double(p[0]);
-        s2 += double(p[1]);
+        const float* p = a.part + ((nn * a.B + b) * a.c + ch) * 3;
+        // voxels of block b per channel
+        const double cnt = double((b + 1) * a.rows / a.B - b * a.rows / a.B) * double(a.ext[2]);
+        const double d1 = double(p[0]), d2 = double(p[1]), piv = double(p[2]);
+        s1 += d1 + cnt * piv;
+        s2 += d2 + (2.0 * piv) * d1 + cnt * piv * piv;
     }
     red[0][threadIdx.x] = s1;
     red[1][threadIdx.x] = s2;
@@ -293,7 +316,7 @@ unsigned grid_of(int64_t total) { return unsigned(std::max<int64_t>(1, std::min<
 size_t norm_workspace(const Tile3& t, int64_t groups)
 {
     const NormArgs a = make_norm(t, groups);
-    return size_t(std::max(a.n * a.B * a.c * 2, a.n * a.c * 2)) * sizeof(float);
+    return size_t(std::max(a.n * a.B * a.c * 3, a.n * a.c * 2)) * sizeof(float);
 }
 
 hipError_t launch_norm_stats(const Tile3& t, shard_dtype_t dt, const void* tile, int64_t groups, double* sums,

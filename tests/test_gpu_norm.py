@@ -202,3 +202,40 @@ def test_full_size_stats_and_sampled_planes(sc, name):
         err = cases.norm_max_err(got, exp)
         log(f"  plane {p}: normalised max err {err:.3e}")
         assert err <= cases.TOL[w.dtype], (p, err)
+
+
+@pytest.mark.parametrize("name", ["c3r", "c5r", "c2r"])
+def test_offset_data_keeps_its_variance(sc, name):
+    """Inputs whose mean is large against their spread, N(1000, 1): one-pass
+    binary32 sums of x and x^2 would lose the variance to cancellation. The
+    variance from the shards' summed statistics must match the oracle's
+    (relative 1e-3), and the sharded normalisation the whole-domain one."""
+    import torch
+    dist = (synth.NORMAL, (1000.0, 1.0))
+    w = cases.REDUCED[name]
+    groups = max(1, w.cin // 8)
+    x_full = cases.to_ncdhw(cases.as_f64(w.x_box([0] * w.nd, list(w.G), dist), w))
+    shards = [_shard(sc, w, idx, dist) for idx in w.shards()]
+    tiles = [dev(t[2]) for t in shards]
+    total = torch.zeros((w.N, groups, 2), dtype=torch.float64, device="cuda")
+    for (sg, desc, _, _), tile in zip(shards, tiles):
+        total += _stats(sc, w, desc, tile, groups)
+    count = int(np.prod(w.G)) * (w.cin // groups)
+    got = total.cpu().numpy()
+    ref = onorm.sums(x_full, groups)
+    var_got = got[..., 1] / count - (got[..., 0] / count) ** 2
+    var_ref = ref[..., 1] / count - (ref[..., 0] / count) ** 2
+    log(f"offset norm {name}: variance {var_ref.ravel()[:2]} got {var_got.ravel()[:2]}")
+    assert np.all(np.abs(var_got - var_ref) <= 1e-3 * var_ref)
+    gamma = np.ones(w.cin, dtype=np.float32)
+    beta = np.zeros(w.cin, dtype=np.float32)
+    exp = onorm.group_norm(x_full, groups, EPS, gamma.astype(np.float64), beta.astype(np.float64))
+    g_d, b_d = torch.from_numpy(gamma).cuda(), torch.from_numpy(beta).cuda()
+    for (sg, desc, tile_h, inner), tile in zip(shards, tiles):
+        n = sc.shard_norm_workspace_bytes(desc, _code(sc, w), groups)
+        ws = torch.empty(max(n, 16), dtype=torch.uint8, device="cuda")
+        out = dev(np.full_like(tile_h, canary_for(w)))
+        sc.shard_norm_apply(desc, tile, total, count, EPS, groups, g_d, b_d, out, ws)
+        box = (slice(None), slice(None)) + tuple(slice(o, o + e) for o, e in zip(sg.off, sg.ext))
+        err = cases.norm_max_err(cases.to_ncdhw(cases.as_f64(host(out)[inner], w)), exp[box])
+        assert err <= cases.TOL[w.dtype], (sg.off, err)
