@@ -881,9 +881,15 @@ inline DlLayout dl_layout(const WgArgs& a)
     return L;
 }
 
-template <int TPW>
+// FOLD: the halo along axis 0 folded into the loads (the only axis with
+// margins): padded planes below fold.lo[0] come from the lo slab, planes from
+// fold.lo[0] + fold.ext[0] on from the hi slab (plane strides as in the tile; a
+// missing slab is a zero-length buffer, so its planes load as zeros). A lane
+// picks its buffer per unit; the load of each buffer goes out under the exec
+// mask of its lanes.
+template <int TPW, bool FOLD>
 __global__ __launch_bounds__(kThreads, 2) void wgrad_f32_dl(WgArgs a, int dy_off, int tab_off, uint32_t xbatch,
-                                                            uint32_t dbatch)
+                                                            uint32_t dbatch, uint32_t fbatch_lo, uint32_t fbatch_hi)
 {
     extern __shared__ uint4 lds4[];
     char* lds = reinterpret_cast<char*>(lds4);
@@ -965,6 +971,16 @@ __global__ __launch_bounds__(kThreads, 2) void wgrad_f32_dl(WgArgs a, int dy_off
             const_cast<char*>(a.tile) + int64_t(nn) * xbatch, short(0), int(xbatch), 0x00020000);
         const __amdgpu_buffer_rsrc_t rd = __builtin_amdgcn_make_buffer_rsrc(
             const_cast<char*>(a.dy) + int64_t(nn) * dbatch, short(0), int(dbatch), 0x00020000);
+        __amdgpu_buffer_rsrc_t rl = rx, rh = rx;
+        if (FOLD) {
+            const char* sl = a.fold.slab[0][0];
+            const char* sh = a.fold.slab[0][1];
+            rl = __builtin_amdgcn_make_buffer_rsrc(const_cast<char*>(sl ? sl + int64_t(nn) * fbatch_lo : a.tile),
+                                                   short(0), sl ? int(fbatch_lo) : 0, 0x00020000);
+            rh = __builtin_amdgcn_make_buffer_rsrc(const_cast<char*>(sh ? sh + int64_t(nn) * fbatch_hi : a.tile),
+                                                   short(0), sh ? int(fbatch_hi) : 0, 0x00020000);
+        }
+        const int flo = FOLD ? int(a.fold.lo[0]) : 0, fhi = FOLD ? int(a.fold.lo[0] + a.fold.ext[0]) : P0;
 #pragma unroll
         for (int i = 0; i < kDlXU; ++i) {
             if (i < nxi) {
@@ -974,8 +990,15 @@ __global__ __launch_bounds__(kThreads, 2) void wgrad_f32_dl(WgArgs a, int dy_off
                                 uint32_t(t2) < uint32_t(P2);
                 const uint32_t off = ((uint32_t(t0 * P1 + t1) * uint32_t(P2) + uint32_t(t2)) * uint32_t(cin) +
                                       uint32_t(ci0 + 4 * q)) * 4u;
-                __builtin_amdgcn_raw_ptr_buffer_load_lds(rx, SC_LDSW(lds + i * 4096 + wave * 1024), 16,
-                                                         ok ? off : kOut, 0, 0, 0);
+                char* dst = lds + i * 4096 + wave * 1024;
+                if (FOLD && t0 < flo) {
+                    __builtin_amdgcn_raw_ptr_buffer_load_lds(rl, SC_LDSW(dst), 16, ok ? off : kOut, 0, 0, 0);
+                } else if (FOLD && t0 >= fhi) {
+                    const uint32_t o = off - uint32_t(fhi) * uint32_t(P1) * uint32_t(P2) * uint32_t(cin) * 4u;
+                    __builtin_amdgcn_raw_ptr_buffer_load_lds(rh, SC_LDSW(dst), 16, ok ? o : kOut, 0, 0, 0);
+                } else {
+                    __builtin_amdgcn_raw_ptr_buffer_load_lds(rx, SC_LDSW(dst), 16, ok ? off : kOut, 0, 0, 0);
+                }
             }
         }
 #pragma unroll
@@ -1315,20 +1338,25 @@ hipError_t launch_f32(const Tile3& t, const Conv3& cv, const PlanW& pl, hipStrea
     const int64_t xb = t.P[0] * t.P[1] * t.P[2] * t.c * 4, db = cv.O[0] * cv.O[1] * cv.O[2] * cv.cout * 4;
     const DlLayout L = dl_layout(a);
     const int64_t bov = int64_t(a.BO[0]) * a.BO[1] * a.BO[2];
-    const bool dl = !a.fold.mask && a.xvec && a.dvec && t.c % 4 == 0 && cv.cout % 4 == 0 && xb < (int64_t(1) << 32) - 64 &&
+    // a folded halo: margins along axis 0 only, slabs of < 4 GiB per batch item
+    const int64_t plane = t.P[1] * t.P[2] * t.c * 4;
+    const int64_t fb_lo = t.lo[0] * plane, fb_hi = t.hi[0] * plane;
+    const bool fold_ok = !a.fold.mask || (a.fold.mask == 1u && fb_lo < (int64_t(1) << 32) - 64 &&
+                                          fb_hi < (int64_t(1) << 32) - 64);
+    const bool dl = fold_ok && a.xvec && a.dvec && t.c % 4 == 0 && cv.cout % 4 == 0 && xb < (int64_t(1) << 32) - 64 &&
                     db < (int64_t(1) << 32) - 64 && a.biz < 1024 && a.biy < 1024 && a.bix < 1024 &&
                     dl_round(a.biz * a.biy * a.bix * 8) <= kDlXU * kThreads &&
                     dl_round(int(bov + (bov & 1)) * 8) <= kDlDU * kThreads && bov + 1 <= kDlTab &&
                     L.bytes <= 80 * 1024;
     if (!dl) return launch_with_lds(&wgrad_f32_tiled<7>, pl, s);
-    auto fn = &wgrad_f32_dl<7>;
+    auto fn = a.fold.mask ? &wgrad_f32_dl<7, true> : &wgrad_f32_dl<7, false>;
     hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(fn), hipFuncAttributeMaxDynamicSharedMemorySize,
                                        L.bytes);
     if (e != hipSuccess) return e;
     WgArgs aa = a;
     int dyo = L.dy_off, tabo = L.tab_off;
-    uint32_t xbu = uint32_t(xb), dbu = uint32_t(db);
-    void* args[] = {&aa, &dyo, &tabo, &xbu, &dbu};
+    uint32_t xbu = uint32_t(xb), dbu = uint32_t(db), flu = uint32_t(fb_lo), fhu = uint32_t(fb_hi);
+    void* args[] = {&aa, &dyo, &tabo, &xbu, &dbu, &flu, &fhu};
     return hipLaunchKernel(reinterpret_cast<const void*>(fn), dim3(unsigned(aa.nblocks)), dim3(kThreads), args,
                            size_t(L.bytes), s);
 }
