@@ -259,8 +259,8 @@ def main():
             detail[label] = {"ms": round(cms, 4), "gbs": round(gbs, 1), "frac_hbm_peak": round(gbs / HBM_PEAK, 4),
                              "bytes": int(work), "in_step_ms": round(ms, 4),
                              "protocol": "cold: 8 consecutive launches on 8 buffer sets (tile and slabs, 8 x the bytes "
-                                         "> the 256 MB last-level cache) between one event pair, per launch; "
-                                         "median of the repeats"}
+                                         "> the 256 MB last-level cache), replayed from a captured graph between "
+                                         "one event pair, per launch; median of the repeats"}
     dom = max(("conv_fwd", "conv_wgrad"), key=lambda k: per_op[k][2])
     ach = per_op[dom][1] / (per_op[dom][2] * 1e-3) / 1e12
     roofline = {"kernel": dom, "bound": "mfma", "achieved": round(ach, 2), "peak": PEAK[dt], "unit": "TFLOP/s",
@@ -292,8 +292,9 @@ def time_halo_cold(sc, w, desc, tile, ops, send, recv, args, stream):
     the tile and of every slab, used in turn by 8 consecutive launches between
     one event pair (each set was last touched 7 launches earlier, 7 x its bytes
     ago: more than the last-level cache holds at the workloads' sizes), median
-    over `steps` repeats. One event pair over 8 launches also amortises the
-    event overhead, so the figure is close to the kernel time."""
+    over `steps` repeats. The launches are replayed from a captured graph and
+    one event pair spans all 8, so neither host call overhead nor the event
+    overhead enters the figure, which is close to the kernel time."""
     import numpy as np
     import torch
     NS = 8
@@ -304,7 +305,7 @@ def time_halo_cold(sc, w, desc, tile, ops, send, recv, args, stream):
     out = {}
     for label, kind in halo:
         axis = int(label.split("_a")[1])
-        calls = []
+        calls, outs = [], []
         for k in range(NS):
             if kind == "pack":
                 sends = {side: (nwidth, buf) for (a_, side, nwidth, buf, _) in send if a_ == axis}
@@ -312,6 +313,7 @@ def time_halo_cold(sc, w, desc, tile, ops, send, recv, args, stream):
                 wh, bh = sends.get(1, (0, None))
                 bl = torch.empty_like(bl) if bl is not None else None
                 bh = torch.empty_like(bh) if bh is not None else None
+                outs += [b for b in (bl, bh) if b is not None]
                 calls.append(lambda t=tiles[k], wl=wl, bl=bl, wh=wh, bh=bh:
                              sc.shard_halo_pack_pair(desc, t, axis, wl, bl, wh, bh))
             else:
@@ -324,17 +326,31 @@ def time_halo_cold(sc, w, desc, tile, ops, send, recv, args, stream):
         for c in calls:
             c()
         torch.cuda.synchronize()
+        # the 8 launches are replayed from a captured graph, so that the host's
+        # per-call cost (argument checks, the binding) cannot leave the GPU idle
+        # between kernels of ~10 us; the graph's first replay is checked bit for
+        # bit against the eager calls' result
+        ref = [t.clone() for t in outs] if outs else None
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph):
+            for c in calls:
+                c()
+        for t in outs:
+            t.zero_()
+        graph.replay()
+        torch.cuda.synchronize()
+        if ref is not None and not all(torch.equal(a, b) for a, b in zip(ref, outs)):
+            raise RuntimeError(f"{label}: graph replay differs from the eager launches")
         times = []
         for _ in range(max(3, args.steps)):
             e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
             e0.record(stream)
-            for c in calls:
-                c()
+            graph.replay()
             e1.record(stream)
             torch.cuda.synchronize()
             times.append(e0.elapsed_time(e1) / NS)
         out[label] = float(np.median(times))
-        del calls
+        del calls, graph, ref
     del tiles
     torch.cuda.empty_cache()
     log("cold halo launches timed")
