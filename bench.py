@@ -409,7 +409,7 @@ def time_backward(sc, w, g, desc, wt, dy, send, flops, args, stream):
     torch.cuda.synchronize()
     out = {}
     for i, (label, kind, work, _) in enumerate(ops):
-        ms = float(np.mean([ev[k][i][0].elapsed_time(ev[k][i][1]) for k in range(args.steps)]))
+        ms = _median_ms(label, [ev[k][i][0].elapsed_time(ev[k][i][1]) for k in range(args.steps)])
         if kind == "dgrad":
             tf = work / (ms * 1e-3) / 1e12
             out[label] = {"ms": round(ms, 4), "tflops": round(tf, 2), "frac_mfma_peak": round(tf / PEAK[w.dtype], 4)}
@@ -419,6 +419,18 @@ def time_backward(sc, w, g, desc, wt, dy, send, flops, args, stream):
                           "bytes": int(work)}
     log("backward ops timed")
     return out
+
+
+def _median_ms(label, times):
+    """Median of the event-timed repeats of a side op (the step's own ops are
+    averaged). A repeat far above the median is reported on stderr: one-off
+    stalls outside the kernels (seen as a single slow repeat) then cannot move
+    the reported figure."""
+    import numpy as np
+    med = float(np.median(times))
+    if max(times) > 1.5 * med:
+        log(f"{label}: repeats {', '.join(f'{t:.3f}' for t in times)} ms (median {med:.3f})")
+    return med
 
 
 def _time_ops(ops, args, stream):
@@ -438,7 +450,7 @@ def _time_ops(ops, args, stream):
     torch.cuda.synchronize()
     out = {}
     for i, (label, kind, work, _) in enumerate(ops):
-        ms = float(np.mean([ev[k][i][0].elapsed_time(ev[k][i][1]) for k in range(args.steps)]))
+        ms = _median_ms(label, [ev[k][i][0].elapsed_time(ev[k][i][1]) for k in range(args.steps)])
         if kind.startswith("mfma:"):
             tf = work / (ms * 1e-3) / 1e12
             out[label] = {"ms": round(ms, 4), "tflops": round(tf, 2),

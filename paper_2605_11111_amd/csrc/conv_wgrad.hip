@@ -19,6 +19,7 @@
 // straight from channels-last LDS copies; the four waves split the taps.
 #include <algorithm>
 #include <cstdlib>
+#include <utility>
 
 #include "common.h"
 #include "internal.h"
@@ -495,61 +496,110 @@ __global__ __launch_bounds__(kThreads, 2) void wgrad_bf16_pipe(WgArgs a)
     for (int i = 0; i < TG; ++i) out[i * 64 + lane] = make_float4(acc[i][0], acc[i][1], acc[i][2], acc[i][3]);
 }
 
-// bf16, 16 input channels, one kd plane of taps per workgroup (the general
-// kernel's decomposition for large 3D kernels such as 5 x 5 x 5), without any
-// transposition while staging: the brick's input rows and dy are copied to LDS
-// channels-last by direct global->LDS loads, and every operand is read with
-// ds_read_b64_tr_b16 (within each 16-lane group, lane i addresses voxel
-// row k0 + i/4 at channels 4 (i % 4) ..; lane j receives channel j of voxels
-// k0 .. k0 + 3). v_mfma_f32_16x16x32_bf16: M = 16 output channels (wave w owns
-// channels 16 w ..), N = the 16 input channels, K = 32 output voxels, lane
-// group g = lane / 16 holding voxels 8 g .. 8 g + 7 of the K step.
-//  * A (dy): two reads of four voxels.
-//  * B (input row (kd, kh)): three reads give the lane 12 consecutive voxels
-//    8 g .. 8 g + 11 of its channel; the operand of tap kw is the window
-//    kw .. kw + 7 (dword aligned for even kw, one v_alignbit per dword for odd).
-// LDS layouts (16-byte units written by the loads, swizzled through the
-// lane -> source mapping so that the reads hit distinct banks):
-//  * input: voxel v of the brick (row pitch bixp8, a multiple of 8) at 32-byte
-//    slot v ^ (((v >> 3) & 1) << 2);
-//  * dy: voxel f at 128 f, its 32-byte channel chunk k at chunk
-//    k ^ (((f >> 1) & 1) | (((f >> 3) & 1) << 1)).
-// Bricks, K steps, taps and the partial layout are those of wgrad_bf16_tiled
-// with 4 waves of 16 output channels: the partials are bit-identical.
-constexpr int kTrXU = 8;   // input load instructions per thread
-constexpr int kTrDU = 8;   // dy load instructions per thread
+// Staging budget of the row-pair kernel below: load instructions per thread.
+constexpr int kTrXU = 4;   // input
+constexpr int kTrDU = 4;   // dy
 
-struct TrLayout {
-    int bixp8, dy_off, bytes;
+// bf16, 16 input channels, one kd plane of taps per workgroup (the general
+// kernel's decomposition for large 3D kernels such as 5 x 5 x 5): the row-pair
+// kernel. No transposition while staging: the brick's input rows and dy are
+// copied to LDS channels-last by direct global->LDS loads, and every operand is
+// read with ds_read_b64_tr_b16 (lane i of a 16-lane group addresses voxel
+// k0 + i / 4 at channels 4 (i % 4) ..; lane j receives channel j of voxels
+// k0 .. k0 + 3). v_mfma_f32_32x32x16_bf16: M = 32 output channels (wave w owns
+// channels 32 (w % 2) .. of the block's 64), K = 16 output voxels (one W run
+// of the brick; lane k-half lane / 32 holds voxels 8 (lane / 32) ..), N = two
+// taps of the 16 input channels: lane half h = (lane / 16) % 2 supplies columns
+// 16 h .. of one tap. A tile is
+//  * a row pair: taps (2 p + h, kw), 0 <= kw < K2, read from rows 2 p + h, or
+//  * for odd K1, a W pair of the last row: taps (K1 - 1, 2 q + h), lane half h
+//    reading the row one voxel further on (a tap past the kernel is computed
+//    and dropped).
+// Waves 0, 1 take the first ceil(T / 2) of the T tiles, waves 2, 3 the rest.
+// Every lane addresses its own voxel rows, so a tile's B operand (voxels
+// w .. w + 7 of its row, w = kw or 2 q) is two reads at voxel offsets w and
+// w + 4 landing in the operand registers: no shuffles.
+// LDS, per buffer: input voxel (z, y, x) of the brick at 32 (row rp + x), row =
+// z biy + y, with a row pitch rp = 4 mod 8 voxels, so the two rows of a pair
+// fall in opposite halves of the banks; dy voxel f at 128 f with its 32-byte
+// channel chunk k at k ^ 2 ((f / 2) % 2). Two buffers: the loads of brick b + 1
+// go out when brick b's compute starts, and one barrier per brick both
+// publishes a brick and frees the other buffer. The operand reads of K step
+// s + 1 are issued before the products of step s.
+// The partials take the general kernel's layout; the sum over a K step is in
+// a different order than there, so they match it to rounding, not bitwise.
+template <int K1, int K2>
+struct PrTiles {
+    static_assert(K2 <= 5, "a 12-voxel run covers five W taps");
+    static constexpr int NR = K1 / 2;                       // row-pair runs
+    static constexpr int NW = K1 % 2 ? (K2 + 1) / 2 : 0;   // W-pair tiles
+    static constexpr int T = NR * K2 + NW;
+    static constexpr int NT0 = (T + 1) / 2;
+    static constexpr int NRUN = NR + K1 % 2;
+    static constexpr int run(int t) { return t < NR * K2 ? t / K2 : NR; }
+    static constexpr int win(int t) { return t < NR * K2 ? t % K2 : 2 * (t - NR * K2); }
+    static constexpr int kh(int t, int h) { return t < NR * K2 ? 2 * (t / K2) + h : K1 - 1; }
+    static constexpr int kw(int t, int h) { return t < NR * K2 ? t % K2 : 2 * (t - NR * K2) + h; }
+    static constexpr int first(int th) { return th == 0 ? 0 : NT0; }
+    static constexpr int count(int th) { return th == 0 ? NT0 : T - NT0; }
+    static constexpr bool uses(int th, int r)
+    {
+        for (int t = first(th); t < first(th) + count(th); ++t)
+            if (run(t) == r) return true;
+        return false;
+    }
 };
 
-inline TrLayout tr_layout(const WgArgs& a)
+struct PrLayout {
+    int rp, dy_off, bufb, bytes;
+};
+
+inline PrLayout pr_layout(const WgArgs& a)
 {
-    TrLayout L;
-    L.bixp8 = (a.bix + 7) / 8 * 8;
-    const int xunits = a.biz * a.biy * L.bixp8 * 2;
+    PrLayout L;
+    L.rp = (a.bix + 3) / 4 * 4;
+    if (L.rp % 8 == 0) L.rp += 4;
     const int bov = a.BO[0] * a.BO[1] * a.BO[2];
-    L.dy_off = dl_round(xunits) * 16;
-    L.bytes = L.dy_off + dl_round(bov * 8) * 16;
+    L.dy_off = dl_round(a.biz * a.biy * L.rp * 2) * 16;
+    L.bufb = L.dy_off + dl_round(bov * 8) * 16;
+    L.bytes = 2 * L.bufb;
     return L;
 }
 
-__device__ __forceinline__ int tr_xslot(int v) { return v ^ (((v >> 3) & 1) << 2); }
-__device__ __forceinline__ int tr_dswz(int f) { return ((f >> 1) & 1) | (((f >> 3) & 1) << 1); }
-
-template <int K1, int K2>
-__global__ __launch_bounds__(kThreads, 2) void wgrad_bf16_dl(WgArgs a, int bixp8, int dy_off, uint32_t xbatch,
-                                                             uint32_t dbatch)
+// f(std::integral_constant<int, i>) for i = 0 .. N - 1, unrolled at compile time
+template <typename F, int... Is>
+__device__ __forceinline__ void static_for_impl(F&& f, std::integer_sequence<int, Is...>)
 {
-    static_assert(K2 <= 5, "a 12-voxel run covers five W taps");
+    (f(std::integral_constant<int, Is>{}), ...);
+}
+template <int N, typename F>
+__device__ __forceinline__ void static_for(F&& f)
+{
+    static_for_impl(f, std::make_integer_sequence<int, N>{});
+}
+
+// one K step's operands: dy (A) and the input window of each of the wave's tiles
+template <int NT>
+struct PrOps {
+    uint2 a[2];
+    uint2 b[NT > 0 ? NT : 1][2];
+};
+
+template <int K1, int K2, int TH>
+__device__ __forceinline__ void wgrad_bf16_pr_body(const WgArgs& a, int rp, int dy_off, int bufb, uint32_t xbatch,
+                                                   uint32_t dbatch)
+{
+    using TL = PrTiles<K1, K2>;
+    constexpr int NT = TL::count(TH), T0 = TL::first(TH);
     constexpr int TG = K1 * K2;
     extern __shared__ uint4 lds4[];
     char* lds = reinterpret_cast<char*>(lds4);
     const int tid = threadIdx.x;
     const int lane = tid & 63;
     const int wave = tid >> 6;
-    const int g = lane >> 4;
-    const int li = lane & 15;
+    const int ch = wave & 1;
+    const int li = lane & 15, vr = li >> 2;
+    const int gh = (lane >> 4) & 1, gk = lane >> 5;
 
     int64_t b = xcd_remap(blockIdx.x, a.nblocks);
     const int tg = int(b % a.ntg);
@@ -561,27 +611,26 @@ __global__ __launch_bounds__(kThreads, 2) void wgrad_bf16_dl(WgArgs a, int bixp8
     const int kd0 = tg;
     const int co0 = mb * 64;
     const int bov = a.BO[0] * a.BO[1] * a.BO[2];
-    const int nxv = a.biz * a.biy * bixp8;
+    const int nxv = a.biz * a.biy * rp;
     const int nxi = dl_round(nxv * 2) / kThreads, ndi = dl_round(bov * 8) / kThreads;
 
-    // the thread's load units, brick invariant. Input: slot s = 32-byte voxel
-    // slot s >> 1 (voxel v = its swizzle inverse), half h = s & 1 (channels
-    // 8 h ..); packed z << 20 | y << 10 | x << 1 | h, -1 past the row or brick.
-    // dy: slot s = voxel f = s >> 3, 16-byte unit p = s & 7 of its 128 bytes,
-    // holding global unit q = p ^ 2 swz(f) (channels 8 q ..); packed
-    // oz << 22 | oy << 12 | ox << 3 | q.
+    // the thread's load units, brick invariant. Input: unit s = 16-byte half
+    // s & 1 (channels 8 (s & 1) ..) of voxel slot s >> 1; packed
+    // z << 20 | y << 10 | x << 1 | half, -1 past the row or brick. dy: unit s =
+    // 16-byte unit p = s & 7 of voxel f = s >> 3, holding channels 8 q .., q =
+    // p ^ 4 ((f / 2) % 2); packed oz << 22 | oy << 12 | ox << 3 | q.
     int px[kTrXU], pd[kTrDU];
 #pragma unroll
     for (int i = 0; i < kTrXU; ++i) {
         const int sl = tid + i * kThreads;
-        const int v = tr_xslot(sl >> 1), h = sl & 1;
-        const int x = v % bixp8, r = v / bixp8;
+        const int v = sl >> 1, h = sl & 1;
+        const int x = v % rp, r = v / rp;
         px[i] = (v < nxv && x < a.bix) ? (((r / a.biy) << 20) | ((r % a.biy) << 10) | (x << 1) | h) : -1;
     }
 #pragma unroll
     for (int i = 0; i < kTrDU; ++i) {
         const int sl = tid + i * kThreads;
-        const int f = sl >> 3, q = (sl & 7) ^ (2 * tr_dswz(f));
+        const int f = sl >> 3, q = (sl & 7) ^ (((f >> 1) & 1) << 2);
         const int ox = f % a.BO[2], oy = (f / a.BO[2]) % a.BO[1], oz = f / (a.BO[2] * a.BO[1]);
         pd[i] = f < bov ? ((oz << 22) | (oy << 12) | (ox << 3) | q) : -1;
     }
@@ -590,18 +639,12 @@ __global__ __launch_bounds__(kThreads, 2) void wgrad_bf16_dl(WgArgs a, int bixp8
     const int cout = int(a.cout);
     constexpr uint32_t kOut = 0xFFFFFFF0u;
 
-    f32x4_w acc[TG];
-#pragma unroll
-    for (int i = 0; i < TG; ++i) acc[i] = f32x4_w{0.f, 0.f, 0.f, 0.f};
-
-    const uint32_t lds0 = lds_addr(lds);
-    const uint32_t colb = uint32_t((li & 3) * 8);
-    for (int64_t br = br0; br < br1; ++br) {
+    // loads of brick br into the buffer at byte offset boff
+    auto stage = [&](int64_t br, int boff) {
         int64_t nn, ob[3];
         brick_origin(a, br, nn, ob);
         const int i0 = int(ob[0]) * a.S[0] + kd0 - a.pad[0], i1 = int(ob[1]) * a.S[1] - a.pad[1],
                   i2 = int(ob[2]) - a.pad[2];
-        __syncthreads();  // every wave is done reading the previous brick
         const __amdgpu_buffer_rsrc_t rx = __builtin_amdgcn_make_buffer_rsrc(
             const_cast<char*>(a.tile) + int64_t(nn) * xbatch, short(0), int(xbatch), 0x00020000);
         const __amdgpu_buffer_rsrc_t rd = __builtin_amdgcn_make_buffer_rsrc(
@@ -615,7 +658,7 @@ __global__ __launch_bounds__(kThreads, 2) void wgrad_bf16_dl(WgArgs a, int bixp8
                                 uint32_t(t2) < uint32_t(P2);
                 const uint32_t off = ((uint32_t(t0 * P1 + t1) * uint32_t(P2) + uint32_t(t2)) * 16u +
                                       uint32_t(8 * (c & 1))) * 2u;
-                __builtin_amdgcn_raw_ptr_buffer_load_lds(rx, SC_LDSW(lds + i * 4096 + wave * 1024), 16,
+                __builtin_amdgcn_raw_ptr_buffer_load_lds(rx, SC_LDSW(lds + boff + i * 4096 + wave * 1024), 16,
                                                          ok ? off : kOut, 0, 0, 0);
             }
         }
@@ -628,77 +671,138 @@ __global__ __launch_bounds__(kThreads, 2) void wgrad_bf16_dl(WgArgs a, int bixp8
                 const bool ok = c >= 0 && o0 < O0 && o1 < O1 && o2 < O2;
                 const uint32_t off = ((uint32_t(o0 * O1 + o1) * uint32_t(O2) + uint32_t(o2)) * uint32_t(cout) +
                                       uint32_t(co0 + 8 * (c & 7))) * 2u;
-                __builtin_amdgcn_raw_ptr_buffer_load_lds(rd, SC_LDSW(lds + dy_off + i * 4096 + wave * 1024), 16,
-                                                         ok ? off : kOut, 0, 0, 0);
+                __builtin_amdgcn_raw_ptr_buffer_load_lds(
+                    rd, SC_LDSW(lds + boff + dy_off + i * 4096 + wave * 1024), 16, ok ? off : kOut, 0, 0, 0);
             }
         }
-        wait_vm_barrier<0>();  // the brick's loads have landed, for every wave
+    };
 
-        int ox0 = (8 * g) % a.BO[2], oy = ((8 * g) / a.BO[2]) % a.BO[1], oz = (8 * g) / (a.BO[2] * a.BO[1]);
-        for (int ks = 0; ks < bov / 32; ++ks) {
-            const int f0 = ks * 32 + 8 * g;
-            if (ks > 0) {
-                ox0 += 32;
-                while (ox0 >= a.BO[2]) {
-                    ox0 -= a.BO[2];
+    f32x16_w acc[NT > 0 ? NT : 1];  // a 1x1 kernel leaves waves 2, 3 without tiles
+#pragma unroll
+    for (int i = 0; i < NT; ++i)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) acc[i][r] = 0.f;
+
+    const uint32_t lds0 = lds_addr(lds);
+    const uint32_t colb = uint32_t((li & 3) * 8);
+    // per-lane read offsets within a buffer. A: voxel 8 gk + vr (+ 4) of the K
+    // step, chunk 2 ch + gh; run p: row 2 p + gh; W run: row K1 - 1, one voxel
+    // further on for gh = 1
+    const uint32_t cA = uint32_t(dy_off) + uint32_t((8 * gk + vr) * 128) +
+                        uint32_t(((2 * ch + gh) ^ (((vr >> 1) & 1) << 1)) * 32) + colb;
+    uint32_t cX[TL::NRUN];
+#pragma unroll
+    for (int r = 0; r < TL::NRUN; ++r)
+        cX[r] = r < TL::NR ? uint32_t(((2 * r + gh) * rp + 8 * gk + vr) * 32) + colb
+                           : uint32_t(((K1 - 1) * rp + 8 * gk + gh + vr) * 32) + colb;
+    const int nks = bov / 16;
+
+    // operand reads of K step ks (voxels 16 ks .. of the brick, at (oz, oy, ox)):
+    // a tile's window w .. w + 7 is two reads at voxel offsets w and w + 4 of its
+    // run, straight into the product's operand registers
+    auto issue = [&](PrOps<NT>& o, uint32_t aA, uint32_t U) {
+        o.a[0] = lds_read_tr16_b64(aA);
+        o.a[1] = lds_read_tr16_b64<512>(aA);
+        uint32_t ad[TL::NRUN];
+#pragma unroll
+        for (int r = 0; r < TL::NRUN; ++r)
+            if (TL::uses(TH, r)) ad[r] = U + cX[r];
+        static_for<NT>([&](auto ic) {
+            constexpr int t = T0 + decltype(ic)::value;
+            o.b[decltype(ic)::value][0] = lds_read_tr16_b64<32 * TL::win(t)>(ad[TL::run(t)]);
+            o.b[decltype(ic)::value][1] = lds_read_tr16_b64<32 * TL::win(t) + 128>(ad[TL::run(t)]);
+        });
+    };
+    auto compute = [&](PrOps<NT>& o) {
+        uint2 a0 = o.a[0], a1 = o.a[1];
+        lds_ready(a0);
+        lds_ready(a1);
+        const uint4 av = make_uint4(a0.x, a0.y, a1.x, a1.y);
+#pragma unroll
+        for (int i = 0; i < NT; ++i) {
+            uint2 b0 = o.b[i][0], b1 = o.b[i][1];
+            lds_ready(b0);
+            lds_ready(b1);
+            const uint4 bv = make_uint4(b0.x, b0.y, b1.x, b1.y);
+            acc[i] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8_w, av),
+                                                              __builtin_bit_cast(bf16x8_w, bv), acc[i], 0, 0, 0);
+        }
+    };
+
+    if (br0 < br1) stage(br0, 0);
+    for (int64_t br = br0; br < br1; ++br) {
+        const int cur = int((br - br0) & 1);
+        // this thread's loads of brick br have landed; after the barrier every
+        // thread's have, and every wave is done with the other buffer
+        wait_vm_barrier<0>();
+        if (br + 1 < br1) stage(br + 1, (cur ^ 1) * bufb);
+        if constexpr (NT > 0) {
+            // step positions advance by 16 voxels along W, then by a row, then
+            // by a plane of the brick: byte offsets of the run starts (U) and
+            // of dy (aA) move by wave-uniform increments
+            const uint32_t base = lds0 + uint32_t(cur * bufb);
+            const uint32_t rowstep = uint32_t((rp - a.BO[2]) * 32);
+            const uint32_t planestep = uint32_t((a.biy - a.BO[1]) * rp * 32);
+            uint32_t aA = base + cA, U = base;
+            int ox = 0, oy = 0;
+            auto advance = [&]() {
+                aA += 2048u;
+                U += 512u;
+                ox += 16;
+                if (ox == a.BO[2]) {
+                    ox = 0;
+                    U += rowstep;
                     if (++oy == a.BO[1]) {
                         oy = 0;
-                        ++oz;
+                        U += planestep;
                     }
                 }
-            }
-            // A: dy voxels f0 .. f0 + 7, channels 16 wave ..
-            uint2 ar[2];
-#pragma unroll
-            for (int r = 0; r < 2; ++r) {
-                const int f = f0 + 4 * r + (li >> 2);
-                ar[r] = lds_read_tr16_b64(lds0 + uint32_t(dy_off + f * 128 + ((wave ^ tr_dswz(f)) * 32)) + colb);
-            }
-            // B rows: input plane oz * S0 (the tap group's kd is in the brick
-            // origin), rows oy + kh, voxels ox0 .. ox0 + 11 of the row
-            // a run starts at a multiple of 8, vb: its blocks vb, vb + 4, vb + 8 sit
-            // at slots vb + 4 B, vb + 4 (1 - B), vb + 8 + 4 (1 - B), B = bit 3 of vb
-            const int vrow = (oz * a.S[0] * a.biy + oy) * bixp8 + ox0;
-            uint2 xr[K1][3];
-#pragma unroll
-            for (int kh = 0; kh < K1; ++kh) {
-                const int vb = vrow + kh * bixp8;
-                const uint32_t hb = uint32_t((vb >> 3) & 1) * 128u;
-                const uint32_t rb = lds0 + uint32_t((vb + (li >> 2)) * 32) + colb;
-                xr[kh][0] = lds_read_tr16_b64(rb + hb);
-                xr[kh][1] = lds_read_tr16_b64(rb + (128u - hb));
-                xr[kh][2] = lds_read_tr16_b64(rb + 256u + (128u - hb));
-            }
-            lds_wait<0>();
-            const uint4 av = make_uint4(ar[0].x, ar[0].y, ar[1].x, ar[1].y);
-#pragma unroll
-            for (int kh = 0; kh < K1; ++kh) {
-                lds_ready(xr[kh][0]);
-                lds_ready(xr[kh][1]);
-                lds_ready(xr[kh][2]);
-                const uint32_t d[6] = {xr[kh][0].x, xr[kh][0].y, xr[kh][1].x, xr[kh][1].y, xr[kh][2].x, xr[kh][2].y};
-#pragma unroll
-                for (int kw = 0; kw < K2; ++kw) {
-                    uint4 bv;
-                    if (kw % 2 == 0) {
-                        bv = make_uint4(d[kw / 2], d[kw / 2 + 1], d[kw / 2 + 2], d[kw / 2 + 3]);
-                    } else {
-                        const int h = kw / 2;
-                        bv = make_uint4(__builtin_amdgcn_alignbit(d[h + 1], d[h], 16),
-                                        __builtin_amdgcn_alignbit(d[h + 2], d[h + 1], 16),
-                                        __builtin_amdgcn_alignbit(d[h + 3], d[h + 2], 16),
-                                        __builtin_amdgcn_alignbit(d[h + 4], d[h + 3], 16));
-                    }
-                    acc[kh * K2 + kw] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
-                        __builtin_bit_cast(bf16x8_w, av), __builtin_bit_cast(bf16x8_w, bv), acc[kh * K2 + kw], 0, 0, 0);
-                }
+            };
+            PrOps<NT> o0, o1;
+            issue(o0, aA, U);
+            for (int ks = 0; ks < nks; ks += 2) {  // nks is even
+                advance();
+                lds_wait<0>();
+                issue(o1, aA, U);
+                compute(o0);
+                // the last pair re-reads its second step: same registers every
+                // iteration, no step past the brick
+                if (ks + 2 < nks) advance();
+                lds_wait<0>();
+                issue(o0, aA, U);
+                compute(o1);
             }
         }
     }
-    float4* out = reinterpret_cast<float4*>(a.part + ((((split * a.nmb + mb) * a.ncb) * a.ntg + tg) * int64_t(a.blk)) +
-                                            int64_t(wave) * TG * 256);
+    lds_wait<0>();  // the last re-read has landed
+    // accumulator element e of lane l: output channel 32 ch + 8 (e / 4) +
+    // 4 (l / 32) + e % 4, column l % 32 = 16 gh + ci; stored in the layout
+    // [16-channel group][tap][16 (co % 16 / 4) + ci][co % 4]
+    float* out = a.part + ((((split * a.nmb + mb) * a.ncb) * a.ntg + tg) * int64_t(a.blk));
 #pragma unroll
-    for (int i = 0; i < TG; ++i) out[i * 64 + lane] = make_float4(acc[i][0], acc[i][1], acc[i][2], acc[i][3]);
+    for (int i = 0; i < NT; ++i) {
+        const int t = T0 + i;
+        const int kh = gh ? TL::kh(t, 1) : TL::kh(t, 0), kw = gh ? TL::kw(t, 1) : TL::kw(t, 0);
+        if (kh >= K1 || kw >= K2) continue;
+        const int ti = kh * K2 + kw;
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+            const int co = 32 * ch + 8 * (e >> 2) + 4 * gk + (e & 3);
+            out[(((co >> 4) * TG + ti) * 64 + 16 * ((co & 15) >> 2) + li) * 4 + (co & 3)] = acc[i][e];
+        }
+    }
+}
+
+template <int K1, int K2>
+__global__ __launch_bounds__(kThreads, 2) void wgrad_bf16_pr(WgArgs a, int rp, int dy_off, int bufb, uint32_t xbatch,
+                                                             uint32_t dbatch)
+{
+    // waves 0, 1 and waves 2, 3 (a wave-uniform choice, made scalar so that the
+    // compiler keeps the step's bookkeeping in scalar registers)
+    if (__builtin_amdgcn_readfirstlane(threadIdx.x >> 7) == 0)
+        wgrad_bf16_pr_body<K1, K2, 0>(a, rp, dy_off, bufb, xbatch, dbatch);
+    else
+        wgrad_bf16_pr_body<K1, K2, 1>(a, rp, dy_off, bufb, xbatch, dbatch);
 }
 
 template <int TPW>
@@ -1135,9 +1239,56 @@ PlanW plan_wgrad(const Tile3& t, const Conv3& cv, shard_dtype_t dt)
         if (!bf16_instance(kdg, int(cv.K[1]), int(cv.K[2]))) return pl;
         const int wco = t.c <= 16 ? 4 : 2, wci = 4 / wco;
         const int nco = wco * 16, nci = wci * 16;
-        // brick: W extent a multiple of 8 (an 8-voxel K group stays in one row)
+        // the row-pair kernel's brick (when its shape applies): W extent a
+        // multiple of 16 (a K step is one W run), double-buffered staging within
+        // two workgroups' LDS per CU
         double best = 1e300;
+        const bool pr_shape = kdg == 1 && t.c == 16 && cv.cout % 64 == 0 && cv.K[2] <= 5 && cv.S[0] == 1 &&
+                              cv.S[1] == 1 && cv.S[2] == 1 && !force_tiled();
+        for (int b2 : {16, 32, 64}) {
+            for (int b1 = 1; b1 <= 64 && pr_shape; b1 *= 2) {
+                for (int b0 = 1; b0 <= 64; b0 *= 2) {
+                    const int bov = b0 * b1 * b2;
+                    if (bov % 32 != 0 || bov > kTrDU * kThreads / 8) continue;
+                    if ((b0 > 1 && b0 > cv.O[0]) || (b1 > 1 && b1 > cv.O[1])) continue;
+                    WgArgs c{};
+                    c.BO[0] = b0;
+                    c.BO[1] = b1;
+                    c.BO[2] = b2;
+                    c.biz = b0;
+                    c.biy = int(b1 - 1 + cv.K[1]);
+                    c.bix = int(b2 + cv.K[2] - 1);
+                    const PrLayout L = pr_layout(c);
+                    if (c.biz * c.biy * L.rp * 2 > kTrXU * kThreads || L.bytes > int(kLds)) continue;
+                    const int bixp = b2 + 8;
+                    const int cs = int(round_up(c.biz * c.biy * bixp, 16) + 8), csd = int(round_up(bov, 16) + 8);
+                    const int dy_off = int(round_up(int64_t(nci) * cs * 2, 16));
+                    const size_t lds = size_t(dy_off) + size_t(nco) * csd * 2;  // the tiled kernels' need
+                    if (lds > kLds) continue;
+                    double eff = 1.0;
+                    const int64_t bo[3] = {b0, b1, b2};
+                    for (int k = 0; k < 3; ++k) eff *= double(cv.O[k]) / double(ceil_div(cv.O[k], bo[k]) * bo[k]);
+                    const double cost = double(c.biz * c.biy * L.rp * 32 + bov * 128) / bov / eff + 8192.0 / bov;
+                    if (cost < best) {
+                        best = cost;
+                        a.BO[0] = b0;
+                        a.BO[1] = b1;
+                        a.BO[2] = b2;
+                        a.biz = c.biz;
+                        a.biy = c.biy;
+                        a.bix = c.bix;
+                        a.bixp = bixp;
+                        a.cs = cs;
+                        a.csd = csd;
+                        a.dy_off = dy_off;
+                        pl.lds = lds;
+                    }
+                }
+            }
+        }
+        // otherwise: W extent a multiple of 8 (an 8-voxel K group stays in one row)
         for (int b2 : {32, 64, 16, 8}) {
+            if (best < 1e299) break;
             for (int b1 = 1; b1 <= 64; b1 *= 2) {
                 for (int b0 = 1; b0 <= 64; b0 *= 2) {
                     const int bov = b0 * b1 * b2;
@@ -1234,7 +1385,9 @@ PlanW plan_wgrad(const Tile3& t, const Conv3& cv, shard_dtype_t dt)
     for (int k = 0; k < 3; ++k) a.NB[k] = int32_t(ceil_div(cv.O[k], a.BO[k]));
     a.nbricks = t.n * int64_t(a.NB[0]) * a.NB[1] * a.NB[2];
     const int64_t groups = int64_t(a.nmb) * a.ncb * a.ntg;
-    a.nsplit = int32_t(std::max<int64_t>(1, std::min<int64_t>(a.nbricks, ceil_div(kTargetBlocks, groups))));
+    // at most one round of resident workgroups: a few workgroups past the
+    // 512 slots would start only when others finish and double the time
+    a.nsplit = int32_t(std::max<int64_t>(1, std::min<int64_t>(a.nbricks, kTargetBlocks / groups)));
     a.nblocks = groups * a.nsplit;
     if (a.nblocks >= (int64_t(1) << 31) || a.nbricks == 0) {
         pl.kind = 0;
@@ -1275,47 +1428,47 @@ bool bf16_pipe_ok(const PlanW& pl)
            nxu <= int64_t(kPipeBXU) * kThreads && ndu <= int64_t(kPipeBDU) * kThreads;
 }
 
-// The direct-load transposed-read kernel: 16 input channels, output channels
-// in whole blocks of 64, unit stride, one kd plane per tap group, no folded
-// halo, tile and dy of < 4 GiB per batch item, packed coordinates in range and
-// staging within its instruction budget and two workgroups' LDS per CU.
+// The row-pair kernel: 16 input channels, output channels in whole blocks of
+// 64, unit stride, one kd plane per tap group, no folded halo, tile and dy of
+// < 4 GiB per batch item, packed coordinates in range, the brick of its own
+// shape (W extent a multiple of 16, an even number of K steps) and staging
+// within its instruction budget and two workgroups' LDS per CU.
 template <int K1, int K2>
-hipError_t launch_bf16_dl(const PlanW& pl, hipStream_t s)
+hipError_t launch_bf16_pr(const PlanW& pl, hipStream_t s)
 {
     const WgArgs& a = pl.a;
-    const TrLayout L = tr_layout(a);
-    auto fn = &wgrad_bf16_dl<K1, K2>;
+    const PrLayout L = pr_layout(a);
+    auto fn = &wgrad_bf16_pr<K1, K2>;
     hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(fn), hipFuncAttributeMaxDynamicSharedMemorySize,
                                        L.bytes);
     if (e != hipSuccess) return e;
     WgArgs aa = a;
-    int bx = L.bixp8, dyo = L.dy_off;
+    int rp = L.rp, dyo = L.dy_off, bufb = L.bufb;
     uint32_t xbu = uint32_t(a.P[0] * a.P[1] * a.P[2] * a.cin * 2);
     uint32_t dbu = uint32_t(a.O[0] * a.O[1] * a.O[2] * a.cout * 2);
-    void* args[] = {&aa, &bx, &dyo, &xbu, &dbu};
+    void* args[] = {&aa, &rp, &dyo, &bufb, &xbu, &dbu};
     return hipLaunchKernel(reinterpret_cast<const void*>(fn), dim3(unsigned(aa.nblocks)), dim3(kThreads), args,
                            size_t(L.bytes), s);
 }
 
-bool bf16_dl_ok(const PlanW& pl)
+bool bf16_pr_ok(const PlanW& pl)
 {
     const WgArgs& a = pl.a;
-    const TrLayout L = tr_layout(a);
+    const PrLayout L = pr_layout(a);
     const int64_t bov = int64_t(a.BO[0]) * a.BO[1] * a.BO[2];
     const int64_t xb = a.P[0] * a.P[1] * a.P[2] * a.cin * 2, db = a.O[0] * a.O[1] * a.O[2] * a.cout * 2;
     return pl.kdg == 1 && pl.wco == 4 && a.cin == 16 && a.cout % 64 == 0 && a.S[0] == 1 && a.S[1] == 1 &&
            a.S[2] == 1 && !a.fold.mask && a.xvec && a.dvec && a.K[2] <= 5 && xb < (int64_t(1) << 32) - 64 &&
-           db < (int64_t(1) << 32) - 64 && a.BO[2] % 8 == 0 && bov % 32 == 0 && L.bixp8 < 512 && a.biy < 1024 &&
-           a.biz < 1024 && a.BO[2] < 512 && a.BO[1] < 1024 && a.BO[0] < 512 &&
-           dl_round(a.biz * a.biy * L.bixp8 * 2) <= kTrXU * kThreads && dl_round(int(bov) * 8) <= kTrDU * kThreads &&
-           L.bytes <= 80 * 1024;
+           db < (int64_t(1) << 32) - 64 && a.BO[2] % 16 == 0 && bov % 32 == 0 && L.rp < 512 && a.biy < 1024 &&
+           a.biz < 1024 && a.BO[2] < 512 && a.BO[1] < 1024 && a.BO[0] < 512 && a.biz == a.BO[0] &&
+           a.biz * a.biy * L.rp * 2 <= kTrXU * kThreads && bov * 8 <= kTrDU * kThreads && L.bytes <= 80 * 1024;
 }
 
 template <int KDG, int K1, int K2, int WCO>
 hipError_t launch_bf16_t(const PlanW& pl, hipStream_t s)
 {
     if constexpr (KDG == 1 && WCO == 4 && K2 <= 5)
-        if (bf16_dl_ok(pl)) return launch_bf16_dl<K1, K2>(pl, s);
+        if (!force_tiled() && bf16_pr_ok(pl)) return launch_bf16_pr<K1, K2>(pl, s);
     if (!bf16_pipe_ok(pl)) return launch_with_lds(&wgrad_bf16_tiled<KDG, K1, K2, WCO>, pl, s);
     const WgArgs& a = pl.a;
     const int64_t nxu = int64_t(a.biz) * a.biy * ((a.bix + 3) / 4) * ((4 / WCO) * 2);
