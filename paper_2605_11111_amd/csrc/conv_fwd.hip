@@ -359,9 +359,13 @@ __global__ __launch_bounds__(256) void wfrag_kernel(const T* w, uint4* wfrag, in
 }
 
 template <typename T>
-PlanF plan_fwd_t(const Tile3& t, const Conv3& cv)
+PlanF plan_fwd_t(const Tile3& t, const Conv3& cv, const int64_t* oext = nullptr, int64_t fix_cc = 0)
 {
+    // oext: the extent of the outputs to compute (a region; default the whole
+    // box); fix_cc: a channel pass width to keep (a region's outputs are then
+    // summed in the same order as in the whole box's plan)
     PlanF pl{};
+    const int64_t O[3] = {oext ? oext[0] : cv.O[0], oext ? oext[1] : cv.O[1], oext ? oext[2] : cv.O[2]};
     constexpr int kc = Traits<T>::kc;
     constexpr int esz = Traits<T>::esz;
     const int64_t nt = ceil_div(cv.cout, 32);
@@ -390,13 +394,16 @@ PlanF plan_fwd_t(const Tile3& t, const Conv3& cv)
         }
         // channel pass width: the largest multiple of kc whose brick fits
         int64_t cc = cfull;
-        while (cc > kc && size_t(biv * cc * esz) > kLdsPref) cc = round_up(cc / 2, kc);
+        if (fix_cc > 0)
+            cc = fix_cc;
+        else
+            while (cc > kc && size_t(biv * cc * esz) > kLdsPref) cc = round_up(cc / 2, kc);
         size_t lds = size_t(biv * cc * esz);
         if (lds > kLdsMax) return;
         double eff = double(b0 * b1 * b2) / double(cap);
         for (int k = 0; k < 3; ++k) {
-            const int64_t nb = ceil_div(cv.O[k], bo[k]);
-            eff *= double(cv.O[k]) / double(nb * bo[k]);
+            const int64_t nb = ceil_div(O[k], bo[k]);
+            eff *= double(O[k]) / double(nb * bo[k]);
         }
         double cost = double(biv) / double(b0 * b1 * b2) / eff;
         if (lds > kLdsPref) cost *= 1.5;
@@ -415,10 +422,10 @@ PlanF plan_fwd_t(const Tile3& t, const Conv3& cv)
         }
     };
     for (int64_t b2 = 1; b2 <= cap; b2 *= 2) {
-        const int64_t w2 = std::min(b2, cv.O[2]);
+        const int64_t w2 = std::min(b2, O[2]);
         for (int64_t b1 = 1; b1 * w2 <= cap; b1 *= 2) {
-            const int64_t w1 = std::min(b1, cv.O[1]);
-            const int64_t w0 = std::min(cap / (w1 * w2), cv.O[0]);
+            const int64_t w1 = std::min(b1, O[1]);
+            const int64_t w0 = std::min(cap / (w1 * w2), O[0]);
             consider(w0, w1, w2);
             for (int64_t b0 = 1; b0 < w0; b0 *= 2) consider(b0, w1, w2);
         }
@@ -508,10 +515,17 @@ template <typename T>
 hipError_t run_fwd(const Tile3& t, const Conv3& cv, const void* tile, const void* w, void* y, const OutMap& om,
                    const Region& rg, const Fold* fold, bool rows, void* ws, bool frags_ready, hipStream_t s)
 {
-    // the plan of the whole output box, its brick grid cut to the region: every
-    // output is summed in the same order whatever region computes it
+    // the plan of the whole output box; a region smaller than it takes bricks
+    // of its own shape with the same channel passes, so that every output is
+    // summed in the same order whatever region computes it
     PlanF pl = plan_fwd_t<T>(t, cv);
     if (!pl.ok) return hipErrorInvalidValue;
+    if (rg.ext[0] != cv.O[0] || rg.ext[1] != cv.O[1] || rg.ext[2] != cv.O[2]) {
+        const PlanF pr = plan_fwd_t<T>(t, cv, rg.ext, pl.a.cc);
+        if (pr.ok && pr.rm == pl.rm && pr.rn == pl.rn && pr.a.cc == pl.a.cc && pr.a.npass == pl.a.npass &&
+            pr.a.nkc == pl.a.nkc && pr.a.nt == pl.a.nt)
+            pl = pr;
+    }
     for (int k = 0; k < 3; ++k) {
         pl.a.O[k] = rg.ext[k];
         pl.a.NB[k] = int32_t(ceil_div(rg.ext[k], pl.a.BO[k]));
