@@ -298,11 +298,12 @@ shard_status_t shard_conv_wgrad(const shard_tile_t* x, shard_dtype_t dtype, cons
  * comes from the slab of its margin (`halo`, NULL = every margin zero), a
  * corner voxel from the later axis's slab. dw equals shard_halo_unpack of every
  * slab followed by shard_conv_wgrad: bit for bit when both select the same
- * kernel (margins on one axis, 16-byte aligned slabs, shapes outside the
- * transposed-read kernels': 3x3x3 or 1x3x3 at unit stride, and 16 input
- * channels at unit stride with output channels in blocks of 64; or both calls
- * under SHARD_KERNELS_TILED) and on integer-valued data, otherwise up to the
- * order of the binary32 sums. Other arguments, workspace and errors: as
+ * kernel (16-byte aligned slabs; shapes outside the transposed-read kernel
+ * for 3x3x3 or 1x3x3 at unit stride with channel counts other than 32 and 64;
+ * margins on one axis unless the shape has 16 input channels at unit stride
+ * with output channels in blocks of 64; or both calls under
+ * SHARD_KERNELS_TILED) and on integer-valued data, otherwise up to the order
+ * of the binary32 sums. Other arguments, workspace and errors: as
  * shard_conv_wgrad; SHARD_ERR_INVALID also for a slab not aligned to the
  * element size.
  */

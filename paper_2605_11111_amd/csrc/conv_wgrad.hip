@@ -65,6 +65,7 @@ struct WgArgs {
     int32_t xvec, dvec;   // 16-byte vector loads allowed (alignment of base and channel rows)
     int64_t nblocks;
     Fold fold;            // halo folded into the loads when fold.mask != 0
+    const char* zeros;    // 16 zero bytes in device memory (the status block's)
 };
 
 struct PlanW {
@@ -585,7 +586,7 @@ struct PrOps {
     uint2 b[NT > 0 ? NT : 1][2];
 };
 
-template <int K1, int K2, int TH>
+template <int K1, int K2, int TH, bool FOLD>
 __device__ __forceinline__ void wgrad_bf16_pr_body(const WgArgs& a, int rp, int dy_off, int bufb, uint32_t xbatch,
                                                    uint32_t dbatch)
 {
@@ -638,6 +639,18 @@ __device__ __forceinline__ void wgrad_bf16_pr_body(const WgArgs& a, int rp, int 
     const int O0 = int(a.O[0]), O1 = int(a.O[1]), O2 = int(a.O[2]);
     const int cout = int(a.cout);
     constexpr uint32_t kOut = 0xFFFFFFF0u;
+    // per axis: first tile row with data and the count of such rows (all P
+    // rows; with a folded halo, a margin without a slab is zero, not read)
+    int V[6] = {0, P0, 0, P1, 0, P2};
+    if constexpr (FOLD) {
+        for (int k = 0; k < 3; ++k) {
+            if (!((a.fold.mask >> k) & 1u)) continue;
+            const int lo = a.fold.slab[k][0] ? 0 : int(a.fold.lo[k]);
+            const int hi = a.fold.slab[k][1] ? int(a.P[k]) : int(a.fold.lo[k] + a.fold.ext[k]);
+            V[2 * k] = lo;
+            V[2 * k + 1] = hi - lo;
+        }
+    }
 
     // loads of brick br into the buffer at byte offset boff
     auto stage = [&](int64_t br, int boff) {
@@ -649,17 +662,49 @@ __device__ __forceinline__ void wgrad_bf16_pr_body(const WgArgs& a, int rp, int 
             const_cast<char*>(a.tile) + int64_t(nn) * xbatch, short(0), int(xbatch), 0x00020000);
         const __amdgpu_buffer_rsrc_t rd = __builtin_amdgcn_make_buffer_rsrc(
             const_cast<char*>(a.dy) + int64_t(nn) * dbatch, short(0), int(dbatch), 0x00020000);
+        // with a folded halo, a brick whose input rows touch a margin takes each
+        // voxel from its own buffer (tile or slab, per lane: global->LDS loads
+        // with per-lane addresses, zero padding from a zeroed source); every
+        // other brick reads the tile as without one
+        bool plain = true;
+        if constexpr (FOLD) {
+            const int64_t fi[3] = {i0, i1, i2}, fe[3] = {a.biz, a.biy, a.bix};
+            for (int k = 0; k < 3; ++k)
+                if ((a.fold.mask >> k) & 1u)
+                    plain = plain && (fi[k] >= a.fold.lo[k] || !a.fold.slab[k][0]) &&
+                            (fi[k] + fe[k] <= a.fold.lo[k] + a.fold.ext[k] || !a.fold.slab[k][1]);
+        }
+        if (plain) {
 #pragma unroll
-        for (int i = 0; i < kTrXU; ++i) {
-            if (i < nxi) {
-                const int c = px[i];
-                const int t0 = i0 + (c >> 20), t1 = i1 + ((c >> 10) & 1023), t2 = i2 + ((c >> 1) & 511);
-                const bool ok = c >= 0 && uint32_t(t0) < uint32_t(P0) && uint32_t(t1) < uint32_t(P1) &&
-                                uint32_t(t2) < uint32_t(P2);
-                const uint32_t off = ((uint32_t(t0 * P1 + t1) * uint32_t(P2) + uint32_t(t2)) * 16u +
-                                      uint32_t(8 * (c & 1))) * 2u;
-                __builtin_amdgcn_raw_ptr_buffer_load_lds(rx, SC_LDSW(lds + boff + i * 4096 + wave * 1024), 16,
-                                                         ok ? off : kOut, 0, 0, 0);
+            for (int i = 0; i < kTrXU; ++i) {
+                if (i < nxi) {
+                    const int c = px[i];
+                    const int t0 = i0 + (c >> 20), t1 = i1 + ((c >> 10) & 1023), t2 = i2 + ((c >> 1) & 511);
+                    // in range of the tile's rows that hold data (margins without a
+                    // slab are zero)
+                    const bool ok = c >= 0 && uint32_t(t0 - V[0]) < uint32_t(V[1]) &&
+                                    uint32_t(t1 - V[2]) < uint32_t(V[3]) && uint32_t(t2 - V[4]) < uint32_t(V[5]);
+                    const uint32_t off = ((uint32_t(t0 * P1 + t1) * uint32_t(P2) + uint32_t(t2)) * 16u +
+                                          uint32_t(8 * (c & 1))) * 2u;
+                    __builtin_amdgcn_raw_ptr_buffer_load_lds(rx, SC_LDSW(lds + boff + i * 4096 + wave * 1024), 16,
+                                                             ok ? off : kOut, 0, 0, 0);
+                }
+            }
+        } else {
+#pragma unroll
+            for (int i = 0; i < kTrXU; ++i) {
+                if (i < nxi) {
+                    const int c = px[i];
+                    const int t0 = i0 + (c >> 20), t1 = i1 + ((c >> 10) & 1023), t2 = i2 + ((c >> 1) & 511);
+                    const bool ok = c >= 0 && uint32_t(t0) < uint32_t(P0) && uint32_t(t1) < uint32_t(P1) &&
+                                    uint32_t(t2) < uint32_t(P2);
+                    const char* src = a.zeros;
+                    if (ok) {
+                        const char* v = fold_voxel(a.fold, a.tile, nn, t0, t1, t2, 32);
+                        if (v) src = v + 16 * (c & 1);
+                    }
+                    __builtin_amdgcn_global_load_lds(src, SC_LDSW(lds + boff + i * 4096 + wave * 1024), 16, 0, 0);
+                }
             }
         }
 #pragma unroll
@@ -793,16 +838,16 @@ __device__ __forceinline__ void wgrad_bf16_pr_body(const WgArgs& a, int rp, int 
     }
 }
 
-template <int K1, int K2>
+template <int K1, int K2, bool FOLD>
 __global__ __launch_bounds__(kThreads, 2) void wgrad_bf16_pr(WgArgs a, int rp, int dy_off, int bufb, uint32_t xbatch,
                                                              uint32_t dbatch)
 {
     // waves 0, 1 and waves 2, 3 (a wave-uniform choice, made scalar so that the
     // compiler keeps the step's bookkeeping in scalar registers)
     if (__builtin_amdgcn_readfirstlane(threadIdx.x >> 7) == 0)
-        wgrad_bf16_pr_body<K1, K2, 0>(a, rp, dy_off, bufb, xbatch, dbatch);
+        wgrad_bf16_pr_body<K1, K2, 0, FOLD>(a, rp, dy_off, bufb, xbatch, dbatch);
     else
-        wgrad_bf16_pr_body<K1, K2, 1>(a, rp, dy_off, bufb, xbatch, dbatch);
+        wgrad_bf16_pr_body<K1, K2, 1, FOLD>(a, rp, dy_off, bufb, xbatch, dbatch);
 }
 
 template <int TPW>
@@ -1429,7 +1474,8 @@ bool bf16_pipe_ok(const PlanW& pl)
 }
 
 // The row-pair kernel: 16 input channels, output channels in whole blocks of
-// 64, unit stride, one kd plane per tap group, no folded halo, tile and dy of
+// 64, unit stride, one kd plane per tap group (a folded halo on any axes, from
+// 16-byte aligned slabs, as the alignment checks require), tile and dy of
 // < 4 GiB per batch item, packed coordinates in range, the brick of its own
 // shape (W extent a multiple of 16, an even number of K steps) and staging
 // within its instruction budget and two workgroups' LDS per CU.
@@ -1438,7 +1484,7 @@ hipError_t launch_bf16_pr(const PlanW& pl, hipStream_t s)
 {
     const WgArgs& a = pl.a;
     const PrLayout L = pr_layout(a);
-    auto fn = &wgrad_bf16_pr<K1, K2>;
+    auto fn = a.fold.mask ? &wgrad_bf16_pr<K1, K2, true> : &wgrad_bf16_pr<K1, K2, false>;
     hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(fn), hipFuncAttributeMaxDynamicSharedMemorySize,
                                        L.bytes);
     if (e != hipSuccess) return e;
@@ -1458,7 +1504,7 @@ bool bf16_pr_ok(const PlanW& pl)
     const int64_t bov = int64_t(a.BO[0]) * a.BO[1] * a.BO[2];
     const int64_t xb = a.P[0] * a.P[1] * a.P[2] * a.cin * 2, db = a.O[0] * a.O[1] * a.O[2] * a.cout * 2;
     return pl.kdg == 1 && pl.wco == 4 && a.cin == 16 && a.cout % 64 == 0 && a.S[0] == 1 && a.S[1] == 1 &&
-           a.S[2] == 1 && !a.fold.mask && a.xvec && a.dvec && a.K[2] <= 5 && xb < (int64_t(1) << 32) - 64 &&
+           a.S[2] == 1 && a.xvec && a.dvec && a.K[2] <= 5 && xb < (int64_t(1) << 32) - 64 &&
            db < (int64_t(1) << 32) - 64 && a.BO[2] % 16 == 0 && bov % 32 == 0 && L.rp < 512 && a.biy < 1024 &&
            a.biz < 1024 && a.BO[2] < 512 && a.BO[1] < 1024 && a.BO[0] < 512 && a.biz == a.BO[0] &&
            a.biz * a.biy * L.rp * 2 <= kTrXU * kThreads && bov * 8 <= kTrDU * kThreads && L.bytes <= 80 * 1024;
@@ -1553,7 +1599,8 @@ namespace {
 
 __global__ void wgrad_status_clear(uint32_t* status)
 {
-    if (threadIdx.x == 0) status[0] = 0u;
+    // the status word and the zero source (status block bytes 0 .. 127)
+    if (threadIdx.x < 32) status[threadIdx.x] = 0u;
 }
 
 }  // namespace
@@ -1617,6 +1664,7 @@ hipError_t run_wgrad(const Tile3& t, const Conv3& cv, shard_dtype_t dt, const vo
     pl.a.dvec = (reinterpret_cast<uintptr_t>(dy) % 16 == 0) && (cv.cout * esz) % 16 == 0;
     pl.a.part = static_cast<float*>(ws);
     pl.a.dw = dw;
+    pl.a.zeros = static_cast<const char*>(ws_all) + kWgradZeroOff;
     hipError_t e = pl.kind == 1 ? launch_bf16(pl, s) : launch_f32(t, cv, pl, s);
     if (e != hipSuccess) return e;
     const int64_t total = int64_t(pl.a.nmb) * pl.a.ncb * pl.a.ntg * pl.a.blk;

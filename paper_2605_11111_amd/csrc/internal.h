@@ -196,8 +196,10 @@ bool force_tiled();
 
 // The weight-gradient workspace starts with a status block: its first 32-bit
 // word is 0 after a call completed normally and nonzero when a bounded wait of
-// the kernel gave up (dw then holds NaN). Cleared by every call.
+// the kernel gave up (dw then holds NaN); bytes [kWgradZeroOff, +64) are zeros,
+// a source for loads of zero padding. Cleared by every call.
 constexpr size_t kWgradStatusBytes = 256;
+constexpr size_t kWgradZeroOff = 64;
 constexpr uint32_t kDefaultWaitPolls = 1u << 20;
 hipError_t launch_wgrad_status_clear(uint32_t* status, hipStream_t s);
 

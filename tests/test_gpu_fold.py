@@ -229,7 +229,7 @@ def test_folded_wgrad_kernel_variants_integer_exact(sc, name, algo):
     assert np.array_equal(got, ref)
 
 
-@pytest.mark.parametrize("name", ["c3_3d_bf16", "c2_2d_bf16"])
+@pytest.mark.parametrize("name", ["c3_3d_bf16", "c2_2d_bf16", "c4_3d_bf16_k5"])
 def test_full_size_folded_wgrad_equals_unpacked(sc, name):
     import torch
     from gpu_util import dy_box, run_wgrad
