@@ -175,6 +175,69 @@ size_t wt_bytes(const Phase& ph)
     return size_t(round_up(ph.cf.cout * ph.tf.c * ph.cf.taps() * ph.tf.esz, 256));
 }
 
+// W pairing. A phase whose outputs have 16 channels fills only half of a
+// 32-wide matrix tile. With unit stride along W, output row u = 2 u' + p and
+// input row u + k - pad = 2 (u' + m) + q for m = floor((p + k - pad) / 2),
+// q = (p + k - pad) mod 2, so the phase is also a convolution over the
+// W-halved grid with channels (p, ci) out and (q, co) in: dy read as
+// [..][O2 / 2][2 cout] and the tile rows as [..][M2 / 2][2 cin] are the same
+// bytes (channels-last), and the kernel along W has ceil taps m - mlo,
+//   w2[p cin + ci][q cout + co][u0][u1][m'] = w_phi[ci][co][u0][u1][2 (m' + mlo) + q - p + pad]
+// (zero where that tap is outside the kernel). 32 output channels fill the
+// tile; the zero taps cost (2 ceil(...) ) / K2 - 1 of extra products instead of
+// the half tile.
+struct Paired {
+    bool ok;
+    Phase ph;    // the W-halved problem
+    int32_t mlo; // first m
+};
+
+Paired pair_w(const Tile3& t, const Phase& ph)
+{
+    Paired pr{};
+    pr.ok = false;
+    if (force_tiled() || ph.empty || ph.zero || t.c != 16 || ph.k.S[2] != 1 || ph.tf.P[2] % 2 != 0 ||
+        ph.cf.O[2] % 2 != 0 || ph.om.str[3] != t.c)
+        return pr;
+    const int64_t K = ph.cf.K[2], pad = ph.cf.pad[2];
+    auto fdiv = [](int64_t a, int64_t b) { return a >= 0 ? a / b : -((-a + b - 1) / b); };
+    const int64_t mlo = fdiv(-pad, 2), mhi = fdiv(1 + (K - 1) - pad, 2);
+    pr.ph = ph;
+    pr.ph.tf.c = 2 * ph.tf.c;
+    pr.ph.tf.P[2] = pr.ph.tf.ext[2] = ph.tf.P[2] / 2;
+    pr.ph.cf.cout = 2 * ph.cf.cout;
+    pr.ph.cf.K[2] = mhi - mlo + 1;
+    pr.ph.cf.pad[2] = -mlo;
+    pr.ph.cf.O[2] = ph.cf.O[2] / 2;
+    pr.ph.om.str[3] = 2 * ph.om.str[3];
+    pr.mlo = int32_t(mlo);
+    pr.ok = true;
+    return pr;
+}
+
+template <typename T>
+__global__ __launch_bounds__(256) void dgrad_weights_paired(const T* __restrict__ w, T* __restrict__ wt, int64_t cin,
+                                                            int64_t cout, SubKernel k, int32_t K2p, int32_t mlo,
+                                                            int32_t pad2)
+{
+    const int64_t taps = int64_t(k.Ku[0]) * k.Ku[1] * K2p;
+    const int64_t total = 4 * cin * cout * taps;
+    for (int64_t e = int64_t(blockIdx.x) * 256 + threadIdx.x; e < total; e += int64_t(gridDim.x) * 256) {
+        const int64_t mp = e % K2p, u1 = (e / K2p) % k.Ku[1], u0 = (e / (int64_t(k.Ku[1]) * K2p)) % k.Ku[0];
+        const int64_t ic = (e / taps) % (2 * cout), oc = e / (taps * 2 * cout);
+        const int64_t p = oc / cin, ci = oc % cin, q = ic / cout, co = ic % cout;
+        const int64_t u2 = 2 * (mp + mlo) + q - p + pad2;
+        T v = T(0);
+        if (u2 >= 0 && u2 < k.Ku[2]) {
+            const int64_t t0 = k.r[0] + int64_t(k.S[0]) * (k.Ku[0] - 1 - u0);
+            const int64_t t1 = k.r[1] + int64_t(k.S[1]) * (k.Ku[1] - 1 - u1);
+            const int64_t t2 = k.r[2] + int64_t(k.S[2]) * (k.Ku[2] - 1 - u2);
+            v = w[(((co * cin + ci) * k.K[0] + t0) * k.K[1] + t1) * k.K[2] + t2];
+        }
+        wt[e] = v;
+    }
+}
+
 }  // namespace
 
 size_t conv_dgrad_workspace(const Tile3& t, const Conv3& cv, shard_dtype_t dt)
@@ -182,7 +245,10 @@ size_t conv_dgrad_workspace(const Tile3& t, const Conv3& cv, shard_dtype_t dt)
     if (force_generic()) return 0;
     size_t need = 0;
     for_each_phase(t, cv, [&](const Phase& ph) {
-        if (!ph.empty && !ph.zero) need = std::max(need, wt_bytes(ph) + conv_fwd_workspace(ph.tf, ph.cf, dt));
+        if (ph.empty || ph.zero) return;
+        const Paired pr = pair_w(t, ph);
+        const Phase& q = pr.ok ? pr.ph : ph;
+        need = std::max(need, wt_bytes(q) + conv_fwd_workspace(q.tf, q.cf, dt));
     });
     return need;
 }
@@ -210,6 +276,26 @@ hipError_t launch_conv_dgrad(const Tile3& t, const Conv3& cv, shard_dtype_t dt, 
                 return;
             }
             char* wt = static_cast<char*>(ws);
+            const Paired pr = pair_w(t, ph);
+            if (pr.ok) {
+                const Phase& q = pr.ph;
+                const int64_t total = q.cf.cout * q.tf.c * q.cf.taps();
+                const unsigned grid =
+                    unsigned(std::max<int64_t>(1, std::min<int64_t>(ceil_div(total, 256), 4096)));
+                const int32_t K2p = int32_t(q.cf.K[2]), pad2 = int32_t(ph.cf.pad[2]);
+                if (dt == SHARD_BF16)
+                    hipLaunchKernelGGL(dgrad_weights_paired<bf16_t>, dim3(grid), dim3(256), 0, s,
+                                       static_cast<const bf16_t*>(w), reinterpret_cast<bf16_t*>(wt), t.c, cv.cout,
+                                       ph.k, K2p, pr.mlo, pad2);
+                else
+                    hipLaunchKernelGGL(dgrad_weights_paired<float>, dim3(grid), dim3(256), 0, s,
+                                       static_cast<const float*>(w), reinterpret_cast<float*>(wt), t.c, cv.cout,
+                                       ph.k, K2p, pr.mlo, pad2);
+                err = hipGetLastError();
+                if (err == hipSuccess)
+                    err = launch_conv_fwd_mapped(q.tf, q.cf, dt, dy, wt, dtile, q.om, wt + wt_bytes(q), s);
+                return;
+            }
             const int64_t total = t.c * cv.cout * ph.cf.taps();
             const unsigned grid = unsigned(std::max<int64_t>(1, std::min<int64_t>(ceil_div(total, 256), 4096)));
             if (dt == SHARD_BF16)
