@@ -162,6 +162,13 @@ EDGE = [
     # the 32-channel K chunk in the second)
     ("3d_narrow_out", "bf16", 1, 64, 16, (10, 12, 40), (2, 1, 1), (3, 3, 3), (1, 1, 1)),
     ("2d_narrow_out_k5", "bf16", 2, 48, 12, (21, 33), (2, 1), (5, 5), (1, 1)),
+    # 16 input channels, output channels in blocks of 64: the row-pair weight
+    # gradient (row pairs and W pairs; a 1x1 kernel leaves half the waves
+    # without tiles; ragged W runs; two output-channel blocks)
+    ("2d_c16_k3_rowpair", "bf16", 2, 16, 64, (34, 50), (2, 1), (3, 3), (1, 1)),
+    ("2d_c16_k1_rowpair", "bf16", 1, 16, 64, (33, 45), (2, 1), (1, 1), (1, 1)),
+    ("1d_c16_k5_rowpair", "bf16", 1, 16, 128, (300,), (3,), (5,), (1,)),
+    ("3d_c16_k5_ragged", "bf16", 1, 16, 64, (11, 13, 37), (2, 1, 1), (5, 5, 5), (1, 1, 1)),
 ]
 
 

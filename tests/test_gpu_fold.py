@@ -260,6 +260,11 @@ EDGE = [
     # two batch items, three shards along D: both boundary planes of the middle
     # shard go in one W-march launch
     ("3d_batch2_split_d", "bf16", 2, 32, 32, (12, 10, 40), (3, 1, 1), (3, 3, 3), (1, 1, 1)),
+    # the row-pair weight gradient's per-lane slab loads: margins on two axes,
+    # a W split, a 5x5x5 corner shard
+    ("2d_c16_k3_two_axes", "bf16", 2, 16, 64, (26, 40), (2, 2), (3, 3), (1, 1)),
+    ("1d_c16_k5_split_w", "bf16", 1, 16, 64, (200,), (3,), (5,), (1,)),
+    ("3d_c16_k5_two_axes", "bf16", 1, 16, 64, (12, 14, 36), (2, 2, 1), (5, 5, 5), (1, 1, 1)),
 ]
 
 
