@@ -245,32 +245,49 @@ __global__ __launch_bounds__(kThreads, 2) void conv_fwd_tiled(FwdArgs a)
         // iteration it multiplies; every load is unconditional (the one past the
         // last iteration re-reads the last, in bounds), so the waits before each
         // set's MFMAs cover exactly that set's loads.
+        // The iteration state is advanced by uniform increments (scalar
+        // registers): the weight fragments' base moves by one K-chunk per
+        // iteration and skips the other passes' chunks at the end of a tap;
+        // the tap's brick offset moves by one voxel, and by the rest of a row
+        // or plane where kw or kh wraps. A lane adds only its own offsets.
         struct TapIt {
-            int t0, t1, t2, kc;
+            const uint4* b;  // fragment (tap, chunk) of N tile nt0
+            int toff;        // brick voxel offset of the tap
+            int kc, t2, t1;
         };
+        const int64_t ks = int64_t(a.nt) * 64;                 // one K-chunk
+        const int64_t ts = int64_t(a.nkc - kcp) * a.nt * 64;  // the other passes' chunks
+        const int wrap2 = a.BI[2] - a.K[2], wrap1 = plane - a.K[1] * a.BI[2];
         auto step_tap = [&](TapIt& s) {
+            s.b += ks;
             if (++s.kc == kcp) {
                 s.kc = 0;
+                s.b += ts;
+                ++s.toff;
                 if (++s.t2 == a.K[2]) {
                     s.t2 = 0;
+                    s.toff += wrap2;
                     if (++s.t1 == a.K[1]) {
                         s.t1 = 0;
-                        ++s.t0;
+                        s.toff += wrap1;
                     }
                 }
             }
         };
+        // the A fragment's byte address: voxel v's unit q ^ swz(v) (16 bytes),
+        // formed with a 24-bit multiply-add (LDS offsets are far below 2^24)
+        const uint32_t nq16 = uint32_t(a.nq) * 16u, qm = uint32_t(a.qmask);
+        const int vsh = a.vpl_sh;
+        const char* ldsb = reinterpret_cast<const char*>(lds);
         auto load = [&](const TapIt& s, uint4 (&av)[RM], uint4 (&bv)[RN]) {
-            const int tap = (s.t0 * a.K[1] + s.t1) * a.K[2] + s.t2;
-            const int64_t fb = (int64_t(tap) * a.nkc + p * kcp + s.kc) * a.nt + nt0;
 #pragma unroll
-            for (int j = 0; j < RN; ++j) bv[j] = a.wfrag[(fb + j) * 64 + lane];
-            const int toff = s.t0 * plane + s.t1 * a.BI[2] + s.t2;
-            const int q = 2 * s.kc + g;
+            for (int j = 0; j < RN; ++j) bv[j] = s.b[j * 64 + lane];
+            const uint32_t q = uint32_t(2 * s.kc + g);
 #pragma unroll
             for (int i = 0; i < RM; ++i) {
-                const int v = vbase[i] + toff;
-                av[i] = lds[v * a.nq + (q ^ swz(v, a.vpl_sh, a.qmask))];
+                const uint32_t v = uint32_t(vbase[i] + s.toff);
+                const uint32_t u = (q ^ ((v >> vsh) & qm)) << 4;
+                av[i] = *reinterpret_cast<const uint4*>(ldsb + (__umul24(v, nq16) + u));
             }
         };
         auto mma = [&](const uint4 (&av)[RM], const uint4 (&bv)[RN]) {
@@ -279,7 +296,7 @@ __global__ __launch_bounds__(kThreads, 2) void conv_fwd_tiled(FwdArgs a)
 #pragma unroll
                 for (int j = 0; j < RN; ++j) mfma_step<T>(acc[i][j], av[i], bv[j]);
         };
-        TapIt nx{0, 0, 0, 0};
+        TapIt nx{a.wfrag + (int64_t(p) * kcp * a.nt + nt0) * 64, 0, 0, 0, 0};
         uint4 a0[RM], b0[RN], a1[RM], b1[RN];
         load(nx, a0, b0);
         int it = 0;
