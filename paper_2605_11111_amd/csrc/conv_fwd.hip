@@ -18,9 +18,10 @@
 // The B operand (weights) is pre-arranged by `wfrag_kernel` so that one
 // coalesced 1 KiB load per wave yields a ready fragment.
 //
-// LDS layout: voxel v of the input brick occupies NQ 16-byte units; unit q
-// of voxel v sits at v*NQ + (q ^ swz(v)), an XOR swizzle that spreads the 16
-// lanes of a ds_read_b128 phase over distinct bank groups for unit-stride rows.
+// LDS layout: voxel v of the input brick occupies NQ 16-byte units, stored
+// unit-major: unit q of voxel v at q * NV + v (NV the brick's voxels), so that
+// lanes reading consecutive voxels read consecutive 16-byte words and a lane's
+// address for a tap is its own fixed part plus a uniform offset.
 #include <algorithm>
 #include <cstdlib>
 #include <type_traits>
@@ -50,8 +51,6 @@ struct FwdArgs {
     int32_t BI[3];     // input brick
     int32_t NB[3];     // bricks per axis
     int32_t nq;        // 16-byte units per voxel in LDS (per pass)
-    int32_t vpl_sh;    // swizzle period, log2 (voxels per 256 B line times the W stride, rounded down to 2^k)
-    int32_t qmask;     // swizzle mask
     int32_t cc;        // channels per pass
     int32_t npass;
     int32_t nkc;       // K-chunks over all input channels
@@ -83,8 +82,6 @@ struct Traits<float> {
     static constexpr int kc = 8;
     static constexpr int esz = 4;
 };
-
-__device__ __forceinline__ int swz(int v, int vpl_sh, int qmask) { return (v >> vpl_sh) & qmask; }
 
 // Visit every 16-byte unit (voxel v = (z, y, x) of the brick, channel unit q)
 // once across the block. When a (z, y) row of units fits the block, a thread
@@ -123,6 +120,7 @@ __device__ __forceinline__ void stage_brick(const FwdArgs& a, uint4* lds, int64_
 {
     constexpr int kPerUnit = 16 / Traits<T>::esz;
     const bool vec_ok = a.vec != 0;
+    const int nvp = a.BI[0] * a.BI[1] * a.BI[2];  // voxels per unit plane
     if (a.fold.mask) {
         // margin voxels come from the received slabs (or are zero)
         for_each_unit(a, [&](int v, int q, int z, int y, int x) {
@@ -143,7 +141,7 @@ __device__ __forceinline__ void stage_brick(const FwdArgs& a, uint4* lds, int64_
                     }
                 }
             }
-            lds[v * a.nq + (q ^ swz(v, a.vpl_sh, a.qmask))] = val;
+            lds[q * nvp + v] = val;
         });
         return;
     }
@@ -163,7 +161,7 @@ __device__ __forceinline__ void stage_brick(const FwdArgs& a, uint4* lds, int64_
                 val = *reinterpret_cast<const uint4*>(tmp);
             }
         }
-        lds[v * a.nq + (q ^ swz(v, a.vpl_sh, a.qmask))] = val;
+        lds[q * nvp + v] = val;
     });
 }
 
@@ -274,21 +272,19 @@ __global__ __launch_bounds__(kThreads, 2) void conv_fwd_tiled(FwdArgs a)
                 }
             }
         };
-        // the A fragment's byte address: voxel v's unit q ^ swz(v) (16 bytes),
-        // formed with a 24-bit multiply-add (LDS offsets are far below 2^24)
-        const uint32_t nq16 = uint32_t(a.nq) * 16u, qm = uint32_t(a.qmask);
-        const int vsh = a.vpl_sh;
+        // the A fragment's byte address: unit plane 2 kc + g, voxel
+        // vbase + toff; the lane's part is fixed, the rest uniform
         const char* ldsb = reinterpret_cast<const char*>(lds);
+        const uint32_t plane16 = uint32_t(a.BI[0] * a.BI[1] * a.BI[2]) * 16u;
+        uint32_t abase[RM];
+#pragma unroll
+        for (int i = 0; i < RM; ++i) abase[i] = uint32_t(g) * plane16 + uint32_t(vbase[i]) * 16u;
         auto load = [&](const TapIt& s, uint4 (&av)[RM], uint4 (&bv)[RN]) {
 #pragma unroll
             for (int j = 0; j < RN; ++j) bv[j] = s.b[j * 64 + lane];
-            const uint32_t q = uint32_t(2 * s.kc + g);
+            const uint32_t u = uint32_t(2 * s.kc) * plane16 + uint32_t(s.toff) * 16u;
 #pragma unroll
-            for (int i = 0; i < RM; ++i) {
-                const uint32_t v = uint32_t(vbase[i] + s.toff);
-                const uint32_t u = (q ^ ((v >> vsh) & qm)) << 4;
-                av[i] = *reinterpret_cast<const uint4*>(ldsb + (__umul24(v, nq16) + u));
-            }
+            for (int i = 0; i < RM; ++i) av[i] = *reinterpret_cast<const uint4*>(ldsb + (abase[i] + u));
         };
         auto mma = [&](const uint4 (&av)[RM], const uint4 (&bv)[RN]) {
 #pragma unroll
@@ -460,11 +456,6 @@ PlanF plan_fwd_t(const Tile3& t, const Conv3& cv, const int64_t* oext = nullptr,
         a.pad[k] = int32_t(cv.pad[k]);
     }
     a.nq = int32_t(a.cc * esz / 16);
-    const int vpl = std::max(1, 16 / a.nq);
-    a.vpl_sh = 0;
-    while ((int64_t(2) << a.vpl_sh) <= int64_t(vpl) * a.S[2]) ++a.vpl_sh;
-    // XOR swizzle only when the unit count is a power of two (stays inside the voxel)
-    a.qmask = (a.nq & (a.nq - 1)) == 0 ? int32_t(std::min(a.nq, 16) - 1) : 0;
     a.npass = int32_t(ceil_div(cfull, a.cc));
     // fragment counts cover every index the kernel forms: npass * (cc / kc)
     // K-chunks and ng * rn N tiles; the padding holds zero weights
