@@ -57,6 +57,7 @@ struct FwdArgs {
     int32_t nt;        // 32-wide N tiles over all output channels
     int32_t ng;        // N groups (workgroups along N)
     int32_t vec;       // 16-byte loads allowed (tile base and channel rows aligned)
+    int32_t yvec;      // 16-byte output stores allowed (y, the output map and cout aligned)
     int64_t nblocks;
     int64_t ybase, ys[4];  // output map: element of (n, o0, o1, o2, co) = ybase + n*ys0 + ... + co
     int64_t org[3];        // origin of the computed region of outputs (O is its extent)
@@ -307,10 +308,64 @@ __global__ __launch_bounds__(kThreads, 2) void conv_fwd_tiled(FwdArgs a)
         if (it < iters) mma(a0, b0);
     }
 
-    // epilogue: lane holds column lane%32, rows 8*(r/4) + 4*g + (r%4); the
-    // brick coordinates of a row are advanced from the previous row's (carries
-    // instead of divisions)
-    T* y = reinterpret_cast<T*>(a.y);
+    // epilogue: lane holds column lane%32, rows 8*(r/4) + 4*g + (r%4). The
+    // brick's output origin and the extents left from it, formed once
+    T* y = reinterpret_cast<T*>(a.y) + a.ybase + nn * a.ys[0] + (a.org[0] + ob[0]) * a.ys[1] +
+           (a.org[1] + ob[1]) * a.ys[2] + (a.org[2] + ob[2]) * a.ys[3];
+    const int rem0 = int(a.O[0] - ob[0]), rem1 = int(a.O[1] - ob[1]), rem2 = int(a.O[2] - ob[2]);
+    const int64_t ys1 = a.ys[1], ys2 = a.ys[2], ys3 = a.ys[3];
+    const int cout_left = int(std::min<int64_t>(a.cout - int64_t(nt0) * 32, int64_t(RN) * 32));
+    T* const ycol = y + int64_t(nt0) * 32;
+    if (a.yvec) {
+        // Through LDS, one 32 x 32 tile at a time in a region of the wave's own
+        // (the brick is no longer read once every wave is past the barrier):
+        // the lanes write their elements, then each lane stores whole 16-byte
+        // runs of output channels of one voxel. Brick coordinates of a lane's
+        // rows advance by carries from one division per tile.
+        __syncthreads();
+        constexpr int VE = 16 / int(sizeof(T));  // elements per 16 bytes
+        constexpr int CPR = 32 / VE;             // 16-byte runs per tile row
+        constexpr int RSTEP = 64 / CPR;          // rows between a lane's runs
+        T* tl = reinterpret_cast<T*>(lds) + wave * 32 * 32;
+        const int crow = lane / CPR, ccol = (lane % CPR) * VE;
+#pragma unroll
+        for (int i = 0; i < RM; ++i) {
+            const int f0 = (wave * RM + i) * 32 + crow;
+            int ox0 = f0 % a.BO[2], oy0 = (f0 / a.BO[2]) % a.BO[1], oz0 = f0 / (a.BO[2] * a.BO[1]);
+#pragma unroll
+            for (int j = 0; j < RN; ++j) {
+#pragma unroll
+                for (int r = 0; r < 16; ++r)
+                    tl[(8 * (r >> 2) + 4 * g + (r & 3)) * 32 + (lane & 31)] = from_f32<T>(acc[i][j][r]);
+                // a wave's LDS accesses complete in issue order: its reads
+                // below see its writes above, and the next tile's writes come
+                // after these reads
+                int ox = ox0, oy = oy0, oz = oz0;
+#pragma unroll
+                for (int k = 0; k < 32 / RSTEP; ++k) {
+                    if (k > 0) {
+                        ox += RSTEP;
+                        while (ox >= a.BO[2]) {
+                            ox -= a.BO[2];
+                            if (++oy == a.BO[1]) {
+                                oy = 0;
+                                ++oz;
+                            }
+                        }
+                    }
+                    const int row = crow + k * RSTEP;
+                    const uint4 v = *reinterpret_cast<const uint4*>(tl + row * 32 + ccol);
+                    const int f = f0 + k * RSTEP;
+                    const int co = j * 32 + ccol;
+                    if (f < bov && oz < rem0 && oy < rem1 && ox < rem2 && co < cout_left)
+                        *reinterpret_cast<uint4*>(ycol + oz * ys1 + oy * ys2 + ox * ys3 + co) = v;
+                }
+            }
+        }
+        return;
+    }
+    // otherwise element by element; the brick coordinates of a row are
+    // advanced from the previous row's (carries instead of divisions)
 #pragma unroll
     for (int i = 0; i < RM; ++i) {
         const int fb = (wave * RM + i) * 32 + 4 * g;
@@ -331,14 +386,12 @@ __global__ __launch_bounds__(kThreads, 2) void conv_fwd_tiled(FwdArgs a)
             }
             const int f = fb + 8 * (r >> 2) + (r & 3);
             if (f >= bov) continue;
-            const int64_t o0 = ob[0] + oz, o1 = ob[1] + oy, o2 = ob[2] + ox;
-            if (o0 >= a.O[0] || o1 >= a.O[1] || o2 >= a.O[2]) continue;
-            const int64_t vox = a.ybase + nn * a.ys[0] + (a.org[0] + o0) * a.ys[1] + (a.org[1] + o1) * a.ys[2] +
-                                (a.org[2] + o2) * a.ys[3];
+            if (oz >= rem0 || oy >= rem1 || ox >= rem2) continue;
+            T* const yv = ycol + oz * ys1 + oy * ys2 + ox * ys3;
 #pragma unroll
             for (int j = 0; j < RN; ++j) {
-                const int64_t co = int64_t(nt0 + j) * 32 + row;
-                if (co < a.cout) y[vox + co] = from_f32<T>(acc[i][j][r]);
+                const int co = j * 32 + row;
+                if (co < cout_left) yv[co] = from_f32<T>(acc[i][j][r]);
             }
         }
     }
@@ -547,6 +600,12 @@ hipError_t run_fwd(const Tile3& t, const Conv3& cv, const void* tile, const void
     if (fold) pl.a.fold = *fold;
     pl.a.tile = static_cast<const char*>(tile);
     pl.a.vec = loads_aligned(tile, fold) && (t.c * Traits<T>::esz) % 16 == 0;
+    {
+        const int64_t ve = 16 / Traits<T>::esz;
+        bool yv = reinterpret_cast<uintptr_t>(y) % 16 == 0 && cv.cout % ve == 0 && om.base % ve == 0;
+        for (int k = 0; k < 4; ++k) yv = yv && om.str[k] % ve == 0;
+        pl.a.yvec = yv ? 1 : 0;
+    }
     pl.a.wfrag = static_cast<const uint4*>(ws);
     pl.a.y = static_cast<char*>(y);
     // the weight fragments depend on (t, cv) only: a call over several regions
