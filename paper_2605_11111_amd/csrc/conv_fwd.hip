@@ -425,11 +425,13 @@ __global__ __launch_bounds__(256) void wfrag_kernel(const T* w, uint4* wfrag, in
 }
 
 template <typename T>
-PlanF plan_fwd_t(const Tile3& t, const Conv3& cv, const int64_t* oext = nullptr, int64_t fix_cc = 0)
+PlanF plan_fwd_t(const Tile3& t, const Conv3& cv, const int64_t* oext = nullptr, int64_t fix_cc = 0,
+                 int rm_over = 0)
 {
     // oext: the extent of the outputs to compute (a region; default the whole
     // box); fix_cc: a channel pass width to keep (a region's outputs are then
-    // summed in the same order as in the whole box's plan)
+    // summed in the same order as in the whole box's plan: the order depends
+    // on the passes, not on the tile shape); rm_over: M tiles per wave
     PlanF pl{};
     const int64_t O[3] = {oext ? oext[0] : cv.O[0], oext ? oext[1] : cv.O[1], oext ? oext[2] : cv.O[2]};
     constexpr int kc = Traits<T>::kc;
@@ -438,7 +440,7 @@ PlanF plan_fwd_t(const Tile3& t, const Conv3& cv, const int64_t* oext = nullptr,
     int rn, rm;
     if (std::is_same<T, bf16_t>::value) {
         rn = nt >= 2 ? 2 : 1;
-        rm = 4;
+        rm = rm_over == 2 && rn == 2 ? 2 : 4;
     } else {
         rn = nt >= 4 ? 4 : (nt >= 2 ? 2 : 1);
         rm = rn == 4 ? 1 : (rn == 2 ? 2 : 4);
@@ -582,10 +584,22 @@ hipError_t run_fwd(const Tile3& t, const Conv3& cv, const void* tile, const void
     PlanF pl = plan_fwd_t<T>(t, cv);
     if (!pl.ok) return hipErrorInvalidValue;
     if (rg.ext[0] != cv.O[0] || rg.ext[1] != cv.O[1] || rg.ext[2] != cv.O[2]) {
-        const PlanF pr = plan_fwd_t<T>(t, cv, rg.ext, pl.a.cc);
-        if (pr.ok && pr.rm == pl.rm && pr.rn == pl.rn && pr.a.cc == pl.a.cc && pr.a.npass == pl.a.npass &&
-            pr.a.nkc == pl.a.nkc && pr.a.nt == pl.a.nt)
-            pl = pr;
+        auto same_passes = [&](const PlanF& q) {
+            return q.ok && q.rn == pl.rn && q.a.cc == pl.a.cc && q.a.npass == pl.a.npass && q.a.nkc == pl.a.nkc &&
+                   q.a.nt == pl.a.nt;
+        };
+        PlanF pr = plan_fwd_t<T>(t, cv, rg.ext, pl.a.cc);
+        // a thin region with fewer bricks than the 512 resident workgroups
+        // takes half-height bricks (two M tiles per wave) where that exists
+        auto region_blocks = [&](const PlanF& q) {
+            return t.n * ceil_div(rg.ext[0], q.a.BO[0]) * ceil_div(rg.ext[1], q.a.BO[1]) *
+                   ceil_div(rg.ext[2], q.a.BO[2]) * q.a.ng;
+        };
+        if (same_passes(pr) && pr.rm == 4 && pr.rn == 2 && region_blocks(pr) < 512) {
+            const PlanF p2 = plan_fwd_t<T>(t, cv, rg.ext, pl.a.cc, 2);
+            if (same_passes(p2) && p2.rm == 2) pr = p2;
+        }
+        if (same_passes(pr)) pl = pr;
     }
     for (int k = 0; k < 3; ++k) {
         pl.a.O[k] = rg.ext[k];
