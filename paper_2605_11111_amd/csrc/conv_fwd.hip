@@ -58,6 +58,7 @@ struct FwdArgs {
     int32_t ng;        // N groups (workgroups along N)
     int32_t vec;       // 16-byte loads allowed (tile base and channel rows aligned)
     int32_t yvec;      // 16-byte output stores allowed (y, the output map and cout aligned)
+    int32_t rperm;     // M-tile rows take voxels transposed (see rows_transposed; needs yvec)
     int64_t nblocks;
     int64_t ybase, ys[4];  // output map: element of (n, o0, o1, o2, co) = ybase + n*ys0 + ... + co
     int64_t org[3];        // origin of the computed region of outputs (O is its extent)
@@ -210,11 +211,15 @@ __global__ __launch_bounds__(kThreads, 2) void conv_fwd_tiled(FwdArgs a)
     const int nt0 = ngi * RN;
     const int bov = a.BO[0] * a.BO[1] * a.BO[2];
 
-    // per-lane LDS voxel base of each of this wave's M tiles
+    // per-lane LDS voxel base of each of this wave's M tiles. A-row `row` of a
+    // tile holds brick voxel tile*32 + row, or with rperm (8-voxel brick rows)
+    // voxel tile*32 + 8 (row % 4) + row / 4: the 16 lanes that the LDS serves
+    // together then read four brick rows, which spreads them over the banks
+    const int prow = a.rperm ? 8 * (row & 3) + (row >> 2) : row;
     int vbase[RM];
 #pragma unroll
     for (int i = 0; i < RM; ++i) {
-        const int f = (wave * RM + i) * 32 + row;
+        const int f = (wave * RM + i) * 32 + prow;
         const int ff = f < bov ? f : 0;
         const int ox = ff % a.BO[2];
         const int oy = (ff / a.BO[2]) % a.BO[1];
@@ -334,9 +339,18 @@ __global__ __launch_bounds__(kThreads, 2) void conv_fwd_tiled(FwdArgs a)
             int ox0 = f0 % a.BO[2], oy0 = (f0 / a.BO[2]) % a.BO[1], oz0 = f0 / (a.BO[2] * a.BO[1]);
 #pragma unroll
             for (int j = 0; j < RN; ++j) {
+                // accumulator row 8 (r / 4) + 4 g + r % 4 is brick voxel tile*32 + that
+                // row, or (rperm) tile*32 + 8 (r % 4) + 2 (r / 4) + g; the LDS tile is
+                // indexed by voxel
+                if (a.rperm) {
 #pragma unroll
-                for (int r = 0; r < 16; ++r)
-                    tl[(8 * (r >> 2) + 4 * g + (r & 3)) * 32 + (lane & 31)] = from_f32<T>(acc[i][j][r]);
+                    for (int r = 0; r < 16; ++r)
+                        tl[(8 * (r & 3) + 2 * (r >> 2) + g) * 32 + (lane & 31)] = from_f32<T>(acc[i][j][r]);
+                } else {
+#pragma unroll
+                    for (int r = 0; r < 16; ++r)
+                        tl[(8 * (r >> 2) + 4 * g + (r & 3)) * 32 + (lane & 31)] = from_f32<T>(acc[i][j][r]);
+                }
                 // a wave's LDS accesses complete in issue order: its reads
                 // below see its writes above, and the next tile's writes come
                 // after these reads
@@ -557,6 +571,20 @@ hipError_t launch_tiled(const PlanF& pl, hipStream_t s)
 }
 
 // Whether every buffer the loads may read is 16-byte aligned.
+// Whether the M-tile rows take brick voxels transposed. The A reads of an
+// M tile put 32 brick voxels, four rows of 8 when the brick is 8 voxels wide,
+// on 32 lanes, the rows BI2 voxels apart in LDS. Measured for 16-byte reads
+// (cycles per wave instruction, 4 waves per CU): rows 10 apart 48 in order
+// against 32 transposed, 12 apart 32 against 27, 14 apart 48 against 32; rows
+// 8 apart (a dense brick) 27 in order, 32 transposed; odd distances and wider
+// bricks gain nothing. In the kernel only the 10-apart case pays (C4's
+// W-paired input gradient, 3.5 % faster); with rows 12 apart (C4's forward) the
+// kernel ran 2.5 % slower, so it keeps the order there.
+bool rows_transposed(const FwdArgs& a)
+{
+    return a.BO[2] == 8 && a.S[2] == 1 && a.BI[2] == 10;
+}
+
 bool loads_aligned(const void* tile, const Fold* fold)
 {
     if (reinterpret_cast<uintptr_t>(tile) % 16 != 0) return false;
@@ -620,6 +648,7 @@ hipError_t run_fwd(const Tile3& t, const Conv3& cv, const void* tile, const void
         for (int k = 0; k < 4; ++k) yv = yv && om.str[k] % ve == 0;
         pl.a.yvec = yv ? 1 : 0;
     }
+    pl.a.rperm = pl.a.yvec && rows_transposed(pl.a) ? 1 : 0;
     pl.a.wfrag = static_cast<const uint4*>(ws);
     pl.a.y = static_cast<char*>(y);
     // the weight fragments depend on (t, cv) only: a call over several regions
