@@ -614,11 +614,18 @@ shard_status_t shard_conv_fwd_folded(const shard_tile_t* x, shard_dtype_t dtype,
     auto nonempty = [&](const Region& r) { return t.n * r.ext[0] * r.ext[1] * r.ext[2] > 0; };
     for (int i = 0; i < nb; ++i) {
         // two regions of the W-march kernel that differ along axis 0 only (the
-        // boundary planes of a tile sharded along axis 0) go in one launch
-        if (fam == FWD_ROWS && i + 1 < nb && folded[i] == folded[i + 1] && nonempty(boxes[i]) &&
-            nonempty(boxes[i + 1])) {
-            const hipError_t e = launch_conv_fwd_region_pair(t, cv, dtype, tile, w, y, boxes[i], boxes[i + 1],
-                                                             folded[i] ? fold : nullptr, ws, stream, laid);
+        // boundary planes of a tile sharded along axis 0), or any two regions
+        // of the tiled kernel (boundary slabs, too thin to fill the part one
+        // by one), go in one launch
+        if ((fam == FWD_ROWS || fam == FWD_TILED) && i + 1 < nb && folded[i] == folded[i + 1] &&
+            nonempty(boxes[i]) && nonempty(boxes[i + 1])) {
+            const Fold* fi = folded[i] ? fold : nullptr;
+            const hipError_t e =
+                fam == FWD_ROWS
+                    ? launch_conv_fwd_region_pair(t, cv, dtype, tile, w, y, boxes[i], boxes[i + 1], fi, ws, stream,
+                                                  laid)
+                    : launch_conv_fwd_tiled_pair(t, cv, dtype, tile, w, y, om, boxes[i], boxes[i + 1], fi, ws, stream,
+                                                 laid);
             if (e == hipSuccess) {
                 laid = true;
                 ++i;

@@ -65,6 +65,14 @@ struct FwdArgs {
     Fold fold;             // halo folded into the loads when fold.mask != 0
 };
 
+// One launch over one or two output regions of the same plan family (the
+// boundary slabs of a split forward): blocks [0, nb0) take region 0, the rest
+// region 1.
+struct FwdLaunch {
+    FwdArgs r[2];
+    int64_t nb0;
+};
+
 struct PlanF {
     int rm, rn;
     FwdArgs a;
@@ -187,7 +195,7 @@ __device__ __forceinline__ void mfma_step<float>(f32x16_t& acc, uint4 av, uint4 
 }
 
 template <typename T, int RM, int RN>
-__global__ __launch_bounds__(kThreads, 2) void conv_fwd_tiled(FwdArgs a)
+__global__ __launch_bounds__(kThreads, 2) void conv_fwd_tiled(FwdLaunch la)
 {
     extern __shared__ uint4 lds[];
     const int lane = threadIdx.x & 63;
@@ -195,8 +203,11 @@ __global__ __launch_bounds__(kThreads, 2) void conv_fwd_tiled(FwdArgs a)
     const int g = lane >> 5;
     const int row = lane & 31;
 
-    // block -> (n, brick, N group), XCD-aware
-    int64_t b = xcd_remap(blockIdx.x, a.nblocks);
+    // block -> (region, n, brick, N group), XCD-aware
+    int64_t b = xcd_remap(blockIdx.x, gridDim.x);
+    const bool second = b >= la.nb0;
+    const FwdArgs& a = la.r[second ? 1 : 0];
+    if (second) b -= la.nb0;
     const int ngi = int(b % a.ng);
     b /= a.ng;
     const int bx = int(b % a.NB[2]);
@@ -558,16 +569,32 @@ size_t wfrag_bytes(const Tile3& t, const Conv3& cv)
 }
 
 template <typename T, int RM, int RN>
-hipError_t launch_tiled(const PlanF& pl, hipStream_t s)
+hipError_t launch_tiled(const PlanF& pl, const PlanF* pl2, hipStream_t s)
 {
     auto fn = &conv_fwd_tiled<T, RM, RN>;
+    const size_t lds = pl2 ? std::max(pl.lds, pl2->lds) : pl.lds;
     hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(fn), hipFuncAttributeMaxDynamicSharedMemorySize,
-                                       int(pl.lds));
+                                       int(lds));
     if (e != hipSuccess) return e;
-    FwdArgs a = pl.a;
-    void* args[] = {&a};
-    return hipLaunchKernel(reinterpret_cast<const void*>(fn), dim3(unsigned(a.nblocks)), dim3(kThreads), args,
-                           pl.lds, s);
+    FwdLaunch la{};
+    la.r[0] = pl.a;
+    la.r[1] = pl2 ? pl2->a : pl.a;
+    la.nb0 = pl.a.nblocks;
+    const int64_t total = pl.a.nblocks + (pl2 ? pl2->a.nblocks : 0);
+    if (total >= (int64_t(1) << 31)) return hipErrorInvalidValue;
+    void* args[] = {&la};
+    return hipLaunchKernel(reinterpret_cast<const void*>(fn), dim3(unsigned(total)), dim3(kThreads), args, lds, s);
+}
+
+template <typename T>
+hipError_t launch_tiled_plans(const PlanF& pl, const PlanF* pl2, hipStream_t s)
+{
+    if (pl2 && (pl2->rm != pl.rm || pl2->rn != pl.rn)) return hipErrorNotSupported;
+    if (pl.rm == 4 && pl.rn == 1) return launch_tiled<T, 4, 1>(pl, pl2, s);
+    if (pl.rm == 4 && pl.rn == 2) return launch_tiled<T, 4, 2>(pl, pl2, s);
+    if (pl.rm == 2 && pl.rn == 2) return launch_tiled<T, 2, 2>(pl, pl2, s);
+    if (pl.rm == 1 && pl.rn == 4) return launch_tiled<T, 1, 4>(pl, pl2, s);
+    return hipErrorInvalidValue;
 }
 
 // Whether every buffer the loads may read is 16-byte aligned.
@@ -602,15 +629,16 @@ bool dense_map(const Conv3& cv, const OutMap& om)
            om.str[3] == dm.str[3];
 }
 
+// The plan of region rg of the output box, every argument filled in. A
+// region smaller than the box takes bricks of its own shape with the box's
+// channel passes, so that every output is summed in the same order whatever
+// region computes it.
 template <typename T>
-hipError_t run_fwd(const Tile3& t, const Conv3& cv, const void* tile, const void* w, void* y, const OutMap& om,
-                   const Region& rg, const Fold* fold, bool rows, void* ws, bool frags_ready, hipStream_t s)
+PlanF plan_region(const Tile3& t, const Conv3& cv, const void* tile, void* y, const OutMap& om, const Region& rg,
+                  const Fold* fold, void* ws)
 {
-    // the plan of the whole output box; a region smaller than it takes bricks
-    // of its own shape with the same channel passes, so that every output is
-    // summed in the same order whatever region computes it
     PlanF pl = plan_fwd_t<T>(t, cv);
-    if (!pl.ok) return hipErrorInvalidValue;
+    if (!pl.ok) return pl;
     if (rg.ext[0] != cv.O[0] || rg.ext[1] != cv.O[1] || rg.ext[2] != cv.O[2]) {
         auto same_passes = [&](const PlanF& q) {
             return q.ok && q.rn == pl.rn && q.a.cc == pl.a.cc && q.a.npass == pl.a.npass && q.a.nkc == pl.a.nkc &&
@@ -651,25 +679,55 @@ hipError_t run_fwd(const Tile3& t, const Conv3& cv, const void* tile, const void
     pl.a.rperm = pl.a.yvec && rows_transposed(pl.a) ? 1 : 0;
     pl.a.wfrag = static_cast<const uint4*>(ws);
     pl.a.y = static_cast<char*>(y);
-    // the weight fragments depend on (t, cv) only: a call over several regions
-    // lays them out once
+    return pl;
+}
+
+// Lay out the weight fragments of (t, cv) in ws; they depend on (t, cv) only,
+// so a call over several regions lays them out once.
+template <typename T>
+hipError_t lay_wfrag(const Tile3& t, const Conv3& cv, const PlanF& pl, const void* w, void* ws, hipStream_t s)
+{
+    const int taps = int(cv.taps());
+    const int64_t frag_total = int64_t(taps) * pl.a.nkc * pl.a.nt * 64;
+    const unsigned fg = unsigned(std::max<int64_t>(1, std::min<int64_t>(ceil_div(frag_total, 256), 4096)));
+    hipLaunchKernelGGL(wfrag_kernel<T>, dim3(fg), dim3(256), 0, s, static_cast<const T*>(w), static_cast<uint4*>(ws),
+                       t.c, cv.cout, taps, pl.a.nkc, pl.a.nt);
+    return hipGetLastError();
+}
+
+template <typename T>
+hipError_t run_fwd(const Tile3& t, const Conv3& cv, const void* tile, const void* w, void* y, const OutMap& om,
+                   const Region& rg, const Fold* fold, bool rows, void* ws, bool frags_ready, hipStream_t s)
+{
+    const PlanF pl = plan_region<T>(t, cv, tile, y, om, rg, fold, ws);
+    if (!pl.ok) return hipErrorInvalidValue;
     if (!frags_ready) {
-        const int taps = int(cv.taps());
-        const int64_t frag_total = int64_t(taps) * pl.a.nkc * pl.a.nt * 64;
-        const unsigned fg = unsigned(std::max<int64_t>(1, std::min<int64_t>(ceil_div(frag_total, 256), 4096)));
-        hipLaunchKernelGGL(wfrag_kernel<T>, dim3(fg), dim3(256), 0, s, static_cast<const T*>(w),
-                           static_cast<uint4*>(ws), t.c, cv.cout, taps, pl.a.nkc, pl.a.nt);
-        const hipError_t e = hipGetLastError();
+        const hipError_t e = lay_wfrag<T>(t, cv, pl, w, ws, s);
         if (e != hipSuccess) return e;
     }
     if (rows)
         return launch_conv_fwd_rows(t, cv, std::is_same<T, bf16_t>::value ? SHARD_BF16 : SHARD_F32, tile, ws,
                                     pl.a.nkc, pl.a.nt, y, rg, fold, s);
-    if (pl.rm == 4 && pl.rn == 1) return launch_tiled<T, 4, 1>(pl, s);
-    if (pl.rm == 4 && pl.rn == 2) return launch_tiled<T, 4, 2>(pl, s);
-    if (pl.rm == 2 && pl.rn == 2) return launch_tiled<T, 2, 2>(pl, s);
-    if (pl.rm == 1 && pl.rn == 4) return launch_tiled<T, 1, 4>(pl, s);
-    return hipErrorInvalidValue;
+    return launch_tiled_plans<T>(pl, nullptr, s);
+}
+
+// Two regions in one launch of the tiled kernel; hipErrorNotSupported, with
+// nothing launched, when their plans take different kernels.
+template <typename T>
+hipError_t run_fwd_pair(const Tile3& t, const Conv3& cv, const void* tile, const void* w, void* y, const OutMap& om,
+                        const Region& ra, const Region& rb, const Fold* fold, void* ws, bool frags_ready,
+                        hipStream_t s)
+{
+    const PlanF pa = plan_region<T>(t, cv, tile, y, om, ra, fold, ws);
+    const PlanF pb = plan_region<T>(t, cv, tile, y, om, rb, fold, ws);
+    if (!pa.ok || !pb.ok) return hipErrorInvalidValue;
+    if (pa.rm != pb.rm || pa.rn != pb.rn || pa.a.nblocks + pb.a.nblocks >= (int64_t(1) << 31))
+        return hipErrorNotSupported;
+    if (!frags_ready) {
+        const hipError_t e = lay_wfrag<T>(t, cv, pa, w, ws, s);
+        if (e != hipSuccess) return e;
+    }
+    return launch_tiled_plans<T>(pa, &pb, s);
 }
 
 }  // namespace
@@ -740,6 +798,14 @@ hipError_t launch_conv_fwd_region_pair(const Tile3& t, const Conv3& cv, shard_dt
         if (e != hipSuccess) return e;
     }
     return launch_conv_fwd_rows(t, cv, dt, tile, ws, pl.a.nkc, pl.a.nt, y, ra, fold, s, &rb);
+}
+
+hipError_t launch_conv_fwd_tiled_pair(const Tile3& t, const Conv3& cv, shard_dtype_t dt, const void* tile,
+                                      const void* w, void* y, const OutMap& om, const Region& ra, const Region& rb,
+                                      const Fold* fold, void* ws, hipStream_t s, bool frags_ready)
+{
+    return dt == SHARD_BF16 ? run_fwd_pair<bf16_t>(t, cv, tile, w, y, om, ra, rb, fold, ws, frags_ready, s)
+                            : run_fwd_pair<float>(t, cv, tile, w, y, om, ra, rb, fold, ws, frags_ready, s);
 }
 
 hipError_t launch_conv_fwd_mapped(const Tile3& t, const Conv3& cv, shard_dtype_t dt, const void* tile,
