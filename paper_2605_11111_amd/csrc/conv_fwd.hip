@@ -131,7 +131,16 @@ __device__ __forceinline__ void stage_brick(const FwdArgs& a, uint4* lds, int64_
     constexpr int kPerUnit = 16 / Traits<T>::esz;
     const bool vec_ok = a.vec != 0;
     const int nvp = a.BI[0] * a.BI[1] * a.BI[2];  // voxels per unit plane
-    if (a.fold.mask) {
+    // a brick whose footprint (clipped to the tile) stays off every folded
+    // margin reads the tile alone: the plain loads below
+    bool margin = false;
+    for (int k = 0; k < 3; ++k) {
+        if (!((a.fold.mask >> k) & 1u)) continue;
+        const int64_t f0 = i0[k] > 0 ? i0[k] : 0;
+        const int64_t f1 = i0[k] + a.BI[k] < a.P[k] ? i0[k] + a.BI[k] : a.P[k];
+        margin = margin || (f0 < f1 && (f0 < a.fold.lo[k] || f1 > a.fold.lo[k] + a.fold.ext[k]));
+    }
+    if (margin) {
         // margin voxels come from the received slabs (or are zero)
         for_each_unit(a, [&](int v, int q, int z, int y, int x) {
             const int64_t t0 = i0[0] + z, t1 = i0[1] + y, t2 = i0[2] + x;
