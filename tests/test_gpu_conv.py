@@ -169,6 +169,11 @@ EDGE = [
     ("2d_c16_k1_rowpair", "bf16", 1, 16, 64, (33, 45), (2, 1), (1, 1), (1, 1)),
     ("1d_c16_k5_rowpair", "bf16", 1, 16, 128, (300,), (3,), (5,), (1,)),
     ("3d_c16_k5_ragged", "bf16", 1, 16, 64, (11, 13, 37), (2, 1, 1), (5, 5, 5), (1, 1, 1)),
+    # shards of 8 x 16 x 24 outputs: the general forward takes bricks 8 voxels
+    # wide whose rows lie 10 voxels apart in LDS, read with the transposed
+    # M-row order (one and two N tiles; a ragged N tile of 40 channels)
+    ("3d_bricks_8_wide", "bf16", 1, 16, 32, (16, 16, 24), (2, 1, 1), (3, 3, 3), (1, 1, 1)),
+    ("3d_bricks_8_wide_c48", "bf16", 2, 48, 40, (16, 16, 24), (2, 1, 1), (3, 3, 3), (1, 1, 1)),
 ]
 
 
