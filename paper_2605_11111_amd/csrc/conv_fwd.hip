@@ -203,8 +203,9 @@ __device__ __forceinline__ void mfma_step<float>(f32x16_t& acc, uint4 av, uint4 
     acc = __builtin_amdgcn_mfma_f32_32x32x2f32(__uint_as_float(av.w), __uint_as_float(bv.w), acc, 0, 0, 0);
 }
 
+// Brick b (in the XCD-aware order) of one region.
 template <typename T, int RM, int RN>
-__global__ __launch_bounds__(kThreads, 2) void conv_fwd_tiled(FwdLaunch la)
+__device__ __forceinline__ void fwd_tiled_body(const FwdArgs& a, int64_t b)
 {
     extern __shared__ uint4 lds[];
     const int lane = threadIdx.x & 63;
@@ -212,11 +213,7 @@ __global__ __launch_bounds__(kThreads, 2) void conv_fwd_tiled(FwdLaunch la)
     const int g = lane >> 5;
     const int row = lane & 31;
 
-    // block -> (region, n, brick, N group), XCD-aware
-    int64_t b = xcd_remap(blockIdx.x, gridDim.x);
-    const bool second = b >= la.nb0;
-    const FwdArgs& a = la.r[second ? 1 : 0];
-    if (second) b -= la.nb0;
+    // block -> (n, brick, N group)
     const int ngi = int(b % a.ng);
     b /= a.ng;
     const int bx = int(b % a.NB[2]);
@@ -431,6 +428,24 @@ __global__ __launch_bounds__(kThreads, 2) void conv_fwd_tiled(FwdLaunch la)
     }
 }
 
+template <typename T, int RM, int RN>
+__global__ __launch_bounds__(kThreads, 2) void conv_fwd_tiled(FwdArgs a)
+{
+    fwd_tiled_body<T, RM, RN>(a, xcd_remap(blockIdx.x, a.nblocks));
+}
+
+// Two regions in one launch: each takes its own inlined copy of the body, so
+// that its arguments are read from a fixed place.
+template <typename T, int RM, int RN>
+__global__ __launch_bounds__(kThreads, 2) void conv_fwd_tiled2(FwdLaunch la)
+{
+    const int64_t b = xcd_remap(blockIdx.x, gridDim.x);
+    if (b < la.nb0)
+        fwd_tiled_body<T, RM, RN>(la.r[0], b);
+    else
+        fwd_tiled_body<T, RM, RN>(la.r[1], b - la.nb0);
+}
+
 // wfrag[((tap * nkc + kc) * nt + ntile) * 64 + lane] = 16 bytes of weights in
 // MFMA B-fragment order (see the file comment); zero past cin / cout.
 template <typename T>
@@ -580,19 +595,24 @@ size_t wfrag_bytes(const Tile3& t, const Conv3& cv)
 template <typename T, int RM, int RN>
 hipError_t launch_tiled(const PlanF& pl, const PlanF* pl2, hipStream_t s)
 {
-    auto fn = &conv_fwd_tiled<T, RM, RN>;
+    const void* fn = pl2 ? reinterpret_cast<const void*>(&conv_fwd_tiled2<T, RM, RN>)
+                         : reinterpret_cast<const void*>(&conv_fwd_tiled<T, RM, RN>);
     const size_t lds = pl2 ? std::max(pl.lds, pl2->lds) : pl.lds;
-    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(fn), hipFuncAttributeMaxDynamicSharedMemorySize,
-                                       int(lds));
+    hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, int(lds));
     if (e != hipSuccess) return e;
-    FwdLaunch la{};
-    la.r[0] = pl.a;
-    la.r[1] = pl2 ? pl2->a : pl.a;
-    la.nb0 = pl.a.nblocks;
     const int64_t total = pl.a.nblocks + (pl2 ? pl2->a.nblocks : 0);
     if (total >= (int64_t(1) << 31)) return hipErrorInvalidValue;
+    if (!pl2) {
+        FwdArgs a = pl.a;
+        void* args[] = {&a};
+        return hipLaunchKernel(fn, dim3(unsigned(total)), dim3(kThreads), args, lds, s);
+    }
+    FwdLaunch la{};
+    la.r[0] = pl.a;
+    la.r[1] = pl2->a;
+    la.nb0 = pl.a.nblocks;
     void* args[] = {&la};
-    return hipLaunchKernel(reinterpret_cast<const void*>(fn), dim3(unsigned(total)), dim3(kThreads), args, lds, s);
+    return hipLaunchKernel(fn, dim3(unsigned(total)), dim3(kThreads), args, lds, s);
 }
 
 template <typename T>
