@@ -255,8 +255,14 @@ __global__ __launch_bounds__(256, 1) void conv_fwd_xm(XmArgs a)
     // load it of a unit goes out in MFMA step step_of(it) of the tile before (the
     // last in the last step), behind that step's first MFMA
     constexpr int S_STEPS = R * KD * C::NKC;
-    static_assert(S_STEPS >= C::NIT, "at most one staging load per MFMA step");
-    auto step_of = [](int it) { return ((it + 1) * S_STEPS) / C::NIT - 1; };
+    // at most one staging load per MFMA step; two where the stage is single
+    // buffered ahead (NBUF = 2: each tile starts by waiting for every load and
+    // store, so the order of a tile's loads does not matter)
+    static_assert(S_STEPS >= C::NIT || (NBUF == 2 && 2 * S_STEPS >= C::NIT), "staging loads per MFMA step");
+    // (the last load in the last step either way)
+    auto step_of = [](int it) {
+        return C::NIT <= S_STEPS ? ((it + 1) * S_STEPS) / C::NIT - 1 : (it * S_STEPS) / C::NIT;
+    };
     // Where a group count leaves the tile's last step without epilogue stores
     // (six or more groups), a step's load goes out behind its first MFMA; else
     // after the step's epilogue piece, so that a tile's last staging load
@@ -698,7 +704,9 @@ hipError_t launch_conv_fwd_rows(const Tile3& t, const Conv3& cv, shard_dtype_t d
     const int64_t ext0 = std::max<int64_t>(rg.ext[0], rg2 ? rg2->ext[0] : 0);
     if (t.c == 32) {
         // thin regions along axis 0 (the boundary planes of a D-sharded tile) take
-        // bricks two rows deep; per-output arithmetic is the same in both
+        // bricks one plane deep (8 rows high; the stage of 30 input rows fits LDS
+        // twice) or two; per-output arithmetic is the same in all
+        if (ext0 == 1) return launch_xm<32, 3, 3, 1, 4, 1, 2, 2>(t, cv, tile, wfrag, y, rg, rg2, fold, s);
         if (ext0 <= 2) return launch_xm<32, 3, 3, 2, 2, 1, 2, 3>(t, cv, tile, wfrag, y, rg, rg2, fold, s);
         return launch_xm<32, 3, 3, 4, 1, 1, 2, 3>(t, cv, tile, wfrag, y, rg, rg2, fold, s);
     }
