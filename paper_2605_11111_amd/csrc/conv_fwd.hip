@@ -140,6 +140,44 @@ __device__ __forceinline__ void stage_brick(const FwdArgs& a, uint4* lds, int64_
         const int64_t f1 = i0[k] + a.BI[k] < a.P[k] ? i0[k] + a.BI[k] : a.P[k];
         margin = margin || (f0 < f1 && (f0 < a.fold.lo[k] || f1 > a.fold.lo[k] + a.fold.ext[k]));
     }
+    const uint32_t fm = a.fold.mask;
+    if (margin && (fm == 1u || fm == 2u || fm == 4u)) {
+        // margins on one axis k: a voxel comes from the tile, or from the slab
+        // of its side, whose layout is the tile's with axis k cut to the margin
+        const int k = fm == 1u ? 0 : (fm == 2u ? 1 : 2);
+        const int64_t lok = a.fold.lo[k], hik = a.fold.lo[k] + a.fold.ext[k], Pk = a.P[k];
+        const char* slo = a.fold.slab[k][0];
+        const char* shi = a.fold.slab[k][1];
+        const int64_t vb = a.cin * Traits<T>::esz;
+        for_each_unit(a, [&](int v, int q, int z, int y, int x) {
+            const int64_t t0 = i0[0] + z, t1 = i0[1] + y, t2 = i0[2] + x;
+            const int c = c0 + q * kPerUnit;
+            uint4 val = make_uint4(0, 0, 0, 0);
+            if (t0 >= 0 && t0 < a.P[0] && t1 >= 0 && t1 < a.P[1] && t2 >= 0 && t2 < a.P[2] && c < a.cin) {
+                const int64_t tk = k == 0 ? t0 : (k == 1 ? t1 : t2);
+                const bool lo = tk < lok, hi = tk >= hik;
+                const char* base = lo ? slo : (hi ? shi : a.tile);
+                const int64_t ek = lo ? lok : (hi ? Pk - hik : Pk);
+                const int64_t ck = hi ? tk - hik : tk;
+                const int64_t e1 = k == 1 ? ek : a.P[1], e2 = k == 2 ? ek : a.P[2];
+                const int64_t d0 = k == 0 ? ek : a.P[0];
+                const int64_t u0 = k == 0 ? ck : t0, u1 = k == 1 ? ck : t1, u2 = k == 2 ? ck : t2;
+                if (base) {
+                    const T* src = reinterpret_cast<const T*>(base + (((nn * d0 + u0) * e1 + u1) * e2 + u2) * vb) + c;
+                    if (vec_ok && c + kPerUnit <= a.cin) {
+                        val = *reinterpret_cast<const uint4*>(src);
+                    } else {
+                        T tmp[kPerUnit];
+#pragma unroll
+                        for (int e = 0; e < kPerUnit; ++e) tmp[e] = (c + e < a.cin) ? src[e] : T(0);
+                        val = *reinterpret_cast<const uint4*>(tmp);
+                    }
+                }
+            }
+            lds[q * nvp + v] = val;
+        });
+        return;
+    }
     if (margin) {
         // margin voxels come from the received slabs (or are zero)
         for_each_unit(a, [&](int v, int q, int z, int y, int x) {
