@@ -20,8 +20,8 @@
 //    key order with ds_read_b64_tr_b16 (transpose on read). A query's rescale
 //    factor is then one scalar per lane.
 //  * K and V blocks of 32 keys are staged by direct global->LDS loads, double
-//    buffered, 16-byte units XOR-swizzled by key so that the fragment reads are
-//    free of bank conflicts; keys past the block end load as zero and are
+//    buffered, 16-byte units XOR-swizzled by key so that the fragment reads
+//    spread over the banks; keys past the block end load as zero and are
 //    masked to -inf in the scores, queries past the end load as zero and are
 //    not stored.
 //  * Softmax runs in base 2 on fp32 (scores scaled by scale * log2 e) against a
