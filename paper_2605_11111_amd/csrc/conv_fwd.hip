@@ -93,13 +93,19 @@ struct Traits<float> {
     static constexpr int esz = 4;
 };
 
-// Visit every 16-byte unit (voxel v = (z, y, x) of the brick, channel unit q)
-// once across the block. When a (z, y) row of units fits the block, a thread
+// Stage every 16-byte unit (voxel v = (z, y, x) of the brick, channel unit q)
+// once across the block: fetch(v, q, z, y, x) gives its value, stored at
+// lds[q * nvp + v]. A thread fetches kStageBatch units before it stores them,
+// so that their loads are in flight together (one at a time, each store
+// waited for its load). When a (z, y) row of units fits the block, a thread
 // keeps its column (x, q) and steps over rows: one division per row instead of
 // three per unit.
+constexpr int kStageBatch = 4;
+
 template <typename F>
-__device__ __forceinline__ void for_each_unit(const FwdArgs& a, F&& fn)
+__device__ __forceinline__ void stage_units(const FwdArgs& a, uint4* lds, int nvp, F&& fetch)
 {
+    constexpr int B = kStageBatch;
     const int nq = a.nq;
     const int rowlen = a.BI[2] * nq;
     if (rowlen <= kThreads) {
@@ -108,19 +114,43 @@ __device__ __forceinline__ void for_each_unit(const FwdArgs& a, F&& fn)
         if (r0 >= rpp) return;
         const int x = cu / nq, q = cu - x * nq;
         const int rows = a.BI[0] * a.BI[1];
-        for (int r = r0; r < rows; r += rpp) {
-            const int z = r / a.BI[1], y = r - z * a.BI[1];
-            fn(r * a.BI[2] + x, q, z, y, x);
+        for (int r = r0; r < rows; r += B * rpp) {
+            uint4 val[B];
+#pragma unroll
+            for (int j = 0; j < B; ++j) {
+                const int rr = r + j * rpp;
+                val[j] = make_uint4(0, 0, 0, 0);
+                if (rr < rows) {
+                    const int z = rr / a.BI[1], y = rr - z * a.BI[1];
+                    val[j] = fetch(rr * a.BI[2] + x, q, z, y, x);
+                }
+            }
+#pragma unroll
+            for (int j = 0; j < B; ++j) {
+                const int rr = r + j * rpp;
+                if (rr < rows) lds[q * nvp + rr * a.BI[2] + x] = val[j];
+            }
         }
         return;
     }
     const int total = a.BI[0] * a.BI[1] * a.BI[2] * nq;
-    for (int u = threadIdx.x; u < total; u += kThreads) {
-        const int q = u % nq;
-        const int v = u / nq;
-        const int x = v % a.BI[2];
-        const int yz = v / a.BI[2];
-        fn(v, q, yz / a.BI[1], yz % a.BI[1], x);
+    for (int u = threadIdx.x; u < total; u += B * kThreads) {
+        uint4 val[B];
+#pragma unroll
+        for (int j = 0; j < B; ++j) {
+            const int uu = u + j * kThreads;
+            val[j] = make_uint4(0, 0, 0, 0);
+            if (uu < total) {
+                const int q = uu % nq, v = uu / nq;
+                const int x = v % a.BI[2], yz = v / a.BI[2];
+                val[j] = fetch(v, q, yz / a.BI[1], yz % a.BI[1], x);
+            }
+        }
+#pragma unroll
+        for (int j = 0; j < B; ++j) {
+            const int uu = u + j * kThreads;
+            if (uu < total) lds[(uu % nq) * nvp + uu / nq] = val[j];
+        }
     }
 }
 
@@ -149,7 +179,7 @@ __device__ __forceinline__ void stage_brick(const FwdArgs& a, uint4* lds, int64_
         const char* slo = a.fold.slab[k][0];
         const char* shi = a.fold.slab[k][1];
         const int64_t vb = a.cin * Traits<T>::esz;
-        for_each_unit(a, [&](int v, int q, int z, int y, int x) {
+        stage_units(a, lds, nvp, [&](int v, int q, int z, int y, int x) {
             const int64_t t0 = i0[0] + z, t1 = i0[1] + y, t2 = i0[2] + x;
             const int c = c0 + q * kPerUnit;
             uint4 val = make_uint4(0, 0, 0, 0);
@@ -174,13 +204,13 @@ __device__ __forceinline__ void stage_brick(const FwdArgs& a, uint4* lds, int64_
                     }
                 }
             }
-            lds[q * nvp + v] = val;
+            return val;
         });
         return;
     }
     if (margin) {
         // margin voxels come from the received slabs (or are zero)
-        for_each_unit(a, [&](int v, int q, int z, int y, int x) {
+        stage_units(a, lds, nvp, [&](int v, int q, int z, int y, int x) {
             const int64_t t0 = i0[0] + z, t1 = i0[1] + y, t2 = i0[2] + x;
             const int c = c0 + q * kPerUnit;
             uint4 val = make_uint4(0, 0, 0, 0);
@@ -198,11 +228,11 @@ __device__ __forceinline__ void stage_brick(const FwdArgs& a, uint4* lds, int64_
                     }
                 }
             }
-            lds[q * nvp + v] = val;
+            return val;
         });
         return;
     }
-    for_each_unit(a, [&](int v, int q, int z, int y, int x) {
+    stage_units(a, lds, nvp, [&](int v, int q, int z, int y, int x) {
         const int64_t t0 = i0[0] + z, t1 = i0[1] + y, t2 = i0[2] + x;
         const int c = c0 + q * kPerUnit;
         uint4 val = make_uint4(0, 0, 0, 0);
@@ -218,7 +248,7 @@ __device__ __forceinline__ void stage_brick(const FwdArgs& a, uint4* lds, int64_
                 val = *reinterpret_cast<const uint4*>(tmp);
             }
         }
-        lds[q * nvp + v] = val;
+        return val;
     });
 }
 
