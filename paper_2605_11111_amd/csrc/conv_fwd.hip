@@ -154,8 +154,73 @@ __device__ __forceinline__ void stage_units(const FwdArgs& a, uint4* lds, int nv
     }
 }
 
-// Stage the input brick channels [c0, c0 + cc) into LDS.
-template <typename T>
+// The plain staging of a brick that reaches no folded margin, when a (z, y)
+// row of 16-byte units fits the block and every unit is a whole aligned
+// vector: a thread keeps its column (x, q) and steps over rows, with the
+// row's tile offset, its place in LDS and its (z, y) advanced by increments
+// and its bounds tested in 32 bits (no division or 64-bit product per unit).
+// The same units as stage_units' row mode, in the same places.
+template <typename T, int B>
+__device__ __forceinline__ void stage_rows_plain(const FwdArgs& a, uint4* lds, int nvp, int64_t nn,
+                                                 const int64_t i0[3], int c0)
+{
+    constexpr int kPerUnit = 16 / Traits<T>::esz;
+    constexpr int64_t esz = Traits<T>::esz;
+    // the thread's column is formed anew in every pass (an opaque copy of the
+    // thread index), so that none of this stays live across the MFMA loop
+    int tid = int(threadIdx.x);
+    asm volatile("" : "+v"(tid));
+    const int nq = a.nq;
+    const int rowlen = a.BI[2] * nq;
+    const int rpp = kThreads / rowlen;
+    const int r0 = tid / rowlen;
+    if (r0 >= rpp) return;
+    const int cu = tid - r0 * rowlen;
+    const int x = cu / nq, q = cu - x * nq;
+    const int64_t t2 = i0[2] + x;
+    const int c = c0 + q * kPerUnit;
+    const bool colok = t2 >= 0 && t2 < a.P[2] && c < a.cin;
+    // rows z of the brick with i0[0] + z inside the tile are [zlo, zhi); same for y
+    const int BI0 = a.BI[0], BI1 = a.BI[1];
+    const int zlo = int(std::min<int64_t>(std::max<int64_t>(-i0[0], 0), BI0));
+    const int zhi = int(std::min<int64_t>(std::max<int64_t>(a.P[0] - i0[0], 0), BI0));
+    const int ylo = int(std::min<int64_t>(std::max<int64_t>(-i0[1], 0), BI1));
+    const int yhi = int(std::min<int64_t>(std::max<int64_t>(a.P[1] - i0[1], 0), BI1));
+    // byte offset of unit (z, y) of the column: ((nn P0 + i0[0] + z) P1 + i0[1] + y) rowb + (t2 cin + c) esz
+    const int64_t rowb = a.P[2] * a.cin * esz;
+    const int dz = rpp / BI1, dy = rpp - dz * BI1;
+    int z = r0 / BI1, y = r0 - z * BI1;
+    int64_t off = ((nn * a.P[0] + i0[0] + z) * a.P[1] + i0[1] + y) * rowb + (t2 * a.cin + c) * esz;
+    const int64_t step = (int64_t(dz) * a.P[1] + dy) * rowb, wrap = (a.P[1] - BI1) * rowb;
+    const int rows = BI0 * BI1;
+    const int dstep = rpp * a.BI[2];
+    uint4* dst = lds + q * nvp + r0 * a.BI[2] + x;
+    for (int r = r0; r < rows; r += B * rpp) {
+        uint4 val[B];
+#pragma unroll
+        for (int j = 0; j < B; ++j) {
+            val[j] = make_uint4(0, 0, 0, 0);
+            if (r + j * rpp < rows && colok && z >= zlo && z < zhi && y >= ylo && y < yhi)
+                val[j] = *reinterpret_cast<const uint4*>(a.tile + off);
+            z += dz;
+            y += dy;
+            off += step;
+            if (y >= BI1) {
+                y -= BI1;
+                ++z;
+                off += wrap;
+            }
+        }
+#pragma unroll
+        for (int j = 0; j < B; ++j)
+            if (r + j * rpp < rows) dst[j * dstep] = val[j];
+        dst += B * dstep;
+    }
+}
+
+// Stage the input brick channels [c0, c0 + cc) into LDS; SB units in flight
+// per thread on the plain row path.
+template <typename T, int SB>
 __device__ __forceinline__ void stage_brick(const FwdArgs& a, uint4* lds, int64_t nn, const int64_t i0[3], int c0)
 {
     constexpr int kPerUnit = 16 / Traits<T>::esz;
@@ -230,6 +295,10 @@ __device__ __forceinline__ void stage_brick(const FwdArgs& a, uint4* lds, int64_
             }
             return val;
         });
+        return;
+    }
+    if (vec_ok && a.cin % kPerUnit == 0 && a.BI[2] * a.nq <= kThreads) {
+        stage_rows_plain<T, SB>(a, lds, nvp, nn, i0, c0);
         return;
     }
     stage_units(a, lds, nvp, [&](int v, int q, int z, int y, int x) {
@@ -325,7 +394,7 @@ __device__ __forceinline__ void fwd_tiled_body(const FwdArgs& a, int64_t b)
     const int plane = a.BI[1] * a.BI[2];
     for (int p = 0; p < a.npass; ++p) {
         if (p > 0) __syncthreads();
-        stage_brick<T>(a, lds, nn, i0, p * a.cc);
+        stage_brick<T, kStageBatch>(a, lds, nn, i0, p * a.cc);
         __syncthreads();
         const int iters = taps * kcp;
         // Iteration = (tap, channel chunk). Software pipeline over two operand
