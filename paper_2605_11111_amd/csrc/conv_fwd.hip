@@ -154,15 +154,20 @@ __device__ __forceinline__ void stage_units(const FwdArgs& a, uint4* lds, int nv
     }
 }
 
-// The plain staging of a brick that reaches no folded margin, when a (z, y)
-// row of 16-byte units fits the block and every unit is a whole aligned
-// vector: a thread keeps its column (x, q) and steps over rows, with the
-// row's tile offset, its place in LDS and its (z, y) advanced by increments
-// and its bounds tested in 32 bits (no division or 64-bit product per unit).
-// The same units as stage_units' row mode, in the same places.
-template <typename T, int B>
-__device__ __forceinline__ void stage_rows_plain(const FwdArgs& a, uint4* lds, int nvp, int64_t nn,
-                                                 const int64_t i0[3], int c0)
+// Row-mode staging of a brick, when a (z, y) row of 16-byte units fits the
+// block and every unit is a whole aligned vector: a thread keeps its column
+// (x, q) and steps over rows, with (z, y), its place in LDS and (where the
+// source buffer cannot change from row to row) the row's byte offset
+// advanced by increments and the bounds tested in 32 bits: no division and,
+// on the plain path, no 64-bit product per unit. The same units as
+// stage_units' row mode, in the same places. FK < 0: the tile alone (a brick
+// that reaches no folded margin); FK = k: margins folded on axis k only, a
+// voxel coming from the tile or from the slab of its side (the tile's layout
+// with axis k cut to the margin). Along W (k = 2) the column decides the
+// buffer; along D or H the row does, and its offset is formed per unit.
+template <typename T, int B, int FK>
+__device__ __forceinline__ void stage_rows(const FwdArgs& a, uint4* lds, int nvp, int64_t nn, const int64_t i0[3],
+                                           int c0)
 {
     constexpr int kPerUnit = 16 / Traits<T>::esz;
     constexpr int64_t esz = Traits<T>::esz;
@@ -179,18 +184,37 @@ __device__ __forceinline__ void stage_rows_plain(const FwdArgs& a, uint4* lds, i
     const int x = cu / nq, q = cu - x * nq;
     const int64_t t2 = i0[2] + x;
     const int c = c0 + q * kPerUnit;
-    const bool colok = t2 >= 0 && t2 < a.P[2] && c < a.cin;
+    const int64_t vb = a.cin * esz;
+    // the column's buffer, its W extent and the column's W coordinate in it
+    const char* src = a.tile;
+    int64_t e2 = a.P[2], u2 = t2;
+    int64_t lok = 0, hik = 0;
+    const char *slo = nullptr, *shi = nullptr;
+    if constexpr (FK >= 0) {
+        lok = a.fold.lo[FK];
+        hik = lok + a.fold.ext[FK];
+        slo = a.fold.slab[FK][0];
+        shi = a.fold.slab[FK][1];
+    }
+    if constexpr (FK == 2) {
+        const bool lo = t2 < lok, hi = t2 >= hik;
+        src = lo ? slo : (hi ? shi : a.tile);
+        e2 = lo ? lok : (hi ? a.P[2] - hik : a.P[2]);
+        u2 = hi ? t2 - hik : t2;
+    }
+    const bool colok = t2 >= 0 && t2 < a.P[2] && c < a.cin && src != nullptr;
     // rows z of the brick with i0[0] + z inside the tile are [zlo, zhi); same for y
     const int BI0 = a.BI[0], BI1 = a.BI[1];
     const int zlo = int(std::min<int64_t>(std::max<int64_t>(-i0[0], 0), BI0));
     const int zhi = int(std::min<int64_t>(std::max<int64_t>(a.P[0] - i0[0], 0), BI0));
     const int ylo = int(std::min<int64_t>(std::max<int64_t>(-i0[1], 0), BI1));
     const int yhi = int(std::min<int64_t>(std::max<int64_t>(a.P[1] - i0[1], 0), BI1));
-    // byte offset of unit (z, y) of the column: ((nn P0 + i0[0] + z) P1 + i0[1] + y) rowb + (t2 cin + c) esz
-    const int64_t rowb = a.P[2] * a.cin * esz;
+    // byte offset of unit (z, y) of the column in its buffer:
+    // ((nn P0 + i0[0] + z) P1 + i0[1] + y) rowb + colb
+    const int64_t rowb = e2 * vb, colb = u2 * vb + int64_t(c) * esz;
     const int dz = rpp / BI1, dy = rpp - dz * BI1;
     int z = r0 / BI1, y = r0 - z * BI1;
-    int64_t off = ((nn * a.P[0] + i0[0] + z) * a.P[1] + i0[1] + y) * rowb + (t2 * a.cin + c) * esz;
+    int64_t off = ((nn * a.P[0] + i0[0] + z) * a.P[1] + i0[1] + y) * rowb + colb;
     const int64_t step = (int64_t(dz) * a.P[1] + dy) * rowb, wrap = (a.P[1] - BI1) * rowb;
     const int rows = BI0 * BI1;
     const int dstep = rpp * a.BI[2];
@@ -200,8 +224,21 @@ __device__ __forceinline__ void stage_rows_plain(const FwdArgs& a, uint4* lds, i
 #pragma unroll
         for (int j = 0; j < B; ++j) {
             val[j] = make_uint4(0, 0, 0, 0);
-            if (r + j * rpp < rows && colok && z >= zlo && z < zhi && y >= ylo && y < yhi)
-                val[j] = *reinterpret_cast<const uint4*>(a.tile + off);
+            if (r + j * rpp < rows && colok && z >= zlo && z < zhi && y >= ylo && y < yhi) {
+                if constexpr (FK == 0 || FK == 1) {
+                    // the row's buffer: the row index in it times the row bytes
+                    const int64_t t0 = i0[0] + z, t1 = i0[1] + y;
+                    const int64_t tk = FK == 0 ? t0 : t1;
+                    const bool lo = tk < lok, hi = tk >= hik;
+                    const char* base = lo ? slo : (hi ? shi : a.tile);
+                    const int64_t ek = lo ? lok : (hi ? a.P[FK] - hik : a.P[FK]);
+                    const int64_t ck = hi ? tk - hik : tk;
+                    const int64_t row = FK == 0 ? (nn * ek + ck) * a.P[1] + t1 : (nn * a.P[0] + t0) * ek + ck;
+                    if (base) val[j] = *reinterpret_cast<const uint4*>(base + row * rowb + colb);
+                } else {
+                    val[j] = *reinterpret_cast<const uint4*>(src + off);
+                }
+            }
             z += dz;
             y += dy;
             off += step;
@@ -236,6 +273,16 @@ __device__ __forceinline__ void stage_brick(const FwdArgs& a, uint4* lds, int64_
         margin = margin || (f0 < f1 && (f0 < a.fold.lo[k] || f1 > a.fold.lo[k] + a.fold.ext[k]));
     }
     const uint32_t fm = a.fold.mask;
+    const bool rows_ok = vec_ok && a.cin % kPerUnit == 0 && a.BI[2] * a.nq <= kThreads;
+    if (margin && rows_ok && (fm == 1u || fm == 2u || fm == 4u)) {
+        if (fm == 1u)
+            stage_rows<T, SB, 0>(a, lds, nvp, nn, i0, c0);
+        else if (fm == 2u)
+            stage_rows<T, SB, 1>(a, lds, nvp, nn, i0, c0);
+        else
+            stage_rows<T, SB, 2>(a, lds, nvp, nn, i0, c0);
+        return;
+    }
     if (margin && (fm == 1u || fm == 2u || fm == 4u)) {
         // margins on one axis k: a voxel comes from the tile, or from the slab
         // of its side, whose layout is the tile's with axis k cut to the margin
@@ -297,8 +344,8 @@ __device__ __forceinline__ void stage_brick(const FwdArgs& a, uint4* lds, int64_
         });
         return;
     }
-    if (vec_ok && a.cin % kPerUnit == 0 && a.BI[2] * a.nq <= kThreads) {
-        stage_rows_plain<T, SB>(a, lds, nvp, nn, i0, c0);
+    if (rows_ok) {
+        stage_rows<T, SB, -1>(a, lds, nvp, nn, i0, c0);
         return;
     }
     stage_units(a, lds, nvp, [&](int v, int q, int z, int y, int x) {
