@@ -174,6 +174,11 @@ EDGE = [
     # M-row order (one and two N tiles; a ragged N tile of 40 channels)
     ("3d_bricks_8_wide", "bf16", 1, 16, 32, (16, 16, 24), (2, 1, 1), (3, 3, 3), (1, 1, 1)),
     ("3d_bricks_8_wide_c48", "bf16", 2, 48, 40, (16, 16, 24), (2, 1, 1), (3, 3, 3), (1, 1, 1)),
+    # one N tile over 8x8x8 bricks, ragged along H and W: a partial channel
+    # chunk (24), output channels ending inside a 16-byte run (20), three chunks (40)
+    ("3d_one_ntile_k5_c24", "bf16", 1, 24, 24, (16, 14, 14), (2, 1, 1), (3, 5, 3), (1, 1, 1)),
+    ("3d_one_ntile_k5_c20", "bf16", 1, 16, 20, (16, 14, 14), (2, 1, 1), (5, 5, 5), (1, 1, 1)),
+    ("3d_one_ntile_k3_c40", "bf16", 1, 40, 16, (16, 14, 14), (2, 1, 1), (3, 3, 5), (1, 1, 1)),
 ]
 
 

@@ -329,6 +329,7 @@ EDGE = [
     ("3d_s3_negative_pad", "f32", 1, 8, 16, (25, 9, 14), (2, 1, 1), (3, 3, 3), (3, 1, 2)),
     ("3d_thin_w", "bf16", 1, 32, 32, (10, 11, 3), (2, 1, 1), (3, 3, 3), (1, 1, 1)),
     ("3d_long_rows", "bf16", 1, 32, 32, (6, 5, 700), (2, 1, 1), (3, 3, 3), (1, 1, 1)),
+    ("3d_k5_16_channels", "bf16", 1, 16, 64, (16, 14, 28), (2, 1, 1), (5, 5, 5), (1, 1, 1)),
 ]
 
 
