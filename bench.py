@@ -44,6 +44,12 @@ sys.path.insert(0, ROOT)
 
 PEAK = {"bf16": 2516.6, "f32": 157.3}   # dense MFMA TFLOP/s, MI355X (AMD spec)
 HBM_PEAK = 8000.0                        # GB/s
+# Targets of the hot path: the convolutions at half the bf16 MFMA peak on the
+# bf16 workloads; the halo copies at 70 % of the HBM peak on the two largest
+# shards (the smaller ones are launch-bound and not held to it).
+CONV_TARGET = 0.50
+HALO_TARGET = 0.70
+HALO_TARGET_WORKLOADS = ("c3", "c5")
 
 DESCR = {
     "c1": "2d_fp32_c8_64x64_split2H_shard0_k3",
@@ -247,6 +253,10 @@ def main():
         if kind in ("fwd", "wgrad"):
             tf = work / (ms * 1e-3) / 1e12
             detail[label] = {"ms": round(ms, 4), "tflops": round(tf, 2), "frac_mfma_peak": round(tf / PEAK[dt], 4)}
+            if dt == "bf16":
+                # the stated target for the convolutions on the bf16 workloads
+                detail[label]["target_frac_mfma_peak"] = CONV_TARGET
+                detail[label]["meets_target"] = bool(tf / PEAK[dt] >= CONV_TARGET)
             ctr = measured_counters(label, args.workload)
             if ctr:
                 detail[label]["mfma_busy_frac"] = ctr["mfma_busy_frac"]
@@ -261,6 +271,10 @@ def main():
                              "protocol": "cold: 8 consecutive launches on 8 buffer sets (tile and slabs, 8 x the bytes "
                                          "> the 256 MB last-level cache), replayed from a captured graph between "
                                          "one event pair, per launch; median of the repeats"}
+            if args.workload in HALO_TARGET_WORKLOADS:
+                # the stated target for the halo copies on the largest shards
+                detail[label]["target_frac_hbm_peak"] = HALO_TARGET
+                detail[label]["meets_target"] = bool(gbs / HBM_PEAK >= HALO_TARGET)
     dom = max(("conv_fwd", "conv_wgrad"), key=lambda k: per_op[k][2])
     ach = per_op[dom][1] / (per_op[dom][2] * 1e-3) / 1e12
     roofline = {"kernel": dom, "bound": "mfma", "achieved": round(ach, 2), "peak": PEAK[dt], "unit": "TFLOP/s",
