@@ -248,6 +248,7 @@ def main():
 
     dt = w.dtype
     value = 2 * flops / (ms_step * 1e-3) / 1e12
+    halo_kernel = measured_halo_kernel(args.workload)
     detail = {}
     for label, (kind, work, ms) in per_op.items():
         if kind in ("fwd", "wgrad"):
@@ -271,6 +272,13 @@ def main():
                              "protocol": "cold: 8 consecutive launches on 8 buffer sets (tile and slabs, 8 x the bytes "
                                          "> the 256 MB last-level cache), replayed from a captured graph between "
                                          "one event pair, per launch; median of the repeats"}
+            hk = halo_kernel.get(kind) if halo_kernel and label.endswith("_a0") else None
+            if hk:
+                # the same launches' kernel time from the committed rocprofv3 trace
+                # (the event-timed figure adds the gaps between graph nodes)
+                detail[label]["kernel_ms_rocprof"] = round(hk * 1e-3, 4)
+                detail[label]["frac_hbm_peak_kernel"] = round(work / (hk * 1e-6) / 1e9 / HBM_PEAK, 4)
+                detail[label]["kernel_source"] = halo_kernel["source"]
             if args.workload in HALO_TARGET_WORKLOADS:
                 # the stated target for the halo copies on the largest shards
                 detail[label]["target_frac_hbm_peak"] = HALO_TARGET
@@ -645,6 +653,7 @@ def time_group_norm(sc, w, g, desc, tile, args, stream):
 KERNEL_SOURCES = {
     "conv_fwd": ["conv_fwd.hip", "conv_fwd_rows.hip", "common.h", "internal.h"],
     "conv_wgrad": ["conv_wgrad.hip", "conv_wgrad_xm.hip", "common.h", "internal.h"],
+    "halo": ["halo.hip", "common.h", "internal.h"],
 }
 
 
@@ -687,6 +696,28 @@ def measured_counters(op, workload):
     out["kernel"] = rec.get("kernel")
     out["source"] = f"profiles/{op}_{workload}_counters.txt"
     return out
+
+
+def measured_halo_kernel(workload):
+    """rocprofv3 kernel durations (µs, medians) of the cold graph-replayed pack
+    and unpack launches from the committed kernel trace summary, or None when
+    there is none or the halo sources changed since it was taken."""
+    path = os.path.join(ROOT, "profiles", f"halo_{workload}_kernel_trace.txt")
+    if not os.path.exists(path):
+        return None
+    rec = {}
+    with open(path) as fh:
+        for line in fh:
+            if ":" in line and not line.startswith("#"):
+                k, v = line.split(":", 1)
+                rec[k.strip()] = v.strip()
+    if rec.get("source_sha256") != source_hash("halo"):
+        return None
+    try:
+        return {"pack": float(rec["pack_cold_kernel_us"]), "unpack": float(rec["unpack_cold_kernel_us"]),
+                "source": f"profiles/halo_{workload}_kernel_trace.txt"}
+    except (KeyError, ValueError):
+        return None
 
 
 def measured_traffic(op, workload):
