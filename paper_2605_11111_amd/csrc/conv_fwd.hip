@@ -810,21 +810,22 @@ hipError_t launch_tiled_plans(const PlanF& pl, const PlanF* pl2, hipStream_t s)
     return hipErrorInvalidValue;
 }
 
-// Whether every buffer the loads may read is 16-byte aligned.
 // Whether the M-tile rows take brick voxels transposed. The A reads of an
 // M tile put 32 brick voxels, four rows of 8 when the brick is 8 voxels wide,
 // on 32 lanes, the rows BI2 voxels apart in LDS. Measured for 16-byte reads
 // (cycles per wave instruction, 4 waves per CU): rows 10 apart 48 in order
 // against 32 transposed, 12 apart 32 against 27, 14 apart 48 against 32; rows
 // 8 apart (a dense brick) 27 in order, 32 transposed; odd distances and wider
-// bricks gain nothing. In the kernel only the 10-apart case pays (C4's
-// W-paired input gradient, 3.5 % faster); with rows 12 apart (C4's forward) the
-// kernel ran 2.5 % slower, so it keeps the order there.
+// bricks gain nothing. In the kernel: rows 10 apart (C4's W-paired input
+// gradient) 3.5 % faster; rows 12 apart (C4's forward) bank-conflict cycles
+// 2.4 -> 0.12 per LDS-active cycle at the same matrix-core utilisation and
+// time within 1 %.
 bool rows_transposed(const FwdArgs& a)
 {
-    return a.BO[2] == 8 && a.S[2] == 1 && a.BI[2] == 10;
+    return a.BO[2] == 8 && a.S[2] == 1 && (a.BI[2] == 10 || a.BI[2] == 12);
 }
 
+// Whether every buffer the loads may read is 16-byte aligned.
 bool loads_aligned(const void* tile, const Fold* fold)
 {
     if (reinterpret_cast<uintptr_t>(tile) % 16 != 0) return false;
