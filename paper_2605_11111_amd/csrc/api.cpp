@@ -614,18 +614,31 @@ shard_status_t shard_conv_fwd_folded(const shard_tile_t* x, shard_dtype_t dtype,
     auto nonempty = [&](const Region& r) { return t.n * r.ext[0] * r.ext[1] * r.ext[2] > 0; };
     for (int i = 0; i < nb; ++i) {
         // two regions of the W-march kernel that differ along axis 0 only (the
-        // boundary planes of a tile sharded along axis 0), or any two regions
-        // of the tiled kernel (boundary slabs, too thin to fill the part one
-        // by one), go in one launch
-        if ((fam == FWD_ROWS || fam == FWD_TILED) && i + 1 < nb && folded[i] == folded[i + 1] &&
-            nonempty(boxes[i]) && nonempty(boxes[i + 1])) {
+        // boundary planes of a tile sharded along axis 0), or up to four
+        // regions of the tiled kernel (boundary slabs, too thin to fill the
+        // part one by one), go in one launch
+        if (fam == FWD_TILED) {
+            int run = 0;  // consecutive non-empty regions with the same folding
+            while (i + run < nb && run < 4 && folded[i + run] == folded[i] && nonempty(boxes[i + run])) ++run;
+            bool done = false;
+            for (int k = run; k >= 2 && !done; --k) {
+                const hipError_t e = launch_conv_fwd_tiled_group(t, cv, dtype, tile, w, y, om, boxes + i, k,
+                                                                 folded[i] ? fold : nullptr, ws, stream, laid);
+                if (e == hipSuccess) {
+                    laid = true;
+                    i += k - 1;
+                    done = true;
+                } else if (e != hipErrorNotSupported) {
+                    return SHARD_ERR_HIP;
+                }
+            }
+            if (done) continue;
+        }
+        if (fam == FWD_ROWS && i + 1 < nb && folded[i] == folded[i + 1] && nonempty(boxes[i]) &&
+            nonempty(boxes[i + 1])) {
             const Fold* fi = folded[i] ? fold : nullptr;
             const hipError_t e =
-                fam == FWD_ROWS
-                    ? launch_conv_fwd_region_pair(t, cv, dtype, tile, w, y, boxes[i], boxes[i + 1], fi, ws, stream,
-                                                  laid)
-                    : launch_conv_fwd_tiled_pair(t, cv, dtype, tile, w, y, om, boxes[i], boxes[i + 1], fi, ws, stream,
-                                                 laid);
+                launch_conv_fwd_region_pair(t, cv, dtype, tile, w, y, boxes[i], boxes[i + 1], fi, ws, stream, laid);
             if (e == hipSuccess) {
                 laid = true;
                 ++i;

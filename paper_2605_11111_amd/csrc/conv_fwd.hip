@@ -65,12 +65,14 @@ struct FwdArgs {
     Fold fold;             // halo folded into the loads when fold.mask != 0
 };
 
-// One launch over one or two output regions of the same plan family (the
-// boundary slabs of a split forward): blocks [0, nb0) take region 0, the rest
-// region 1.
+// One launch over two to four output regions of the same plan family (the
+// boundary slabs of a split forward): blocks [0, end[0]) take region 0, blocks
+// [end[0], end[1]) region 1, and so on (the ends of absent regions repeat the
+// total).
+constexpr int kMaxRegions = 4;
 struct FwdLaunch {
-    FwdArgs r[2];
-    int64_t nb0;
+    FwdArgs r[kMaxRegions];
+    int64_t end[kMaxRegions - 1];
 };
 
 struct PlanF {
@@ -618,16 +620,20 @@ __global__ __launch_bounds__(kThreads, 2) void conv_fwd_tiled(FwdArgs a)
     fwd_tiled_body<T, RM, RN>(a, xcd_remap(blockIdx.x, a.nblocks));
 }
 
-// Two regions in one launch: each takes its own inlined copy of the body, so
-// that its arguments are read from a fixed place.
+// Several regions in one launch: each takes its own inlined copy of the body,
+// so that its arguments are read from a fixed place.
 template <typename T, int RM, int RN>
-__global__ __launch_bounds__(kThreads, 2) void conv_fwd_tiled2(FwdLaunch la)
+__global__ __launch_bounds__(kThreads, 2) void conv_fwd_tiledn(FwdLaunch la)
 {
     const int64_t b = xcd_remap(blockIdx.x, gridDim.x);
-    if (b < la.nb0)
+    if (b < la.end[0])
         fwd_tiled_body<T, RM, RN>(la.r[0], b);
+    else if (b < la.end[1])
+        fwd_tiled_body<T, RM, RN>(la.r[1], b - la.end[0]);
+    else if (b < la.end[2])
+        fwd_tiled_body<T, RM, RN>(la.r[2], b - la.end[1]);
     else
-        fwd_tiled_body<T, RM, RN>(la.r[1], b - la.nb0);
+        fwd_tiled_body<T, RM, RN>(la.r[3], b - la.end[2]);
 }
 
 // wfrag[((tap * nkc + kc) * nt + ntile) * 64 + lane] = 16 bytes of weights in
@@ -776,37 +782,50 @@ size_t wfrag_bytes(const Tile3& t, const Conv3& cv)
     return size_t(cv.taps()) * size_t(pl.a.nkc) * size_t(pl.a.nt) * 64 * 16;
 }
 
+// n (1 to kMaxRegions) plans in one launch
 template <typename T, int RM, int RN>
-hipError_t launch_tiled(const PlanF& pl, const PlanF* pl2, hipStream_t s)
+hipError_t launch_tiled(const PlanF* pl, int n, hipStream_t s)
 {
-    const void* fn = pl2 ? reinterpret_cast<const void*>(&conv_fwd_tiled2<T, RM, RN>)
-                         : reinterpret_cast<const void*>(&conv_fwd_tiled<T, RM, RN>);
-    const size_t lds = pl2 ? std::max(pl.lds, pl2->lds) : pl.lds;
+    const void* fn = n > 1 ? reinterpret_cast<const void*>(&conv_fwd_tiledn<T, RM, RN>)
+                           : reinterpret_cast<const void*>(&conv_fwd_tiled<T, RM, RN>);
+    size_t lds = 0;
+    int64_t total = 0;
+    for (int i = 0; i < n; ++i) {
+        lds = std::max(lds, pl[i].lds);
+        total += pl[i].a.nblocks;
+    }
     hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, int(lds));
     if (e != hipSuccess) return e;
-    const int64_t total = pl.a.nblocks + (pl2 ? pl2->a.nblocks : 0);
     if (total >= (int64_t(1) << 31)) return hipErrorInvalidValue;
-    if (!pl2) {
-        FwdArgs a = pl.a;
+    if (n == 1) {
+        FwdArgs a = pl[0].a;
         void* args[] = {&a};
         return hipLaunchKernel(fn, dim3(unsigned(total)), dim3(kThreads), args, lds, s);
     }
     FwdLaunch la{};
-    la.r[0] = pl.a;
-    la.r[1] = pl2->a;
-    la.nb0 = pl.a.nblocks;
+    int64_t acc = 0;
+    for (int i = 0; i < kMaxRegions; ++i) {
+        if (i < n) {
+            la.r[i] = pl[i].a;
+            acc += pl[i].a.nblocks;
+        }
+        if (i < kMaxRegions - 1) la.end[i] = acc;
+    }
     void* args[] = {&la};
     return hipLaunchKernel(fn, dim3(unsigned(total)), dim3(kThreads), args, lds, s);
 }
 
 template <typename T>
-hipError_t launch_tiled_plans(const PlanF& pl, const PlanF* pl2, hipStream_t s)
+hipError_t launch_tiled_plans(const PlanF* pl, int n, hipStream_t s)
 {
-    if (pl2 && (pl2->rm != pl.rm || pl2->rn != pl.rn)) return hipErrorNotSupported;
-    if (pl.rm == 4 && pl.rn == 1) return launch_tiled<T, 4, 1>(pl, pl2, s);
-    if (pl.rm == 4 && pl.rn == 2) return launch_tiled<T, 4, 2>(pl, pl2, s);
-    if (pl.rm == 2 && pl.rn == 2) return launch_tiled<T, 2, 2>(pl, pl2, s);
-    if (pl.rm == 1 && pl.rn == 4) return launch_tiled<T, 1, 4>(pl, pl2, s);
+    if (n < 1 || n > kMaxRegions) return hipErrorInvalidValue;
+    for (int i = 1; i < n; ++i)
+        if (pl[i].rm != pl[0].rm || pl[i].rn != pl[0].rn) return hipErrorNotSupported;
+    const int rm = pl[0].rm, rn = pl[0].rn;
+    if (rm == 4 && rn == 1) return launch_tiled<T, 4, 1>(pl, n, s);
+    if (rm == 4 && rn == 2) return launch_tiled<T, 4, 2>(pl, n, s);
+    if (rm == 2 && rn == 2) return launch_tiled<T, 2, 2>(pl, n, s);
+    if (rm == 1 && rn == 4) return launch_tiled<T, 1, 4>(pl, n, s);
     return hipErrorInvalidValue;
 }
 
@@ -922,26 +941,31 @@ hipError_t run_fwd(const Tile3& t, const Conv3& cv, const void* tile, const void
     if (rows)
         return launch_conv_fwd_rows(t, cv, std::is_same<T, bf16_t>::value ? SHARD_BF16 : SHARD_F32, tile, ws,
                                     pl.a.nkc, pl.a.nt, y, rg, fold, s);
-    return launch_tiled_plans<T>(pl, nullptr, s);
+    return launch_tiled_plans<T>(&pl, 1, s);
 }
 
-// Two regions in one launch of the tiled kernel; hipErrorNotSupported, with
-// nothing launched, when their plans take different kernels.
+// n (2 to kMaxRegions) regions in one launch of the tiled kernel;
+// hipErrorNotSupported, with nothing launched, when their plans take
+// different kernels.
 template <typename T>
-hipError_t run_fwd_pair(const Tile3& t, const Conv3& cv, const void* tile, const void* w, void* y, const OutMap& om,
-                        const Region& ra, const Region& rb, const Fold* fold, void* ws, bool frags_ready,
-                        hipStream_t s)
+hipError_t run_fwd_group(const Tile3& t, const Conv3& cv, const void* tile, const void* w, void* y, const OutMap& om,
+                         const Region* rs, int n, const Fold* fold, void* ws, bool frags_ready, hipStream_t s)
 {
-    const PlanF pa = plan_region<T>(t, cv, tile, y, om, ra, fold, ws);
-    const PlanF pb = plan_region<T>(t, cv, tile, y, om, rb, fold, ws);
-    if (!pa.ok || !pb.ok) return hipErrorInvalidValue;
-    if (pa.rm != pb.rm || pa.rn != pb.rn || pa.a.nblocks + pb.a.nblocks >= (int64_t(1) << 31))
-        return hipErrorNotSupported;
+    if (n < 2 || n > kMaxRegions) return hipErrorNotSupported;
+    PlanF pl[kMaxRegions];
+    int64_t total = 0;
+    for (int i = 0; i < n; ++i) {
+        pl[i] = plan_region<T>(t, cv, tile, y, om, rs[i], fold, ws);
+        if (!pl[i].ok) return hipErrorInvalidValue;
+        if (pl[i].rm != pl[0].rm || pl[i].rn != pl[0].rn) return hipErrorNotSupported;
+        total += pl[i].a.nblocks;
+    }
+    if (total >= (int64_t(1) << 31)) return hipErrorNotSupported;
     if (!frags_ready) {
-        const hipError_t e = lay_wfrag<T>(t, cv, pa, w, ws, s);
+        const hipError_t e = lay_wfrag<T>(t, cv, pl[0], w, ws, s);
         if (e != hipSuccess) return e;
     }
-    return launch_tiled_plans<T>(pa, &pb, s);
+    return launch_tiled_plans<T>(pl, n, s);
 }
 
 }  // namespace
@@ -1014,12 +1038,12 @@ hipError_t launch_conv_fwd_region_pair(const Tile3& t, const Conv3& cv, shard_dt
     return launch_conv_fwd_rows(t, cv, dt, tile, ws, pl.a.nkc, pl.a.nt, y, ra, fold, s, &rb);
 }
 
-hipError_t launch_conv_fwd_tiled_pair(const Tile3& t, const Conv3& cv, shard_dtype_t dt, const void* tile,
-                                      const void* w, void* y, const OutMap& om, const Region& ra, const Region& rb,
-                                      const Fold* fold, void* ws, hipStream_t s, bool frags_ready)
+hipError_t launch_conv_fwd_tiled_group(const Tile3& t, const Conv3& cv, shard_dtype_t dt, const void* tile,
+                                       const void* w, void* y, const OutMap& om, const Region* rs, int n,
+                                       const Fold* fold, void* ws, hipStream_t s, bool frags_ready)
 {
-    return dt == SHARD_BF16 ? run_fwd_pair<bf16_t>(t, cv, tile, w, y, om, ra, rb, fold, ws, frags_ready, s)
-                            : run_fwd_pair<float>(t, cv, tile, w, y, om, ra, rb, fold, ws, frags_ready, s);
+    return dt == SHARD_BF16 ? run_fwd_group<bf16_t>(t, cv, tile, w, y, om, rs, n, fold, ws, frags_ready, s)
+                            : run_fwd_group<float>(t, cv, tile, w, y, om, rs, n, fold, ws, frags_ready, s);
 }
 
 hipError_t launch_conv_fwd_mapped(const Tile3& t, const Conv3& cv, shard_dtype_t dt, const void* tile,

@@ -140,12 +140,12 @@ hipError_t launch_conv_fwd_region(const Tile3& t, const Conv3& cv, shard_dtype_t
 hipError_t launch_conv_fwd_region_pair(const Tile3& t, const Conv3& cv, shard_dtype_t dt, const void* tile,
                                        const void* w, void* y, const Region& ra, const Region& rb, const Fold* fold,
                                        void* ws, hipStream_t s, bool frags_ready);
-// Two regions in one launch of the tiled kernel (FWD_TILED), each with bricks
-// of its own shape; hipErrorNotSupported when their plans take different
-// kernels (nothing launched).
-hipError_t launch_conv_fwd_tiled_pair(const Tile3& t, const Conv3& cv, shard_dtype_t dt, const void* tile,
-                                      const void* w, void* y, const OutMap& om, const Region& ra, const Region& rb,
-                                      const Fold* fold, void* ws, hipStream_t s, bool frags_ready);
+// n (2 to 4) regions in one launch of the tiled kernel (FWD_TILED), each with
+// bricks of its own shape; hipErrorNotSupported when their plans take
+// different kernels (nothing launched).
+hipError_t launch_conv_fwd_tiled_group(const Tile3& t, const Conv3& cv, shard_dtype_t dt, const void* tile,
+                                       const void* w, void* y, const OutMap& om, const Region* rs, int n,
+                                       const Fold* fold, void* ws, hipStream_t s, bool frags_ready);
 // The forward with its workspace in the library's per-device scratch array
 // (noalloc.hip): bytes it holds, and the launch (the caller has checked that
 // conv_fwd_workspace fits).
