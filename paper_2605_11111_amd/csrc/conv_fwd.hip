@@ -258,7 +258,7 @@ __device__ __forceinline__ void stage_rows(const FwdArgs& a, uint4* lds, int nvp
 }
 
 // Stage the input brick channels [c0, c0 + cc) into LDS; SB units in flight
-// per thread on the plain row path.
+// per thread on the row paths.
 template <typename T, int SB>
 __device__ __forceinline__ void stage_brick(const FwdArgs& a, uint4* lds, int64_t nn, const int64_t i0[3], int c0)
 {
