@@ -137,7 +137,8 @@ def test_sequential_exchange_between_all_shards(sc, name):
                 sc.shard_halo_unpack(desc, tiles[idx], axis, side, slab)
     for idx in w.shards():
         sg, _ = geo[idx]
-        assert _bits_equal(host(tiles[idx]), cases.x_box(w, sg.tile_lo, sg.tile_hi, out)), idx
+        want = _oracle_box(w, sg.tile_lo, sg.tile_hi)
+        assert np.array_equal(cases.as_f64(host(tiles[idx]), w), want), idx
 
 
 def test_unaligned_buffers_take_the_element_path(sc):
@@ -192,6 +193,9 @@ def _pair_case(sc, w, idx):
     import torch
     sg = cases.shard_geom(w, idx)
     full_h = cases.x_box(w, sg.tile_lo, sg.tile_hi, cases.out_code(w))
+    # expected values from the oracle's definition of the padded tile (the
+    # generator's box only feeds the device)
+    want_tile = _oracle_box(w, sg.tile_lo, sg.tile_hi)
     lo, hi = sg.g["halo_lo"], sg.g["halo_hi"]
     desc = sc.tile_desc(w.N, w.cin, sg.ext, lo, hi)
     tile = dev(full_h)
@@ -206,8 +210,8 @@ def _pair_case(sc, w, idx):
             rows = ohalo.pack_rows(axis, side, widths[side], lo, sg.ext)
             b0, b1 = ohalo.face_box(axis, rows, lo, sg.ext, hi)
             box = (slice(None),) + tuple(slice(a, b) for a, b in zip(b0, b1)) + (slice(None),)
-            want = np.ascontiguousarray(full_h[box])
-            assert _bits_equal(host(slabs[side]).reshape(want.shape), want), (idx, axis, side)
+            want = want_tile[box]
+            assert np.array_equal(cases.as_f64(host(slabs[side]), w).reshape(want.shape), want), (idx, axis, side)
     # margins from canaries: received slabs where a neighbour exists, zero at a boundary
     tile_h = np.full_like(full_h, canary_for(w))
     inner = (slice(None),) + tuple(slice(l, l + e) for l, e in zip(lo, sg.ext)) + (slice(None),)
@@ -224,7 +228,7 @@ def _pair_case(sc, w, idx):
             else:
                 recv.append(None)
         sc.shard_halo_unpack_pair(desc, t2, axis, recv[0], recv[1])
-    assert _bits_equal(host(t2), full_h), idx
+    assert np.array_equal(cases.as_f64(host(t2), w), want_tile), idx
 
 
 @pytest.mark.parametrize("name", list(cases.REDUCED))
