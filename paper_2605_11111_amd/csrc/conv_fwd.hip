@@ -574,8 +574,11 @@ __device__ __forceinline__ void fwd_tiled_body(const FwdArgs& a, int64_t b)
                     const uint4 v = *reinterpret_cast<const uint4*>(tl + row * 32 + ccol);
                     const int f = f0 + k * RSTEP;
                     const int co = j * 32 + ccol;
+                    // nontemporal: the outputs are not read again by this kernel
                     if (f < bov && oz < rem0 && oy < rem1 && ox < rem2 && co < cout_left)
-                        *reinterpret_cast<uint4*>(ycol + oz * ys1 + oy * ys2 + ox * ys3 + co) = v;
+                        __builtin_nontemporal_store(__builtin_bit_cast(lds_u32x4, v),
+                                                    reinterpret_cast<lds_u32x4*>(ycol + oz * ys1 + oy * ys2 +
+                                                                                 ox * ys3 + co));
                 }
             }
         }

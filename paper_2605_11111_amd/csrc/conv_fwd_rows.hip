@@ -389,7 +389,9 @@ __global__ __launch_bounds__(256, 1) void conv_fwd_xm(XmArgs a)
                 const uint32_t off =
                     ok ? ((rbase + uint32_t(ox)) * uint32_t(a.cout) + uint32_t(wc * 32 + uu * 8)) * 2u
                        : a.ybatch_bytes;
-                __builtin_amdgcn_raw_buffer_store_b128(ed[it], yr, off, 0, 0);
+                // nontemporal (cache policy NT): the outputs are not read again
+                // by this kernel (1-1.5 % faster on C3 than cached stores)
+                __builtin_amdgcn_raw_buffer_store_b128(ed[it], yr, off, 0, 2);
             }
         }
     };
