@@ -313,9 +313,10 @@ __global__ __launch_bounds__(256 * KS, 1) void wgrad_xm(WxArgs a)
             const int zb = (RKY * kk) / BY, yb0 = (RKY * kk) % BY;
             const bool ok = st_oky && st_o0 + zb < a.O[0] && st_o1 + yb0 + wry < a.O[1];
             const uint32_t u = st_yorg + uint32_t(zb) * a.yplane + uint32_t(yb0) * a.yrow + lyw;
+            // dy is read once per brick: nontemporal (cache policy NT)
             __builtin_amdgcn_raw_ptr_buffer_load_lds(st_ry,
                                                      SC_LDSW(st_dst + C::X_BYTES + C::XH_BYTES + 4 * kk * 1024), 16,
-                                                     ok ? u : a.dy_bytes, 0, 0, 0);
+                                                     ok ? u : a.dy_bytes, 0, 0, 2);
         }
     };
     // rows of a tile over which the loads of the next unit are spread (the rest
@@ -366,8 +367,10 @@ __global__ __launch_bounds__(256 * KS, 1) void wgrad_xm(WxArgs a)
             const bool ok = live & (o0 + zb < a.O[0]) & (o1 + yb < a.O[1]) & (o2 + pc * YPI + vy < a.O[2]);
             const uint32_t u = yorg + uint32_t(zb) * a.yplane + uint32_t(yb) * a.yrow + lym +
                                uint32_t(pc * YPI * C::COUT * 2);
+            // dy is read once per brick: nontemporal (cache policy NT; the C3
+            // weight gradient 1-1.5 % faster than with cached loads)
             __builtin_amdgcn_raw_ptr_buffer_load_lds(ry, SC_LDSW(dst + C::X_BYTES + C::XH_BYTES + j * 1024), 16,
-                                                     ok ? u : a.dy_bytes, 0, 0, 0);
+                                                     ok ? u : a.dy_bytes, 0, 0, 2);
         }
     };
     if (KS == 2 && simd == 3) {
